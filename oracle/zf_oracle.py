@@ -1,0 +1,355 @@
+"""Plain CPU oracle of the selective-update hot path (TEST INFRASTRUCTURE).
+
+Only tests/, __graft_entry__.smoke() and bench.py's cpu_baseline leg may
+import this module.  The product path never calls it, and it shares no code
+with the HIP library or its Python binding.
+
+It restates, in slow and direct numpy, what ZenFlow's GPU side computes for
+one weight matrix (paper: "ZenFlow Design", Asynchronous Offloading Workflow
+and Gradient Selection; Convergence Analysis for the accumulate-then-apply
+rule):
+
+* colnorm     -- per-input-channel squared gradient norm (Gradient Selection,
+                 "Lightweight Proxy for Gradient Ranking").  The definition,
+                 summed in fp64 in row order and rounded once to fp32.
+* select_topk -- the k columns with the largest score (Problem #3 top-k
+                 selection applied to channels).  A plain sort.
+* remap       -- states follow their columns when the selection is refreshed
+                 (selective optimizer initialised only with the chosen
+                 subset; swap-in of states, Zero-stall Pipeline).
+* adam_selected -- Adam (Kingma & Ba) / AdamW decoupled decay on the selected
+                 columns' fp32 master, first and second moments, in place,
+                 then the bf16 write-back (Asynchronous Offloading Workflow,
+                 Implementation "Selective GPU-side Optimizer").
+* pack_accumulate / unpack -- unselected columns summed over an interval of
+                 S steps and handed over as one dense buffer (Asynchronous
+                 Offloading Workflow; the S-step rule of the Convergence
+                 Analysis, whose 1/S mean is unpack's scale).
+* schedule    -- which step refreshes the selection, starts or ends an
+                 accumulation interval.
+
+Precision.  The workloads fix fp32 master weights, moments and accumulation
+buffer, and the selective optimizer extends PyTorch's fp32 Adam
+(Implementation).  So Adam, pack and unpack are written as IEEE fp32
+operations, one rounding per operation, in the order given in each function
+(numpy float32 ufuncs: no fused multiply-add, correctly rounded sqrt and
+division, subnormals kept).  Column norms are summed in fp64.  Every
+function is pinned by tests/test_oracle_*.py against closed forms, brute
+force, exact rational arithmetic, library routines or invariants.
+"""
+
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass
+from typing import Optional, Tuple
+
+import numpy as np
+
+__all__ = [
+    "Selection", "AdamConsts", "StepKind",
+    "widen", "bf16_round", "colnorm", "k_from_ratio", "select_topk",
+    "slots_of", "remap", "adam_selected", "pack_accumulate", "unpack",
+    "schedule", "MatrixOracle",
+]
+
+
+# ---------------------------------------------------------------------------
+# bf16 <-> fp32 (BF16 training: parameters and gradients in bf16, Background
+# "Training Memory Breakdown")
+# ---------------------------------------------------------------------------
+
+def widen(bits: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns (uint16) -> fp32: the bf16 bits are the top half of
+    an fp32 word, so the widening is exact."""
+    b = np.asarray(bits, dtype=np.uint16)
+    return (b.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def bf16_round(x: np.ndarray) -> np.ndarray:
+    """fp32 -> bf16 bit patterns, round to nearest, ties to even.  NaN stays
+    NaN (quiet bit set); overflow past the largest bf16 gives infinity."""
+    u = np.asarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    is_nan = (u & 0x7FFFFFFF) > 0x7F800000
+    lsb = (u >> 16) & 1
+    r = ((u + 0x7FFF + lsb) >> 16) & 0xFFFF
+    r = np.where(is_nan, ((u >> 16) | 0x40) & 0xFFFF, r)
+    return r.astype(np.uint16)
+
+
+# ---------------------------------------------------------------------------
+# a1: column scores
+# ---------------------------------------------------------------------------
+
+def colnorm(G: np.ndarray) -> np.ndarray:
+    """s_j = sum_i g_ij^2 over the rows of an n x m bf16 gradient (uint16
+    bits), one score per input channel j (Gradient Selection, "Lightweight
+    Proxy": per-column squared norms).  Squares of bf16 values are exact in
+    fp64; the fp64 row-order sum is rounded once to fp32."""
+    G = np.asarray(G, dtype=np.uint16)
+    n, m = G.shape
+    acc = np.zeros(m, dtype=np.float64)
+    for i in range(n):
+        g = widen(G[i]).astype(np.float64)
+        acc += g * g
+    return acc.astype(np.float32)
+
+
+# ---------------------------------------------------------------------------
+# a2: top-k selection
+# ---------------------------------------------------------------------------
+
+def k_from_ratio(ratio: float, m: int) -> int:
+    """Number of selected columns for a top-k ratio (Evaluation, ZenFlow
+    hyperparameters "topk_ratio").  Reading: round half up, k = floor(ratio*m
+    + 1/2) in double, clamped to [0, m]."""
+    if not (0.0 <= ratio <= 1.0) or m < 0:
+        raise ValueError("ratio must lie in [0, 1] and m >= 0")
+    return max(0, min(m, int(math.floor(ratio * m + 0.5))))
+
+
+@dataclass
+class Selection:
+    sel: np.ndarray      # int32 [k], ascending column indices
+    unsel: np.ndarray    # int32 [m-k], ascending column indices
+    mask: np.ndarray     # uint64 [ceil(m/64)], bit b of word w <=> column 64w+b selected
+    prefix: np.ndarray   # int32 [ceil(m/64)], selected columns with index < 64w
+    m: int
+
+    @property
+    def k(self) -> int:
+        return int(self.sel.size)
+
+
+def _mask_and_prefix(sel: np.ndarray, m: int) -> Tuple[np.ndarray, np.ndarray]:
+    words = (m + 63) // 64
+    mask = np.zeros(words, dtype=np.uint64)
+    for j in sel.tolist():
+        mask[j // 64] |= np.uint64(1) << np.uint64(j % 64)
+    prefix = np.zeros(words, dtype=np.int32)
+    count = 0
+    for w in range(words):
+        prefix[w] = count
+        count += bin(int(mask[w])).count("1")
+    return mask, prefix
+
+
+def select_topk(scores: np.ndarray, k: int) -> Selection:
+    """The k columns with the largest score.  Order: larger score first, and
+    among equal scores (-0.0 equals +0.0) the lower column index first; the
+    chosen set and its complement are returned in ascending index order."""
+    s = np.asarray(scores, dtype=np.float32)
+    m = int(s.size)
+    if not 0 <= k <= m:
+        raise ValueError("k must lie in [0, m]")
+    idx = np.arange(m)
+    # np.lexsort sorts by the last key first: descending score, then index.
+    order = np.lexsort((idx, -s.astype(np.float64)))
+    sel = np.sort(order[:k]).astype(np.int32)
+    unsel = np.sort(order[k:]).astype(np.int32)
+    mask, prefix = _mask_and_prefix(sel, m)
+    return Selection(sel, unsel, mask, prefix, m)
+
+
+def slots_of(cols: np.ndarray, m: int) -> np.ndarray:
+    """slot[j] = position of column j in the ascending list `cols`, -1 if
+    absent (row-compact layout: slot r of a row <-> column cols[r])."""
+    slot = np.full(m, -1, dtype=np.int64)
+    slot[np.asarray(cols, dtype=np.int64)] = np.arange(len(cols))
+    return slot
+
+
+# ---------------------------------------------------------------------------
+# a3 + a4: Adam on the selected columns and bf16 write-back
+# ---------------------------------------------------------------------------
+
+@dataclass(frozen=True)
+class AdamConsts:
+    """Per-step constants, each computed in double and rounded once to fp32."""
+    B1: np.float32
+    B2: np.float32
+    C1: np.float32
+    C2: np.float32
+    LR: np.float32
+    EPS: np.float32
+    WD: np.float32     # lr * weight_decay (AdamW decoupled decay)
+    IB1: np.float32    # 1 / (1 - beta1^t)
+    IB2: np.float32    # 1 / (1 - beta2^t)
+
+    @staticmethod
+    def at_step(lr: float, beta1: float, beta2: float, eps: float,
+                weight_decay: float, t: int) -> "AdamConsts":
+        if t < 1:
+            raise ValueError("the step counter is 1-based")
+        f = np.float32
+        return AdamConsts(
+            B1=f(beta1), B2=f(beta2), C1=f(1.0 - beta1), C2=f(1.0 - beta2),
+            LR=f(lr), EPS=f(eps), WD=f(lr * weight_decay),
+            IB1=f(1.0 / (1.0 - beta1 ** t)), IB2=f(1.0 / (1.0 - beta2 ** t)))
+
+
+def adam_selected(G: np.ndarray, sel: np.ndarray, P: np.ndarray, M: np.ndarray,
+                  V: np.ndarray, c: AdamConsts):
+    """One Adam/AdamW step on the selected columns.
+
+    G: bf16 gradient bits [n, m]; sel: ascending selected columns [k];
+    P, M, V: row-compact fp32 states [n, k] (slot r <-> column sel[r]).
+    Returns (P', M', V', W_sel) with W_sel the bf16 bits of P' for the
+    selected columns.  Each line is one fp32 operation per element:
+
+        m' = B1*m + C1*g
+        v' = B2*v + C2*(g*g)
+        d  = sqrt(v'*IB2) + EPS            (IB2 = 1/(1-beta2^t))
+        u  = (m'*IB1) / d                  (IB1 = 1/(1-beta1^t))
+        p  = p - WD*p                      (only when weight decay != 0)
+        p' = p - LR*u
+        w  = bf16(p')
+    """
+    g = widen(np.asarray(G)[:, np.asarray(sel, dtype=np.int64)])
+    P = np.asarray(P, dtype=np.float32)
+    M = np.asarray(M, dtype=np.float32)
+    V = np.asarray(V, dtype=np.float32)
+    m1 = c.B1 * M + c.C1 * g
+    v1 = c.B2 * V + c.C2 * (g * g)
+    d = np.sqrt(v1 * c.IB2) + c.EPS
+    u = (m1 * c.IB1) / d
+    p = P - c.WD * P if c.WD != 0 else P
+    p1 = p - c.LR * u
+    return p1.astype(np.float32), m1.astype(np.float32), v1.astype(np.float32), bf16_round(p1)
+
+
+def remap(prev: Optional[Selection], new: Selection, P: Optional[np.ndarray],
+          M: Optional[np.ndarray], V: Optional[np.ndarray], W: np.ndarray,
+          master: Optional[np.ndarray] = None):
+    """Compact states for a new selection.  A column that stays selected keeps
+    its (p, m, v) -- moved to its new slot; a newly selected column starts
+    with m = v = 0 and p taken from the fp32 `master` [n, m] when given, else
+    from the widened bf16 weight W [n, m].  `prev` None means no column was
+    selected before."""
+    W = np.asarray(W, dtype=np.uint16)
+    n = W.shape[0]
+    k = new.k
+    P2 = np.zeros((n, k), dtype=np.float32)
+    M2 = np.zeros((n, k), dtype=np.float32)
+    V2 = np.zeros((n, k), dtype=np.float32)
+    old_slot = slots_of(prev.sel, new.m) if prev is not None else np.full(new.m, -1)
+    for r, j in enumerate(new.sel.tolist()):
+        ro = int(old_slot[j])
+        if ro >= 0:
+            P2[:, r] = P[:, ro]
+            M2[:, r] = M[:, ro]
+            V2[:, r] = V[:, ro]
+        elif master is not None:
+            P2[:, r] = np.asarray(master, dtype=np.float32)[:, j]
+        else:
+            P2[:, r] = widen(W[:, j])
+    return P2, M2, V2
+
+
+# ---------------------------------------------------------------------------
+# a5 + a6: accumulation of the unselected columns, hand-over
+# ---------------------------------------------------------------------------
+
+def pack_accumulate(G: np.ndarray, unsel: np.ndarray, A: Optional[np.ndarray],
+                    step_in_interval: int) -> np.ndarray:
+    """A[i, u] = g[i, unsel[u]] on the first step of an interval, else
+    A[i, u] + g[i, unsel[u]] (one fp32 addition).  Row-compact [n, m-k]."""
+    g = widen(np.asarray(G)[:, np.asarray(unsel, dtype=np.int64)])
+    if step_in_interval < 1:
+        raise ValueError("step_in_interval is 1-based")
+    if step_in_interval == 1:
+        return g.copy()
+    return (np.asarray(A, dtype=np.float32) + g).astype(np.float32)
+
+
+def unpack(A: np.ndarray, sel: Selection, scale: float = 1.0) -> np.ndarray:
+    """Dense [n, m] fp32: +0.0 at selected columns, scale * A[i, u] at the
+    unselected column unsel[u] (one fp32 multiply; scale 1 copies)."""
+    A = np.asarray(A, dtype=np.float32)
+    n = A.shape[0]
+    D = np.zeros((n, sel.m), dtype=np.float32)
+    D[:, sel.unsel.astype(np.int64)] = A * np.float32(scale)
+    return D
+
+
+# ---------------------------------------------------------------------------
+# schedule
+# ---------------------------------------------------------------------------
+
+@dataclass(frozen=True)
+class StepKind:
+    refresh: bool           # recompute scores and the selection at this step
+    step_in_interval: int   # 1 = first step of an accumulation interval
+    interval_end: bool      # hand the accumulated buffer over after this step
+
+
+def _is_refresh(t: int, R: int) -> bool:
+    return (t - 1) % R == 0
+
+
+def _is_start(t: int, R: int, S: int) -> bool:
+    return _is_refresh(t, R) or (t - 1) % S == 0
+
+
+def schedule(t: int, R: int, S: int) -> StepKind:
+    """Step kinds for 1-based step t, selection refresh interval R and
+    accumulation interval S.  Reading: the selection is recomputed when
+    (t-1) mod R = 0 (index reuse between refreshes, Gradient Selection
+    "Temporal Locality"); an interval starts every S steps (the t mod S rule
+    of the Convergence Analysis) and also at every refresh, because the packed
+    layout follows the selection; an interval ends right before the next
+    one starts."""
+    if t < 1 or R < 1 or S < 1:
+        raise ValueError("t, R and S are 1-based / positive")
+    start = t
+    while not _is_start(start, R, S):
+        start -= 1
+    return StepKind(refresh=_is_refresh(t, R), step_in_interval=t - start + 1,
+                    interval_end=_is_start(t + 1, R, S))
+
+
+# ---------------------------------------------------------------------------
+# one matrix across steps
+# ---------------------------------------------------------------------------
+
+class MatrixOracle:
+    """Runs the per-step composition for one weight matrix:
+    refresh -> colnorm, select_topk, remap; every step -> adam_selected and
+    pack_accumulate; interval end -> unpack with scale 1/(interval length)
+    (the 1/S mean of the Convergence Analysis)."""
+
+    def __init__(self, master: np.ndarray, W: np.ndarray, ratio: float,
+                 lr: float, beta1: float, beta2: float, eps: float,
+                 weight_decay: float, R: int, S: int):
+        self.master = np.asarray(master, dtype=np.float32)
+        self.W = np.array(W, dtype=np.uint16, copy=True)
+        self.n, self.m = self.W.shape
+        self.k = k_from_ratio(ratio, self.m)
+        self.hyper = (lr, beta1, beta2, eps, weight_decay)
+        self.R, self.S = R, S
+        self.t = 0
+        self.sel: Optional[Selection] = None
+        self.P = self.M = self.V = None
+        self.A: Optional[np.ndarray] = None
+
+    def step(self, G: np.ndarray) -> dict:
+        self.t += 1
+        kind = schedule(self.t, self.R, self.S)
+        out = {"kind": kind}
+        if kind.refresh:
+            s = colnorm(G)
+            new = select_topk(s, self.k)
+            first = self.sel is None
+            self.P, self.M, self.V = remap(self.sel, new, self.P, self.M, self.V,
+                                           self.W, self.master if first else None)
+            self.sel = new
+            out["norms"] = s
+        c = AdamConsts.at_step(*self.hyper, self.t)
+        self.P, self.M, self.V, wsel = adam_selected(G, self.sel.sel, self.P, self.M,
+                                                     self.V, c)
+        self.W[:, self.sel.sel.astype(np.int64)] = wsel
+        self.A = pack_accumulate(G, self.sel.unsel, self.A, kind.step_in_interval)
+        if kind.interval_end:
+            out["unpacked"] = unpack(self.A, self.sel,
+                                     float(np.float32(1.0 / kind.step_in_interval)))
+        return out
