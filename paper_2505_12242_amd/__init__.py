@@ -1,0 +1,31 @@
+"""MI355X-native selective-update hot path of ZenFlow (arXiv 2505.12242).
+
+Per bf16 weight gradient: per-input-channel squared norms, top-k channel
+selection, in-place Adam on the selected channels' fp32 states with bf16
+write-back, and S-step accumulation of the unselected channels in a packed
+fp32 buffer handed over as a dense matrix.  All of it runs in the HIP
+kernels of libzf.so (C ABI in include/zf.h); this package only binds it.
+"""
+
+from ._lib import (  # noqa: F401
+    LIB,
+    LIB_PATH,
+    STATES_INIT,
+    STATES_INPLACE,
+    STATES_REMAP,
+    AdamHparams,
+    MatrixBuffers,
+    Plan,
+    Selection,
+    StateSource,
+    ZfError,
+    adam_selected,
+    colnorm,
+    colnorm_workspace_bytes,
+    k_from_ratio,
+    pack_accumulate,
+    topk_select,
+    unpack,
+    update_fused,
+)
+from .runner import SelectiveUpdateRunner, StepKind, schedule  # noqa: F401

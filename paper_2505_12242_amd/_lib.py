@@ -1,0 +1,401 @@
+"""ctypes binding of libzf (include/zf.h).
+
+Argument marshalling only: tensors are checked for dtype, device and
+row-major layout, then their device addresses and row strides are passed to
+the C ABI; every step of the path runs in the HIP kernels.  Importing this
+module raises if libzf.so has not been built -- there is no fallback.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import List, Optional, Sequence
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libzf.so")
+
+ZF_OK, ZF_EINVAL, ZF_EWORKSPACE, ZF_EHIP, ZF_ENOMEM = 0, 1, 2, 3, 4
+STATES_INPLACE, STATES_REMAP, STATES_INIT = 0, 1, 2
+
+c_i64, c_i32, c_dbl, c_flt, c_vp, c_sz = (ctypes.c_int64, ctypes.c_int32, ctypes.c_double,
+                                          ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t)
+
+
+class ZfAdamHparams(ctypes.Structure):
+    _fields_ = [("lr", c_dbl), ("beta1", c_dbl), ("beta2", c_dbl), ("eps", c_dbl),
+                ("weight_decay", c_dbl)]
+
+
+class ZfSelection(ctypes.Structure):
+    _fields_ = [("sel_idx", c_vp), ("unsel_idx", c_vp), ("sel_mask", c_vp), ("sel_prefix", c_vp)]
+
+
+class ZfStateSource(ctypes.Structure):
+    _fields_ = [("prev_mask", c_vp), ("prev_prefix", c_vp), ("prev_master", c_vp),
+                ("prev_exp_avg", c_vp), ("prev_exp_avg_sq", c_vp), ("ld_prev", c_i64),
+                ("init_master", c_vp), ("ld_init", c_i64)]
+
+
+class ZfMatrix(ctypes.Structure):
+    _fields_ = [("n", c_i64), ("m", c_i64), ("k", c_i64),
+                ("grad", c_vp), ("ld_grad", c_i64),
+                ("weight", c_vp), ("ld_weight", c_i64),
+                ("master", c_vp), ("exp_avg", c_vp), ("exp_avg_sq", c_vp), ("ld_state", c_i64),
+                ("acc", c_vp), ("ld_acc", c_i64),
+                ("norms_sq", c_vp),
+                ("sel", ZfSelection),
+                ("unpacked", c_vp), ("ld_unpacked", c_i64),
+                ("src", ZfStateSource)]
+
+
+# (name, restype, argtypes) of every exported entry point of include/zf.h.
+SIGNATURES = [
+    ("zf_status_string", ctypes.c_char_p, [ctypes.c_int]),
+    ("zf_last_hip_error", ctypes.c_int, []),
+    ("zf_k_from_ratio", c_i64, [c_dbl, c_i64]),
+    ("zf_colnorm_workspace_bytes", c_sz, [c_i64, c_i64]),
+    ("zf_colnorm", ctypes.c_int, [c_vp, c_i64, c_i64, c_i64, c_vp, c_vp, c_sz, c_vp]),
+    ("zf_topk_select", ctypes.c_int,
+     [c_vp, c_i64, c_dbl, ctypes.POINTER(ZfSelection), ctypes.POINTER(c_i64), c_vp]),
+    ("zf_adam_selected", ctypes.c_int,
+     [c_vp, c_i64, c_i64, c_i64, ctypes.POINTER(ZfSelection), c_i64, c_vp, c_vp, c_vp, c_i64,
+      c_vp, c_i64, ctypes.POINTER(ZfAdamHparams), c_i64, c_i32, ctypes.POINTER(ZfStateSource),
+      c_vp]),
+    ("zf_pack_accumulate", ctypes.c_int,
+     [c_vp, c_i64, c_i64, c_i64, ctypes.POINTER(ZfSelection), c_i64, c_vp, c_i64, c_i64, c_i64,
+      c_vp]),
+    ("zf_update_fused", ctypes.c_int,
+     [c_vp, c_i64, c_i64, c_i64, ctypes.POINTER(ZfSelection), c_i64, c_vp, c_vp, c_vp, c_i64,
+      c_vp, c_i64, ctypes.POINTER(ZfAdamHparams), c_i64, c_i32, ctypes.POINTER(ZfStateSource),
+      c_vp, c_i64, c_i64, c_i64, c_vp]),
+    ("zf_unpack", ctypes.c_int,
+     [c_vp, c_i64, ctypes.POINTER(ZfSelection), c_i64, c_i64, c_i64, c_flt, c_vp, c_i64, c_vp]),
+    ("zf_plan_create", ctypes.c_int, [ctypes.POINTER(ZfMatrix), c_i32, ctypes.POINTER(c_vp)]),
+    ("zf_plan_destroy", None, [c_vp]),
+    ("zf_plan_device_bytes", c_sz, [c_vp]),
+    ("zf_plan_colnorm", ctypes.c_int, [c_vp, c_vp]),
+    ("zf_plan_topk_select", ctypes.c_int, [c_vp, c_vp]),
+    ("zf_plan_update", ctypes.c_int,
+     [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, c_i32, c_i64, c_i64, c_i32, c_i32, c_vp]),
+    ("zf_plan_unpack", ctypes.c_int, [c_vp, c_flt, c_vp]),
+]
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    if not os.path.exists(path):
+        raise RuntimeError(
+            f"libzf.so is not built ({path} missing); run `python -m paper_2505_12242_amd.build`")
+    lib = ctypes.CDLL(path)
+    for name, res, args in SIGNATURES:
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+LIB = load()
+
+
+class ZfError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        msg = LIB.zf_status_string(status).decode()
+        if status == ZF_EHIP:
+            msg += f" (hipError {LIB.zf_last_hip_error()})"
+        super().__init__(f"{fn}: {msg}")
+        self.status = status
+
+
+def _check(fn: str, status: int) -> None:
+    if status != ZF_OK:
+        raise ZfError(fn, status)
+
+
+# ---------------------------------------------------------------------------
+# tensor marshalling
+# ---------------------------------------------------------------------------
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None or t.numel() == 0 else t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def _mat(t: torch.Tensor, dtype, name: str, rows: Optional[int] = None,
+         cols: Optional[int] = None) -> int:
+    """Checks a row-major 2-D device tensor and returns its row stride."""
+    if t.dtype != dtype:
+        raise TypeError(f"{name}: expected {dtype}, got {t.dtype}")
+    if t.dim() != 2:
+        raise ValueError(f"{name}: expected a 2-D tensor, got shape {tuple(t.shape)}")
+    if rows is not None and t.shape[0] != rows:
+        raise ValueError(f"{name}: expected {rows} rows, got {t.shape[0]}")
+    if cols is not None and t.shape[1] != cols:
+        raise ValueError(f"{name}: expected {cols} columns, got {t.shape[1]}")
+    if t.numel() and not t.is_cuda:
+        raise ValueError(f"{name}: must live on a GPU")
+    if t.shape[0] > 1 and t.shape[1] > 1 and t.stride(1) != 1:
+        raise ValueError(f"{name}: rows must be contiguous (stride(1) == 1)")
+    return t.stride(0) if t.shape[0] > 1 else t.shape[1]
+
+
+def _vec(t: torch.Tensor, dtype, name: str, size: int) -> None:
+    if t.dtype != dtype or t.dim() != 1 or t.shape[0] != size:
+        raise ValueError(f"{name}: expected a [{size}] {dtype} tensor, got "
+                         f"{tuple(t.shape)} {t.dtype}")
+    if size and (not t.is_cuda or not t.is_contiguous()):
+        raise ValueError(f"{name}: must be a contiguous GPU tensor")
+
+
+@dataclass
+class AdamHparams:
+    lr: float = 1e-5
+    beta1: float = 0.9
+    beta2: float = 0.999
+    eps: float = 1e-8
+    weight_decay: float = 0.0
+
+    def as_c(self) -> ZfAdamHparams:
+        return ZfAdamHparams(self.lr, self.beta1, self.beta2, self.eps, self.weight_decay)
+
+
+class Selection:
+    """Device buffers of one selection of k out of m columns."""
+
+    def __init__(self, m: int, k: int, device=None):
+        device = device if device is not None else torch.device("cuda")
+        words = (m + 63) // 64
+        self.m, self.k = m, k
+        self.sel_idx = torch.empty(k, dtype=torch.int32, device=device)
+        self.unsel_idx = torch.empty(m - k, dtype=torch.int32, device=device)
+        self.mask = torch.empty(words, dtype=torch.int64, device=device)  # uint64 bit patterns
+        self.prefix = torch.empty(words, dtype=torch.int32, device=device)
+
+    def as_c(self) -> ZfSelection:
+        return ZfSelection(_ptr(self.sel_idx), _ptr(self.unsel_idx), _ptr(self.mask),
+                           _ptr(self.prefix))
+
+
+def k_from_ratio(ratio: float, m: int) -> int:
+    k = LIB.zf_k_from_ratio(float(ratio), int(m))
+    if k < 0:
+        raise ValueError("ratio must lie in [0, 1] and m >= 0")
+    return k
+
+
+def colnorm_workspace_bytes(n: int, m: int) -> int:
+    return LIB.zf_colnorm_workspace_bytes(n, m)
+
+
+def colnorm(grad: torch.Tensor, out: Optional[torch.Tensor] = None,
+            workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    n, m = grad.shape
+    ld = _mat(grad, torch.bfloat16, "grad")
+    if out is None:
+        out = torch.empty(m, dtype=torch.float32, device=grad.device)
+    _vec(out, torch.float32, "out", m)
+    need = colnorm_workspace_bytes(n, m)
+    if workspace is None:
+        workspace = torch.empty(max(need, 8), dtype=torch.uint8, device=grad.device)
+    _check("zf_colnorm", LIB.zf_colnorm(_ptr(grad), n, m, ld, _ptr(out), _ptr(workspace),
+                                        workspace.numel(), _stream(stream)))
+    return out
+
+
+def topk_select(norms: torch.Tensor, ratio: float, out: Optional[Selection] = None,
+                stream=None) -> Selection:
+    m = norms.shape[0]
+    k = k_from_ratio(ratio, m)
+    _vec(norms, torch.float32, "norms", m)
+    if out is None:
+        out = Selection(m, k, norms.device)
+    if out.m != m or out.k != k:
+        raise ValueError(f"selection buffers are for m={out.m}, k={out.k}; need m={m}, k={k}")
+    c_sel = out.as_c()
+    k_out = c_i64(-1)
+    _check("zf_topk_select", LIB.zf_topk_select(_ptr(norms), m, float(ratio), ctypes.byref(c_sel),
+                                                ctypes.byref(k_out), _stream(stream)))
+    return out
+
+
+@dataclass
+class StateSource:
+    """Where the selected columns' states come from (see zf_state_mode)."""
+    prev: Optional[Selection] = None
+    prev_master: Optional[torch.Tensor] = None
+    prev_exp_avg: Optional[torch.Tensor] = None
+    prev_exp_avg_sq: Optional[torch.Tensor] = None
+    init_master: Optional[torch.Tensor] = None
+
+    def as_c(self) -> ZfStateSource:
+        ld_prev = 0
+        if self.prev_master is not None:
+            ld_prev = _mat(self.prev_master, torch.float32, "prev_master")
+            _mat(self.prev_exp_avg, torch.float32, "prev_exp_avg")
+            _mat(self.prev_exp_avg_sq, torch.float32, "prev_exp_avg_sq")
+        ld_init = 0
+        if self.init_master is not None:
+            ld_init = _mat(self.init_master, torch.float32, "init_master")
+        return ZfStateSource(
+            _ptr(self.prev.mask) if self.prev else None,
+            _ptr(self.prev.prefix) if self.prev else None,
+            _ptr(self.prev_master), _ptr(self.prev_exp_avg), _ptr(self.prev_exp_avg_sq), ld_prev,
+            _ptr(self.init_master), ld_init)
+
+
+def _states(n, k, master, exp_avg, exp_avg_sq):
+    ld = _mat(master, torch.float32, "master", n, k)
+    if (_mat(exp_avg, torch.float32, "exp_avg", n, k) != ld
+            or _mat(exp_avg_sq, torch.float32, "exp_avg_sq", n, k) != ld):
+        raise ValueError("master, exp_avg and exp_avg_sq must share one row stride")
+    return ld
+
+
+def adam_selected(grad, sel: Selection, master, exp_avg, exp_avg_sq, weight, hp: AdamHparams,
+                  step: int, mode: int = STATES_INPLACE, src: Optional[StateSource] = None,
+                  stream=None) -> None:
+    n, m = grad.shape
+    ldg = _mat(grad, torch.bfloat16, "grad")
+    lds = _states(n, sel.k, master, exp_avg, exp_avg_sq)
+    ldw = _mat(weight, torch.bfloat16, "weight", n, m)
+    c_sel, c_hp = sel.as_c(), hp.as_c()
+    c_src = src.as_c() if src is not None else None
+    _check("zf_adam_selected", LIB.zf_adam_selected(
+        _ptr(grad), n, m, ldg, ctypes.byref(c_sel), sel.k, _ptr(master), _ptr(exp_avg),
+        _ptr(exp_avg_sq), lds, _ptr(weight), ldw, ctypes.byref(c_hp), step, mode,
+        ctypes.byref(c_src) if c_src is not None else None, _stream(stream)))
+
+
+def pack_accumulate(grad, sel: Selection, acc, step_in_interval: int, accum_interval: int,
+                    stream=None) -> None:
+    n, m = grad.shape
+    ldg = _mat(grad, torch.bfloat16, "grad")
+    lda = _mat(acc, torch.float32, "acc", n, m - sel.k)
+    c_sel = sel.as_c()
+    _check("zf_pack_accumulate", LIB.zf_pack_accumulate(
+        _ptr(grad), n, m, ldg, ctypes.byref(c_sel), sel.k, _ptr(acc), lda, step_in_interval,
+        accum_interval, _stream(stream)))
+
+
+def update_fused(grad, sel: Selection, master, exp_avg, exp_avg_sq, weight, hp: AdamHparams,
+                 step: int, acc, step_in_interval: int, accum_interval: int,
+                 mode: int = STATES_INPLACE, src: Optional[StateSource] = None,
+                 stream=None) -> None:
+    n, m = grad.shape
+    ldg = _mat(grad, torch.bfloat16, "grad")
+    lds = _states(n, sel.k, master, exp_avg, exp_avg_sq)
+    ldw = _mat(weight, torch.bfloat16, "weight", n, m)
+    lda = _mat(acc, torch.float32, "acc", n, m - sel.k)
+    c_sel, c_hp = sel.as_c(), hp.as_c()
+    c_src = src.as_c() if src is not None else None
+    _check("zf_update_fused", LIB.zf_update_fused(
+        _ptr(grad), n, m, ldg, ctypes.byref(c_sel), sel.k, _ptr(master), _ptr(exp_avg),
+        _ptr(exp_avg_sq), lds, _ptr(weight), ldw, ctypes.byref(c_hp), step, mode,
+        ctypes.byref(c_src) if c_src is not None else None, _ptr(acc), lda, step_in_interval,
+        accum_interval, _stream(stream)))
+
+
+def unpack(acc, sel: Selection, scale: float = 1.0, out: Optional[torch.Tensor] = None,
+           stream=None) -> torch.Tensor:
+    n = acc.shape[0]
+    m = sel.m
+    lda = _mat(acc, torch.float32, "acc", n, m - sel.k)
+    if out is None:
+        out = torch.empty(n, m, dtype=torch.float32, device=acc.device)
+    ldo = _mat(out, torch.float32, "out", n, m)
+    c_sel = sel.as_c()
+    _check("zf_unpack", LIB.zf_unpack(_ptr(acc), lda, ctypes.byref(c_sel), sel.k, n, m,
+                                      float(scale), _ptr(out), ldo, _stream(stream)))
+    return out
+
+
+# ---------------------------------------------------------------------------
+# batched plans
+# ---------------------------------------------------------------------------
+
+@dataclass
+class MatrixBuffers:
+    """Device tensors of one matrix of a batch; unused stages may be None."""
+    grad: torch.Tensor
+    k: int
+    sel: Selection
+    weight: Optional[torch.Tensor] = None
+    master: Optional[torch.Tensor] = None
+    exp_avg: Optional[torch.Tensor] = None
+    exp_avg_sq: Optional[torch.Tensor] = None
+    acc: Optional[torch.Tensor] = None
+    norms: Optional[torch.Tensor] = None
+    unpacked: Optional[torch.Tensor] = None
+    src: Optional[StateSource] = None
+
+    def as_c(self) -> ZfMatrix:
+        n, m = self.grad.shape
+        x = ZfMatrix()
+        x.n, x.m, x.k = n, m, self.k
+        x.grad, x.ld_grad = _ptr(self.grad), _mat(self.grad, torch.bfloat16, "grad")
+        if self.weight is not None:
+            x.weight, x.ld_weight = _ptr(self.weight), _mat(self.weight, torch.bfloat16, "weight", n, m)
+        if self.master is not None:
+            x.master, x.exp_avg, x.exp_avg_sq = (_ptr(self.master), _ptr(self.exp_avg),
+                                                 _ptr(self.exp_avg_sq))
+            x.ld_state = _states(n, self.k, self.master, self.exp_avg, self.exp_avg_sq)
+        if self.acc is not None:
+            x.acc, x.ld_acc = _ptr(self.acc), _mat(self.acc, torch.float32, "acc", n, m - self.k)
+        if self.norms is not None:
+            _vec(self.norms, torch.float32, "norms", m)
+            x.norms_sq = _ptr(self.norms)
+        x.sel = self.sel.as_c()
+        if self.unpacked is not None:
+            x.unpacked = _ptr(self.unpacked)
+            x.ld_unpacked = _mat(self.unpacked, torch.float32, "unpacked", n, m)
+        if self.src is not None:
+            x.src = self.src.as_c()
+        return x
+
+
+class Plan:
+    """A batch of matrices run by one launch per kernel (zf_plan_*)."""
+
+    def __init__(self, mats: Sequence[MatrixBuffers]):
+        self.mats: List[MatrixBuffers] = list(mats)  # keeps the tensors alive
+        arr = (ZfMatrix * len(self.mats))(*[b.as_c() for b in self.mats])
+        h = c_vp()
+        _check("zf_plan_create", LIB.zf_plan_create(arr, len(self.mats), ctypes.byref(h)))
+        self._h = h
+
+    @property
+    def device_bytes(self) -> int:
+        return LIB.zf_plan_device_bytes(self._h)
+
+    def colnorm(self, stream=None) -> None:
+        _check("zf_plan_colnorm", LIB.zf_plan_colnorm(self._h, _stream(stream)))
+
+    def topk_select(self, stream=None) -> None:
+        _check("zf_plan_topk_select", LIB.zf_plan_topk_select(self._h, _stream(stream)))
+
+    def update(self, hp: AdamHparams, step: int, mode: int, step_in_interval: int,
+               accum_interval: int, adam: bool = True, pack: bool = True, stream=None) -> None:
+        c_hp = hp.as_c()
+        _check("zf_plan_update", LIB.zf_plan_update(
+            self._h, ctypes.byref(c_hp), step, mode, step_in_interval, accum_interval,
+            int(adam), int(pack), _stream(stream)))
+
+    def unpack(self, scale: float, stream=None) -> None:
+        _check("zf_plan_unpack", LIB.zf_plan_unpack(self._h, float(scale), _stream(stream)))
+
+    def close(self) -> None:
+        if getattr(self, "_h", None):
+            LIB.zf_plan_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,623 @@
+// Host entry points of libzf: argument validation, launch geometry, Adam
+// constants and the batched plan.  Every check runs before the first HIP
+// call, so invalid arguments enqueue nothing (and never touch a device).
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "zf.h"
+#include "zf_internal.hpp"
+
+using zf::AdamK;
+using zf::DevMat;
+using zf::Table;
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+zf_status hip_fail(hipError_t e) {
+  g_last_hip_error = static_cast<int>(e);
+  return ZF_EHIP;
+}
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// A row-major [rows][ld] buffer of `width` used elements per row must have
+// ld >= width, be present when it holds data, and be element-aligned.
+bool matrix_ok(const void* p, int64_t rows, int64_t width, int64_t ld, size_t elem) {
+  if (rows < 0 || width < 0 || ld < width) return false;
+  if (rows == 0 || width == 0) return true;
+  return p != nullptr && aligned(p, elem);
+}
+
+bool vector_ok(const void* p, int64_t count, size_t elem) {
+  if (count < 0) return false;
+  if (count == 0) return true;
+  return p != nullptr && aligned(p, elem);
+}
+
+struct Span {
+  uintptr_t lo = 0, hi = 0;
+};
+
+Span span_of(const void* p, int64_t rows, int64_t width, int64_t ld, size_t elem) {
+  Span s;
+  if (p == nullptr || rows <= 0 || width <= 0) return s;
+  s.lo = reinterpret_cast<uintptr_t>(p);
+  s.hi = s.lo + static_cast<uintptr_t>(((rows - 1) * ld + width)) * elem;
+  return s;
+}
+
+bool overlaps(const Span& a, const Span& b) {
+  return a.hi > a.lo && b.hi > b.lo && a.lo < b.hi && b.lo < a.hi;
+}
+
+bool hparams_ok(const zf_adam_hparams* hp) {
+  if (hp == nullptr) return false;
+  const auto fin = [](double x) { return std::isfinite(x); };
+  return fin(hp->lr) && hp->lr >= 0.0 && fin(hp->eps) && hp->eps >= 0.0 && fin(hp->beta1) &&
+         hp->beta1 >= 0.0 && hp->beta1 < 1.0 && fin(hp->beta2) && hp->beta2 >= 0.0 &&
+         hp->beta2 < 1.0 && fin(hp->weight_decay) && hp->weight_decay >= 0.0;
+}
+
+AdamK adam_consts(const zf_adam_hparams& hp, int64_t step) {
+  const double t = static_cast<double>(step);
+  AdamK c;
+  c.b1 = static_cast<float>(hp.beta1);
+  c.b2 = static_cast<float>(hp.beta2);
+  c.c1 = static_cast<float>(1.0 - hp.beta1);
+  c.c2 = static_cast<float>(1.0 - hp.beta2);
+  c.lr = static_cast<float>(hp.lr);
+  c.eps = static_cast<float>(hp.eps);
+  c.wd = static_cast<float>(hp.lr * hp.weight_decay);
+  c.ib1 = static_cast<float>(1.0 / (1.0 - std::pow(hp.beta1, t)));
+  c.ib2 = static_cast<float>(1.0 / (1.0 - std::pow(hp.beta2, t)));
+  return c;
+}
+
+// ---- geometry -------------------------------------------------------------
+
+constexpr int64_t kMinBlocks = 2048;          // enough blocks to fill 256 CUs
+constexpr int64_t kMaxBlocks = int64_t(1) << 23;  // grid x block stays < 2^32
+
+int64_t colnorm_blocks(int64_t n, int64_t m, int rpb) {
+  if (n <= 0 || m <= 0) return 0;
+  return ceil_div(m, zf::kColnormCols) * ceil_div(n, rpb);
+}
+
+int64_t update_blocks(int64_t n, int64_t m, int rows) {
+  if (n <= 0 || m <= 0) return 0;
+  return ceil_div(m, zf::kUpdateCols) * ceil_div(n, rows);
+}
+
+// Rows per colnorm block: 256 (partials cost 8 B per column per 256 rows,
+// ~1.6% of G), halved down to 16 while the whole grid is too small.
+int pick_colnorm_rows(const std::vector<std::pair<int64_t, int64_t>>& shapes) {
+  int rpb = 256;
+  for (;;) {
+    int64_t total = 0;
+    for (auto& s : shapes) total += colnorm_blocks(s.first, s.second, rpb);
+    if (total >= kMinBlocks || rpb <= 16) return rpb;
+    rpb >>= 1;
+  }
+}
+
+int pick_update_rows(const std::vector<std::pair<int64_t, int64_t>>& shapes) {
+  int rows = 64;
+  for (;;) {
+    int64_t total = 0;
+    for (auto& s : shapes) total += update_blocks(s.first, s.second, rows);
+    if (total > kMaxBlocks && rows < (1 << 20)) {
+      rows <<= 1;
+      continue;
+    }
+    if (total >= kMinBlocks || rows <= 4) return rows;
+    rows >>= 1;
+  }
+}
+
+void set_geometry(DevMat& d, int cn_rows, int up_rows) {
+  d.cn_rpb = cn_rows;
+  d.cn_cb = static_cast<int32_t>(ceil_div(d.m, zf::kColnormCols));
+  d.cn_rb = d.n > 0 ? static_cast<int32_t>(ceil_div(d.n, cn_rows)) : 0;
+  d.up_rows = up_rows;
+  d.up_cb = static_cast<int32_t>(ceil_div(d.m, zf::kUpdateCols));
+  d.up_rb = d.n > 0 ? static_cast<int32_t>(ceil_div(d.n, up_rows)) : 0;
+  d.vec = (d.grad != nullptr && aligned(d.grad, 16) && d.ld_grad % 8 == 0) ? 1 : 0;
+}
+
+DevMat blank() {
+  DevMat d;
+  std::memset(&d, 0, sizeof(d));
+  return d;
+}
+
+Table single_table() { return Table{nullptr, nullptr, 1}; }
+
+hipStream_t as_stream(zf_stream s) { return reinterpret_cast<hipStream_t>(s); }
+
+// ---- per-matrix validation -------------------------------------------------
+
+bool selection_ok(const zf_selection* s, int64_t m, int64_t k, bool need_idx) {
+  if (s == nullptr) return false;
+  const int64_t words = ceil_div(m, 64);
+  if (!vector_ok(s->sel_mask, words, 8) || !vector_ok(s->sel_prefix, words, 4)) return false;
+  if (need_idx && (!vector_ok(s->sel_idx, k, 4) || !vector_ok(s->unsel_idx, m - k, 4)))
+    return false;
+  return true;
+}
+
+bool shape_ok(int64_t n, int64_t m, int64_t k) {
+  return n >= 0 && m >= 0 && k >= 0 && k <= m && n < (int64_t(1) << 40) &&
+         m < (int64_t(1) << 31);
+}
+
+// Checks of one Adam step's buffers (selection mask/prefix already checked).
+bool adam_args_ok(const DevMat& d, int32_t mode, Span g) {
+  const int64_t n = d.n, m = d.m, k = d.k;
+  if (!matrix_ok(d.P, n, k, d.ld_state, 4) || !matrix_ok(d.M, n, k, d.ld_state, 4) ||
+      !matrix_ok(d.V, n, k, d.ld_state, 4) || !matrix_ok(d.weight, n, m, d.ld_weight, 2))
+    return false;
+  if (mode != zf::kInplace && mode != zf::kRemap && mode != zf::kInit) return false;
+  if (mode == zf::kRemap) {
+    const int64_t words = ceil_div(m, 64);
+    if (!vector_ok(d.prev_mask, words, 8) || !vector_ok(d.prev_prefix, words, 4)) return false;
+    // previous states may hold up to m slots; their width is checked per use
+    // on the device side by construction (prev_prefix + lanes < previous k).
+    if (n > 0 && k > 0 &&
+        (d.prev_P == nullptr || d.prev_M == nullptr || d.prev_V == nullptr ||
+         !aligned(d.prev_P, 4) || !aligned(d.prev_M, 4) || !aligned(d.prev_V, 4) ||
+         d.ld_prev < 0))
+      return false;
+  }
+  if (mode != zf::kInplace && d.init_P != nullptr &&
+      !matrix_ok(d.init_P, n, m, d.ld_init, 4))
+    return false;
+  const Span outs[4] = {span_of(d.P, n, k, d.ld_state, 4), span_of(d.M, n, k, d.ld_state, 4),
+                        span_of(d.V, n, k, d.ld_state, 4),
+                        span_of(d.weight, n, m, d.ld_weight, 2)};
+  for (int a = 0; a < 4; ++a) {
+    if (overlaps(outs[a], g)) return false;
+    for (int b = a + 1; b < 4; ++b)
+      if (overlaps(outs[a], outs[b])) return false;
+  }
+  return true;
+}
+
+bool pack_args_ok(const DevMat& d, int64_t sii, int64_t S, Span g) {
+  if (S < 1 || sii < 1 || sii > S) return false;
+  if (!matrix_ok(d.acc, d.n, d.m - d.k, d.ld_acc, 4)) return false;
+  return !overlaps(span_of(d.acc, d.n, d.m - d.k, d.ld_acc, 4), g);
+}
+
+DevMat base_mat(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
+                const zf_selection* sel, int64_t k) {
+  DevMat d = blank();
+  d.n = n;
+  d.m = m;
+  d.k = k;
+  d.grad = grad;
+  d.ld_grad = ld_grad;
+  if (sel != nullptr) {
+    d.sel_idx = sel->sel_idx;
+    d.unsel_idx = sel->unsel_idx;
+    d.mask = sel->sel_mask;
+    d.prefix = sel->sel_prefix;
+  }
+  return d;
+}
+
+void apply_source(DevMat& d, const zf_state_source* src) {
+  if (src == nullptr) return;
+  d.prev_mask = src->prev_mask;
+  d.prev_prefix = src->prev_prefix;
+  d.prev_P = src->prev_master;
+  d.prev_M = src->prev_exp_avg;
+  d.prev_V = src->prev_exp_avg_sq;
+  d.ld_prev = src->ld_prev;
+  d.init_P = src->init_master;
+  d.ld_init = src->ld_init;
+}
+
+zf_status run_update(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
+                     const zf_selection* sel, int64_t k, float* master, float* exp_avg,
+                     float* exp_avg_sq, int64_t ld_state, uint16_t* weight, int64_t ld_weight,
+                     const zf_adam_hparams* hp, int64_t step, int32_t mode,
+                     const zf_state_source* src, float* acc, int64_t ld_acc, int64_t sii,
+                     int64_t S, bool adam, bool pack, zf_stream stream) {
+  if (!shape_ok(n, m, k) || !matrix_ok(grad, n, m, ld_grad, 2)) return ZF_EINVAL;
+  if (!selection_ok(sel, m, k, false)) return ZF_EINVAL;
+  DevMat d = base_mat(grad, n, m, ld_grad, sel, k);
+  const Span g = span_of(grad, n, m, ld_grad, 2);
+  AdamK c{};
+  if (adam) {
+    if (!hparams_ok(hp) || step < 1) return ZF_EINVAL;
+    if (mode == zf::kRemap && src == nullptr) return ZF_EINVAL;
+    d.P = master;
+    d.M = exp_avg;
+    d.V = exp_avg_sq;
+    d.ld_state = ld_state;
+    d.weight = weight;
+    d.ld_weight = ld_weight;
+    apply_source(d, src);
+    if (!adam_args_ok(d, mode, g)) return ZF_EINVAL;
+    c = adam_consts(*hp, step);
+  }
+  if (pack) {
+    d.acc = acc;
+    d.ld_acc = ld_acc;
+    if (!pack_args_ok(d, sii, S, g)) return ZF_EINVAL;
+    if (adam) {
+      const Span a = span_of(acc, n, m - k, ld_acc, 4);
+      if (overlaps(a, span_of(master, n, k, ld_state, 4)) ||
+          overlaps(a, span_of(exp_avg, n, k, ld_state, 4)) ||
+          overlaps(a, span_of(exp_avg_sq, n, k, ld_state, 4)) ||
+          overlaps(a, span_of(weight, n, m, ld_weight, 2)))
+        return ZF_EINVAL;
+    }
+  }
+  if ((!adam || k == 0) && (!pack || k == m)) return ZF_OK;  // no column to touch
+  const int rows = pick_update_rows({{n, m}});
+  set_geometry(d, 256, rows);
+  const int64_t blocks = update_blocks(n, m, rows);
+  if (blocks == 0) return ZF_OK;
+  const hipError_t e = zf::launch_update(single_table(), d, blocks, c, adam ? mode : 0,
+                                         sii == 1 ? 1 : 0, adam, pack, as_stream(stream));
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
+}  // namespace
+
+// ===========================================================================
+// C ABI
+// ===========================================================================
+
+extern "C" {
+
+const char* zf_status_string(int status) {
+  switch (status) {
+    case ZF_OK: return "ZF_OK";
+    case ZF_EINVAL: return "ZF_EINVAL: invalid argument";
+    case ZF_EWORKSPACE: return "ZF_EWORKSPACE: workspace too small";
+    case ZF_EHIP: return "ZF_EHIP: HIP call failed";
+    case ZF_ENOMEM: return "ZF_ENOMEM: device allocation failed";
+    default: return "unknown zf status";
+  }
+}
+
+int zf_last_hip_error(void) { return g_last_hip_error; }
+
+int64_t zf_k_from_ratio(double ratio, int64_t m) {
+  if (!(ratio >= 0.0 && ratio <= 1.0) || m < 0) return -1;
+  const double k = std::floor(ratio * static_cast<double>(m) + 0.5);
+  return std::max<int64_t>(0, std::min<int64_t>(m, static_cast<int64_t>(k)));
+}
+
+size_t zf_colnorm_workspace_bytes(int64_t n, int64_t m) {
+  if (n <= 0 || m <= 0) return 0;
+  const int rpb = pick_colnorm_rows({{n, m}});
+  return static_cast<size_t>(ceil_div(n, rpb)) * static_cast<size_t>(m) * sizeof(double);
+}
+
+zf_status zf_colnorm(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
+                     float* norms_sq, void* ws, size_t ws_bytes, zf_stream stream) {
+  if (!shape_ok(n, m, 0) || !matrix_ok(grad, n, m, ld_grad, 2) ||
+      !vector_ok(norms_sq, m, 4))
+    return ZF_EINVAL;
+  if (overlaps(span_of(grad, n, m, ld_grad, 2), span_of(norms_sq, 1, m, m, 4))) return ZF_EINVAL;
+  const size_t need = zf_colnorm_workspace_bytes(n, m);
+  if (need > 0 && (ws == nullptr || ws_bytes < need || !aligned(ws, 8))) return ZF_EWORKSPACE;
+  if (need > 0 && overlaps(Span{reinterpret_cast<uintptr_t>(ws),
+                                reinterpret_cast<uintptr_t>(ws) + need},
+                           span_of(norms_sq, 1, m, m, 4)))
+    return ZF_EINVAL;
+  if (m == 0) return ZF_OK;
+  DevMat d = base_mat(grad, n, m, ld_grad, nullptr, 0);
+  d.norms = norms_sq;
+  set_geometry(d, n > 0 ? pick_colnorm_rows({{n, m}}) : 256, 64);
+  d.cn_ws = 0;
+  const hipError_t e = zf::launch_colnorm(single_table(), d, colnorm_blocks(n, m, d.cn_rpb),
+                                          single_table(), ceil_div(m, zf::kFinalizeCols),
+                                          static_cast<double*>(ws), as_stream(stream));
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
+zf_status zf_topk_select(const float* norms_sq, int64_t m, double ratio, const zf_selection* out,
+                         int64_t* k_out, zf_stream stream) {
+  const int64_t k = zf_k_from_ratio(ratio, m);
+  if (k < 0 || !shape_ok(0, m, k) || !vector_ok(norms_sq, m, 4) ||
+      !selection_ok(out, m, k, true))
+    return ZF_EINVAL;
+  if (m >= (int64_t(1) << 31)) return ZF_EINVAL;
+  const Span in = span_of(norms_sq, 1, m, m, 4);
+  const Span outs[4] = {span_of(out->sel_idx, 1, k, k, 4), span_of(out->unsel_idx, 1, m - k, m - k, 4),
+                        span_of(out->sel_mask, 1, ceil_div(m, 64), ceil_div(m, 64), 8),
+                        span_of(out->sel_prefix, 1, ceil_div(m, 64), ceil_div(m, 64), 4)};
+  for (int a = 0; a < 4; ++a) {
+    if (overlaps(outs[a], in)) return ZF_EINVAL;
+    for (int b = a + 1; b < 4; ++b)
+      if (overlaps(outs[a], outs[b])) return ZF_EINVAL;
+  }
+  if (k_out != nullptr) *k_out = k;
+  if (m == 0) return ZF_OK;
+  DevMat d = base_mat(nullptr, 0, m, m, out, k);
+  d.norms = const_cast<float*>(norms_sq);
+  const hipError_t e = zf::launch_topk(single_table(), d, 1, as_stream(stream));
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
+zf_status zf_adam_selected(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
+                           const zf_selection* sel, int64_t k, float* master, float* exp_avg,
+                           float* exp_avg_sq, int64_t ld_state, uint16_t* weight,
+                           int64_t ld_weight, const zf_adam_hparams* hp, int64_t step,
+                           int32_t mode, const zf_state_source* src, zf_stream stream) {
+  return run_update(grad, n, m, ld_grad, sel, k, master, exp_avg, exp_avg_sq, ld_state, weight,
+                    ld_weight, hp, step, mode, src, nullptr, 0, 1, 1, true, false, stream);
+}
+
+zf_status zf_pack_accumulate(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
+                             const zf_selection* sel, int64_t k, float* acc, int64_t ld_acc,
+                             int64_t step_in_interval, int64_t accum_interval,
+                             zf_stream stream) {
+  return run_update(grad, n, m, ld_grad, sel, k, nullptr, nullptr, nullptr, 0, nullptr, 0,
+                    nullptr, 1, 0, nullptr, acc, ld_acc, step_in_interval, accum_interval, false,
+                    true, stream);
+}
+
+zf_status zf_update_fused(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
+                          const zf_selection* sel, int64_t k, float* master, float* exp_avg,
+                          float* exp_avg_sq, int64_t ld_state, uint16_t* weight,
+                          int64_t ld_weight, const zf_adam_hparams* hp, int64_t step,
+                          int32_t mode, const zf_state_source* src, float* acc, int64_t ld_acc,
+                          int64_t step_in_interval, int64_t accum_interval, zf_stream stream) {
+  return run_update(grad, n, m, ld_grad, sel, k, master, exp_avg, exp_avg_sq, ld_state, weight,
+                    ld_weight, hp, step, mode, src, acc, ld_acc, step_in_interval,
+                    accum_interval, true, true, stream);
+}
+
+zf_status zf_unpack(const float* acc, int64_t ld_acc, const zf_selection* sel, int64_t k,
+                    int64_t n, int64_t m, float scale, float* out, int64_t ld_out,
+                    zf_stream stream) {
+  if (!shape_ok(n, m, k) || !selection_ok(sel, m, k, false) ||
+      !matrix_ok(acc, n, m - k, ld_acc, 4) || !matrix_ok(out, n, m, ld_out, 4))
+    return ZF_EINVAL;
+  if (overlaps(span_of(acc, n, m - k, ld_acc, 4), span_of(out, n, m, ld_out, 4)))
+    return ZF_EINVAL;
+  DevMat d = base_mat(nullptr, n, m, 0, sel, k);
+  d.acc = const_cast<float*>(acc);
+  d.ld_acc = ld_acc;
+  d.out = out;
+  d.ld_out = ld_out;
+  const int rows = pick_update_rows({{n, m}});
+  set_geometry(d, 256, rows);
+  const int64_t blocks = update_blocks(n, m, rows);
+  if (blocks == 0) return ZF_OK;
+  const hipError_t e = zf::launch_unpack(single_table(), d, blocks, scale, as_stream(stream));
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
+}  // extern "C"
+
+// ===========================================================================
+// Plans
+// ===========================================================================
+
+struct zf_plan {
+  int32_t nmats = 0;
+  std::vector<DevMat> mats;
+  void* dev = nullptr;
+  size_t dev_bytes = 0;
+  DevMat* d_mats = nullptr;
+  int64_t* d_off_cn = nullptr;
+  int64_t* d_off_fin = nullptr;
+  int64_t* d_off_top = nullptr;
+  int64_t* d_off_up = nullptr;
+  double* d_ws = nullptr;
+  int64_t blk_cn = 0, blk_fin = 0, blk_top = 0, blk_up = 0;
+  bool can_colnorm = true, can_topk = true, can_adam = true, can_remap = true, can_pack = true,
+       can_unpack = true;
+};
+
+namespace {
+
+// Validates what a descriptor provides; records which stages it can run.
+zf_status check_plan_matrix(const zf_matrix& x, zf_plan& p) {
+  const int64_t n = x.n, m = x.m, k = x.k;
+  if (!shape_ok(n, m, k)) return ZF_EINVAL;
+  const int64_t words = ceil_div(m, 64);
+  const Span g = span_of(x.grad, n, m, x.ld_grad, 2);
+  const bool have_grad = matrix_ok(x.grad, n, m, x.ld_grad, 2) && (x.grad || n * m == 0);
+  const bool have_mask = vector_ok(x.sel.sel_mask, words, 8) && vector_ok(x.sel.sel_prefix, words, 4) &&
+                         ((x.sel.sel_mask && x.sel.sel_prefix) || words == 0);
+  const bool have_idx = vector_ok(x.sel.sel_idx, k, 4) && vector_ok(x.sel.unsel_idx, m - k, 4) &&
+                        (x.sel.sel_idx || k == 0) && (x.sel.unsel_idx || m - k == 0);
+  const bool have_norms = vector_ok(x.norms_sq, m, 4) && (x.norms_sq || m == 0);
+  p.can_colnorm = p.can_colnorm && have_grad && have_norms && !overlaps(g, span_of(x.norms_sq, 1, m, m, 4));
+  p.can_topk = p.can_topk && have_norms && have_mask && have_idx;
+
+  DevMat d = base_mat(x.grad, n, m, x.ld_grad, &x.sel, k);
+  d.P = x.master;
+  d.M = x.exp_avg;
+  d.V = x.exp_avg_sq;
+  d.ld_state = x.ld_state;
+  d.weight = x.weight;
+  d.ld_weight = x.ld_weight;
+  apply_source(d, &x.src);
+  const bool have_states = (n * k == 0) || (x.master && x.exp_avg && x.exp_avg_sq && x.weight) ||
+                           (n * m == 0);
+  p.can_adam = p.can_adam && have_grad && have_mask && have_states &&
+               (n * k == 0 || adam_args_ok(d, zf::kInplace, g));
+  p.can_remap = p.can_remap && p.can_adam && (n * k == 0 || adam_args_ok(d, zf::kRemap, g));
+  d.acc = x.acc;
+  d.ld_acc = x.ld_acc;
+  const bool have_acc = (n * (m - k) == 0) || x.acc != nullptr;
+  p.can_pack = p.can_pack && have_grad && have_mask && have_acc && pack_args_ok(d, 1, 1, g);
+  const bool have_out = (n * m == 0) || x.unpacked != nullptr;
+  p.can_unpack = p.can_unpack && have_mask && have_acc && have_out &&
+                 matrix_ok(x.acc, n, m - k, x.ld_acc, 4) &&
+                 matrix_ok(x.unpacked, n, m, x.ld_unpacked, 4) &&
+                 !overlaps(span_of(x.acc, n, m - k, x.ld_acc, 4),
+                           span_of(x.unpacked, n, m, x.ld_unpacked, 4));
+  // Strides must be valid whenever the buffer is given.
+  if (x.weight && !matrix_ok(x.weight, n, m, x.ld_weight, 2)) return ZF_EINVAL;
+  if (x.acc && !matrix_ok(x.acc, n, m - k, x.ld_acc, 4)) return ZF_EINVAL;
+  if (x.unpacked && !matrix_ok(x.unpacked, n, m, x.ld_unpacked, 4)) return ZF_EINVAL;
+  if (x.grad && !have_grad) return ZF_EINVAL;
+  return ZF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
+  if (mats == nullptr || nmats < 1 || out == nullptr) return ZF_EINVAL;
+  zf_plan* p = new (std::nothrow) zf_plan();
+  if (p == nullptr) return ZF_ENOMEM;
+  p->nmats = nmats;
+  std::vector<std::pair<int64_t, int64_t>> shapes;
+  for (int32_t q = 0; q < nmats; ++q) {
+    const zf_status st = check_plan_matrix(mats[q], *p);
+    if (st != ZF_OK) {
+      delete p;
+      return st;
+    }
+    shapes.emplace_back(mats[q].n, mats[q].m);
+  }
+  const int cn_rows = pick_colnorm_rows(shapes);
+  const int up_rows = pick_update_rows(shapes);
+  std::vector<int64_t> off_cn(nmats + 1), off_fin(nmats + 1), off_top(nmats + 1),
+      off_up(nmats + 1);
+  int64_t ws_doubles = 0;
+  p->mats.resize(nmats);
+  for (int32_t q = 0; q < nmats; ++q) {
+    const zf_matrix& x = mats[q];
+    DevMat d = base_mat(x.grad, x.n, x.m, x.ld_grad, &x.sel, x.k);
+    d.P = x.master;
+    d.M = x.exp_avg;
+    d.V = x.exp_avg_sq;
+    d.ld_state = x.ld_state;
+    d.weight = x.weight;
+    d.ld_weight = x.ld_weight;
+    d.acc = x.acc;
+    d.ld_acc = x.ld_acc;
+    d.norms = x.norms_sq;
+    d.out = x.unpacked;
+    d.ld_out = x.ld_unpacked;
+    apply_source(d, &x.src);
+    set_geometry(d, cn_rows, up_rows);
+    d.cn_ws = ws_doubles;
+    ws_doubles += static_cast<int64_t>(d.cn_rb) * d.m;
+    off_cn[q] = p->blk_cn;
+    off_fin[q] = p->blk_fin;
+    off_top[q] = p->blk_top;
+    off_up[q] = p->blk_up;
+    p->blk_cn += colnorm_blocks(d.n, d.m, cn_rows);
+    p->blk_fin += ceil_div(d.m, zf::kFinalizeCols);
+    p->blk_top += 1;
+    p->blk_up += update_blocks(d.n, d.m, up_rows);
+    p->mats[q] = d;
+  }
+  off_cn[nmats] = p->blk_cn;
+  off_fin[nmats] = p->blk_fin;
+  off_top[nmats] = p->blk_top;
+  off_up[nmats] = p->blk_up;
+
+  const size_t mats_bytes = sizeof(DevMat) * nmats;
+  const size_t off_bytes = sizeof(int64_t) * (nmats + 1);
+  const size_t head = (mats_bytes + 4 * off_bytes + 255) & ~size_t(255);
+  p->dev_bytes = head + sizeof(double) * static_cast<size_t>(ws_doubles);
+  hipError_t e = hipMalloc(&p->dev, p->dev_bytes);
+  if (e != hipSuccess) {
+    g_last_hip_error = static_cast<int>(e);
+    delete p;
+    return ZF_ENOMEM;
+  }
+  char* base = static_cast<char*>(p->dev);
+  p->d_mats = reinterpret_cast<DevMat*>(base);
+  p->d_off_cn = reinterpret_cast<int64_t*>(base + mats_bytes);
+  p->d_off_fin = p->d_off_cn + (nmats + 1);
+  p->d_off_top = p->d_off_fin + (nmats + 1);
+  p->d_off_up = p->d_off_top + (nmats + 1);
+  p->d_ws = reinterpret_cast<double*>(base + head);
+  std::vector<char> host(head, 0);
+  std::memcpy(host.data(), p->mats.data(), mats_bytes);
+  std::memcpy(host.data() + mats_bytes, off_cn.data(), off_bytes);
+  std::memcpy(host.data() + mats_bytes + off_bytes, off_fin.data(), off_bytes);
+  std::memcpy(host.data() + mats_bytes + 2 * off_bytes, off_top.data(), off_bytes);
+  std::memcpy(host.data() + mats_bytes + 3 * off_bytes, off_up.data(), off_bytes);
+  e = hipMemcpy(p->dev, host.data(), head, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    g_last_hip_error = static_cast<int>(e);
+    (void)hipFree(p->dev);
+    delete p;
+    return ZF_EHIP;
+  }
+  *out = p;
+  return ZF_OK;
+}
+
+void zf_plan_destroy(zf_plan* plan) {
+  if (plan == nullptr) return;
+  if (plan->dev != nullptr) {
+    (void)hipDeviceSynchronize();
+    (void)hipFree(plan->dev);
+  }
+  delete plan;
+}
+
+size_t zf_plan_device_bytes(const zf_plan* plan) { return plan ? plan->dev_bytes : 0; }
+
+zf_status zf_plan_colnorm(zf_plan* p, zf_stream stream) {
+  if (p == nullptr || !p->can_colnorm) return ZF_EINVAL;
+  const Table t{p->d_mats, p->d_off_cn, p->nmats};
+  const Table tf{p->d_mats, p->d_off_fin, p->nmats};
+  const hipError_t e = zf::launch_colnorm(t, p->mats[0], p->blk_cn, tf, p->blk_fin, p->d_ws,
+                                          as_stream(stream));
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
+zf_status zf_plan_topk_select(zf_plan* p, zf_stream stream) {
+  if (p == nullptr || !p->can_topk) return ZF_EINVAL;
+  const Table t{p->d_mats, p->d_off_top, p->nmats};
+  const hipError_t e = zf::launch_topk(t, p->mats[0], p->blk_top, as_stream(stream));
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
+zf_status zf_plan_update(zf_plan* p, const zf_adam_hparams* hp, int64_t step, int32_t mode,
+                         int64_t step_in_interval, int64_t accum_interval, int32_t do_adam,
+                         int32_t do_pack, zf_stream stream) {
+  if (p == nullptr || (!do_adam && !do_pack)) return ZF_EINVAL;
+  AdamK c{};
+  if (do_adam) {
+    if (!p->can_adam || !hparams_ok(hp) || step < 1) return ZF_EINVAL;
+    if (mode != zf::kInplace && mode != zf::kRemap && mode != zf::kInit) return ZF_EINVAL;
+    if (mode == zf::kRemap && !p->can_remap) return ZF_EINVAL;
+    c = adam_consts(*hp, step);
+  }
+  if (do_pack) {
+    if (!p->can_pack || accum_interval < 1 || step_in_interval < 1 ||
+        step_in_interval > accum_interval)
+      return ZF_EINVAL;
+  }
+  const Table t{p->d_mats, p->d_off_up, p->nmats};
+  const hipError_t e =
+      zf::launch_update(t, p->mats[0], p->blk_up, c, do_adam ? mode : 0,
+                        step_in_interval == 1 ? 1 : 0, do_adam != 0, do_pack != 0,
+                        as_stream(stream));
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
+zf_status zf_plan_unpack(zf_plan* p, float scale, zf_stream stream) {
+  if (p == nullptr || !p->can_unpack) return ZF_EINVAL;
+  const Table t{p->d_mats, p->d_off_up, p->nmats};
+  const hipError_t e = zf::launch_unpack(t, p->mats[0], p->blk_up, scale, as_stream(stream));
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
+}  // extern "C"

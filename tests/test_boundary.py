@@ -1,0 +1,180 @@
+"""The C ABI without a GPU: the library loads, exports every function that
+include/zf.h declares, and rejects invalid arguments on the host before any
+HIP call (fake device addresses are never dereferenced)."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+from tests.conftest import ROOT
+
+zf = pytest.importorskip("paper_2505_12242_amd")
+from paper_2505_12242_amd import _lib  # noqa: E402
+
+LIB = _lib.LIB
+OK, EINVAL, EWS = _lib.ZF_OK, _lib.ZF_EINVAL, _lib.ZF_EWORKSPACE
+A = 0x7F0000000000  # a 256-byte aligned fake device address
+B = A + (1 << 30)
+C = A + (2 << 30)
+D = A + (3 << 30)
+E = A + (4 << 30)
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "zf.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(zf_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_function_is_exported_and_bound():
+    names = header_functions()
+    assert len(names) >= 16
+    raw = ctypes.CDLL(_lib.LIB_PATH)
+    bound = {s[0] for s in _lib.SIGNATURES}
+    for name in names:
+        assert hasattr(raw, name), name
+        assert name in bound, name
+
+
+def test_status_strings():
+    for s in range(5):
+        assert LIB.zf_status_string(s).decode().startswith("ZF_")
+    assert b"unknown" in LIB.zf_status_string(99)
+    assert LIB.zf_last_hip_error() == 0
+
+
+@pytest.mark.parametrize("ratio,m,k", [(0.1, 4096, 410), (0.25, 2, 1), (0.0, 5, 0), (1.0, 5, 5),
+                                       (0.05, 11008, 550), (0.1, 28672, 2867), (0.5, 0, 0)])
+def test_k_from_ratio(ratio, m, k):
+    assert LIB.zf_k_from_ratio(ratio, m) == k
+
+
+@pytest.mark.parametrize("ratio,m", [(-0.01, 5), (1.01, 5), (math.nan, 5), (0.5, -1)])
+def test_k_from_ratio_invalid(ratio, m):
+    assert LIB.zf_k_from_ratio(ratio, m) == -1
+
+
+def sel(m, k, base=C):
+    words = (m + 63) // 64
+    return _lib.ZfSelection(base, base + 4 * max(k, 1) + 256, base + (1 << 20), base + (2 << 20))
+
+
+def test_colnorm_validation():
+    ws = LIB.zf_colnorm_workspace_bytes(64, 64)
+    assert ws > 0 and LIB.zf_colnorm_workspace_bytes(0, 64) == 0
+    call = LIB.zf_colnorm
+    assert call(None, 4, 4, 4, B, C, ws, None) == EINVAL          # null gradient
+    assert call(A, 4, 4, 3, B, C, ws, None) == EINVAL             # ld < m
+    assert call(A + 1, 4, 4, 4, B, C, ws, None) == EINVAL         # misaligned bf16
+    assert call(A, 4, 4, 4, B + 2, C, ws, None) == EINVAL         # misaligned fp32
+    assert call(A, -1, 4, 4, B, C, ws, None) == EINVAL            # n < 0
+    assert call(A, 4, 4, 4, A + 8, C, ws, None) == EINVAL         # output inside gradient
+    assert call(A, 64, 64, 64, B, None, 0, None) == EWS           # no workspace
+    assert call(A, 64, 64, 64, B, C, ws - 8, None) == EWS         # small workspace
+    assert call(A, 4, 0, 4, None, None, 0, None) == OK            # m = 0: nothing to do
+
+
+def test_topk_validation():
+    s = sel(100, 10)
+    call = LIB.zf_topk_select
+    kout = ctypes.c_int64(-7)
+    assert call(A, 100, 1.5, ctypes.byref(s), ctypes.byref(kout), None) == EINVAL
+    assert call(A, 100, math.nan, ctypes.byref(s), None, None) == EINVAL
+    assert call(A, 100, 0.1, None, None, None) == EINVAL
+    assert call(None, 100, 0.1, ctypes.byref(s), None, None) == EINVAL
+    bad = _lib.ZfSelection(C, None, C + (1 << 20), C + (2 << 20))
+    assert call(A, 100, 0.1, ctypes.byref(bad), None, None) == EINVAL   # unsel missing
+    alias = _lib.ZfSelection(A, C + 4096, C + (1 << 20), C + (2 << 20))
+    assert call(A, 100, 0.1, ctypes.byref(alias), None, None) == EINVAL  # writes over scores
+    assert call(None, 0, 0.1, ctypes.byref(s), ctypes.byref(kout), None) == OK
+    assert kout.value == 0
+
+
+def adam_args(**over):
+    hp = _lib.ZfAdamHparams(1e-5, 0.9, 0.999, 1e-8, 0.0)
+    args = dict(grad=A, n=8, m=64, ld=64, sel=sel(64, 6), k=6, P=B, M=B + (1 << 20),
+                V=B + (2 << 20), lds=6, W=D, ldw=64, hp=hp, step=1, mode=0, src=None)
+    args.update(over)
+    return args
+
+
+def call_adam(a):
+    return LIB.zf_adam_selected(a["grad"], a["n"], a["m"], a["ld"], ctypes.byref(a["sel"]),
+                                a["k"], a["P"], a["M"], a["V"], a["lds"], a["W"], a["ldw"],
+                                ctypes.byref(a["hp"]), a["step"], a["mode"],
+                                ctypes.byref(a["src"]) if a["src"] is not None else None, None)
+
+
+@pytest.mark.parametrize("over", [
+    dict(step=0),
+    dict(k=65),
+    dict(lds=5),
+    dict(ldw=63),
+    dict(mode=7),
+    dict(mode=1),                                  # remap without a source
+    dict(M=B),                                     # exp_avg aliases master
+    dict(W=A + 64),                                # weight overlaps gradient
+    dict(P=None),
+    dict(hp=_lib.ZfAdamHparams(1e-5, 1.0, 0.999, 1e-8, 0.0)),
+    dict(hp=_lib.ZfAdamHparams(1e-5, 0.9, 0.999, -1.0, 0.0)),
+    dict(hp=_lib.ZfAdamHparams(math.inf, 0.9, 0.999, 1e-8, 0.0)),
+    dict(hp=_lib.ZfAdamHparams(1e-5, 0.9, 0.999, 1e-8, -0.1)),
+])
+def test_adam_validation(over):
+    assert call_adam(adam_args(**over)) == EINVAL
+
+
+def test_adam_remap_needs_previous_states():
+    src = _lib.ZfStateSource(E, E + 4096, None, None, None, 0, None, 0)
+    assert call_adam(adam_args(mode=1, src=src)) == EINVAL
+
+
+def test_adam_empty_is_ok_without_device():
+    assert call_adam(adam_args(n=0)) == OK
+    assert call_adam(adam_args(k=0, P=None, M=None, V=None, lds=0, sel=sel(64, 0))) == OK
+
+
+@pytest.mark.parametrize("sii,S", [(0, 4), (5, 4), (1, 0)])
+def test_pack_validation(sii, S):
+    s = sel(64, 6)
+    assert LIB.zf_pack_accumulate(A, 8, 64, 64, ctypes.byref(s), 6, B, 58, sii, S, None) == EINVAL
+
+
+def test_pack_rejects_short_stride_and_alias():
+    s = sel(64, 6)
+    assert LIB.zf_pack_accumulate(A, 8, 64, 64, ctypes.byref(s), 6, B, 57, 1, 4, None) == EINVAL
+    assert LIB.zf_pack_accumulate(A, 8, 64, 64, ctypes.byref(s), 6, A, 58, 1, 4, None) == EINVAL
+    assert LIB.zf_pack_accumulate(A, 0, 64, 64, ctypes.byref(s), 6, B, 58, 1, 4, None) == OK
+
+
+def test_unpack_validation():
+    s = sel(64, 6)
+    assert LIB.zf_unpack(B, 58, ctypes.byref(s), 6, 8, 64, 1.0, B + 64, 64, None) == EINVAL
+    assert LIB.zf_unpack(B, 58, ctypes.byref(s), 6, 8, 64, 1.0, D, 63, None) == EINVAL
+    assert LIB.zf_unpack(B, 58, None, 6, 8, 64, 1.0, D, 64, None) == EINVAL
+    assert LIB.zf_unpack(B, 58, ctypes.byref(s), 70, 8, 64, 1.0, D, 64, None) == EINVAL
+
+
+def test_update_fused_validation():
+    s = sel(64, 6)
+    hp = _lib.ZfAdamHparams(1e-5, 0.9, 0.999, 1e-8, 0.0)
+    # accumulator aliasing the master states
+    assert LIB.zf_update_fused(A, 8, 64, 64, ctypes.byref(s), 6, B, B + (1 << 20), B + (2 << 20), 6,
+                               D, 64, ctypes.byref(hp), 1, 0, None, B, 58, 1, 4, None) == EINVAL
+    assert LIB.zf_update_fused(A, 8, 64, 64, ctypes.byref(s), 6, B, B + (1 << 20), B + (2 << 20), 6,
+                               D, 64, ctypes.byref(hp), 1, 0, None, E, 58, 2, 1, None) == EINVAL
+
+
+def test_plan_validation():
+    h = ctypes.c_void_p()
+    assert LIB.zf_plan_create(None, 1, ctypes.byref(h)) == EINVAL
+    arr = (_lib.ZfMatrix * 1)()
+    assert LIB.zf_plan_create(arr, 0, ctypes.byref(h)) == EINVAL
+    arr[0].n, arr[0].m, arr[0].k = 4, 4, 5          # k > m
+    assert LIB.zf_plan_create(arr, 1, ctypes.byref(h)) == EINVAL
+    assert LIB.zf_plan_colnorm(None, None) == EINVAL
+    assert LIB.zf_plan_update(None, None, 1, 0, 1, 1, 1, 1, None) == EINVAL
+    assert LIB.zf_plan_device_bytes(None) == 0
+    LIB.zf_plan_destroy(None)
