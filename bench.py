@@ -1,0 +1,328 @@
+#!/usr/bin/env python3
+"""Throughput of the selective-update hot path on one MI355X.
+
+Workload (default): the full Llama-2-7B-shaped gradient set -- embedding,
+32 decoder layers (q/k/v/o 4096x4096, gate/up 11008x4096, down 4096x11008)
+and LM head, 226 matrices, 6,738,149,376 parameters -- with bf16 gradients
+(lognormal(0, 1.5) column scales, 5% temporal jitter), fp32 compact Adam
+states, top-k ratio 10%, selection refresh R = 4 and accumulation interval
+S = 4.  Gradients live in a ring of device buffers generated before timing
+(step t reads slot (t-1) mod slots), so every input is resident in HBM when
+the timed region starts.
+
+A step is one pass of the whole hot path over the set: on refresh steps
+column scores + top-k, then the fused Adam/pack pass (states remapped on
+refresh), and on interval ends the dense hand-over (unpack).  Warm-up steps
+are untimed; the timed steps are bracketed by device synchronisation.
+
+Prints one JSON line: algorithmic GB/s (value), fraction of the 8 TB/s HBM
+peak, params/s, per-kernel times, the roofline of the dominant kernel
+(the fused Adam/pack pass) and the CPU oracle timed on a bounded sample.
+"""
+
+from __future__ import annotations
+
+import argparse
+import contextlib
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
+PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "update_kernel_llama2-7b-full_traffic.md")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2505_12242_amd", "csrc", "zf_kernels.hip")
+
+
+def parse_args(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=16)
+    ap.add_argument("--warmup", type=int, default=4)
+    ap.add_argument("--workload", default="llama2-7b-full")
+    ap.add_argument("--slots", type=int, default=3, help="gradient buffers in the ring")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-steps", type=int, default=4)
+    ap.add_argument("--calibration-copy-gib", type=float, default=1.0,
+                    help="size of the plain copy launched once for PMC calibration (0: skip)")
+    return ap.parse_args(argv)
+
+
+# ---------------------------------------------------------------------------
+# byte model: the bytes each kernel must move, per matrix
+# ---------------------------------------------------------------------------
+
+def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool) -> dict:
+    """Algorithmic HBM bytes of one step, by kernel.
+
+    colnorm  2nm (read G) + 4m (write scores)          refresh steps
+    topk     4m (read scores) + 4m (write indices)
+             + 12 ceil(m/64) (mask and prefix)         refresh steps
+    update   28nk: per selected element G 2 + P/M/V 12 read + 12 write + W 2;
+             6nu / 10nu: per unselected element G 2 + A 4 write (+ A 4 read
+             after the interval's first step)
+    unpack   4nu (read A) + 4nm (write the dense buffer)  interval ends
+    """
+    out = {"colnorm": 0, "topk_select": 0, "update": 0, "unpack": 0}
+    for (n, m), k in zip(shapes, ks):
+        u = m - k
+        if refresh:
+            out["colnorm"] += 2 * n * m + 4 * m
+            out["topk_select"] += 8 * m + 12 * ((m + 63) // 64)
+        out["update"] += 28 * n * k + (6 if first else 10) * n * u
+        if end:
+            out["unpack"] += 4 * n * u + 4 * n * m
+    return out
+
+
+# ---------------------------------------------------------------------------
+# device-resident synthetic gradient set
+# ---------------------------------------------------------------------------
+
+def build_set(wl, slots: int, device):
+    import torch
+    from workloads import derive_seed, gradient, master_weights, step_scales
+    import paper_2505_12242_amd as zf
+
+    shapes = [(mt.n, mt.m) for mt in wl.matrices]
+    ks = [zf.k_from_ratio(wl.ratio, m) for _, m in shapes]
+    grad_slots = []
+    for s in range(slots):
+        t = s + 1
+        buf = []
+        for q, (n, m) in enumerate(shapes):
+            sc = step_scales(wl, q, t, k_boundary=ks[q])
+            buf.append(gradient(n, m, sc, derive_seed(wl.seed, q, "grad", t), device=device))
+        grad_slots.append(buf)
+    weights = []
+    for q, (n, m) in enumerate(shapes):
+        w = master_weights(n, m, derive_seed(wl.seed, q, "master"), wl.master_std, device=device)
+        weights.append(w.to(torch.bfloat16))
+        del w
+    return shapes, ks, grad_slots, weights
+
+
+# ---------------------------------------------------------------------------
+# CPU oracle baseline on a bounded sample
+# ---------------------------------------------------------------------------
+
+def cpu_baseline(wl, shapes, ks, grad_slots, weights0, steps: int) -> dict:
+    """Times the oracle (as it stands) over the first decoder layer's seven
+    matrices for `steps` steps of the workload's schedule, on the host."""
+    import numpy as np
+    import torch
+    import oracle as O
+
+    qs = [q for q, mt in enumerate(wl.matrices) if mt.name.startswith("layers.0.")]
+    if not qs:
+        qs = [0]
+    hp = wl.hyper
+    host_g = {}
+    for q in qs:
+        for t in range(1, steps + 1):
+            s = (t - 1) % len(grad_slots)
+            if (q, s) not in host_g:
+                host_g[(q, s)] = grad_slots[s][q].view(torch.int16).cpu().numpy().view(np.uint16)
+    elapsed = 0.0
+    nbytes = 0
+    for q in qs:
+        W = weights0[q]
+        orc = O.MatrixOracle(O.widen(W), W, wl.ratio, hp.lr, hp.beta1, hp.beta2, hp.eps,
+                             hp.weight_decay, wl.refresh, wl.accum)
+        for t in range(1, steps + 1):
+            G = host_g[(q, (t - 1) % len(grad_slots))]
+            t0 = time.perf_counter()
+            out = orc.step(G)
+            elapsed += time.perf_counter() - t0
+            kind = out["kind"]
+            b = step_bytes([shapes[q]], [ks[q]], kind.refresh, kind.step_in_interval == 1,
+                           kind.interval_end)
+            nbytes += sum(b.values())
+    params = sum(shapes[q][0] * shapes[q][1] for q in qs)
+    return {
+        "value": round(nbytes / elapsed / 1e9, 4),
+        "unit": "GB/s",
+        "params_per_s": round(params * steps / elapsed, 1),
+        "seconds": round(elapsed, 3),
+        "cores": 1,
+        "kind": "oracle",
+        "sample": (f"{len(qs)} matrices of the first decoder layer "
+                   f"({params:,} params), steps 1-{steps} of the R={wl.refresh}, "
+                   f"S={wl.accum} schedule, numpy oracle on one host thread"),
+    }
+
+
+# ---------------------------------------------------------------------------
+# PMC traffic recorded for the current kernel source
+# ---------------------------------------------------------------------------
+
+def kernel_source_hash() -> str:
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def recorded_traffic():
+    """Bytes per launch of the fused update kernel measured with rocprofv3
+    PMC counters (scaled by a plain copy's counter reading), if recorded for
+    the current kernel source."""
+    if not os.path.exists(PROFILE_TRAFFIC):
+        return None
+    text = open(PROFILE_TRAFFIC).read()
+    h = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
+    v = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not h or not v or h.group(1) != kernel_source_hash():
+        return None
+    return float(v.group(1))
+
+
+# ---------------------------------------------------------------------------
+
+def main(argv=None) -> int:
+    args = parse_args(argv)
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this build runs on one GPU only: the hot path of one GPU's "
+                                   "share is measured; --gpus must be 1"}), flush=True)
+        return 2
+
+    import numpy as np
+    import torch
+    import paper_2505_12242_amd as zf
+    from workloads import get_workload
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}), flush=True)
+        return 1
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    wl = get_workload(args.workload)
+    hp = zf.AdamHparams(wl.hyper.lr, wl.hyper.beta1, wl.hyper.beta2, wl.hyper.eps,
+                        wl.hyper.weight_decay)
+
+    t0 = time.perf_counter()
+    shapes, ks, grad_slots, weights = build_set(wl, args.slots, dev)
+    weights0 = None
+    if not args.no_cpu_baseline:
+        qs0 = [q for q, mt in enumerate(wl.matrices) if mt.name.startswith("layers.0.")] or [0]
+        weights0 = {q: weights[q].view(torch.int16).cpu().numpy().view(np.uint16) for q in qs0}
+    runner = zf.SelectiveUpdateRunner(shapes, wl.ratio, hp, wl.refresh, wl.accum, grad_slots,
+                                      weights, device=dev)
+    torch.cuda.synchronize()
+    setup_s = time.perf_counter() - t0
+    print(f"# setup {setup_s:.1f}s: {len(shapes)} matrices, {wl.params:,} params, "
+          f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB allocated", file=sys.stderr, flush=True)
+
+    # one plain copy of known size: the calibration point for PMC byte counters
+    if args.calibration_copy_gib > 0:
+        nb = int(args.calibration_copy_gib * 2**30)
+        src = torch.empty(nb // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    for _ in range(args.warmup):
+        runner.step()
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    spans = []  # (name, start event, end event)
+
+    @contextlib.contextmanager
+    def recorder(name):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        yield
+        b.record(stream)
+        spans.append((name, a, b))
+
+    kinds = []
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for _ in range(args.steps):
+        kinds.append(runner.step(recorder=recorder))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+
+    per_kernel_ms = {}
+    for name, a, b in spans:
+        per_kernel_ms.setdefault(name, []).append(a.elapsed_time(b))
+    totals = {"colnorm": 0, "topk_select": 0, "update": 0, "unpack": 0}
+    update_bytes = 0
+    for kind in kinds:
+        b = step_bytes(shapes, ks, kind.refresh, kind.step_in_interval == 1, kind.interval_end)
+        for key in totals:
+            totals[key] += b[key]
+    all_bytes = sum(totals.values())
+    update_bytes = totals["update"]
+    upd_ms = per_kernel_ms.get("update", []) + per_kernel_ms.get("update_first", [])
+    upd_launches = len(upd_ms)
+    upd_avg_ms = sum(upd_ms) / max(upd_launches, 1)
+    achieved = update_bytes / upd_launches / (upd_avg_ms * 1e-3) / 1e9 if upd_launches else 0.0
+
+    value = all_bytes / wall / 1e9
+    kernels = {}
+    for name, lst in per_kernel_ms.items():
+        key = "update" if name.startswith("update") else name
+        kernels.setdefault(name, {"launches": len(lst), "avg_ms": round(sum(lst) / len(lst), 4)})
+    for name in ("colnorm", "topk_select", "unpack"):
+        if name in per_kernel_ms and totals[name]:
+            tot_ms = sum(per_kernel_ms[name])
+            kernels[name]["GB/s"] = round(totals[name] / (tot_ms * 1e-3) / 1e9, 1)
+
+    traffic = recorded_traffic()
+    result = {
+        "metric": "GB/s and fraction of HBM peak per full step; params/s",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp32",
+        "data": "synthetic",
+        "frac_of_hbm_peak": round(value / HBM_PEAK_GBS, 4),
+        "params_per_s": round(wl.params * args.steps / wall, 1),
+        "config": {
+            "workload": wl.name,
+            "matrices": len(shapes),
+            "params": wl.params,
+            "grad_dtype": "bf16",
+            "state_dtype": "fp32",
+            "topk_ratio": wl.ratio,
+            "refresh_interval": wl.refresh,
+            "accum_interval": wl.accum,
+            "grad_slots": args.slots,
+            "algorithmic_GB_per_step": round(all_bytes / args.steps / 1e9, 3),
+        },
+        "kernels": kernels,
+        "roofline": {
+            "kernel": "update_kernel<true,true> (fused Adam + bf16 write-back + pack)",
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": traffic,
+            "bytes_per_launch": round(update_bytes / max(upd_launches, 1)),
+            "avg_launch_ms": round(upd_avg_ms, 4),
+        },
+    }
+    if not args.no_cpu_baseline:
+        print("# timing the CPU oracle on a sample ...", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(wl, shapes, ks, grad_slots, weights0,
+                                              args.cpu_sample_steps)
+    runner.close()
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

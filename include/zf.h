@@ -182,7 +182,8 @@ zf_status zf_topk_select(const float* norms_sq, int64_t m, double ratio,
  * operation is one fp32 IEEE operation (no contraction, correctly rounded
  * sqrt and division).  Unselected columns of W are not touched.
  * step: 1-based step counter used for bias correction.
- * sel: HOST struct; only sel_mask and sel_prefix are read. */
+ * sel: HOST struct; all four arrays are read and must describe one
+ * consistent selection (as zf_topk_select writes it). */
 zf_status zf_adam_selected(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
                            const zf_selection* sel, int64_t k,
                            float* master, float* exp_avg, float* exp_avg_sq, int64_t ld_state,
@@ -196,8 +197,8 @@ zf_status zf_adam_selected(const uint16_t* grad, int64_t n, int64_t m, int64_t l
  *   A[i][u] = G[i][j]              if step_in_interval == 1 (overwrite),
  *   A[i][u] = A[i][u] + G[i][j]    otherwise (one fp32 addition).
  * step_in_interval: 1-based position inside the accumulation interval of
- * accum_interval (= S) steps.  sel: HOST struct; sel_mask and sel_prefix are
- * read. */
+ * accum_interval (= S) steps.  sel: HOST struct; all four arrays are read
+ * and must describe one consistent selection. */
 zf_status zf_pack_accumulate(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
                              const zf_selection* sel, int64_t k,
                              float* acc, int64_t ld_acc,

@@ -107,8 +107,12 @@ int pick_colnorm_rows(const std::vector<std::pair<int64_t, int64_t>>& shapes) {
   }
 }
 
+#ifndef ZF_UPDATE_ROWS
+#define ZF_UPDATE_ROWS 8
+#endif
+
 int pick_update_rows(const std::vector<std::pair<int64_t, int64_t>>& shapes) {
-  int rows = 64;
+  int rows = ZF_UPDATE_ROWS;
   for (;;) {
     int64_t total = 0;
     for (auto& s : shapes) total += update_blocks(s.first, s.second, rows);
@@ -231,7 +235,7 @@ zf_status run_update(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad
                      const zf_state_source* src, float* acc, int64_t ld_acc, int64_t sii,
                      int64_t S, bool adam, bool pack, zf_stream stream) {
   if (!shape_ok(n, m, k) || !matrix_ok(grad, n, m, ld_grad, 2)) return ZF_EINVAL;
-  if (!selection_ok(sel, m, k, false)) return ZF_EINVAL;
+  if (!selection_ok(sel, m, k, true)) return ZF_EINVAL;
   DevMat d = base_mat(grad, n, m, ld_grad, sel, k);
   const Span g = span_of(grad, n, m, ld_grad, 2);
   AdamK c{};
@@ -450,13 +454,14 @@ zf_status check_plan_matrix(const zf_matrix& x, zf_plan& p) {
   apply_source(d, &x.src);
   const bool have_states = (n * k == 0) || (x.master && x.exp_avg && x.exp_avg_sq && x.weight) ||
                            (n * m == 0);
-  p.can_adam = p.can_adam && have_grad && have_mask && have_states &&
+  p.can_adam = p.can_adam && have_grad && have_mask && have_idx && have_states &&
                (n * k == 0 || adam_args_ok(d, zf::kInplace, g));
   p.can_remap = p.can_remap && p.can_adam && (n * k == 0 || adam_args_ok(d, zf::kRemap, g));
   d.acc = x.acc;
   d.ld_acc = x.ld_acc;
   const bool have_acc = (n * (m - k) == 0) || x.acc != nullptr;
-  p.can_pack = p.can_pack && have_grad && have_mask && have_acc && pack_args_ok(d, 1, 1, g);
+  p.can_pack = p.can_pack && have_grad && have_mask && have_idx && have_acc &&
+               pack_args_ok(d, 1, 1, g);
   const bool have_out = (n * m == 0) || x.unpacked != nullptr;
   p.can_unpack = p.can_unpack && have_mask && have_acc && have_out &&
                  matrix_ok(x.acc, n, m - k, x.ld_acc, 4) &&

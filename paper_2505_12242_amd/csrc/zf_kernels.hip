@@ -30,19 +30,62 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
                                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
 }
 
-__device__ __forceinline__ DevMat get_mat(const Table& t, const DevMat& one, int64_t b,
-                                          int64_t& local) {
-  if (t.mats == nullptr) {
+// Descriptor of the matrix block b belongs to.  BATCHED kernels read it
+// from the plan's device table (scalar loads); single-matrix kernels take it
+// by value.  Keeping the two apart avoids a generic pointer that would turn
+// the descriptor loads into flat vector loads.
+template <bool BATCHED>
+__device__ __forceinline__ DevMat get_mat(const DevMat* __restrict__ mats,
+                                          const int64_t* __restrict__ off, int32_t nmats,
+                                          const DevMat& one, int64_t b, int64_t& local) {
+  if constexpr (!BATCHED) {
     local = b;
     return one;
+  } else {
+    int lo = 0, hi = nmats - 1;
+    while (lo < hi) {  // largest q with off[q] <= b
+      const int mid = (lo + hi + 1) >> 1;
+      if (off[mid] <= b) lo = mid; else hi = mid - 1;
+    }
+    local = b - off[lo];
+    return mats[lo];
   }
-  int lo = 0, hi = t.nmats - 1;
-  while (lo < hi) {  // largest q with off[q] <= b
-    const int mid = (lo + hi + 1) >> 1;
-    if (t.off[mid] <= b) lo = mid; else hi = mid - 1;
-  }
-  local = b - t.off[lo];
-  return t.mats[lo];
+}
+
+// Raw buffer resources (gfx9 family word 3).  A resource is based at the
+// first row a block touches; lanes pass one 32-bit byte offset that is the
+// same for every row, the row part goes in the scalar offset.  num_records
+// is the exact byte span of the block's rows, so an access outside them is
+// dropped by the hardware rather than reaching other memory.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr int kRsrcWord3 = 0x00020000;
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, int64_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
+                                           static_cast<int>(bytes), kRsrcWord3);
+}
+
+// Resource over rows [i0, i1) of a row-major [.][ld] array of `width` used
+// elements of T per row.
+template <typename T>
+__device__ __forceinline__ rsrc_t rows_rsrc(const T* base, int64_t i0, int64_t i1, int64_t ld,
+                                            int64_t width) {
+  const int64_t rows = i1 - i0;
+  const int64_t bytes = rows > 0 ? ((rows - 1) * ld + width) * static_cast<int64_t>(sizeof(T)) : 0;
+  return make_rsrc(base + i0 * ld, bytes);
+}
+
+__device__ __forceinline__ float buf_f32(rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+}
+__device__ __forceinline__ uint16_t buf_u16(rsrc_t r, uint32_t voff, uint32_t soff) {
+  return static_cast<uint16_t>(__builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0));
+}
+__device__ __forceinline__ void buf_put_f32(float v, rsrc_t r, uint32_t voff, uint32_t soff) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, voff, soff, 0);
+}
+__device__ __forceinline__ void buf_put_u16(uint16_t v, rsrc_t r, uint32_t voff, uint32_t soff) {
+  __builtin_amdgcn_raw_buffer_store_b16(v, r, voff, soff, 0);
 }
 
 // ---------------------------------------------------------------------------
@@ -65,10 +108,11 @@ __device__ __forceinline__ void accum8(double (&acc)[8], uint4 v) {
   }
 }
 
-__global__ __launch_bounds__(kThreads) void colnorm_partial_kernel(Table t, DevMat one,
+template <bool BATCHED>
+__global__ __launch_bounds__(kThreads) void colnorm_partial_kernel(const DevMat* __restrict__ mats, const int64_t* __restrict__ off, int32_t nmats, DevMat one,
                                                                    double* __restrict__ ws) {
   int64_t local;
-  const DevMat d = get_mat(t, one, blockIdx.x, local);
+  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, blockIdx.x, local);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int64_t cblk = local % d.cn_cb;
@@ -127,10 +171,11 @@ __global__ __launch_bounds__(kThreads) void colnorm_partial_kernel(Table t, DevM
   }
 }
 
+template <bool BATCHED>
 __global__ __launch_bounds__(kFinalizeCols) void colnorm_finalize_kernel(
-    Table t, DevMat one, const double* __restrict__ ws) {
+    const DevMat* __restrict__ mats, const int64_t* __restrict__ off, int32_t nmats, DevMat one, const double* __restrict__ ws) {
   int64_t local;
-  const DevMat d = get_mat(t, one, blockIdx.x, local);
+  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, blockIdx.x, local);
   const int64_t j = local * kFinalizeCols + threadIdx.x;
   if (j >= d.m) return;
   double s = 0.0;
@@ -180,9 +225,10 @@ __device__ __forceinline__ uint32_t block_excl_count(bool flag, uint32_t* sh_wav
   return before + lanes_below(b);
 }
 
-__global__ __launch_bounds__(kTopkThreads) void topk_kernel(Table t, DevMat one) {
+template <bool BATCHED>
+__global__ __launch_bounds__(kTopkThreads) void topk_kernel(const DevMat* __restrict__ mats, const int64_t* __restrict__ off, int32_t nmats, DevMat one) {
   int64_t local;
-  const DevMat d = get_mat(t, one, blockIdx.x, local);
+  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, blockIdx.x, local);
   const int64_t m = d.m;
   const int64_t k = d.k;
   if (m == 0) return;
@@ -290,12 +336,16 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(Table t, DevMat one)
 
 // ---------------------------------------------------------------------------
 // a3-a5: selective Adam with bf16 write-back, and packing of the unselected
-// columns, in one pass over G.  Wave w of a block owns the 64 columns of
-// selection-mask word `word`; lane l owns column 64*word + l, so its slot in
-// the compact states is prefix[word] + (selected lanes below l) and its slot
-// in the accumulation buffer is column - that.  Consecutive lanes therefore
-// touch consecutive slots: coalesced state and accumulator traffic.  Rows
-// are processed four at a time to keep loads in flight.
+// columns, in one pass over G.  A block owns a 256-column tile (four mask
+// words) and a range of rows.  Its columns split into cu unselected slots
+// [us, us+cu) of the accumulation buffer and cs selected slots [rs, rs+cs)
+// of the compact states, both contiguous; thread t < cu owns unselected
+// slot us+t, thread cu <= t < cu+cs owns selected slot rs+t-cu.  Each
+// thread reads its column index once and then walks the rows: consecutive
+// lanes touch consecutive slots (fully coalesced A and P/M/V traffic), the
+// G gathers of a wave fall in one or two cache lines, and only the one or
+// two waves holding selected slots execute the Adam arithmetic.  Rows are
+// processed kRowBatch at a time with all loads issued before use.
 // ---------------------------------------------------------------------------
 
 __device__ __forceinline__ void adam_step(float g, float& p, float& m, float& v, const AdamK& c) {
@@ -307,94 +357,217 @@ __device__ __forceinline__ void adam_step(float g, float& p, float& m, float& v,
   p = p - c.lr * u;
 }
 
-constexpr int kRowBatch = 4;
+#ifndef ZF_PACK_BATCH
+#define ZF_PACK_BATCH 8
+#endif
+#ifndef ZF_ADAM_BATCH
+#define ZF_ADAM_BATCH 8
+#endif
+constexpr int kRowBatch = ZF_PACK_BATCH;   // rows in flight per pack lane (and unpack)
+constexpr int kAdamBatch = ZF_ADAM_BATCH;  // rows in flight per Adam lane
 
-template <bool ADAM, bool PACK>
-__global__ __launch_bounds__(kThreads) void update_kernel(Table t, DevMat one, AdamK c,
+// Selected and unselected slot ranges of the tile starting at column c0.
+struct TileSlots {
+  int64_t rs, cs, us, cu, width;
+};
+
+__device__ __forceinline__ TileSlots tile_slots(const DevMat& d, int64_t c0) {
+  TileSlots ts;
+  ts.width = min(static_cast<int64_t>(kUpdateCols), d.m - c0);
+  const int64_t words = (d.m + 63) >> 6;
+  const int64_t w1 = (c0 + ts.width + 63) >> 6;
+  ts.rs = d.prefix[c0 >> 6];
+  const int64_t re = (w1 < words) ? static_cast<int64_t>(d.prefix[w1]) : d.k;
+  ts.cs = re - ts.rs;
+  ts.cu = ts.width - ts.cs;
+  ts.us = c0 - ts.rs;
+  return ts;
+}
+
+// Pack lane: A[i][u] (+)= G[i][j] over the block's rows.
+template <bool FIRST>
+__device__ __forceinline__ void pack_rows(rsrc_t rG, uint32_t vG, uint32_t sG, rsrc_t rA,
+                                          uint32_t vA, uint32_t sA, int32_t rows) {
+  int32_t i = 0;
+  for (; i + kRowBatch <= rows; i += kRowBatch) {
+    uint16_t gb[kRowBatch];
+    float a[kRowBatch];
+#pragma unroll
+    for (int b = 0; b < kRowBatch; ++b) gb[b] = buf_u16(rG, vG, (i + b) * sG);
+    if constexpr (!FIRST) {
+#pragma unroll
+      for (int b = 0; b < kRowBatch; ++b) a[b] = buf_f32(rA, vA, (i + b) * sA);
+#pragma unroll
+      for (int b = 0; b < kRowBatch; ++b) a[b] = a[b] + widen_bf16(gb[b]);
+    } else {
+#pragma unroll
+      for (int b = 0; b < kRowBatch; ++b) a[b] = widen_bf16(gb[b]);
+    }
+#pragma unroll
+    for (int b = 0; b < kRowBatch; ++b) buf_put_f32(a[b], rA, vA, (i + b) * sA);
+  }
+  for (; i < rows; ++i) {
+    const float g = widen_bf16(buf_u16(rG, vG, i * sG));
+    if constexpr (FIRST) buf_put_f32(g, rA, vA, i * sA);
+    else buf_put_f32(buf_f32(rA, vA, i * sA) + g, rA, vA, i * sA);
+  }
+}
+
+// Where an Adam lane's (p, m, v) come from; see zf_state_mode.
+struct AdamSrc {
+  rsrc_t rP, rM, rV, rW;        // states and weight being written
+  uint32_t vS, sS, vG, sW;      // slot / column byte offsets, row strides
+  rsrc_t rSP, rSM, rSV;         // previous states (remap)
+  uint32_t vPrev, sPrev;
+  bool was;                     // column was selected before (remap)
+  rsrc_t rI;                    // fp32 init master (init from master)
+  uint32_t vI, sI;
+};
+
+enum SrcKind { kSrcInplace = 0, kSrcRemapW, kSrcRemapMaster, kSrcInitW, kSrcInitMaster };
+
+template <int SRC>
+__device__ __forceinline__ void load_state(const AdamSrc& a, int32_t i, float& p, float& m,
+                                           float& v) {
+  if constexpr (SRC == kSrcInplace) {
+    p = buf_f32(a.rP, a.vS, i * a.sS);
+    m = buf_f32(a.rM, a.vS, i * a.sS);
+    v = buf_f32(a.rV, a.vS, i * a.sS);
+  } else {
+    // init value of p for a newly selected column
+    float pi;
+    if constexpr (SRC == kSrcRemapMaster || SRC == kSrcInitMaster)
+      pi = buf_f32(a.rI, a.vI, i * a.sI);
+    else
+      pi = widen_bf16(buf_u16(a.rW, a.vG, i * a.sW));
+    if constexpr (SRC == kSrcRemapW || SRC == kSrcRemapMaster) {
+      // both sources are read; the lane keeps the one that applies
+      const float pp = buf_f32(a.rSP, a.vPrev, i * a.sPrev);
+      const float mp = buf_f32(a.rSM, a.vPrev, i * a.sPrev);
+      const float vp = buf_f32(a.rSV, a.vPrev, i * a.sPrev);
+      p = a.was ? pp : pi;
+      m = a.was ? mp : 0.0f;
+      v = a.was ? vp : 0.0f;
+    } else {
+      p = pi;
+      m = 0.0f;
+      v = 0.0f;
+    }
+  }
+}
+
+template <int SRC>
+__device__ __forceinline__ void adam_rows(const AdamSrc& a, rsrc_t rG, uint32_t sG,
+                                          const AdamK& c, int32_t rows) {
+  int32_t i = 0;
+  for (; i + kAdamBatch <= rows; i += kAdamBatch) {
+    uint16_t gb[kAdamBatch];
+    float p[kAdamBatch], mm[kAdamBatch], vv[kAdamBatch];
+#pragma unroll
+    for (int b = 0; b < kAdamBatch; ++b) gb[b] = buf_u16(rG, a.vG, (i + b) * sG);
+#pragma unroll
+    for (int b = 0; b < kAdamBatch; ++b) load_state<SRC>(a, i + b, p[b], mm[b], vv[b]);
+#pragma unroll
+    for (int b = 0; b < kAdamBatch; ++b) {
+      adam_step(widen_bf16(gb[b]), p[b], mm[b], vv[b], c);
+      const uint32_t so = (i + b) * a.sS;
+      buf_put_f32(p[b], a.rP, a.vS, so);
+      buf_put_f32(mm[b], a.rM, a.vS, so);
+      buf_put_f32(vv[b], a.rV, a.vS, so);
+      buf_put_u16(round_bf16(p[b]), a.rW, a.vG, (i + b) * a.sW);
+    }
+  }
+  for (; i < rows; ++i) {
+    float p, mm, vv;
+    const float g = widen_bf16(buf_u16(rG, a.vG, i * sG));
+    load_state<SRC>(a, i, p, mm, vv);
+    adam_step(g, p, mm, vv, c);
+    buf_put_f32(p, a.rP, a.vS, i * a.sS);
+    buf_put_f32(mm, a.rM, a.vS, i * a.sS);
+    buf_put_f32(vv, a.rV, a.vS, i * a.sS);
+    buf_put_u16(round_bf16(p), a.rW, a.vG, i * a.sW);
+  }
+}
+
+template <bool BATCHED, bool ADAM, bool PACK>
+__global__ __launch_bounds__(kThreads) void update_kernel(const DevMat* __restrict__ mats,
+                                                          const int64_t* __restrict__ off,
+                                                          int32_t nmats, DevMat one, AdamK c,
                                                           int32_t mode, int32_t first) {
   int64_t local;
-  const DevMat d = get_mat(t, one, blockIdx.x, local);
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, blockIdx.x, local);
   const int64_t cblk = local % d.up_cb;
   const int64_t rblk = local / d.up_cb;
-  const int64_t word = cblk * (kUpdateCols / 64) + wave;
-  const int64_t j = word * 64 + lane;
-  if (j >= d.m) return;
-
-  const uint64_t mw = d.mask[word];
-  const bool sel = (mw >> lane) & 1ull;
-  const int64_t r = static_cast<int64_t>(d.prefix[word]) + lanes_below(mw);
-  const int64_t u = j - r;
-  bool was = false;
-  int64_t ro = 0;
-  if (ADAM && mode == kRemap) {
-    const uint64_t pm = d.prev_mask[word];
-    was = (pm >> lane) & 1ull;
-    ro = static_cast<int64_t>(d.prev_prefix[word]) + lanes_below(pm);
-  }
-  const bool do_adam = ADAM && sel;
-  const bool do_pack = PACK && !sel;
-  if (!do_adam && !do_pack) return;
+  const int64_t c0 = cblk * kUpdateCols;
+  const TileSlots ts = tile_slots(d, c0);
+  const int tid = threadIdx.x;
+  const bool is_pack = PACK && tid < ts.cu;
+  const bool is_adam = ADAM && tid >= ts.cu && tid < ts.width;
+  if (!is_pack && !is_adam) return;
 
   const int64_t i0 = rblk * d.up_rows;
   const int64_t i1 = min(i0 + static_cast<int64_t>(d.up_rows), d.n);
-  const uint16_t* __restrict__ G = d.grad;
+  const int32_t rows = static_cast<int32_t>(i1 - i0);
+  const rsrc_t rG = rows_rsrc(d.grad, i0, i1, d.ld_grad, d.m);
+  const uint32_t sG = static_cast<uint32_t>(d.ld_grad * 2);  // bytes per G row
 
-  for (int64_t i = i0; i < i1; i += kRowBatch) {
-    float g[kRowBatch];
-#pragma unroll
-    for (int b = 0; b < kRowBatch; ++b)
-      g[b] = (i + b < i1) ? widen_bf16(G[(i + b) * d.ld_grad + j]) : 0.0f;
+  if (is_pack) {
+    const uint32_t u = static_cast<uint32_t>(ts.us + tid);
+    const uint32_t vG = static_cast<uint32_t>(d.unsel_idx[u]) * 2u;
+    const rsrc_t rA = rows_rsrc(d.acc, i0, i1, d.ld_acc, d.m - d.k);
+    const uint32_t sA = static_cast<uint32_t>(d.ld_acc * 4);
+    if (first) pack_rows<true>(rG, vG, sG, rA, u * 4u, sA, rows);
+    else pack_rows<false>(rG, vG, sG, rA, u * 4u, sA, rows);
+    return;
+  }
 
-    if (do_adam) {
-      float p[kRowBatch], mm[kRowBatch], vv[kRowBatch];
-#pragma unroll
-      for (int b = 0; b < kRowBatch; ++b) {
-        if (i + b >= i1) continue;
-        const int64_t row = i + b;
-        if (mode == kInplace) {
-          const int64_t o = row * d.ld_state + r;
-          p[b] = d.P[o];
-          mm[b] = d.M[o];
-          vv[b] = d.V[o];
-        } else if (mode == kRemap && was) {
-          const int64_t o = row * d.ld_prev + ro;
-          p[b] = d.prev_P[o];
-          mm[b] = d.prev_M[o];
-          vv[b] = d.prev_V[o];
-        } else {
-          p[b] = d.init_P ? d.init_P[row * d.ld_init + j]
-                          : widen_bf16(d.weight[row * d.ld_weight + j]);
-          mm[b] = 0.0f;
-          vv[b] = 0.0f;
-        }
-      }
-#pragma unroll
-      for (int b = 0; b < kRowBatch; ++b) {
-        if (i + b >= i1) continue;
-        const int64_t row = i + b;
-        adam_step(g[b], p[b], mm[b], vv[b], c);
-        const int64_t o = row * d.ld_state + r;
-        d.P[o] = p[b];
-        d.M[o] = mm[b];
-        d.V[o] = vv[b];
-        d.weight[row * d.ld_weight + j] = round_bf16(p[b]);
-      }
-    }
-    if (do_pack) {
-      float a[kRowBatch];
-#pragma unroll
-      for (int b = 0; b < kRowBatch; ++b) {
-        if (i + b >= i1) continue;
-        a[b] = first ? g[b] : d.acc[(i + b) * d.ld_acc + u] + g[b];
-      }
-#pragma unroll
-      for (int b = 0; b < kRowBatch; ++b) {
-        if (i + b >= i1) continue;
-        d.acc[(i + b) * d.ld_acc + u] = a[b];
-      }
-    }
+  // Adam lane: selected slot r, column j.
+  AdamSrc a;
+  const uint32_t r = static_cast<uint32_t>(ts.rs + (tid - ts.cu));
+  const uint32_t j = static_cast<uint32_t>(d.sel_idx[r]);
+  a.vS = r * 4u;
+  a.vG = j * 2u;
+  a.rP = rows_rsrc(d.P, i0, i1, d.ld_state, d.k);
+  a.rM = rows_rsrc(d.M, i0, i1, d.ld_state, d.k);
+  a.rV = rows_rsrc(d.V, i0, i1, d.ld_state, d.k);
+  a.sS = static_cast<uint32_t>(d.ld_state * 4);
+  a.rW = rows_rsrc(d.weight, i0, i1, d.ld_weight, d.m);
+  a.sW = static_cast<uint32_t>(d.ld_weight * 2);
+  a.rSP = a.rP;
+  a.rSM = a.rM;
+  a.rSV = a.rV;
+  a.vPrev = 0;
+  a.sPrev = 0;
+  a.was = false;
+  a.rI = a.rW;
+  a.vI = 0;
+  a.sI = 0;
+  const bool master = d.init_P != nullptr;
+  if (mode != kInplace && master) {
+    a.rI = rows_rsrc(d.init_P, i0, i1, d.ld_init, d.m);
+    a.vI = j * 4u;
+    a.sI = static_cast<uint32_t>(d.ld_init * 4);
+  }
+  if (mode == kRemap) {
+    const uint32_t w = j >> 6;
+    const uint64_t pm = d.prev_mask[w];
+    a.was = (pm >> (j & 63u)) & 1ull;
+    const uint32_t ro = static_cast<uint32_t>(d.prev_prefix[w]) +
+                        static_cast<uint32_t>(__popcll(pm & ((uint64_t(1) << (j & 63u)) - 1)));
+    // a column that was not selected reads slot 0 (any valid slot), unused
+    a.vPrev = (a.was ? ro : 0u) * 4u;
+    a.sPrev = static_cast<uint32_t>(d.ld_prev * 4);
+    a.rSP = rows_rsrc(d.prev_P, i0, i1, d.ld_prev, d.m);
+    a.rSM = rows_rsrc(d.prev_M, i0, i1, d.ld_prev, d.m);
+    a.rSV = rows_rsrc(d.prev_V, i0, i1, d.ld_prev, d.m);
+  }
+  if (mode == kInplace) adam_rows<kSrcInplace>(a, rG, sG, c, rows);
+  else if (mode == kRemap) {
+    if (master) adam_rows<kSrcRemapMaster>(a, rG, sG, c, rows);
+    else adam_rows<kSrcRemapW>(a, rG, sG, c, rows);
+  } else {
+    if (master) adam_rows<kSrcInitMaster>(a, rG, sG, c, rows);
+    else adam_rows<kSrcInitW>(a, rG, sG, c, rows);
   }
 }
 
@@ -402,9 +575,13 @@ __global__ __launch_bounds__(kThreads) void update_kernel(Table t, DevMat one, A
 // a6: hand-over.  Same column mapping as the update pass.
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(kThreads) void unpack_kernel(Table t, DevMat one, float scale) {
+template <bool BATCHED>
+__global__ __launch_bounds__(kThreads) void unpack_kernel(const DevMat* __restrict__ mats,
+                                                          const int64_t* __restrict__ off,
+                                                          int32_t nmats, DevMat one,
+                                                          float scale) {
   int64_t local;
-  const DevMat d = get_mat(t, one, blockIdx.x, local);
+  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, blockIdx.x, local);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int64_t cblk = local % d.up_cb;
@@ -414,53 +591,88 @@ __global__ __launch_bounds__(kThreads) void unpack_kernel(Table t, DevMat one, f
   if (j >= d.m) return;
   const uint64_t mw = d.mask[word];
   const bool sel = (mw >> lane) & 1ull;
-  const int64_t u = j - (static_cast<int64_t>(d.prefix[word]) + lanes_below(mw));
+  const uint32_t u =
+      static_cast<uint32_t>(j - (static_cast<int64_t>(d.prefix[word]) + lanes_below(mw)));
   const int64_t i0 = rblk * d.up_rows;
   const int64_t i1 = min(i0 + static_cast<int64_t>(d.up_rows), d.n);
-  for (int64_t i = i0; i < i1; i += kRowBatch) {
+  const int32_t rows = static_cast<int32_t>(i1 - i0);
+  const rsrc_t rA = rows_rsrc(d.acc, i0, i1, d.ld_acc, d.m - d.k);
+  const rsrc_t rD = rows_rsrc(d.out, i0, i1, d.ld_out, d.m);
+  const uint32_t sA = static_cast<uint32_t>(d.ld_acc * 4);
+  const uint32_t sD = static_cast<uint32_t>(d.ld_out * 4);
+  const uint32_t vD = static_cast<uint32_t>(j) * 4u;
+  int32_t i = 0;
+  if (d.m == d.k) {  // every column selected: no accumulated data to read
+    for (; i < rows; ++i) buf_put_f32(0.0f, rD, vD, i * sD);
+    return;
+  }
+  // A selected lane reads a neighbouring valid slot (same cache lines as its
+  // wave) and writes +0.0, so the wave runs one uniform loop.
+  const uint32_t vA = min(u, static_cast<uint32_t>(d.m - d.k - 1)) * 4u;
+  for (; i + kRowBatch <= rows; i += kRowBatch) {
     float a[kRowBatch];
 #pragma unroll
-    for (int b = 0; b < kRowBatch; ++b)
-      a[b] = (!sel && i + b < i1) ? d.acc[(i + b) * d.ld_acc + u] * scale : 0.0f;
+    for (int b = 0; b < kRowBatch; ++b) a[b] = buf_f32(rA, vA, (i + b) * sA);
 #pragma unroll
     for (int b = 0; b < kRowBatch; ++b)
-      if (i + b < i1) d.out[(i + b) * d.ld_out + j] = a[b];
+      buf_put_f32(sel ? 0.0f : a[b] * scale, rD, vD, (i + b) * sD);
+  }
+  for (; i < rows; ++i) {
+    const float a = buf_f32(rA, vA, i * sA);
+    buf_put_f32(sel ? 0.0f : a * scale, rD, vD, i * sD);
   }
 }
 
 }  // namespace
 
+#define ZF_LAUNCH(KERNEL, GRID, BLOCK, STREAM, T, ...)                                      \
+  do {                                                                                     \
+    if ((T).mats != nullptr)                                                               \
+      hipLaunchKernelGGL((KERNEL<true>), GRID, BLOCK, 0, STREAM, (T).mats, (T).off,          \
+                         (T).nmats, __VA_ARGS__);                                          \
+    else                                                                                   \
+      hipLaunchKernelGGL((KERNEL<false>), GRID, BLOCK, 0, STREAM, (T).mats, (T).off,         \
+                         (T).nmats, __VA_ARGS__);                                          \
+  } while (0)
+
 hipError_t launch_colnorm(const Table& t, const DevMat& one, int64_t blocks, const Table& tf,
                           int64_t fin_blocks, double* ws, hipStream_t s) {
   (void)hipGetLastError();
   if (blocks > 0)
-    hipLaunchKernelGGL(colnorm_partial_kernel, dim3(static_cast<uint32_t>(blocks)),
-                       dim3(kThreads), 0, s, t, one, ws);
+    ZF_LAUNCH(colnorm_partial_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), s, t,
+              one, ws);
   if (fin_blocks > 0)
-    hipLaunchKernelGGL(colnorm_finalize_kernel, dim3(static_cast<uint32_t>(fin_blocks)),
-                       dim3(kFinalizeCols), 0, s, tf, one, static_cast<const double*>(ws));
+    ZF_LAUNCH(colnorm_finalize_kernel, dim3(static_cast<uint32_t>(fin_blocks)),
+              dim3(kFinalizeCols), s, tf, one, static_cast<const double*>(ws));
   return hipGetLastError();
 }
 
 hipError_t launch_topk(const Table& t, const DevMat& one, int64_t blocks, hipStream_t s) {
   (void)hipGetLastError();
   if (blocks > 0)
-    hipLaunchKernelGGL(topk_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kTopkThreads), 0,
-                       s, t, one);
+    ZF_LAUNCH(topk_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kTopkThreads), s, t, one);
   return hipGetLastError();
+}
+
+template <bool ADAM, bool PACK>
+static void launch_update_t(const Table& t, const DevMat& one, dim3 grid, const AdamK& c,
+                            int32_t mode, int32_t first, hipStream_t s) {
+  if (t.mats != nullptr)
+    hipLaunchKernelGGL((update_kernel<true, ADAM, PACK>), grid, dim3(kThreads), 0, s, t.mats,
+                       t.off, t.nmats, one, c, mode, first);
+  else
+    hipLaunchKernelGGL((update_kernel<false, ADAM, PACK>), grid, dim3(kThreads), 0, s, t.mats,
+                       t.off, t.nmats, one, c, mode, first);
 }
 
 hipError_t launch_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
                          int32_t mode, int32_t first, bool adam, bool pack, hipStream_t s) {
   (void)hipGetLastError();
   if (blocks <= 0) return hipSuccess;
-  const dim3 grid(static_cast<uint32_t>(blocks)), block(kThreads);
-  if (adam && pack)
-    hipLaunchKernelGGL((update_kernel<true, true>), grid, block, 0, s, t, one, c, mode, first);
-  else if (adam)
-    hipLaunchKernelGGL((update_kernel<true, false>), grid, block, 0, s, t, one, c, mode, first);
-  else if (pack)
-    hipLaunchKernelGGL((update_kernel<false, true>), grid, block, 0, s, t, one, c, mode, first);
+  const dim3 grid(static_cast<uint32_t>(blocks));
+  if (adam && pack) launch_update_t<true, true>(t, one, grid, c, mode, first, s);
+  else if (adam) launch_update_t<true, false>(t, one, grid, c, mode, first, s);
+  else if (pack) launch_update_t<false, true>(t, one, grid, c, mode, first, s);
   return hipGetLastError();
 }
 
@@ -468,8 +680,8 @@ hipError_t launch_unpack(const Table& t, const DevMat& one, int64_t blocks, floa
                          hipStream_t s) {
   (void)hipGetLastError();
   if (blocks > 0)
-    hipLaunchKernelGGL(unpack_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0, s,
-                       t, one, scale);
+    ZF_LAUNCH(unpack_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), s, t, one,
+              scale);
   return hipGetLastError();
 }
 

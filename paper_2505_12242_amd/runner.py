@@ -48,6 +48,18 @@ def schedule(t: int, R: int, S: int) -> StepKind:
                     interval_end=(nxt - 1) % R == 0 or (nxt - 1) % S == 0)
 
 
+class _NoRecord:
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        return False
+
+
+def _no_record(name):
+    return _NoRecord()
+
+
 class SelectiveUpdateRunner:
     def __init__(self, shapes: Sequence[Tuple[int, int]], ratio: float, hp: AdamHparams,
                  refresh: int, accum: int, grad_slots: Sequence[Sequence[torch.Tensor]],
@@ -101,25 +113,32 @@ class SelectiveUpdateRunner:
     def state(self):
         return self.states[self.cur]
 
-    def step(self, stream=None) -> StepKind:
-        """Enqueues one step (no synchronisation)."""
+    def step(self, stream=None, recorder=None) -> StepKind:
+        """Enqueues one step (no synchronisation).  `recorder`, if given, is
+        called as recorder(name) -> context manager around each launch (used
+        to bracket launches with events on the launch stream)."""
         self.t += 1
         t = self.t
         kind = schedule(t, self.R, self.S)
         slot = (t - 1) % len(self.grad_slots)
+        rec = recorder if recorder is not None else _no_record
         if kind.refresh:
             nxt = 0 if t == 1 else 1 - self.cur
             plan = self.plans[slot][nxt]
-            plan.colnorm(stream)
-            plan.topk_select(stream)
+            with rec("colnorm"):
+                plan.colnorm(stream)
+            with rec("topk_select"):
+                plan.topk_select(stream)
             mode = STATES_INIT if t == 1 else STATES_REMAP
             self.cur = nxt
         else:
             plan = self.plans[slot][self.cur]
             mode = STATES_INPLACE
-        plan.update(self.hp, t, mode, kind.step_in_interval, self.S, stream=stream)
+        with rec("update_first" if kind.step_in_interval == 1 else "update"):
+            plan.update(self.hp, t, mode, kind.step_in_interval, self.S, stream=stream)
         if kind.interval_end:
-            plan.unpack(1.0 / kind.step_in_interval, stream)
+            with rec("unpack"):
+                plan.unpack(1.0 / kind.step_in_interval, stream)
         return kind
 
     def close(self) -> None:
