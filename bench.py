@@ -215,12 +215,14 @@ def main(argv=None) -> int:
     print(f"# setup {setup_s:.1f}s: {len(shapes)} matrices, {wl.params:,} params, "
           f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB allocated", file=sys.stderr, flush=True)
 
-    # one plain copy of known size: the calibration point for PMC byte counters
+    # one plain streaming kernel of known size (reads and writes exactly
+    # calibration_copy_gib GiB each): the calibration point for PMC counters
     if args.calibration_copy_gib > 0:
         nb = int(args.calibration_copy_gib * 2**30)
-        src = torch.empty(nb // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        src = torch.empty(nb // 4, dtype=torch.float32, device=dev).fill_(4.0)
         dst = torch.empty_like(src)
-        dst.copy_(src)
+        torch.cuda.synchronize()
+        torch.sqrt(src, out=dst)
         torch.cuda.synchronize()
         del src, dst
 
