@@ -34,7 +34,9 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "update_kernel_llama2-7b-full_traffic.md")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2505_12242_amd", "csrc", "zf_kernels.hip")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2505_12242_amd", "csrc", f)
+                  for f in ("zf_device.hpp", "zf_internal.hpp", "zf_kernels.hip",
+                            "zf_kernels_cm.hip")]
 
 
 def parse_args(argv=None):
@@ -44,6 +46,10 @@ def parse_args(argv=None):
     ap.add_argument("--warmup", type=int, default=4)
     ap.add_argument("--workload", default="llama2-7b-full")
     ap.add_argument("--slots", type=int, default=3, help="gradient buffers in the ring")
+    ap.add_argument("--layout", choices=["channel-major", "row-major"], default="channel-major",
+                    help="storage of every matrix: channel-major (each input channel one "
+                         "contiguous row, the paper's column-major gradient storage) or "
+                         "PyTorch's row-major [out, in]")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-steps", type=int, default=4)
     ap.add_argument("--calibration-copy-gib", type=float, default=1.0,
@@ -82,10 +88,16 @@ def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool) -> dict:
 # device-resident synthetic gradient set
 # ---------------------------------------------------------------------------
 
-def build_set(wl, slots: int, device):
+def build_set(wl, slots: int, device, layout: int = 0):
+    """Gradient ring and bf16 weights of workload wl on the device, stored in
+    `layout` (channel-major tensors are the transposes of the logical
+    [out, in] matrices)."""
     import torch
     from workloads import derive_seed, gradient, master_weights, step_scales
     import paper_2505_12242_amd as zf
+
+    def store(x):
+        return x if layout == zf.ROW_MAJOR else x.t().contiguous()
 
     shapes = [(mt.n, mt.m) for mt in wl.matrices]
     ks = [zf.k_from_ratio(wl.ratio, m) for _, m in shapes]
@@ -95,12 +107,13 @@ def build_set(wl, slots: int, device):
         buf = []
         for q, (n, m) in enumerate(shapes):
             sc = step_scales(wl, q, t, k_boundary=ks[q])
-            buf.append(gradient(n, m, sc, derive_seed(wl.seed, q, "grad", t), device=device))
+            buf.append(store(gradient(n, m, sc, derive_seed(wl.seed, q, "grad", t),
+                                      device=device)))
         grad_slots.append(buf)
     weights = []
     for q, (n, m) in enumerate(shapes):
         w = master_weights(n, m, derive_seed(wl.seed, q, "master"), wl.master_std, device=device)
-        weights.append(w.to(torch.bfloat16))
+        weights.append(store(w.to(torch.bfloat16)))
         del w
     return shapes, ks, grad_slots, weights
 
@@ -109,12 +122,17 @@ def build_set(wl, slots: int, device):
 # CPU oracle baseline on a bounded sample
 # ---------------------------------------------------------------------------
 
-def cpu_baseline(wl, shapes, ks, grad_slots, weights0, steps: int) -> dict:
+def cpu_baseline(wl, shapes, ks, grad_slots, weights0, steps: int, layout: int = 0) -> dict:
     """Times the oracle (as it stands) over the first decoder layer's seven
-    matrices for `steps` steps of the workload's schedule, on the host."""
+    matrices for `steps` steps of the workload's schedule, on the host.
+    Inputs are copied to the host in the logical [out, in] layout before
+    timing."""
     import numpy as np
     import torch
     import oracle as O
+
+    def logical(t):
+        return t if layout == 0 else t.t()
 
     qs = [q for q, mt in enumerate(wl.matrices) if mt.name.startswith("layers.0.")]
     if not qs:
@@ -125,7 +143,9 @@ def cpu_baseline(wl, shapes, ks, grad_slots, weights0, steps: int) -> dict:
         for t in range(1, steps + 1):
             s = (t - 1) % len(grad_slots)
             if (q, s) not in host_g:
-                host_g[(q, s)] = grad_slots[s][q].view(torch.int16).cpu().numpy().view(np.uint16)
+                host_g[(q, s)] = np.ascontiguousarray(
+                    logical(grad_slots[s][q]).contiguous().view(torch.int16).cpu().numpy()
+                    .view(np.uint16))
     elapsed = 0.0
     nbytes = 0
     for q in qs:
@@ -160,8 +180,11 @@ def cpu_baseline(wl, shapes, ks, grad_slots, weights0, steps: int) -> dict:
 # ---------------------------------------------------------------------------
 
 def kernel_source_hash() -> str:
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def recorded_traffic():
@@ -199,17 +222,21 @@ def main(argv=None) -> int:
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     wl = get_workload(args.workload)
+    layout = zf.CHANNEL_MAJOR if args.layout == "channel-major" else zf.ROW_MAJOR
     hp = zf.AdamHparams(wl.hyper.lr, wl.hyper.beta1, wl.hyper.beta2, wl.hyper.eps,
                         wl.hyper.weight_decay)
 
     t0 = time.perf_counter()
-    shapes, ks, grad_slots, weights = build_set(wl, args.slots, dev)
+    shapes, ks, grad_slots, weights = build_set(wl, args.slots, dev, layout)
     weights0 = None
     if not args.no_cpu_baseline:
         qs0 = [q for q, mt in enumerate(wl.matrices) if mt.name.startswith("layers.0.")] or [0]
-        weights0 = {q: weights[q].view(torch.int16).cpu().numpy().view(np.uint16) for q in qs0}
+        weights0 = {}
+        for q in qs0:
+            w = weights[q] if layout == zf.ROW_MAJOR else weights[q].t()
+            weights0[q] = w.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
     runner = zf.SelectiveUpdateRunner(shapes, wl.ratio, hp, wl.refresh, wl.accum, grad_slots,
-                                      weights, device=dev)
+                                      weights, device=dev, layout=layout)
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t0
     print(f"# setup {setup_s:.1f}s: {len(shapes)} matrices, {wl.params:,} params, "
@@ -296,6 +323,7 @@ def main(argv=None) -> int:
             "workload": wl.name,
             "matrices": len(shapes),
             "params": wl.params,
+            "layout": args.layout,
             "grad_dtype": "bf16",
             "state_dtype": "fp32",
             "topk_ratio": wl.ratio,
@@ -306,7 +334,8 @@ def main(argv=None) -> int:
         },
         "kernels": kernels,
         "roofline": {
-            "kernel": "update_kernel<true,true> (fused Adam + bf16 write-back + pack)",
+            "kernel": ("cm_update_kernel" if layout == zf.CHANNEL_MAJOR else "update_kernel")
+                      + " (fused Adam + bf16 write-back + pack)",
             "bound": "hbm",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,
@@ -320,7 +349,7 @@ def main(argv=None) -> int:
     if not args.no_cpu_baseline:
         print("# timing the CPU oracle on a sample ...", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(wl, shapes, ks, grad_slots, weights0,
-                                              args.cpu_sample_steps)
+                                              args.cpu_sample_steps, layout)
     runner.close()
     print(json.dumps(result), flush=True)
     return 0

@@ -37,12 +37,20 @@
  * Streams.  Work is enqueued on `stream` (a hipStream_t; NULL = the null
  *           stream); calls return without synchronising.  Device-side
  *           faults surface at the caller's next synchronisation.
- * Layouts.  G, W (bf16, passed as uint16_t bit patterns) and the dense
- *           unpack output are row-major [n][ld] with ld >= m.  The compact
- *           optimizer states P (master), M (first moment), V (second moment)
- *           are row-major [n][ld_state >= k]: slot r of a row belongs to
- *           column sel_idx[r].  The accumulation buffer A is row-major
- *           [n][ld_acc >= m-k]: slot u belongs to column unsel_idx[u].
+ * Layouts.  Every matrix of a call is stored in one of two layouts
+ *           (zf_layout).  ZF_LAYOUT_ROW_MAJOR is PyTorch's [out, in]: G, W
+ *           (bf16, passed as uint16_t bit patterns) and the dense unpack
+ *           output are [n][ld >= m]; the compact optimizer states P (master),
+ *           M (first moment), V (second moment) are [n][ld_state >= k], slot
+ *           r of a row belonging to column sel_idx[r]; the accumulation
+ *           buffer A is [n][ld_acc >= m-k], slot u belonging to column
+ *           unsel_idx[u].  ZF_LAYOUT_CHANNEL_MAJOR stores each of these
+ *           transposed, so that an input channel is one contiguous row (the
+ *           paper reorganises gradients column-major for channel access,
+ *           Implementation, "Fully Segmented Gradient Selection"): G, W and
+ *           the unpack output are [m][ld >= n], P/M/V are [k][ld_state >= n]
+ *           (row r = column sel_idx[r]), A is [m-k][ld_acc >= n] (row u =
+ *           column unsel_idx[u]).  Results are identical in both layouts.
  * Selection.  sel_idx[k] and unsel_idx[m-k] are ascending column indices;
  *           sel_mask[ceil(m/64)] has bit b of word w set iff column 64w+b is
  *           selected (bits at columns >= m are 0); sel_prefix[ceil(m/64)]
@@ -57,7 +65,10 @@
  *           ZF_EHIP: a HIP call failed (zf_last_hip_error() gives its code,
  *           per thread).  ZF_ENOMEM: a plan's device allocation failed.
  *           Sizes n = 0 or m = 0 are valid and enqueue no work, except that
- *           zf_colnorm with n = 0 writes zeros to its m scores.
+ *           zf_colnorm with n = 0 writes zeros to its m scores.  Limits:
+ *           n, m < 2^30; in the row-major layout the update and unpack
+ *           kernels address 8-row blocks through 32-bit offsets, so a row
+ *           stride times 8 must stay below 2 GiB.
  * Threads.  Entry points are reentrant.  Calls that share an output buffer,
  *           a workspace or a plan must be ordered by the caller.
  */
@@ -72,6 +83,11 @@ extern "C" {
 #endif
 
 typedef void* zf_stream; /* a hipStream_t */
+
+typedef enum zf_layout {
+  ZF_LAYOUT_ROW_MAJOR = 0,
+  ZF_LAYOUT_CHANNEL_MAJOR = 1
+} zf_layout;
 
 typedef enum zf_status {
   ZF_OK = 0,
@@ -122,7 +138,10 @@ typedef enum zf_state_mode {
 
 /* HOST struct of DEVICE pointers; fields unused by the chosen mode may be
  * NULL.  prev_mask / prev_prefix describe the previous selection of the same
- * matrix (same m); prev_* states are [n][ld_prev]. */
+ * matrix (same m); the prev_* states are compact states of that selection
+ * (as many slots as it has columns) with row stride ld_prev, in the call's
+ * layout; init_master is a full fp32 n x m master in the call's layout with
+ * row stride ld_init. */
 typedef struct zf_state_source {
   const uint64_t* prev_mask;
   const int32_t* prev_prefix;
@@ -147,16 +166,18 @@ int64_t zf_k_from_ratio(double ratio, int64_t m);
 
 /* ---- a1: column scores ------------------------------------------------- */
 
-/* Workspace bytes zf_colnorm needs for an n x m gradient. */
-size_t zf_colnorm_workspace_bytes(int64_t n, int64_t m);
+/* Workspace bytes zf_colnorm needs for an n x m gradient in `layout` (0 for
+ * the channel-major layout). */
+size_t zf_colnorm_workspace_bytes(int64_t n, int64_t m, int32_t layout);
 
 /* norms_sq[j] = sum over i < n of G[i][j]^2 (fp32 result; squares summed in
  * fp64, deterministic order), for j < m.
- * grad: [n][ld_grad] bf16; norms_sq: [m] fp32 output; ws: device workspace of
- * at least zf_colnorm_workspace_bytes(n, m) bytes (may be NULL if that is 0),
- * contents overwritten. */
+ * grad: bf16 in `layout` with row stride ld_grad; norms_sq: [m] fp32 output;
+ * ws: device workspace of at least zf_colnorm_workspace_bytes(n, m, layout)
+ * bytes (may be NULL if that is 0), contents overwritten. */
 zf_status zf_colnorm(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
-                     float* norms_sq, void* ws, size_t ws_bytes, zf_stream stream);
+                     int32_t layout, float* norms_sq, void* ws, size_t ws_bytes,
+                     zf_stream stream);
 
 /* ---- a2: selection ------------------------------------------------------ */
 
@@ -185,7 +206,7 @@ zf_status zf_topk_select(const float* norms_sq, int64_t m, double ratio,
  * sel: HOST struct; all four arrays are read and must describe one
  * consistent selection (as zf_topk_select writes it). */
 zf_status zf_adam_selected(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
-                           const zf_selection* sel, int64_t k,
+                           int32_t layout, const zf_selection* sel, int64_t k,
                            float* master, float* exp_avg, float* exp_avg_sq, int64_t ld_state,
                            uint16_t* weight, int64_t ld_weight,
                            const zf_adam_hparams* hp, int64_t step,
@@ -200,7 +221,7 @@ zf_status zf_adam_selected(const uint16_t* grad, int64_t n, int64_t m, int64_t l
  * accum_interval (= S) steps.  sel: HOST struct; all four arrays are read
  * and must describe one consistent selection. */
 zf_status zf_pack_accumulate(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
-                             const zf_selection* sel, int64_t k,
+                             int32_t layout, const zf_selection* sel, int64_t k,
                              float* acc, int64_t ld_acc,
                              int64_t step_in_interval, int64_t accum_interval,
                              zf_stream stream);
@@ -208,7 +229,7 @@ zf_status zf_pack_accumulate(const uint16_t* grad, int64_t n, int64_t m, int64_t
 /* zf_adam_selected and zf_pack_accumulate for the same step, one pass over G.
  * Arguments as in those two calls. */
 zf_status zf_update_fused(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
-                          const zf_selection* sel, int64_t k,
+                          int32_t layout, const zf_selection* sel, int64_t k,
                           float* master, float* exp_avg, float* exp_avg_sq, int64_t ld_state,
                           uint16_t* weight, int64_t ld_weight,
                           const zf_adam_hparams* hp, int64_t step,
@@ -224,8 +245,8 @@ zf_status zf_update_fused(const uint16_t* grad, int64_t n, int64_t m, int64_t ld
  * acc: [n][ld_acc]; out: [n][ld_out] fp32 dense.  sel: HOST struct; sel_mask
  * and sel_prefix are read. */
 zf_status zf_unpack(const float* acc, int64_t ld_acc, const zf_selection* sel, int64_t k,
-                    int64_t n, int64_t m, float scale, float* out, int64_t ld_out,
-                    zf_stream stream);
+                    int64_t n, int64_t m, int32_t layout, float scale, float* out,
+                    int64_t ld_out, zf_stream stream);
 
 /* ---- batched plans ------------------------------------------------------ */
 
@@ -235,6 +256,7 @@ zf_status zf_unpack(const float* acc, int64_t ld_acc, const zf_selection* sel, i
  * (zf_plan_create takes k as given). */
 typedef struct zf_matrix {
   int64_t n, m, k;
+  int32_t layout; /* zf_layout; every matrix of a plan uses the same one */
   const uint16_t* grad;
   int64_t ld_grad;
   uint16_t* weight;

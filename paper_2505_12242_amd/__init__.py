@@ -8,8 +8,10 @@ kernels of libzf.so (C ABI in include/zf.h); this package only binds it.
 """
 
 from ._lib import (  # noqa: F401
+    CHANNEL_MAJOR,
     LIB,
     LIB_PATH,
+    ROW_MAJOR,
     STATES_INIT,
     STATES_INPLACE,
     STATES_REMAP,

@@ -19,6 +19,11 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libzf.so")
 
 ZF_OK, ZF_EINVAL, ZF_EWORKSPACE, ZF_EHIP, ZF_ENOMEM = 0, 1, 2, 3, 4
 STATES_INPLACE, STATES_REMAP, STATES_INIT = 0, 1, 2
+# Storage layouts (zf_layout).  A logical n x m matrix (n outputs, m input
+# channels) is an [n, ld] tensor in ROW_MAJOR and an [m, ld] tensor (its
+# transpose) in CHANNEL_MAJOR; compact states are [n, k] / [k, n] and the
+# packed buffer [n, m-k] / [m-k, n] accordingly.
+ROW_MAJOR, CHANNEL_MAJOR = 0, 1
 
 c_i64, c_i32, c_dbl, c_flt, c_vp, c_sz = (ctypes.c_int64, ctypes.c_int32, ctypes.c_double,
                                           ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t)
@@ -40,7 +45,7 @@ class ZfStateSource(ctypes.Structure):
 
 
 class ZfMatrix(ctypes.Structure):
-    _fields_ = [("n", c_i64), ("m", c_i64), ("k", c_i64),
+    _fields_ = [("n", c_i64), ("m", c_i64), ("k", c_i64), ("layout", c_i32),
                 ("grad", c_vp), ("ld_grad", c_i64),
                 ("weight", c_vp), ("ld_weight", c_i64),
                 ("master", c_vp), ("exp_avg", c_vp), ("exp_avg_sq", c_vp), ("ld_state", c_i64),
@@ -56,23 +61,24 @@ SIGNATURES = [
     ("zf_status_string", ctypes.c_char_p, [ctypes.c_int]),
     ("zf_last_hip_error", ctypes.c_int, []),
     ("zf_k_from_ratio", c_i64, [c_dbl, c_i64]),
-    ("zf_colnorm_workspace_bytes", c_sz, [c_i64, c_i64]),
-    ("zf_colnorm", ctypes.c_int, [c_vp, c_i64, c_i64, c_i64, c_vp, c_vp, c_sz, c_vp]),
+    ("zf_colnorm_workspace_bytes", c_sz, [c_i64, c_i64, c_i32]),
+    ("zf_colnorm", ctypes.c_int, [c_vp, c_i64, c_i64, c_i64, c_i32, c_vp, c_vp, c_sz, c_vp]),
     ("zf_topk_select", ctypes.c_int,
      [c_vp, c_i64, c_dbl, ctypes.POINTER(ZfSelection), ctypes.POINTER(c_i64), c_vp]),
     ("zf_adam_selected", ctypes.c_int,
-     [c_vp, c_i64, c_i64, c_i64, ctypes.POINTER(ZfSelection), c_i64, c_vp, c_vp, c_vp, c_i64,
+     [c_vp, c_i64, c_i64, c_i64, c_i32, ctypes.POINTER(ZfSelection), c_i64, c_vp, c_vp, c_vp, c_i64,
       c_vp, c_i64, ctypes.POINTER(ZfAdamHparams), c_i64, c_i32, ctypes.POINTER(ZfStateSource),
       c_vp]),
     ("zf_pack_accumulate", ctypes.c_int,
-     [c_vp, c_i64, c_i64, c_i64, ctypes.POINTER(ZfSelection), c_i64, c_vp, c_i64, c_i64, c_i64,
+     [c_vp, c_i64, c_i64, c_i64, c_i32, ctypes.POINTER(ZfSelection), c_i64, c_vp, c_i64, c_i64, c_i64,
       c_vp]),
     ("zf_update_fused", ctypes.c_int,
-     [c_vp, c_i64, c_i64, c_i64, ctypes.POINTER(ZfSelection), c_i64, c_vp, c_vp, c_vp, c_i64,
+     [c_vp, c_i64, c_i64, c_i64, c_i32, ctypes.POINTER(ZfSelection), c_i64, c_vp, c_vp, c_vp, c_i64,
       c_vp, c_i64, ctypes.POINTER(ZfAdamHparams), c_i64, c_i32, ctypes.POINTER(ZfStateSource),
       c_vp, c_i64, c_i64, c_i64, c_vp]),
     ("zf_unpack", ctypes.c_int,
-     [c_vp, c_i64, ctypes.POINTER(ZfSelection), c_i64, c_i64, c_i64, c_flt, c_vp, c_i64, c_vp]),
+     [c_vp, c_i64, ctypes.POINTER(ZfSelection), c_i64, c_i64, c_i64, c_i32, c_flt, c_vp, c_i64,
+      c_vp]),
     ("zf_plan_create", ctypes.c_int, [ctypes.POINTER(ZfMatrix), c_i32, ctypes.POINTER(c_vp)]),
     ("zf_plan_destroy", None, [c_vp]),
     ("zf_plan_device_bytes", c_sz, [c_vp]),
@@ -145,6 +151,23 @@ def _mat(t: torch.Tensor, dtype, name: str, rows: Optional[int] = None,
     return t.stride(0) if t.shape[0] > 1 else t.shape[1]
 
 
+def _logical(t: torch.Tensor, layout: int):
+    """(n, m) of a matrix stored as tensor t in `layout`."""
+    if layout not in (ROW_MAJOR, CHANNEL_MAJOR):
+        raise ValueError(f"unknown layout {layout}")
+    return (t.shape[0], t.shape[1]) if layout == ROW_MAJOR else (t.shape[1], t.shape[0])
+
+
+def _stored(layout: int, rows_l: int, cols_l: int):
+    """Tensor shape of a logical rows_l x cols_l matrix in `layout`."""
+    return (rows_l, cols_l) if layout == ROW_MAJOR else (cols_l, rows_l)
+
+
+def _lmat(t, dtype, name, layout, rows_l=None, cols_l=None) -> int:
+    r, c = (rows_l, cols_l) if layout == ROW_MAJOR else (cols_l, rows_l)
+    return _mat(t, dtype, name, r, c)
+
+
 def _vec(t: torch.Tensor, dtype, name: str, size: int) -> None:
     if t.dtype != dtype or t.dim() != 1 or t.shape[0] != size:
         raise ValueError(f"{name}: expected a [{size}] {dtype} tensor, got "
@@ -189,22 +212,23 @@ def k_from_ratio(ratio: float, m: int) -> int:
     return k
 
 
-def colnorm_workspace_bytes(n: int, m: int) -> int:
-    return LIB.zf_colnorm_workspace_bytes(n, m)
+def colnorm_workspace_bytes(n: int, m: int, layout: int = ROW_MAJOR) -> int:
+    return LIB.zf_colnorm_workspace_bytes(n, m, layout)
 
 
 def colnorm(grad: torch.Tensor, out: Optional[torch.Tensor] = None,
-            workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    n, m = grad.shape
+            workspace: Optional[torch.Tensor] = None, layout: int = ROW_MAJOR,
+            stream=None) -> torch.Tensor:
+    n, m = _logical(grad, layout)
     ld = _mat(grad, torch.bfloat16, "grad")
     if out is None:
         out = torch.empty(m, dtype=torch.float32, device=grad.device)
     _vec(out, torch.float32, "out", m)
-    need = colnorm_workspace_bytes(n, m)
+    need = colnorm_workspace_bytes(n, m, layout)
     if workspace is None:
         workspace = torch.empty(max(need, 8), dtype=torch.uint8, device=grad.device)
-    _check("zf_colnorm", LIB.zf_colnorm(_ptr(grad), n, m, ld, _ptr(out), _ptr(workspace),
-                                        workspace.numel(), _stream(stream)))
+    _check("zf_colnorm", LIB.zf_colnorm(_ptr(grad), n, m, ld, layout, _ptr(out),
+                                        _ptr(workspace), workspace.numel(), _stream(stream)))
     return out
 
 
@@ -226,7 +250,8 @@ def topk_select(norms: torch.Tensor, ratio: float, out: Optional[Selection] = No
 
 @dataclass
 class StateSource:
-    """Where the selected columns' states come from (see zf_state_mode)."""
+    """Where the selected columns' states come from (see zf_state_mode).
+    Tensors are stored in the same layout as the call that uses them."""
     prev: Optional[Selection] = None
     prev_master: Optional[torch.Tensor] = None
     prev_exp_avg: Optional[torch.Tensor] = None
@@ -237,8 +262,9 @@ class StateSource:
         ld_prev = 0
         if self.prev_master is not None:
             ld_prev = _mat(self.prev_master, torch.float32, "prev_master")
-            _mat(self.prev_exp_avg, torch.float32, "prev_exp_avg")
-            _mat(self.prev_exp_avg_sq, torch.float32, "prev_exp_avg_sq")
+            if (_mat(self.prev_exp_avg, torch.float32, "prev_exp_avg") != ld_prev
+                    or _mat(self.prev_exp_avg_sq, torch.float32, "prev_exp_avg_sq") != ld_prev):
+                raise ValueError("previous states must share one row stride")
         ld_init = 0
         if self.init_master is not None:
             ld_init = _mat(self.init_master, torch.float32, "init_master")
@@ -249,68 +275,68 @@ class StateSource:
             _ptr(self.init_master), ld_init)
 
 
-def _states(n, k, master, exp_avg, exp_avg_sq):
-    ld = _mat(master, torch.float32, "master", n, k)
-    if (_mat(exp_avg, torch.float32, "exp_avg", n, k) != ld
-            or _mat(exp_avg_sq, torch.float32, "exp_avg_sq", n, k) != ld):
+def _states(n, k, master, exp_avg, exp_avg_sq, layout):
+    ld = _lmat(master, torch.float32, "master", layout, n, k)
+    if (_lmat(exp_avg, torch.float32, "exp_avg", layout, n, k) != ld
+            or _lmat(exp_avg_sq, torch.float32, "exp_avg_sq", layout, n, k) != ld):
         raise ValueError("master, exp_avg and exp_avg_sq must share one row stride")
     return ld
 
 
 def adam_selected(grad, sel: Selection, master, exp_avg, exp_avg_sq, weight, hp: AdamHparams,
                   step: int, mode: int = STATES_INPLACE, src: Optional[StateSource] = None,
-                  stream=None) -> None:
-    n, m = grad.shape
+                  layout: int = ROW_MAJOR, stream=None) -> None:
+    n, m = _logical(grad, layout)
     ldg = _mat(grad, torch.bfloat16, "grad")
-    lds = _states(n, sel.k, master, exp_avg, exp_avg_sq)
-    ldw = _mat(weight, torch.bfloat16, "weight", n, m)
+    lds = _states(n, sel.k, master, exp_avg, exp_avg_sq, layout)
+    ldw = _lmat(weight, torch.bfloat16, "weight", layout, n, m)
     c_sel, c_hp = sel.as_c(), hp.as_c()
     c_src = src.as_c() if src is not None else None
     _check("zf_adam_selected", LIB.zf_adam_selected(
-        _ptr(grad), n, m, ldg, ctypes.byref(c_sel), sel.k, _ptr(master), _ptr(exp_avg),
+        _ptr(grad), n, m, ldg, layout, ctypes.byref(c_sel), sel.k, _ptr(master), _ptr(exp_avg),
         _ptr(exp_avg_sq), lds, _ptr(weight), ldw, ctypes.byref(c_hp), step, mode,
         ctypes.byref(c_src) if c_src is not None else None, _stream(stream)))
 
 
 def pack_accumulate(grad, sel: Selection, acc, step_in_interval: int, accum_interval: int,
-                    stream=None) -> None:
-    n, m = grad.shape
+                    layout: int = ROW_MAJOR, stream=None) -> None:
+    n, m = _logical(grad, layout)
     ldg = _mat(grad, torch.bfloat16, "grad")
-    lda = _mat(acc, torch.float32, "acc", n, m - sel.k)
+    lda = _lmat(acc, torch.float32, "acc", layout, n, m - sel.k)
     c_sel = sel.as_c()
     _check("zf_pack_accumulate", LIB.zf_pack_accumulate(
-        _ptr(grad), n, m, ldg, ctypes.byref(c_sel), sel.k, _ptr(acc), lda, step_in_interval,
-        accum_interval, _stream(stream)))
+        _ptr(grad), n, m, ldg, layout, ctypes.byref(c_sel), sel.k, _ptr(acc), lda,
+        step_in_interval, accum_interval, _stream(stream)))
 
 
 def update_fused(grad, sel: Selection, master, exp_avg, exp_avg_sq, weight, hp: AdamHparams,
                  step: int, acc, step_in_interval: int, accum_interval: int,
                  mode: int = STATES_INPLACE, src: Optional[StateSource] = None,
-                 stream=None) -> None:
-    n, m = grad.shape
+                 layout: int = ROW_MAJOR, stream=None) -> None:
+    n, m = _logical(grad, layout)
     ldg = _mat(grad, torch.bfloat16, "grad")
-    lds = _states(n, sel.k, master, exp_avg, exp_avg_sq)
-    ldw = _mat(weight, torch.bfloat16, "weight", n, m)
-    lda = _mat(acc, torch.float32, "acc", n, m - sel.k)
+    lds = _states(n, sel.k, master, exp_avg, exp_avg_sq, layout)
+    ldw = _lmat(weight, torch.bfloat16, "weight", layout, n, m)
+    lda = _lmat(acc, torch.float32, "acc", layout, n, m - sel.k)
     c_sel, c_hp = sel.as_c(), hp.as_c()
     c_src = src.as_c() if src is not None else None
     _check("zf_update_fused", LIB.zf_update_fused(
-        _ptr(grad), n, m, ldg, ctypes.byref(c_sel), sel.k, _ptr(master), _ptr(exp_avg),
+        _ptr(grad), n, m, ldg, layout, ctypes.byref(c_sel), sel.k, _ptr(master), _ptr(exp_avg),
         _ptr(exp_avg_sq), lds, _ptr(weight), ldw, ctypes.byref(c_hp), step, mode,
         ctypes.byref(c_src) if c_src is not None else None, _ptr(acc), lda, step_in_interval,
         accum_interval, _stream(stream)))
 
 
 def unpack(acc, sel: Selection, scale: float = 1.0, out: Optional[torch.Tensor] = None,
-           stream=None) -> torch.Tensor:
-    n = acc.shape[0]
+           layout: int = ROW_MAJOR, stream=None) -> torch.Tensor:
     m = sel.m
-    lda = _mat(acc, torch.float32, "acc", n, m - sel.k)
+    n = acc.shape[0] if layout == ROW_MAJOR else acc.shape[1]
+    lda = _lmat(acc, torch.float32, "acc", layout, n, m - sel.k)
     if out is None:
-        out = torch.empty(n, m, dtype=torch.float32, device=acc.device)
-    ldo = _mat(out, torch.float32, "out", n, m)
+        out = torch.empty(*_stored(layout, n, m), dtype=torch.float32, device=acc.device)
+    ldo = _lmat(out, torch.float32, "out", layout, n, m)
     c_sel = sel.as_c()
-    _check("zf_unpack", LIB.zf_unpack(_ptr(acc), lda, ctypes.byref(c_sel), sel.k, n, m,
+    _check("zf_unpack", LIB.zf_unpack(_ptr(acc), lda, ctypes.byref(c_sel), sel.k, n, m, layout,
                                       float(scale), _ptr(out), ldo, _stream(stream)))
     return out
 
@@ -321,7 +347,8 @@ def unpack(acc, sel: Selection, scale: float = 1.0, out: Optional[torch.Tensor] 
 
 @dataclass
 class MatrixBuffers:
-    """Device tensors of one matrix of a batch; unused stages may be None."""
+    """Device tensors of one matrix of a batch, all in `layout`; unused
+    stages may be None."""
     grad: torch.Tensor
     k: int
     sel: Selection
@@ -333,27 +360,31 @@ class MatrixBuffers:
     norms: Optional[torch.Tensor] = None
     unpacked: Optional[torch.Tensor] = None
     src: Optional[StateSource] = None
+    layout: int = ROW_MAJOR
 
     def as_c(self) -> ZfMatrix:
-        n, m = self.grad.shape
+        L = self.layout
+        n, m = _logical(self.grad, L)
         x = ZfMatrix()
-        x.n, x.m, x.k = n, m, self.k
+        x.n, x.m, x.k, x.layout = n, m, self.k, L
         x.grad, x.ld_grad = _ptr(self.grad), _mat(self.grad, torch.bfloat16, "grad")
         if self.weight is not None:
-            x.weight, x.ld_weight = _ptr(self.weight), _mat(self.weight, torch.bfloat16, "weight", n, m)
+            x.weight = _ptr(self.weight)
+            x.ld_weight = _lmat(self.weight, torch.bfloat16, "weight", L, n, m)
         if self.master is not None:
             x.master, x.exp_avg, x.exp_avg_sq = (_ptr(self.master), _ptr(self.exp_avg),
                                                  _ptr(self.exp_avg_sq))
-            x.ld_state = _states(n, self.k, self.master, self.exp_avg, self.exp_avg_sq)
+            x.ld_state = _states(n, self.k, self.master, self.exp_avg, self.exp_avg_sq, L)
         if self.acc is not None:
-            x.acc, x.ld_acc = _ptr(self.acc), _mat(self.acc, torch.float32, "acc", n, m - self.k)
+            x.acc = _ptr(self.acc)
+            x.ld_acc = _lmat(self.acc, torch.float32, "acc", L, n, m - self.k)
         if self.norms is not None:
             _vec(self.norms, torch.float32, "norms", m)
             x.norms_sq = _ptr(self.norms)
         x.sel = self.sel.as_c()
         if self.unpacked is not None:
             x.unpacked = _ptr(self.unpacked)
-            x.ld_unpacked = _mat(self.unpacked, torch.float32, "unpacked", n, m)
+            x.ld_unpacked = _lmat(self.unpacked, torch.float32, "unpacked", L, n, m)
         if self.src is not None:
             x.src = self.src.as_c()
         return x

@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libzf.so")
 ARCH = "gfx950"
 
-SOURCES = ["zf_api.hip", "zf_kernels.hip"]
+SOURCES = ["zf_api.hip", "zf_kernels.hip", "zf_kernels_cm.hip"]
 
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared", "-Wall",

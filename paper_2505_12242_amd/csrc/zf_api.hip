@@ -147,6 +147,28 @@ hipStream_t as_stream(zf_stream s) { return reinterpret_cast<hipStream_t>(s); }
 
 // ---- per-matrix validation -------------------------------------------------
 
+// Storage extent of a logical [rows_l][cols_l] matrix: row-major keeps
+// [rows_l][ld], channel-major stores the transpose [cols_l][ld].
+struct Ext {
+  int64_t rows, width;
+};
+
+Ext ext(int32_t layout, int64_t rows_l, int64_t cols_l) {
+  return layout == zf::kChannelMajor ? Ext{cols_l, rows_l} : Ext{rows_l, cols_l};
+}
+
+bool mat_ok(const void* p, Ext e, int64_t ld, size_t elem) {
+  return matrix_ok(p, e.rows, e.width, ld, elem);
+}
+
+Span span(const void* p, Ext e, int64_t ld, size_t elem) {
+  return span_of(p, e.rows, e.width, ld, elem);
+}
+
+bool layout_ok(int32_t layout) {
+  return layout == zf::kRowMajor || layout == zf::kChannelMajor;
+}
+
 bool selection_ok(const zf_selection* s, int64_t m, int64_t k, bool need_idx) {
   if (s == nullptr) return false;
   const int64_t words = ceil_div(m, 64);
@@ -157,34 +179,37 @@ bool selection_ok(const zf_selection* s, int64_t m, int64_t k, bool need_idx) {
 }
 
 bool shape_ok(int64_t n, int64_t m, int64_t k) {
-  return n >= 0 && m >= 0 && k >= 0 && k <= m && n < (int64_t(1) << 40) &&
-         m < (int64_t(1) << 31);
+  return n >= 0 && m >= 0 && k >= 0 && k <= m && n < (int64_t(1) << 30) &&
+         m < (int64_t(1) << 30);
 }
 
 // Checks of one Adam step's buffers (selection mask/prefix already checked).
 bool adam_args_ok(const DevMat& d, int32_t mode, Span g) {
   const int64_t n = d.n, m = d.m, k = d.k;
-  if (!matrix_ok(d.P, n, k, d.ld_state, 4) || !matrix_ok(d.M, n, k, d.ld_state, 4) ||
-      !matrix_ok(d.V, n, k, d.ld_state, 4) || !matrix_ok(d.weight, n, m, d.ld_weight, 2))
+  const int32_t L = d.layout;
+  if (!mat_ok(d.P, ext(L, n, k), d.ld_state, 4) || !mat_ok(d.M, ext(L, n, k), d.ld_state, 4) ||
+      !mat_ok(d.V, ext(L, n, k), d.ld_state, 4) ||
+      !mat_ok(d.weight, ext(L, n, m), d.ld_weight, 2))
     return false;
   if (mode != zf::kInplace && mode != zf::kRemap && mode != zf::kInit) return false;
   if (mode == zf::kRemap) {
     const int64_t words = ceil_div(m, 64);
     if (!vector_ok(d.prev_mask, words, 8) || !vector_ok(d.prev_prefix, words, 4)) return false;
-    // previous states may hold up to m slots; their width is checked per use
-    // on the device side by construction (prev_prefix + lanes < previous k).
+    // The previous states hold as many slots as the previous selection has
+    // columns (device data); only presence, alignment and stride are checked.
     if (n > 0 && k > 0 &&
         (d.prev_P == nullptr || d.prev_M == nullptr || d.prev_V == nullptr ||
          !aligned(d.prev_P, 4) || !aligned(d.prev_M, 4) || !aligned(d.prev_V, 4) ||
-         d.ld_prev < 0))
+         d.ld_prev < (L == zf::kChannelMajor ? n : 0)))
       return false;
   }
   if (mode != zf::kInplace && d.init_P != nullptr &&
-      !matrix_ok(d.init_P, n, m, d.ld_init, 4))
+      !mat_ok(d.init_P, ext(L, n, m), d.ld_init, 4))
     return false;
-  const Span outs[4] = {span_of(d.P, n, k, d.ld_state, 4), span_of(d.M, n, k, d.ld_state, 4),
-                        span_of(d.V, n, k, d.ld_state, 4),
-                        span_of(d.weight, n, m, d.ld_weight, 2)};
+  const Span outs[4] = {span(d.P, ext(L, n, k), d.ld_state, 4),
+                        span(d.M, ext(L, n, k), d.ld_state, 4),
+                        span(d.V, ext(L, n, k), d.ld_state, 4),
+                        span(d.weight, ext(L, n, m), d.ld_weight, 2)};
   for (int a = 0; a < 4; ++a) {
     if (overlaps(outs[a], g)) return false;
     for (int b = a + 1; b < 4; ++b)
@@ -195,11 +220,12 @@ bool adam_args_ok(const DevMat& d, int32_t mode, Span g) {
 
 bool pack_args_ok(const DevMat& d, int64_t sii, int64_t S, Span g) {
   if (S < 1 || sii < 1 || sii > S) return false;
-  if (!matrix_ok(d.acc, d.n, d.m - d.k, d.ld_acc, 4)) return false;
-  return !overlaps(span_of(d.acc, d.n, d.m - d.k, d.ld_acc, 4), g);
+  const Ext e = ext(d.layout, d.n, d.m - d.k);
+  if (!mat_ok(d.acc, e, d.ld_acc, 4)) return false;
+  return !overlaps(span(d.acc, e, d.ld_acc, 4), g);
 }
 
-DevMat base_mat(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
+DevMat base_mat(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad, int32_t layout,
                 const zf_selection* sel, int64_t k) {
   DevMat d = blank();
   d.n = n;
@@ -207,6 +233,7 @@ DevMat base_mat(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
   d.k = k;
   d.grad = grad;
   d.ld_grad = ld_grad;
+  d.layout = layout;
   if (sel != nullptr) {
     d.sel_idx = sel->sel_idx;
     d.unsel_idx = sel->unsel_idx;
@@ -228,16 +255,71 @@ void apply_source(DevMat& d, const zf_state_source* src) {
   d.ld_init = src->ld_init;
 }
 
-zf_status run_update(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
+// Channel-major vector path: n a multiple of 8 and every present row start
+// 16-byte aligned.
+bool cm_vec_ok(const DevMat& d) {
+  if (d.n % 8 != 0) return false;
+  const auto ok = [](const void* p, int64_t ld, int64_t per16) {
+    return p == nullptr || (aligned(p, 16) && ld % per16 == 0);
+  };
+  return ok(d.grad, d.ld_grad, 8) && ok(d.weight, d.ld_weight, 8) && ok(d.P, d.ld_state, 4) &&
+         ok(d.M, d.ld_state, 4) && ok(d.V, d.ld_state, 4) && ok(d.acc, d.ld_acc, 4) &&
+         ok(d.out, d.ld_out, 4) && ok(d.prev_P, d.ld_prev, 4) && ok(d.prev_M, d.ld_prev, 4) &&
+         ok(d.prev_V, d.ld_prev, 4) && ok(d.init_P, d.ld_init, 4);
+}
+
+// Row-major update/unpack blocks address up_rows rows through 32-bit buffer
+// offsets: every row stride times up_rows must stay below 2^31 bytes.
+bool rm_strides_ok(const DevMat& d) {
+  const int64_t lim = (int64_t(1) << 31) / std::max<int64_t>(d.up_rows, 1);
+  return d.ld_grad * 2 < lim && d.ld_weight * 2 < lim && d.ld_state * 4 < lim &&
+         d.ld_acc * 4 < lim && d.ld_out * 4 < lim && d.ld_prev * 4 < lim && d.ld_init * 4 < lim;
+}
+
+void finish_geometry(DevMat& d, int cn_rows, int up_rows) {
+  set_geometry(d, cn_rows, up_rows);
+  if (d.layout == zf::kChannelMajor) {
+    d.cm_nch = d.n > 0 ? static_cast<int32_t>(ceil_div(d.n, zf::kCmChunk)) : 0;
+    d.vec = cm_vec_ok(d) ? 1 : 0;
+  }
+}
+
+int64_t colnorm_grid(const DevMat& d) {
+  if (d.layout == zf::kChannelMajor) return ceil_div(d.m, zf::kCmColnormCols);
+  return colnorm_blocks(d.n, d.m, d.cn_rpb);
+}
+
+int64_t update_grid(const DevMat& d) {
+  if (d.layout == zf::kChannelMajor) return d.m * d.cm_nch;
+  return update_blocks(d.n, d.m, d.up_rows);
+}
+
+hipError_t launch_update_any(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
+                             int32_t mode, int32_t first, bool adam, bool pack, int32_t layout,
+                             hipStream_t s) {
+  return layout == zf::kChannelMajor
+             ? zf::launch_cm_update(t, one, blocks, c, mode, first, adam, pack, s)
+             : zf::launch_update(t, one, blocks, c, mode, first, adam, pack, s);
+}
+
+hipError_t launch_unpack_any(const Table& t, const DevMat& one, int64_t blocks, float scale,
+                             int32_t layout, hipStream_t s) {
+  return layout == zf::kChannelMajor ? zf::launch_cm_unpack(t, one, blocks, scale, s)
+                                     : zf::launch_unpack(t, one, blocks, scale, s);
+}
+
+zf_status run_update(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad, int32_t layout,
                      const zf_selection* sel, int64_t k, float* master, float* exp_avg,
                      float* exp_avg_sq, int64_t ld_state, uint16_t* weight, int64_t ld_weight,
                      const zf_adam_hparams* hp, int64_t step, int32_t mode,
                      const zf_state_source* src, float* acc, int64_t ld_acc, int64_t sii,
                      int64_t S, bool adam, bool pack, zf_stream stream) {
-  if (!shape_ok(n, m, k) || !matrix_ok(grad, n, m, ld_grad, 2)) return ZF_EINVAL;
+  if (!layout_ok(layout) || !shape_ok(n, m, k) ||
+      !mat_ok(grad, ext(layout, n, m), ld_grad, 2))
+    return ZF_EINVAL;
   if (!selection_ok(sel, m, k, true)) return ZF_EINVAL;
-  DevMat d = base_mat(grad, n, m, ld_grad, sel, k);
-  const Span g = span_of(grad, n, m, ld_grad, 2);
+  DevMat d = base_mat(grad, n, m, ld_grad, layout, sel, k);
+  const Span g = span(grad, ext(layout, n, m), ld_grad, 2);
   AdamK c{};
   if (adam) {
     if (!hparams_ok(hp) || step < 1) return ZF_EINVAL;
@@ -257,21 +339,23 @@ zf_status run_update(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad
     d.ld_acc = ld_acc;
     if (!pack_args_ok(d, sii, S, g)) return ZF_EINVAL;
     if (adam) {
-      const Span a = span_of(acc, n, m - k, ld_acc, 4);
-      if (overlaps(a, span_of(master, n, k, ld_state, 4)) ||
-          overlaps(a, span_of(exp_avg, n, k, ld_state, 4)) ||
-          overlaps(a, span_of(exp_avg_sq, n, k, ld_state, 4)) ||
-          overlaps(a, span_of(weight, n, m, ld_weight, 2)))
+      const Span a = span(acc, ext(layout, n, m - k), ld_acc, 4);
+      const Ext es = ext(layout, n, k);
+      if (overlaps(a, span(master, es, ld_state, 4)) ||
+          overlaps(a, span(exp_avg, es, ld_state, 4)) ||
+          overlaps(a, span(exp_avg_sq, es, ld_state, 4)) ||
+          overlaps(a, span(weight, ext(layout, n, m), ld_weight, 2)))
         return ZF_EINVAL;
     }
   }
   if ((!adam || k == 0) && (!pack || k == m)) return ZF_OK;  // no column to touch
-  const int rows = pick_update_rows({{n, m}});
-  set_geometry(d, 256, rows);
-  const int64_t blocks = update_blocks(n, m, rows);
+  finish_geometry(d, 256, pick_update_rows({{n, m}}));
+  if (layout == zf::kRowMajor && !rm_strides_ok(d)) return ZF_EINVAL;
+  const int64_t blocks = update_grid(d);
   if (blocks == 0) return ZF_OK;
-  const hipError_t e = zf::launch_update(single_table(), d, blocks, c, adam ? mode : 0,
-                                         sii == 1 ? 1 : 0, adam, pack, as_stream(stream));
+  const hipError_t e = launch_update_any(single_table(), d, blocks, c, adam ? mode : 0,
+                                         sii == 1 ? 1 : 0, adam, pack, layout,
+                                         as_stream(stream));
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
@@ -302,32 +386,38 @@ int64_t zf_k_from_ratio(double ratio, int64_t m) {
   return std::max<int64_t>(0, std::min<int64_t>(m, static_cast<int64_t>(k)));
 }
 
-size_t zf_colnorm_workspace_bytes(int64_t n, int64_t m) {
-  if (n <= 0 || m <= 0) return 0;
+size_t zf_colnorm_workspace_bytes(int64_t n, int64_t m, int32_t layout) {
+  if (n <= 0 || m <= 0 || layout == zf::kChannelMajor) return 0;
   const int rpb = pick_colnorm_rows({{n, m}});
   return static_cast<size_t>(ceil_div(n, rpb)) * static_cast<size_t>(m) * sizeof(double);
 }
 
 zf_status zf_colnorm(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
-                     float* norms_sq, void* ws, size_t ws_bytes, zf_stream stream) {
-  if (!shape_ok(n, m, 0) || !matrix_ok(grad, n, m, ld_grad, 2) ||
-      !vector_ok(norms_sq, m, 4))
+                     int32_t layout, float* norms_sq, void* ws, size_t ws_bytes,
+                     zf_stream stream) {
+  if (!layout_ok(layout) || !shape_ok(n, m, 0) ||
+      !mat_ok(grad, ext(layout, n, m), ld_grad, 2) || !vector_ok(norms_sq, m, 4))
     return ZF_EINVAL;
-  if (overlaps(span_of(grad, n, m, ld_grad, 2), span_of(norms_sq, 1, m, m, 4))) return ZF_EINVAL;
-  const size_t need = zf_colnorm_workspace_bytes(n, m);
+  if (overlaps(span(grad, ext(layout, n, m), ld_grad, 2), span_of(norms_sq, 1, m, m, 4)))
+    return ZF_EINVAL;
+  const size_t need = zf_colnorm_workspace_bytes(n, m, layout);
   if (need > 0 && (ws == nullptr || ws_bytes < need || !aligned(ws, 8))) return ZF_EWORKSPACE;
   if (need > 0 && overlaps(Span{reinterpret_cast<uintptr_t>(ws),
                                 reinterpret_cast<uintptr_t>(ws) + need},
                            span_of(norms_sq, 1, m, m, 4)))
     return ZF_EINVAL;
   if (m == 0) return ZF_OK;
-  DevMat d = base_mat(grad, n, m, ld_grad, nullptr, 0);
+  DevMat d = base_mat(grad, n, m, ld_grad, layout, nullptr, 0);
   d.norms = norms_sq;
-  set_geometry(d, n > 0 ? pick_colnorm_rows({{n, m}}) : 256, 64);
+  finish_geometry(d, n > 0 ? pick_colnorm_rows({{n, m}}) : 256, 64);
   d.cn_ws = 0;
-  const hipError_t e = zf::launch_colnorm(single_table(), d, colnorm_blocks(n, m, d.cn_rpb),
-                                          single_table(), ceil_div(m, zf::kFinalizeCols),
-                                          static_cast<double*>(ws), as_stream(stream));
+  hipError_t e;
+  if (layout == zf::kChannelMajor)
+    e = zf::launch_cm_colnorm(single_table(), d, colnorm_grid(d), as_stream(stream));
+  else
+    e = zf::launch_colnorm(single_table(), d, colnorm_grid(d), single_table(),
+                           ceil_div(m, zf::kFinalizeCols), static_cast<double*>(ws),
+                           as_stream(stream));
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
@@ -337,7 +427,6 @@ zf_status zf_topk_select(const float* norms_sq, int64_t m, double ratio, const z
   if (k < 0 || !shape_ok(0, m, k) || !vector_ok(norms_sq, m, 4) ||
       !selection_ok(out, m, k, true))
     return ZF_EINVAL;
-  if (m >= (int64_t(1) << 31)) return ZF_EINVAL;
   const Span in = span_of(norms_sq, 1, m, m, 4);
   const Span outs[4] = {span_of(out->sel_idx, 1, k, k, 4), span_of(out->unsel_idx, 1, m - k, m - k, 4),
                         span_of(out->sel_mask, 1, ceil_div(m, 64), ceil_div(m, 64), 8),
@@ -349,59 +438,62 @@ zf_status zf_topk_select(const float* norms_sq, int64_t m, double ratio, const z
   }
   if (k_out != nullptr) *k_out = k;
   if (m == 0) return ZF_OK;
-  DevMat d = base_mat(nullptr, 0, m, m, out, k);
+  DevMat d = base_mat(nullptr, 0, m, m, zf::kRowMajor, out, k);
   d.norms = const_cast<float*>(norms_sq);
   const hipError_t e = zf::launch_topk(single_table(), d, 1, as_stream(stream));
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
 zf_status zf_adam_selected(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
-                           const zf_selection* sel, int64_t k, float* master, float* exp_avg,
-                           float* exp_avg_sq, int64_t ld_state, uint16_t* weight,
+                           int32_t layout, const zf_selection* sel, int64_t k, float* master,
+                           float* exp_avg, float* exp_avg_sq, int64_t ld_state, uint16_t* weight,
                            int64_t ld_weight, const zf_adam_hparams* hp, int64_t step,
                            int32_t mode, const zf_state_source* src, zf_stream stream) {
-  return run_update(grad, n, m, ld_grad, sel, k, master, exp_avg, exp_avg_sq, ld_state, weight,
-                    ld_weight, hp, step, mode, src, nullptr, 0, 1, 1, true, false, stream);
+  return run_update(grad, n, m, ld_grad, layout, sel, k, master, exp_avg, exp_avg_sq, ld_state,
+                    weight, ld_weight, hp, step, mode, src, nullptr, 0, 1, 1, true, false,
+                    stream);
 }
 
 zf_status zf_pack_accumulate(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
-                             const zf_selection* sel, int64_t k, float* acc, int64_t ld_acc,
-                             int64_t step_in_interval, int64_t accum_interval,
+                             int32_t layout, const zf_selection* sel, int64_t k, float* acc,
+                             int64_t ld_acc, int64_t step_in_interval, int64_t accum_interval,
                              zf_stream stream) {
-  return run_update(grad, n, m, ld_grad, sel, k, nullptr, nullptr, nullptr, 0, nullptr, 0,
-                    nullptr, 1, 0, nullptr, acc, ld_acc, step_in_interval, accum_interval, false,
-                    true, stream);
+  return run_update(grad, n, m, ld_grad, layout, sel, k, nullptr, nullptr, nullptr, 0, nullptr,
+                    0, nullptr, 1, 0, nullptr, acc, ld_acc, step_in_interval, accum_interval,
+                    false, true, stream);
 }
 
 zf_status zf_update_fused(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
-                          const zf_selection* sel, int64_t k, float* master, float* exp_avg,
-                          float* exp_avg_sq, int64_t ld_state, uint16_t* weight,
+                          int32_t layout, const zf_selection* sel, int64_t k, float* master,
+                          float* exp_avg, float* exp_avg_sq, int64_t ld_state, uint16_t* weight,
                           int64_t ld_weight, const zf_adam_hparams* hp, int64_t step,
                           int32_t mode, const zf_state_source* src, float* acc, int64_t ld_acc,
                           int64_t step_in_interval, int64_t accum_interval, zf_stream stream) {
-  return run_update(grad, n, m, ld_grad, sel, k, master, exp_avg, exp_avg_sq, ld_state, weight,
-                    ld_weight, hp, step, mode, src, acc, ld_acc, step_in_interval,
+  return run_update(grad, n, m, ld_grad, layout, sel, k, master, exp_avg, exp_avg_sq, ld_state,
+                    weight, ld_weight, hp, step, mode, src, acc, ld_acc, step_in_interval,
                     accum_interval, true, true, stream);
 }
 
 zf_status zf_unpack(const float* acc, int64_t ld_acc, const zf_selection* sel, int64_t k,
-                    int64_t n, int64_t m, float scale, float* out, int64_t ld_out,
+                    int64_t n, int64_t m, int32_t layout, float scale, float* out, int64_t ld_out,
                     zf_stream stream) {
-  if (!shape_ok(n, m, k) || !selection_ok(sel, m, k, false) ||
-      !matrix_ok(acc, n, m - k, ld_acc, 4) || !matrix_ok(out, n, m, ld_out, 4))
+  if (!layout_ok(layout) || !shape_ok(n, m, k) || !selection_ok(sel, m, k, false) ||
+      !mat_ok(acc, ext(layout, n, m - k), ld_acc, 4) ||
+      !mat_ok(out, ext(layout, n, m), ld_out, 4))
     return ZF_EINVAL;
-  if (overlaps(span_of(acc, n, m - k, ld_acc, 4), span_of(out, n, m, ld_out, 4)))
+  if (overlaps(span(acc, ext(layout, n, m - k), ld_acc, 4), span(out, ext(layout, n, m), ld_out, 4)))
     return ZF_EINVAL;
-  DevMat d = base_mat(nullptr, n, m, 0, sel, k);
+  DevMat d = base_mat(nullptr, n, m, 0, layout, sel, k);
   d.acc = const_cast<float*>(acc);
   d.ld_acc = ld_acc;
   d.out = out;
   d.ld_out = ld_out;
-  const int rows = pick_update_rows({{n, m}});
-  set_geometry(d, 256, rows);
-  const int64_t blocks = update_blocks(n, m, rows);
+  finish_geometry(d, 256, pick_update_rows({{n, m}}));
+  if (layout == zf::kRowMajor && !rm_strides_ok(d)) return ZF_EINVAL;
+  const int64_t blocks = update_grid(d);
   if (blocks == 0) return ZF_OK;
-  const hipError_t e = zf::launch_unpack(single_table(), d, blocks, scale, as_stream(stream));
+  const hipError_t e =
+      launch_unpack_any(single_table(), d, blocks, scale, layout, as_stream(stream));
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
@@ -413,6 +505,7 @@ zf_status zf_unpack(const float* acc, int64_t ld_acc, const zf_selection* sel, i
 
 struct zf_plan {
   int32_t nmats = 0;
+  int32_t layout = 0;
   std::vector<DevMat> mats;
   void* dev = nullptr;
   size_t dev_bytes = 0;
@@ -429,49 +522,51 @@ struct zf_plan {
 
 namespace {
 
-// Validates what a descriptor provides; records which stages it can run.
-zf_status check_plan_matrix(const zf_matrix& x, zf_plan& p) {
-  const int64_t n = x.n, m = x.m, k = x.k;
-  if (!shape_ok(n, m, k)) return ZF_EINVAL;
-  const int64_t words = ceil_div(m, 64);
-  const Span g = span_of(x.grad, n, m, x.ld_grad, 2);
-  const bool have_grad = matrix_ok(x.grad, n, m, x.ld_grad, 2) && (x.grad || n * m == 0);
-  const bool have_mask = vector_ok(x.sel.sel_mask, words, 8) && vector_ok(x.sel.sel_prefix, words, 4) &&
-                         ((x.sel.sel_mask && x.sel.sel_prefix) || words == 0);
-  const bool have_idx = vector_ok(x.sel.sel_idx, k, 4) && vector_ok(x.sel.unsel_idx, m - k, 4) &&
-                        (x.sel.sel_idx || k == 0) && (x.sel.unsel_idx || m - k == 0);
-  const bool have_norms = vector_ok(x.norms_sq, m, 4) && (x.norms_sq || m == 0);
-  p.can_colnorm = p.can_colnorm && have_grad && have_norms && !overlaps(g, span_of(x.norms_sq, 1, m, m, 4));
-  p.can_topk = p.can_topk && have_norms && have_mask && have_idx;
-
-  DevMat d = base_mat(x.grad, n, m, x.ld_grad, &x.sel, k);
+DevMat plan_mat(const zf_matrix& x) {
+  DevMat d = base_mat(x.grad, x.n, x.m, x.ld_grad, x.layout, &x.sel, x.k);
   d.P = x.master;
   d.M = x.exp_avg;
   d.V = x.exp_avg_sq;
   d.ld_state = x.ld_state;
   d.weight = x.weight;
   d.ld_weight = x.ld_weight;
-  apply_source(d, &x.src);
-  const bool have_states = (n * k == 0) || (x.master && x.exp_avg && x.exp_avg_sq && x.weight) ||
-                           (n * m == 0);
-  p.can_adam = p.can_adam && have_grad && have_mask && have_idx && have_states &&
-               (n * k == 0 || adam_args_ok(d, zf::kInplace, g));
-  p.can_remap = p.can_remap && p.can_adam && (n * k == 0 || adam_args_ok(d, zf::kRemap, g));
   d.acc = x.acc;
   d.ld_acc = x.ld_acc;
-  const bool have_acc = (n * (m - k) == 0) || x.acc != nullptr;
-  p.can_pack = p.can_pack && have_grad && have_mask && have_idx && have_acc &&
-               pack_args_ok(d, 1, 1, g);
-  const bool have_out = (n * m == 0) || x.unpacked != nullptr;
-  p.can_unpack = p.can_unpack && have_mask && have_acc && have_out &&
-                 matrix_ok(x.acc, n, m - k, x.ld_acc, 4) &&
-                 matrix_ok(x.unpacked, n, m, x.ld_unpacked, 4) &&
-                 !overlaps(span_of(x.acc, n, m - k, x.ld_acc, 4),
-                           span_of(x.unpacked, n, m, x.ld_unpacked, 4));
+  d.norms = x.norms_sq;
+  d.out = x.unpacked;
+  d.ld_out = x.ld_unpacked;
+  apply_source(d, &x.src);
+  return d;
+}
+
+// Validates what a descriptor provides; records which stages it can run.
+zf_status check_plan_matrix(const zf_matrix& x, zf_plan& p) {
+  const int64_t n = x.n, m = x.m, k = x.k;
+  const int32_t L = x.layout;
+  if (!layout_ok(L) || L != p.layout || !shape_ok(n, m, k)) return ZF_EINVAL;
+  const int64_t words = ceil_div(m, 64);
+  const Ext eg = ext(L, n, m), ea = ext(L, n, m - k);
+  const Span g = span(x.grad, eg, x.ld_grad, 2);
+  const bool have_grad = mat_ok(x.grad, eg, x.ld_grad, 2);
+  const bool have_mask = vector_ok(x.sel.sel_mask, words, 8) && vector_ok(x.sel.sel_prefix, words, 4);
+  const bool have_idx = vector_ok(x.sel.sel_idx, k, 4) && vector_ok(x.sel.unsel_idx, m - k, 4);
+  const bool have_norms = vector_ok(x.norms_sq, m, 4);
+  p.can_colnorm = p.can_colnorm && have_grad && have_norms &&
+                  !overlaps(g, span_of(x.norms_sq, 1, m, m, 4));
+  p.can_topk = p.can_topk && have_norms && have_mask && have_idx;
+
+  DevMat d = plan_mat(x);
+  p.can_adam = p.can_adam && have_grad && have_mask && have_idx &&
+               (n * k == 0 || adam_args_ok(d, zf::kInplace, g));
+  p.can_remap = p.can_remap && p.can_adam && (n * k == 0 || adam_args_ok(d, zf::kRemap, g));
+  p.can_pack = p.can_pack && have_grad && have_mask && have_idx && pack_args_ok(d, 1, 1, g);
+  p.can_unpack = p.can_unpack && have_mask && mat_ok(x.acc, ea, x.ld_acc, 4) &&
+                 mat_ok(x.unpacked, eg, x.ld_unpacked, 4) &&
+                 !overlaps(span(x.acc, ea, x.ld_acc, 4), span(x.unpacked, eg, x.ld_unpacked, 4));
   // Strides must be valid whenever the buffer is given.
-  if (x.weight && !matrix_ok(x.weight, n, m, x.ld_weight, 2)) return ZF_EINVAL;
-  if (x.acc && !matrix_ok(x.acc, n, m - k, x.ld_acc, 4)) return ZF_EINVAL;
-  if (x.unpacked && !matrix_ok(x.unpacked, n, m, x.ld_unpacked, 4)) return ZF_EINVAL;
+  if (x.weight && !mat_ok(x.weight, eg, x.ld_weight, 2)) return ZF_EINVAL;
+  if (x.acc && !mat_ok(x.acc, ea, x.ld_acc, 4)) return ZF_EINVAL;
+  if (x.unpacked && !mat_ok(x.unpacked, eg, x.ld_unpacked, 4)) return ZF_EINVAL;
   if (x.grad && !have_grad) return ZF_EINVAL;
   return ZF_OK;
 }
@@ -485,6 +580,7 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   zf_plan* p = new (std::nothrow) zf_plan();
   if (p == nullptr) return ZF_ENOMEM;
   p->nmats = nmats;
+  p->layout = mats[0].layout;
   std::vector<std::pair<int64_t, int64_t>> shapes;
   for (int32_t q = 0; q < nmats; ++q) {
     const zf_status st = check_plan_matrix(mats[q], *p);
@@ -499,39 +595,35 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   std::vector<int64_t> off_cn(nmats + 1), off_fin(nmats + 1), off_top(nmats + 1),
       off_up(nmats + 1);
   int64_t ws_doubles = 0;
+  const bool cm = p->layout == zf::kChannelMajor;
   p->mats.resize(nmats);
   for (int32_t q = 0; q < nmats; ++q) {
-    const zf_matrix& x = mats[q];
-    DevMat d = base_mat(x.grad, x.n, x.m, x.ld_grad, &x.sel, x.k);
-    d.P = x.master;
-    d.M = x.exp_avg;
-    d.V = x.exp_avg_sq;
-    d.ld_state = x.ld_state;
-    d.weight = x.weight;
-    d.ld_weight = x.ld_weight;
-    d.acc = x.acc;
-    d.ld_acc = x.ld_acc;
-    d.norms = x.norms_sq;
-    d.out = x.unpacked;
-    d.ld_out = x.ld_unpacked;
-    apply_source(d, &x.src);
-    set_geometry(d, cn_rows, up_rows);
+    DevMat d = plan_mat(mats[q]);
+    finish_geometry(d, cn_rows, up_rows);
+    if (!cm && !rm_strides_ok(d)) {
+      delete p;
+      return ZF_EINVAL;
+    }
     d.cn_ws = ws_doubles;
-    ws_doubles += static_cast<int64_t>(d.cn_rb) * d.m;
+    if (!cm) ws_doubles += static_cast<int64_t>(d.cn_rb) * d.m;
     off_cn[q] = p->blk_cn;
     off_fin[q] = p->blk_fin;
     off_top[q] = p->blk_top;
     off_up[q] = p->blk_up;
-    p->blk_cn += colnorm_blocks(d.n, d.m, cn_rows);
-    p->blk_fin += ceil_div(d.m, zf::kFinalizeCols);
+    p->blk_cn += colnorm_grid(d);
+    p->blk_fin += cm ? 0 : ceil_div(d.m, zf::kFinalizeCols);
     p->blk_top += 1;
-    p->blk_up += update_blocks(d.n, d.m, up_rows);
+    p->blk_up += update_grid(d);
     p->mats[q] = d;
   }
   off_cn[nmats] = p->blk_cn;
   off_fin[nmats] = p->blk_fin;
   off_top[nmats] = p->blk_top;
   off_up[nmats] = p->blk_up;
+  if (p->blk_cn >= (int64_t(1) << 31) / zf::kThreads || p->blk_up >= (int64_t(1) << 31) / zf::kThreads) {
+    delete p;
+    return ZF_EINVAL;  // grid too large for one launch
+  }
 
   const size_t mats_bytes = sizeof(DevMat) * nmats;
   const size_t off_bytes = sizeof(int64_t) * (nmats + 1);
@@ -581,9 +673,13 @@ size_t zf_plan_device_bytes(const zf_plan* plan) { return plan ? plan->dev_bytes
 zf_status zf_plan_colnorm(zf_plan* p, zf_stream stream) {
   if (p == nullptr || !p->can_colnorm) return ZF_EINVAL;
   const Table t{p->d_mats, p->d_off_cn, p->nmats};
-  const Table tf{p->d_mats, p->d_off_fin, p->nmats};
-  const hipError_t e = zf::launch_colnorm(t, p->mats[0], p->blk_cn, tf, p->blk_fin, p->d_ws,
-                                          as_stream(stream));
+  hipError_t e;
+  if (p->layout == zf::kChannelMajor) {
+    e = zf::launch_cm_colnorm(t, p->mats[0], p->blk_cn, as_stream(stream));
+  } else {
+    const Table tf{p->d_mats, p->d_off_fin, p->nmats};
+    e = zf::launch_colnorm(t, p->mats[0], p->blk_cn, tf, p->blk_fin, p->d_ws, as_stream(stream));
+  }
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
@@ -611,17 +707,17 @@ zf_status zf_plan_update(zf_plan* p, const zf_adam_hparams* hp, int64_t step, in
       return ZF_EINVAL;
   }
   const Table t{p->d_mats, p->d_off_up, p->nmats};
-  const hipError_t e =
-      zf::launch_update(t, p->mats[0], p->blk_up, c, do_adam ? mode : 0,
-                        step_in_interval == 1 ? 1 : 0, do_adam != 0, do_pack != 0,
-                        as_stream(stream));
+  const hipError_t e = launch_update_any(t, p->mats[0], p->blk_up, c, do_adam ? mode : 0,
+                                         step_in_interval == 1 ? 1 : 0, do_adam != 0,
+                                         do_pack != 0, p->layout, as_stream(stream));
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
 zf_status zf_plan_unpack(zf_plan* p, float scale, zf_stream stream) {
   if (p == nullptr || !p->can_unpack) return ZF_EINVAL;
   const Table t{p->d_mats, p->d_off_up, p->nmats};
-  const hipError_t e = zf::launch_unpack(t, p->mats[0], p->blk_up, scale, as_stream(stream));
+  const hipError_t e =
+      launch_unpack_any(t, p->mats[0], p->blk_up, scale, p->layout, as_stream(stream));
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 

@@ -17,7 +17,18 @@ constexpr int kUpdateCols = 256;
 constexpr int kFinalizeCols = 256;
 constexpr int kTopkThreads = 1024;
 
+// Channel-major layout: an update / unpack block covers one channel and
+// kCmChunk of its rows (kCmVpt 16-byte groups per thread); a colnorm block
+// covers kThreads / 64 channels, one per wave.
+#ifndef ZF_CM_VPT
+#define ZF_CM_VPT 2
+#endif
+constexpr int kCmVpt = ZF_CM_VPT;
+constexpr int kCmChunk = kThreads * 8 * kCmVpt;
+constexpr int kCmColnormCols = kThreads / 64;
+
 enum StateMode : int32_t { kInplace = 0, kRemap = 1, kInit = 2 };
+enum Layout : int32_t { kRowMajor = 0, kChannelMajor = 1 };
 
 // One matrix as the kernels see it.  Host-computed geometry is appended.
 struct DevMat {
@@ -55,8 +66,9 @@ struct DevMat {
   int32_t up_rows;   // rows per update / unpack block
   int32_t up_rb;     // update row blocks
   int32_t up_cb;     // update column blocks
-  int32_t vec;       // grad rows allow aligned 16-byte loads
-  int32_t pad_;
+  int32_t vec;       // 16-byte vector path allowed (alignment, strides, sizes)
+  int32_t layout;    // Layout
+  int32_t cm_nch;    // channel-major: row chunks per channel
 };
 
 // Per-kernel view of a batch: a device array of matrices and the first
@@ -81,5 +93,12 @@ hipError_t launch_update(const Table& t, const DevMat& one, int64_t blocks, cons
                          int32_t mode, int32_t first, bool adam, bool pack, hipStream_t s);
 hipError_t launch_unpack(const Table& t, const DevMat& one, int64_t blocks, float scale,
                          hipStream_t s);
+
+// Channel-major kernels (zf_kernels_cm.hip).
+hipError_t launch_cm_colnorm(const Table& t, const DevMat& one, int64_t blocks, hipStream_t s);
+hipError_t launch_cm_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
+                            int32_t mode, int32_t first, bool adam, bool pack, hipStream_t s);
+hipError_t launch_cm_unpack(const Table& t, const DevMat& one, int64_t blocks, float scale,
+                            hipStream_t s);
 
 }  // namespace zf

@@ -7,86 +7,10 @@
 //
 // Compiled with -ffp-contract=off and correctly rounded fp32 division and
 // square root, so that each arithmetic line below is one IEEE operation.
-#include "zf_internal.hpp"
+#include "zf_device.hpp"
 
 namespace zf {
 namespace {
-
-__device__ __forceinline__ float widen_bf16(uint16_t b) {
-  return __uint_as_float(static_cast<uint32_t>(b) << 16);
-}
-
-// fp32 -> bf16, round to nearest, ties to even; NaN stays a (quiet) NaN.
-__device__ __forceinline__ uint16_t round_bf16(float x) {
-  uint32_t u = __float_as_uint(x);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return static_cast<uint16_t>(u >> 16);
-}
-
-// Number of set bits of `mask` at lane positions below the calling lane.
-__device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
-  return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
-                                   __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
-}
-
-// Descriptor of the matrix block b belongs to.  BATCHED kernels read it
-// from the plan's device table (scalar loads); single-matrix kernels take it
-// by value.  Keeping the two apart avoids a generic pointer that would turn
-// the descriptor loads into flat vector loads.
-template <bool BATCHED>
-__device__ __forceinline__ DevMat get_mat(const DevMat* __restrict__ mats,
-                                          const int64_t* __restrict__ off, int32_t nmats,
-                                          const DevMat& one, int64_t b, int64_t& local) {
-  if constexpr (!BATCHED) {
-    local = b;
-    return one;
-  } else {
-    int lo = 0, hi = nmats - 1;
-    while (lo < hi) {  // largest q with off[q] <= b
-      const int mid = (lo + hi + 1) >> 1;
-      if (off[mid] <= b) lo = mid; else hi = mid - 1;
-    }
-    local = b - off[lo];
-    return mats[lo];
-  }
-}
-
-// Raw buffer resources (gfx9 family word 3).  A resource is based at the
-// first row a block touches; lanes pass one 32-bit byte offset that is the
-// same for every row, the row part goes in the scalar offset.  num_records
-// is the exact byte span of the block's rows, so an access outside them is
-// dropped by the hardware rather than reaching other memory.
-typedef __amdgpu_buffer_rsrc_t rsrc_t;
-constexpr int kRsrcWord3 = 0x00020000;
-
-__device__ __forceinline__ rsrc_t make_rsrc(const void* base, int64_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), static_cast<short>(0),
-                                           static_cast<int>(bytes), kRsrcWord3);
-}
-
-// Resource over rows [i0, i1) of a row-major [.][ld] array of `width` used
-// elements of T per row.
-template <typename T>
-__device__ __forceinline__ rsrc_t rows_rsrc(const T* base, int64_t i0, int64_t i1, int64_t ld,
-                                            int64_t width) {
-  const int64_t rows = i1 - i0;
-  const int64_t bytes = rows > 0 ? ((rows - 1) * ld + width) * static_cast<int64_t>(sizeof(T)) : 0;
-  return make_rsrc(base + i0 * ld, bytes);
-}
-
-__device__ __forceinline__ float buf_f32(rsrc_t r, uint32_t voff, uint32_t soff) {
-  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
-}
-__device__ __forceinline__ uint16_t buf_u16(rsrc_t r, uint32_t voff, uint32_t soff) {
-  return static_cast<uint16_t>(__builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0));
-}
-__device__ __forceinline__ void buf_put_f32(float v, rsrc_t r, uint32_t voff, uint32_t soff) {
-  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, voff, soff, 0);
-}
-__device__ __forceinline__ void buf_put_u16(uint16_t v, rsrc_t r, uint32_t voff, uint32_t soff) {
-  __builtin_amdgcn_raw_buffer_store_b16(v, r, voff, soff, 0);
-}
 
 // ---------------------------------------------------------------------------
 // a1: column scores.  Stage 1: a block sums the squares of a 512-column x
@@ -348,14 +272,6 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(const DevMat* __rest
 // processed kRowBatch at a time with all loads issued before use.
 // ---------------------------------------------------------------------------
 
-__device__ __forceinline__ void adam_step(float g, float& p, float& m, float& v, const AdamK& c) {
-  m = c.b1 * m + c.c1 * g;
-  v = c.b2 * v + c.c2 * (g * g);
-  const float den = sqrtf(v * c.ib2) + c.eps;
-  const float u = (m * c.ib1) / den;
-  if (c.wd != 0.0f) p = p - c.wd * p;
-  p = p - c.lr * u;
-}
 
 #ifndef ZF_PACK_BATCH
 #define ZF_PACK_BATCH 8

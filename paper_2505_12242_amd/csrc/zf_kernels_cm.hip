@@ -1,0 +1,401 @@
+// gfx950 kernels for the channel-major layout.
+//
+// The paper stores gradients column-major so that an input channel can be
+// accessed as one unit (Implementation, "Fully Segmented Gradient
+// Selection").  Here a logical n x m weight (n outputs, m input channels) is
+// held as its transpose, [m][ld >= n]: channel j is one contiguous row of n
+// values.  The compact states are [k][ld_state >= n] (slot r = channel
+// sel_idx[r]), the packed buffer [m-k][ld_acc >= n] (slot u = channel
+// unsel_idx[u]) and the hand-over buffer [m][ld_out >= n].  Every access of
+// the hot path is then a contiguous 16-byte-per-lane stream, and the bf16
+// write-back writes whole cache lines.
+//
+// Work unit of update / unpack: one channel x one chunk of kCmChunk rows.
+// Whether the channel is selected, and its slot, are uniform per block, so
+// a block is either an Adam block or a pack block.  A block's buffer
+// resources cover exactly its chunk, so 16-byte groups past the end of a
+// channel (the last chunk) read zeros and their stores are dropped by the
+// hardware range check; the loops carry no per-group conditions.  The vector
+// path requires n % 8 == 0 and 16-byte aligned rows (DevMat::vec); other
+// shapes take an element-wise path.
+#include "zf_device.hpp"
+
+namespace zf {
+namespace {
+
+constexpr int kGroup = 8;  // bf16 elements in 16 bytes
+
+// bf16 x 8 (four dwords) -> fp32 x 8
+__device__ __forceinline__ void widen8(u32x4 v, float (&f)[kGroup]) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int h = 0; h < 4; ++h) {
+    f[2 * h] = __uint_as_float(w[h] << 16);
+    f[2 * h + 1] = __uint_as_float(w[h] & 0xffff0000u);
+  }
+}
+
+__device__ __forceinline__ u32x4 narrow8(const float (&f)[kGroup]) {
+  u32x4 v;
+  v.x = static_cast<uint32_t>(round_bf16(f[0])) | (static_cast<uint32_t>(round_bf16(f[1])) << 16);
+  v.y = static_cast<uint32_t>(round_bf16(f[2])) | (static_cast<uint32_t>(round_bf16(f[3])) << 16);
+  v.z = static_cast<uint32_t>(round_bf16(f[4])) | (static_cast<uint32_t>(round_bf16(f[5])) << 16);
+  v.w = static_cast<uint32_t>(round_bf16(f[6])) | (static_cast<uint32_t>(round_bf16(f[7])) << 16);
+  return v;
+}
+
+__device__ __forceinline__ void f32x8_load(rsrc_t r, uint32_t byte_off, float (&f)[kGroup]) {
+  const u32x4 a = buf_b128(r, byte_off, 0);
+  const u32x4 b = buf_b128(r, byte_off + 16, 0);
+  f[0] = __uint_as_float(a.x); f[1] = __uint_as_float(a.y);
+  f[2] = __uint_as_float(a.z); f[3] = __uint_as_float(a.w);
+  f[4] = __uint_as_float(b.x); f[5] = __uint_as_float(b.y);
+  f[6] = __uint_as_float(b.z); f[7] = __uint_as_float(b.w);
+}
+
+__device__ __forceinline__ void f32x8_store(rsrc_t r, uint32_t byte_off, const float (&f)[kGroup]) {
+  u32x4 a, b;
+  a.x = __float_as_uint(f[0]); a.y = __float_as_uint(f[1]);
+  a.z = __float_as_uint(f[2]); a.w = __float_as_uint(f[3]);
+  b.x = __float_as_uint(f[4]); b.y = __float_as_uint(f[5]);
+  b.z = __float_as_uint(f[6]); b.w = __float_as_uint(f[7]);
+  buf_put_b128(a, r, byte_off, 0);
+  buf_put_b128(b, r, byte_off + 16, 0);
+}
+
+// Byte offset, within the block's chunk, of group g of thread tid.
+__device__ __forceinline__ uint32_t group_elem(int g, int tid) {
+  return static_cast<uint32_t>((g * kThreads + tid) * kGroup);
+}
+
+// ---------------------------------------------------------------------------
+// a1: column scores.  One wave per channel: lanes stride through the row
+// with 16-byte loads and sum squares in fp64 (exact squares), then a fixed
+// xor-butterfly across the wave.  Deterministic, no workspace.
+// ---------------------------------------------------------------------------
+
+template <bool BATCHED>
+__global__ __launch_bounds__(kThreads) void cm_colnorm_kernel(const DevMat* __restrict__ mats,
+                                                             const int64_t* __restrict__ off,
+                                                             int32_t nmats, DevMat one) {
+  int64_t local;
+  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, blockIdx.x, local);
+  const int lane = threadIdx.x & 63;
+  const int64_t j = local * (kThreads / 64) + (threadIdx.x >> 6);
+  if (j >= d.m) return;
+  const int64_t n = d.n;
+  const rsrc_t r = make_rsrc(d.grad + j * d.ld_grad, n * 2);
+  double a0 = 0.0, a1 = 0.0;
+  if (d.vec) {
+    constexpr int kStride = 64 * kGroup;  // elements per wave per load
+    int64_t e = static_cast<int64_t>(lane) * kGroup;
+    for (; e + 3 * kStride < n; e += 4 * kStride) {
+      u32x4 v[4];
+#pragma unroll
+      for (int b = 0; b < 4; ++b) v[b] = buf_b128(r, static_cast<uint32_t>((e + b * kStride) * 2), 0);
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        float f[kGroup];
+        widen8(v[b], f);
+#pragma unroll
+        for (int c = 0; c < kGroup; c += 2) {
+          a0 = __builtin_fma(static_cast<double>(f[c]), static_cast<double>(f[c]), a0);
+          a1 = __builtin_fma(static_cast<double>(f[c + 1]), static_cast<double>(f[c + 1]), a1);
+        }
+      }
+    }
+    for (; e < n; e += kStride) {
+      float f[kGroup];
+      widen8(buf_b128(r, static_cast<uint32_t>(e * 2), 0), f);
+#pragma unroll
+      for (int c = 0; c < kGroup; c += 2) {
+        a0 = __builtin_fma(static_cast<double>(f[c]), static_cast<double>(f[c]), a0);
+        a1 = __builtin_fma(static_cast<double>(f[c + 1]), static_cast<double>(f[c + 1]), a1);
+      }
+    }
+  } else {
+    for (int64_t e = lane; e < n; e += 64) {
+      const double x = static_cast<double>(widen_bf16(buf_u16(r, static_cast<uint32_t>(e * 2), 0)));
+      a0 = __builtin_fma(x, x, a0);
+    }
+  }
+  double s = a0 + a1;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
+  if (lane == 0) d.norms[j] = static_cast<float>(s);
+}
+
+// ---------------------------------------------------------------------------
+// a3-a5: fused Adam (selected channels) and pack (unselected channels).
+// ---------------------------------------------------------------------------
+
+enum CmSrc { kCmInplace = 0, kCmPrev, kCmInitW, kCmInitMaster };
+
+// Adam over one chunk of channel j (slot r), vector path.  SRC picks where
+// (p, m, v) come from; rS* are the source rows (the slot's own rows in place).
+template <int SRC>
+__device__ __forceinline__ void cm_adam_vec(rsrc_t rG, rsrc_t rP, rsrc_t rM, rsrc_t rV,
+                                            rsrc_t rW, rsrc_t rSP, rsrc_t rSM, rsrc_t rSV,
+                                            rsrc_t rI, const AdamK& c) {
+  const int tid = threadIdx.x;
+  float g[kCmVpt][kGroup], p[kCmVpt][kGroup], m[kCmVpt][kGroup], v[kCmVpt][kGroup];
+  u32x4 gv[kCmVpt];
+#pragma unroll
+  for (int q = 0; q < kCmVpt; ++q) gv[q] = buf_b128(rG, group_elem(q, tid) * 2, 0);
+#pragma unroll
+  for (int q = 0; q < kCmVpt; ++q) {
+    const uint32_t e = group_elem(q, tid);
+    if constexpr (SRC == kCmInplace || SRC == kCmPrev) {
+      f32x8_load(rSP, e * 4, p[q]);
+      f32x8_load(rSM, e * 4, m[q]);
+      f32x8_load(rSV, e * 4, v[q]);
+    } else {
+      if constexpr (SRC == kCmInitMaster) f32x8_load(rI, e * 4, p[q]);
+      else widen8(buf_b128(rI, e * 2, 0), p[q]);
+#pragma unroll
+      for (int i = 0; i < kGroup; ++i) m[q][i] = v[q][i] = 0.0f;
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < kCmVpt; ++q) {
+    widen8(gv[q], g[q]);
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) adam_step(g[q][i], p[q][i], m[q][i], v[q][i], c);
+    const uint32_t e = group_elem(q, tid);
+    f32x8_store(rP, e * 4, p[q]);
+    f32x8_store(rM, e * 4, m[q]);
+    f32x8_store(rV, e * 4, v[q]);
+    buf_put_b128(narrow8(p[q]), rW, e * 2, 0);
+  }
+}
+
+// Element-wise fallback of the same update (any n, any alignment).
+template <int SRC>
+__device__ __forceinline__ void cm_adam_elem(rsrc_t rG, rsrc_t rP, rsrc_t rM, rsrc_t rV,
+                                             rsrc_t rW, rsrc_t rSP, rsrc_t rSM, rsrc_t rSV,
+                                             rsrc_t rI, const AdamK& c, int64_t len) {
+  for (int64_t e = threadIdx.x; e < len; e += kThreads) {
+    const uint32_t o = static_cast<uint32_t>(e);
+    const float g = widen_bf16(buf_u16(rG, o * 2, 0));
+    float p, m, v;
+    if constexpr (SRC == kCmInplace || SRC == kCmPrev) {
+      p = buf_f32(rSP, o * 4, 0);
+      m = buf_f32(rSM, o * 4, 0);
+      v = buf_f32(rSV, o * 4, 0);
+    } else {
+      p = (SRC == kCmInitMaster) ? buf_f32(rI, o * 4, 0) : widen_bf16(buf_u16(rI, o * 2, 0));
+      m = v = 0.0f;
+    }
+    adam_step(g, p, m, v, c);
+    buf_put_f32(p, rP, o * 4, 0);
+    buf_put_f32(m, rM, o * 4, 0);
+    buf_put_f32(v, rV, o * 4, 0);
+    buf_put_u16(round_bf16(p), rW, o * 2, 0);
+  }
+}
+
+template <bool FIRST>
+__device__ __forceinline__ void cm_pack_vec(rsrc_t rG, rsrc_t rA) {
+  const int tid = threadIdx.x;
+  u32x4 gv[kCmVpt];
+  float a[kCmVpt][kGroup];
+#pragma unroll
+  for (int q = 0; q < kCmVpt; ++q) gv[q] = buf_b128(rG, group_elem(q, tid) * 2, 0);
+  if constexpr (!FIRST) {
+#pragma unroll
+    for (int q = 0; q < kCmVpt; ++q) f32x8_load(rA, group_elem(q, tid) * 4, a[q]);
+  }
+#pragma unroll
+  for (int q = 0; q < kCmVpt; ++q) {
+    float g[kGroup];
+    widen8(gv[q], g);
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) a[q][i] = FIRST ? g[i] : a[q][i] + g[i];
+    f32x8_store(rA, group_elem(q, tid) * 4, a[q]);
+  }
+}
+
+template <bool FIRST>
+__device__ __forceinline__ void cm_pack_elem(rsrc_t rG, rsrc_t rA, int64_t len) {
+  for (int64_t e = threadIdx.x; e < len; e += kThreads) {
+    const uint32_t o = static_cast<uint32_t>(e);
+    const float g = widen_bf16(buf_u16(rG, o * 2, 0));
+    buf_put_f32(FIRST ? g : buf_f32(rA, o * 4, 0) + g, rA, o * 4, 0);
+  }
+}
+
+template <bool BATCHED, bool ADAM, bool PACK>
+__global__ __launch_bounds__(kThreads) void cm_update_kernel(const DevMat* __restrict__ mats,
+                                                            const int64_t* __restrict__ off,
+                                                            int32_t nmats, DevMat one, AdamK c,
+                                                            int32_t mode, int32_t first) {
+  int64_t local;
+  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, blockIdx.x, local);
+  const int64_t j = local / d.cm_nch;
+  const int64_t e0 = (local % d.cm_nch) * kCmChunk;
+  const int64_t len = min(static_cast<int64_t>(kCmChunk), d.n - e0);
+  const int64_t w = j >> 6;
+  const uint64_t mw = d.mask[w];
+  const bool sel = (mw >> (j & 63)) & 1ull;
+  const int64_t r = static_cast<int64_t>(d.prefix[w]) +
+                    __popcll(mw & ((uint64_t(1) << (j & 63)) - 1));
+  const rsrc_t rG = make_rsrc(d.grad + j * d.ld_grad + e0, len * 2);
+
+  if (!sel) {
+    if constexpr (PACK) {
+      const int64_t u = j - r;
+      const rsrc_t rA = make_rsrc(d.acc + u * d.ld_acc + e0, len * 4);
+      if (d.vec) {
+        if (first) cm_pack_vec<true>(rG, rA);
+        else cm_pack_vec<false>(rG, rA);
+      } else {
+        if (first) cm_pack_elem<true>(rG, rA, len);
+        else cm_pack_elem<false>(rG, rA, len);
+      }
+    }
+    return;
+  }
+  if constexpr (ADAM) {
+    const rsrc_t rP = make_rsrc(d.P + r * d.ld_state + e0, len * 4);
+    const rsrc_t rM = make_rsrc(d.M + r * d.ld_state + e0, len * 4);
+    const rsrc_t rV = make_rsrc(d.V + r * d.ld_state + e0, len * 4);
+    const rsrc_t rW = make_rsrc(d.weight + j * d.ld_weight + e0, len * 2);
+    int src = kCmInplace;
+    rsrc_t rSP = rP, rSM = rM, rSV = rV, rI = rW;
+    if (mode == kRemap) {
+      const uint64_t pm = d.prev_mask[w];
+      if ((pm >> (j & 63)) & 1ull) {
+        const int64_t ro = static_cast<int64_t>(d.prev_prefix[w]) +
+                           __popcll(pm & ((uint64_t(1) << (j & 63)) - 1));
+        rSP = make_rsrc(d.prev_P + ro * d.ld_prev + e0, len * 4);
+        rSM = make_rsrc(d.prev_M + ro * d.ld_prev + e0, len * 4);
+        rSV = make_rsrc(d.prev_V + ro * d.ld_prev + e0, len * 4);
+        src = kCmPrev;
+      } else {
+        src = d.init_P ? kCmInitMaster : kCmInitW;
+      }
+    } else if (mode == kInit) {
+      src = d.init_P ? kCmInitMaster : kCmInitW;
+    }
+    if (src == kCmInitMaster) rI = make_rsrc(d.init_P + j * d.ld_init + e0, len * 4);
+    if (d.vec) {
+      switch (src) {
+        case kCmInplace: cm_adam_vec<kCmInplace>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c); break;
+        case kCmPrev: cm_adam_vec<kCmPrev>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c); break;
+        case kCmInitW: cm_adam_vec<kCmInitW>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c); break;
+        default: cm_adam_vec<kCmInitMaster>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c); break;
+      }
+    } else {
+      switch (src) {
+        case kCmInplace: cm_adam_elem<kCmInplace>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, len); break;
+        case kCmPrev: cm_adam_elem<kCmPrev>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, len); break;
+        case kCmInitW: cm_adam_elem<kCmInitW>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, len); break;
+        default: cm_adam_elem<kCmInitMaster>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, len); break;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// a6: hand-over.  Channel j of the dense buffer is +0.0 when selected, else
+// scale times its packed row.
+// ---------------------------------------------------------------------------
+
+template <bool BATCHED>
+__global__ __launch_bounds__(kThreads) void cm_unpack_kernel(const DevMat* __restrict__ mats,
+                                                            const int64_t* __restrict__ off,
+                                                            int32_t nmats, DevMat one,
+                                                            float scale) {
+  int64_t local;
+  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, blockIdx.x, local);
+  const int64_t j = local / d.cm_nch;
+  const int64_t e0 = (local % d.cm_nch) * kCmChunk;
+  const int64_t len = min(static_cast<int64_t>(kCmChunk), d.n - e0);
+  const int64_t w = j >> 6;
+  const uint64_t mw = d.mask[w];
+  const bool sel = (mw >> (j & 63)) & 1ull;
+  const rsrc_t rD = make_rsrc(d.out + j * d.ld_out + e0, len * 4);
+  const int tid = threadIdx.x;
+  if (sel) {
+    const float z[kGroup] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    if (d.vec) {
+#pragma unroll
+      for (int q = 0; q < kCmVpt; ++q) f32x8_store(rD, group_elem(q, tid) * 4, z);
+    } else {
+      for (int64_t e = tid; e < len; e += kThreads) buf_put_f32(0.0f, rD, static_cast<uint32_t>(e) * 4, 0);
+    }
+    return;
+  }
+  const int64_t u = j - (static_cast<int64_t>(d.prefix[w]) +
+                         __popcll(mw & ((uint64_t(1) << (j & 63)) - 1)));
+  const rsrc_t rA = make_rsrc(d.acc + u * d.ld_acc + e0, len * 4);
+  if (d.vec) {
+    float a[kCmVpt][kGroup];
+#pragma unroll
+    for (int q = 0; q < kCmVpt; ++q) f32x8_load(rA, group_elem(q, tid) * 4, a[q]);
+#pragma unroll
+    for (int q = 0; q < kCmVpt; ++q) {
+#pragma unroll
+      for (int i = 0; i < kGroup; ++i) a[q][i] = a[q][i] * scale;
+      f32x8_store(rD, group_elem(q, tid) * 4, a[q]);
+    }
+  } else {
+    for (int64_t e = tid; e < len; e += kThreads) {
+      const uint32_t o = static_cast<uint32_t>(e) * 4;
+      buf_put_f32(buf_f32(rA, o, 0) * scale, rD, o, 0);
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_cm_colnorm(const Table& t, const DevMat& one, int64_t blocks, hipStream_t s) {
+  (void)hipGetLastError();
+  if (blocks > 0) {
+    if (t.mats != nullptr)
+      hipLaunchKernelGGL((cm_colnorm_kernel<true>), dim3(static_cast<uint32_t>(blocks)),
+                         dim3(kThreads), 0, s, t.mats, t.off, t.nmats, one);
+    else
+      hipLaunchKernelGGL((cm_colnorm_kernel<false>), dim3(static_cast<uint32_t>(blocks)),
+                         dim3(kThreads), 0, s, t.mats, t.off, t.nmats, one);
+  }
+  return hipGetLastError();
+}
+
+template <bool ADAM, bool PACK>
+static void launch_cm_update_t(const Table& t, const DevMat& one, dim3 grid, const AdamK& c,
+                               int32_t mode, int32_t first, hipStream_t s) {
+  if (t.mats != nullptr)
+    hipLaunchKernelGGL((cm_update_kernel<true, ADAM, PACK>), grid, dim3(kThreads), 0, s, t.mats,
+                       t.off, t.nmats, one, c, mode, first);
+  else
+    hipLaunchKernelGGL((cm_update_kernel<false, ADAM, PACK>), grid, dim3(kThreads), 0, s, t.mats,
+                       t.off, t.nmats, one, c, mode, first);
+}
+
+hipError_t launch_cm_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
+                            int32_t mode, int32_t first, bool adam, bool pack, hipStream_t s) {
+  (void)hipGetLastError();
+  if (blocks <= 0) return hipSuccess;
+  const dim3 grid(static_cast<uint32_t>(blocks));
+  if (adam && pack) launch_cm_update_t<true, true>(t, one, grid, c, mode, first, s);
+  else if (adam) launch_cm_update_t<true, false>(t, one, grid, c, mode, first, s);
+  else if (pack) launch_cm_update_t<false, true>(t, one, grid, c, mode, first, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_cm_unpack(const Table& t, const DevMat& one, int64_t blocks, float scale,
+                            hipStream_t s) {
+  (void)hipGetLastError();
+  if (blocks > 0) {
+    if (t.mats != nullptr)
+      hipLaunchKernelGGL((cm_unpack_kernel<true>), dim3(static_cast<uint32_t>(blocks)),
+                         dim3(kThreads), 0, s, t.mats, t.off, t.nmats, one, scale);
+    else
+      hipLaunchKernelGGL((cm_unpack_kernel<false>), dim3(static_cast<uint32_t>(blocks)),
+                         dim3(kThreads), 0, s, t.mats, t.off, t.nmats, one, scale);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace zf

@@ -14,7 +14,8 @@ selection and new states into the other buffer while reading the previous
 ones (ZF_STATES_REMAP), so a column that stays selected carries its moments
 (the selective optimizer follows its subset, Zero-stall Pipeline "Swapping
 out/in") without a separate pass.  Gradients come from caller-owned slots;
-step t reads slot (t-1) mod len(slots).
+step t reads slot (t-1) mod len(slots).  Every tensor of the runner is
+stored in one layout (ROW_MAJOR or CHANNEL_MAJOR, see the binding).
 """
 
 from __future__ import annotations
@@ -24,8 +25,8 @@ from typing import List, Optional, Sequence, Tuple
 
 import torch
 
-from ._lib import (STATES_INIT, STATES_INPLACE, STATES_REMAP, AdamHparams, MatrixBuffers, Plan,
-                   Selection, StateSource, k_from_ratio)
+from ._lib import (ROW_MAJOR, STATES_INIT, STATES_INPLACE, STATES_REMAP, AdamHparams,
+                   MatrixBuffers, Plan, Selection, StateSource, _stored, k_from_ratio)
 
 
 @dataclass(frozen=True)
@@ -65,11 +66,13 @@ class SelectiveUpdateRunner:
                  refresh: int, accum: int, grad_slots: Sequence[Sequence[torch.Tensor]],
                  weights: Sequence[torch.Tensor],
                  init_master: Optional[Sequence[torch.Tensor]] = None,
-                 device=None, keep_unpacked: bool = True):
+                 device=None, keep_unpacked: bool = True, layout: int = ROW_MAJOR):
         self.device = torch.device(device) if device is not None else torch.device("cuda")
         self.shapes = [(int(n), int(m)) for n, m in shapes]
         self.ratio, self.hp, self.R, self.S = ratio, hp, int(refresh), int(accum)
         self.ks = [k_from_ratio(ratio, m) for _, m in self.shapes]
+        self.layout = layout
+        self.keep_unpacked = keep_unpacked
         self.weights = list(weights)
         self.init_master = list(init_master) if init_master is not None else None
         dev = self.device
@@ -80,12 +83,12 @@ class SelectiveUpdateRunner:
         for (n, m), k in zip(self.shapes, self.ks):
             for p in range(2):
                 self.sels[p].append(Selection(m, k, dev))
-                self.states[p].append(tuple(torch.empty(n, k, dtype=f32, device=dev)
-                                            for _ in range(3)))
-            self.acc.append(torch.empty(n, m - k, dtype=f32, device=dev))
+                self.states[p].append(tuple(torch.empty(*_stored(layout, n, k), dtype=f32,
+                                                        device=dev) for _ in range(3)))
+            self.acc.append(torch.empty(*_stored(layout, n, m - k), dtype=f32, device=dev))
             self.norms.append(torch.empty(m, dtype=f32, device=dev))
-            self.unpacked.append(torch.empty(n, m, dtype=f32, device=dev) if keep_unpacked
-                                 else torch.empty(0, m, dtype=f32, device=dev))
+            self.unpacked.append(torch.empty(*_stored(layout, n, m), dtype=f32, device=dev)
+                                 if keep_unpacked else None)
         self.grad_slots = [list(s) for s in grad_slots]
         self.plans = [[self._plan(slot, p) for p in range(2)] for slot in range(len(self.grad_slots))]
         self.t = 0
@@ -102,7 +105,7 @@ class SelectiveUpdateRunner:
             q_bufs.append(MatrixBuffers(
                 grad=self.grad_slots[slot][q], k=k, sel=self.sels[p][q], weight=self.weights[q],
                 master=P, exp_avg=M, exp_avg_sq=V, acc=self.acc[q], norms=self.norms[q],
-                unpacked=self.unpacked[q] if self.unpacked[q].shape[0] == n else None, src=src))
+                unpacked=self.unpacked[q], src=src, layout=self.layout))
         return Plan(q_bufs)
 
     @property
@@ -136,7 +139,7 @@ class SelectiveUpdateRunner:
             mode = STATES_INPLACE
         with rec("update_first" if kind.step_in_interval == 1 else "update"):
             plan.update(self.hp, t, mode, kind.step_in_interval, self.S, stream=stream)
-        if kind.interval_end:
+        if kind.interval_end and self.keep_unpacked:
             with rec("unpack"):
                 plan.unpack(1.0 / kind.step_in_interval, stream)
         return kind

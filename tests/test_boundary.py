@@ -15,6 +15,7 @@ from paper_2505_12242_amd import _lib  # noqa: E402
 
 LIB = _lib.LIB
 OK, EINVAL, EWS = _lib.ZF_OK, _lib.ZF_EINVAL, _lib.ZF_EWORKSPACE
+RM, CM = _lib.ROW_MAJOR, _lib.CHANNEL_MAJOR
 A = 0x7F0000000000  # a 256-byte aligned fake device address
 B = A + (1 << 30)
 C = A + (2 << 30)
@@ -62,18 +63,23 @@ def sel(m, k, base=C):
 
 
 def test_colnorm_validation():
-    ws = LIB.zf_colnorm_workspace_bytes(64, 64)
-    assert ws > 0 and LIB.zf_colnorm_workspace_bytes(0, 64) == 0
+    ws = LIB.zf_colnorm_workspace_bytes(64, 64, RM)
+    assert ws > 0 and LIB.zf_colnorm_workspace_bytes(0, 64, RM) == 0
+    assert LIB.zf_colnorm_workspace_bytes(64, 64, CM) == 0
     call = LIB.zf_colnorm
-    assert call(None, 4, 4, 4, B, C, ws, None) == EINVAL          # null gradient
-    assert call(A, 4, 4, 3, B, C, ws, None) == EINVAL             # ld < m
-    assert call(A + 1, 4, 4, 4, B, C, ws, None) == EINVAL         # misaligned bf16
-    assert call(A, 4, 4, 4, B + 2, C, ws, None) == EINVAL         # misaligned fp32
-    assert call(A, -1, 4, 4, B, C, ws, None) == EINVAL            # n < 0
-    assert call(A, 4, 4, 4, A + 8, C, ws, None) == EINVAL         # output inside gradient
-    assert call(A, 64, 64, 64, B, None, 0, None) == EWS           # no workspace
-    assert call(A, 64, 64, 64, B, C, ws - 8, None) == EWS         # small workspace
-    assert call(A, 4, 0, 4, None, None, 0, None) == OK            # m = 0: nothing to do
+    assert call(None, 4, 4, 4, RM, B, C, ws, None) == EINVAL          # null gradient
+    assert call(A, 4, 4, 3, RM, B, C, ws, None) == EINVAL             # ld < m
+    assert call(A, 4, 4, 4, 7, B, C, ws, None) == EINVAL              # unknown layout
+    assert call(A + 1, 4, 4, 4, RM, B, C, ws, None) == EINVAL         # misaligned bf16
+    assert call(A, 4, 4, 4, RM, B + 2, C, ws, None) == EINVAL         # misaligned fp32
+    assert call(A, -1, 4, 4, RM, B, C, ws, None) == EINVAL            # n < 0
+    assert call(A, 4, 4, 4, RM, A + 8, C, ws, None) == EINVAL         # output inside gradient
+    assert call(A, 64, 64, 64, RM, B, None, 0, None) == EWS           # no workspace
+    assert call(A, 64, 64, 64, RM, B, C, ws - 8, None) == EWS         # small workspace
+    assert call(A, 4, 0, 4, RM, None, None, 0, None) == OK            # m = 0: nothing to do
+    # channel-major: the gradient is [m][ld >= n]
+    assert call(A, 8, 4, 7, CM, B, None, 0, None) == EINVAL           # ld < n
+    assert call(A, 8, 0, 8, CM, None, None, 0, None) == OK
 
 
 def test_topk_validation():
@@ -94,14 +100,15 @@ def test_topk_validation():
 
 def adam_args(**over):
     hp = _lib.ZfAdamHparams(1e-5, 0.9, 0.999, 1e-8, 0.0)
-    args = dict(grad=A, n=8, m=64, ld=64, sel=sel(64, 6), k=6, P=B, M=B + (1 << 20),
+    args = dict(grad=A, n=8, m=64, ld=64, layout=RM, sel=sel(64, 6), k=6, P=B, M=B + (1 << 20),
                 V=B + (2 << 20), lds=6, W=D, ldw=64, hp=hp, step=1, mode=0, src=None)
     args.update(over)
     return args
 
 
 def call_adam(a):
-    return LIB.zf_adam_selected(a["grad"], a["n"], a["m"], a["ld"], ctypes.byref(a["sel"]),
+    return LIB.zf_adam_selected(a["grad"], a["n"], a["m"], a["ld"], a["layout"],
+                                ctypes.byref(a["sel"]),
                                 a["k"], a["P"], a["M"], a["V"], a["lds"], a["W"], a["ldw"],
                                 ctypes.byref(a["hp"]), a["step"], a["mode"],
                                 ctypes.byref(a["src"]) if a["src"] is not None else None, None)
@@ -109,6 +116,8 @@ def call_adam(a):
 
 @pytest.mark.parametrize("over", [
     dict(step=0),
+    dict(layout=2),
+    dict(layout=CM),                               # [k][ld >= n] states: lds=6 < n=8
     dict(k=65),
     dict(lds=5),
     dict(ldw=63),
@@ -139,32 +148,38 @@ def test_adam_empty_is_ok_without_device():
 @pytest.mark.parametrize("sii,S", [(0, 4), (5, 4), (1, 0)])
 def test_pack_validation(sii, S):
     s = sel(64, 6)
-    assert LIB.zf_pack_accumulate(A, 8, 64, 64, ctypes.byref(s), 6, B, 58, sii, S, None) == EINVAL
+    assert LIB.zf_pack_accumulate(A, 8, 64, 64, RM, ctypes.byref(s), 6, B, 58, sii, S,
+                                  None) == EINVAL
 
 
 def test_pack_rejects_short_stride_and_alias():
     s = sel(64, 6)
-    assert LIB.zf_pack_accumulate(A, 8, 64, 64, ctypes.byref(s), 6, B, 57, 1, 4, None) == EINVAL
-    assert LIB.zf_pack_accumulate(A, 8, 64, 64, ctypes.byref(s), 6, A, 58, 1, 4, None) == EINVAL
-    assert LIB.zf_pack_accumulate(A, 0, 64, 64, ctypes.byref(s), 6, B, 58, 1, 4, None) == OK
+    assert LIB.zf_pack_accumulate(A, 8, 64, 64, RM, ctypes.byref(s), 6, B, 57, 1, 4, None) == EINVAL
+    assert LIB.zf_pack_accumulate(A, 8, 64, 64, RM, ctypes.byref(s), 6, A, 58, 1, 4, None) == EINVAL
+    assert LIB.zf_pack_accumulate(A, 0, 64, 64, RM, ctypes.byref(s), 6, B, 58, 1, 4, None) == OK
+    # channel-major packed buffer is [m-k][ld >= n]
+    assert LIB.zf_pack_accumulate(A, 8, 64, 8, CM, ctypes.byref(s), 6, B, 7, 1, 4, None) == EINVAL
 
 
 def test_unpack_validation():
     s = sel(64, 6)
-    assert LIB.zf_unpack(B, 58, ctypes.byref(s), 6, 8, 64, 1.0, B + 64, 64, None) == EINVAL
-    assert LIB.zf_unpack(B, 58, ctypes.byref(s), 6, 8, 64, 1.0, D, 63, None) == EINVAL
-    assert LIB.zf_unpack(B, 58, None, 6, 8, 64, 1.0, D, 64, None) == EINVAL
-    assert LIB.zf_unpack(B, 58, ctypes.byref(s), 70, 8, 64, 1.0, D, 64, None) == EINVAL
+    assert LIB.zf_unpack(B, 58, ctypes.byref(s), 6, 8, 64, RM, 1.0, B + 64, 64, None) == EINVAL
+    assert LIB.zf_unpack(B, 58, ctypes.byref(s), 6, 8, 64, RM, 1.0, D, 63, None) == EINVAL
+    assert LIB.zf_unpack(B, 58, None, 6, 8, 64, RM, 1.0, D, 64, None) == EINVAL
+    assert LIB.zf_unpack(B, 58, ctypes.byref(s), 70, 8, 64, RM, 1.0, D, 64, None) == EINVAL
+    assert LIB.zf_unpack(B, 8, ctypes.byref(s), 6, 8, 64, CM, 1.0, D, 7, None) == EINVAL
 
 
 def test_update_fused_validation():
     s = sel(64, 6)
     hp = _lib.ZfAdamHparams(1e-5, 0.9, 0.999, 1e-8, 0.0)
     # accumulator aliasing the master states
-    assert LIB.zf_update_fused(A, 8, 64, 64, ctypes.byref(s), 6, B, B + (1 << 20), B + (2 << 20), 6,
-                               D, 64, ctypes.byref(hp), 1, 0, None, B, 58, 1, 4, None) == EINVAL
-    assert LIB.zf_update_fused(A, 8, 64, 64, ctypes.byref(s), 6, B, B + (1 << 20), B + (2 << 20), 6,
-                               D, 64, ctypes.byref(hp), 1, 0, None, E, 58, 2, 1, None) == EINVAL
+    assert LIB.zf_update_fused(A, 8, 64, 64, RM, ctypes.byref(s), 6, B, B + (1 << 20),
+                               B + (2 << 20), 6, D, 64, ctypes.byref(hp), 1, 0, None, B, 58, 1, 4,
+                               None) == EINVAL
+    assert LIB.zf_update_fused(A, 8, 64, 64, RM, ctypes.byref(s), 6, B, B + (1 << 20),
+                               B + (2 << 20), 6, D, 64, ctypes.byref(hp), 1, 0, None, E, 58, 2, 1,
+                               None) == EINVAL
 
 
 def test_plan_validation():
@@ -174,6 +189,10 @@ def test_plan_validation():
     assert LIB.zf_plan_create(arr, 0, ctypes.byref(h)) == EINVAL
     arr[0].n, arr[0].m, arr[0].k = 4, 4, 5          # k > m
     assert LIB.zf_plan_create(arr, 1, ctypes.byref(h)) == EINVAL
+    arr2 = (_lib.ZfMatrix * 2)()
+    arr2[0].n, arr2[0].m, arr2[0].k, arr2[0].layout = 0, 4, 1, RM
+    arr2[1].n, arr2[1].m, arr2[1].k, arr2[1].layout = 0, 4, 1, CM   # mixed layouts
+    assert LIB.zf_plan_create(arr2, 2, ctypes.byref(h)) == EINVAL
     assert LIB.zf_plan_colnorm(None, None) == EINVAL
     assert LIB.zf_plan_update(None, None, 1, 0, 1, 1, 1, 1, None) == EINVAL
     assert LIB.zf_plan_device_bytes(None) == 0

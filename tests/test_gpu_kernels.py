@@ -16,6 +16,30 @@ pytestmark = pytest.mark.gpu
 
 zf = pytest.importorskip("paper_2505_12242_amd")
 HP = zf.AdamHparams(lr=1e-5, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0)
+LAYOUTS = [pytest.param(zf.ROW_MAJOR, id="rm"), pytest.param(zf.CHANNEL_MAJOR, id="cm")]
+
+
+def T(a, layout):
+    """Logical [rows][cols] host array -> its storage in `layout`."""
+    return a if layout == zf.ROW_MAJOR else np.ascontiguousarray(np.asarray(a).T)
+
+
+def bits_dev(bits, layout, **kw):
+    return bf16_dev(T(bits, layout), **kw)
+
+
+def f32_dev_l(a, layout):
+    return f32_dev(T(a, layout))
+
+
+def f32_host(t, layout):
+    a = f32_np(t)
+    return a if layout == zf.ROW_MAJOR else np.ascontiguousarray(a.T)
+
+
+def bits_host(t, layout):
+    b = bits_np(t)
+    return b if layout == zf.ROW_MAJOR else np.ascontiguousarray(b.T)
 
 
 def grad_bits(n, m, seed, sigma=1.5):
@@ -44,17 +68,19 @@ SHAPES = [(1, 1), (1, 513), (2, 3), (3, 7), (7, 8), (8, 63), (63, 64), (64, 65),
 
 
 @pytest.mark.parametrize("n,m", SHAPES)
-@pytest.mark.parametrize("layout", ["dense", "padded", "offset"])
-def test_colnorm(n, m, layout):
+@pytest.mark.parametrize("storage", ["dense", "padded", "offset"])
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_colnorm(n, m, storage, layout):
     bits = grad_bits(n, m, derive_seed("cn", n, m))
     bits[:, ::7] = 0  # zero columns must give exactly 0
-    if layout == "dense":
-        G = bf16_dev(bits)
-    elif layout == "padded":
-        G = bf16_dev(bits, ld=((m + 7) // 8) * 8 + 8)
+    width = m if layout == zf.ROW_MAJOR else n
+    if storage == "dense":
+        G = bits_dev(bits, layout)
+    elif storage == "padded":
+        G = bits_dev(bits, layout, ld=((width + 7) // 8) * 8 + 8)
     else:
-        G = bf16_dev(bits, ld=m + 3, offset=1)
-    got = f32_np(zf.colnorm(G))
+        G = bits_dev(bits, layout, ld=width + 3, offset=1)
+    got = f32_np(zf.colnorm(G, layout=layout))
     torch.cuda.synchronize()
     want = O.colnorm(bits)
     ok, worst = rel_close(got, want, 1e-5)
@@ -64,12 +90,13 @@ def test_colnorm(n, m, layout):
         assert same_bits(got, want)
 
 
-def test_colnorm_exact_cases():
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_colnorm_exact_cases(layout):
     n, m = 300, 70
     bits = np.zeros((n, m), np.uint16)
     bits[:, 5] = 0x3E00  # 0.125 -> n/64 exactly
     bits[::3, 9] = 0xC100  # -8
-    got = f32_np(zf.colnorm(bf16_dev(bits)))
+    got = f32_np(zf.colnorm(bits_dev(bits, layout), layout=layout))
     assert got[5] == np.float32(n / 64) and got[9] == np.float32(100 * 64)
     assert np.count_nonzero(got) == 2
 
@@ -124,30 +151,36 @@ def check_states(P, M, V, Pw, Mw, Vw, g_abs, Mprev):
                                        (513, 1000, 0.25), (130, 4097, 0.01), (7, 64, 1.0)])
 @pytest.mark.parametrize("wd", [0.0, 0.01])
 @pytest.mark.parametrize("step", [1, 7])
-def test_adam_inplace(n, m, ratio, wd, step):
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_adam_inplace(n, m, ratio, wd, step, layout):
     bits, sel, P, M, V, W = adam_case(n, m, ratio, derive_seed("adam", n, m))
     hp = zf.AdamHparams(weight_decay=wd)
-    Pd, Md, Vd, Wd = f32_dev(P), f32_dev(M), f32_dev(V), bf16_dev(W)
-    zf.adam_selected(bf16_dev(bits, ld=m + 5), sel_from_oracle(sel), Pd, Md, Vd, Wd, hp, step)
+    Pd, Md, Vd, Wd = f32_dev_l(P, layout), f32_dev_l(M, layout), f32_dev_l(V, layout), \
+        bits_dev(W, layout)
+    ld = (m if layout == zf.ROW_MAJOR else n) + 5
+    zf.adam_selected(bits_dev(bits, layout, ld=ld), sel_from_oracle(sel), Pd, Md, Vd, Wd, hp,
+                     step, layout=layout)
     torch.cuda.synchronize()
     Pw, Mw, Vw, wsel = O.adam_selected(bits, sel.sel, P, M, V, oracle_consts(hp, step))
     g_abs = np.abs(O.widen(bits[:, sel.sel.astype(np.int64)]))
-    check_states(f32_np(Pd), f32_np(Md), f32_np(Vd), Pw, Mw, Vw, g_abs, M)
-    Wgot = bits_np(Wd)
+    Pg, Mg, Vg = f32_host(Pd, layout), f32_host(Md, layout), f32_host(Vd, layout)
+    check_states(Pg, Mg, Vg, Pw, Mw, Vw, g_abs, M)
+    Wgot = bits_host(Wd, layout)
     Wwant = W.copy()
     Wwant[:, sel.sel.astype(np.int64)] = wsel
-    same = same_bits(f32_np(Pd), Pw)
+    same = same_bits(Pg, Pw)
     if same:
         assert np.array_equal(Wgot, Wwant)
     else:
         diff = np.abs(Wgot.astype(np.int32) - Wwant.astype(np.int32))
         assert diff.max() <= 1
     # report exactness (the kernel is written to reproduce the oracle's rounding)
-    assert same_bits(f32_np(Md), Mw) and same_bits(f32_np(Vd), Vw) and same
+    assert same_bits(Mg, Mw) and same_bits(Vg, Vw) and same
 
 
 @pytest.mark.parametrize("use_master", [False, True])
-def test_adam_remap_and_init(use_master):
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_adam_remap_and_init(use_master, layout):
     n, m = 33, 300
     rng = np.random.default_rng(5)
     bits = grad_bits(n, m, 17)
@@ -159,69 +192,82 @@ def test_adam_remap_and_init(use_master):
     M = (rng.standard_normal((n, 40)) * 1e-3).astype(np.float32)
     V = (rng.random((n, 40)) * 1e-4).astype(np.float32)
     old_d, new_d = sel_from_oracle(old), sel_from_oracle(new)
-    Pn = torch.full((n, 45), np.nan, device="cuda")
+    shape = (n, 45) if layout == zf.ROW_MAJOR else (45, n)
+    Pn = torch.full(shape, np.nan, device="cuda")
     Mn, Vn = torch.full_like(Pn, np.nan), torch.full_like(Pn, np.nan)
-    Wd = bf16_dev(W)
-    src = zf.StateSource(prev=old_d, prev_master=f32_dev(P), prev_exp_avg=f32_dev(M),
-                         prev_exp_avg_sq=f32_dev(V),
-                         init_master=f32_dev(master) if use_master else None)
-    zf.adam_selected(bf16_dev(bits), new_d, Pn, Mn, Vn, Wd, HP, 3, mode=zf.STATES_REMAP, src=src)
+    Wd = bits_dev(W, layout)
+    src = zf.StateSource(prev=old_d, prev_master=f32_dev_l(P, layout),
+                         prev_exp_avg=f32_dev_l(M, layout), prev_exp_avg_sq=f32_dev_l(V, layout),
+                         init_master=f32_dev_l(master, layout) if use_master else None)
+    zf.adam_selected(bits_dev(bits, layout), new_d, Pn, Mn, Vn, Wd, HP, 3, mode=zf.STATES_REMAP,
+                     src=src, layout=layout)
     torch.cuda.synchronize()
     P2, M2, V2 = O.remap(old, new, P, M, V, W, master if use_master else None)
     Pw, Mw, Vw, wsel = O.adam_selected(bits, new.sel, P2, M2, V2, oracle_consts(HP, 3))
-    assert same_bits(f32_np(Pn), Pw) and same_bits(f32_np(Mn), Mw) and same_bits(f32_np(Vn), Vw)
-    assert np.array_equal(bits_np(Wd)[:, new.sel.astype(np.int64)], wsel)
+    assert same_bits(f32_host(Pn, layout), Pw) and same_bits(f32_host(Mn, layout), Mw)
+    assert same_bits(f32_host(Vn, layout), Vw)
+    assert np.array_equal(bits_host(Wd, layout)[:, new.sel.astype(np.int64)], wsel)
     # INIT: every selected column starts fresh
-    Pi, Mi, Vi = (torch.zeros(n, 45, device="cuda") for _ in range(3))
-    Wd2 = bf16_dev(W)
-    zf.adam_selected(bf16_dev(bits), new_d, Pi, Mi, Vi, Wd2, HP, 1, mode=zf.STATES_INIT,
-                     src=zf.StateSource(init_master=f32_dev(master) if use_master else None))
+    Pi, Mi, Vi = (torch.zeros(shape, device="cuda") for _ in range(3))
+    Wd2 = bits_dev(W, layout)
+    zf.adam_selected(bits_dev(bits, layout), new_d, Pi, Mi, Vi, Wd2, HP, 1, mode=zf.STATES_INIT,
+                     src=zf.StateSource(init_master=f32_dev_l(master, layout) if use_master
+                                        else None), layout=layout)
     torch.cuda.synchronize()
     P3, M3, V3 = O.remap(None, new, None, None, None, W, master if use_master else None)
     Pw, Mw, Vw, _ = O.adam_selected(bits, new.sel, P3, M3, V3, oracle_consts(HP, 1))
-    assert same_bits(f32_np(Pi), Pw) and same_bits(f32_np(Mi), Mw) and same_bits(f32_np(Vi), Vw)
+    assert same_bits(f32_host(Pi, layout), Pw) and same_bits(f32_host(Mi, layout), Mw)
+    assert same_bits(f32_host(Vi, layout), Vw)
 
 
 # ---------------------------------------------------------------- pack / unpack / fused
 
 @pytest.mark.parametrize("n,m,ratio", [(1, 1, 0.0), (2, 3, 0.34), (65, 513, 0.1),
-                                       (300, 4097, 0.05), (17, 64, 1.0), (9, 700, 0.0)])
-def test_pack_accumulate_and_unpack(n, m, ratio):
+                                       (300, 4097, 0.05), (17, 64, 1.0), (9, 700, 0.0),
+                                       (4104, 40, 0.1), (8200, 3, 0.34)])
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_pack_accumulate_and_unpack(n, m, ratio, layout):
     rng = np.random.default_rng(n * 1000 + m)
     sel = O.select_topk(rng.random(m).astype(np.float32), O.k_from_ratio(ratio, m))
     sd = sel_from_oracle(sel)
     u = m - sel.k
     S = 4
-    A = torch.full((n, u + 3), np.nan, device="cuda")[:, :u]  # padded stride, junk content
+    rows, width = (n, u) if layout == zf.ROW_MAJOR else (u, n)
+    A = torch.full((rows, width + 4), np.nan, device="cuda")[:, :width]  # padded, junk content
     Aw = None
     for t in range(1, S + 1):
         bits = grad_bits(n, m, derive_seed("pack", n, m, t))
         bits[0, ::5] = 0x8000  # -0.0 survives the overwrite
-        zf.pack_accumulate(bf16_dev(bits), sd, A, t, S)
+        zf.pack_accumulate(bits_dev(bits, layout), sd, A, t, S, layout=layout)
         Aw = O.pack_accumulate(bits, sel.unsel, Aw, t)
         torch.cuda.synchronize()
-        assert same_bits(f32_np(A), Aw), t
+        assert same_bits(f32_host(A, layout), Aw), t
+    drows, dwidth = (n, m) if layout == zf.ROW_MAJOR else (m, n)
     for scale in (1.0, 0.25, 1.0 / 3.0):
-        D = torch.full((n, m + 2), 7.0, device="cuda")[:, :m]
-        zf.unpack(A, sd, scale, out=D)
+        D = torch.full((drows, dwidth + 4), 7.0, device="cuda")[:, :dwidth]
+        zf.unpack(A, sd, scale, out=D, layout=layout)
         torch.cuda.synchronize()
-        assert same_bits(f32_np(D), O.unpack(Aw, sel, float(np.float32(scale))))
+        assert same_bits(f32_host(D, layout), O.unpack(Aw, sel, float(np.float32(scale))))
 
 
-@pytest.mark.parametrize("n,m,ratio", [(65, 513, 0.1), (200, 4096, 0.1), (5, 9, 0.5)])
-def test_fused_equals_separate(n, m, ratio):
+@pytest.mark.parametrize("n,m,ratio", [(65, 513, 0.1), (200, 4096, 0.1), (5, 9, 0.5),
+                                       (4104, 70, 0.1)])
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_fused_equals_separate(n, m, ratio, layout):
     bits, sel, P, M, V, W = adam_case(n, m, ratio, derive_seed("fused", n, m))
     sd = sel_from_oracle(sel)
-    G = bf16_dev(bits)
-    a = [f32_dev(P), f32_dev(M), f32_dev(V), bf16_dev(W)]
-    b = [f32_dev(P), f32_dev(M), f32_dev(V), bf16_dev(W)]
-    A1 = torch.zeros(n, m - sel.k, device="cuda")
-    A2 = torch.zeros(n, m - sel.k, device="cuda")
-    zf.update_fused(G, sd, *a, HP, 2, A1, 1, 4)
-    zf.update_fused(G, sd, *a, HP, 3, A1, 2, 4)
+    G = bits_dev(bits, layout)
+    L = layout
+    a = [f32_dev_l(P, L), f32_dev_l(M, L), f32_dev_l(V, L), bits_dev(W, L)]
+    b = [f32_dev_l(P, L), f32_dev_l(M, L), f32_dev_l(V, L), bits_dev(W, L)]
+    ashape = (n, m - sel.k) if L == zf.ROW_MAJOR else (m - sel.k, n)
+    A1 = torch.zeros(ashape, device="cuda")
+    A2 = torch.zeros(ashape, device="cuda")
+    zf.update_fused(G, sd, *a, HP, 2, A1, 1, 4, layout=L)
+    zf.update_fused(G, sd, *a, HP, 3, A1, 2, 4, layout=L)
     for step, sii in ((2, 1), (3, 2)):
-        zf.adam_selected(G, sd, *b, HP, step)
-        zf.pack_accumulate(G, sd, A2, sii, 4)
+        zf.adam_selected(G, sd, *b, HP, step, layout=L)
+        zf.pack_accumulate(G, sd, A2, sii, 4, layout=L)
     torch.cuda.synchronize()
     for x, y in zip(a, b):
         assert torch.equal(x.view(torch.int32) if x.dtype == torch.float32 else x.view(torch.int16),
@@ -232,8 +278,11 @@ def test_fused_equals_separate(n, m, ratio):
 def test_empty_sizes_are_no_ops():
     G = torch.empty(0, 9, dtype=torch.bfloat16, device="cuda")
     s = zf.colnorm(G)
+    s_cm = zf.colnorm(torch.empty(9, 0, dtype=torch.bfloat16, device="cuda"),
+                      layout=zf.CHANNEL_MAJOR)
     torch.cuda.synchronize()
     assert torch.equal(s, torch.zeros(9, device="cuda"))
+    assert torch.equal(s_cm, torch.zeros(9, device="cuda"))
     sel = zf.topk_select(torch.empty(0, device="cuda"), 0.1)
     assert sel.k == 0
     sd = zf.topk_select(torch.rand(9, device="cuda"), 0.5)
@@ -241,11 +290,12 @@ def test_empty_sizes_are_no_ops():
     torch.cuda.synchronize()
 
 
-def test_deterministic_reruns():
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_deterministic_reruns(layout):
     n, m = 2000, 3000
-    G = bf16_dev(grad_bits(n, m, 99))
-    a = zf.colnorm(G)
-    b = zf.colnorm(G)
+    G = bits_dev(grad_bits(n, m, 99), layout)
+    a = zf.colnorm(G, layout=layout)
+    b = zf.colnorm(G, layout=layout)
     sa = zf.topk_select(a, 0.1)
     sb = zf.topk_select(b, 0.1)
     torch.cuda.synchronize()

@@ -15,7 +15,11 @@ pytestmark = pytest.mark.gpu
 zf = pytest.importorskip("paper_2505_12242_amd")
 
 
-def run_workload(name, use_master):
+def T(a, layout):
+    return a if layout == zf.ROW_MAJOR else np.ascontiguousarray(np.asarray(a).T)
+
+
+def run_workload(name, use_master, layout=0):
     wl = get_workload(name)
     hp = zf.AdamHparams(wl.hyper.lr, wl.hyper.beta1, wl.hyper.beta2, wl.hyper.eps,
                         wl.hyper.weight_decay)
@@ -27,23 +31,27 @@ def run_workload(name, use_master):
         slot = []
         for q, (n, m) in enumerate(shapes):
             s = step_scales(wl, q, t, k_boundary=ks[q])
-            slot.append(gradient(n, m, s, derive_seed(wl.seed, q, "grad", t), device=dev))
+            g = gradient(n, m, s, derive_seed(wl.seed, q, "grad", t), device=dev)
+            slot.append(g if layout == zf.ROW_MAJOR else g.t().contiguous())
         slots.append(slot)
     for q, (n, m) in enumerate(shapes):
         mw = master_weights(n, m, derive_seed(wl.seed, q, "master"), wl.master_std, device=dev)
+        if layout == zf.CHANNEL_MAJOR:
+            mw = mw.t().contiguous()
         masters.append(mw)
         weights.append(mw.to(torch.bfloat16))
-    w0 = [bits_np(w) for w in weights]
+    w0 = [T(bits_np(w), layout) for w in weights]
     runner = zf.SelectiveUpdateRunner(shapes, wl.ratio, hp, wl.refresh, wl.accum, slots, weights,
-                                      init_master=masters if use_master else None)
-    orcs = [O.MatrixOracle(f32_np(masters[q]) if use_master else O.widen(w0[q]), w0[q], wl.ratio,
+                                      init_master=masters if use_master else None, layout=layout)
+    orcs = [O.MatrixOracle(T(f32_np(masters[q]), layout) if use_master else O.widen(w0[q]), w0[q],
+                           wl.ratio,
                            hp.lr, hp.beta1, hp.beta2, hp.eps, hp.weight_decay, wl.refresh,
                            wl.accum) for q in range(len(shapes))]
     for t in range(1, wl.steps + 1):
         kind = runner.step()
         torch.cuda.synchronize()
         for q, orc in enumerate(orcs):
-            out = orc.step(bits_np(slots[t - 1][q]))
+            out = orc.step(T(bits_np(slots[t - 1][q]), layout))
             name_q = wl.matrices[q].name
             if kind.refresh:
                 ok, worst = rel_close(f32_np(runner.norms[q]), out["norms"], 1e-5)
@@ -53,24 +61,30 @@ def run_workload(name, use_master):
                 assert np.array_equal(sel.unsel_idx.cpu().numpy(), orc.sel.unsel), (name_q, t)
                 assert np.array_equal(mask_np(sel.mask), orc.sel.mask), (name_q, t)
                 assert np.array_equal(sel.prefix.cpu().numpy(), orc.sel.prefix), (name_q, t)
-            assert same_bits(f32_np(runner.acc[q]), orc.A), (name_q, t)
-            P, M, V = (f32_np(x) for x in runner.state[q])
+            assert same_bits(T(f32_np(runner.acc[q]), layout), orc.A), (name_q, t)
+            P, M, V = (T(f32_np(x), layout) for x in runner.state[q])
             ok, w = rel_close(P, orc.P, 2e-6)
             assert ok, (name_q, t, "P", w)
             ok, w = rel_close(V, orc.V, 2e-6)
             assert ok, (name_q, t, "V", w)
             assert same_bits(P, orc.P) and same_bits(M, orc.M) and same_bits(V, orc.V), (name_q, t)
-            assert np.array_equal(bits_np(weights[q]), orc.W), (name_q, t)
+            assert np.array_equal(T(bits_np(weights[q]), layout), orc.W), (name_q, t)
             if kind.interval_end:
-                assert same_bits(f32_np(runner.unpacked[q]), out["unpacked"]), (name_q, t)
+                assert same_bits(T(f32_np(runner.unpacked[q]), layout), out["unpacked"]), \
+                    (name_q, t)
     runner.close()
 
 
+LAYOUTS = [pytest.param(zf.ROW_MAJOR, id="rm"), pytest.param(zf.CHANNEL_MAJOR, id="cm")]
+
+
 @pytest.mark.timeout(300)
-def test_linear_4096_fresh_selection_step():
-    run_workload("linear-4096x4096", use_master=True)
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_linear_4096_fresh_selection_step(layout):
+    run_workload("linear-4096x4096", use_master=True, layout=layout)
 
 
 @pytest.mark.timeout(900)
-def test_llama2_7b_layer_four_steps():
-    run_workload("llama2-7b-layer", use_master=False)
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_llama2_7b_layer_four_steps(layout):
+    run_workload("llama2-7b-layer", use_master=False, layout=layout)
