@@ -70,26 +70,38 @@ __device__ __forceinline__ rsrc_t rows_rsrc(const T* base, int64_t i0, int64_t i
   return make_rsrc(base + i0 * ld, bytes);
 }
 
+// Cache policy of a buffer access.  Every stream of the hot path is read or
+// written once per kernel, so the kernels mark their traffic non-temporal
+// (kStream); kCached is the default policy.
+constexpr int kCached = 0;
+constexpr int kStream = 2;  // "nt"
+
+template <int AUX = kCached>
 __device__ __forceinline__ float buf_f32(rsrc_t r, uint32_t voff, uint32_t soff) {
-  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, AUX));
 }
+template <int AUX = kCached>
 __device__ __forceinline__ uint16_t buf_u16(rsrc_t r, uint32_t voff, uint32_t soff) {
-  return static_cast<uint16_t>(__builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0));
+  return static_cast<uint16_t>(__builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, AUX));
 }
+template <int AUX = kCached>
 __device__ __forceinline__ void buf_put_f32(float v, rsrc_t r, uint32_t voff, uint32_t soff) {
-  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, voff, soff, 0);
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, voff, soff, AUX);
 }
+template <int AUX = kCached>
 __device__ __forceinline__ void buf_put_u16(uint16_t v, rsrc_t r, uint32_t voff, uint32_t soff) {
-  __builtin_amdgcn_raw_buffer_store_b16(v, r, voff, soff, 0);
+  __builtin_amdgcn_raw_buffer_store_b16(v, r, voff, soff, AUX);
 }
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
+template <int AUX = kCached>
 __device__ __forceinline__ u32x4 buf_b128(rsrc_t r, uint32_t voff, uint32_t soff) {
-  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, AUX);
 }
+template <int AUX = kCached>
 __device__ __forceinline__ void buf_put_b128(u32x4 v, rsrc_t r, uint32_t voff, uint32_t soff) {
-  __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, soff, 0);
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, soff, AUX);
 }
 
 // One Adam/AdamW element update; each line is one fp32 operation (the

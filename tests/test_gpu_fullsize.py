@@ -1,0 +1,90 @@
+"""Parity at full size, in the launch configuration bench.py times: the whole
+Llama-2-7B-shaped gradient set (226 matrices, channel-major, batched plans,
+three-slot gradient ring) for 8 steps of the R = S = 4 schedule -- first
+selection, accumulation, hand-over at step 4, refresh with state remap at
+step 5, hand-over at step 8.
+
+* Sampled matrices (embedding, LM head and four decoder weights of three
+  shapes) are run through the oracle step by step and every output is
+  compared in full.
+* Every matrix is checked for properties that hold at any size: the
+  selection is a partition of size k that ranks the scores the kernels
+  produced, and the scores sum to the squared Frobenius norm of the
+  gradient computed by torch in fp64.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from tests._gpu import bits_np, f32_np, mask_np, rel_close, same_bits
+
+pytestmark = pytest.mark.gpu
+
+zf = pytest.importorskip("paper_2505_12242_amd")
+bench = pytest.importorskip("bench")
+
+SAMPLES = ["embed_tokens", "layers.0.q_proj", "layers.0.down_proj", "layers.17.gate_proj",
+           "layers.31.v_proj", "lm_head"]
+STEPS = 8
+
+
+def logical(t):
+    return t.t()
+
+
+@pytest.mark.timeout(1200)
+def test_llama2_7b_full_set_sampled_parity():
+    from workloads import get_workload
+    wl = get_workload("llama2-7b-full")
+    hp = zf.AdamHparams(wl.hyper.lr, wl.hyper.beta1, wl.hyper.beta2, wl.hyper.eps,
+                        wl.hyper.weight_decay)
+    dev = torch.device("cuda")
+    layout = zf.CHANNEL_MAJOR
+    shapes, ks, slots, weights = bench.build_set(wl, 3, dev, layout)
+    names = [mt.name for mt in wl.matrices]
+    qs = [names.index(s) for s in SAMPLES]
+    w0 = {q: bits_np(logical(weights[q]).contiguous()) for q in qs}
+    g_host = {(q, s): bits_np(logical(slots[s][q]).contiguous()) for q in qs for s in range(3)}
+    runner = zf.SelectiveUpdateRunner(shapes, wl.ratio, hp, wl.refresh, wl.accum, slots, weights,
+                                      device=dev, layout=layout)
+    orcs = {q: O.MatrixOracle(O.widen(w0[q]), w0[q], wl.ratio, hp.lr, hp.beta1, hp.beta2,
+                              hp.eps, hp.weight_decay, wl.refresh, wl.accum) for q in qs}
+    for t in range(1, STEPS + 1):
+        kind = runner.step()
+        torch.cuda.synchronize()
+        slot = (t - 1) % 3
+        print(f"# step {t} ({'refresh' if kind.refresh else 'accumulate'})", file=sys.stderr,
+              flush=True)
+        if kind.refresh:
+            for q, (n, m) in enumerate(shapes):
+                s = f32_np(runner.norms[q]).astype(np.float64)
+                sel = runner.selection[q]
+                a = sel.sel_idx.cpu().numpy()
+                b = sel.unsel_idx.cpu().numpy()
+                assert a.size == ks[q] and b.size == m - ks[q]
+                assert np.array_equal(np.sort(np.concatenate([a, b])), np.arange(m))
+                assert s[a].min() >= s[b].max(), names[q]
+                frob = torch.sum(slots[slot][q].double() ** 2).item()
+                assert abs(s.sum() - frob) <= 1e-6 * frob, names[q]
+        for q in qs:
+            out = orcs[q].step(g_host[(q, slot)])
+            orc = orcs[q]
+            nm = names[q]
+            if kind.refresh:
+                ok, worst = rel_close(f32_np(runner.norms[q]), out["norms"], 1e-5)
+                assert ok, (nm, t, worst)
+                sel = runner.selection[q]
+                assert np.array_equal(sel.sel_idx.cpu().numpy(), orc.sel.sel), (nm, t)
+                assert np.array_equal(sel.unsel_idx.cpu().numpy(), orc.sel.unsel), (nm, t)
+                assert np.array_equal(mask_np(sel.mask), orc.sel.mask), (nm, t)
+                assert np.array_equal(sel.prefix.cpu().numpy(), orc.sel.prefix), (nm, t)
+            P, M, V = (f32_np(logical(x)) for x in runner.state[q])
+            assert same_bits(P, orc.P) and same_bits(M, orc.M) and same_bits(V, orc.V), (nm, t)
+            assert same_bits(f32_np(logical(runner.acc[q])), orc.A), (nm, t)
+            assert np.array_equal(bits_np(logical(weights[q]).contiguous()), orc.W), (nm, t)
+            if kind.interval_end:
+                assert same_bits(f32_np(logical(runner.unpacked[q])), out["unpacked"]), (nm, t)
+    runner.close()
