@@ -33,7 +33,7 @@ import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
-PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "update_kernel_llama2-7b-full_traffic.md")
+PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2505_12242_amd", "csrc", f)
                   for f in ("zf_device.hpp", "zf_internal.hpp", "zf_kernels.hip",
                             "zf_kernels_cm.hip")]
@@ -187,13 +187,14 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def recorded_traffic():
+def recorded_traffic(kernel: str, workload: str):
     """Bytes per launch of the fused update kernel measured with rocprofv3
-    PMC counters (scaled by a plain copy's counter reading), if recorded for
-    the current kernel source."""
-    if not os.path.exists(PROFILE_TRAFFIC):
+    PMC counters (scaled by a plain streaming kernel's counter reading), if
+    recorded for this workload and the current kernel source."""
+    path = os.path.join(PROFILES, f"{kernel}_{workload}_traffic.md")
+    if not os.path.exists(path):
         return None
-    text = open(PROFILE_TRAFFIC).read()
+    text = open(path).read()
     h = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
     v = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
     if not h or not v or h.group(1) != kernel_source_hash():
@@ -303,7 +304,8 @@ def main(argv=None) -> int:
             tot_ms = sum(per_kernel_ms[name])
             kernels[name]["GB/s"] = round(totals[name] / (tot_ms * 1e-3) / 1e9, 1)
 
-    traffic = recorded_traffic()
+    upd_kernel = "cm_update_kernel" if layout == zf.CHANNEL_MAJOR else "update_kernel"
+    traffic = recorded_traffic(upd_kernel, wl.name)
     result = {
         "metric": "GB/s and fraction of HBM peak per full step; params/s",
         "value": round(value, 2),
@@ -334,8 +336,7 @@ def main(argv=None) -> int:
         },
         "kernels": kernels,
         "roofline": {
-            "kernel": ("cm_update_kernel" if layout == zf.CHANNEL_MAJOR else "update_kernel")
-                      + " (fused Adam + bf16 write-back + pack)",
+            "kernel": upd_kernel + " (fused Adam + bf16 write-back + pack)",
             "bound": "hbm",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,
