@@ -43,7 +43,7 @@ def parse_args(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=16)
-    ap.add_argument("--warmup", type=int, default=4)
+    ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--workload", default="llama2-7b-full")
     ap.add_argument("--slots", type=int, default=3, help="gradient buffers in the ring")
     ap.add_argument("--layout", choices=["channel-major", "row-major"], default="channel-major",

@@ -280,6 +280,7 @@ void finish_geometry(DevMat& d, int cn_rows, int up_rows) {
   set_geometry(d, cn_rows, up_rows);
   if (d.layout == zf::kChannelMajor) {
     d.cm_nch = d.n > 0 ? static_cast<int32_t>(ceil_div(d.n, zf::kCmChunk)) : 0;
+    d.cm_unch = d.n > 0 ? static_cast<int32_t>(ceil_div(d.n, zf::kCmUnpackChunk)) : 0;
     d.vec = cm_vec_ok(d) ? 1 : 0;
   }
 }
@@ -291,6 +292,11 @@ int64_t colnorm_grid(const DevMat& d) {
 
 int64_t update_grid(const DevMat& d) {
   if (d.layout == zf::kChannelMajor) return d.m * d.cm_nch;
+  return update_blocks(d.n, d.m, d.up_rows);
+}
+
+int64_t unpack_grid(const DevMat& d) {
+  if (d.layout == zf::kChannelMajor) return d.m * d.cm_unch;
   return update_blocks(d.n, d.m, d.up_rows);
 }
 
@@ -490,7 +496,7 @@ zf_status zf_unpack(const float* acc, int64_t ld_acc, const zf_selection* sel, i
   d.ld_out = ld_out;
   finish_geometry(d, 256, pick_update_rows({{n, m}}));
   if (layout == zf::kRowMajor && !rm_strides_ok(d)) return ZF_EINVAL;
-  const int64_t blocks = update_grid(d);
+  const int64_t blocks = unpack_grid(d);
   if (blocks == 0) return ZF_OK;
   const hipError_t e =
       launch_unpack_any(single_table(), d, blocks, scale, layout, as_stream(stream));
@@ -514,8 +520,9 @@ struct zf_plan {
   int64_t* d_off_fin = nullptr;
   int64_t* d_off_top = nullptr;
   int64_t* d_off_up = nullptr;
+  int64_t* d_off_unp = nullptr;
   double* d_ws = nullptr;
-  int64_t blk_cn = 0, blk_fin = 0, blk_top = 0, blk_up = 0;
+  int64_t blk_cn = 0, blk_fin = 0, blk_top = 0, blk_up = 0, blk_unp = 0;
   bool can_colnorm = true, can_topk = true, can_adam = true, can_remap = true, can_pack = true,
        can_unpack = true;
 };
@@ -593,7 +600,7 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   const int cn_rows = pick_colnorm_rows(shapes);
   const int up_rows = pick_update_rows(shapes);
   std::vector<int64_t> off_cn(nmats + 1), off_fin(nmats + 1), off_top(nmats + 1),
-      off_up(nmats + 1);
+      off_up(nmats + 1), off_unp(nmats + 1);
   int64_t ws_doubles = 0;
   const bool cm = p->layout == zf::kChannelMajor;
   p->mats.resize(nmats);
@@ -610,24 +617,28 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
     off_fin[q] = p->blk_fin;
     off_top[q] = p->blk_top;
     off_up[q] = p->blk_up;
+    off_unp[q] = p->blk_unp;
     p->blk_cn += colnorm_grid(d);
     p->blk_fin += cm ? 0 : ceil_div(d.m, zf::kFinalizeCols);
     p->blk_top += 1;
     p->blk_up += update_grid(d);
+    p->blk_unp += unpack_grid(d);
     p->mats[q] = d;
   }
   off_cn[nmats] = p->blk_cn;
   off_fin[nmats] = p->blk_fin;
   off_top[nmats] = p->blk_top;
   off_up[nmats] = p->blk_up;
-  if (p->blk_cn >= (int64_t(1) << 31) / zf::kThreads || p->blk_up >= (int64_t(1) << 31) / zf::kThreads) {
+  off_unp[nmats] = p->blk_unp;
+  const int64_t max_blocks = (int64_t(1) << 31) / zf::kThreads;
+  if (p->blk_cn >= max_blocks || p->blk_up >= max_blocks || p->blk_unp >= max_blocks) {
     delete p;
     return ZF_EINVAL;  // grid too large for one launch
   }
 
   const size_t mats_bytes = sizeof(DevMat) * nmats;
   const size_t off_bytes = sizeof(int64_t) * (nmats + 1);
-  const size_t head = (mats_bytes + 4 * off_bytes + 255) & ~size_t(255);
+  const size_t head = (mats_bytes + 5 * off_bytes + 255) & ~size_t(255);
   p->dev_bytes = head + sizeof(double) * static_cast<size_t>(ws_doubles);
   hipError_t e = hipMalloc(&p->dev, p->dev_bytes);
   if (e != hipSuccess) {
@@ -641,6 +652,7 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   p->d_off_fin = p->d_off_cn + (nmats + 1);
   p->d_off_top = p->d_off_fin + (nmats + 1);
   p->d_off_up = p->d_off_top + (nmats + 1);
+  p->d_off_unp = p->d_off_up + (nmats + 1);
   p->d_ws = reinterpret_cast<double*>(base + head);
   std::vector<char> host(head, 0);
   std::memcpy(host.data(), p->mats.data(), mats_bytes);
@@ -648,6 +660,7 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   std::memcpy(host.data() + mats_bytes + off_bytes, off_fin.data(), off_bytes);
   std::memcpy(host.data() + mats_bytes + 2 * off_bytes, off_top.data(), off_bytes);
   std::memcpy(host.data() + mats_bytes + 3 * off_bytes, off_up.data(), off_bytes);
+  std::memcpy(host.data() + mats_bytes + 4 * off_bytes, off_unp.data(), off_bytes);
   e = hipMemcpy(p->dev, host.data(), head, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     g_last_hip_error = static_cast<int>(e);
@@ -715,9 +728,9 @@ zf_status zf_plan_update(zf_plan* p, const zf_adam_hparams* hp, int64_t step, in
 
 zf_status zf_plan_unpack(zf_plan* p, float scale, zf_stream stream) {
   if (p == nullptr || !p->can_unpack) return ZF_EINVAL;
-  const Table t{p->d_mats, p->d_off_up, p->nmats};
+  const Table t{p->d_mats, p->d_off_unp, p->nmats};
   const hipError_t e =
-      launch_unpack_any(t, p->mats[0], p->blk_up, scale, p->layout, as_stream(stream));
+      launch_unpack_any(t, p->mats[0], p->blk_unp, scale, p->layout, as_stream(stream));
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 

@@ -25,14 +25,32 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
                                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
 }
 
-// Descriptor of the matrix block b belongs to.  BATCHED kernels read it
-// from the plan's device table (scalar loads); single-matrix kernels take it
-// by value.  Keeping the two apart avoids a generic pointer that would turn
-// the descriptor loads into flat vector loads.
+// Workgroups are dispatched to the 8 XCDs of the chip round-robin by block
+// id.  Remapping the id so that XCD x handles one contiguous range of the
+// grid gives each XCD (and its L2) a contiguous address stream, which
+// measured 4-5% faster for the streaming passes.  A bijection on [0, B) for
+// any B (the first B mod 8 XCDs take one block more).
+#ifndef ZF_XCD_REMAP
+#define ZF_XCD_REMAP 1
+#endif
+constexpr int kXcds = 8;
+
+__device__ __forceinline__ int64_t xcd_remap(int64_t b, int64_t B) {
+  if constexpr (ZF_XCD_REMAP == 0) return b;
+  const int64_t q = B / kXcds, r = B % kXcds;
+  const int64_t x = b % kXcds, i = b / kXcds;
+  return x < r ? x * (q + 1) + i : r * (q + 1) + (x - r) * q + i;
+}
+
+// Descriptor of the matrix the (remapped) block belongs to.  BATCHED kernels
+// read it from the plan's device table (scalar loads); single-matrix kernels
+// take it by value.  Keeping the two apart avoids a generic pointer that
+// would turn the descriptor loads into flat vector loads.
 template <bool BATCHED>
 __device__ __forceinline__ DevMat get_mat(const DevMat* __restrict__ mats,
                                           const int64_t* __restrict__ off, int32_t nmats,
-                                          const DevMat& one, int64_t b, int64_t& local) {
+                                          const DevMat& one, int64_t, int64_t& local) {
+  const int64_t b = xcd_remap(blockIdx.x, gridDim.x);
   if constexpr (!BATCHED) {
     local = b;
     return one;

@@ -17,14 +17,20 @@ constexpr int kUpdateCols = 256;
 constexpr int kFinalizeCols = 256;
 constexpr int kTopkThreads = 1024;
 
-// Channel-major layout: an update / unpack block covers one channel and
-// kCmChunk of its rows (kCmVpt 16-byte groups per thread); a colnorm block
-// covers kThreads / 64 channels, one per wave.
+// Channel-major layout: an update block covers one channel and kCmChunk of
+// its rows (kCmVpt 16-byte groups per thread), an unpack block one channel
+// and kCmUnpackChunk rows; a colnorm block covers kThreads / 64 channels,
+// one per wave.
 #ifndef ZF_CM_VPT
 #define ZF_CM_VPT 2
 #endif
+#ifndef ZF_CM_UNPACK_VPT
+#define ZF_CM_UNPACK_VPT 1
+#endif
 constexpr int kCmVpt = ZF_CM_VPT;
 constexpr int kCmChunk = kThreads * 8 * kCmVpt;
+constexpr int kCmUnpackVpt = ZF_CM_UNPACK_VPT;
+constexpr int kCmUnpackChunk = kThreads * 8 * kCmUnpackVpt;
 constexpr int kCmColnormCols = kThreads / 64;
 
 enum StateMode : int32_t { kInplace = 0, kRemap = 1, kInit = 2 };
@@ -68,7 +74,8 @@ struct DevMat {
   int32_t up_cb;     // update column blocks
   int32_t vec;       // 16-byte vector path allowed (alignment, strides, sizes)
   int32_t layout;    // Layout
-  int32_t cm_nch;    // channel-major: row chunks per channel
+  int32_t cm_nch;    // channel-major: row chunks per channel (update)
+  int32_t cm_unch;   // channel-major: row chunks per channel (unpack)
 };
 
 // Per-kernel view of a batch: a device array of matrices and the first

@@ -333,9 +333,9 @@ __global__ __launch_bounds__(kThreads) void cm_unpack_kernel(const DevMat* __res
                                                             float scale) {
   int64_t local;
   const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, blockIdx.x, local);
-  const int64_t j = local / d.cm_nch;
-  const int64_t e0 = (local % d.cm_nch) * kCmChunk;
-  const int64_t len = min(static_cast<int64_t>(kCmChunk), d.n - e0);
+  const int64_t j = local / d.cm_unch;
+  const int64_t e0 = (local % d.cm_unch) * kCmUnpackChunk;
+  const int64_t len = min(static_cast<int64_t>(kCmUnpackChunk), d.n - e0);
   const int64_t w = j >> 6;
   const uint64_t mw = d.mask[w];
   const bool sel = (mw >> (j & 63)) & 1ull;
@@ -345,9 +345,10 @@ __global__ __launch_bounds__(kThreads) void cm_unpack_kernel(const DevMat* __res
     const float z[kGroup] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     if (d.vec) {
 #pragma unroll
-      for (int q = 0; q < kCmVpt; ++q) f32x8_store<kAuxWO>(rD, group_elem(q, tid) * 4, z);
+      for (int q = 0; q < kCmUnpackVpt; ++q) f32x8_store<kAuxWO>(rD, group_elem(q, tid) * 4, z);
     } else {
-      for (int64_t e = tid; e < len; e += kThreads) buf_put_f32<kAuxWO>(0.0f, rD, static_cast<uint32_t>(e) * 4, 0);
+      for (int64_t e = tid; e < len; e += kThreads)
+        buf_put_f32<kAuxWO>(0.0f, rD, static_cast<uint32_t>(e) * 4, 0);
     }
     return;
   }
@@ -355,11 +356,11 @@ __global__ __launch_bounds__(kThreads) void cm_unpack_kernel(const DevMat* __res
                          __popcll(mw & ((uint64_t(1) << (j & 63)) - 1)));
   const rsrc_t rA = make_rsrc(d.acc + u * d.ld_acc + e0, len * 4);
   if (d.vec) {
-    float a[kCmVpt][kGroup];
+    float a[kCmUnpackVpt][kGroup];
 #pragma unroll
-    for (int q = 0; q < kCmVpt; ++q) f32x8_load<kAuxRO>(rA, group_elem(q, tid) * 4, a[q]);
+    for (int q = 0; q < kCmUnpackVpt; ++q) f32x8_load<kAuxRO>(rA, group_elem(q, tid) * 4, a[q]);
 #pragma unroll
-    for (int q = 0; q < kCmVpt; ++q) {
+    for (int q = 0; q < kCmUnpackVpt; ++q) {
 #pragma unroll
       for (int i = 0; i < kGroup; ++i) a[q][i] = a[q][i] * scale;
       f32x8_store<kAuxWO>(rD, group_elem(q, tid) * 4, a[q]);
