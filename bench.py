@@ -50,6 +50,9 @@ def parse_args(argv=None):
                     help="storage of every matrix: channel-major (each input channel one "
                          "contiguous row, the paper's column-major gradient storage) or "
                          "PyTorch's row-major [out, in]")
+    ap.add_argument("--ratio", type=float, default=None, help="override the top-k ratio")
+    ap.add_argument("--refresh", type=int, default=None, help="override the refresh interval R")
+    ap.add_argument("--accum", type=int, default=None, help="override the accumulation interval S")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-steps", type=int, default=4)
     ap.add_argument("--calibration-copy-gib", type=float, default=1.0,
@@ -223,6 +226,10 @@ def main(argv=None) -> int:
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     wl = get_workload(args.workload)
+    over = {k: v for k, v in (("ratio", args.ratio), ("refresh", args.refresh),
+                              ("accum", args.accum)) if v is not None}
+    if over:
+        wl = wl.with_(**over)
     layout = zf.CHANNEL_MAJOR if args.layout == "channel-major" else zf.ROW_MAJOR
     hp = zf.AdamHparams(wl.hyper.lr, wl.hyper.beta1, wl.hyper.beta2, wl.hyper.eps,
                         wl.hyper.weight_decay)

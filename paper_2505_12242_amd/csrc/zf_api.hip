@@ -279,7 +279,21 @@ bool rm_strides_ok(const DevMat& d) {
 void finish_geometry(DevMat& d, int cn_rows, int up_rows) {
   set_geometry(d, cn_rows, up_rows);
   if (d.layout == zf::kChannelMajor) {
-    d.cm_nch = d.n > 0 ? static_cast<int32_t>(ceil_div(d.n, zf::kCmChunk)) : 0;
+    // groups per thread: the larger of 1..kCmVpt that fills at least as many
+    // lanes of the last chunk (fewer, fuller blocks)
+    int best = 1;
+    double best_fill = 0.0;
+    for (int v = 1; v <= zf::kCmVpt; ++v) {
+      const int64_t chunk = static_cast<int64_t>(v) * zf::kThreads * 8;
+      const int64_t nch = std::max<int64_t>(1, ceil_div(d.n, chunk));
+      const double fill = static_cast<double>(d.n) / static_cast<double>(nch * chunk);
+      if (fill >= best_fill - 1e-12) {
+        best = v;
+        best_fill = fill;
+      }
+    }
+    d.cm_vpt = best;
+    d.cm_nch = d.n > 0 ? static_cast<int32_t>(ceil_div(d.n, int64_t(best) * zf::kThreads * 8)) : 0;
     d.cm_unch = d.n > 0 ? static_cast<int32_t>(ceil_div(d.n, zf::kCmUnpackChunk)) : 0;
     d.vec = cm_vec_ok(d) ? 1 : 0;
   }

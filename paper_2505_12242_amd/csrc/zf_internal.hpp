@@ -17,10 +17,11 @@ constexpr int kUpdateCols = 256;
 constexpr int kFinalizeCols = 256;
 constexpr int kTopkThreads = 1024;
 
-// Channel-major layout: an update block covers one channel and kCmChunk of
-// its rows (kCmVpt 16-byte groups per thread), an unpack block one channel
-// and kCmUnpackChunk rows; a colnorm block covers kThreads / 64 channels,
-// one per wave.
+// Channel-major layout: an update block covers one channel and
+// cm_vpt * kThreads * 8 of its rows (cm_vpt 16-byte groups per thread, at
+// most kCmVpt, chosen per matrix to fill the lanes), an unpack block one
+// channel and kCmUnpackChunk rows; a colnorm block covers kThreads / 64
+// channels, one per wave.
 #ifndef ZF_CM_VPT
 #define ZF_CM_VPT 2
 #endif
@@ -76,6 +77,8 @@ struct DevMat {
   int32_t layout;    // Layout
   int32_t cm_nch;    // channel-major: row chunks per channel (update)
   int32_t cm_unch;   // channel-major: row chunks per channel (unpack)
+  int32_t cm_vpt;    // channel-major: 16-byte groups per thread in the update (1 or 2)
+  int32_t pad_;
 };
 
 // Per-kernel view of a batch: a device array of matrices and the first

@@ -10,7 +10,7 @@
 // the hot path is then a contiguous 16-byte-per-lane stream, and the bf16
 // write-back writes whole cache lines.
 //
-// Work unit of update / unpack: one channel x one chunk of kCmChunk rows.
+// Work unit of update / unpack: one channel x one chunk of its rows.
 // Whether the channel is selected, and its slot, are uniform per block, so
 // a block is either an Adam block or a pack block.  A block's buffer
 // resources cover exactly its chunk, so 16-byte groups past the end of a
@@ -157,17 +157,17 @@ enum CmSrc { kCmInplace = 0, kCmPrev, kCmInitW, kCmInitMaster };
 
 // Adam over one chunk of channel j (slot r), vector path.  SRC picks where
 // (p, m, v) come from; rS* are the source rows (the slot's own rows in place).
-template <int SRC>
+template <int SRC, int VPT>
 __device__ __forceinline__ void cm_adam_vec(rsrc_t rG, rsrc_t rP, rsrc_t rM, rsrc_t rV,
                                             rsrc_t rW, rsrc_t rSP, rsrc_t rSM, rsrc_t rSV,
                                             rsrc_t rI, const AdamK& c) {
   const int tid = threadIdx.x;
-  float g[kCmVpt][kGroup], p[kCmVpt][kGroup], m[kCmVpt][kGroup], v[kCmVpt][kGroup];
-  u32x4 gv[kCmVpt];
+  float g[VPT][kGroup], p[VPT][kGroup], m[VPT][kGroup], v[VPT][kGroup];
+  u32x4 gv[VPT];
 #pragma unroll
-  for (int q = 0; q < kCmVpt; ++q) gv[q] = buf_b128<kAuxRO>(rG, group_elem(q, tid) * 2, 0);
+  for (int q = 0; q < VPT; ++q) gv[q] = buf_b128<kAuxRO>(rG, group_elem(q, tid) * 2, 0);
 #pragma unroll
-  for (int q = 0; q < kCmVpt; ++q) {
+  for (int q = 0; q < VPT; ++q) {
     const uint32_t e = group_elem(q, tid);
     if constexpr (SRC == kCmInplace || SRC == kCmPrev) {
       f32x8_load<kAuxRMW>(rSP, e * 4, p[q]);
@@ -181,7 +181,7 @@ __device__ __forceinline__ void cm_adam_vec(rsrc_t rG, rsrc_t rP, rsrc_t rM, rsr
     }
   }
 #pragma unroll
-  for (int q = 0; q < kCmVpt; ++q) {
+  for (int q = 0; q < VPT; ++q) {
     widen8(gv[q], g[q]);
 #pragma unroll
     for (int i = 0; i < kGroup; ++i) adam_step(g[q][i], p[q][i], m[q][i], v[q][i], c);
@@ -218,19 +218,19 @@ __device__ __forceinline__ void cm_adam_elem(rsrc_t rG, rsrc_t rP, rsrc_t rM, rs
   }
 }
 
-template <bool FIRST>
+template <bool FIRST, int VPT>
 __device__ __forceinline__ void cm_pack_vec(rsrc_t rG, rsrc_t rA) {
   const int tid = threadIdx.x;
-  u32x4 gv[kCmVpt];
-  float a[kCmVpt][kGroup];
+  u32x4 gv[VPT];
+  float a[VPT][kGroup];
 #pragma unroll
-  for (int q = 0; q < kCmVpt; ++q) gv[q] = buf_b128<kAuxRO>(rG, group_elem(q, tid) * 2, 0);
+  for (int q = 0; q < VPT; ++q) gv[q] = buf_b128<kAuxRO>(rG, group_elem(q, tid) * 2, 0);
   if constexpr (!FIRST) {
 #pragma unroll
-    for (int q = 0; q < kCmVpt; ++q) f32x8_load<kAuxRMW>(rA, group_elem(q, tid) * 4, a[q]);
+    for (int q = 0; q < VPT; ++q) f32x8_load<kAuxRMW>(rA, group_elem(q, tid) * 4, a[q]);
   }
 #pragma unroll
-  for (int q = 0; q < kCmVpt; ++q) {
+  for (int q = 0; q < VPT; ++q) {
     float g[kGroup];
     widen8(gv[q], g);
 #pragma unroll
@@ -249,6 +249,20 @@ __device__ __forceinline__ void cm_pack_elem(rsrc_t rG, rsrc_t rA, int64_t len) 
   }
 }
 
+template <int SRC>
+__device__ __forceinline__ void cm_adam_vec_any(int vpt, rsrc_t rG, rsrc_t rP, rsrc_t rM,
+                                                rsrc_t rV, rsrc_t rW, rsrc_t rSP, rsrc_t rSM,
+                                                rsrc_t rSV, rsrc_t rI, const AdamK& c) {
+  if (vpt >= 2) cm_adam_vec<SRC, kCmVpt>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c);
+  else cm_adam_vec<SRC, 1>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c);
+}
+
+template <bool FIRST>
+__device__ __forceinline__ void cm_pack_vec_any(int vpt, rsrc_t rG, rsrc_t rA) {
+  if (vpt >= 2) cm_pack_vec<FIRST, kCmVpt>(rG, rA);
+  else cm_pack_vec<FIRST, 1>(rG, rA);
+}
+
 template <bool BATCHED, bool ADAM, bool PACK>
 __global__ __launch_bounds__(kThreads) void cm_update_kernel(const DevMat* __restrict__ mats,
                                                             const int64_t* __restrict__ off,
@@ -256,9 +270,10 @@ __global__ __launch_bounds__(kThreads) void cm_update_kernel(const DevMat* __res
                                                             int32_t mode, int32_t first) {
   int64_t local;
   const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, blockIdx.x, local);
+  const int64_t chunk = static_cast<int64_t>(d.cm_vpt) * kThreads * kGroup;
   const int64_t j = local / d.cm_nch;
-  const int64_t e0 = (local % d.cm_nch) * kCmChunk;
-  const int64_t len = min(static_cast<int64_t>(kCmChunk), d.n - e0);
+  const int64_t e0 = (local % d.cm_nch) * chunk;
+  const int64_t len = min(chunk, d.n - e0);
   const int64_t w = j >> 6;
   const uint64_t mw = d.mask[w];
   const bool sel = (mw >> (j & 63)) & 1ull;
@@ -271,8 +286,8 @@ __global__ __launch_bounds__(kThreads) void cm_update_kernel(const DevMat* __res
       const int64_t u = j - r;
       const rsrc_t rA = make_rsrc(d.acc + u * d.ld_acc + e0, len * 4);
       if (d.vec) {
-        if (first) cm_pack_vec<true>(rG, rA);
-        else cm_pack_vec<false>(rG, rA);
+        if (first) cm_pack_vec_any<true>(d.cm_vpt, rG, rA);
+        else cm_pack_vec_any<false>(d.cm_vpt, rG, rA);
       } else {
         if (first) cm_pack_elem<true>(rG, rA, len);
         else cm_pack_elem<false>(rG, rA, len);
@@ -305,10 +320,10 @@ __global__ __launch_bounds__(kThreads) void cm_update_kernel(const DevMat* __res
     if (src == kCmInitMaster) rI = make_rsrc(d.init_P + j * d.ld_init + e0, len * 4);
     if (d.vec) {
       switch (src) {
-        case kCmInplace: cm_adam_vec<kCmInplace>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c); break;
-        case kCmPrev: cm_adam_vec<kCmPrev>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c); break;
-        case kCmInitW: cm_adam_vec<kCmInitW>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c); break;
-        default: cm_adam_vec<kCmInitMaster>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c); break;
+        case kCmInplace: cm_adam_vec_any<kCmInplace>(d.cm_vpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c); break;
+        case kCmPrev: cm_adam_vec_any<kCmPrev>(d.cm_vpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c); break;
+        case kCmInitW: cm_adam_vec_any<kCmInitW>(d.cm_vpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c); break;
+        default: cm_adam_vec_any<kCmInitMaster>(d.cm_vpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c); break;
       }
     } else {
       switch (src) {
