@@ -289,13 +289,12 @@ def main(argv=None) -> int:
     for name, a, b in spans:
         per_kernel_ms.setdefault(name, []).append(a.elapsed_time(b))
     totals = {"colnorm": 0, "topk_select": 0, "update": 0, "unpack": 0}
-    update_bytes = 0
     for kind in kinds:
         b = step_bytes(shapes, ks, kind.refresh, kind.step_in_interval == 1, kind.interval_end)
         for key in totals:
             totals[key] += b[key]
     all_bytes = sum(totals.values())
-    update_bytes = totals["update"]
+    update_bytes = totals["update"]  # both update kinds
     upd_ms = per_kernel_ms.get("update", []) + per_kernel_ms.get("update_first", [])
     upd_launches = len(upd_ms)
     upd_avg_ms = sum(upd_ms) / max(upd_launches, 1)
@@ -304,8 +303,7 @@ def main(argv=None) -> int:
     value = all_bytes / wall / 1e9
     kernels = {}
     for name, lst in per_kernel_ms.items():
-        key = "update" if name.startswith("update") else name
-        kernels.setdefault(name, {"launches": len(lst), "avg_ms": round(sum(lst) / len(lst), 4)})
+        kernels[name] = {"launches": len(lst), "avg_ms": round(sum(lst) / len(lst), 4)}
     for name in ("colnorm", "topk_select", "unpack"):
         if name in per_kernel_ms and totals[name]:
             tot_ms = sum(per_kernel_ms[name])

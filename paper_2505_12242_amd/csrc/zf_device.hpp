@@ -49,7 +49,7 @@ __device__ __forceinline__ int64_t xcd_remap(int64_t b, int64_t B) {
 template <bool BATCHED>
 __device__ __forceinline__ DevMat get_mat(const DevMat* __restrict__ mats,
                                           const int64_t* __restrict__ off, int32_t nmats,
-                                          const DevMat& one, int64_t, int64_t& local) {
+                                          const DevMat& one, int64_t& local) {
   const int64_t b = xcd_remap(blockIdx.x, gridDim.x);
   if constexpr (!BATCHED) {
     local = b;

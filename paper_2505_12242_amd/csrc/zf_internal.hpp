@@ -29,7 +29,6 @@ constexpr int kTopkThreads = 1024;
 #define ZF_CM_UNPACK_VPT 1
 #endif
 constexpr int kCmVpt = ZF_CM_VPT;
-constexpr int kCmChunk = kThreads * 8 * kCmVpt;
 constexpr int kCmUnpackVpt = ZF_CM_UNPACK_VPT;
 constexpr int kCmUnpackChunk = kThreads * 8 * kCmUnpackVpt;
 constexpr int kCmColnormCols = kThreads / 64;

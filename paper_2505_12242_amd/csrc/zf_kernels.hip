@@ -36,7 +36,7 @@ template <bool BATCHED>
 __global__ __launch_bounds__(kThreads) void colnorm_partial_kernel(const DevMat* __restrict__ mats, const int64_t* __restrict__ off, int32_t nmats, DevMat one,
                                                                    double* __restrict__ ws) {
   int64_t local;
-  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, blockIdx.x, local);
+  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, local);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int64_t cblk = local % d.cn_cb;
@@ -99,7 +99,7 @@ template <bool BATCHED>
 __global__ __launch_bounds__(kFinalizeCols) void colnorm_finalize_kernel(
     const DevMat* __restrict__ mats, const int64_t* __restrict__ off, int32_t nmats, DevMat one, const double* __restrict__ ws) {
   int64_t local;
-  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, blockIdx.x, local);
+  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, local);
   const int64_t j = local * kFinalizeCols + threadIdx.x;
   if (j >= d.m) return;
   double s = 0.0;
@@ -152,7 +152,7 @@ __device__ __forceinline__ uint32_t block_excl_count(bool flag, uint32_t* sh_wav
 template <bool BATCHED>
 __global__ __launch_bounds__(kTopkThreads) void topk_kernel(const DevMat* __restrict__ mats, const int64_t* __restrict__ off, int32_t nmats, DevMat one) {
   int64_t local;
-  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, blockIdx.x, local);
+  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, local);
   const int64_t m = d.m;
   const int64_t k = d.k;
   if (m == 0) return;
@@ -411,7 +411,7 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const DevMat* __restri
                                                           int32_t nmats, DevMat one, AdamK c,
                                                           int32_t mode, int32_t first) {
   int64_t local;
-  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, blockIdx.x, local);
+  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, local);
   const int64_t cblk = local % d.up_cb;
   const int64_t rblk = local / d.up_cb;
   const int64_t c0 = cblk * kUpdateCols;
@@ -497,7 +497,7 @@ __global__ __launch_bounds__(kThreads) void unpack_kernel(const DevMat* __restri
                                                           int32_t nmats, DevMat one,
                                                           float scale) {
   int64_t local;
-  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, blockIdx.x, local);
+  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, local);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int64_t cblk = local % d.up_cb;

@@ -103,7 +103,7 @@ __global__ __launch_bounds__(kThreads) void cm_colnorm_kernel(const DevMat* __re
                                                              const int64_t* __restrict__ off,
                                                              int32_t nmats, DevMat one) {
   int64_t local;
-  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, blockIdx.x, local);
+  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, local);
   const int lane = threadIdx.x & 63;
   const int64_t j = local * (kThreads / 64) + (threadIdx.x >> 6);
   if (j >= d.m) return;
@@ -269,7 +269,7 @@ __global__ __launch_bounds__(kThreads) void cm_update_kernel(const DevMat* __res
                                                             int32_t nmats, DevMat one, AdamK c,
                                                             int32_t mode, int32_t first) {
   int64_t local;
-  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, blockIdx.x, local);
+  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, local);
   const int64_t chunk = static_cast<int64_t>(d.cm_vpt) * kThreads * kGroup;
   const int64_t j = local / d.cm_nch;
   const int64_t e0 = (local % d.cm_nch) * chunk;
@@ -347,7 +347,7 @@ __global__ __launch_bounds__(kThreads) void cm_unpack_kernel(const DevMat* __res
                                                             int32_t nmats, DevMat one,
                                                             float scale) {
   int64_t local;
-  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, blockIdx.x, local);
+  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, local);
   const int64_t j = local / d.cm_unch;
   const int64_t e0 = (local % d.cm_unch) * kCmUnpackChunk;
   const int64_t len = min(static_cast<int64_t>(kCmUnpackChunk), d.n - e0);

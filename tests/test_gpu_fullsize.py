@@ -1,8 +1,9 @@
-"""Parity at full size, in the launch configuration bench.py times: the whole
-Llama-2-7B-shaped gradient set (226 matrices, channel-major, batched plans,
-three-slot gradient ring) for 8 steps of the R = S = 4 schedule -- first
+"""Parity at full size, in the launch configuration bench.py times (channel-
+major, batched plans, three-slot gradient ring): the whole Llama-2-7B-shaped
+gradient set (226 matrices) for 8 steps of the R = S = 4 schedule -- first
 selection, accumulation, hand-over at step 4, refresh with state remap at
-step 5, hand-over at step 8.
+step 5, hand-over at step 8 -- and one R = S = 8 interval of the 70B share
+(heavy-tailed scales, GQA k/v weights, 28672-channel down projections).
 
 * Sampled matrices (embedding, LM head and four decoder weights of three
   shapes) are run through the oracle step by step and every output is
@@ -26,9 +27,14 @@ pytestmark = pytest.mark.gpu
 zf = pytest.importorskip("paper_2505_12242_amd")
 bench = pytest.importorskip("bench")
 
-SAMPLES = ["embed_tokens", "layers.0.q_proj", "layers.0.down_proj", "layers.17.gate_proj",
-           "layers.31.v_proj", "lm_head"]
-STEPS = 8
+CASES = {
+    # first selection, accumulation, hand-over at 4, refresh + remap at 5, hand-over at 8
+    "llama2-7b-full": (["embed_tokens", "layers.0.q_proj", "layers.0.down_proj",
+                        "layers.17.gate_proj", "layers.31.v_proj", "lm_head"], 8, 3),
+    # one R = S = 8 interval of the 70B share: heavy-tailed scales, GQA k/v
+    # (1024 rows), a 28672-channel down projection
+    "llama2-70b-10layers": (["layers.0.k_proj", "layers.3.o_proj", "layers.9.down_proj"], 8, 3),
+}
 
 
 def logical(t):
@@ -36,18 +42,21 @@ def logical(t):
 
 
 @pytest.mark.timeout(1200)
-def test_llama2_7b_full_set_sampled_parity():
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_full_set_sampled_parity(name):
     from workloads import get_workload
-    wl = get_workload("llama2-7b-full")
+    SAMPLES, STEPS, NSLOTS = CASES[name]
+    wl = get_workload(name)
     hp = zf.AdamHparams(wl.hyper.lr, wl.hyper.beta1, wl.hyper.beta2, wl.hyper.eps,
                         wl.hyper.weight_decay)
     dev = torch.device("cuda")
     layout = zf.CHANNEL_MAJOR
-    shapes, ks, slots, weights = bench.build_set(wl, 3, dev, layout)
+    shapes, ks, slots, weights = bench.build_set(wl, NSLOTS, dev, layout)
     names = [mt.name for mt in wl.matrices]
     qs = [names.index(s) for s in SAMPLES]
     w0 = {q: bits_np(logical(weights[q]).contiguous()) for q in qs}
-    g_host = {(q, s): bits_np(logical(slots[s][q]).contiguous()) for q in qs for s in range(3)}
+    g_host = {(q, s): bits_np(logical(slots[s][q]).contiguous()) for q in qs
+              for s in range(NSLOTS)}
     runner = zf.SelectiveUpdateRunner(shapes, wl.ratio, hp, wl.refresh, wl.accum, slots, weights,
                                       device=dev, layout=layout)
     orcs = {q: O.MatrixOracle(O.widen(w0[q]), w0[q], wl.ratio, hp.lr, hp.beta1, hp.beta2,
@@ -55,7 +64,7 @@ def test_llama2_7b_full_set_sampled_parity():
     for t in range(1, STEPS + 1):
         kind = runner.step()
         torch.cuda.synchronize()
-        slot = (t - 1) % 3
+        slot = (t - 1) % NSLOTS
         print(f"# step {t} ({'refresh' if kind.refresh else 'accumulate'})", file=sys.stderr,
               flush=True)
         if kind.refresh:
@@ -88,3 +97,5 @@ def test_llama2_7b_full_set_sampled_parity():
             if kind.interval_end:
                 assert same_bits(f32_np(logical(runner.unpacked[q])), out["unpacked"]), (nm, t)
     runner.close()
+    del runner, slots, weights
+    torch.cuda.empty_cache()

@@ -107,7 +107,7 @@ KINDS = ["lognormal", "wide", "ties", "few-distinct", "constant", "zeros", "sign
 
 
 @pytest.mark.parametrize("kind", KINDS)
-@pytest.mark.parametrize("m", [1, 5, 63, 64, 65, 1000, 4096, 11008, 28672])
+@pytest.mark.parametrize("m", [1, 5, 63, 64, 65, 1000, 4096, 11008, 28672, 70001])
 def test_topk(kind, m):
     s = score_vector(m, seed=derive_seed("tk", kind, m), kind=kind).numpy()
     S = f32_dev(s)

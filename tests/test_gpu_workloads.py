@@ -7,7 +7,7 @@ import pytest
 import torch
 
 import oracle as O
-from tests._gpu import bf16_dev, bits_np, f32_np, mask_np, rel_close, same_bits
+from tests._gpu import bits_np, f32_np, mask_np, rel_close, same_bits
 from workloads import derive_seed, get_workload, gradient, master_weights, step_scales
 
 pytestmark = pytest.mark.gpu
@@ -17,6 +17,7 @@ zf = pytest.importorskip("paper_2505_12242_amd")
 
 def T(a, layout):
     return a if layout == zf.ROW_MAJOR else np.ascontiguousarray(np.asarray(a).T)
+
 
 
 def run_workload(name, use_master, layout=0):
@@ -88,3 +89,46 @@ def test_linear_4096_fresh_selection_step(layout):
 @pytest.mark.parametrize("layout", LAYOUTS)
 def test_llama2_7b_layer_four_steps(layout):
     run_workload("llama2-7b-layer", use_master=False, layout=layout)
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_batched_shapes_with_unaligned_schedule(layout):
+    """Several shapes in one plan (odd sizes take the element-wise paths),
+    refresh every 3 steps and accumulation interval 2, so refreshes cut
+    intervals short; every output compared with the oracle at every step."""
+    shapes = [(264, 300), (97, 130), (1, 64), (4104, 65), (8, 1000)]
+    ratio, R, S, steps = 0.2, 3, 2, 8
+    hp = zf.AdamHparams(weight_decay=0.01)
+    dev = torch.device("cuda")
+    slots, weights, w0 = [], [], []
+    for t in range(1, steps + 1):
+        slot = []
+        for q, (n, m) in enumerate(shapes):
+            g = torch.Generator().manual_seed(q * 100 + t)
+            s = torch.exp(1.5 * torch.randn(m, generator=g, dtype=torch.float64))
+            s = torch.from_numpy(np.sort(s.numpy()) * np.exp(np.arange(m) * 3e-3))[torch.randperm(m, generator=g)]
+            gd = gradient(n, m, s, derive_seed("unaligned", q, t), device=dev)
+            slot.append(gd if layout == zf.ROW_MAJOR else gd.t().contiguous())
+        slots.append(slot)
+    for q, (n, m) in enumerate(shapes):
+        mw = master_weights(n, m, derive_seed("unaligned", q), device=dev).to(torch.bfloat16)
+        w0.append(bits_np(mw))
+        weights.append(mw if layout == zf.ROW_MAJOR else mw.t().contiguous())
+    runner = zf.SelectiveUpdateRunner(shapes, ratio, hp, R, S, slots, weights, layout=layout)
+    orcs = [O.MatrixOracle(O.widen(w0[q]), w0[q], ratio, hp.lr, hp.beta1, hp.beta2, hp.eps,
+                           hp.weight_decay, R, S) for q in range(len(shapes))]
+    for t in range(1, steps + 1):
+        kind = runner.step()
+        torch.cuda.synchronize()
+        for q, orc in enumerate(orcs):
+            out = orc.step(T(bits_np(slots[t - 1][q]), layout))
+            if kind.refresh:
+                assert np.array_equal(runner.selection[q].sel_idx.cpu().numpy(), orc.sel.sel), (q, t)
+            P, M, V = (T(f32_np(x), layout) for x in runner.state[q])
+            assert same_bits(P, orc.P) and same_bits(M, orc.M) and same_bits(V, orc.V), (q, t)
+            assert same_bits(T(f32_np(runner.acc[q]), layout), orc.A), (q, t)
+            assert np.array_equal(T(bits_np(weights[q]), layout), orc.W), (q, t)
+            if kind.interval_end:
+                assert same_bits(T(f32_np(runner.unpacked[q]), layout), out["unpacked"]), (q, t)
+    runner.close()
