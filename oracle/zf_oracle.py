@@ -27,6 +27,12 @@ rule):
                  Analysis, whose 1/S mean is unpack's scale).
 * schedule    -- which step refreshes the selection, starts or ends an
                  accumulation interval.
+* Zen-auto    -- the adaptive interval (Zero-stall Pipeline, "Hyperparameter
+                 Auto-tuning"): channel norms of the accumulated buffer and of
+                 the selected channels' gradient, their means over the whole
+                 gradient set, and a trigger that ends the interval early
+                 (column_sq_norms, zen_auto_stats, zen_auto_trigger,
+                 ZenAutoOracle).
 
 Precision.  The workloads fix fp32 master weights, moments and accumulation
 buffer, and the selective optimizer extends PyTorch's fp32 Adam
@@ -51,6 +57,8 @@ __all__ = [
     "widen", "bf16_round", "colnorm", "k_from_ratio", "select_topk",
     "slots_of", "remap", "adam_selected", "pack_accumulate", "unpack",
     "schedule", "MatrixOracle",
+    "column_sq_norms", "zen_auto_stats", "ZenAutoTotals", "zen_auto_trigger",
+    "ZenAutoOracle",
 ]
 
 
@@ -333,10 +341,22 @@ class MatrixOracle:
         self.A: Optional[np.ndarray] = None
 
     def step(self, G: np.ndarray) -> dict:
+        """One step of the fixed schedule (refresh every R steps, intervals
+        of S steps)."""
+        kind = schedule(self.t + 1, self.R, self.S)
+        out = self.advance(G, kind.refresh, kind.step_in_interval)
+        out["kind"] = kind
+        if kind.interval_end:
+            out["unpacked"] = self.hand_over(kind.step_in_interval)
+        return out
+
+    def advance(self, G: np.ndarray, refresh: bool, step_in_interval: int) -> dict:
+        """Everything of a step up to the hand-over: scores, selection and
+        state remap when `refresh`, then Adam on the selected columns and the
+        accumulation of the others (`step_in_interval` = 1 overwrites)."""
         self.t += 1
-        kind = schedule(self.t, self.R, self.S)
-        out = {"kind": kind}
-        if kind.refresh:
+        out = {}
+        if refresh:
             s = colnorm(G)
             new = select_topk(s, self.k)
             first = self.sel is None
@@ -344,12 +364,109 @@ class MatrixOracle:
                                            self.W, self.master if first else None)
             self.sel = new
             out["norms"] = s
+        elif self.sel is None:
+            raise ValueError("the first step must refresh the selection")
         c = AdamConsts.at_step(*self.hyper, self.t)
         self.P, self.M, self.V, wsel = adam_selected(G, self.sel.sel, self.P, self.M,
                                                      self.V, c)
         self.W[:, self.sel.sel.astype(np.int64)] = wsel
-        self.A = pack_accumulate(G, self.sel.unsel, self.A, kind.step_in_interval)
-        if kind.interval_end:
-            out["unpacked"] = unpack(self.A, self.sel,
-                                     float(np.float32(1.0 / kind.step_in_interval)))
+        self.A = pack_accumulate(G, self.sel.unsel, self.A, step_in_interval)
         return out
+
+    def hand_over(self, steps: int) -> np.ndarray:
+        """The dense hand-over buffer of an interval of `steps` steps, scaled
+        by the fp32 value of 1/steps (the mean of the Convergence Analysis)."""
+        return unpack(self.A, self.sel, float(np.float32(1.0 / steps)))
+
+
+# ---------------------------------------------------------------------------
+# Zen-auto: adaptive accumulation interval
+# ---------------------------------------------------------------------------
+
+def column_sq_norms(X: np.ndarray) -> np.ndarray:
+    """Squared norm of every column of an fp32 matrix: squares of fp32 values
+    are exact in fp64 (24-bit significands), the fp64 row-order sum is
+    rounded once to fp32 (the same definition as colnorm, for fp32 data)."""
+    X = np.asarray(X, dtype=np.float32)
+    acc = np.zeros(X.shape[1], dtype=np.float64)
+    for i in range(X.shape[0]):
+        x = X[i].astype(np.float64)
+        acc += x * x
+    return acc.astype(np.float32)
+
+
+def zen_auto_stats(G: np.ndarray, sel: Selection, A: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """Per-channel quantities Zen-auto tracks (Zero-stall Pipeline,
+    "Hyperparameter Auto-tuning"), taken after a step's accumulation:
+    sel_sq[r] = squared norm of this step's gradient column sel[r] (the
+    important part), acc_sq[u] = squared norm of the accumulated column in
+    packed slot u (the unimportant part).  Reading: the important part is
+    measured on the current step's gradient, which the selective optimizer
+    applies at once."""
+    g = widen(np.asarray(G)[:, np.asarray(sel.sel, dtype=np.int64)])
+    return column_sq_norms(g), column_sq_norms(A)
+
+
+@dataclass(frozen=True)
+class ZenAutoTotals:
+    sum_sel: float   # sum over every selected channel of its norm
+    k: int           # selected channels
+    sum_acc: float   # sum over every unselected channel of its accumulated norm
+    u: int           # unselected channels
+    trigger: bool
+
+
+def zen_auto_trigger(stats, tau: float) -> ZenAutoTotals:
+    """Zen-auto's decision over a whole gradient set (a list of
+    (sel_sq, acc_sq) per matrix).  The mean accumulated channel norm of the
+    unimportant part, sum_acc / u, is compared with the mean channel norm of
+    the important part, sum_sel / k.  Reading of "comparable": the hand-over
+    is triggered when sum_acc / u >= tau * sum_sel / k, evaluated without
+    division as sum_acc * k >= (tau * sum_sel) * u in fp64; norms are the fp64
+    square roots of the fp32 squared norms, summed in fp64 matrix by matrix
+    in slot order.  No trigger when either part is empty."""
+    sum_sel = 0.0
+    sum_acc = 0.0
+    k = u = 0
+    for sel_sq, acc_sq in stats:
+        for x in np.asarray(sel_sq, dtype=np.float32):
+            sum_sel += math.sqrt(float(x))
+        for x in np.asarray(acc_sq, dtype=np.float32):
+            sum_acc += math.sqrt(float(x))
+        k += len(sel_sq)
+        u += len(acc_sq)
+    trig = k > 0 and u > 0 and sum_acc * float(k) >= (float(tau) * sum_sel) * float(u)
+    return ZenAutoTotals(sum_sel, k, sum_acc, u, bool(trig))
+
+
+class ZenAutoOracle:
+    """Several matrices under Zen-auto's adaptive interval.  Reading of the
+    schedule: the selection is refreshed when (t-1) mod R = 0 as in the fixed
+    schedule; an interval starts at a refresh or after a hand-over, and ends
+    (hand-over with scale 1/length) when the trigger fires, when it reaches
+    S_max steps, or before a refresh.  Interval lengths count from the
+    interval's start, not from a global t mod S grid; so with tau = +inf this
+    is the fixed schedule with S = S_max whenever R is a multiple of S_max
+    (or R = 1)."""
+
+    def __init__(self, oracles, R: int, S_max: int, tau: float):
+        self.orcs = list(oracles)
+        self.R, self.S_max, self.tau = R, S_max, tau
+        self.t = 0
+        self.length = 0
+        self.ended = True
+
+    def step(self, grads) -> dict:
+        self.t += 1
+        refresh = _is_refresh(self.t, self.R)
+        self.length = 1 if (refresh or self.ended) else self.length + 1
+        outs = [o.advance(G, refresh, self.length) for o, G in zip(self.orcs, grads)]
+        stats = [zen_auto_stats(G, o.sel, o.A) for o, G in zip(self.orcs, grads)]
+        tot = zen_auto_trigger(stats, self.tau)
+        end = tot.trigger or self.length >= self.S_max or _is_refresh(self.t + 1, self.R)
+        self.ended = end
+        res = {"refresh": refresh, "step_in_interval": self.length, "interval_end": end,
+               "totals": tot, "stats": stats, "outs": outs}
+        if end:
+            res["unpacked"] = [o.hand_over(self.length) for o in self.orcs]
+        return res
