@@ -27,6 +27,14 @@ rule):
                  Analysis, whose 1/S mean is unpack's scale).
 * schedule    -- which step refreshes the selection, starts or ends an
                  accumulation interval.
+* swap_states / deferred_adam / OffloadOracle -- the offloaded optimizer:
+                 a full-state store backs the selective optimizer (states of
+                 columns leaving the selection are swapped out to it, those
+                 of entering columns swapped in, Zero-stall Pipeline
+                 "Swapping out/in"), and at every interval end the
+                 accumulated mean gradient updates the unselected columns
+                 from the store (Asynchronous Offloading Workflow; the
+                 delayed-coordinate rule of the Convergence Analysis).
 * Zen-auto    -- the adaptive interval (Zero-stall Pipeline, "Hyperparameter
                  Auto-tuning"): channel norms of the accumulated buffer and of
                  the selected channels' gradient, their means over the whole
@@ -59,6 +67,7 @@ __all__ = [
     "schedule", "MatrixOracle",
     "column_sq_norms", "zen_auto_stats", "ZenAutoTotals", "zen_auto_trigger",
     "ZenAutoOracle",
+    "swap_states", "deferred_adam", "OffloadOracle",
 ]
 
 
@@ -377,6 +386,135 @@ class MatrixOracle:
         """The dense hand-over buffer of an interval of `steps` steps, scaled
         by the fp32 value of 1/steps (the mean of the Convergence Analysis)."""
         return unpack(self.A, self.sel, float(np.float32(1.0 / steps)))
+
+
+# ---------------------------------------------------------------------------
+# Offloaded optimizer states: swap at a refresh, deferred host update
+# ---------------------------------------------------------------------------
+
+def swap_states(prev: Optional[Selection], new: Selection, P: Optional[np.ndarray],
+                M: Optional[np.ndarray], V: Optional[np.ndarray], store):
+    """Compact states for a new selection when a full-state store (the
+    offloaded optimizer's fp32 master, first and second moments of every
+    column, [n, m] each) backs the selective optimizer (Zero-stall Pipeline,
+    "Swapping out/in"):
+
+    * a column selected before and after keeps its compact (p, m, v), moved
+      to its new slot;
+    * a column that leaves the selection writes its compact (p, m, v) back to
+      its column of the store (swap-out);
+    * a column that enters reads (p, m, v) from its column of the store
+      (swap-in).
+
+    Leaving and entering columns are disjoint, so the order of the two
+    copies does not matter.  `prev` None means nothing was selected before.
+    Returns (P2, M2, V2, store2) with store2 a new (SP, SM, SV) tuple."""
+    SP, SM, SV = (np.array(x, dtype=np.float32, copy=True) for x in store)
+    n = SP.shape[0]
+    old_slot = slots_of(prev.sel, new.m) if prev is not None else np.full(new.m, -1)
+    new_slot = slots_of(new.sel, new.m)
+    if prev is not None:
+        for ro, j in enumerate(prev.sel.tolist()):
+            if new_slot[j] < 0:
+                SP[:, j] = P[:, ro]
+                SM[:, j] = M[:, ro]
+                SV[:, j] = V[:, ro]
+    k = new.k
+    P2 = np.zeros((n, k), dtype=np.float32)
+    M2 = np.zeros((n, k), dtype=np.float32)
+    V2 = np.zeros((n, k), dtype=np.float32)
+    for r, j in enumerate(new.sel.tolist()):
+        ro = int(old_slot[j])
+        if ro >= 0:
+            P2[:, r], M2[:, r], V2[:, r] = P[:, ro], M[:, ro], V[:, ro]
+        else:
+            P2[:, r], M2[:, r], V2[:, r] = SP[:, j], SM[:, j], SV[:, j]
+    return P2, M2, V2, (SP, SM, SV)
+
+
+def deferred_adam(A: np.ndarray, unsel: np.ndarray, scale: float, store, c: AdamConsts):
+    """The deferred update of the unselected columns (Asynchronous Offloading
+    Workflow: the accumulated unimportant gradients are applied by the
+    offloaded optimizer; Convergence Analysis: the delayed coordinates move
+    by the mean of the S accumulated gradients).  For every unselected
+    column j = unsel[u] and every row i:
+
+        g = A[i, u] * scale        (one fp32 multiply; scale = fp32(1/S)
+                                    gives the interval's mean gradient)
+
+    followed by the Adam/AdamW sequence of adam_selected on the store's
+    (p, m, v) of column j, with the constants `c` of the offloaded
+    optimizer's own step.  Returns (store2, W_unsel) with W_unsel the bf16
+    bits [n, m-k] of the new master of the unselected columns (slot order);
+    selected columns of the store are unchanged."""
+    SP, SM, SV = (np.array(x, dtype=np.float32, copy=True) for x in store)
+    cols = np.asarray(unsel, dtype=np.int64)
+    g = np.asarray(A, dtype=np.float32) * np.float32(scale)
+    p0, m0, v0 = SP[:, cols], SM[:, cols], SV[:, cols]
+    m1 = c.B1 * m0 + c.C1 * g
+    v1 = c.B2 * v0 + c.C2 * (g * g)
+    d = np.sqrt(v1 * c.IB2) + c.EPS
+    u = (m1 * c.IB1) / d
+    p = p0 - c.WD * p0 if c.WD != 0 else p0
+    p1 = (p - c.LR * u).astype(np.float32)
+    SP[:, cols], SM[:, cols], SV[:, cols] = p1, m1.astype(np.float32), v1.astype(np.float32)
+    return (SP, SM, SV), bf16_round(p1)
+
+
+class OffloadOracle:
+    """One matrix under the whole method with offloaded optimizer states.
+    The store holds every column's (p, m, v) -- initially the fp32 master
+    and zero moments.  A refresh scores, selects and swaps states against
+    the store (swap_states); every step updates the selected columns (the
+    selective optimizer, global step t) and accumulates the others; every
+    interval end applies the deferred update (deferred_adam with scale
+    fp32(1/length), constants of the offloaded optimizer's own step counter
+    th = 1, 2, ... -- one step per hand-over, reading) and writes the new
+    bf16 weights of the unselected columns into W.  The hand-over is applied
+    before the next step: an implementation that overlaps it with later
+    steps must give the same result, which holds when it lands before the
+    next refresh (only a refresh reads the store; only the unselected
+    columns of W change)."""
+
+    def __init__(self, master: np.ndarray, W: np.ndarray, ratio: float, lr: float,
+                 beta1: float, beta2: float, eps: float, weight_decay: float, R: int, S: int):
+        master = np.asarray(master, dtype=np.float32)
+        self.W = np.array(W, dtype=np.uint16, copy=True)
+        self.n, self.m = self.W.shape
+        self.k = k_from_ratio(ratio, self.m)
+        self.hyper = (lr, beta1, beta2, eps, weight_decay)
+        self.R, self.S = R, S
+        self.t = 0
+        self.th = 0
+        self.sel: Optional[Selection] = None
+        self.P = self.M = self.V = None
+        self.A: Optional[np.ndarray] = None
+        z = np.zeros_like(master)
+        self.store = (master.copy(), z, z.copy())
+
+    def step(self, G: np.ndarray) -> dict:
+        kind = schedule(self.t + 1, self.R, self.S)
+        self.t += 1
+        out = {"kind": kind}
+        if kind.refresh:
+            s = colnorm(G)
+            new = select_topk(s, self.k)
+            self.P, self.M, self.V, self.store = swap_states(self.sel, new, self.P, self.M,
+                                                             self.V, self.store)
+            self.sel = new
+            out["norms"] = s
+        c = AdamConsts.at_step(*self.hyper, self.t)
+        self.P, self.M, self.V, wsel = adam_selected(G, self.sel.sel, self.P, self.M, self.V, c)
+        self.W[:, self.sel.sel.astype(np.int64)] = wsel
+        self.A = pack_accumulate(G, self.sel.unsel, self.A, kind.step_in_interval)
+        if kind.interval_end:
+            self.th += 1
+            ch = AdamConsts.at_step(*self.hyper, self.th)
+            scale = float(np.float32(1.0 / kind.step_in_interval))
+            self.store, wun = deferred_adam(self.A, self.sel.unsel, scale, self.store, ch)
+            self.W[:, self.sel.unsel.astype(np.int64)] = wun
+            out["weight_cols"] = wun
+        return out
 
 
 # ---------------------------------------------------------------------------
