@@ -53,6 +53,9 @@ def parse_args(argv=None):
     ap.add_argument("--ratio", type=float, default=None, help="override the top-k ratio")
     ap.add_argument("--refresh", type=int, default=None, help="override the refresh interval R")
     ap.add_argument("--accum", type=int, default=None, help="override the accumulation interval S")
+    ap.add_argument("--zen-tau", type=float, default=None,
+                    help="run Zen-auto (adaptive interval, at most --accum steps) with this "
+                         "threshold instead of the fixed schedule (channel-major only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-steps", type=int, default=4)
     ap.add_argument("--calibration-copy-gib", type=float, default=1.0,
@@ -244,7 +247,7 @@ def main(argv=None) -> int:
             w = weights[q] if layout == zf.ROW_MAJOR else weights[q].t()
             weights0[q] = w.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
     runner = zf.SelectiveUpdateRunner(shapes, wl.ratio, hp, wl.refresh, wl.accum, grad_slots,
-                                      weights, device=dev, layout=layout)
+                                      weights, device=dev, layout=layout, zen_tau=args.zen_tau)
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t0
     print(f"# setup {setup_s:.1f}s: {len(shapes)} matrices, {wl.params:,} params, "
@@ -295,7 +298,8 @@ def main(argv=None) -> int:
             totals[key] += b[key]
     all_bytes = sum(totals.values())
     update_bytes = totals["update"]  # both update kinds
-    upd_ms = per_kernel_ms.get("update", []) + per_kernel_ms.get("update_first", [])
+    upd_ms = [ms for name, lst in per_kernel_ms.items() if name.startswith("update")
+              for ms in lst]
     upd_launches = len(upd_ms)
     upd_avg_ms = sum(upd_ms) / max(upd_launches, 1)
     achieved = update_bytes / upd_launches / (upd_avg_ms * 1e-3) / 1e9 if upd_launches else 0.0
@@ -310,6 +314,8 @@ def main(argv=None) -> int:
             kernels[name]["GB/s"] = round(totals[name] / (tot_ms * 1e-3) / 1e9, 1)
 
     upd_kernel = "cm_update_kernel" if layout == zf.CHANNEL_MAJOR else "update_kernel"
+    if args.zen_tau is not None:
+        upd_kernel += " (with Zen-auto statistics)"
     traffic = recorded_traffic(upd_kernel, wl.name)
     result = {
         "metric": "GB/s and fraction of HBM peak per full step; params/s",
@@ -336,6 +342,8 @@ def main(argv=None) -> int:
             "topk_ratio": wl.ratio,
             "refresh_interval": wl.refresh,
             "accum_interval": wl.accum,
+            "zen_auto_tau": args.zen_tau,
+            "interval_ends": sum(1 for k in kinds if k.interval_end),
             "grad_slots": args.slots,
             "algorithmic_GB_per_step": round(all_bytes / args.steps / 1e9, 3),
         },

@@ -27,7 +27,9 @@
  *                       over G.
  *
  * plus a batched "plan" that runs each of these over many matrices in one
- * launch per kernel.
+ * launch per kernel, and, on a plan, the statistics of Zen-auto (the
+ * adaptive accumulation interval) fused into the update pass
+ * (zf_plan_update_zen).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -141,7 +143,19 @@ typedef enum zf_state_mode {
  * matrix (same m); the prev_* states are compact states of that selection
  * (as many slots as it has columns) with row stride ld_prev, in the call's
  * layout; init_master is a full fp32 n x m master in the call's layout with
- * row stride ld_init. */
+ * row stride ld_init.
+ *
+ * Full-state store (the offloaded optimizer's states of every column; paper,
+ * Zero-stall Pipeline, "Swapping out/in": the selective optimizer's states
+ * are swapped out to the host and back in).  store_* are full fp32 n x m
+ * master / first / second moment arrays in the call's layout with row
+ * stride ld_store, in device memory or in pinned host memory that the
+ * kernels access in place.  When store_master is not NULL it replaces the
+ * init source: in ZF_STATES_INIT and ZF_STATES_REMAP a newly selected column
+ * reads (p, m, v) from its column of the store (swap-in), and in
+ * ZF_STATES_REMAP a column that was selected before but no longer is writes
+ * its previous compact (p, m, v) to its column of the store (swap-out).  The
+ * store must not overlap any other buffer of the call. */
 typedef struct zf_state_source {
   const uint64_t* prev_mask;
   const int32_t* prev_prefix;
@@ -151,6 +165,10 @@ typedef struct zf_state_source {
   int64_t ld_prev;
   const float* init_master;
   int64_t ld_init;
+  float* store_master;
+  float* store_exp_avg;
+  float* store_exp_avg_sq;
+  int64_t ld_store;
 } zf_state_source;
 
 /* Text for a status code (static storage). */
@@ -248,6 +266,49 @@ zf_status zf_unpack(const float* acc, int64_t ld_acc, const zf_selection* sel, i
                     int64_t n, int64_t m, int32_t layout, float scale, float* out,
                     int64_t ld_out, zf_stream stream);
 
+/* ---- deferred update of the unselected columns (offloaded optimizer) ---- */
+
+/* HOST function (host pointers only; no device work): one Adam/AdamW step
+ * of every unselected column with the accumulation interval's mean gradient,
+ * on the offloaded optimizer's states (paper, Asynchronous Offloading
+ * Workflow: the accumulated unimportant gradients are applied by the CPU
+ * optimizer; Convergence Analysis: the delayed coordinates move by the mean
+ * of the S accumulated gradients; Implementation, "Concurrent CPU-side
+ * Optimizer").  For every unselected slot u (column j = unsel_idx[u]) and
+ * row i:
+ *   g = acc[i][u] * scale;  (p, m, v) = state column j;  the element
+ *   sequence of zf_adam_selected with the constants of step `step`;
+ *   state column j = (p', m', v');  weight_cols[i][u] = bf16_rne(p').
+ * acc: packed sums [n][ld_acc >= m-k] (channel-major: [m-k][ld_acc >= n]),
+ *   e.g. a host copy of the device buffer zf_pack_accumulate fills;
+ * unsel_idx: [m-k] strictly ascending column indices in [0, m);
+ * master / exp_avg / exp_avg_sq: full n x m fp32 states with row stride
+ *   ld_state in `layout`, updated in place at the unselected columns only;
+ * weight_cols: bf16 output [n][ld_wcols >= m-k] (channel-major [m-k][..]);
+ * scale: fp32 factor of the sums (1/S for the mean), finite;
+ * step: the offloaded optimizer's own 1-based step counter;
+ * nthreads: worker threads (0 = all hardware threads); the call returns
+ *   when every thread has finished.
+ * ZF_EINVAL (nothing written) for invalid sizes, strides, hyperparameters,
+ * indices that are not strictly ascending in [0, m), or overlapping
+ * buffers.  Results are bit-identical to the device's element sequence. */
+zf_status zf_host_adam_unselected(const float* acc, int64_t ld_acc, const int32_t* unsel_idx,
+                                  int64_t n, int64_t m, int64_t k, int32_t layout, float scale,
+                                  float* master, float* exp_avg, float* exp_avg_sq,
+                                  int64_t ld_state, uint16_t* weight_cols, int64_t ld_wcols,
+                                  const zf_adam_hparams* hp, int64_t step, int32_t nthreads);
+
+/* Write-back of the deferred update: W[i][unsel_idx[u]] = weight_cols[i][u]
+ * for every unselected slot u and row i; selected columns of W are not
+ * touched.  weight_cols: bf16 [n][ld_wcols >= m-k] (channel-major
+ * [m-k][ld_wcols >= n]) in device memory or pinned host memory (read in
+ * place); weight: bf16 n x m in `layout`.  sel: HOST struct; sel_mask and
+ * sel_prefix are read (the selection the columns were updated under). */
+zf_status zf_scatter_weights(const uint16_t* weight_cols, int64_t ld_wcols,
+                             const zf_selection* sel, int64_t k, int64_t n, int64_t m,
+                             int32_t layout, uint16_t* weight, int64_t ld_weight,
+                             zf_stream stream);
+
 /* ---- batched plans ------------------------------------------------------ */
 
 /* HOST struct describing one matrix of a batch.  Pointers as in the single
@@ -272,6 +333,10 @@ typedef struct zf_matrix {
   float* unpacked;
   int64_t ld_unpacked;
   zf_state_source src;
+  float* sel_sq; /* Zen-auto only: [k] fp32, channel-major plans (else NULL)   */
+  float* acc_sq; /* Zen-auto only: [m - k] fp32, channel-major plans (else NULL) */
+  const uint16_t* weight_cols; /* deferred update only: bf16 [n][m-k] / cm [m-k][n] */
+  int64_t ld_weight_cols;
 } zf_matrix;
 
 typedef struct zf_plan zf_plan;
@@ -303,6 +368,51 @@ zf_status zf_plan_update(zf_plan* plan, const zf_adam_hparams* hp, int64_t step,
 
 /* zf_unpack over every matrix into its `unpacked` buffer. */
 zf_status zf_plan_unpack(zf_plan* plan, float scale, zf_stream stream);
+
+/* zf_scatter_weights over every matrix (weight_cols of each descriptor). */
+zf_status zf_plan_scatter_weights(zf_plan* plan, zf_stream stream);
+
+/* ---- Zen-auto: adaptive accumulation interval ---------------------------- */
+
+/* Totals of one Zen-auto step over a whole plan, as written to DEVICE memory
+ * by zf_plan_update_zen (40 bytes, 8-byte aligned). */
+typedef struct zf_zen_totals {
+  double sum_sel;  /* sum over every selected channel of sqrt(sel_sq)    */
+  double sum_acc;  /* sum over every unselected channel of sqrt(acc_sq)  */
+  int64_t k_total; /* selected channels of the plan                      */
+  int64_t u_total; /* unselected channels of the plan                    */
+  int32_t trigger; /* 1: hand the accumulated buffers over after this step */
+  int32_t pad;
+} zf_zen_totals;
+
+/* The fused update (zf_plan_update with do_adam = do_pack = 1, same
+ * arguments and results) that also measures what Zen-auto compares (paper,
+ * Zero-stall Pipeline, "Hyperparameter Auto-tuning": the unimportant part's
+ * average accumulated channel norm against the important part's average
+ * channel norm; the deferred update is triggered once they are comparable):
+ *   sel_sq[r] = sum_i g_ij^2 for the selected channel j = sel_idx[r], g this
+ *               step's gradient (the important part, applied at once);
+ *   acc_sq[u] = sum_i A_iu^2 over the accumulated column of slot u after
+ *               this step's accumulation (the unimportant part);
+ * each summed in fp64 (exact squares) in a fixed order and rounded once to
+ * fp32.  Then, over every matrix of the plan, in fp64:
+ *   sum_sel = sum of sqrt(sel_sq), sum_acc = sum of sqrt(acc_sq),
+ *   trigger = k_total > 0 && u_total > 0 &&
+ *             sum_acc * k_total >= (tau * sum_sel) * u_total,
+ * i.e. the pooled mean accumulated norm reaches tau times the pooled mean
+ * selected norm (reading of "comparable": tau = 1).  The result goes to
+ * *totals (DEVICE).  The caller ends the interval (zf_plan_unpack with scale
+ * 1/step_in_interval) when trigger is set; the next step then starts a new
+ * interval (step_in_interval = 1).
+ * Requirements: a channel-major plan whose every descriptor provides
+ * sel_sq [k] and acc_sq [m - k] (device fp32, disjoint from each other and
+ * from the update's buffers), tau >= 0 (+inf allowed, never triggers when
+ * sum_sel > 0), totals 8-byte aligned; else ZF_EINVAL with nothing
+ * enqueued.  The plan's Zen-auto workspace is shared: do not run two
+ * zf_plan_update_zen calls of one plan concurrently. */
+zf_status zf_plan_update_zen(zf_plan* plan, const zf_adam_hparams* hp, int64_t step,
+                             int32_t mode, int64_t step_in_interval, int64_t accum_interval,
+                             double tau, zf_zen_totals* totals, zf_stream stream);
 
 #ifdef __cplusplus
 }

@@ -20,12 +20,16 @@ from ._lib import (  # noqa: F401
     Plan,
     Selection,
     StateSource,
+    ZEN_TOTALS_BYTES,
+    ZenTotals,
     ZfError,
     adam_selected,
     colnorm,
     colnorm_workspace_bytes,
+    host_adam_unselected,
     k_from_ratio,
     pack_accumulate,
+    scatter_weights,
     topk_select,
     unpack,
     update_fused,

@@ -41,7 +41,9 @@ class ZfSelection(ctypes.Structure):
 class ZfStateSource(ctypes.Structure):
     _fields_ = [("prev_mask", c_vp), ("prev_prefix", c_vp), ("prev_master", c_vp),
                 ("prev_exp_avg", c_vp), ("prev_exp_avg_sq", c_vp), ("ld_prev", c_i64),
-                ("init_master", c_vp), ("ld_init", c_i64)]
+                ("init_master", c_vp), ("ld_init", c_i64),
+                ("store_master", c_vp), ("store_exp_avg", c_vp), ("store_exp_avg_sq", c_vp),
+                ("ld_store", c_i64)]
 
 
 class ZfMatrix(ctypes.Structure):
@@ -53,7 +55,14 @@ class ZfMatrix(ctypes.Structure):
                 ("norms_sq", c_vp),
                 ("sel", ZfSelection),
                 ("unpacked", c_vp), ("ld_unpacked", c_i64),
-                ("src", ZfStateSource)]
+                ("src", ZfStateSource),
+                ("sel_sq", c_vp), ("acc_sq", c_vp),
+                ("weight_cols", c_vp), ("ld_weight_cols", c_i64)]
+
+
+class ZfZenTotals(ctypes.Structure):
+    _fields_ = [("sum_sel", c_dbl), ("sum_acc", c_dbl), ("k_total", c_i64), ("u_total", c_i64),
+                ("trigger", c_i32), ("pad", c_i32)]
 
 
 # (name, restype, argtypes) of every exported entry point of include/zf.h.
@@ -87,6 +96,14 @@ SIGNATURES = [
     ("zf_plan_update", ctypes.c_int,
      [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, c_i32, c_i64, c_i64, c_i32, c_i32, c_vp]),
     ("zf_plan_unpack", ctypes.c_int, [c_vp, c_flt, c_vp]),
+    ("zf_host_adam_unselected", ctypes.c_int,
+     [c_vp, c_i64, c_vp, c_i64, c_i64, c_i64, c_i32, c_flt, c_vp, c_vp, c_vp, c_i64, c_vp, c_i64,
+      ctypes.POINTER(ZfAdamHparams), c_i64, c_i32]),
+    ("zf_scatter_weights", ctypes.c_int,
+     [c_vp, c_i64, ctypes.POINTER(ZfSelection), c_i64, c_i64, c_i64, c_i32, c_vp, c_i64, c_vp]),
+    ("zf_plan_scatter_weights", ctypes.c_int, [c_vp, c_vp]),
+    ("zf_plan_update_zen", ctypes.c_int,
+     [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, c_i32, c_i64, c_i64, c_dbl, c_vp, c_vp]),
 ]
 
 
@@ -134,8 +151,10 @@ def _stream(stream) -> Optional[int]:
 
 
 def _mat(t: torch.Tensor, dtype, name: str, rows: Optional[int] = None,
-         cols: Optional[int] = None) -> int:
-    """Checks a row-major 2-D device tensor and returns its row stride."""
+         cols: Optional[int] = None, device_ok: bool = False, host: bool = False) -> int:
+    """Checks a row-major 2-D tensor and returns its row stride.  The tensor
+    must live on a GPU; device_ok also accepts pinned host memory (which the
+    kernels access in place); host requires a CPU tensor."""
     if t.dtype != dtype:
         raise TypeError(f"{name}: expected {dtype}, got {t.dtype}")
     if t.dim() != 2:
@@ -144,8 +163,13 @@ def _mat(t: torch.Tensor, dtype, name: str, rows: Optional[int] = None,
         raise ValueError(f"{name}: expected {rows} rows, got {t.shape[0]}")
     if cols is not None and t.shape[1] != cols:
         raise ValueError(f"{name}: expected {cols} columns, got {t.shape[1]}")
-    if t.numel() and not t.is_cuda:
-        raise ValueError(f"{name}: must live on a GPU")
+    if t.numel():
+        if host:
+            if t.is_cuda:
+                raise ValueError(f"{name}: must be a host (CPU) tensor")
+        elif not (t.is_cuda or (device_ok and t.is_pinned())):
+            raise ValueError(f"{name}: must live on a GPU" +
+                             (" or in pinned host memory" if device_ok else ""))
     if t.shape[0] > 1 and t.shape[1] > 1 and t.stride(1) != 1:
         raise ValueError(f"{name}: rows must be contiguous (stride(1) == 1)")
     return t.stride(0) if t.shape[0] > 1 else t.shape[1]
@@ -163,9 +187,9 @@ def _stored(layout: int, rows_l: int, cols_l: int):
     return (rows_l, cols_l) if layout == ROW_MAJOR else (cols_l, rows_l)
 
 
-def _lmat(t, dtype, name, layout, rows_l=None, cols_l=None) -> int:
+def _lmat(t, dtype, name, layout, rows_l=None, cols_l=None, **kw) -> int:
     r, c = (rows_l, cols_l) if layout == ROW_MAJOR else (cols_l, rows_l)
-    return _mat(t, dtype, name, r, c)
+    return _mat(t, dtype, name, r, c, **kw)
 
 
 def _vec(t: torch.Tensor, dtype, name: str, size: int) -> None:
@@ -257,6 +281,10 @@ class StateSource:
     prev_exp_avg: Optional[torch.Tensor] = None
     prev_exp_avg_sq: Optional[torch.Tensor] = None
     init_master: Optional[torch.Tensor] = None
+    # full-state store (swap-in / swap-out); device or pinned host tensors
+    store_master: Optional[torch.Tensor] = None
+    store_exp_avg: Optional[torch.Tensor] = None
+    store_exp_avg_sq: Optional[torch.Tensor] = None
 
     def as_c(self) -> ZfStateSource:
         ld_prev = 0
@@ -268,11 +296,20 @@ class StateSource:
         ld_init = 0
         if self.init_master is not None:
             ld_init = _mat(self.init_master, torch.float32, "init_master")
+        ld_store = 0
+        if self.store_master is not None:
+            ld_store = _mat(self.store_master, torch.float32, "store_master", device_ok=True)
+            if (_mat(self.store_exp_avg, torch.float32, "store_exp_avg", device_ok=True) != ld_store
+                    or _mat(self.store_exp_avg_sq, torch.float32, "store_exp_avg_sq",
+                            device_ok=True) != ld_store):
+                raise ValueError("the store's three arrays must share one row stride")
         return ZfStateSource(
             _ptr(self.prev.mask) if self.prev else None,
             _ptr(self.prev.prefix) if self.prev else None,
             _ptr(self.prev_master), _ptr(self.prev_exp_avg), _ptr(self.prev_exp_avg_sq), ld_prev,
-            _ptr(self.init_master), ld_init)
+            _ptr(self.init_master), ld_init,
+            _ptr(self.store_master), _ptr(self.store_exp_avg), _ptr(self.store_exp_avg_sq),
+            ld_store)
 
 
 def _states(n, k, master, exp_avg, exp_avg_sq, layout):
@@ -341,6 +378,49 @@ def unpack(acc, sel: Selection, scale: float = 1.0, out: Optional[torch.Tensor] 
     return out
 
 
+def host_adam_unselected(acc: torch.Tensor, unsel_idx: torch.Tensor, n: int, m: int, k: int,
+                         scale: float, master: torch.Tensor, exp_avg: torch.Tensor,
+                         exp_avg_sq: torch.Tensor, weight_cols: torch.Tensor, hp: AdamHparams,
+                         step: int, layout: int = ROW_MAJOR, nthreads: int = 0) -> None:
+    """The deferred host update (zf_host_adam_unselected): every argument is
+    a host (CPU) tensor; runs on `nthreads` host threads (0 = all)."""
+    u = m - k
+    lda = _lmat(acc, torch.float32, "acc", layout, n, u, host=True) if n * u else max(u, n, 1)
+    if unsel_idx.is_cuda or unsel_idx.dtype != torch.int32 or unsel_idx.numel() != u \
+            or not unsel_idx.is_contiguous():
+        raise ValueError(f"unsel_idx: expected a contiguous [{u}] int32 host tensor")
+    for t, name in ((acc, "acc"), (master, "master"), (exp_avg, "exp_avg"),
+                    (exp_avg_sq, "exp_avg_sq"), (weight_cols, "weight_cols")):
+        if t.is_cuda:
+            raise ValueError(f"{name}: must be a host (CPU) tensor")
+    lds = _lmat(master, torch.float32, "master", layout, n, m, host=True)
+    if (_lmat(exp_avg, torch.float32, "exp_avg", layout, n, m, host=True) != lds
+            or _lmat(exp_avg_sq, torch.float32, "exp_avg_sq", layout, n, m, host=True) != lds):
+        raise ValueError("master, exp_avg and exp_avg_sq must share one row stride")
+    ldw = (_lmat(weight_cols, torch.bfloat16, "weight_cols", layout, n, u, host=True)
+           if n * u else max(u, n, 1))
+    c_hp = hp.as_c()
+    _check("zf_host_adam_unselected", LIB.zf_host_adam_unselected(
+        _ptr(acc), lda, _ptr(unsel_idx), n, m, k, layout, float(scale), _ptr(master),
+        _ptr(exp_avg), _ptr(exp_avg_sq), lds, _ptr(weight_cols), ldw, ctypes.byref(c_hp),
+        int(step), int(nthreads)))
+
+
+def scatter_weights(weight_cols: torch.Tensor, sel: Selection, weight: torch.Tensor,
+                    layout: int = ROW_MAJOR, stream=None) -> None:
+    """W[:, unsel] = weight_cols (zf_scatter_weights); weight_cols may be a
+    device tensor or a pinned host tensor."""
+    n, m = _logical(weight, layout)
+    ldw = _mat(weight, torch.bfloat16, "weight")
+    r, c = _stored(layout, n, m - sel.k)
+    ldc = (_mat(weight_cols, torch.bfloat16, "weight_cols", r, c, device_ok=True) if r * c
+           else max(c, 1))
+    c_sel = sel.as_c()
+    _check("zf_scatter_weights", LIB.zf_scatter_weights(
+        _ptr(weight_cols), ldc, ctypes.byref(c_sel), sel.k, n, m, layout, _ptr(weight), ldw,
+        _stream(stream)))
+
+
 # ---------------------------------------------------------------------------
 # batched plans
 # ---------------------------------------------------------------------------
@@ -361,6 +441,9 @@ class MatrixBuffers:
     unpacked: Optional[torch.Tensor] = None
     src: Optional[StateSource] = None
     layout: int = ROW_MAJOR
+    sel_sq: Optional[torch.Tensor] = None   # Zen-auto statistics, [k] fp32
+    acc_sq: Optional[torch.Tensor] = None   # Zen-auto statistics, [m-k] fp32
+    weight_cols: Optional[torch.Tensor] = None  # deferred update: bf16 unselected columns
 
     def as_c(self) -> ZfMatrix:
         L = self.layout
@@ -387,7 +470,36 @@ class MatrixBuffers:
             x.ld_unpacked = _lmat(self.unpacked, torch.float32, "unpacked", L, n, m)
         if self.src is not None:
             x.src = self.src.as_c()
+        if self.sel_sq is not None:
+            _vec(self.sel_sq, torch.float32, "sel_sq", self.k)
+            x.sel_sq = _ptr(self.sel_sq)
+        if self.acc_sq is not None:
+            _vec(self.acc_sq, torch.float32, "acc_sq", m - self.k)
+            x.acc_sq = _ptr(self.acc_sq)
+        if self.weight_cols is not None:
+            r, c = _stored(L, n, m - self.k)
+            x.weight_cols = _ptr(self.weight_cols)
+            x.ld_weight_cols = _mat(self.weight_cols, torch.bfloat16, "weight_cols", r, c,
+                                    device_ok=True)
         return x
+
+
+ZEN_TOTALS_BYTES = ctypes.sizeof(ZfZenTotals)
+
+
+@dataclass(frozen=True)
+class ZenTotals:
+    """Set-wide Zen-auto totals of one step (zf_zen_totals)."""
+    sum_sel: float
+    sum_acc: float
+    k_total: int
+    u_total: int
+    trigger: bool
+
+    @staticmethod
+    def from_bytes(raw: bytes) -> "ZenTotals":
+        t = ZfZenTotals.from_buffer_copy(bytes(raw[:ZEN_TOTALS_BYTES]))
+        return ZenTotals(t.sum_sel, t.sum_acc, t.k_total, t.u_total, bool(t.trigger))
 
 
 class Plan:
@@ -419,6 +531,24 @@ class Plan:
 
     def unpack(self, scale: float, stream=None) -> None:
         _check("zf_plan_unpack", LIB.zf_plan_unpack(self._h, float(scale), _stream(stream)))
+
+    def scatter_weights(self, stream=None) -> None:
+        """W[:, unsel] = weight_cols of every matrix (zf_plan_scatter_weights)."""
+        _check("zf_plan_scatter_weights", LIB.zf_plan_scatter_weights(self._h, _stream(stream)))
+
+    def update_zen(self, hp: AdamHparams, step: int, mode: int, step_in_interval: int,
+                   accum_interval: int, tau: float, totals: torch.Tensor, stream=None) -> None:
+        """Fused update plus the Zen-auto statistics of every matrix (its
+        sel_sq / acc_sq) and the set-wide totals, written to `totals` (a
+        device tensor of ZEN_TOTALS_BYTES bytes, see ZenTotals)."""
+        if (totals.device.type != "cuda" or not totals.is_contiguous()
+                or totals.numel() * totals.element_size() < ZEN_TOTALS_BYTES):
+            raise ValueError(f"totals: expected a contiguous GPU tensor of at least "
+                             f"{ZEN_TOTALS_BYTES} bytes")
+        c_hp = hp.as_c()
+        _check("zf_plan_update_zen", LIB.zf_plan_update_zen(
+            self._h, ctypes.byref(c_hp), step, mode, step_in_interval, accum_interval,
+            float(tau), totals.data_ptr(), _stream(stream)))
 
     def close(self) -> None:
         if getattr(self, "_h", None):

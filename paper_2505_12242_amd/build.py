@@ -18,10 +18,11 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libzf.so")
 ARCH = "gfx950"
 
-SOURCES = ["zf_api.hip", "zf_kernels.hip", "zf_kernels_cm.hip"]
+SOURCES = ["zf_api.hip", "zf_kernels.hip", "zf_kernels_cm.hip", "zf_kernels_zen.hip",
+           "zf_kernels_offload.hip", "zf_host.cpp"]
 
 FLAGS = [
-    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared", "-Wall",
+    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared", "-Wall", "-pthread",
     "-ffp-contract=off", "-fhip-fp32-correctly-rounded-divide-sqrt",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]

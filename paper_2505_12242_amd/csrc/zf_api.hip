@@ -10,6 +10,35 @@
 #include "zf.h"
 #include "zf_internal.hpp"
 
+namespace zf {
+
+bool hparams_ok(const zf_adam_hparams* hp) {
+  if (hp == nullptr) return false;
+  const auto fin = [](double x) { return std::isfinite(x); };
+  return fin(hp->lr) && hp->lr >= 0.0 && fin(hp->eps) && hp->eps >= 0.0 && fin(hp->beta1) &&
+         hp->beta1 >= 0.0 && hp->beta1 < 1.0 && fin(hp->beta2) && hp->beta2 >= 0.0 &&
+         hp->beta2 < 1.0 && fin(hp->weight_decay) && hp->weight_decay >= 0.0;
+}
+
+AdamK adam_consts(const zf_adam_hparams& hp, int64_t step) {
+  const double t = static_cast<double>(step);
+  AdamK c;
+  c.b1 = static_cast<float>(hp.beta1);
+  c.b2 = static_cast<float>(hp.beta2);
+  c.c1 = static_cast<float>(1.0 - hp.beta1);
+  c.c2 = static_cast<float>(1.0 - hp.beta2);
+  c.lr = static_cast<float>(hp.lr);
+  c.eps = static_cast<float>(hp.eps);
+  c.wd = static_cast<float>(hp.lr * hp.weight_decay);
+  c.ib1 = static_cast<float>(1.0 / (1.0 - std::pow(hp.beta1, t)));
+  c.ib2 = static_cast<float>(1.0 / (1.0 - std::pow(hp.beta2, t)));
+  return c;
+}
+
+}  // namespace zf
+
+using zf::adam_consts;
+using zf::hparams_ok;
 using zf::AdamK;
 using zf::DevMat;
 using zf::Table;
@@ -55,29 +84,6 @@ Span span_of(const void* p, int64_t rows, int64_t width, int64_t ld, size_t elem
 
 bool overlaps(const Span& a, const Span& b) {
   return a.hi > a.lo && b.hi > b.lo && a.lo < b.hi && b.lo < a.hi;
-}
-
-bool hparams_ok(const zf_adam_hparams* hp) {
-  if (hp == nullptr) return false;
-  const auto fin = [](double x) { return std::isfinite(x); };
-  return fin(hp->lr) && hp->lr >= 0.0 && fin(hp->eps) && hp->eps >= 0.0 && fin(hp->beta1) &&
-         hp->beta1 >= 0.0 && hp->beta1 < 1.0 && fin(hp->beta2) && hp->beta2 >= 0.0 &&
-         hp->beta2 < 1.0 && fin(hp->weight_decay) && hp->weight_decay >= 0.0;
-}
-
-AdamK adam_consts(const zf_adam_hparams& hp, int64_t step) {
-  const double t = static_cast<double>(step);
-  AdamK c;
-  c.b1 = static_cast<float>(hp.beta1);
-  c.b2 = static_cast<float>(hp.beta2);
-  c.c1 = static_cast<float>(1.0 - hp.beta1);
-  c.c2 = static_cast<float>(1.0 - hp.beta2);
-  c.lr = static_cast<float>(hp.lr);
-  c.eps = static_cast<float>(hp.eps);
-  c.wd = static_cast<float>(hp.lr * hp.weight_decay);
-  c.ib1 = static_cast<float>(1.0 / (1.0 - std::pow(hp.beta1, t)));
-  c.ib2 = static_cast<float>(1.0 / (1.0 - std::pow(hp.beta2, t)));
-  return c;
 }
 
 // ---- geometry -------------------------------------------------------------
@@ -183,6 +189,31 @@ bool shape_ok(int64_t n, int64_t m, int64_t k) {
          m < (int64_t(1) << 30);
 }
 
+// Buffers that the kernels may find in pinned host memory (the full-state
+// store, the host-produced weight columns) must be device memory or host
+// memory mapped at the same address for the device; anything else (pageable
+// host memory, an address HIP does not know) is rejected before it can reach
+// a kernel.  Queries the runtime; enqueues nothing.
+bool device_accessible(const void* p) {
+  if (p == nullptr) return true;
+  hipPointerAttribute_t a;
+  std::memset(&a, 0, sizeof(a));
+  const hipError_t e = hipPointerGetAttributes(&a, p);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();  // leave no sticky error behind
+    return false;
+  }
+  if (a.type == hipMemoryTypeDevice || a.type == hipMemoryTypeManaged) return true;
+  // pinned host memory: usable in place when the device maps it at the host
+  // address (both pointers refer to the same spot of the allocation)
+  if (a.type == hipMemoryTypeHost) return a.devicePointer != nullptr && a.devicePointer == a.hostPointer;
+  return false;
+}
+
+bool store_accessible(const DevMat& d) {
+  return device_accessible(d.st_P) && device_accessible(d.st_M) && device_accessible(d.st_V);
+}
+
 // Checks of one Adam step's buffers (selection mask/prefix already checked).
 bool adam_args_ok(const DevMat& d, int32_t mode, Span g) {
   const int64_t n = d.n, m = d.m, k = d.k;
@@ -206,16 +237,34 @@ bool adam_args_ok(const DevMat& d, int32_t mode, Span g) {
   if (mode != zf::kInplace && d.init_P != nullptr &&
       !mat_ok(d.init_P, ext(L, n, m), d.ld_init, 4))
     return false;
-  const Span outs[4] = {span(d.P, ext(L, n, k), d.ld_state, 4),
+  const bool store = mode != zf::kInplace && d.st_P != nullptr;
+  if (store && (!store_accessible(d) || !mat_ok(d.st_P, ext(L, n, m), d.ld_store, 4) ||
+                !mat_ok(d.st_M, ext(L, n, m), d.ld_store, 4) ||
+                !mat_ok(d.st_V, ext(L, n, m), d.ld_store, 4) ||
+                (n > 0 && m > 0 && (d.st_M == nullptr || d.st_V == nullptr))))
+    return false;
+  const Span outs[7] = {span(d.P, ext(L, n, k), d.ld_state, 4),
                         span(d.M, ext(L, n, k), d.ld_state, 4),
                         span(d.V, ext(L, n, k), d.ld_state, 4),
-                        span(d.weight, ext(L, n, m), d.ld_weight, 2)};
-  for (int a = 0; a < 4; ++a) {
+                        span(d.weight, ext(L, n, m), d.ld_weight, 2),
+                        store ? span(d.st_P, ext(L, n, m), d.ld_store, 4) : Span{},
+                        store ? span(d.st_M, ext(L, n, m), d.ld_store, 4) : Span{},
+                        store ? span(d.st_V, ext(L, n, m), d.ld_store, 4) : Span{}};
+  for (int a = 0; a < 7; ++a) {
     if (overlaps(outs[a], g)) return false;
-    for (int b = a + 1; b < 4; ++b)
+    for (int b = a + 1; b < 7; ++b)
       if (overlaps(outs[a], outs[b])) return false;
   }
   return true;
+}
+
+// The full-state store (if any) against another buffer.
+bool store_overlaps(const DevMat& d, Span other) {
+  if (d.st_P == nullptr) return false;
+  const Ext e = ext(d.layout, d.n, d.m);
+  return overlaps(span(d.st_P, e, d.ld_store, 4), other) ||
+         overlaps(span(d.st_M, e, d.ld_store, 4), other) ||
+         overlaps(span(d.st_V, e, d.ld_store, 4), other);
 }
 
 bool pack_args_ok(const DevMat& d, int64_t sii, int64_t S, Span g) {
@@ -253,6 +302,10 @@ void apply_source(DevMat& d, const zf_state_source* src) {
   d.ld_prev = src->ld_prev;
   d.init_P = src->init_master;
   d.ld_init = src->ld_init;
+  d.st_P = src->store_master;
+  d.st_M = src->store_exp_avg;
+  d.st_V = src->store_exp_avg_sq;
+  d.ld_store = src->ld_store;
 }
 
 // Channel-major vector path: n a multiple of 8 and every present row start
@@ -265,7 +318,8 @@ bool cm_vec_ok(const DevMat& d) {
   return ok(d.grad, d.ld_grad, 8) && ok(d.weight, d.ld_weight, 8) && ok(d.P, d.ld_state, 4) &&
          ok(d.M, d.ld_state, 4) && ok(d.V, d.ld_state, 4) && ok(d.acc, d.ld_acc, 4) &&
          ok(d.out, d.ld_out, 4) && ok(d.prev_P, d.ld_prev, 4) && ok(d.prev_M, d.ld_prev, 4) &&
-         ok(d.prev_V, d.ld_prev, 4) && ok(d.init_P, d.ld_init, 4);
+         ok(d.prev_V, d.ld_prev, 4) && ok(d.init_P, d.ld_init, 4) && ok(d.st_P, d.ld_store, 4) &&
+         ok(d.st_M, d.ld_store, 4) && ok(d.st_V, d.ld_store, 4);
 }
 
 // Row-major update/unpack blocks address up_rows rows through 32-bit buffer
@@ -273,7 +327,8 @@ bool cm_vec_ok(const DevMat& d) {
 bool rm_strides_ok(const DevMat& d) {
   const int64_t lim = (int64_t(1) << 31) / std::max<int64_t>(d.up_rows, 1);
   return d.ld_grad * 2 < lim && d.ld_weight * 2 < lim && d.ld_state * 4 < lim &&
-         d.ld_acc * 4 < lim && d.ld_out * 4 < lim && d.ld_prev * 4 < lim && d.ld_init * 4 < lim;
+         d.ld_acc * 4 < lim && d.ld_out * 4 < lim && d.ld_prev * 4 < lim && d.ld_init * 4 < lim &&
+         d.ld_store * 4 < lim;
 }
 
 void finish_geometry(DevMat& d, int cn_rows, int up_rows) {
@@ -296,6 +351,10 @@ void finish_geometry(DevMat& d, int cn_rows, int up_rows) {
     d.cm_nch = d.n > 0 ? static_cast<int32_t>(ceil_div(d.n, int64_t(best) * zf::kThreads * 8)) : 0;
     d.cm_unch = d.n > 0 ? static_cast<int32_t>(ceil_div(d.n, zf::kCmUnpackChunk)) : 0;
     d.vec = cm_vec_ok(d) ? 1 : 0;
+    const auto al16 = [](const void* p, int64_t ld) {
+      return p != nullptr && aligned(p, 16) && ld % 8 == 0;
+    };
+    d.scat_vec = (d.n % 8 == 0 && al16(d.wcols, d.ld_wcols) && al16(d.weight, d.ld_weight)) ? 1 : 0;
   }
 }
 
@@ -318,7 +377,7 @@ hipError_t launch_update_any(const Table& t, const DevMat& one, int64_t blocks, 
                              int32_t mode, int32_t first, bool adam, bool pack, int32_t layout,
                              hipStream_t s) {
   return layout == zf::kChannelMajor
-             ? zf::launch_cm_update(t, one, blocks, c, mode, first, adam, pack, s)
+             ? zf::launch_cm_update(t, one, blocks, c, mode, first, adam, pack, nullptr, s)
              : zf::launch_update(t, one, blocks, c, mode, first, adam, pack, s);
 }
 
@@ -364,7 +423,7 @@ zf_status run_update(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad
       if (overlaps(a, span(master, es, ld_state, 4)) ||
           overlaps(a, span(exp_avg, es, ld_state, 4)) ||
           overlaps(a, span(exp_avg_sq, es, ld_state, 4)) ||
-          overlaps(a, span(weight, ext(layout, n, m), ld_weight, 2)))
+          overlaps(a, span(weight, ext(layout, n, m), ld_weight, 2)) || store_overlaps(d, a))
         return ZF_EINVAL;
     }
   }
@@ -517,6 +576,30 @@ zf_status zf_unpack(const float* acc, int64_t ld_acc, const zf_selection* sel, i
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
+zf_status zf_scatter_weights(const uint16_t* weight_cols, int64_t ld_wcols,
+                             const zf_selection* sel, int64_t k, int64_t n, int64_t m,
+                             int32_t layout, uint16_t* weight, int64_t ld_weight,
+                             zf_stream stream) {
+  if (!layout_ok(layout) || !shape_ok(n, m, k) || !selection_ok(sel, m, k, false) ||
+      !mat_ok(weight_cols, ext(layout, n, m - k), ld_wcols, 2) ||
+      !mat_ok(weight, ext(layout, n, m), ld_weight, 2))
+    return ZF_EINVAL;
+  if (overlaps(span(weight_cols, ext(layout, n, m - k), ld_wcols, 2),
+               span(weight, ext(layout, n, m), ld_weight, 2)))
+    return ZF_EINVAL;
+  if (n > 0 && m > k && !device_accessible(weight_cols)) return ZF_EINVAL;
+  DevMat d = base_mat(nullptr, n, m, 0, layout, sel, k);
+  d.wcols = weight_cols;
+  d.ld_wcols = ld_wcols;
+  d.weight = weight;
+  d.ld_weight = ld_weight;
+  finish_geometry(d, 256, pick_update_rows({{n, m}}));
+  const int64_t blocks = unpack_grid(d);
+  if (blocks == 0 || k == m) return ZF_OK;
+  const hipError_t e = zf::launch_scatter(single_table(), d, blocks, layout, as_stream(stream));
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
 }  // extern "C"
 
 // ===========================================================================
@@ -535,10 +618,14 @@ struct zf_plan {
   int64_t* d_off_top = nullptr;
   int64_t* d_off_up = nullptr;
   int64_t* d_off_unp = nullptr;
+  int64_t* d_off_zen = nullptr;
   double* d_ws = nullptr;
-  int64_t blk_cn = 0, blk_fin = 0, blk_top = 0, blk_up = 0, blk_unp = 0;
+  double* d_zs = nullptr;  // Zen-auto per-wave partials
+  double* d_zb = nullptr;  // Zen-auto per-finalize-block sums
+  int64_t blk_cn = 0, blk_fin = 0, blk_top = 0, blk_up = 0, blk_unp = 0, blk_zen = 0;
+  int64_t k_total = 0, u_total = 0;
   bool can_colnorm = true, can_topk = true, can_adam = true, can_remap = true, can_pack = true,
-       can_unpack = true;
+       can_unpack = true, can_zen = true, can_scatter = true;
 };
 
 namespace {
@@ -556,6 +643,10 @@ DevMat plan_mat(const zf_matrix& x) {
   d.norms = x.norms_sq;
   d.out = x.unpacked;
   d.ld_out = x.ld_unpacked;
+  d.sel_sq = x.sel_sq;
+  d.acc_sq = x.acc_sq;
+  d.wcols = x.weight_cols;
+  d.ld_wcols = x.ld_weight_cols;
   apply_source(d, &x.src);
   return d;
 }
@@ -579,11 +670,31 @@ zf_status check_plan_matrix(const zf_matrix& x, zf_plan& p) {
   DevMat d = plan_mat(x);
   p.can_adam = p.can_adam && have_grad && have_mask && have_idx &&
                (n * k == 0 || adam_args_ok(d, zf::kInplace, g));
-  p.can_remap = p.can_remap && p.can_adam && (n * k == 0 || adam_args_ok(d, zf::kRemap, g));
+  p.can_remap = p.can_remap && p.can_adam && (n * k == 0 || adam_args_ok(d, zf::kRemap, g)) &&
+                !store_overlaps(d, span(x.acc, ea, x.ld_acc, 4));
   p.can_pack = p.can_pack && have_grad && have_mask && have_idx && pack_args_ok(d, 1, 1, g);
   p.can_unpack = p.can_unpack && have_mask && mat_ok(x.acc, ea, x.ld_acc, 4) &&
                  mat_ok(x.unpacked, eg, x.ld_unpacked, 4) &&
                  !overlaps(span(x.acc, ea, x.ld_acc, 4), span(x.unpacked, eg, x.ld_unpacked, 4));
+  p.can_scatter = p.can_scatter && have_mask && mat_ok(x.weight_cols, ea, x.ld_weight_cols, 2) &&
+                  (n * (m - k) == 0 || device_accessible(x.weight_cols)) &&
+                  mat_ok(x.weight, eg, x.ld_weight, 2) &&
+                  !overlaps(span(x.weight_cols, ea, x.ld_weight_cols, 2),
+                            span(x.weight, eg, x.ld_weight, 2));
+  // Zen-auto statistics: channel-major only; [k] and [m-k] fp32 outputs that
+  // overlap neither each other nor any buffer the fused update touches.
+  {
+    const Span zsel = span_of(x.sel_sq, 1, k, k, 4), zacc = span_of(x.acc_sq, 1, m - k, m - k, 4);
+    const Span others[6] = {g, span(x.acc, ea, x.ld_acc, 4),
+                            span(x.master, ext(L, n, k), x.ld_state, 4),
+                            span(x.exp_avg, ext(L, n, k), x.ld_state, 4),
+                            span(x.exp_avg_sq, ext(L, n, k), x.ld_state, 4),
+                            span(x.weight, eg, x.ld_weight, 2)};
+    bool ok = L == zf::kChannelMajor && vector_ok(x.sel_sq, k, 4) &&
+              vector_ok(x.acc_sq, m - k, 4) && !overlaps(zsel, zacc);
+    for (int a = 0; ok && a < 6; ++a) ok = !overlaps(zsel, others[a]) && !overlaps(zacc, others[a]);
+    p.can_zen = p.can_zen && ok;
+  }
   // Strides must be valid whenever the buffer is given.
   if (x.weight && !mat_ok(x.weight, eg, x.ld_weight, 2)) return ZF_EINVAL;
   if (x.acc && !mat_ok(x.acc, ea, x.ld_acc, 4)) return ZF_EINVAL;
@@ -614,8 +725,8 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   const int cn_rows = pick_colnorm_rows(shapes);
   const int up_rows = pick_update_rows(shapes);
   std::vector<int64_t> off_cn(nmats + 1), off_fin(nmats + 1), off_top(nmats + 1),
-      off_up(nmats + 1), off_unp(nmats + 1);
-  int64_t ws_doubles = 0;
+      off_up(nmats + 1), off_unp(nmats + 1), off_zen(nmats + 1);
+  int64_t ws_doubles = 0, zs_doubles = 0;
   const bool cm = p->layout == zf::kChannelMajor;
   p->mats.resize(nmats);
   for (int32_t q = 0; q < nmats; ++q) {
@@ -627,6 +738,14 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
     }
     d.cn_ws = ws_doubles;
     if (!cm) ws_doubles += static_cast<int64_t>(d.cn_rb) * d.m;
+    d.zs_off = zs_doubles;
+    if (cm && p->can_zen) {
+      zs_doubles += d.m * static_cast<int64_t>(d.cm_nch) * zf::kCmWaves;
+      off_zen[q] = p->blk_zen;
+      p->blk_zen += ceil_div(d.m, zf::kZenCols);
+    }
+    p->k_total += d.k;
+    p->u_total += d.m - d.k;
     off_cn[q] = p->blk_cn;
     off_fin[q] = p->blk_fin;
     off_top[q] = p->blk_top;
@@ -644,6 +763,7 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   off_top[nmats] = p->blk_top;
   off_up[nmats] = p->blk_up;
   off_unp[nmats] = p->blk_unp;
+  off_zen[nmats] = p->blk_zen;
   const int64_t max_blocks = (int64_t(1) << 31) / zf::kThreads;
   if (p->blk_cn >= max_blocks || p->blk_up >= max_blocks || p->blk_unp >= max_blocks) {
     delete p;
@@ -652,8 +772,9 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
 
   const size_t mats_bytes = sizeof(DevMat) * nmats;
   const size_t off_bytes = sizeof(int64_t) * (nmats + 1);
-  const size_t head = (mats_bytes + 5 * off_bytes + 255) & ~size_t(255);
-  p->dev_bytes = head + sizeof(double) * static_cast<size_t>(ws_doubles);
+  const size_t head = (mats_bytes + 6 * off_bytes + 255) & ~size_t(255);
+  const int64_t zb_doubles = p->can_zen ? 2 * p->blk_zen : 0;
+  p->dev_bytes = head + sizeof(double) * static_cast<size_t>(ws_doubles + zs_doubles + zb_doubles);
   hipError_t e = hipMalloc(&p->dev, p->dev_bytes);
   if (e != hipSuccess) {
     g_last_hip_error = static_cast<int>(e);
@@ -667,7 +788,10 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   p->d_off_top = p->d_off_fin + (nmats + 1);
   p->d_off_up = p->d_off_top + (nmats + 1);
   p->d_off_unp = p->d_off_up + (nmats + 1);
+  p->d_off_zen = p->d_off_unp + (nmats + 1);
   p->d_ws = reinterpret_cast<double*>(base + head);
+  p->d_zs = p->d_ws + ws_doubles;
+  p->d_zb = p->d_zs + zs_doubles;
   std::vector<char> host(head, 0);
   std::memcpy(host.data(), p->mats.data(), mats_bytes);
   std::memcpy(host.data() + mats_bytes, off_cn.data(), off_bytes);
@@ -675,6 +799,7 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   std::memcpy(host.data() + mats_bytes + 2 * off_bytes, off_top.data(), off_bytes);
   std::memcpy(host.data() + mats_bytes + 3 * off_bytes, off_up.data(), off_bytes);
   std::memcpy(host.data() + mats_bytes + 4 * off_bytes, off_unp.data(), off_bytes);
+  std::memcpy(host.data() + mats_bytes + 5 * off_bytes, off_zen.data(), off_bytes);
   e = hipMemcpy(p->dev, host.data(), head, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     g_last_hip_error = static_cast<int>(e);
@@ -745,6 +870,38 @@ zf_status zf_plan_unpack(zf_plan* p, float scale, zf_stream stream) {
   const Table t{p->d_mats, p->d_off_unp, p->nmats};
   const hipError_t e =
       launch_unpack_any(t, p->mats[0], p->blk_unp, scale, p->layout, as_stream(stream));
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
+zf_status zf_plan_scatter_weights(zf_plan* p, zf_stream stream) {
+  if (p == nullptr || !p->can_scatter) return ZF_EINVAL;
+  const Table t{p->d_mats, p->d_off_unp, p->nmats};
+  const hipError_t e = zf::launch_scatter(t, p->mats[0], p->blk_unp, p->layout, as_stream(stream));
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
+zf_status zf_plan_update_zen(zf_plan* p, const zf_adam_hparams* hp, int64_t step, int32_t mode,
+                             int64_t step_in_interval, int64_t accum_interval, double tau,
+                             zf_zen_totals* totals, zf_stream stream) {
+  if (p == nullptr || !p->can_zen || !p->can_adam || !p->can_pack) return ZF_EINVAL;
+  if (!hparams_ok(hp) || step < 1) return ZF_EINVAL;
+  if (mode != zf::kInplace && mode != zf::kRemap && mode != zf::kInit) return ZF_EINVAL;
+  if (mode == zf::kRemap && !p->can_remap) return ZF_EINVAL;
+  if (accum_interval < 1 || step_in_interval < 1 || step_in_interval > accum_interval)
+    return ZF_EINVAL;
+  if (!(tau >= 0.0) || totals == nullptr || !aligned(totals, 8)) return ZF_EINVAL;
+  static_assert(sizeof(zf_zen_totals) == sizeof(zf::ZenTotals), "zen totals layout");
+  const AdamK c = adam_consts(*hp, step);
+  const hipStream_t s = as_stream(stream);
+  const Table t{p->d_mats, p->d_off_up, p->nmats};
+  hipError_t e = zf::launch_cm_update(t, p->mats[0], p->blk_up, c, mode,
+                                      step_in_interval == 1 ? 1 : 0, true, true, p->d_zs, s);
+  if (e != hipSuccess) return hip_fail(e);
+  const Table tz{p->d_mats, p->d_off_zen, p->nmats};
+  e = zf::launch_zen_finalize(tz, p->mats[0], p->blk_zen, p->d_zs, p->d_zb, s);
+  if (e != hipSuccess) return hip_fail(e);
+  e = zf::launch_zen_total(p->d_zb, p->blk_zen, p->k_total, p->u_total, tau,
+                           reinterpret_cast<zf::ZenTotals*>(totals), s);
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 

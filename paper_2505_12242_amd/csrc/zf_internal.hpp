@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "zf.h"
+
 namespace zf {
 
 // Tile shapes.  A colnorm block covers 512 columns (64 lanes x 8 bf16 = one
@@ -32,6 +34,11 @@ constexpr int kCmVpt = ZF_CM_VPT;
 constexpr int kCmUnpackVpt = ZF_CM_UNPACK_VPT;
 constexpr int kCmUnpackChunk = kThreads * 8 * kCmUnpackVpt;
 constexpr int kCmColnormCols = kThreads / 64;
+constexpr int kCmWaves = kThreads / 64;  // waves per update block (one statistics partial each)
+
+// Zen-auto: channels per finalize block; threads of the one-block total.
+constexpr int kZenCols = 256;
+constexpr int kZenTotalThreads = 256;
 
 enum StateMode : int32_t { kInplace = 0, kRemap = 1, kInit = 2 };
 enum Layout : int32_t { kRowMajor = 0, kChannelMajor = 1 };
@@ -64,7 +71,16 @@ struct DevMat {
   int64_t ld_prev;
   const float* init_P;
   int64_t ld_init;
+  float* st_P;       // full-state store (swap in / out), n x m in the layout
+  float* st_M;
+  float* st_V;
+  int64_t ld_store;
+  const uint16_t* wcols;  // deferred update: bf16 weights of the unselected columns (slot order)
+  int64_t ld_wcols;
+  float* sel_sq;     // Zen-auto: [k] squared norms of the selected channels' gradient
+  float* acc_sq;     // Zen-auto: [m-k] squared norms of the accumulated channels
   // geometry
+  int64_t zs_off;    // offset (in doubles) of this matrix's Zen-auto partials
   int64_t cn_ws;     // offset (in doubles) of this matrix's colnorm partials
   int32_t cn_rpb;    // rows per colnorm block
   int32_t cn_rb;     // colnorm row blocks (0 when n == 0)
@@ -77,7 +93,7 @@ struct DevMat {
   int32_t cm_nch;    // channel-major: row chunks per channel (update)
   int32_t cm_unch;   // channel-major: row chunks per channel (unpack)
   int32_t cm_vpt;    // channel-major: 16-byte groups per thread in the update (1 or 2)
-  int32_t pad_;
+  int32_t scat_vec;  // channel-major: 16-byte path of the weight scatter
 };
 
 // Per-kernel view of a batch: a device array of matrices and the first
@@ -94,6 +110,13 @@ struct AdamK {
   float b1, b2, c1, c2, lr, eps, wd, ib1, ib2;
 };
 
+// Hyperparameter validation and the constants of a 1-based step
+// (zf_api.hip): B1 = beta1, C1 = 1 - beta1, B2 = beta2, C2 = 1 - beta2,
+// LR = lr, EPS = eps, WD = lr * weight_decay, IB1 = 1 / (1 - beta1^t),
+// IB2 = 1 / (1 - beta2^t), each computed in double and rounded once.
+bool hparams_ok(const zf_adam_hparams* hp);
+AdamK adam_consts(const zf_adam_hparams& hp, int64_t step);
+
 // Kernel launchers (zf_kernels.hip).  `blocks` is the grid size.
 hipError_t launch_colnorm(const Table& t, const DevMat& one, int64_t blocks,
                           const Table& tf, int64_t fin_blocks, double* ws, hipStream_t s);
@@ -105,9 +128,35 @@ hipError_t launch_unpack(const Table& t, const DevMat& one, int64_t blocks, floa
 
 // Channel-major kernels (zf_kernels_cm.hip).
 hipError_t launch_cm_colnorm(const Table& t, const DevMat& one, int64_t blocks, hipStream_t s);
+// zs != nullptr: fused Adam + pack that also writes the Zen-auto partials.
 hipError_t launch_cm_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
-                            int32_t mode, int32_t first, bool adam, bool pack, hipStream_t s);
+                            int32_t mode, int32_t first, bool adam, bool pack, double* zs,
+                            hipStream_t s);
 hipError_t launch_cm_unpack(const Table& t, const DevMat& one, int64_t blocks, float scale,
                             hipStream_t s);
+
+// Deferred update write-back (zf_kernels_offload.hip): W[:, unsel[u]] =
+// wcols[:, u] in either layout (grid: unpack geometry).
+hipError_t launch_scatter(const Table& t, const DevMat& one, int64_t blocks, int32_t layout,
+                          hipStream_t s);
+
+// Zen-auto reductions (zf_kernels_zen.hip).  Totals as written to device
+// memory; the layout equals the public zf_zen_totals.
+struct ZenTotals {
+  double sum_sel;
+  double sum_acc;
+  int64_t k_total;
+  int64_t u_total;
+  int32_t trigger;
+  int32_t pad_;
+};
+
+// Per-channel statistics from the partials zs, and two fp64 partial sums
+// (selected, accumulated) per finalize block into zb[2 * blocks].
+hipError_t launch_zen_finalize(const Table& t, const DevMat& one, int64_t blocks,
+                               const double* zs, double* zb, hipStream_t s);
+// One block: sums zb in a fixed order and evaluates the trigger.
+hipError_t launch_zen_total(const double* zb, int64_t blocks, int64_t k_total, int64_t u_total,
+                            double tau, ZenTotals* out, hipStream_t s);
 
 }  // namespace zf

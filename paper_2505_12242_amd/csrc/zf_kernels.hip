@@ -338,9 +338,14 @@ struct AdamSrc {
   bool was;                     // column was selected before (remap)
   rsrc_t rI;                    // fp32 init master (init from master)
   uint32_t vI, sI;
+  rsrc_t rTP, rTM, rTV;         // full-state store (swap-in)
+  uint32_t vT, sT;
 };
 
-enum SrcKind { kSrcInplace = 0, kSrcRemapW, kSrcRemapMaster, kSrcInitW, kSrcInitMaster };
+enum SrcKind {
+  kSrcInplace = 0, kSrcRemapW, kSrcRemapMaster, kSrcInitW, kSrcInitMaster,
+  kSrcRemapStore, kSrcInitStore  // swap-in of new columns from the full-state store
+};
 
 template <int SRC>
 __device__ __forceinline__ void load_state(const AdamSrc& a, int32_t i, float& p, float& m,
@@ -349,6 +354,23 @@ __device__ __forceinline__ void load_state(const AdamSrc& a, int32_t i, float& p
     p = buf_f32(a.rP, a.vS, i * a.sS);
     m = buf_f32(a.rM, a.vS, i * a.sS);
     v = buf_f32(a.rV, a.vS, i * a.sS);
+  } else if constexpr (SRC == kSrcRemapStore || SRC == kSrcInitStore) {
+    const float pt = buf_f32(a.rTP, a.vT, i * a.sT);
+    const float mt = buf_f32(a.rTM, a.vT, i * a.sT);
+    const float vt = buf_f32(a.rTV, a.vT, i * a.sT);
+    if constexpr (SRC == kSrcRemapStore) {
+      // both sources are read; the lane keeps the one that applies
+      const float pp = buf_f32(a.rSP, a.vPrev, i * a.sPrev);
+      const float mp = buf_f32(a.rSM, a.vPrev, i * a.sPrev);
+      const float vp = buf_f32(a.rSV, a.vPrev, i * a.sPrev);
+      p = a.was ? pp : pt;
+      m = a.was ? mp : mt;
+      v = a.was ? vp : vt;
+    } else {
+      p = pt;
+      m = mt;
+      v = vt;
+    }
   } else {
     // init value of p for a newly selected column
     float pi;
@@ -417,9 +439,10 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const DevMat* __restri
   const int64_t c0 = cblk * kUpdateCols;
   const TileSlots ts = tile_slots(d, c0);
   const int tid = threadIdx.x;
-  const bool is_pack = PACK && tid < ts.cu;
+  const bool swap_out = mode == kRemap && d.st_P != nullptr;
+  const bool is_unsel = (PACK || swap_out) && tid < ts.cu;
   const bool is_adam = ADAM && tid >= ts.cu && tid < ts.width;
-  if (!is_pack && !is_adam) return;
+  if (!is_unsel && !is_adam) return;
 
   const int64_t i0 = rblk * d.up_rows;
   const int64_t i1 = min(i0 + static_cast<int64_t>(d.up_rows), d.n);
@@ -427,13 +450,29 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const DevMat* __restri
   const rsrc_t rG = rows_rsrc(d.grad, i0, i1, d.ld_grad, d.m);
   const uint32_t sG = static_cast<uint32_t>(d.ld_grad * 2);  // bytes per G row
 
-  if (is_pack) {
+  if (is_unsel) {
     const uint32_t u = static_cast<uint32_t>(ts.us + tid);
-    const uint32_t vG = static_cast<uint32_t>(d.unsel_idx[u]) * 2u;
-    const rsrc_t rA = rows_rsrc(d.acc, i0, i1, d.ld_acc, d.m - d.k);
-    const uint32_t sA = static_cast<uint32_t>(d.ld_acc * 4);
-    if (first) pack_rows<true>(rG, vG, sG, rA, u * 4u, sA, rows);
-    else pack_rows<false>(rG, vG, sG, rA, u * 4u, sA, rows);
+    const uint32_t j = static_cast<uint32_t>(d.unsel_idx[u]);
+    if (swap_out) {
+      // a column that left the selection: previous compact (p, m, v) -> store
+      const uint64_t pm = d.prev_mask[j >> 6];
+      if ((pm >> (j & 63u)) & 1ull) {
+        const int64_t ro = static_cast<int64_t>(d.prev_prefix[j >> 6]) +
+                           __popcll(pm & ((uint64_t(1) << (j & 63u)) - 1));
+        for (int64_t i = i0; i < i1; ++i) {
+          d.st_P[i * d.ld_store + j] = d.prev_P[i * d.ld_prev + ro];
+          d.st_M[i * d.ld_store + j] = d.prev_M[i * d.ld_prev + ro];
+          d.st_V[i * d.ld_store + j] = d.prev_V[i * d.ld_prev + ro];
+        }
+      }
+    }
+    if constexpr (PACK) {
+      const uint32_t vG = j * 2u;
+      const rsrc_t rA = rows_rsrc(d.acc, i0, i1, d.ld_acc, d.m - d.k);
+      const uint32_t sA = static_cast<uint32_t>(d.ld_acc * 4);
+      if (first) pack_rows<true>(rG, vG, sG, rA, u * 4u, sA, rows);
+      else pack_rows<false>(rG, vG, sG, rA, u * 4u, sA, rows);
+    }
     return;
   }
 
@@ -459,10 +498,21 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const DevMat* __restri
   a.vI = 0;
   a.sI = 0;
   const bool master = d.init_P != nullptr;
+  const bool store = d.st_P != nullptr;
   if (mode != kInplace && master) {
     a.rI = rows_rsrc(d.init_P, i0, i1, d.ld_init, d.m);
     a.vI = j * 4u;
     a.sI = static_cast<uint32_t>(d.ld_init * 4);
+  }
+  a.rTP = a.rTM = a.rTV = a.rP;
+  a.vT = 0;
+  a.sT = 0;
+  if (mode != kInplace && store) {
+    a.rTP = rows_rsrc(d.st_P, i0, i1, d.ld_store, d.m);
+    a.rTM = rows_rsrc(d.st_M, i0, i1, d.ld_store, d.m);
+    a.rTV = rows_rsrc(d.st_V, i0, i1, d.ld_store, d.m);
+    a.vT = j * 4u;
+    a.sT = static_cast<uint32_t>(d.ld_store * 4);
   }
   if (mode == kRemap) {
     const uint32_t w = j >> 6;
@@ -479,10 +529,12 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const DevMat* __restri
   }
   if (mode == kInplace) adam_rows<kSrcInplace>(a, rG, sG, c, rows);
   else if (mode == kRemap) {
-    if (master) adam_rows<kSrcRemapMaster>(a, rG, sG, c, rows);
+    if (store) adam_rows<kSrcRemapStore>(a, rG, sG, c, rows);
+    else if (master) adam_rows<kSrcRemapMaster>(a, rG, sG, c, rows);
     else adam_rows<kSrcRemapW>(a, rG, sG, c, rows);
   } else {
-    if (master) adam_rows<kSrcInitMaster>(a, rG, sG, c, rows);
+    if (store) adam_rows<kSrcInitStore>(a, rG, sG, c, rows);
+    else if (master) adam_rows<kSrcInitMaster>(a, rG, sG, c, rows);
     else adam_rows<kSrcInitW>(a, rG, sG, c, rows);
   }
 }

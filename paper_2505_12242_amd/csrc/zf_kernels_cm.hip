@@ -92,6 +92,14 @@ __device__ __forceinline__ uint32_t group_elem(int g, int tid) {
   return static_cast<uint32_t>((g * kThreads + tid) * kGroup);
 }
 
+// ss += x^2 over eight fp32 values, in fp64 (squares of fp32 values are
+// exact in fp64).
+__device__ __forceinline__ void sum_squares8(const float (&f)[kGroup], double& ss) {
+#pragma unroll
+  for (int i = 0; i < kGroup; ++i)
+    ss = __builtin_fma(static_cast<double>(f[i]), static_cast<double>(f[i]), ss);
+}
+
 // ---------------------------------------------------------------------------
 // a1: column scores.  One wave per channel: lanes stride through the row
 // with 16-byte loads and sum squares in fp64 (exact squares), then a fixed
@@ -157,10 +165,10 @@ enum CmSrc { kCmInplace = 0, kCmPrev, kCmInitW, kCmInitMaster };
 
 // Adam over one chunk of channel j (slot r), vector path.  SRC picks where
 // (p, m, v) come from; rS* are the source rows (the slot's own rows in place).
-template <int SRC, int VPT>
+template <int SRC, int VPT, bool STATS>
 __device__ __forceinline__ void cm_adam_vec(rsrc_t rG, rsrc_t rP, rsrc_t rM, rsrc_t rV,
                                             rsrc_t rW, rsrc_t rSP, rsrc_t rSM, rsrc_t rSV,
-                                            rsrc_t rI, const AdamK& c) {
+                                            rsrc_t rI, const AdamK& c, double& ss) {
   const int tid = threadIdx.x;
   float g[VPT][kGroup], p[VPT][kGroup], m[VPT][kGroup], v[VPT][kGroup];
   u32x4 gv[VPT];
@@ -183,6 +191,7 @@ __device__ __forceinline__ void cm_adam_vec(rsrc_t rG, rsrc_t rP, rsrc_t rM, rsr
 #pragma unroll
   for (int q = 0; q < VPT; ++q) {
     widen8(gv[q], g[q]);
+    if constexpr (STATS) sum_squares8(g[q], ss);
 #pragma unroll
     for (int i = 0; i < kGroup; ++i) adam_step(g[q][i], p[q][i], m[q][i], v[q][i], c);
     const uint32_t e = group_elem(q, tid);
@@ -194,13 +203,14 @@ __device__ __forceinline__ void cm_adam_vec(rsrc_t rG, rsrc_t rP, rsrc_t rM, rsr
 }
 
 // Element-wise fallback of the same update (any n, any alignment).
-template <int SRC>
+template <int SRC, bool STATS>
 __device__ __forceinline__ void cm_adam_elem(rsrc_t rG, rsrc_t rP, rsrc_t rM, rsrc_t rV,
                                              rsrc_t rW, rsrc_t rSP, rsrc_t rSM, rsrc_t rSV,
-                                             rsrc_t rI, const AdamK& c, int64_t len) {
+                                             rsrc_t rI, const AdamK& c, int64_t len, double& ss) {
   for (int64_t e = threadIdx.x; e < len; e += kThreads) {
     const uint32_t o = static_cast<uint32_t>(e);
     const float g = widen_bf16(buf_u16<kAuxRO>(rG, o * 2, 0));
+    if constexpr (STATS) ss = __builtin_fma(static_cast<double>(g), static_cast<double>(g), ss);
     float p, m, v;
     if constexpr (SRC == kCmInplace || SRC == kCmPrev) {
       p = buf_f32<kAuxRMW>(rSP, o * 4, 0);
@@ -218,8 +228,8 @@ __device__ __forceinline__ void cm_adam_elem(rsrc_t rG, rsrc_t rP, rsrc_t rM, rs
   }
 }
 
-template <bool FIRST, int VPT>
-__device__ __forceinline__ void cm_pack_vec(rsrc_t rG, rsrc_t rA) {
+template <bool FIRST, int VPT, bool STATS>
+__device__ __forceinline__ void cm_pack_vec(rsrc_t rG, rsrc_t rA, double& ss) {
   const int tid = threadIdx.x;
   u32x4 gv[VPT];
   float a[VPT][kGroup];
@@ -235,44 +245,88 @@ __device__ __forceinline__ void cm_pack_vec(rsrc_t rG, rsrc_t rA) {
     widen8(gv[q], g);
 #pragma unroll
     for (int i = 0; i < kGroup; ++i) a[q][i] = FIRST ? g[i] : a[q][i] + g[i];
+    if constexpr (STATS) sum_squares8(a[q], ss);
     f32x8_store<FIRST ? kAuxWO : kAuxRMW>(rA, group_elem(q, tid) * 4, a[q]);
   }
 }
 
-template <bool FIRST>
-__device__ __forceinline__ void cm_pack_elem(rsrc_t rG, rsrc_t rA, int64_t len) {
+template <bool FIRST, bool STATS>
+__device__ __forceinline__ void cm_pack_elem(rsrc_t rG, rsrc_t rA, int64_t len, double& ss) {
   for (int64_t e = threadIdx.x; e < len; e += kThreads) {
     const uint32_t o = static_cast<uint32_t>(e);
     const float g = widen_bf16(buf_u16<kAuxRO>(rG, o * 2, 0));
-    if constexpr (FIRST) buf_put_f32<kAuxWO>(g, rA, o * 4, 0);
-    else buf_put_f32<kAuxRMW>(buf_f32<kAuxRMW>(rA, o * 4, 0) + g, rA, o * 4, 0);
+    const float a = FIRST ? g : buf_f32<kAuxRMW>(rA, o * 4, 0) + g;
+    if constexpr (STATS) ss = __builtin_fma(static_cast<double>(a), static_cast<double>(a), ss);
+    buf_put_f32<FIRST ? kAuxWO : kAuxRMW>(a, rA, o * 4, 0);
   }
 }
 
-template <int SRC>
+template <int SRC, bool STATS>
 __device__ __forceinline__ void cm_adam_vec_any(int vpt, rsrc_t rG, rsrc_t rP, rsrc_t rM,
                                                 rsrc_t rV, rsrc_t rW, rsrc_t rSP, rsrc_t rSM,
-                                                rsrc_t rSV, rsrc_t rI, const AdamK& c) {
-  if (vpt >= 2) cm_adam_vec<SRC, kCmVpt>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c);
-  else cm_adam_vec<SRC, 1>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c);
+                                                rsrc_t rSV, rsrc_t rI, const AdamK& c,
+                                                double& ss) {
+  if (vpt >= 2) cm_adam_vec<SRC, kCmVpt, STATS>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss);
+  else cm_adam_vec<SRC, 1, STATS>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss);
 }
 
-template <bool FIRST>
-__device__ __forceinline__ void cm_pack_vec_any(int vpt, rsrc_t rG, rsrc_t rA) {
-  if (vpt >= 2) cm_pack_vec<FIRST, kCmVpt>(rG, rA);
-  else cm_pack_vec<FIRST, 1>(rG, rA);
+template <bool FIRST, bool STATS>
+__device__ __forceinline__ void cm_pack_vec_any(int vpt, rsrc_t rG, rsrc_t rA, double& ss) {
+  if (vpt >= 2) cm_pack_vec<FIRST, kCmVpt, STATS>(rG, rA, ss);
+  else cm_pack_vec<FIRST, 1, STATS>(rG, rA, ss);
 }
 
-template <bool BATCHED, bool ADAM, bool PACK>
+// Swap-out of one chunk of a channel that left the selection: its previous
+// compact (p, m, v) rows are copied to its rows of the full-state store.
+__device__ __forceinline__ void cm_swap_out(const DevMat& d, int64_t j, int64_t w, int64_t e0,
+                                            int64_t len) {
+  const uint64_t pm = d.prev_mask[w];
+  if (!((pm >> (j & 63)) & 1ull)) return;
+  const int64_t ro = static_cast<int64_t>(d.prev_prefix[w]) +
+                     __popcll(pm & ((uint64_t(1) << (j & 63)) - 1));
+  const rsrc_t src[3] = {make_rsrc(d.prev_P + ro * d.ld_prev + e0, len * 4),
+                         make_rsrc(d.prev_M + ro * d.ld_prev + e0, len * 4),
+                         make_rsrc(d.prev_V + ro * d.ld_prev + e0, len * 4)};
+  const rsrc_t dst[3] = {make_rsrc(d.st_P + j * d.ld_store + e0, len * 4),
+                         make_rsrc(d.st_M + j * d.ld_store + e0, len * 4),
+                         make_rsrc(d.st_V + j * d.ld_store + e0, len * 4)};
+  if (d.vec) {
+    for (int64_t g = threadIdx.x; g * kGroup < len; g += kThreads) {
+      const uint32_t o = static_cast<uint32_t>(g * kGroup * 4);
+#pragma unroll
+      for (int a = 0; a < 3; ++a) {
+        float f[kGroup];
+        f32x8_load<kAuxRO>(src[a], o, f);
+        f32x8_store<kAuxWO>(dst[a], o, f);
+      }
+    }
+  } else {
+    for (int64_t e = threadIdx.x; e < len; e += kThreads) {
+      const uint32_t o = static_cast<uint32_t>(e) * 4;
+#pragma unroll
+      for (int a = 0; a < 3; ++a) buf_put_f32<kAuxWO>(buf_f32<kAuxRO>(src[a], o, 0), dst[a], o, 0);
+    }
+  }
+}
+
+// STATS (fused Adam + pack only): every wave also sums, in fp64, the squares
+// of the values its lanes handled -- the gradient of a selected channel, the
+// new accumulated value of an unselected one -- after a fixed xor butterfly,
+// and writes that partial to zs[zs_off + (j * cm_nch + chunk) * 4 + wave].
+// The partials of a channel are combined in a fixed order by the Zen-auto
+// finalize kernel; no barriers, no atomics.
+template <bool BATCHED, bool ADAM, bool PACK, bool STATS>
 __global__ __launch_bounds__(kThreads) void cm_update_kernel(const DevMat* __restrict__ mats,
                                                             const int64_t* __restrict__ off,
                                                             int32_t nmats, DevMat one, AdamK c,
-                                                            int32_t mode, int32_t first) {
+                                                            int32_t mode, int32_t first,
+                                                            double* __restrict__ zs) {
   int64_t local;
   const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, local);
   const int64_t chunk = static_cast<int64_t>(d.cm_vpt) * kThreads * kGroup;
   const int64_t j = local / d.cm_nch;
-  const int64_t e0 = (local % d.cm_nch) * chunk;
+  const int64_t ci = local % d.cm_nch;
+  const int64_t e0 = ci * chunk;
   const int64_t len = min(chunk, d.n - e0);
   const int64_t w = j >> 6;
   const uint64_t mw = d.mask[w];
@@ -280,22 +334,22 @@ __global__ __launch_bounds__(kThreads) void cm_update_kernel(const DevMat* __res
   const int64_t r = static_cast<int64_t>(d.prefix[w]) +
                     __popcll(mw & ((uint64_t(1) << (j & 63)) - 1));
   const rsrc_t rG = make_rsrc(d.grad + j * d.ld_grad + e0, len * 2);
+  double ss = 0.0;
 
   if (!sel) {
+    if (mode == kRemap && d.st_P != nullptr) cm_swap_out(d, j, w, e0, len);
     if constexpr (PACK) {
       const int64_t u = j - r;
       const rsrc_t rA = make_rsrc(d.acc + u * d.ld_acc + e0, len * 4);
       if (d.vec) {
-        if (first) cm_pack_vec_any<true>(d.cm_vpt, rG, rA);
-        else cm_pack_vec_any<false>(d.cm_vpt, rG, rA);
+        if (first) cm_pack_vec_any<true, STATS>(d.cm_vpt, rG, rA, ss);
+        else cm_pack_vec_any<false, STATS>(d.cm_vpt, rG, rA, ss);
       } else {
-        if (first) cm_pack_elem<true>(rG, rA, len);
-        else cm_pack_elem<false>(rG, rA, len);
+        if (first) cm_pack_elem<true, STATS>(rG, rA, len, ss);
+        else cm_pack_elem<false, STATS>(rG, rA, len, ss);
       }
     }
-    return;
-  }
-  if constexpr (ADAM) {
+  } else if constexpr (ADAM) {
     const rsrc_t rP = make_rsrc(d.P + r * d.ld_state + e0, len * 4);
     const rsrc_t rM = make_rsrc(d.M + r * d.ld_state + e0, len * 4);
     const rsrc_t rV = make_rsrc(d.V + r * d.ld_state + e0, len * 4);
@@ -317,22 +371,35 @@ __global__ __launch_bounds__(kThreads) void cm_update_kernel(const DevMat* __res
     } else if (mode == kInit) {
       src = d.init_P ? kCmInitMaster : kCmInitW;
     }
+    if (mode != kInplace && src != kCmPrev && d.st_P != nullptr) {
+      // swap-in from the full-state store: the same loads as a moved column
+      rSP = make_rsrc(d.st_P + j * d.ld_store + e0, len * 4);
+      rSM = make_rsrc(d.st_M + j * d.ld_store + e0, len * 4);
+      rSV = make_rsrc(d.st_V + j * d.ld_store + e0, len * 4);
+      src = kCmPrev;
+    }
     if (src == kCmInitMaster) rI = make_rsrc(d.init_P + j * d.ld_init + e0, len * 4);
     if (d.vec) {
       switch (src) {
-        case kCmInplace: cm_adam_vec_any<kCmInplace>(d.cm_vpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c); break;
-        case kCmPrev: cm_adam_vec_any<kCmPrev>(d.cm_vpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c); break;
-        case kCmInitW: cm_adam_vec_any<kCmInitW>(d.cm_vpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c); break;
-        default: cm_adam_vec_any<kCmInitMaster>(d.cm_vpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c); break;
+        case kCmInplace: cm_adam_vec_any<kCmInplace, STATS>(d.cm_vpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss); break;
+        case kCmPrev: cm_adam_vec_any<kCmPrev, STATS>(d.cm_vpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss); break;
+        case kCmInitW: cm_adam_vec_any<kCmInitW, STATS>(d.cm_vpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss); break;
+        default: cm_adam_vec_any<kCmInitMaster, STATS>(d.cm_vpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss); break;
       }
     } else {
       switch (src) {
-        case kCmInplace: cm_adam_elem<kCmInplace>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, len); break;
-        case kCmPrev: cm_adam_elem<kCmPrev>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, len); break;
-        case kCmInitW: cm_adam_elem<kCmInitW>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, len); break;
-        default: cm_adam_elem<kCmInitMaster>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, len); break;
+        case kCmInplace: cm_adam_elem<kCmInplace, STATS>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, len, ss); break;
+        case kCmPrev: cm_adam_elem<kCmPrev, STATS>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, len, ss); break;
+        case kCmInitW: cm_adam_elem<kCmInitW, STATS>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, len, ss); break;
+        default: cm_adam_elem<kCmInitMaster, STATS>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, len, ss); break;
       }
     }
+  }
+  if constexpr (STATS) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o, 64);
+    if ((threadIdx.x & 63) == 0)
+      zs[d.zs_off + (j * d.cm_nch + ci) * kCmWaves + (threadIdx.x >> 6)] = ss;
   }
 }
 
@@ -403,25 +470,33 @@ hipError_t launch_cm_colnorm(const Table& t, const DevMat& one, int64_t blocks, 
   return hipGetLastError();
 }
 
-template <bool ADAM, bool PACK>
+template <bool ADAM, bool PACK, bool STATS>
 static void launch_cm_update_t(const Table& t, const DevMat& one, dim3 grid, const AdamK& c,
-                               int32_t mode, int32_t first, hipStream_t s) {
+                               int32_t mode, int32_t first, double* zs, hipStream_t s) {
   if (t.mats != nullptr)
-    hipLaunchKernelGGL((cm_update_kernel<true, ADAM, PACK>), grid, dim3(kThreads), 0, s, t.mats,
-                       t.off, t.nmats, one, c, mode, first);
+    hipLaunchKernelGGL((cm_update_kernel<true, ADAM, PACK, STATS>), grid, dim3(kThreads), 0, s,
+                       t.mats, t.off, t.nmats, one, c, mode, first, zs);
   else
-    hipLaunchKernelGGL((cm_update_kernel<false, ADAM, PACK>), grid, dim3(kThreads), 0, s, t.mats,
-                       t.off, t.nmats, one, c, mode, first);
+    hipLaunchKernelGGL((cm_update_kernel<false, ADAM, PACK, STATS>), grid, dim3(kThreads), 0, s,
+                       t.mats, t.off, t.nmats, one, c, mode, first, zs);
 }
 
 hipError_t launch_cm_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
-                            int32_t mode, int32_t first, bool adam, bool pack, hipStream_t s) {
+                            int32_t mode, int32_t first, bool adam, bool pack, double* zs,
+                            hipStream_t s) {
   (void)hipGetLastError();
   if (blocks <= 0) return hipSuccess;
   const dim3 grid(static_cast<uint32_t>(blocks));
-  if (adam && pack) launch_cm_update_t<true, true>(t, one, grid, c, mode, first, s);
-  else if (adam) launch_cm_update_t<true, false>(t, one, grid, c, mode, first, s);
-  else if (pack) launch_cm_update_t<false, true>(t, one, grid, c, mode, first, s);
+  if (zs != nullptr) {
+    if (!(adam && pack)) return hipErrorInvalidValue;
+    launch_cm_update_t<true, true, true>(t, one, grid, c, mode, first, zs, s);
+  } else if (adam && pack) {
+    launch_cm_update_t<true, true, false>(t, one, grid, c, mode, first, nullptr, s);
+  } else if (adam) {
+    launch_cm_update_t<true, false, false>(t, one, grid, c, mode, first, nullptr, s);
+  } else if (pack) {
+    launch_cm_update_t<false, true, false>(t, one, grid, c, mode, first, nullptr, s);
+  }
   return hipGetLastError();
 }
 

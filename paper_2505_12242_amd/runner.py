@@ -12,21 +12,50 @@ issues one batched launch per kernel per step:
 Compact states and selections are double-buffered: a refresh writes the new
 selection and new states into the other buffer while reading the previous
 ones (ZF_STATES_REMAP), so a column that stays selected carries its moments
-(the selective optimizer follows its subset, Zero-stall Pipeline "Swapping
-out/in") without a separate pass.  Gradients come from caller-owned slots;
-step t reads slot (t-1) mod len(slots).  Every tensor of the runner is
-stored in one layout (ROW_MAJOR or CHANNEL_MAJOR, see the binding).
+without a separate pass.  Gradients come from caller-owned slots; step t
+reads slot (t-1) mod len(slots).  Every tensor of the runner is stored in
+one layout (ROW_MAJOR or CHANNEL_MAJOR, see the binding).
+
+Zen-auto (zen_tau set; the adaptive interval of the paper's Zero-stall
+Pipeline, "Hyperparameter Auto-tuning"): every update is zf_plan_update_zen,
+which also measures the selected channels' gradient norms and the
+accumulated channels' norms; the interval ends after the step whose pooled
+mean accumulated norm reaches zen_tau times the pooled mean selected norm,
+after `accum` (= S_max) steps, or before a refresh.  The decision is taken
+on the host from the 40-byte totals copied back after each update (one
+stream synchronisation per step).
+
+Offloaded optimizer (offload=True; Asynchronous Offloading Workflow and
+Zero-stall Pipeline): every column's fp32 (p, m, v) lives in a full-state
+store in pinned host memory.  A refresh swaps states against it inside the
+update pass (columns entering the selection read their states from the
+store, columns leaving write theirs back; the kernels access the pinned
+store in place).  At every interval end the packed buffer is copied to the
+host on a side stream and the deferred update (zf_host_adam_unselected, on
+host threads, its own step counter) applies the interval's mean gradient to
+the unselected columns of the store and produces their bf16 weights, which
+zf_plan_scatter_weights writes into W.  With overlap=True the device
+buffer is double-buffered, the copy and the host update run while the GPU
+continues with the next interval, and the weights are written back at the
+first step boundary after the host finishes -- and at the latest before the
+next refresh, which is the only step that reads the store, so the results
+equal the synchronous order bit for bit.
 """
 
 from __future__ import annotations
 
+import concurrent.futures
+import os
+import time
 from dataclasses import dataclass
 from typing import List, Optional, Sequence, Tuple
 
+import numpy as np
 import torch
 
-from ._lib import (ROW_MAJOR, STATES_INIT, STATES_INPLACE, STATES_REMAP, AdamHparams,
-                   MatrixBuffers, Plan, Selection, StateSource, _stored, k_from_ratio)
+from ._lib import (ROW_MAJOR, STATES_INIT, STATES_INPLACE, STATES_REMAP, ZEN_TOTALS_BYTES,
+                   AdamHparams, MatrixBuffers, Plan, Selection, StateSource, ZenTotals, _stored,
+                   host_adam_unselected, k_from_ratio)
 
 
 @dataclass(frozen=True)
@@ -61,40 +90,91 @@ def _no_record(name):
     return _NoRecord()
 
 
+def _pinned_like(shape, dtype):
+    return torch.empty(*shape, dtype=dtype, pin_memory=True)
+
+
 class SelectiveUpdateRunner:
     def __init__(self, shapes: Sequence[Tuple[int, int]], ratio: float, hp: AdamHparams,
                  refresh: int, accum: int, grad_slots: Sequence[Sequence[torch.Tensor]],
                  weights: Sequence[torch.Tensor],
                  init_master: Optional[Sequence[torch.Tensor]] = None,
-                 device=None, keep_unpacked: bool = True, layout: int = ROW_MAJOR):
+                 device=None, keep_unpacked: bool = True, layout: int = ROW_MAJOR,
+                 zen_tau: Optional[float] = None, offload: bool = False, overlap: bool = True,
+                 host_threads: Optional[int] = None):
         self.device = torch.device(device) if device is not None else torch.device("cuda")
         self.shapes = [(int(n), int(m)) for n, m in shapes]
         self.ratio, self.hp, self.R, self.S = ratio, hp, int(refresh), int(accum)
         self.ks = [k_from_ratio(ratio, m) for _, m in self.shapes]
         self.layout = layout
-        self.keep_unpacked = keep_unpacked
+        self.offload = bool(offload)
+        self.overlap = bool(overlap) and self.offload
+        self.keep_unpacked = keep_unpacked and not self.offload
         self.weights = list(weights)
         self.init_master = list(init_master) if init_master is not None else None
         dev = self.device
         f32 = torch.float32
+        self.zen_tau = None if zen_tau is None else float(zen_tau)
+        if self.zen_tau is not None:
+            self.zen_totals = torch.zeros(ZEN_TOTALS_BYTES // 8, dtype=torch.int64, device=dev)
+            self._zen_host = torch.zeros(ZEN_TOTALS_BYTES // 8, dtype=torch.int64,
+                                         pin_memory=True)
+        self.last_totals: Optional[ZenTotals] = None
+        self._length = 0
+        self._ended = True
+
         self.sels: List[List[Selection]] = [[], []]
         self.states: List[List[Tuple[torch.Tensor, torch.Tensor, torch.Tensor]]] = [[], []]
-        self.acc, self.norms, self.unpacked = [], [], []
-        for (n, m), k in zip(self.shapes, self.ks):
+        nacc = 2 if self.overlap else 1
+        self.accs: List[List[torch.Tensor]] = [[] for _ in range(nacc)]
+        self.norms, self.unpacked, self.sel_sq, self.acc_sq = [], [], [], []
+        self.store, self.host_acc, self.wcols, self.unsel_host = [], [], [], []
+        for q, ((n, m), k) in enumerate(zip(self.shapes, self.ks)):
+            if self.zen_tau is not None:
+                self.sel_sq.append(torch.empty(k, dtype=f32, device=dev))
+                self.acc_sq.append(torch.empty(m - k, dtype=f32, device=dev))
             for p in range(2):
                 self.sels[p].append(Selection(m, k, dev))
                 self.states[p].append(tuple(torch.empty(*_stored(layout, n, k), dtype=f32,
                                                         device=dev) for _ in range(3)))
-            self.acc.append(torch.empty(*_stored(layout, n, m - k), dtype=f32, device=dev))
+            for a in range(nacc):
+                self.accs[a].append(torch.empty(*_stored(layout, n, m - k), dtype=f32,
+                                                device=dev))
             self.norms.append(torch.empty(m, dtype=f32, device=dev))
             self.unpacked.append(torch.empty(*_stored(layout, n, m), dtype=f32, device=dev)
-                                 if keep_unpacked else None)
+                                 if self.keep_unpacked else None)
+            if self.offload:
+                p0 = (self.init_master[q] if self.init_master is not None
+                      else self.weights[q].float())
+                sp = _pinned_like(p0.shape, f32)
+                sp.copy_(p0)
+                self.store.append((sp, _pinned_like(p0.shape, f32).zero_(),
+                                   _pinned_like(p0.shape, f32).zero_()))
+                self.host_acc.append(_pinned_like(_stored(layout, n, m - k), f32))
+                self.wcols.append(_pinned_like(_stored(layout, n, m - k), torch.bfloat16))
+                self.unsel_host.append(_pinned_like((m - k,), torch.int32))
+        self.acc = self.accs[0]
         self.grad_slots = [list(s) for s in grad_slots]
-        self.plans = [[self._plan(slot, p) for p in range(2)] for slot in range(len(self.grad_slots))]
+        self.plans = [[[self._plan(slot, p, a) for a in range(nacc)] for p in range(2)]
+                      for slot in range(len(self.grad_slots))]
         self.t = 0
         self.cur = 0
+        self.cur_a = 0
+        # offloaded optimizer
+        self.th = 0
+        self.host_threads = host_threads if host_threads is not None else \
+            min(16, os.cpu_count() or 1)
+        self._job: Optional[concurrent.futures.Future] = None
+        self._ev_scatter: Optional[torch.cuda.Event] = None
+        self._acc_free: List[Optional[torch.cuda.Event]] = [None] * nacc
+        self._pool = (concurrent.futures.ThreadPoolExecutor(max_workers=1)
+                      if self.overlap else None)
+        self._copy_stream = torch.cuda.Stream(device=dev) if self.overlap else None
+        self.stall_s = 0.0      # host time spent waiting for the deferred update
+        self.host_update_s = 0.0  # host time inside the deferred update
+        torch.cuda.synchronize(dev)  # store and host buffers ready before any kernel
 
-    def _plan(self, slot: int, p: int) -> Plan:
+    def _plan(self, slot: int, p: int, a: int) -> Plan:
         q_bufs = []
         for q, ((n, m), k) in enumerate(zip(self.shapes, self.ks)):
             P, M, V = self.states[p][q]
@@ -102,10 +182,15 @@ class SelectiveUpdateRunner:
             src = StateSource(prev=self.sels[1 - p][q], prev_master=Pp, prev_exp_avg=Mp,
                               prev_exp_avg_sq=Vp,
                               init_master=self.init_master[q] if self.init_master else None)
+            if self.offload:
+                src.store_master, src.store_exp_avg, src.store_exp_avg_sq = self.store[q]
             q_bufs.append(MatrixBuffers(
                 grad=self.grad_slots[slot][q], k=k, sel=self.sels[p][q], weight=self.weights[q],
-                master=P, exp_avg=M, exp_avg_sq=V, acc=self.acc[q], norms=self.norms[q],
-                unpacked=self.unpacked[q], src=src, layout=self.layout))
+                master=P, exp_avg=M, exp_avg_sq=V, acc=self.accs[a][q], norms=self.norms[q],
+                unpacked=self.unpacked[q], src=src, layout=self.layout,
+                sel_sq=self.sel_sq[q] if self.sel_sq else None,
+                acc_sq=self.acc_sq[q] if self.acc_sq else None,
+                weight_cols=self.wcols[q] if self.offload else None))
         return Plan(q_bufs)
 
     @property
@@ -116,35 +201,157 @@ class SelectiveUpdateRunner:
     def state(self):
         return self.states[self.cur]
 
+    # ------------------------------------------------------------------ steps
+
     def step(self, stream=None, recorder=None) -> StepKind:
-        """Enqueues one step (no synchronisation).  `recorder`, if given, is
-        called as recorder(name) -> context manager around each launch (used
-        to bracket launches with events on the launch stream)."""
+        """Enqueues one step.  Without Zen-auto or the offloaded optimizer the
+        call does not synchronise.  `recorder`, if given, is called as
+        recorder(name) -> context manager around each launch (used to
+        bracket launches with events on the launch stream)."""
+        st = stream if stream is not None else torch.cuda.current_stream(self.device)
+        rec = recorder if recorder is not None else _no_record
         self.t += 1
         t = self.t
-        kind = schedule(t, self.R, self.S)
+        if self.zen_tau is None:
+            kind = schedule(t, self.R, self.S)
+            refresh, length = kind.refresh, kind.step_in_interval
+        else:
+            refresh = (t - 1) % self.R == 0
+            length = 1 if (refresh or self._ended) else self._length + 1
+            self._length = length
+        if self.offload:
+            self._before_step(refresh, length, st, rec)
         slot = (t - 1) % len(self.grad_slots)
-        rec = recorder if recorder is not None else _no_record
-        if kind.refresh:
+        if refresh:
             nxt = 0 if t == 1 else 1 - self.cur
-            plan = self.plans[slot][nxt]
+            plan = self.plans[slot][nxt][self.cur_a]
             with rec("colnorm"):
-                plan.colnorm(stream)
+                plan.colnorm(st)
             with rec("topk_select"):
-                plan.topk_select(stream)
+                plan.topk_select(st)
             mode = STATES_INIT if t == 1 else STATES_REMAP
             self.cur = nxt
         else:
-            plan = self.plans[slot][self.cur]
+            plan = self.plans[slot][self.cur][self.cur_a]
             mode = STATES_INPLACE
-        with rec("update_first" if kind.step_in_interval == 1 else "update"):
-            plan.update(self.hp, t, mode, kind.step_in_interval, self.S, stream=stream)
-        if kind.interval_end and self.keep_unpacked:
-            with rec("unpack"):
-                plan.unpack(1.0 / kind.step_in_interval, stream)
+        if self.zen_tau is None:
+            with rec("update_first" if length == 1 else "update"):
+                plan.update(self.hp, t, mode, length, self.S, stream=st)
+            end = kind.interval_end
+        else:
+            with rec("update_zen_first" if length == 1 else "update_zen"):
+                plan.update_zen(self.hp, t, mode, length, self.S, self.zen_tau,
+                                self.zen_totals, stream=st)
+            with torch.cuda.stream(st):
+                self._zen_host.copy_(self.zen_totals, non_blocking=True)
+            st.synchronize()
+            self.last_totals = ZenTotals.from_bytes(self._zen_host.numpy().tobytes())
+            end = self.last_totals.trigger or length >= self.S or t % self.R == 0
+            self._ended = end
+            kind = StepKind(refresh=refresh, step_in_interval=length, interval_end=end)
+        if end:
+            if self.offload:
+                self._hand_over(length, st, rec)
+            elif self.keep_unpacked:
+                with rec("unpack"):
+                    plan.unpack(1.0 / length, st)
         return kind
 
+    # --------------------------------------------------- offloaded optimizer
+
+    def _before_step(self, refresh: bool, length: int, st, rec) -> None:
+        """Writes back a finished deferred update (always before a refresh,
+        which reads the store), and makes a new interval wait until the
+        device buffer it overwrites has been copied out."""
+        if self._job is not None and (refresh or self._job.done()):
+            t0 = time.perf_counter()
+            self._job.result()
+            self.stall_s += time.perf_counter() - t0
+            self._job = None
+            self._scatter(st, rec)
+        if length == 1 and self._acc_free[self.cur_a] is not None:
+            st.wait_event(self._acc_free[self.cur_a])
+            self._acc_free[self.cur_a] = None
+
+    def _scatter(self, st, rec) -> None:
+        plan = self.plans[0][self.cur][self.cur_a]
+        with rec("scatter_weights"):
+            plan.scatter_weights(st)
+        ev = torch.cuda.Event()
+        ev.record(st)
+        self._ev_scatter = ev
+
+    def _host_update(self, scale: float, th: int, wait_copy, wait_scatter) -> None:
+        if wait_copy is not None:
+            wait_copy.synchronize()
+        if wait_scatter is not None:
+            wait_scatter.synchronize()  # the previous write-back has read wcols
+        t0 = time.perf_counter()
+        for q, ((n, m), k) in enumerate(zip(self.shapes, self.ks)):
+            P, M, V = self.store[q]
+            host_adam_unselected(self.host_acc[q], self.unsel_host[q], n, m, k, scale, P, M, V,
+                                 self.wcols[q], self.hp, th, layout=self.layout,
+                                 nthreads=self.host_threads)
+        self.host_update_s += time.perf_counter() - t0
+
+    def _hand_over(self, length: int, st, rec) -> None:
+        self.th += 1
+        scale = float(np.float32(1.0 / length))
+        if self._job is not None:  # the host is still busy with the previous interval
+            t0 = time.perf_counter()
+            self._job.result()
+            self.stall_s += time.perf_counter() - t0
+            self._job = None
+            self._scatter(st, rec)
+        a = self.cur_a
+        sels = self.sels[self.cur]
+        if not self.overlap:
+            with torch.cuda.stream(st):
+                for q in range(len(self.shapes)):
+                    self.host_acc[q].copy_(self.accs[a][q], non_blocking=True)
+                    self.unsel_host[q].copy_(sels[q].unsel_idx, non_blocking=True)
+            st.synchronize()
+            self._host_update(scale, self.th, None, None)
+            self._scatter(st, rec)
+            return
+        ev = torch.cuda.Event()
+        ev.record(st)
+        cs = self._copy_stream
+        cs.wait_event(ev)
+        with torch.cuda.stream(cs):
+            for q in range(len(self.shapes)):
+                self.host_acc[q].copy_(self.accs[a][q], non_blocking=True)
+                self.unsel_host[q].copy_(sels[q].unsel_idx, non_blocking=True)
+        copied = torch.cuda.Event()
+        copied.record(cs)
+        self._acc_free[a] = copied
+        self._job = self._pool.submit(self._host_update, scale, self.th, copied,
+                                      self._ev_scatter)
+        self.cur_a = 1 - a
+
+    def sync(self, stream=None) -> None:
+        """Finishes every outstanding deferred update and write-back and
+        synchronises the device (the state the synchronous order reaches)."""
+        st = stream if stream is not None else torch.cuda.current_stream(self.device)
+        if self._job is not None:
+            self._job.result()
+            self._job = None
+            self._scatter(st, _no_record)
+        torch.cuda.synchronize(self.device)
+
+    @property
+    def current_acc(self) -> List[torch.Tensor]:
+        """The packed buffers of the current interval (double-buffered when
+        the deferred update overlaps)."""
+        return self.accs[self.cur_a]
+
     def close(self) -> None:
+        if self._job is not None:
+            self._job.result()
+            self._job = None
+        if self._pool is not None:
+            self._pool.shutdown(wait=True)
         for row in self.plans:
-            for p in row:
-                p.close()
+            for pp in row:
+                for plan in pp:
+                    plan.close()

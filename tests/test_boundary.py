@@ -195,5 +195,8 @@ def test_plan_validation():
     assert LIB.zf_plan_create(arr2, 2, ctypes.byref(h)) == EINVAL
     assert LIB.zf_plan_colnorm(None, None) == EINVAL
     assert LIB.zf_plan_update(None, None, 1, 0, 1, 1, 1, 1, None) == EINVAL
+    hp = _lib.ZfAdamHparams(1e-5, 0.9, 0.999, 1e-8, 0.0)
+    assert LIB.zf_plan_update_zen(None, ctypes.byref(hp), 1, 0, 1, 4, 1.0, None, None) == EINVAL
+    assert _lib.ZEN_TOTALS_BYTES == 40
     assert LIB.zf_plan_device_bytes(None) == 0
     LIB.zf_plan_destroy(None)

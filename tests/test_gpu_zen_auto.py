@@ -1,0 +1,257 @@
+"""Parity of Zen-auto (the adaptive accumulation interval, Zero-stall
+Pipeline "Hyperparameter Auto-tuning") on the GPU with the oracle's
+ZenAutoOracle, through zf_plan_update_zen (channel-major plans):
+
+* per channel: the selected channels' squared gradient norms and the
+  accumulated channels' squared norms, within 1e-5 relative (both sides sum
+  exact squares in fp64 and round once to fp32, in different orders);
+* set-wide: the sums of channel norms within 1e-9 relative (fp64 sums of
+  ~10^3 terms in different orders), k and u exactly, and the trigger equal
+  wherever the oracle's comparison is not within 1e-9 of a tie;
+* the schedule it drives (interval lengths, ends, hand-over scale) and every
+  state, packed buffer, weight and hand-over bit for bit, as in the fixed
+  schedule.
+
+Shapes mix the vector path (n % 8 == 0, one and several row chunks per
+channel) with the element-wise path (n % 8 != 0), k = 0 matrices (m < 5 at
+10%), and ragged channel counts.  tau = 0 ends every interval after one
+step, tau = inf never triggers (the fixed schedule with S = S_max), and a
+tau between observed ratios makes the trigger fire mid-interval.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from tests._gpu import bits_np, f32_np, rel_close, same_bits
+from workloads import base_scales, derive_seed, gradient, jittered_scales, space_boundary
+
+pytestmark = pytest.mark.gpu
+
+zf = pytest.importorskip("paper_2505_12242_amd")
+
+SHAPES = [(264, 300), (4104, 70), (43, 77), (8192, 65), (16, 3), (128, 1000)]
+
+
+def _inputs(shapes, ratio, T, seed, dev):
+    """Channel-major device gradients per step and bf16 weights, plus the
+    logical host bit patterns the oracle takes."""
+    slots, host = [], []
+    for t in range(1, T + 1):
+        dslot, hslot = [], []
+        for q, (n, m) in enumerate(shapes):
+            k = O.k_from_ratio(ratio, m)
+            base = base_scales(m, 1.5, derive_seed(seed, q, "base"))
+            s = space_boundary(jittered_scales(base, 0.05, derive_seed(seed, q, "jit", t)), k)
+            g = gradient(n, m, s, derive_seed(seed, q, "grad", t), device=dev)
+            hslot.append(bits_np(g))
+            dslot.append(g.t().contiguous())
+        slots.append(dslot)
+        host.append(hslot)
+    weights, w0 = [], []
+    for q, (n, m) in enumerate(shapes):
+        g = torch.Generator().manual_seed(derive_seed(seed, q, "w") & 0x7fffffff)
+        w = (0.02 * torch.randn(n, m, generator=g)).to(torch.bfloat16)
+        w0.append(bits_np(w))
+        weights.append(w.t().contiguous().to(dev))
+    return slots, host, weights, w0
+
+
+def _oracle(shapes, w0, ratio, hp, R, S_max, tau):
+    orcs = [O.MatrixOracle(O.widen(w0[q]), w0[q], ratio, hp.lr, hp.beta1, hp.beta2, hp.eps,
+                           hp.weight_decay, R, S_max) for q in range(len(shapes))]
+    return O.ZenAutoOracle(orcs, R, S_max, tau)
+
+
+def _ratios(shapes, host, w0, ratio, hp, R, S_max):
+    """(mean accumulated norm) / (mean selected norm) at every step of the
+    fixed schedule (tau = inf), from the oracle."""
+    za = _oracle(shapes, w0, ratio, hp, R, S_max, math.inf)
+    out = []
+    for grads in host:
+        tot = za.step(grads)["totals"]
+        out.append((tot.sum_acc / tot.u) / (tot.sum_sel / tot.k))
+    return out
+
+
+def _host(t):
+    return t.t().contiguous().cpu()
+
+
+def fixed_ends(T, R, S_max):
+    """Interval ends when the trigger never fires: an interval starts at a
+    refresh or after an end and ends at S_max steps or before a refresh."""
+    ends, length, ended = [], 0, True
+    for t in range(1, T + 1):
+        length = 1 if ((t - 1) % R == 0 or ended) else length + 1
+        ended = length >= S_max or t % R == 0
+        ends.append(ended)
+    return ends
+
+
+def run_zen(shapes, ratio, R, S_max, tau, T, seed, host_in=None):
+    dev = torch.device("cuda")
+    hp = zf.AdamHparams(lr=1e-3)
+    slots, host, weights, w0 = host_in or _inputs(shapes, ratio, T, seed, dev)
+    runner = zf.SelectiveUpdateRunner(shapes, ratio, hp, R, S_max, slots, weights, device=dev,
+                                      layout=zf.CHANNEL_MAJOR, zen_tau=tau)
+    za = _oracle(shapes, w0, ratio, hp, R, S_max, tau)
+    ends = []
+    exact_stats = total_stats = 0
+    for t in range(1, T + 1):
+        print(f"# zen-auto tau={tau} step {t}", file=sys.stderr, flush=True)
+        kind = runner.step()
+        torch.cuda.synchronize()
+        ref = za.step(host[t - 1])
+        assert (kind.refresh, kind.step_in_interval, kind.interval_end) == \
+            (ref["refresh"], ref["step_in_interval"], ref["interval_end"]), t
+        got, want = runner.last_totals, ref["totals"]
+        assert (got.k_total, got.u_total) == (want.k, want.u)
+        assert abs(got.sum_sel - want.sum_sel) <= 1e-9 * want.sum_sel, (t, got, want)
+        assert abs(got.sum_acc - want.sum_acc) <= 1e-9 * want.sum_acc, (t, got, want)
+        lhs = want.sum_acc * want.k
+        rhs = tau * want.sum_sel * want.u
+        if want.k and want.u and (math.isinf(tau) or abs(lhs - rhs) > 1e-9 * max(lhs, rhs)):
+            assert got.trigger == want.trigger, (t, got, want)
+        for q in range(len(shapes)):
+            ssq, asq = ref["stats"][q]
+            for dev_t, ref_v, name in ((runner.sel_sq[q], ssq, "sel_sq"),
+                                       (runner.acc_sq[q], asq, "acc_sq")):
+                g = f32_np(dev_t)
+                ok, worst = rel_close(g, ref_v, 1e-5)
+                assert ok, (name, q, t, worst)
+                exact_stats += int(np.sum(g.view(np.uint32) == ref_v.view(np.uint32)))
+                total_stats += g.size
+            orc = za.orcs[q]
+            P, M, V = (_host(x).numpy() for x in runner.state[q])
+            for a, b, name in ((P, orc.P, "master"), (M, orc.M, "exp_avg"),
+                               (V, orc.V, "exp_avg_sq")):
+                assert same_bits(a, b), (name, q, t)
+            assert same_bits(_host(runner.acc[q]).numpy(), orc.A), ("acc", q, t)
+            assert same_bits(bits_np(runner.weights[q].t()), orc.W), ("weight", q, t)
+            if kind.interval_end:
+                assert same_bits(_host(runner.unpacked[q]).numpy(), ref["unpacked"][q]), \
+                    ("hand-over", q, t)
+        ends.append(kind.interval_end)
+    runner.close()
+    return ends, exact_stats, total_stats
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("tau", [0.0, math.inf])
+def test_zen_auto_extreme_thresholds(tau):
+    T, R, S_max = 9, 4, 3
+    ends, exact, total = run_zen(SHAPES, 0.1, R, S_max, tau, T, seed=11)
+    if tau == 0.0:
+        assert all(ends)
+    else:
+        # intervals of S_max steps, cut before each refresh (t = 5, 9)
+        assert ends == fixed_ends(T, R, S_max) == [False, False, True, True, False, False,
+                                                   True, True, False]
+    print(f"# stats bit-exact: {exact}/{total}", file=sys.stderr, flush=True)
+
+
+@pytest.mark.timeout(600)
+def test_zen_auto_threshold_between_observed_ratios():
+    """tau between the ratios the fixed schedule produces after one and after
+    several accumulated steps: the trigger fires mid-interval."""
+    T, R, S_max, ratio = 10, 16, 6, 0.1
+    dev = torch.device("cuda")
+    inputs = _inputs(SHAPES, ratio, T, 12, dev)
+    r = _ratios(SHAPES, inputs[1], inputs[3], ratio, zf.AdamHparams(lr=1e-3), R, S_max)
+    lo, hi = min(r[:2]), max(r[2:S_max])
+    assert hi > lo
+    tau = math.sqrt(lo * hi)
+    ends, _, _ = run_zen(SHAPES, ratio, R, S_max, tau, T, seed=12, host_in=inputs)
+    assert any(ends) and not all(ends)
+    # at least one interval ended by the trigger before reaching S_max
+    lengths, cur = [], 0
+    for e in ends:
+        cur += 1
+        if e:
+            lengths.append(cur)
+            cur = 0
+    assert any(L < S_max for L in lengths), lengths
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("ratio", [0.0, 1.0])
+def test_zen_auto_one_part_empty(ratio):
+    """k = 0 (nothing selected) or k = m (nothing accumulated): the trigger
+    never fires and the schedule is the fixed one."""
+    ends, _, _ = run_zen(SHAPES[:3], ratio, 4, 2, 0.0, 5, seed=13)
+    assert ends == fixed_ends(5, 4, 2) == [False, True, False, True, False]
+
+
+@pytest.mark.timeout(300)
+def test_zen_auto_deterministic():
+    dev = torch.device("cuda")
+    shapes = SHAPES[:4]
+    slots, host, weights, w0 = _inputs(shapes, 0.1, 2, 14, dev)
+    outs = []
+    for _ in range(2):
+        ws = [w.clone() for w in weights]
+        runner = zf.SelectiveUpdateRunner(shapes, 0.1, zf.AdamHparams(), 4, 4, slots, ws,
+                                          device=dev, layout=zf.CHANNEL_MAJOR, zen_tau=1.0)
+        tots = []
+        for _ in range(2):
+            runner.step()
+            tots.append(runner.zen_totals.cpu().numpy().tobytes())
+        outs.append((tots, [f32_np(x).tobytes() for x in runner.acc_sq + runner.sel_sq]))
+        runner.close()
+    assert outs[0] == outs[1]
+
+
+def _plan_buffers(layout, with_stats=True):
+    dev = torch.device("cuda")
+    n, m = 64, 100
+    k = O.k_from_ratio(0.1, m)
+    shp = (lambda r, c: (r, c)) if layout == zf.ROW_MAJOR else (lambda r, c: (c, r))
+    sel = zf.Selection(m, k, dev)
+    f = dict(dtype=torch.float32, device=dev)
+    return zf.MatrixBuffers(
+        grad=torch.zeros(*shp(n, m), dtype=torch.bfloat16, device=dev), k=k, sel=sel,
+        weight=torch.zeros(*shp(n, m), dtype=torch.bfloat16, device=dev),
+        master=torch.zeros(*shp(n, k), **f), exp_avg=torch.zeros(*shp(n, k), **f),
+        exp_avg_sq=torch.zeros(*shp(n, k), **f), acc=torch.zeros(*shp(n, m - k), **f),
+        norms=torch.zeros(m, **f), layout=layout,
+        sel_sq=torch.zeros(k, **f) if with_stats else None,
+        acc_sq=torch.zeros(m - k, **f) if with_stats else None)
+
+
+@pytest.mark.parametrize("layout,with_stats", [(0, True), (1, False)])
+def test_zen_auto_rejected_without_channel_major_statistics(layout, with_stats):
+    """Row-major plans and plans without statistics buffers refuse the call
+    (ZF_EINVAL) and enqueue nothing."""
+    plan = zf.Plan([_plan_buffers(layout, with_stats)])
+    plan.colnorm()
+    plan.topk_select()  # a valid selection, should anything run
+    totals = torch.zeros(5, dtype=torch.int64, device="cuda")
+    with pytest.raises(zf.ZfError, match="invalid argument"):
+        plan.update_zen(zf.AdamHparams(), 1, zf.STATES_INIT, 1, 4, 1.0, totals)
+    torch.cuda.synchronize()
+    assert not totals.any()
+    plan.close()
+
+
+def test_zen_auto_rejects_bad_arguments():
+    plan = zf.Plan([_plan_buffers(zf.CHANNEL_MAJOR)])
+    plan.colnorm()
+    plan.topk_select()  # zero gradient: the first k channels
+    totals = torch.zeros(5, dtype=torch.int64, device="cuda")
+    hp = zf.AdamHparams()
+    for args in ((hp, 1, zf.STATES_INIT, 1, 4, float("nan")),
+                 (hp, 1, zf.STATES_INIT, 1, 4, -1.0),
+                 (hp, 0, zf.STATES_INIT, 1, 4, 1.0),
+                 (hp, 1, zf.STATES_INIT, 5, 4, 1.0)):
+        with pytest.raises(zf.ZfError):
+            plan.update_zen(*args, totals)
+    plan.update_zen(hp, 1, zf.STATES_INIT, 1, 4, 1.0, totals)
+    torch.cuda.synchronize()
+    tot = zf.ZenTotals.from_bytes(totals.cpu().numpy().tobytes())
+    assert (tot.k_total, tot.u_total) == (10, 90)
+    assert tot.sum_sel == 0.0 and tot.sum_acc == 0.0 and tot.trigger  # 0 >= tau * 0
+    plan.close()
