@@ -56,6 +56,16 @@ def parse_args(argv=None):
     ap.add_argument("--zen-tau", type=float, default=None,
                     help="run Zen-auto (adaptive interval, at most --accum steps) with this "
                          "threshold instead of the fixed schedule (channel-major only)")
+    ap.add_argument("--offload", action="store_true",
+                    help="run the whole method with offloaded optimizer states: full-state "
+                         "store in pinned host memory (swapped at refreshes) and the deferred "
+                         "host update of the unselected columns at every interval end, "
+                         "overlapped with the following steps")
+    ap.add_argument("--no-overlap", action="store_true",
+                    help="with --offload: run the deferred update synchronously")
+    ap.add_argument("--host-threads", type=int, default=None,
+                    help="with --offload: host threads of the deferred update (default: "
+                         "min(16, cpu count))")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-steps", type=int, default=4)
     ap.add_argument("--calibration-copy-gib", type=float, default=1.0,
@@ -67,7 +77,7 @@ def parse_args(argv=None):
 # byte model: the bytes each kernel must move, per matrix
 # ---------------------------------------------------------------------------
 
-def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool) -> dict:
+def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool = False) -> dict:
     """Algorithmic HBM bytes of one step, by kernel.
 
     colnorm  2nm (read G) + 4m (write scores)          refresh steps
@@ -77,6 +87,8 @@ def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool) -> dict:
              6nu / 10nu: per unselected element G 2 + A 4 write (+ A 4 read
              after the interval's first step)
     unpack   4nu (read A) + 4nm (write the dense buffer)  interval ends
+             offloaded optimizer instead: 4nu (A read by the device -> host
+             copy) + 2nu (bf16 weights written back by the scatter)
     """
     out = {"colnorm": 0, "topk_select": 0, "update": 0, "unpack": 0}
     for (n, m), k in zip(shapes, ks):
@@ -86,7 +98,7 @@ def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool) -> dict:
             out["topk_select"] += 8 * m + 12 * ((m + 63) // 64)
         out["update"] += 28 * n * k + (6 if first else 10) * n * u
         if end:
-            out["unpack"] += 4 * n * u + 4 * n * m
+            out["unpack"] += (4 * n * u + 2 * n * u) if offload else (4 * n * u + 4 * n * m)
     return out
 
 
@@ -247,7 +259,9 @@ def main(argv=None) -> int:
             w = weights[q] if layout == zf.ROW_MAJOR else weights[q].t()
             weights0[q] = w.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
     runner = zf.SelectiveUpdateRunner(shapes, wl.ratio, hp, wl.refresh, wl.accum, grad_slots,
-                                      weights, device=dev, layout=layout, zen_tau=args.zen_tau)
+                                      weights, device=dev, layout=layout, zen_tau=args.zen_tau,
+                                      offload=args.offload, overlap=not args.no_overlap,
+                                      host_threads=args.host_threads)
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t0
     print(f"# setup {setup_s:.1f}s: {len(shapes)} matrices, {wl.params:,} params, "
@@ -266,6 +280,10 @@ def main(argv=None) -> int:
 
     for _ in range(args.warmup):
         runner.step()
+    if args.offload:
+        runner.sync()
+        runner.stall_s = runner.host_update_s = 0.0
+        th0 = runner.th
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
@@ -285,6 +303,8 @@ def main(argv=None) -> int:
     w0 = time.perf_counter()
     for _ in range(args.steps):
         kinds.append(runner.step(recorder=recorder))
+    if args.offload:
+        runner.sync()  # the last deferred update lands inside the timed region
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
 
@@ -293,7 +313,8 @@ def main(argv=None) -> int:
         per_kernel_ms.setdefault(name, []).append(a.elapsed_time(b))
     totals = {"colnorm": 0, "topk_select": 0, "update": 0, "unpack": 0}
     for kind in kinds:
-        b = step_bytes(shapes, ks, kind.refresh, kind.step_in_interval == 1, kind.interval_end)
+        b = step_bytes(shapes, ks, kind.refresh, kind.step_in_interval == 1, kind.interval_end,
+                       offload=args.offload)
         for key in totals:
             totals[key] += b[key]
     all_bytes = sum(totals.values())
@@ -343,6 +364,7 @@ def main(argv=None) -> int:
             "refresh_interval": wl.refresh,
             "accum_interval": wl.accum,
             "zen_auto_tau": args.zen_tau,
+            "offload": args.offload,
             "interval_ends": sum(1 for k in kinds if k.interval_end),
             "grad_slots": args.slots,
             "algorithmic_GB_per_step": round(all_bytes / args.steps / 1e9, 3),
@@ -360,6 +382,27 @@ def main(argv=None) -> int:
             "avg_launch_ms": round(upd_avg_ms, 4),
         },
     }
+    if args.offload:
+        # host side of the deferred update: per unselected element it reads
+        # the accumulated sum (4 B), reads and writes p, m, v (24 B) and
+        # writes the bf16 weight (2 B); the device -> host copy moves 4 B
+        intervals = runner.th - th0
+        unsel = sum(n * (m - k) for (n, m), k in zip(shapes, ks))
+        host_bytes = 30 * unsel * intervals
+        result["offload"] = {
+            "overlap": not args.no_overlap,
+            "host_threads": runner.host_threads,
+            "intervals": intervals,
+            "host_update_s": round(runner.host_update_s, 4),
+            "host_update_GB/s": round(host_bytes / runner.host_update_s / 1e9, 2)
+            if runner.host_update_s else None,
+            "host_params_per_s": round(unsel * intervals / runner.host_update_s, 1)
+            if runner.host_update_s else None,
+            "d2h_GB_per_interval": round(4 * unsel / 1e9, 3),
+            "stall_s": round(runner.stall_s, 4),
+            "stall_ms_per_step": round(runner.stall_s / args.steps * 1e3, 3),
+            "store": "pinned host memory, read in place by the swap kernels",
+        }
     if not args.no_cpu_baseline:
         print("# timing the CPU oracle on a sample ...", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(wl, shapes, ks, grad_slots, weights0,
