@@ -66,6 +66,9 @@ def parse_args(argv=None):
     ap.add_argument("--host-threads", type=int, default=None,
                     help="with --offload: host threads of the deferred update (default: "
                          "min(16, cpu count))")
+    ap.add_argument("--separate-handover", action="store_true",
+                    help="hand over with a separate unpack pass after the last update of an "
+                         "interval instead of fusing it into that update")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-steps", type=int, default=4)
     ap.add_argument("--calibration-copy-gib", type=float, default=1.0,
@@ -77,7 +80,8 @@ def parse_args(argv=None):
 # byte model: the bytes each kernel must move, per matrix
 # ---------------------------------------------------------------------------
 
-def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool = False) -> dict:
+def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool = False,
+               fused_handover: bool = False) -> dict:
     """Algorithmic HBM bytes of one step, by kernel.
 
     colnorm  2nm (read G) + 4m (write scores)          refresh steps
@@ -89,6 +93,10 @@ def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool 
     unpack   4nu (read A) + 4nm (write the dense buffer)  interval ends
              offloaded optimizer instead: 4nu (A read by the device -> host
              copy) + 2nu (bf16 weights written back by the scatter)
+             fused into the update (the interval's last step): the update
+             writes the hand-over instead of A -- the same 10nu (6nu) for the
+             unselected part -- plus 4nk zeros at the selected columns; A is
+             neither written nor read back
     """
     out = {"colnorm": 0, "topk_select": 0, "update": 0, "unpack": 0}
     for (n, m), k in zip(shapes, ks):
@@ -98,7 +106,12 @@ def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool 
             out["topk_select"] += 8 * m + 12 * ((m + 63) // 64)
         out["update"] += 28 * n * k + (6 if first else 10) * n * u
         if end:
-            out["unpack"] += (4 * n * u + 2 * n * u) if offload else (4 * n * u + 4 * n * m)
+            if offload:
+                out["unpack"] += 4 * n * u + 2 * n * u
+            elif fused_handover:
+                out["update"] += 4 * n * k
+            else:
+                out["unpack"] += 4 * n * u + 4 * n * m
     return out
 
 
@@ -261,7 +274,9 @@ def main(argv=None) -> int:
     runner = zf.SelectiveUpdateRunner(shapes, wl.ratio, hp, wl.refresh, wl.accum, grad_slots,
                                       weights, device=dev, layout=layout, zen_tau=args.zen_tau,
                                       offload=args.offload, overlap=not args.no_overlap,
-                                      host_threads=args.host_threads)
+                                      host_threads=args.host_threads,
+                                      fuse_handover=not args.separate_handover)
+    fused = runner.keep_unpacked and runner.fuse_handover and args.zen_tau is None
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t0
     print(f"# setup {setup_s:.1f}s: {len(shapes)} matrices, {wl.params:,} params, "
@@ -314,7 +329,7 @@ def main(argv=None) -> int:
     totals = {"colnorm": 0, "topk_select": 0, "update": 0, "unpack": 0}
     for kind in kinds:
         b = step_bytes(shapes, ks, kind.refresh, kind.step_in_interval == 1, kind.interval_end,
-                       offload=args.offload)
+                       offload=args.offload, fused_handover=fused)
         for key in totals:
             totals[key] += b[key]
     all_bytes = sum(totals.values())
@@ -366,6 +381,9 @@ def main(argv=None) -> int:
             "zen_auto_tau": args.zen_tau,
             "offload": args.offload,
             "interval_ends": sum(1 for k in kinds if k.interval_end),
+            "handover": "fused into the interval's last update" if fused else
+                        ("device -> host copy of the packed buffer" if args.offload
+                         else "separate unpack pass"),
             "grad_slots": args.slots,
             "algorithmic_GB_per_step": round(all_bytes / args.steps / 1e9, 3),
         },

@@ -256,6 +256,27 @@ zf_status zf_update_fused(const uint16_t* grad, int64_t n, int64_t m, int64_t ld
                           int64_t step_in_interval, int64_t accum_interval,
                           zf_stream stream);
 
+/* zf_update_fused for the last step of an accumulation interval with the
+ * hand-over (zf_unpack) fused in: the same Adam step of the selected
+ * columns, and for every unselected slot u (column j = unsel_idx[u]):
+ *   out[i][j] = scale * G[i][j]                  if step_in_interval == 1,
+ *   out[i][j] = scale * (A[i][u] + G[i][j])      otherwise
+ * (the same two fp32 operations, in the same order, as zf_pack_accumulate
+ * followed by zf_unpack), out[i][j] = +0.0 for selected j.  The packed
+ * buffer A is only read: it keeps the sums of the interval's earlier steps
+ * (the next interval overwrites it).  This moves 8 bytes per unselected
+ * element less than the two separate passes (A is neither written nor read
+ * back).  out: fp32 n x m in `layout` with row stride ld_out, disjoint from
+ * every other buffer of the call.  Other arguments as in zf_update_fused. */
+zf_status zf_update_fused_handover(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
+                                   int32_t layout, const zf_selection* sel, int64_t k,
+                                   float* master, float* exp_avg, float* exp_avg_sq,
+                                   int64_t ld_state, uint16_t* weight, int64_t ld_weight,
+                                   const zf_adam_hparams* hp, int64_t step, int32_t mode,
+                                   const zf_state_source* src, const float* acc, int64_t ld_acc,
+                                   int64_t step_in_interval, int64_t accum_interval, float scale,
+                                   float* out, int64_t ld_out, zf_stream stream);
+
 /* ---- a6: hand-over ------------------------------------------------------ */
 
 /* out[i][j] = +0.0 for selected j, scale * A[i][u] for the unselected column
@@ -368,6 +389,13 @@ zf_status zf_plan_update(zf_plan* plan, const zf_adam_hparams* hp, int64_t step,
 
 /* zf_unpack over every matrix into its `unpacked` buffer. */
 zf_status zf_plan_unpack(zf_plan* plan, float scale, zf_stream stream);
+
+/* zf_update_fused_handover over every matrix (out = its `unpacked` buffer):
+ * the last step of an interval in one pass, Adam + final accumulation +
+ * hand-over. */
+zf_status zf_plan_update_handover(zf_plan* plan, const zf_adam_hparams* hp, int64_t step,
+                                  int32_t mode, int64_t step_in_interval, int64_t accum_interval,
+                                  float scale, zf_stream stream);
 
 /* zf_scatter_weights over every matrix (weight_cols of each descriptor). */
 zf_status zf_plan_scatter_weights(zf_plan* plan, zf_stream stream);

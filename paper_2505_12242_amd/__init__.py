@@ -33,5 +33,6 @@ from ._lib import (  # noqa: F401
     topk_select,
     unpack,
     update_fused,
+    update_fused_handover,
 )
 from .runner import SelectiveUpdateRunner, StepKind, schedule  # noqa: F401

@@ -85,6 +85,10 @@ SIGNATURES = [
      [c_vp, c_i64, c_i64, c_i64, c_i32, ctypes.POINTER(ZfSelection), c_i64, c_vp, c_vp, c_vp, c_i64,
       c_vp, c_i64, ctypes.POINTER(ZfAdamHparams), c_i64, c_i32, ctypes.POINTER(ZfStateSource),
       c_vp, c_i64, c_i64, c_i64, c_vp]),
+    ("zf_update_fused_handover", ctypes.c_int,
+     [c_vp, c_i64, c_i64, c_i64, c_i32, ctypes.POINTER(ZfSelection), c_i64, c_vp, c_vp, c_vp, c_i64,
+      c_vp, c_i64, ctypes.POINTER(ZfAdamHparams), c_i64, c_i32, ctypes.POINTER(ZfStateSource),
+      c_vp, c_i64, c_i64, c_i64, c_flt, c_vp, c_i64, c_vp]),
     ("zf_unpack", ctypes.c_int,
      [c_vp, c_i64, ctypes.POINTER(ZfSelection), c_i64, c_i64, c_i64, c_i32, c_flt, c_vp, c_i64,
       c_vp]),
@@ -102,6 +106,8 @@ SIGNATURES = [
     ("zf_scatter_weights", ctypes.c_int,
      [c_vp, c_i64, ctypes.POINTER(ZfSelection), c_i64, c_i64, c_i64, c_i32, c_vp, c_i64, c_vp]),
     ("zf_plan_scatter_weights", ctypes.c_int, [c_vp, c_vp]),
+    ("zf_plan_update_handover", ctypes.c_int,
+     [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, c_i32, c_i64, c_i64, c_flt, c_vp]),
     ("zf_plan_update_zen", ctypes.c_int,
      [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, c_i32, c_i64, c_i64, c_dbl, c_vp, c_vp]),
 ]
@@ -364,6 +370,32 @@ def update_fused(grad, sel: Selection, master, exp_avg, exp_avg_sq, weight, hp: 
         accum_interval, _stream(stream)))
 
 
+def update_fused_handover(grad, sel: Selection, master, exp_avg, exp_avg_sq, weight,
+                          hp: AdamHparams, step: int, acc, step_in_interval: int,
+                          accum_interval: int, scale: float, out: Optional[torch.Tensor] = None,
+                          mode: int = STATES_INPLACE, src: Optional[StateSource] = None,
+                          layout: int = ROW_MAJOR, stream=None) -> torch.Tensor:
+    """The last step of an interval in one pass: Adam on the selected columns
+    and out = scale * (A + G) at the unselected ones, +0.0 at the selected
+    (zf_update_fused_handover); A is only read."""
+    n, m = _logical(grad, layout)
+    ldg = _mat(grad, torch.bfloat16, "grad")
+    lds = _states(n, sel.k, master, exp_avg, exp_avg_sq, layout)
+    ldw = _lmat(weight, torch.bfloat16, "weight", layout, n, m)
+    lda = _lmat(acc, torch.float32, "acc", layout, n, m - sel.k)
+    if out is None:
+        out = torch.empty(*_stored(layout, n, m), dtype=torch.float32, device=grad.device)
+    ldo = _lmat(out, torch.float32, "out", layout, n, m)
+    c_sel, c_hp = sel.as_c(), hp.as_c()
+    c_src = src.as_c() if src is not None else None
+    _check("zf_update_fused_handover", LIB.zf_update_fused_handover(
+        _ptr(grad), n, m, ldg, layout, ctypes.byref(c_sel), sel.k, _ptr(master), _ptr(exp_avg),
+        _ptr(exp_avg_sq), lds, _ptr(weight), ldw, ctypes.byref(c_hp), step, mode,
+        ctypes.byref(c_src) if c_src is not None else None, _ptr(acc), lda, step_in_interval,
+        accum_interval, float(scale), _ptr(out), ldo, _stream(stream)))
+    return out
+
+
 def unpack(acc, sel: Selection, scale: float = 1.0, out: Optional[torch.Tensor] = None,
            layout: int = ROW_MAJOR, stream=None) -> torch.Tensor:
     m = sel.m
@@ -531,6 +563,16 @@ class Plan:
 
     def unpack(self, scale: float, stream=None) -> None:
         _check("zf_plan_unpack", LIB.zf_plan_unpack(self._h, float(scale), _stream(stream)))
+
+    def update_handover(self, hp: AdamHparams, step: int, mode: int, step_in_interval: int,
+                        accum_interval: int, scale: float, stream=None) -> None:
+        """The last step of an interval with the hand-over fused in
+        (zf_plan_update_handover): every matrix's `unpacked` buffer receives
+        scale * the final sums; the packed buffers are only read."""
+        c_hp = hp.as_c()
+        _check("zf_plan_update_handover", LIB.zf_plan_update_handover(
+            self._h, ctypes.byref(c_hp), step, mode, step_in_interval, accum_interval,
+            float(scale), _stream(stream)))
 
     def scatter_weights(self, stream=None) -> None:
         """W[:, unsel] = weight_cols of every matrix (zf_plan_scatter_weights)."""

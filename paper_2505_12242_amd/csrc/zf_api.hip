@@ -375,10 +375,11 @@ int64_t unpack_grid(const DevMat& d) {
 
 hipError_t launch_update_any(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
                              int32_t mode, int32_t first, bool adam, bool pack, int32_t layout,
-                             hipStream_t s) {
+                             hipStream_t s, bool handover = false, float scale = 1.0f) {
   return layout == zf::kChannelMajor
-             ? zf::launch_cm_update(t, one, blocks, c, mode, first, adam, pack, nullptr, s)
-             : zf::launch_update(t, one, blocks, c, mode, first, adam, pack, s);
+             ? zf::launch_cm_update(t, one, blocks, c, mode, first, adam, pack, nullptr, handover,
+                                    scale, s)
+             : zf::launch_update(t, one, blocks, c, mode, first, adam, pack, handover, scale, s);
 }
 
 hipError_t launch_unpack_any(const Table& t, const DevMat& one, int64_t blocks, float scale,
@@ -392,7 +393,9 @@ zf_status run_update(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad
                      float* exp_avg_sq, int64_t ld_state, uint16_t* weight, int64_t ld_weight,
                      const zf_adam_hparams* hp, int64_t step, int32_t mode,
                      const zf_state_source* src, float* acc, int64_t ld_acc, int64_t sii,
-                     int64_t S, bool adam, bool pack, zf_stream stream) {
+                     int64_t S, bool adam, bool pack, zf_stream stream, float* out = nullptr,
+                     int64_t ld_out = 0, float scale = 1.0f) {
+  const bool handover = out != nullptr;
   if (!layout_ok(layout) || !shape_ok(n, m, k) ||
       !mat_ok(grad, ext(layout, n, m), ld_grad, 2))
     return ZF_EINVAL;
@@ -427,14 +430,28 @@ zf_status run_update(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad
         return ZF_EINVAL;
     }
   }
-  if ((!adam || k == 0) && (!pack || k == m)) return ZF_OK;  // no column to touch
+  if (handover) {
+    // the hand-over buffer is written: it must not overlap anything the pass reads or writes
+    const Ext eo = ext(layout, n, m);
+    if (!mat_ok(out, eo, ld_out, 4)) return ZF_EINVAL;
+    const Span o = span(out, eo, ld_out, 4);
+    const Ext es = ext(layout, n, k);
+    if (overlaps(o, g) || overlaps(o, span(acc, ext(layout, n, m - k), ld_acc, 4)) ||
+        overlaps(o, span(master, es, ld_state, 4)) || overlaps(o, span(exp_avg, es, ld_state, 4)) ||
+        overlaps(o, span(exp_avg_sq, es, ld_state, 4)) ||
+        overlaps(o, span(weight, ext(layout, n, m), ld_weight, 2)) || store_overlaps(d, o))
+      return ZF_EINVAL;
+    d.out = out;
+    d.ld_out = ld_out;
+  }
+  if (!handover && (!adam || k == 0) && (!pack || k == m)) return ZF_OK;  // no column to touch
   finish_geometry(d, 256, pick_update_rows({{n, m}}));
   if (layout == zf::kRowMajor && !rm_strides_ok(d)) return ZF_EINVAL;
   const int64_t blocks = update_grid(d);
   if (blocks == 0) return ZF_OK;
   const hipError_t e = launch_update_any(single_table(), d, blocks, c, adam ? mode : 0,
                                          sii == 1 ? 1 : 0, adam, pack, layout,
-                                         as_stream(stream));
+                                         as_stream(stream), handover, scale);
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
@@ -553,6 +570,21 @@ zf_status zf_update_fused(const uint16_t* grad, int64_t n, int64_t m, int64_t ld
                     accum_interval, true, true, stream);
 }
 
+zf_status zf_update_fused_handover(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
+                                   int32_t layout, const zf_selection* sel, int64_t k,
+                                   float* master, float* exp_avg, float* exp_avg_sq,
+                                   int64_t ld_state, uint16_t* weight, int64_t ld_weight,
+                                   const zf_adam_hparams* hp, int64_t step, int32_t mode,
+                                   const zf_state_source* src, const float* acc, int64_t ld_acc,
+                                   int64_t step_in_interval, int64_t accum_interval, float scale,
+                                   float* out, int64_t ld_out, zf_stream stream) {
+  if (out == nullptr && n > 0 && m > 0) return ZF_EINVAL;
+  if (out == nullptr) return ZF_OK;
+  return run_update(grad, n, m, ld_grad, layout, sel, k, master, exp_avg, exp_avg_sq, ld_state,
+                    weight, ld_weight, hp, step, mode, src, const_cast<float*>(acc), ld_acc,
+                    step_in_interval, accum_interval, true, true, stream, out, ld_out, scale);
+}
+
 zf_status zf_unpack(const float* acc, int64_t ld_acc, const zf_selection* sel, int64_t k,
                     int64_t n, int64_t m, int32_t layout, float scale, float* out, int64_t ld_out,
                     zf_stream stream) {
@@ -625,7 +657,7 @@ struct zf_plan {
   int64_t blk_cn = 0, blk_fin = 0, blk_top = 0, blk_up = 0, blk_unp = 0, blk_zen = 0;
   int64_t k_total = 0, u_total = 0;
   bool can_colnorm = true, can_topk = true, can_adam = true, can_remap = true, can_pack = true,
-       can_unpack = true, can_zen = true, can_scatter = true;
+       can_unpack = true, can_zen = true, can_scatter = true, can_handover = true;
 };
 
 namespace {
@@ -676,6 +708,18 @@ zf_status check_plan_matrix(const zf_matrix& x, zf_plan& p) {
   p.can_unpack = p.can_unpack && have_mask && mat_ok(x.acc, ea, x.ld_acc, 4) &&
                  mat_ok(x.unpacked, eg, x.ld_unpacked, 4) &&
                  !overlaps(span(x.acc, ea, x.ld_acc, 4), span(x.unpacked, eg, x.ld_unpacked, 4));
+  {
+    // fused hand-over: the unpacked buffer must be disjoint from everything the update touches
+    const Span o = span(x.unpacked, eg, x.ld_unpacked, 4);
+    const Ext es = ext(L, n, k);
+    p.can_handover = p.can_handover && mat_ok(x.unpacked, eg, x.ld_unpacked, 4) &&
+                     (n * m == 0 || x.unpacked != nullptr) && !overlaps(o, g) &&
+                     !overlaps(o, span(x.acc, ea, x.ld_acc, 4)) &&
+                     !overlaps(o, span(x.master, es, x.ld_state, 4)) &&
+                     !overlaps(o, span(x.exp_avg, es, x.ld_state, 4)) &&
+                     !overlaps(o, span(x.exp_avg_sq, es, x.ld_state, 4)) &&
+                     !overlaps(o, span(x.weight, eg, x.ld_weight, 2)) && !store_overlaps(d, o);
+  }
   p.can_scatter = p.can_scatter && have_mask && mat_ok(x.weight_cols, ea, x.ld_weight_cols, 2) &&
                   (n * (m - k) == 0 || device_accessible(x.weight_cols)) &&
                   mat_ok(x.weight, eg, x.ld_weight, 2) &&
@@ -873,6 +917,23 @@ zf_status zf_plan_unpack(zf_plan* p, float scale, zf_stream stream) {
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
+zf_status zf_plan_update_handover(zf_plan* p, const zf_adam_hparams* hp, int64_t step,
+                                  int32_t mode, int64_t step_in_interval, int64_t accum_interval,
+                                  float scale, zf_stream stream) {
+  if (p == nullptr || !p->can_adam || !p->can_pack || !p->can_handover) return ZF_EINVAL;
+  if (!hparams_ok(hp) || step < 1) return ZF_EINVAL;
+  if (mode != zf::kInplace && mode != zf::kRemap && mode != zf::kInit) return ZF_EINVAL;
+  if (mode == zf::kRemap && !p->can_remap) return ZF_EINVAL;
+  if (accum_interval < 1 || step_in_interval < 1 || step_in_interval > accum_interval)
+    return ZF_EINVAL;
+  const AdamK c = adam_consts(*hp, step);
+  const Table t{p->d_mats, p->d_off_up, p->nmats};
+  const hipError_t e = launch_update_any(t, p->mats[0], p->blk_up, c, mode,
+                                         step_in_interval == 1 ? 1 : 0, true, true, p->layout,
+                                         as_stream(stream), true, scale);
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
 zf_status zf_plan_scatter_weights(zf_plan* p, zf_stream stream) {
   if (p == nullptr || !p->can_scatter) return ZF_EINVAL;
   const Table t{p->d_mats, p->d_off_unp, p->nmats};
@@ -895,7 +956,8 @@ zf_status zf_plan_update_zen(zf_plan* p, const zf_adam_hparams* hp, int64_t step
   const hipStream_t s = as_stream(stream);
   const Table t{p->d_mats, p->d_off_up, p->nmats};
   hipError_t e = zf::launch_cm_update(t, p->mats[0], p->blk_up, c, mode,
-                                      step_in_interval == 1 ? 1 : 0, true, true, p->d_zs, s);
+                                      step_in_interval == 1 ? 1 : 0, true, true, p->d_zs, false,
+                                      1.0f, s);
   if (e != hipSuccess) return hip_fail(e);
   const Table tz{p->d_mats, p->d_off_zen, p->nmats};
   e = zf::launch_zen_finalize(tz, p->mats[0], p->blk_zen, p->d_zs, p->d_zb, s);

@@ -122,16 +122,20 @@ hipError_t launch_colnorm(const Table& t, const DevMat& one, int64_t blocks,
                           const Table& tf, int64_t fin_blocks, double* ws, hipStream_t s);
 hipError_t launch_topk(const Table& t, const DevMat& one, int64_t blocks, hipStream_t s);
 hipError_t launch_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
-                         int32_t mode, int32_t first, bool adam, bool pack, hipStream_t s);
+                         int32_t mode, int32_t first, bool adam, bool pack, bool handover,
+                         float scale, hipStream_t s);
 hipError_t launch_unpack(const Table& t, const DevMat& one, int64_t blocks, float scale,
                          hipStream_t s);
 
 // Channel-major kernels (zf_kernels_cm.hip).
 hipError_t launch_cm_colnorm(const Table& t, const DevMat& one, int64_t blocks, hipStream_t s);
 // zs != nullptr: fused Adam + pack that also writes the Zen-auto partials.
+// handover: the last step of an interval with the hand-over fused in (the
+// `out` buffer receives scale * the final sums, +0.0 for selected columns;
+// the packed buffer is not written).
 hipError_t launch_cm_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
                             int32_t mode, int32_t first, bool adam, bool pack, double* zs,
-                            hipStream_t s);
+                            bool handover, float scale, hipStream_t s);
 hipError_t launch_cm_unpack(const Table& t, const DevMat& one, int64_t blocks, float scale,
                             hipStream_t s);
 

@@ -300,10 +300,14 @@ __device__ __forceinline__ TileSlots tile_slots(const DevMat& d, int64_t c0) {
   return ts;
 }
 
-// Pack lane: A[i][u] (+)= G[i][j] over the block's rows.
-template <bool FIRST>
+// Pack lane: A[i][u] (+)= G[i][j] over the block's rows.  HAND (last step
+// of an interval, fused hand-over): scale * the new sum goes to D[i][j] (rD,
+// vD, sD) and A is not written.
+template <bool FIRST, bool HAND = false>
 __device__ __forceinline__ void pack_rows(rsrc_t rG, uint32_t vG, uint32_t sG, rsrc_t rA,
-                                          uint32_t vA, uint32_t sA, int32_t rows) {
+                                          uint32_t vA, uint32_t sA, int32_t rows,
+                                          rsrc_t rD = rsrc_t(), uint32_t vD = 0, uint32_t sD = 0,
+                                          float scale = 1.0f) {
   int32_t i = 0;
   for (; i + kRowBatch <= rows; i += kRowBatch) {
     uint16_t gb[kRowBatch];
@@ -320,12 +324,16 @@ __device__ __forceinline__ void pack_rows(rsrc_t rG, uint32_t vG, uint32_t sG, r
       for (int b = 0; b < kRowBatch; ++b) a[b] = widen_bf16(gb[b]);
     }
 #pragma unroll
-    for (int b = 0; b < kRowBatch; ++b) buf_put_f32(a[b], rA, vA, (i + b) * sA);
+    for (int b = 0; b < kRowBatch; ++b) {
+      if constexpr (HAND) buf_put_f32(a[b] * scale, rD, vD, (i + b) * sD);
+      else buf_put_f32(a[b], rA, vA, (i + b) * sA);
+    }
   }
   for (; i < rows; ++i) {
     const float g = widen_bf16(buf_u16(rG, vG, i * sG));
-    if constexpr (FIRST) buf_put_f32(g, rA, vA, i * sA);
-    else buf_put_f32(buf_f32(rA, vA, i * sA) + g, rA, vA, i * sA);
+    const float a = FIRST ? g : buf_f32(rA, vA, i * sA) + g;
+    if constexpr (HAND) buf_put_f32(a * scale, rD, vD, i * sD);
+    else buf_put_f32(a, rA, vA, i * sA);
   }
 }
 
@@ -427,11 +435,12 @@ __device__ __forceinline__ void adam_rows(const AdamSrc& a, rsrc_t rG, uint32_t 
   }
 }
 
-template <bool BATCHED, bool ADAM, bool PACK>
+template <bool BATCHED, bool ADAM, bool PACK, bool HAND>
 __global__ __launch_bounds__(kThreads) void update_kernel(const DevMat* __restrict__ mats,
                                                           const int64_t* __restrict__ off,
                                                           int32_t nmats, DevMat one, AdamK c,
-                                                          int32_t mode, int32_t first) {
+                                                          int32_t mode, int32_t first,
+                                                          float scale) {
   int64_t local;
   const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, local);
   const int64_t cblk = local % d.up_cb;
@@ -470,8 +479,15 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const DevMat* __restri
       const uint32_t vG = j * 2u;
       const rsrc_t rA = rows_rsrc(d.acc, i0, i1, d.ld_acc, d.m - d.k);
       const uint32_t sA = static_cast<uint32_t>(d.ld_acc * 4);
-      if (first) pack_rows<true>(rG, vG, sG, rA, u * 4u, sA, rows);
-      else pack_rows<false>(rG, vG, sG, rA, u * 4u, sA, rows);
+      if constexpr (HAND) {
+        const rsrc_t rD = rows_rsrc(d.out, i0, i1, d.ld_out, d.m);
+        const uint32_t sD = static_cast<uint32_t>(d.ld_out * 4);
+        if (first) pack_rows<true, true>(rG, vG, sG, rA, u * 4u, sA, rows, rD, j * 4u, sD, scale);
+        else pack_rows<false, true>(rG, vG, sG, rA, u * 4u, sA, rows, rD, j * 4u, sD, scale);
+      } else {
+        if (first) pack_rows<true>(rG, vG, sG, rA, u * 4u, sA, rows);
+        else pack_rows<false>(rG, vG, sG, rA, u * 4u, sA, rows);
+      }
     }
     return;
   }
@@ -526,6 +542,12 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const DevMat* __restri
     a.rSP = rows_rsrc(d.prev_P, i0, i1, d.ld_prev, d.m);
     a.rSM = rows_rsrc(d.prev_M, i0, i1, d.ld_prev, d.m);
     a.rSV = rows_rsrc(d.prev_V, i0, i1, d.ld_prev, d.m);
+  }
+  if constexpr (HAND) {
+    // the hand-over buffer is +0.0 at a selected column
+    const rsrc_t rD = rows_rsrc(d.out, i0, i1, d.ld_out, d.m);
+    const uint32_t sD = static_cast<uint32_t>(d.ld_out * 4);
+    for (int32_t i = 0; i < rows; ++i) buf_put_f32(0.0f, rD, j * 4u, i * sD);
   }
   if (mode == kInplace) adam_rows<kSrcInplace>(a, rG, sG, c, rows);
   else if (mode == kRemap) {
@@ -622,25 +644,28 @@ hipError_t launch_topk(const Table& t, const DevMat& one, int64_t blocks, hipStr
   return hipGetLastError();
 }
 
-template <bool ADAM, bool PACK>
+template <bool ADAM, bool PACK, bool HAND>
 static void launch_update_t(const Table& t, const DevMat& one, dim3 grid, const AdamK& c,
-                            int32_t mode, int32_t first, hipStream_t s) {
+                            int32_t mode, int32_t first, float scale, hipStream_t s) {
   if (t.mats != nullptr)
-    hipLaunchKernelGGL((update_kernel<true, ADAM, PACK>), grid, dim3(kThreads), 0, s, t.mats,
-                       t.off, t.nmats, one, c, mode, first);
+    hipLaunchKernelGGL((update_kernel<true, ADAM, PACK, HAND>), grid, dim3(kThreads), 0, s,
+                       t.mats, t.off, t.nmats, one, c, mode, first, scale);
   else
-    hipLaunchKernelGGL((update_kernel<false, ADAM, PACK>), grid, dim3(kThreads), 0, s, t.mats,
-                       t.off, t.nmats, one, c, mode, first);
+    hipLaunchKernelGGL((update_kernel<false, ADAM, PACK, HAND>), grid, dim3(kThreads), 0, s,
+                       t.mats, t.off, t.nmats, one, c, mode, first, scale);
 }
 
 hipError_t launch_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
-                         int32_t mode, int32_t first, bool adam, bool pack, hipStream_t s) {
+                         int32_t mode, int32_t first, bool adam, bool pack, bool handover,
+                         float scale, hipStream_t s) {
   (void)hipGetLastError();
   if (blocks <= 0) return hipSuccess;
   const dim3 grid(static_cast<uint32_t>(blocks));
-  if (adam && pack) launch_update_t<true, true>(t, one, grid, c, mode, first, s);
-  else if (adam) launch_update_t<true, false>(t, one, grid, c, mode, first, s);
-  else if (pack) launch_update_t<false, true>(t, one, grid, c, mode, first, s);
+  if (handover && !(adam && pack)) return hipErrorInvalidValue;
+  if (handover) launch_update_t<true, true, true>(t, one, grid, c, mode, first, scale, s);
+  else if (adam && pack) launch_update_t<true, true, false>(t, one, grid, c, mode, first, 1.0f, s);
+  else if (adam) launch_update_t<true, false, false>(t, one, grid, c, mode, first, 1.0f, s);
+  else if (pack) launch_update_t<false, true, false>(t, one, grid, c, mode, first, 1.0f, s);
   return hipGetLastError();
 }
 

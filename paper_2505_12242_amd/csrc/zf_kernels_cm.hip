@@ -228,8 +228,13 @@ __device__ __forceinline__ void cm_adam_elem(rsrc_t rG, rsrc_t rP, rsrc_t rM, rs
   }
 }
 
-template <bool FIRST, int VPT, bool STATS>
-__device__ __forceinline__ void cm_pack_vec(rsrc_t rG, rsrc_t rA, double& ss) {
+// HAND (the last step of an interval, fused hand-over): the new sums are not
+// stored back; scale * sum goes to the channel's row of the hand-over
+// buffer (rOut) instead -- the same two fp32 operations as accumulating and
+// then unpacking.
+template <bool FIRST, int VPT, bool STATS, bool HAND = false>
+__device__ __forceinline__ void cm_pack_vec(rsrc_t rG, rsrc_t rA, double& ss,
+                                            rsrc_t rOut = rsrc_t(), float scale = 1.0f) {
   const int tid = threadIdx.x;
   u32x4 gv[VPT];
   float a[VPT][kGroup];
@@ -246,18 +251,26 @@ __device__ __forceinline__ void cm_pack_vec(rsrc_t rG, rsrc_t rA, double& ss) {
 #pragma unroll
     for (int i = 0; i < kGroup; ++i) a[q][i] = FIRST ? g[i] : a[q][i] + g[i];
     if constexpr (STATS) sum_squares8(a[q], ss);
-    f32x8_store<FIRST ? kAuxWO : kAuxRMW>(rA, group_elem(q, tid) * 4, a[q]);
+    if constexpr (HAND) {
+#pragma unroll
+      for (int i = 0; i < kGroup; ++i) a[q][i] = a[q][i] * scale;
+      f32x8_store<kAuxWO>(rOut, group_elem(q, tid) * 4, a[q]);
+    } else {
+      f32x8_store<FIRST ? kAuxWO : kAuxRMW>(rA, group_elem(q, tid) * 4, a[q]);
+    }
   }
 }
 
-template <bool FIRST, bool STATS>
-__device__ __forceinline__ void cm_pack_elem(rsrc_t rG, rsrc_t rA, int64_t len, double& ss) {
+template <bool FIRST, bool STATS, bool HAND = false>
+__device__ __forceinline__ void cm_pack_elem(rsrc_t rG, rsrc_t rA, int64_t len, double& ss,
+                                             rsrc_t rOut = rsrc_t(), float scale = 1.0f) {
   for (int64_t e = threadIdx.x; e < len; e += kThreads) {
     const uint32_t o = static_cast<uint32_t>(e);
     const float g = widen_bf16(buf_u16<kAuxRO>(rG, o * 2, 0));
     const float a = FIRST ? g : buf_f32<kAuxRMW>(rA, o * 4, 0) + g;
     if constexpr (STATS) ss = __builtin_fma(static_cast<double>(a), static_cast<double>(a), ss);
-    buf_put_f32<FIRST ? kAuxWO : kAuxRMW>(a, rA, o * 4, 0);
+    if constexpr (HAND) buf_put_f32<kAuxWO>(a * scale, rOut, o * 4, 0);
+    else buf_put_f32<FIRST ? kAuxWO : kAuxRMW>(a, rA, o * 4, 0);
   }
 }
 
@@ -270,10 +283,23 @@ __device__ __forceinline__ void cm_adam_vec_any(int vpt, rsrc_t rG, rsrc_t rP, r
   else cm_adam_vec<SRC, 1, STATS>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss);
 }
 
-template <bool FIRST, bool STATS>
-__device__ __forceinline__ void cm_pack_vec_any(int vpt, rsrc_t rG, rsrc_t rA, double& ss) {
-  if (vpt >= 2) cm_pack_vec<FIRST, kCmVpt, STATS>(rG, rA, ss);
-  else cm_pack_vec<FIRST, 1, STATS>(rG, rA, ss);
+template <bool FIRST, bool STATS, bool HAND = false>
+__device__ __forceinline__ void cm_pack_vec_any(int vpt, rsrc_t rG, rsrc_t rA, double& ss,
+                                                rsrc_t rOut = rsrc_t(), float scale = 1.0f) {
+  if (vpt >= 2) cm_pack_vec<FIRST, kCmVpt, STATS, HAND>(rG, rA, ss, rOut, scale);
+  else cm_pack_vec<FIRST, 1, STATS, HAND>(rG, rA, ss, rOut, scale);
+}
+
+// HAND: a selected channel's row of the hand-over buffer is +0.0.
+__device__ __forceinline__ void cm_zero_rows(const DevMat& d, rsrc_t rOut, int64_t len) {
+  if (d.vec) {
+    const float z[kGroup] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int64_t g = threadIdx.x; g * kGroup < len; g += kThreads)
+      f32x8_store<kAuxWO>(rOut, static_cast<uint32_t>(g * kGroup * 4), z);
+  } else {
+    for (int64_t e = threadIdx.x; e < len; e += kThreads)
+      buf_put_f32<kAuxWO>(0.0f, rOut, static_cast<uint32_t>(e) * 4, 0);
+  }
 }
 
 // Swap-out of one chunk of a channel that left the selection: its previous
@@ -315,12 +341,17 @@ __device__ __forceinline__ void cm_swap_out(const DevMat& d, int64_t j, int64_t 
 // and writes that partial to zs[zs_off + (j * cm_nch + chunk) * 4 + wave].
 // The partials of a channel are combined in a fixed order by the Zen-auto
 // finalize kernel; no barriers, no atomics.
-template <bool BATCHED, bool ADAM, bool PACK, bool STATS>
+//
+// HAND (fused Adam + pack only, the last step of an interval): the hand-over
+// is written instead of the packed sums -- out row j = scale * (A + g) for an
+// unselected channel, +0.0 for a selected one -- and the packed buffer is
+// left as it was (it is overwritten when the next interval starts).
+template <bool BATCHED, bool ADAM, bool PACK, bool STATS, bool HAND>
 __global__ __launch_bounds__(kThreads) void cm_update_kernel(const DevMat* __restrict__ mats,
                                                             const int64_t* __restrict__ off,
                                                             int32_t nmats, DevMat one, AdamK c,
                                                             int32_t mode, int32_t first,
-                                                            double* __restrict__ zs) {
+                                                            double* __restrict__ zs, float scale) {
   int64_t local;
   const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, local);
   const int64_t chunk = static_cast<int64_t>(d.cm_vpt) * kThreads * kGroup;
@@ -341,7 +372,16 @@ __global__ __launch_bounds__(kThreads) void cm_update_kernel(const DevMat* __res
     if constexpr (PACK) {
       const int64_t u = j - r;
       const rsrc_t rA = make_rsrc(d.acc + u * d.ld_acc + e0, len * 4);
-      if (d.vec) {
+      if constexpr (HAND) {
+        const rsrc_t rOut = make_rsrc(d.out + j * d.ld_out + e0, len * 4);
+        if (d.vec) {
+          if (first) cm_pack_vec_any<true, false, true>(d.cm_vpt, rG, rA, ss, rOut, scale);
+          else cm_pack_vec_any<false, false, true>(d.cm_vpt, rG, rA, ss, rOut, scale);
+        } else {
+          if (first) cm_pack_elem<true, false, true>(rG, rA, len, ss, rOut, scale);
+          else cm_pack_elem<false, false, true>(rG, rA, len, ss, rOut, scale);
+        }
+      } else if (d.vec) {
         if (first) cm_pack_vec_any<true, STATS>(d.cm_vpt, rG, rA, ss);
         else cm_pack_vec_any<false, STATS>(d.cm_vpt, rG, rA, ss);
       } else {
@@ -394,6 +434,7 @@ __global__ __launch_bounds__(kThreads) void cm_update_kernel(const DevMat* __res
         default: cm_adam_elem<kCmInitMaster, STATS>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, len, ss); break;
       }
     }
+    if constexpr (HAND) cm_zero_rows(d, make_rsrc(d.out + j * d.ld_out + e0, len * 4), len);
   }
   if constexpr (STATS) {
 #pragma unroll
@@ -470,32 +511,36 @@ hipError_t launch_cm_colnorm(const Table& t, const DevMat& one, int64_t blocks, 
   return hipGetLastError();
 }
 
-template <bool ADAM, bool PACK, bool STATS>
+template <bool ADAM, bool PACK, bool STATS, bool HAND>
 static void launch_cm_update_t(const Table& t, const DevMat& one, dim3 grid, const AdamK& c,
-                               int32_t mode, int32_t first, double* zs, hipStream_t s) {
+                               int32_t mode, int32_t first, double* zs, float scale,
+                               hipStream_t s) {
   if (t.mats != nullptr)
-    hipLaunchKernelGGL((cm_update_kernel<true, ADAM, PACK, STATS>), grid, dim3(kThreads), 0, s,
-                       t.mats, t.off, t.nmats, one, c, mode, first, zs);
+    hipLaunchKernelGGL((cm_update_kernel<true, ADAM, PACK, STATS, HAND>), grid, dim3(kThreads), 0,
+                       s, t.mats, t.off, t.nmats, one, c, mode, first, zs, scale);
   else
-    hipLaunchKernelGGL((cm_update_kernel<false, ADAM, PACK, STATS>), grid, dim3(kThreads), 0, s,
-                       t.mats, t.off, t.nmats, one, c, mode, first, zs);
+    hipLaunchKernelGGL((cm_update_kernel<false, ADAM, PACK, STATS, HAND>), grid, dim3(kThreads), 0,
+                       s, t.mats, t.off, t.nmats, one, c, mode, first, zs, scale);
 }
 
 hipError_t launch_cm_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
                             int32_t mode, int32_t first, bool adam, bool pack, double* zs,
-                            hipStream_t s) {
+                            bool handover, float scale, hipStream_t s) {
   (void)hipGetLastError();
   if (blocks <= 0) return hipSuccess;
   const dim3 grid(static_cast<uint32_t>(blocks));
+  if ((zs != nullptr || handover) && !(adam && pack)) return hipErrorInvalidValue;
+  if (zs != nullptr && handover) return hipErrorInvalidValue;
   if (zs != nullptr) {
-    if (!(adam && pack)) return hipErrorInvalidValue;
-    launch_cm_update_t<true, true, true>(t, one, grid, c, mode, first, zs, s);
+    launch_cm_update_t<true, true, true, false>(t, one, grid, c, mode, first, zs, 1.0f, s);
+  } else if (handover) {
+    launch_cm_update_t<true, true, false, true>(t, one, grid, c, mode, first, nullptr, scale, s);
   } else if (adam && pack) {
-    launch_cm_update_t<true, true, false>(t, one, grid, c, mode, first, nullptr, s);
+    launch_cm_update_t<true, true, false, false>(t, one, grid, c, mode, first, nullptr, 1.0f, s);
   } else if (adam) {
-    launch_cm_update_t<true, false, false>(t, one, grid, c, mode, first, nullptr, s);
+    launch_cm_update_t<true, false, false, false>(t, one, grid, c, mode, first, nullptr, 1.0f, s);
   } else if (pack) {
-    launch_cm_update_t<false, true, false>(t, one, grid, c, mode, first, nullptr, s);
+    launch_cm_update_t<false, true, false, false>(t, one, grid, c, mode, first, nullptr, 1.0f, s);
   }
   return hipGetLastError();
 }

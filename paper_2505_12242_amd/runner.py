@@ -7,7 +7,10 @@ issues one batched launch per kernel per step:
     refresh step : zf_plan_colnorm -> zf_plan_topk_select ->
                    zf_plan_update (states remapped to the new selection)
     other steps  : zf_plan_update (states in place)
-    interval end : zf_plan_unpack with scale 1/(steps in the interval)
+    interval end : zf_plan_update_handover, the update with the hand-over
+                   fused in (out = (1/steps in the interval) x the final sums;
+                   the packed buffer is only read), or zf_plan_update then
+                   zf_plan_unpack when fuse_handover is False
 
 Compact states and selections are double-buffered: a refresh writes the new
 selection and new states into the other buffer while reading the previous
@@ -101,7 +104,7 @@ class SelectiveUpdateRunner:
                  init_master: Optional[Sequence[torch.Tensor]] = None,
                  device=None, keep_unpacked: bool = True, layout: int = ROW_MAJOR,
                  zen_tau: Optional[float] = None, offload: bool = False, overlap: bool = True,
-                 host_threads: Optional[int] = None):
+                 host_threads: Optional[int] = None, fuse_handover: bool = True):
         self.device = torch.device(device) if device is not None else torch.device("cuda")
         self.shapes = [(int(n), int(m)) for n, m in shapes]
         self.ratio, self.hp, self.R, self.S = ratio, hp, int(refresh), int(accum)
@@ -110,6 +113,7 @@ class SelectiveUpdateRunner:
         self.offload = bool(offload)
         self.overlap = bool(overlap) and self.offload
         self.keep_unpacked = keep_unpacked and not self.offload
+        self.fuse_handover = bool(fuse_handover)
         self.weights = list(weights)
         self.init_master = list(init_master) if init_master is not None else None
         dev = self.device
@@ -235,9 +239,13 @@ class SelectiveUpdateRunner:
             plan = self.plans[slot][self.cur][self.cur_a]
             mode = STATES_INPLACE
         if self.zen_tau is None:
+            end = kind.interval_end
+            if end and self.keep_unpacked and self.fuse_handover:
+                with rec("update_handover"):
+                    plan.update_handover(self.hp, t, mode, length, self.S, 1.0 / length, st)
+                return kind
             with rec("update_first" if length == 1 else "update"):
                 plan.update(self.hp, t, mode, length, self.S, stream=st)
-            end = kind.interval_end
         else:
             with rec("update_zen_first" if length == 1 else "update_zen"):
                 plan.update_zen(self.hp, t, mode, length, self.S, self.zen_tau,

@@ -52,8 +52,9 @@ def rel_close(got, want, rtol, floor=None):
 
 
 def same_bits(a, b) -> bool:
+    """Equal shapes, element sizes and bit patterns (no byte-string copies)."""
     a = np.ascontiguousarray(a)
     b = np.ascontiguousarray(b)
-    if a.shape != b.shape:
+    if a.shape != b.shape or a.dtype.itemsize != b.dtype.itemsize:
         return False
-    return a.view(np.uint8).tobytes() == b.view(np.uint8).tobytes()
+    return bool(np.array_equal(a.reshape(-1).view(np.uint8), b.reshape(-1).view(np.uint8)))

@@ -275,6 +275,41 @@ def test_fused_equals_separate(n, m, ratio, layout):
     assert torch.equal(A1.view(torch.int32), A2.view(torch.int32))
 
 
+@pytest.mark.parametrize("n,m,ratio", [(65, 513, 0.1), (200, 4096, 0.1), (5, 9, 0.5),
+                                       (4104, 70, 0.1), (43, 77, 0.2), (16, 3, 0.1), (8, 10, 1.0)])
+@pytest.mark.parametrize("sii", [1, 3])
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_fused_handover_equals_update_then_unpack(n, m, ratio, sii, layout):
+    """The interval's last step in one pass (zf_update_fused_handover) equals
+    zf_update_fused followed by zf_unpack bit for bit -- states, weights and
+    the hand-over -- and leaves the packed buffer untouched."""
+    bits, sel, P, M, V, W = adam_case(n, m, ratio, derive_seed("handover", n, m, sii))
+    sd = sel_from_oracle(sel)
+    G = bits_dev(bits, layout)
+    L = layout
+    a = [f32_dev_l(P, L), f32_dev_l(M, L), f32_dev_l(V, L), bits_dev(W, L)]
+    b = [f32_dev_l(P, L), f32_dev_l(M, L), f32_dev_l(V, L), bits_dev(W, L)]
+    u = m - sel.k
+    rng = np.random.default_rng(n + m + sii)
+    A0 = T(rng.standard_normal((n, u)).astype(np.float32), L)
+    A1, A2 = f32_dev(A0), f32_dev(A0)
+    scale = float(np.float32(1.0 / 3.0))
+    oshape = (n, m) if L == zf.ROW_MAJOR else (m, n)
+    D1 = torch.full((oshape[0], oshape[1] + 4), np.nan, device="cuda")[:, :oshape[1]]  # padded
+    zf.update_fused_handover(G, sd, *a, HP, 7, A1, sii, 4, scale, out=D1, layout=L)
+    zf.update_fused(G, sd, *b, HP, 7, A2, sii, 4, layout=L)
+    D2 = zf.unpack(A2, sd, scale, layout=L)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x.view(torch.int32) if x.dtype == torch.float32 else x.view(torch.int16),
+                           y.view(torch.int32) if y.dtype == torch.float32 else y.view(torch.int16))
+    assert same_bits(f32_np(D1), f32_np(D2))
+    assert same_bits(f32_np(A1), A0)  # only read
+    # and against the oracle's definition
+    A_or = O.pack_accumulate(bits, sel.unsel, T(A0, L), sii)
+    assert same_bits(f32_host(D1, L), O.unpack(A_or, sel, scale))
+
+
 def test_empty_sizes_are_no_ops():
     G = torch.empty(0, 9, dtype=torch.bfloat16, device="cuda")
     s = zf.colnorm(G)

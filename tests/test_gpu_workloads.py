@@ -62,7 +62,9 @@ def run_workload(name, use_master, layout=0):
                 assert np.array_equal(sel.unsel_idx.cpu().numpy(), orc.sel.unsel), (name_q, t)
                 assert np.array_equal(mask_np(sel.mask), orc.sel.mask), (name_q, t)
                 assert np.array_equal(sel.prefix.cpu().numpy(), orc.sel.prefix), (name_q, t)
-            assert same_bits(T(f32_np(runner.acc[q]), layout), orc.A), (name_q, t)
+            if not (kind.interval_end and runner.fuse_handover):
+                # the fused hand-over reads the packed buffer without writing it
+                assert same_bits(T(f32_np(runner.acc[q]), layout), orc.A), (name_q, t)
             P, M, V = (T(f32_np(x), layout) for x in runner.state[q])
             ok, w = rel_close(P, orc.P, 2e-6)
             assert ok, (name_q, t, "P", w)
@@ -92,8 +94,9 @@ def test_llama2_7b_layer_four_steps(layout):
 
 
 @pytest.mark.timeout(300)
+@pytest.mark.parametrize("fuse", [True, False], ids=["fused-handover", "separate-handover"])
 @pytest.mark.parametrize("layout", LAYOUTS)
-def test_batched_shapes_with_unaligned_schedule(layout):
+def test_batched_shapes_with_unaligned_schedule(layout, fuse):
     """Several shapes in one plan (odd sizes take the element-wise paths),
     refresh every 3 steps and accumulation interval 2, so refreshes cut
     intervals short; every output compared with the oracle at every step."""
@@ -115,7 +118,8 @@ def test_batched_shapes_with_unaligned_schedule(layout):
         mw = master_weights(n, m, derive_seed("unaligned", q), device=dev).to(torch.bfloat16)
         w0.append(bits_np(mw))
         weights.append(mw if layout == zf.ROW_MAJOR else mw.t().contiguous())
-    runner = zf.SelectiveUpdateRunner(shapes, ratio, hp, R, S, slots, weights, layout=layout)
+    runner = zf.SelectiveUpdateRunner(shapes, ratio, hp, R, S, slots, weights, layout=layout,
+                                      fuse_handover=fuse)
     orcs = [O.MatrixOracle(O.widen(w0[q]), w0[q], ratio, hp.lr, hp.beta1, hp.beta2, hp.eps,
                            hp.weight_decay, R, S) for q in range(len(shapes))]
     for t in range(1, steps + 1):
@@ -127,7 +131,8 @@ def test_batched_shapes_with_unaligned_schedule(layout):
                 assert np.array_equal(runner.selection[q].sel_idx.cpu().numpy(), orc.sel.sel), (q, t)
             P, M, V = (T(f32_np(x), layout) for x in runner.state[q])
             assert same_bits(P, orc.P) and same_bits(M, orc.M) and same_bits(V, orc.V), (q, t)
-            assert same_bits(T(f32_np(runner.acc[q]), layout), orc.A), (q, t)
+            if not (kind.interval_end and fuse):
+                assert same_bits(T(f32_np(runner.acc[q]), layout), orc.A), (q, t)
             assert np.array_equal(T(bits_np(weights[q]), layout), orc.W), (q, t)
             if kind.interval_end:
                 assert same_bits(T(f32_np(runner.unpacked[q]), layout), out["unpacked"]), (q, t)
