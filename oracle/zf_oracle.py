@@ -493,28 +493,46 @@ class OffloadOracle:
         self.store = (master.copy(), z, z.copy())
 
     def step(self, G: np.ndarray) -> dict:
+        """One step of the fixed schedule (refresh every R steps, intervals
+        of S steps), the deferred update at every interval end."""
         kind = schedule(self.t + 1, self.R, self.S)
+        out = self.advance(G, kind.refresh, kind.step_in_interval)
+        out["kind"] = kind
+        if kind.interval_end:
+            out["weight_cols"] = self.hand_over(kind.step_in_interval)
+        return out
+
+    def advance(self, G: np.ndarray, refresh: bool, step_in_interval: int) -> dict:
+        """Everything of a step before the hand-over: scores, selection and
+        the swap against the store when `refresh`, then Adam on the selected
+        columns and the accumulation of the others."""
         self.t += 1
-        out = {"kind": kind}
-        if kind.refresh:
+        out = {}
+        if refresh:
             s = colnorm(G)
             new = select_topk(s, self.k)
             self.P, self.M, self.V, self.store = swap_states(self.sel, new, self.P, self.M,
                                                              self.V, self.store)
             self.sel = new
             out["norms"] = s
+        elif self.sel is None:
+            raise ValueError("the first step must refresh the selection")
         c = AdamConsts.at_step(*self.hyper, self.t)
         self.P, self.M, self.V, wsel = adam_selected(G, self.sel.sel, self.P, self.M, self.V, c)
         self.W[:, self.sel.sel.astype(np.int64)] = wsel
-        self.A = pack_accumulate(G, self.sel.unsel, self.A, kind.step_in_interval)
-        if kind.interval_end:
-            self.th += 1
-            ch = AdamConsts.at_step(*self.hyper, self.th)
-            scale = float(np.float32(1.0 / kind.step_in_interval))
-            self.store, wun = deferred_adam(self.A, self.sel.unsel, scale, self.store, ch)
-            self.W[:, self.sel.unsel.astype(np.int64)] = wun
-            out["weight_cols"] = wun
+        self.A = pack_accumulate(G, self.sel.unsel, self.A, step_in_interval)
         return out
+
+    def hand_over(self, steps: int) -> np.ndarray:
+        """The deferred update at the end of an interval of `steps` steps
+        (scale fp32(1/steps), the offloaded optimizer's next step); returns
+        the new bf16 weights of the unselected columns, also written into W."""
+        self.th += 1
+        ch = AdamConsts.at_step(*self.hyper, self.th)
+        scale = float(np.float32(1.0 / steps))
+        self.store, wun = deferred_adam(self.A, self.sel.unsel, scale, self.store, ch)
+        self.W[:, self.sel.unsel.astype(np.int64)] = wun
+        return wun
 
 
 # ---------------------------------------------------------------------------
@@ -578,7 +596,9 @@ def zen_auto_trigger(stats, tau: float) -> ZenAutoTotals:
 
 
 class ZenAutoOracle:
-    """Several matrices under Zen-auto's adaptive interval.  Reading of the
+    """Several matrices under Zen-auto's adaptive interval (MatrixOracle:
+    the hand-over is the dense buffer; OffloadOracle: the hand-over is the
+    deferred update of the offloaded optimizer).  Reading of the
     schedule: the selection is refreshed when (t-1) mod R = 0 as in the fixed
     schedule; an interval starts at a refresh or after a hand-over, and ends
     (hand-over with scale 1/length) when the trigger fires, when it reaches

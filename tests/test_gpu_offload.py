@@ -243,3 +243,56 @@ def test_offloaded_steps_match_oracle(layout, R, S, overlap):
     assert runner.th == orcs[0].th
     assert changed > 0  # selections really changed: swaps were exercised
     runner.close()
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("overlap", [False, True])
+def test_zen_auto_triggers_the_deferred_update(overlap):
+    """Zen-auto with the offloaded optimizer (channel-major): the trigger
+    ends the interval and starts the deferred host update.  Against
+    ZenAutoOracle over OffloadOracles: interval ends, totals, and at
+    synchronised points the compact states, the whole store and W, bit for
+    bit; tau sits between the ratios observed after one and after several
+    accumulated steps, so intervals end early."""
+    import math
+    layout, R, S_max, T_ = zf.CHANNEL_MAJOR, 16, 6, 10
+    dev = torch.device("cuda")
+    slots, host, weights, w0 = _inputs(SET, T_, 23, layout, dev)
+
+    def oracles(tau):
+        return O.ZenAutoOracle([O.OffloadOracle(O.widen(w0[q]), w0[q], 0.1, HP.lr, HP.beta1,
+                                                HP.beta2, HP.eps, HP.weight_decay, R, S_max)
+                                for q in range(len(SET))], R, S_max, tau)
+
+    probe = oracles(math.inf)
+    ratios = []
+    for t in range(T_):
+        tot = probe.step(host[t])["totals"]
+        ratios.append((tot.sum_acc / tot.u) / (tot.sum_sel / tot.k))
+    tau = math.sqrt(min(ratios[:2]) * max(ratios[2:S_max]))
+    za = oracles(tau)
+    runner = zf.SelectiveUpdateRunner(SET, 0.1, HP, R, S_max, slots, weights, device=dev,
+                                      layout=layout, zen_tau=tau, offload=True, overlap=overlap,
+                                      host_threads=4)
+    ends = []
+    for t in range(1, T_ + 1):
+        print(f"# zen+offload overlap={overlap} step {t}", file=sys.stderr, flush=True)
+        kind = runner.step()
+        ref = za.step(host[t - 1])
+        assert (kind.refresh, kind.step_in_interval, kind.interval_end) == \
+            (ref["refresh"], ref["step_in_interval"], ref["interval_end"]), t
+        got, want = runner.last_totals, ref["totals"]
+        assert abs(got.sum_acc - want.sum_acc) <= 1e-9 * want.sum_acc
+        assert got.trigger == want.trigger
+        ends.append(kind.interval_end)
+        if t % 3 == 0 or t == T_:
+            runner.sync()
+            for q, o in enumerate(za.orcs):
+                for g_, w_ in zip(runner.state[q], (o.P, o.M, o.V)):
+                    assert same_bits(logical(f32_np(g_), layout), w_), (q, t)
+                for g_, w_ in zip(runner.store[q], o.store):
+                    assert same_bits(logical(g_.numpy(), layout), w_), (q, t)
+                assert np.array_equal(logical(bits_np(runner.weights[q]), layout), o.W), (q, t)
+    assert any(ends) and not all(ends)
+    assert runner.th == za.orcs[0].th == sum(ends)
+    runner.close()

@@ -232,3 +232,34 @@ def test_offload_conserves_state_through_refreshes():
             assert np.array_equal(a, b[:, ucols])
         prev_full = after
     assert prev_full is not None
+
+
+def test_zen_auto_drives_the_deferred_update():
+    """ZenAutoOracle over OffloadOracles: with tau = inf it is the fixed
+    schedule with S = S_max (R a multiple of S_max) bit for bit; with tau = 0
+    every step hands over, i.e. the deferred update runs after every step."""
+    rng = np.random.default_rng(9)
+    shapes = [(6, 40), (9, 17)]
+    masters = [(rng.standard_normal(s) * 0.02).astype(np.float32) for s in shapes]
+    grads = [[bf16(rng.standard_normal(s) * np.exp(rng.standard_normal(s[1]))) for s in shapes]
+             for _ in range(9)]
+
+    def make(R, S):
+        return [O.OffloadOracle(mw, bf16(mw), 0.25, 1e-3, 0.9, 0.999, 1e-8, 0.0, R, S)
+                for mw in masters]
+
+    za = O.ZenAutoOracle(make(6, 3), R=6, S_max=3, tau=float("inf"))
+    fixed = make(6, 3)
+    for step in grads:
+        r = za.step(step)
+        outs = [o.step(G) for o, G in zip(fixed, step)]
+        assert r["interval_end"] == outs[0]["kind"].interval_end
+    for a, b in zip(za.orcs, fixed):
+        assert a.th == b.th == 3
+        for x, y in zip(a.store, b.store):
+            assert np.array_equal(x.view(np.uint32), y.view(np.uint32))
+        assert np.array_equal(a.W, b.W)
+    za0 = O.ZenAutoOracle(make(6, 3), R=6, S_max=3, tau=0.0)
+    for step in grads:
+        assert za0.step(step)["interval_end"]
+    assert all(o.th == len(grads) for o in za0.orcs)
