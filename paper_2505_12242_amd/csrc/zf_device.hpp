@@ -19,6 +19,19 @@ __device__ __forceinline__ uint16_t round_bf16(float x) {
   return static_cast<uint16_t>(u >> 16);
 }
 
+// A value every lane of the wave holds (loaded from the same address, e.g.
+// the selection word of a block's channel) moved to scalar registers.
+// Buffer resources built from it are then scalar as the hardware requires,
+// instead of being wrapped by the compiler in per-access lane loops.
+__device__ __forceinline__ uint64_t uniform_u64(uint64_t x) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(x));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(x >> 32));
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+__device__ __forceinline__ int32_t uniform_i32(int32_t x) {
+  return __builtin_amdgcn_readfirstlane(x);
+}
+
 // Number of set bits of `mask` at lane positions below the calling lane.
 __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
   return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
@@ -47,9 +60,9 @@ __device__ __forceinline__ int64_t xcd_remap(int64_t b, int64_t B) {
 // take it by value.  Keeping the two apart avoids a generic pointer that
 // would turn the descriptor loads into flat vector loads.
 template <bool BATCHED>
-__device__ __forceinline__ DevMat get_mat(const DevMat* __restrict__ mats,
-                                          const int64_t* __restrict__ off, int32_t nmats,
-                                          const DevMat& one, int64_t& local) {
+__device__ __forceinline__ const DevMat& get_mat(const DevMat* __restrict__ mats,
+                                                 const int64_t* __restrict__ off, int32_t nmats,
+                                                 const DevMat& one, int64_t& local) {
   const int64_t b = xcd_remap(blockIdx.x, gridDim.x);
   if constexpr (!BATCHED) {
     local = b;

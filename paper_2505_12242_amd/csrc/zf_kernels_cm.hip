@@ -306,9 +306,9 @@ __device__ __forceinline__ void cm_zero_rows(const DevMat& d, rsrc_t rOut, int64
 // compact (p, m, v) rows are copied to its rows of the full-state store.
 __device__ __forceinline__ void cm_swap_out(const DevMat& d, int64_t j, int64_t w, int64_t e0,
                                             int64_t len) {
-  const uint64_t pm = d.prev_mask[w];
+  const uint64_t pm = uniform_u64(d.prev_mask[w]);
   if (!((pm >> (j & 63)) & 1ull)) return;
-  const int64_t ro = static_cast<int64_t>(d.prev_prefix[w]) +
+  const int64_t ro = static_cast<int64_t>(uniform_i32(d.prev_prefix[w])) +
                      __popcll(pm & ((uint64_t(1) << (j & 63)) - 1));
   const rsrc_t src[3] = {make_rsrc(d.prev_P + ro * d.ld_prev + e0, len * 4),
                          make_rsrc(d.prev_M + ro * d.ld_prev + e0, len * 4),
@@ -346,23 +346,28 @@ __device__ __forceinline__ void cm_swap_out(const DevMat& d, int64_t j, int64_t 
 // is written instead of the packed sums -- out row j = scale * (A + g) for an
 // unselected channel, +0.0 for a selected one -- and the packed buffer is
 // left as it was (it is overwritten when the next interval starts).
+#ifdef ZF_CM_WAVES_PER_EU
+#define ZF_CM_UPDATE_ATTR __attribute__((amdgpu_waves_per_eu(ZF_CM_WAVES_PER_EU)))
+#else
+#define ZF_CM_UPDATE_ATTR
+#endif
 template <bool BATCHED, bool ADAM, bool PACK, bool STATS, bool HAND>
-__global__ __launch_bounds__(kThreads) void cm_update_kernel(const DevMat* __restrict__ mats,
+__global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(const DevMat* __restrict__ mats,
                                                             const int64_t* __restrict__ off,
                                                             int32_t nmats, DevMat one, AdamK c,
                                                             int32_t mode, int32_t first,
                                                             double* __restrict__ zs, float scale) {
   int64_t local;
-  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, local);
+  const DevMat& d = get_mat<BATCHED>(mats, off, nmats, one, local);
   const int64_t chunk = static_cast<int64_t>(d.cm_vpt) * kThreads * kGroup;
   const int64_t j = local / d.cm_nch;
   const int64_t ci = local % d.cm_nch;
   const int64_t e0 = ci * chunk;
   const int64_t len = min(chunk, d.n - e0);
   const int64_t w = j >> 6;
-  const uint64_t mw = d.mask[w];
+  const uint64_t mw = uniform_u64(d.mask[w]);
   const bool sel = (mw >> (j & 63)) & 1ull;
-  const int64_t r = static_cast<int64_t>(d.prefix[w]) +
+  const int64_t r = static_cast<int64_t>(uniform_i32(d.prefix[w])) +
                     __popcll(mw & ((uint64_t(1) << (j & 63)) - 1));
   const rsrc_t rG = make_rsrc(d.grad + j * d.ld_grad + e0, len * 2);
   double ss = 0.0;
@@ -397,9 +402,9 @@ __global__ __launch_bounds__(kThreads) void cm_update_kernel(const DevMat* __res
     int src = kCmInplace;
     rsrc_t rSP = rP, rSM = rM, rSV = rV, rI = rW;
     if (mode == kRemap) {
-      const uint64_t pm = d.prev_mask[w];
+      const uint64_t pm = uniform_u64(d.prev_mask[w]);
       if ((pm >> (j & 63)) & 1ull) {
-        const int64_t ro = static_cast<int64_t>(d.prev_prefix[w]) +
+        const int64_t ro = static_cast<int64_t>(uniform_i32(d.prev_prefix[w])) +
                            __popcll(pm & ((uint64_t(1) << (j & 63)) - 1));
         rSP = make_rsrc(d.prev_P + ro * d.ld_prev + e0, len * 4);
         rSM = make_rsrc(d.prev_M + ro * d.ld_prev + e0, len * 4);
@@ -460,7 +465,7 @@ __global__ __launch_bounds__(kThreads) void cm_unpack_kernel(const DevMat* __res
   const int64_t e0 = (local % d.cm_unch) * kCmUnpackChunk;
   const int64_t len = min(static_cast<int64_t>(kCmUnpackChunk), d.n - e0);
   const int64_t w = j >> 6;
-  const uint64_t mw = d.mask[w];
+  const uint64_t mw = uniform_u64(d.mask[w]);
   const bool sel = (mw >> (j & 63)) & 1ull;
   const rsrc_t rD = make_rsrc(d.out + j * d.ld_out + e0, len * 4);
   const int tid = threadIdx.x;
@@ -475,7 +480,7 @@ __global__ __launch_bounds__(kThreads) void cm_unpack_kernel(const DevMat* __res
     }
     return;
   }
-  const int64_t u = j - (static_cast<int64_t>(d.prefix[w]) +
+  const int64_t u = j - (static_cast<int64_t>(uniform_i32(d.prefix[w])) +
                          __popcll(mw & ((uint64_t(1) << (j & 63)) - 1)));
   const rsrc_t rA = make_rsrc(d.acc + u * d.ld_acc + e0, len * 4);
   if (d.vec) {
@@ -511,16 +516,23 @@ hipError_t launch_cm_colnorm(const Table& t, const DevMat& one, int64_t blocks, 
   return hipGetLastError();
 }
 
+// LDS reserved (and unused) per update block: caps the blocks resident on a
+// CU (160 KiB of LDS per CU) and so the number of concurrent HBM streams.
+#ifndef ZF_CM_UPDATE_LDS
+#define ZF_CM_UPDATE_LDS 0
+#endif
+constexpr unsigned kCmUpdateLds = ZF_CM_UPDATE_LDS;
+
 template <bool ADAM, bool PACK, bool STATS, bool HAND>
 static void launch_cm_update_t(const Table& t, const DevMat& one, dim3 grid, const AdamK& c,
                                int32_t mode, int32_t first, double* zs, float scale,
                                hipStream_t s) {
   if (t.mats != nullptr)
-    hipLaunchKernelGGL((cm_update_kernel<true, ADAM, PACK, STATS, HAND>), grid, dim3(kThreads), 0,
-                       s, t.mats, t.off, t.nmats, one, c, mode, first, zs, scale);
+    hipLaunchKernelGGL((cm_update_kernel<true, ADAM, PACK, STATS, HAND>), grid, dim3(kThreads),
+                       kCmUpdateLds, s, t.mats, t.off, t.nmats, one, c, mode, first, zs, scale);
   else
-    hipLaunchKernelGGL((cm_update_kernel<false, ADAM, PACK, STATS, HAND>), grid, dim3(kThreads), 0,
-                       s, t.mats, t.off, t.nmats, one, c, mode, first, zs, scale);
+    hipLaunchKernelGGL((cm_update_kernel<false, ADAM, PACK, STATS, HAND>), grid, dim3(kThreads),
+                       kCmUpdateLds, s, t.mats, t.off, t.nmats, one, c, mode, first, zs, scale);
 }
 
 hipError_t launch_cm_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,

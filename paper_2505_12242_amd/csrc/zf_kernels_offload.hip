@@ -21,9 +21,9 @@ __global__ __launch_bounds__(kThreads) void cm_scatter_kernel(const DevMat* __re
   const int64_t e0 = (local % d.cm_unch) * kCmUnpackChunk;
   const int64_t len = min(static_cast<int64_t>(kCmUnpackChunk), d.n - e0);
   const int64_t w = j >> 6;
-  const uint64_t mw = d.mask[w];
+  const uint64_t mw = uniform_u64(d.mask[w]);
   if ((mw >> (j & 63)) & 1ull) return;
-  const int64_t u = j - (static_cast<int64_t>(d.prefix[w]) +
+  const int64_t u = j - (static_cast<int64_t>(uniform_i32(d.prefix[w])) +
                          __popcll(mw & ((uint64_t(1) << (j & 63)) - 1)));
   const uint16_t* __restrict__ src = d.wcols + u * d.ld_wcols + e0;
   uint16_t* __restrict__ dst = d.weight + j * d.ld_weight + e0;
