@@ -200,3 +200,20 @@ def test_plan_validation():
     assert _lib.ZEN_TOTALS_BYTES == 40
     assert LIB.zf_plan_device_bytes(None) == 0
     LIB.zf_plan_destroy(None)
+
+
+def test_offload_and_handover_entry_points_validate_on_the_host():
+    hp = _lib.ZfAdamHparams(1e-5, 0.9, 0.999, 1e-8, 0.0)
+    s = _lib.ZfSelection()
+    # no selection struct / null weights with data to write
+    assert LIB.zf_scatter_weights(None, 8, None, 1, 4, 8, RM, None, 8, None) == EINVAL
+    assert LIB.zf_scatter_weights(None, 8, ctypes.byref(s), 1, 4, 8, 7, None, 8, None) == EINVAL
+    # fused hand-over: an output is required when there is data; k > m; bad layout
+    assert LIB.zf_update_fused_handover(None, 4, 8, 8, RM, ctypes.byref(s), 1, None, None, None,
+                                        1, None, 8, ctypes.byref(hp), 1, 0, None, None, 7, 1, 4,
+                                        1.0, None, 8, None) == EINVAL
+    assert LIB.zf_update_fused_handover(None, 0, 0, 0, RM, ctypes.byref(s), 0, None, None, None,
+                                        0, None, 0, ctypes.byref(hp), 1, 0, None, None, 0, 1, 4,
+                                        1.0, None, 0, None) == 0  # nothing to do
+    assert LIB.zf_plan_update_handover(None, ctypes.byref(hp), 1, 0, 1, 4, 1.0, None) == EINVAL
+    assert LIB.zf_plan_scatter_weights(None, None) == EINVAL
