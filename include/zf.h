@@ -354,8 +354,8 @@ typedef struct zf_matrix {
   float* unpacked;
   int64_t ld_unpacked;
   zf_state_source src;
-  float* sel_sq; /* Zen-auto only: [k] fp32, channel-major plans (else NULL)   */
-  float* acc_sq; /* Zen-auto only: [m - k] fp32, channel-major plans (else NULL) */
+  float* sel_sq; /* Zen-auto only: [k] fp32 (else NULL)     */
+  float* acc_sq; /* Zen-auto only: [m - k] fp32 (else NULL) */
   const uint16_t* weight_cols; /* deferred update only: bf16 [n][m-k] / cm [m-k][n] */
   int64_t ld_weight_cols;
 } zf_matrix;
@@ -432,12 +432,18 @@ typedef struct zf_zen_totals {
  * *totals (DEVICE).  The caller ends the interval (zf_plan_unpack with scale
  * 1/step_in_interval) when trigger is set; the next step then starts a new
  * interval (step_in_interval = 1).
- * Requirements: a channel-major plan whose every descriptor provides
- * sel_sq [k] and acc_sq [m - k] (device fp32, disjoint from each other and
- * from the update's buffers), tau >= 0 (+inf allowed, never triggers when
+ * Channel-major plans sum the squares inside the update pass; row-major
+ * plans run the update and then a separate statistics pass (it reads the
+ * selected gradient columns and the packed buffer again, and uses the
+ * plan's column-score workspace).  Both layouts give the same statistics
+ * up to the order of the fp64 sums.
+ * Requirements: every descriptor of the plan provides sel_sq [k] and
+ * acc_sq [m - k] (device fp32, disjoint from each other and from the
+ * update's buffers), tau >= 0 (+inf allowed, never triggers when
  * sum_sel > 0), totals 8-byte aligned; else ZF_EINVAL with nothing
- * enqueued.  The plan's Zen-auto workspace is shared: do not run two
- * zf_plan_update_zen calls of one plan concurrently. */
+ * enqueued.  The plan's workspaces are shared: do not run zf_plan_update_zen
+ * concurrently with another zf_plan_update_zen or zf_plan_colnorm call of
+ * the same plan. */
 zf_status zf_plan_update_zen(zf_plan* plan, const zf_adam_hparams* hp, int64_t step,
                              int32_t mode, int64_t step_in_interval, int64_t accum_interval,
                              double tau, zf_zen_totals* totals, zf_stream stream);

@@ -651,10 +651,11 @@ struct zf_plan {
   int64_t* d_off_up = nullptr;
   int64_t* d_off_unp = nullptr;
   int64_t* d_off_zen = nullptr;
+  int64_t* d_off_zp = nullptr;  // row-major Zen-auto partial pass
   double* d_ws = nullptr;
   double* d_zs = nullptr;  // Zen-auto per-wave partials
   double* d_zb = nullptr;  // Zen-auto per-finalize-block sums
-  int64_t blk_cn = 0, blk_fin = 0, blk_top = 0, blk_up = 0, blk_unp = 0, blk_zen = 0;
+  int64_t blk_cn = 0, blk_fin = 0, blk_top = 0, blk_up = 0, blk_unp = 0, blk_zen = 0, blk_zp = 0;
   int64_t k_total = 0, u_total = 0;
   bool can_colnorm = true, can_topk = true, can_adam = true, can_remap = true, can_pack = true,
        can_unpack = true, can_zen = true, can_scatter = true, can_handover = true;
@@ -725,8 +726,8 @@ zf_status check_plan_matrix(const zf_matrix& x, zf_plan& p) {
                   mat_ok(x.weight, eg, x.ld_weight, 2) &&
                   !overlaps(span(x.weight_cols, ea, x.ld_weight_cols, 2),
                             span(x.weight, eg, x.ld_weight, 2));
-  // Zen-auto statistics: channel-major only; [k] and [m-k] fp32 outputs that
-  // overlap neither each other nor any buffer the fused update touches.
+  // Zen-auto statistics: [k] and [m-k] fp32 outputs that overlap neither
+  // each other nor any buffer the fused update touches.
   {
     const Span zsel = span_of(x.sel_sq, 1, k, k, 4), zacc = span_of(x.acc_sq, 1, m - k, m - k, 4);
     const Span others[6] = {g, span(x.acc, ea, x.ld_acc, 4),
@@ -734,8 +735,8 @@ zf_status check_plan_matrix(const zf_matrix& x, zf_plan& p) {
                             span(x.exp_avg, ext(L, n, k), x.ld_state, 4),
                             span(x.exp_avg_sq, ext(L, n, k), x.ld_state, 4),
                             span(x.weight, eg, x.ld_weight, 2)};
-    bool ok = L == zf::kChannelMajor && vector_ok(x.sel_sq, k, 4) &&
-              vector_ok(x.acc_sq, m - k, 4) && !overlaps(zsel, zacc);
+    bool ok = vector_ok(x.sel_sq, k, 4) && vector_ok(x.acc_sq, m - k, 4) &&
+              !overlaps(zsel, zacc);
     for (int a = 0; ok && a < 6; ++a) ok = !overlaps(zsel, others[a]) && !overlaps(zacc, others[a]);
     p.can_zen = p.can_zen && ok;
   }
@@ -769,7 +770,7 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   const int cn_rows = pick_colnorm_rows(shapes);
   const int up_rows = pick_update_rows(shapes);
   std::vector<int64_t> off_cn(nmats + 1), off_fin(nmats + 1), off_top(nmats + 1),
-      off_up(nmats + 1), off_unp(nmats + 1), off_zen(nmats + 1);
+      off_up(nmats + 1), off_unp(nmats + 1), off_zen(nmats + 1), off_zp(nmats + 1);
   int64_t ws_doubles = 0, zs_doubles = 0;
   const bool cm = p->layout == zf::kChannelMajor;
   p->mats.resize(nmats);
@@ -783,10 +784,14 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
     d.cn_ws = ws_doubles;
     if (!cm) ws_doubles += static_cast<int64_t>(d.cn_rb) * d.m;
     d.zs_off = zs_doubles;
-    if (cm && p->can_zen) {
-      zs_doubles += d.m * static_cast<int64_t>(d.cm_nch) * zf::kCmWaves;
+    if (p->can_zen) {
+      // channel-major: per-wave partials of the fused pass; row-major: the
+      // separate pass reuses the column-score workspace (cn_rb x m doubles)
+      if (cm) zs_doubles += d.m * static_cast<int64_t>(d.cm_nch) * zf::kCmWaves;
       off_zen[q] = p->blk_zen;
       p->blk_zen += ceil_div(d.m, zf::kZenCols);
+      off_zp[q] = p->blk_zp;
+      if (!cm) p->blk_zp += ceil_div(d.m, zf::kZenCols) * static_cast<int64_t>(d.cn_rb);
     }
     p->k_total += d.k;
     p->u_total += d.m - d.k;
@@ -808,15 +813,17 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   off_up[nmats] = p->blk_up;
   off_unp[nmats] = p->blk_unp;
   off_zen[nmats] = p->blk_zen;
+  off_zp[nmats] = p->blk_zp;
   const int64_t max_blocks = (int64_t(1) << 31) / zf::kThreads;
-  if (p->blk_cn >= max_blocks || p->blk_up >= max_blocks || p->blk_unp >= max_blocks) {
+  if (p->blk_cn >= max_blocks || p->blk_up >= max_blocks || p->blk_unp >= max_blocks ||
+      p->blk_zp >= max_blocks) {
     delete p;
     return ZF_EINVAL;  // grid too large for one launch
   }
 
   const size_t mats_bytes = sizeof(DevMat) * nmats;
   const size_t off_bytes = sizeof(int64_t) * (nmats + 1);
-  const size_t head = (mats_bytes + 6 * off_bytes + 255) & ~size_t(255);
+  const size_t head = (mats_bytes + 7 * off_bytes + 255) & ~size_t(255);
   const int64_t zb_doubles = p->can_zen ? 2 * p->blk_zen : 0;
   p->dev_bytes = head + sizeof(double) * static_cast<size_t>(ws_doubles + zs_doubles + zb_doubles);
   hipError_t e = hipMalloc(&p->dev, p->dev_bytes);
@@ -833,6 +840,7 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   p->d_off_up = p->d_off_top + (nmats + 1);
   p->d_off_unp = p->d_off_up + (nmats + 1);
   p->d_off_zen = p->d_off_unp + (nmats + 1);
+  p->d_off_zp = p->d_off_zen + (nmats + 1);
   p->d_ws = reinterpret_cast<double*>(base + head);
   p->d_zs = p->d_ws + ws_doubles;
   p->d_zb = p->d_zs + zs_doubles;
@@ -844,6 +852,7 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   std::memcpy(host.data() + mats_bytes + 3 * off_bytes, off_up.data(), off_bytes);
   std::memcpy(host.data() + mats_bytes + 4 * off_bytes, off_unp.data(), off_bytes);
   std::memcpy(host.data() + mats_bytes + 5 * off_bytes, off_zen.data(), off_bytes);
+  std::memcpy(host.data() + mats_bytes + 6 * off_bytes, off_zp.data(), off_bytes);
   e = hipMemcpy(p->dev, host.data(), head, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     g_last_hip_error = static_cast<int>(e);
@@ -955,12 +964,20 @@ zf_status zf_plan_update_zen(zf_plan* p, const zf_adam_hparams* hp, int64_t step
   const AdamK c = adam_consts(*hp, step);
   const hipStream_t s = as_stream(stream);
   const Table t{p->d_mats, p->d_off_up, p->nmats};
-  hipError_t e = zf::launch_cm_update(t, p->mats[0], p->blk_up, c, mode,
-                                      step_in_interval == 1 ? 1 : 0, true, true, p->d_zs, false,
-                                      1.0f, s);
-  if (e != hipSuccess) return hip_fail(e);
   const Table tz{p->d_mats, p->d_off_zen, p->nmats};
-  e = zf::launch_zen_finalize(tz, p->mats[0], p->blk_zen, p->d_zs, p->d_zb, s);
+  hipError_t e;
+  if (p->layout == zf::kChannelMajor) {
+    e = zf::launch_cm_update(t, p->mats[0], p->blk_up, c, mode, step_in_interval == 1 ? 1 : 0,
+                             true, true, p->d_zs, false, 1.0f, s);
+    if (e != hipSuccess) return hip_fail(e);
+    e = zf::launch_zen_finalize(tz, p->mats[0], p->blk_zen, p->d_zs, p->d_zb, s);
+  } else {
+    e = zf::launch_update(t, p->mats[0], p->blk_up, c, mode, step_in_interval == 1 ? 1 : 0, true,
+                          true, false, 1.0f, s);
+    if (e != hipSuccess) return hip_fail(e);
+    const Table tp{p->d_mats, p->d_off_zp, p->nmats};
+    e = zf::launch_rm_zen(tp, p->blk_zp, tz, p->blk_zen, p->mats[0], p->d_ws, p->d_zb, s);
+  }
   if (e != hipSuccess) return hip_fail(e);
   e = zf::launch_zen_total(p->d_zb, p->blk_zen, p->k_total, p->u_total, tau,
                            reinterpret_cast<zf::ZenTotals*>(totals), s);

@@ -159,6 +159,12 @@ struct ZenTotals {
 // (selected, accumulated) per finalize block into zb[2 * blocks].
 hipError_t launch_zen_finalize(const Table& t, const DevMat& one, int64_t blocks,
                                const double* zs, double* zb, hipStream_t s);
+// Row-major statistics pass (after the update; batched tables only):
+// per-column partials over the column-score row blocks into zs (the plan's
+// column-score workspace), then the row-major finalize into zb.
+hipError_t launch_rm_zen(const Table& tp, int64_t partial_blocks, const Table& tf,
+                         int64_t finalize_blocks, const DevMat& one, double* zs, double* zb,
+                         hipStream_t s);
 // One block: sums zb in a fixed order and evaluates the trigger.
 hipError_t launch_zen_total(const double* zb, int64_t blocks, int64_t k_total, int64_t u_total,
                             double tau, ZenTotals* out, hipStream_t s);

@@ -15,6 +15,15 @@
 //             sum_acc * k >= (tau * sum_sel) * u in fp64 (the pooled means
 //             sum_acc / u and sum_sel / k compared without a division).
 // Every order is fixed, so results are deterministic.
+//
+// Row-major layout: the update's tiles (256 columns x a few rows) leave no
+// per-column partial without atomics, so the statistics come from a
+// separate pass after the update: virtual column c < k is the selected
+// gradient column sel_idx[c], c >= k the packed column u = c - k of the
+// accumulated buffer; a block sums the squares of 256 virtual columns over
+// one row block (the column-score row blocks) in fp64 and stores one
+// partial per column and row block in the plan's column-score workspace;
+// the row-major finalize adds them in row-block order.
 #include "zf_device.hpp"
 
 namespace zf {
@@ -48,6 +57,77 @@ __global__ __launch_bounds__(kZenCols) void zen_finalize_kernel(const DevMat* __
       root_sel = root;
     } else {
       d.acc_sq[j - r] = f;
+      root_acc = root;
+    }
+  }
+  __shared__ double red[2][kZenCols];
+  red[0][tid] = root_sel;
+  red[1][tid] = root_acc;
+  __syncthreads();
+#pragma unroll
+  for (int h = kZenCols / 2; h >= 1; h >>= 1) {
+    if (tid < h) {
+      red[0][tid] += red[0][tid + h];
+      red[1][tid] += red[1][tid + h];
+    }
+    __syncthreads();
+  }
+  if (tid == 0) {
+    zb[2 * b] = red[0][0];
+    zb[2 * b + 1] = red[1][0];
+  }
+}
+
+template <bool BATCHED>
+__global__ __launch_bounds__(kZenCols) void rm_zen_partial_kernel(const DevMat* __restrict__ mats,
+                                                                 const int64_t* __restrict__ off,
+                                                                 int32_t nmats, DevMat one,
+                                                                 double* __restrict__ zs) {
+  int64_t local;
+  const DevMat& d = get_mat<BATCHED>(mats, off, nmats, one, local);
+  const int64_t cb = (d.m + kZenCols - 1) / kZenCols;
+  const int64_t rblk = local / cb;
+  const int64_t c = (local % cb) * kZenCols + threadIdx.x;
+  if (c >= d.m) return;
+  const int64_t i0 = rblk * d.cn_rpb;
+  const int64_t i1 = min(i0 + static_cast<int64_t>(d.cn_rpb), d.n);
+  double s = 0.0;
+  if (c < d.k) {
+    const uint16_t* __restrict__ g = d.grad + d.sel_idx[c];
+    for (int64_t i = i0; i < i1; ++i) {
+      const double x = static_cast<double>(widen_bf16(g[i * d.ld_grad]));
+      s = __builtin_fma(x, x, s);
+    }
+  } else {
+    const float* __restrict__ a = d.acc + (c - d.k);
+    for (int64_t i = i0; i < i1; ++i) {
+      const double x = static_cast<double>(a[i * d.ld_acc]);
+      s = __builtin_fma(x, x, s);
+    }
+  }
+  zs[d.cn_ws + rblk * d.m + c] = s;
+}
+
+template <bool BATCHED>
+__global__ __launch_bounds__(kZenCols) void rm_zen_finalize_kernel(
+    const DevMat* __restrict__ mats, const int64_t* __restrict__ off, int32_t nmats, DevMat one,
+    const double* __restrict__ zs, double* __restrict__ zb) {
+  int64_t local;
+  const DevMat& d = get_mat<BATCHED>(mats, off, nmats, one, local);
+  const int64_t b = xcd_remap(blockIdx.x, gridDim.x);
+  const int tid = threadIdx.x;
+  const int64_t c = local * kZenCols + tid;
+  double root_sel = 0.0, root_acc = 0.0;
+  if (c < d.m) {
+    double s = 0.0;
+    for (int32_t rb = 0; rb < d.cn_rb; ++rb) s += zs[d.cn_ws + static_cast<int64_t>(rb) * d.m + c];
+    const float f = static_cast<float>(s);
+    const double root = sqrt(static_cast<double>(f));
+    if (c < d.k) {
+      d.sel_sq[c] = f;
+      root_sel = root;
+    } else {
+      d.acc_sq[c - d.k] = f;
       root_acc = root;
     }
   }
@@ -119,6 +199,20 @@ hipError_t launch_zen_finalize(const Table& t, const DevMat& one, int64_t blocks
       hipLaunchKernelGGL((zen_finalize_kernel<false>), dim3(static_cast<uint32_t>(blocks)),
                          dim3(kZenCols), 0, s, t.mats, t.off, t.nmats, one, zs, zb);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_rm_zen(const Table& tp, int64_t partial_blocks, const Table& tf,
+                         int64_t finalize_blocks, const DevMat& one, double* zs, double* zb,
+                         hipStream_t s) {
+  (void)hipGetLastError();
+  if (partial_blocks > 0)
+    hipLaunchKernelGGL((rm_zen_partial_kernel<true>), dim3(static_cast<uint32_t>(partial_blocks)),
+                       dim3(kZenCols), 0, s, tp.mats, tp.off, tp.nmats, one, zs);
+  if (finalize_blocks > 0)
+    hipLaunchKernelGGL((rm_zen_finalize_kernel<true>),
+                       dim3(static_cast<uint32_t>(finalize_blocks)), dim3(kZenCols), 0, s, tf.mats,
+                       tf.off, tf.nmats, one, zs, zb);
   return hipGetLastError();
 }
 

@@ -1,6 +1,8 @@
 """Parity of Zen-auto (the adaptive accumulation interval, Zero-stall
 Pipeline "Hyperparameter Auto-tuning") on the GPU with the oracle's
-ZenAutoOracle, through zf_plan_update_zen (channel-major plans):
+ZenAutoOracle, through zf_plan_update_zen, in both layouts (statistics fused
+into the update in the channel-major layout, a separate pass in the
+row-major layout):
 
 * per channel: the selected channels' squared gradient norms and the
   accumulated channels' squared norms, within 1e-5 relative (both sides sum
@@ -36,9 +38,10 @@ zf = pytest.importorskip("paper_2505_12242_amd")
 SHAPES = [(264, 300), (4104, 70), (43, 77), (8192, 65), (16, 3), (128, 1000)]
 
 
-def _inputs(shapes, ratio, T, seed, dev):
-    """Channel-major device gradients per step and bf16 weights, plus the
-    logical host bit patterns the oracle takes."""
+def _inputs(shapes, ratio, T, seed, dev, layout=None):
+    """Device gradients per step and bf16 weights in `layout` (default
+    channel-major), plus the logical host bit patterns the oracle takes."""
+    cm = layout is None or layout == zf.CHANNEL_MAJOR
     slots, host = [], []
     for t in range(1, T + 1):
         dslot, hslot = [], []
@@ -48,7 +51,7 @@ def _inputs(shapes, ratio, T, seed, dev):
             s = space_boundary(jittered_scales(base, 0.05, derive_seed(seed, q, "jit", t)), k)
             g = gradient(n, m, s, derive_seed(seed, q, "grad", t), device=dev)
             hslot.append(bits_np(g))
-            dslot.append(g.t().contiguous())
+            dslot.append(g.t().contiguous() if cm else g)
         slots.append(dslot)
         host.append(hslot)
     weights, w0 = [], []
@@ -56,7 +59,7 @@ def _inputs(shapes, ratio, T, seed, dev):
         g = torch.Generator().manual_seed(derive_seed(seed, q, "w") & 0x7fffffff)
         w = (0.02 * torch.randn(n, m, generator=g)).to(torch.bfloat16)
         w0.append(bits_np(w))
-        weights.append(w.t().contiguous().to(dev))
+        weights.append((w.t().contiguous() if cm else w).to(dev))
     return slots, host, weights, w0
 
 
@@ -77,7 +80,9 @@ def _ratios(shapes, host, w0, ratio, hp, R, S_max):
     return out
 
 
-def _host(t):
+def _host(t, layout=None):
+    if layout == zf.ROW_MAJOR:
+        return t.contiguous().cpu()
     return t.t().contiguous().cpu()
 
 
@@ -92,12 +97,13 @@ def fixed_ends(T, R, S_max):
     return ends
 
 
-def run_zen(shapes, ratio, R, S_max, tau, T, seed, host_in=None):
+def run_zen(shapes, ratio, R, S_max, tau, T, seed, host_in=None, layout=None):
+    layout = zf.CHANNEL_MAJOR if layout is None else layout
     dev = torch.device("cuda")
     hp = zf.AdamHparams(lr=1e-3)
-    slots, host, weights, w0 = host_in or _inputs(shapes, ratio, T, seed, dev)
+    slots, host, weights, w0 = host_in or _inputs(shapes, ratio, T, seed, dev, layout)
     runner = zf.SelectiveUpdateRunner(shapes, ratio, hp, R, S_max, slots, weights, device=dev,
-                                      layout=zf.CHANNEL_MAJOR, zen_tau=tau)
+                                      layout=layout, zen_tau=tau)
     za = _oracle(shapes, w0, ratio, hp, R, S_max, tau)
     ends = []
     exact_stats = total_stats = 0
@@ -126,25 +132,30 @@ def run_zen(shapes, ratio, R, S_max, tau, T, seed, host_in=None):
                 exact_stats += int(np.sum(g.view(np.uint32) == ref_v.view(np.uint32)))
                 total_stats += g.size
             orc = za.orcs[q]
-            P, M, V = (_host(x).numpy() for x in runner.state[q])
+            P, M, V = (_host(x, layout).numpy() for x in runner.state[q])
             for a, b, name in ((P, orc.P, "master"), (M, orc.M, "exp_avg"),
                                (V, orc.V, "exp_avg_sq")):
                 assert same_bits(a, b), (name, q, t)
-            assert same_bits(_host(runner.acc[q]).numpy(), orc.A), ("acc", q, t)
-            assert same_bits(bits_np(runner.weights[q].t()), orc.W), ("weight", q, t)
+            assert same_bits(_host(runner.acc[q], layout).numpy(), orc.A), ("acc", q, t)
+            wl = runner.weights[q] if layout == zf.ROW_MAJOR else runner.weights[q].t()
+            assert same_bits(bits_np(wl), orc.W), ("weight", q, t)
             if kind.interval_end:
-                assert same_bits(_host(runner.unpacked[q]).numpy(), ref["unpacked"][q]), \
-                    ("hand-over", q, t)
+                assert same_bits(_host(runner.unpacked[q], layout).numpy(),
+                                 ref["unpacked"][q]), ("hand-over", q, t)
         ends.append(kind.interval_end)
     runner.close()
     return ends, exact_stats, total_stats
 
 
+LAYOUTS = [pytest.param(zf.ROW_MAJOR, id="rm"), pytest.param(zf.CHANNEL_MAJOR, id="cm")]
+
+
 @pytest.mark.timeout(600)
 @pytest.mark.parametrize("tau", [0.0, math.inf])
-def test_zen_auto_extreme_thresholds(tau):
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_zen_auto_extreme_thresholds(tau, layout):
     T, R, S_max = 9, 4, 3
-    ends, exact, total = run_zen(SHAPES, 0.1, R, S_max, tau, T, seed=11)
+    ends, exact, total = run_zen(SHAPES, 0.1, R, S_max, tau, T, seed=11, layout=layout)
     if tau == 0.0:
         assert all(ends)
     else:
@@ -155,17 +166,18 @@ def test_zen_auto_extreme_thresholds(tau):
 
 
 @pytest.mark.timeout(600)
-def test_zen_auto_threshold_between_observed_ratios():
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_zen_auto_threshold_between_observed_ratios(layout):
     """tau between the ratios the fixed schedule produces after one and after
     several accumulated steps: the trigger fires mid-interval."""
     T, R, S_max, ratio = 10, 16, 6, 0.1
     dev = torch.device("cuda")
-    inputs = _inputs(SHAPES, ratio, T, 12, dev)
+    inputs = _inputs(SHAPES, ratio, T, 12, dev, layout)
     r = _ratios(SHAPES, inputs[1], inputs[3], ratio, zf.AdamHparams(lr=1e-3), R, S_max)
     lo, hi = min(r[:2]), max(r[2:S_max])
     assert hi > lo
     tau = math.sqrt(lo * hi)
-    ends, _, _ = run_zen(SHAPES, ratio, R, S_max, tau, T, seed=12, host_in=inputs)
+    ends, _, _ = run_zen(SHAPES, ratio, R, S_max, tau, T, seed=12, host_in=inputs, layout=layout)
     assert any(ends) and not all(ends)
     # at least one interval ended by the trigger before reaching S_max
     lengths, cur = [], 0
@@ -179,23 +191,25 @@ def test_zen_auto_threshold_between_observed_ratios():
 
 @pytest.mark.timeout(300)
 @pytest.mark.parametrize("ratio", [0.0, 1.0])
-def test_zen_auto_one_part_empty(ratio):
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_zen_auto_one_part_empty(ratio, layout):
     """k = 0 (nothing selected) or k = m (nothing accumulated): the trigger
     never fires and the schedule is the fixed one."""
-    ends, _, _ = run_zen(SHAPES[:3], ratio, 4, 2, 0.0, 5, seed=13)
+    ends, _, _ = run_zen(SHAPES[:3], ratio, 4, 2, 0.0, 5, seed=13, layout=layout)
     assert ends == fixed_ends(5, 4, 2) == [False, True, False, True, False]
 
 
 @pytest.mark.timeout(300)
-def test_zen_auto_deterministic():
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_zen_auto_deterministic(layout):
     dev = torch.device("cuda")
     shapes = SHAPES[:4]
-    slots, host, weights, w0 = _inputs(shapes, 0.1, 2, 14, dev)
+    slots, host, weights, w0 = _inputs(shapes, 0.1, 2, 14, dev, layout)
     outs = []
     for _ in range(2):
         ws = [w.clone() for w in weights]
         runner = zf.SelectiveUpdateRunner(shapes, 0.1, zf.AdamHparams(), 4, 4, slots, ws,
-                                          device=dev, layout=zf.CHANNEL_MAJOR, zen_tau=1.0)
+                                          device=dev, layout=layout, zen_tau=1.0)
         tots = []
         for _ in range(2):
             runner.step()
@@ -222,10 +236,10 @@ def _plan_buffers(layout, with_stats=True):
         acc_sq=torch.zeros(m - k, **f) if with_stats else None)
 
 
-@pytest.mark.parametrize("layout,with_stats", [(0, True), (1, False)])
-def test_zen_auto_rejected_without_channel_major_statistics(layout, with_stats):
-    """Row-major plans and plans without statistics buffers refuse the call
-    (ZF_EINVAL) and enqueue nothing."""
+@pytest.mark.parametrize("layout,with_stats", [(0, False), (1, False)])
+def test_zen_auto_rejected_without_statistics_buffers(layout, with_stats):
+    """Plans without statistics buffers refuse the call (ZF_EINVAL) and
+    enqueue nothing."""
     plan = zf.Plan([_plan_buffers(layout, with_stats)])
     plan.colnorm()
     plan.topk_select()  # a valid selection, should anything run
