@@ -239,8 +239,8 @@ def main(argv=None) -> int:
     args = parse_args(argv)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "this build runs on one GPU only: the hot path of one GPU's "
-                                   "share is measured; --gpus must be 1"}), flush=True)
+        print(json.dumps({"error": "bench.py measures the hot path on one GPU (one GPU's "
+                                   "share of the work); --gpus must be 1"}), flush=True)
         return 2
 
     import numpy as np
