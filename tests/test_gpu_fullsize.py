@@ -103,3 +103,52 @@ def test_full_set_sampled_parity(name):
     runner.close()
     del runner, slots, weights
     torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(900)
+def test_full_set_zen_auto_statistics():
+    """Zen-auto over the whole 7B set in bench.py's launch configuration
+    (channel-major, batched, three-slot ring), 3 steps with tau = inf (the
+    fixed schedule): the device totals equal fp64 sums, recomputed on the
+    host, of the device's own per-channel statistics (all 1.15 M channels),
+    k and u totals are exact, and two sampled matrices' statistics match the
+    oracle within 1e-5 (their states and packed buffers bit for bit)."""
+    import math
+    from workloads import get_workload
+    wl = get_workload("llama2-7b-full")
+    hp = zf.AdamHparams(wl.hyper.lr, wl.hyper.beta1, wl.hyper.beta2, wl.hyper.eps,
+                        wl.hyper.weight_decay)
+    dev = torch.device("cuda")
+    shapes, ks, slots, weights = bench.build_set(wl, 3, dev, zf.CHANNEL_MAJOR)
+    names = [mt.name for mt in wl.matrices]
+    qs = [names.index("layers.5.up_proj"), names.index("lm_head")]
+    w0 = {q: bits_np(logical(weights[q]).contiguous()) for q in qs}
+    runner = zf.SelectiveUpdateRunner(shapes, wl.ratio, hp, wl.refresh, wl.accum, slots, weights,
+                                      device=dev, layout=zf.CHANNEL_MAJOR, zen_tau=math.inf)
+    orcs = {q: O.MatrixOracle(O.widen(w0[q]), w0[q], wl.ratio, hp.lr, hp.beta1, hp.beta2,
+                              hp.eps, hp.weight_decay, wl.refresh, wl.accum) for q in qs}
+    for t in range(1, 4):
+        kind = runner.step()
+        torch.cuda.synchronize()
+        print(f"# zen full set step {t}", file=sys.stderr, flush=True)
+        tot = runner.last_totals
+        assert tot.k_total == sum(ks) and tot.u_total == sum(m - k for (_, m), k in zip(shapes, ks))
+        assert not tot.trigger
+        sel_all = torch.cat(runner.sel_sq).double()
+        acc_all = torch.cat(runner.acc_sq).double()
+        assert abs(torch.sqrt(sel_all).sum().item() - tot.sum_sel) <= 1e-9 * tot.sum_sel
+        assert abs(torch.sqrt(acc_all).sum().item() - tot.sum_acc) <= 1e-9 * tot.sum_acc
+        for q in qs:
+            G = bits_np(logical(slots[(t - 1) % 3][q]).contiguous())
+            orcs[q].advance(G, kind.refresh, kind.step_in_interval)
+            ssq, asq = O.zen_auto_stats(G, orcs[q].sel, orcs[q].A)
+            ok, worst = rel_close(f32_np(runner.sel_sq[q]), ssq, 1e-5)
+            assert ok, (names[q], t, worst)
+            ok, worst = rel_close(f32_np(runner.acc_sq[q]), asq, 1e-5)
+            assert ok, (names[q], t, worst)
+            assert same_bits(f32_np(logical(runner.acc[q])), orcs[q].A), (names[q], t)
+            P = f32_np(logical(runner.state[q][0]))
+            assert same_bits(P, orcs[q].P), (names[q], t)
+    runner.close()
+    del runner, slots, weights
+    torch.cuda.empty_cache()
