@@ -25,16 +25,17 @@ namespace {
 
 constexpr int kGroup = 8;  // bf16 elements in 16 bytes
 
-// Cache policy per stream, chosen by measurement on MI355X: the column-score
-// pass reads G non-temporally (+8% over the default policy); in the update
-// and hand-over passes the default policy is fastest for every stream
-// (non-temporal stores of an overwritten packed row or of the hand-over cost
-// up to 40%).
+// Cache policy per stream, chosen by measurement on MI355X (7B set, three
+// alternating runs per variant): streams read once by a pass -- G in every
+// pass, the init sources -- and the bf16 weight write-back are non-temporal
+// (2% faster steps than the default policy everywhere); the hand-over output
+// and read-modify-write streams keep the default policy (non-temporal stores
+// of the hand-over cost 2-3% there).
 #ifndef ZF_AUX_SCORE
 #define ZF_AUX_SCORE kStream
 #endif
 #ifndef ZF_AUX_RO
-#define ZF_AUX_RO kCached
+#define ZF_AUX_RO kStream
 #endif
 #ifndef ZF_AUX_WO
 #define ZF_AUX_WO kCached
@@ -45,6 +46,14 @@ constexpr int kGroup = 8;  // bf16 elements in 16 bytes
 constexpr int kAuxScore = ZF_AUX_SCORE;  // G in the column-score pass
 constexpr int kAuxRO = ZF_AUX_RO;        // streams only read by a pass
 constexpr int kAuxWO = ZF_AUX_WO;        // streams only written by a pass
+#ifndef ZF_AUX_W
+#define ZF_AUX_W kStream
+#endif
+#ifndef ZF_AUX_AFIRST
+#define ZF_AUX_AFIRST ZF_AUX_WO
+#endif
+constexpr int kAuxW = ZF_AUX_W;            // the bf16 weight write-back
+constexpr int kAuxAFirst = ZF_AUX_AFIRST;  // the packed buffer on an interval's first step
 constexpr int kAuxRMW = ZF_AUX_RMW;      // streams read and written back
 
 // bf16 x 8 (four dwords) -> fp32 x 8
@@ -198,7 +207,7 @@ __device__ __forceinline__ void cm_adam_vec(rsrc_t rG, rsrc_t rP, rsrc_t rM, rsr
     f32x8_store<kAuxRMW>(rP, e * 4, p[q]);
     f32x8_store<kAuxRMW>(rM, e * 4, m[q]);
     f32x8_store<kAuxRMW>(rV, e * 4, v[q]);
-    buf_put_b128<kAuxWO>(narrow8(p[q]), rW, e * 2, 0);
+    buf_put_b128<kAuxW>(narrow8(p[q]), rW, e * 2, 0);
   }
 }
 
@@ -224,7 +233,7 @@ __device__ __forceinline__ void cm_adam_elem(rsrc_t rG, rsrc_t rP, rsrc_t rM, rs
     buf_put_f32<kAuxRMW>(p, rP, o * 4, 0);
     buf_put_f32<kAuxRMW>(m, rM, o * 4, 0);
     buf_put_f32<kAuxRMW>(v, rV, o * 4, 0);
-    buf_put_u16<kAuxWO>(round_bf16(p), rW, o * 2, 0);
+    buf_put_u16<kAuxW>(round_bf16(p), rW, o * 2, 0);
   }
 }
 
@@ -256,7 +265,7 @@ __device__ __forceinline__ void cm_pack_vec(rsrc_t rG, rsrc_t rA, double& ss,
       for (int i = 0; i < kGroup; ++i) a[q][i] = a[q][i] * scale;
       f32x8_store<kAuxWO>(rOut, group_elem(q, tid) * 4, a[q]);
     } else {
-      f32x8_store<FIRST ? kAuxWO : kAuxRMW>(rA, group_elem(q, tid) * 4, a[q]);
+      f32x8_store<FIRST ? kAuxAFirst : kAuxRMW>(rA, group_elem(q, tid) * 4, a[q]);
     }
   }
 }
@@ -270,7 +279,7 @@ __device__ __forceinline__ void cm_pack_elem(rsrc_t rG, rsrc_t rA, int64_t len, 
     const float a = FIRST ? g : buf_f32<kAuxRMW>(rA, o * 4, 0) + g;
     if constexpr (STATS) ss = __builtin_fma(static_cast<double>(a), static_cast<double>(a), ss);
     if constexpr (HAND) buf_put_f32<kAuxWO>(a * scale, rOut, o * 4, 0);
-    else buf_put_f32<FIRST ? kAuxWO : kAuxRMW>(a, rA, o * 4, 0);
+    else buf_put_f32<FIRST ? kAuxAFirst : kAuxRMW>(a, rA, o * 4, 0);
   }
 }
 
