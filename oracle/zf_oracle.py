@@ -304,25 +304,32 @@ def _is_refresh(t: int, R: int) -> bool:
     return (t - 1) % R == 0
 
 
-def _is_start(t: int, R: int, S: int) -> bool:
-    return _is_refresh(t, R) or (t - 1) % S == 0
+def _is_start(t: int, R: int, S: int, warmup: int = 0) -> bool:
+    if t <= warmup + 1:
+        return True
+    return _is_refresh(t, R) or (t - warmup - 1) % S == 0
 
 
-def schedule(t: int, R: int, S: int) -> StepKind:
+def schedule(t: int, R: int, S: int, warmup: int = 0) -> StepKind:
     """Step kinds for 1-based step t, selection refresh interval R and
     accumulation interval S.  Reading: the selection is recomputed when
     (t-1) mod R = 0 (index reuse between refreshes, Gradient Selection
     "Temporal Locality"); an interval starts every S steps (the t mod S rule
     of the Convergence Analysis) and also at every refresh, because the packed
     layout follows the selection; an interval ends right before the next
-    one starts."""
-    if t < 1 or R < 1 or S < 1:
-        raise ValueError("t, R and S are 1-based / positive")
+    one starts.
+
+    warmup = tau: the first tau steps are synchronous (Convergence Analysis,
+    "Warm-up mitigates early-stage staleness"), read as intervals of one
+    step -- the unselected part is handed over after every step, so it is
+    never stale -- and the S-step intervals count from step tau + 1."""
+    if t < 1 or R < 1 or S < 1 or warmup < 0:
+        raise ValueError("t, R and S are 1-based / positive, warmup >= 0")
     start = t
-    while not _is_start(start, R, S):
+    while not _is_start(start, R, S, warmup):
         start -= 1
     return StepKind(refresh=_is_refresh(t, R), step_in_interval=t - start + 1,
-                    interval_end=_is_start(t + 1, R, S))
+                    interval_end=_is_start(t + 1, R, S, warmup))
 
 
 # ---------------------------------------------------------------------------
@@ -337,7 +344,8 @@ class MatrixOracle:
 
     def __init__(self, master: np.ndarray, W: np.ndarray, ratio: float,
                  lr: float, beta1: float, beta2: float, eps: float,
-                 weight_decay: float, R: int, S: int):
+                 weight_decay: float, R: int, S: int, warmup: int = 0):
+        self.warmup = warmup
         self.master = np.asarray(master, dtype=np.float32)
         self.W = np.array(W, dtype=np.uint16, copy=True)
         self.n, self.m = self.W.shape
@@ -351,8 +359,8 @@ class MatrixOracle:
 
     def step(self, G: np.ndarray) -> dict:
         """One step of the fixed schedule (refresh every R steps, intervals
-        of S steps)."""
-        kind = schedule(self.t + 1, self.R, self.S)
+        of S steps after `warmup` one-step intervals)."""
+        kind = schedule(self.t + 1, self.R, self.S, self.warmup)
         out = self.advance(G, kind.refresh, kind.step_in_interval)
         out["kind"] = kind
         if kind.interval_end:
@@ -477,7 +485,9 @@ class OffloadOracle:
     columns of W change)."""
 
     def __init__(self, master: np.ndarray, W: np.ndarray, ratio: float, lr: float,
-                 beta1: float, beta2: float, eps: float, weight_decay: float, R: int, S: int):
+                 beta1: float, beta2: float, eps: float, weight_decay: float, R: int, S: int,
+                 warmup: int = 0):
+        self.warmup = warmup
         master = np.asarray(master, dtype=np.float32)
         self.W = np.array(W, dtype=np.uint16, copy=True)
         self.n, self.m = self.W.shape
@@ -494,8 +504,9 @@ class OffloadOracle:
 
     def step(self, G: np.ndarray) -> dict:
         """One step of the fixed schedule (refresh every R steps, intervals
-        of S steps), the deferred update at every interval end."""
-        kind = schedule(self.t + 1, self.R, self.S)
+        of S steps after `warmup` one-step intervals), the deferred update
+        at every interval end."""
+        kind = schedule(self.t + 1, self.R, self.S, self.warmup)
         out = self.advance(G, kind.refresh, kind.step_in_interval)
         out["kind"] = kind
         if kind.interval_end:
@@ -607,9 +618,10 @@ class ZenAutoOracle:
     is the fixed schedule with S = S_max whenever R is a multiple of S_max
     (or R = 1)."""
 
-    def __init__(self, oracles, R: int, S_max: int, tau: float):
+    def __init__(self, oracles, R: int, S_max: int, tau: float, warmup: int = 0):
         self.orcs = list(oracles)
         self.R, self.S_max, self.tau = R, S_max, tau
+        self.warmup = warmup  # the first `warmup` steps hand over after every step
         self.t = 0
         self.length = 0
         self.ended = True
@@ -617,11 +629,12 @@ class ZenAutoOracle:
     def step(self, grads) -> dict:
         self.t += 1
         refresh = _is_refresh(self.t, self.R)
-        self.length = 1 if (refresh or self.ended) else self.length + 1
+        self.length = 1 if (refresh or self.ended or self.t <= self.warmup) else self.length + 1
         outs = [o.advance(G, refresh, self.length) for o, G in zip(self.orcs, grads)]
         stats = [zen_auto_stats(G, o.sel, o.A) for o, G in zip(self.orcs, grads)]
         tot = zen_auto_trigger(stats, self.tau)
-        end = tot.trigger or self.length >= self.S_max or _is_refresh(self.t + 1, self.R)
+        end = (tot.trigger or self.length >= self.S_max or _is_refresh(self.t + 1, self.R)
+               or self.t <= self.warmup)
         self.ended = end
         res = {"refresh": refresh, "step_in_interval": self.length, "interval_end": end,
                "totals": tot, "stats": stats, "outs": outs}

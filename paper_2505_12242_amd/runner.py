@@ -68,17 +68,23 @@ class StepKind:
     interval_end: bool
 
 
-def schedule(t: int, R: int, S: int) -> StepKind:
+def schedule(t: int, R: int, S: int, warmup: int = 0) -> StepKind:
     """Refresh when (t-1) mod R == 0; an accumulation interval starts every S
-    steps and at every refresh, and ends right before the next start."""
-    if t < 1 or R < 1 or S < 1:
-        raise ValueError("t, R and S must be >= 1")
-    last_refresh = t - (t - 1) % R
-    last_s_start = t - (t - 1) % S
-    start = max(last_refresh, last_s_start)
+    steps and at every refresh, and ends right before the next start.  The
+    first `warmup` steps are synchronous (intervals of one step: the paper's
+    warm-up without staleness); the S-step grid counts from step warmup + 1."""
+    if t < 1 or R < 1 or S < 1 or warmup < 0:
+        raise ValueError("t, R and S must be >= 1 and warmup >= 0")
+
+    def last_start(x):
+        if x <= warmup + 1:
+            return x
+        return max(x - (x - 1) % R, x - (x - warmup - 1) % S)
+
+    start = last_start(t)
     nxt = t + 1
-    return StepKind(refresh=(t - 1) % R == 0, step_in_interval=t - start + 1,
-                    interval_end=(nxt - 1) % R == 0 or (nxt - 1) % S == 0)
+    end = nxt <= warmup + 1 or (nxt - 1) % R == 0 or (nxt - warmup - 1) % S == 0
+    return StepKind(refresh=(t - 1) % R == 0, step_in_interval=t - start + 1, interval_end=end)
 
 
 class _NoRecord:
@@ -104,10 +110,12 @@ class SelectiveUpdateRunner:
                  init_master: Optional[Sequence[torch.Tensor]] = None,
                  device=None, keep_unpacked: bool = True, layout: int = ROW_MAJOR,
                  zen_tau: Optional[float] = None, offload: bool = False, overlap: bool = True,
-                 host_threads: Optional[int] = None, fuse_handover: bool = True):
+                 host_threads: Optional[int] = None, fuse_handover: bool = True,
+                 warmup: int = 0):
         self.device = torch.device(device) if device is not None else torch.device("cuda")
         self.shapes = [(int(n), int(m)) for n, m in shapes]
         self.ratio, self.hp, self.R, self.S = ratio, hp, int(refresh), int(accum)
+        self.warmup = int(warmup)
         self.ks = [k_from_ratio(ratio, m) for _, m in self.shapes]
         self.layout = layout
         self.offload = bool(offload)
@@ -217,11 +225,11 @@ class SelectiveUpdateRunner:
         self.t += 1
         t = self.t
         if self.zen_tau is None:
-            kind = schedule(t, self.R, self.S)
+            kind = schedule(t, self.R, self.S, self.warmup)
             refresh, length = kind.refresh, kind.step_in_interval
         else:
             refresh = (t - 1) % self.R == 0
-            length = 1 if (refresh or self._ended) else self._length + 1
+            length = 1 if (refresh or self._ended or t <= self.warmup) else self._length + 1
             self._length = length
         if self.offload:
             self._before_step(refresh, length, st, rec)
@@ -254,7 +262,8 @@ class SelectiveUpdateRunner:
                 self._zen_host.copy_(self.zen_totals, non_blocking=True)
             st.synchronize()
             self.last_totals = ZenTotals.from_bytes(self._zen_host.numpy().tobytes())
-            end = self.last_totals.trigger or length >= self.S or t % self.R == 0
+            end = (self.last_totals.trigger or length >= self.S or t % self.R == 0
+                   or t <= self.warmup)
             self._ended = end
             kind = StepKind(refresh=refresh, step_in_interval=length, interval_end=end)
         if end:
@@ -336,6 +345,13 @@ class SelectiveUpdateRunner:
         self._job = self._pool.submit(self._host_update, scale, self.th, copied,
                                       self._ev_scatter)
         self.cur_a = 1 - a
+        if self.t <= self.warmup:
+            # warm-up: synchronous, the update lands before the next step
+            t0 = time.perf_counter()
+            self._job.result()
+            self.stall_s += time.perf_counter() - t0
+            self._job = None
+            self._scatter(st, rec)
 
     def sync(self, stream=None) -> None:
         """Finishes every outstanding deferred update and write-back and

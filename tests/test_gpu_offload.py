@@ -207,20 +207,22 @@ def _inputs(shapes, T_, seed, layout, dev):
 
 @pytest.mark.timeout(600)
 @pytest.mark.parametrize("overlap", [False, True])
-@pytest.mark.parametrize("R,S", [(2, 2), (6, 2)])
+@pytest.mark.parametrize("R,S,W", [(2, 2, 0), (6, 2, 0), (6, 2, 3)])
 @pytest.mark.parametrize("layout", LAYOUTS)
-def test_offloaded_steps_match_oracle(layout, R, S, overlap):
+def test_offloaded_steps_match_oracle(layout, R, S, W, overlap):
+    """W > 0: the first W steps are synchronous (one-step intervals, each
+    deferred update landing before the next step)."""
     T_ = 8
     dev = torch.device("cuda")
     slots, host, weights, w0 = _inputs(SET, T_, 21, layout, dev)
     runner = zf.SelectiveUpdateRunner(SET, 0.1, HP, R, S, slots, weights, device=dev,
                                       layout=layout, offload=True, overlap=overlap,
-                                      host_threads=4)
+                                      host_threads=4, warmup=W)
     orcs = [O.OffloadOracle(O.widen(w0[q]), w0[q], 0.1, HP.lr, HP.beta1, HP.beta2, HP.eps,
-                            HP.weight_decay, R, S) for q in range(len(SET))]
+                            HP.weight_decay, R, S, warmup=W) for q in range(len(SET))]
     changed = 0
     for t in range(1, T_ + 1):
-        print(f"# offload layout={layout} R={R} S={S} overlap={overlap} step {t}",
+        print(f"# offload layout={layout} R={R} S={S} W={W} overlap={overlap} step {t}",
               file=sys.stderr, flush=True)
         prev = [s.sel_idx.cpu().numpy().copy() for s in runner.selection] if t > 1 else None
         kind = runner.step()

@@ -263,3 +263,24 @@ def test_zen_auto_drives_the_deferred_update():
     for step in grads:
         assert za0.step(step)["interval_end"]
     assert all(o.th == len(grads) for o in za0.orcs)
+
+
+def test_warmup_steps_are_not_stale():
+    """During the warm-up every step hands over (intervals of one step), so
+    with nothing selected the offloaded optimizer is torch's Adam stepping on
+    every gradient (no accumulation, no staleness)."""
+    rng = np.random.default_rng(11)
+    n, m, T = 12, 10, 6
+    master = (rng.standard_normal((n, m)) * 0.02).astype(np.float32)
+    orc = O.OffloadOracle(master, bf16(master), 0.0, 1e-3, 0.9, 0.999, 1e-8, 0.0, R=4, S=4,
+                          warmup=T)
+    p = torch.nn.Parameter(torch.from_numpy(master.copy()))
+    opt = torch.optim.Adam([p], lr=1e-3, betas=(0.9, 0.999), eps=1e-8, foreach=False)
+    for _ in range(T):
+        G = bf16(rng.standard_normal((n, m)) * np.exp(rng.standard_normal(m)))
+        assert orc.step(G)["kind"].interval_end
+        p.grad = torch.from_numpy(O.widen(G).copy())
+        opt.step()
+    tp = p.detach().numpy()
+    assert orc.th == T
+    assert np.all(np.abs(orc.store[0] - tp) <= 2e-6 * np.abs(tp) + 1e-9)

@@ -51,3 +51,36 @@ def test_bad_arguments():
     for args in [(0, 4, 4), (1, 0, 4), (1, 4, 0)]:
         with pytest.raises(ValueError):
             schedule(*args)
+
+
+def test_warmup_zero_is_the_plain_schedule():
+    for R, S in itertools.product(range(1, 7), range(1, 7)):
+        for t in range(1, 40):
+            assert schedule(t, R, S, 0) == schedule(t, R, S)
+
+
+def test_warmup_table():
+    """tau = 3, R = 8, S = 4: one-step intervals at t = 1..3, then S-step
+    intervals counted from t = 4 (4..7, 8), cut by the refresh at 9."""
+    ks = [schedule(t, 8, 4, 3) for t in range(1, 14)]
+    assert [t for t, k in enumerate(ks, 1) if k.interval_end] == [1, 2, 3, 7, 8, 11]
+    assert [k.step_in_interval for k in ks] == [1, 1, 1, 1, 2, 3, 4, 1, 1, 2, 3, 1, 2]
+    assert [t for t, k in enumerate(ks, 1) if k.refresh] == [1, 9]
+
+
+def test_warmup_longer_than_the_run_hands_over_every_step():
+    for k in (schedule(t, 4, 4, 50) for t in range(1, 51)):
+        assert k.step_in_interval == 1 and k.interval_end
+
+
+@pytest.mark.parametrize("R,S,W", list(itertools.product([1, 2, 4, 7], [1, 3, 4], [0, 1, 5])))
+def test_warmup_consistency(R, S, W):
+    """Lengths increase by one inside an interval and restart at 1 right
+    after every end; an interval never exceeds S steps after the warm-up and
+    one step within it."""
+    prev_end = True
+    for t in range(1, 40):
+        k = schedule(t, R, S, W)
+        assert k.step_in_interval == (1 if prev_end else prev_len + 1)
+        assert k.step_in_interval <= (1 if t <= W else S)
+        prev_end, prev_len = k.interval_end, k.step_in_interval
