@@ -50,7 +50,31 @@ def build(verbose: bool = False) -> str:
     if verbose and noise:
         sys.stderr.write("\n".join(noise) + "\n")
     os.replace(tmp, LIB)
+    build_abi_smoke(verbose)
     return LIB
+
+
+ABI_SMOKE_SRC = os.path.join(ROOT, "tests", "abi", "abi_smoke.cpp")
+ABI_SMOKE_BIN = os.path.join(ROOT, "tests", "abi", "abi_smoke")
+
+
+def build_abi_smoke(verbose: bool = False) -> str:
+    """The C++ consumer of the C ABI used by the native GPU test (links
+    libzf.so from the package directory through its rpath)."""
+    if not os.path.exists(ABI_SMOKE_SRC):
+        return ""
+    tmp = ABI_SMOKE_BIN + ".tmp"
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-O2", "-std=c++17", "-Wall", "-I", INCLUDE,
+           ABI_SMOKE_SRC, "-L", PKG, "-lzf", "-Wl,-rpath,$ORIGIN/../../paper_2505_12242_amd",
+           "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    proc = subprocess.run(cmd, capture_output=True, text=True)
+    if proc.returncode != 0:
+        sys.stderr.write(proc.stdout + proc.stderr)
+        raise RuntimeError(f"hipcc failed on the ABI smoke program (exit {proc.returncode})")
+    os.replace(tmp, ABI_SMOKE_BIN)
+    return ABI_SMOKE_BIN
 
 
 if __name__ == "__main__":
