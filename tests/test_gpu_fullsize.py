@@ -30,10 +30,13 @@ bench = pytest.importorskip("bench")
 CASES = {
     # first selection, accumulation, hand-over at 4, refresh + remap at 5, hand-over at 8
     "llama2-7b-full": (["embed_tokens", "layers.0.q_proj", "layers.0.down_proj",
-                        "layers.17.gate_proj", "layers.31.v_proj", "lm_head"], 8, 3),
-    # one R = S = 8 interval of the 70B share: heavy-tailed scales, GQA k/v
-    # (1024 rows), a 28672-channel down projection
-    "llama2-70b-10layers": (["layers.0.k_proj", "layers.9.down_proj"], 8, 3),
+                        "layers.17.gate_proj", "layers.31.v_proj", "lm_head"], 8, 3, []),
+    # one R = S = 8 interval of the 70B share: heavy-tailed scales, the GQA k/v
+    # weight (1024 rows) against the oracle in full, and a 28672-channel down
+    # projection through cheaper checks (its selection against the oracle's
+    # top-k of the device scores; its hand-over recomputed on the device in
+    # the kernels' fp32 order)
+    "llama2-70b-10layers": (["layers.0.k_proj"], 8, 3, ["layers.9.down_proj"]),
 }
 
 
@@ -45,7 +48,7 @@ def logical(t):
 @pytest.mark.parametrize("name", sorted(CASES))
 def test_full_set_sampled_parity(name):
     from workloads import get_workload
-    SAMPLES, STEPS, NSLOTS = CASES[name]
+    SAMPLES, STEPS, NSLOTS, LIGHT = CASES[name]
     wl = get_workload(name)
     hp = zf.AdamHparams(wl.hyper.lr, wl.hyper.beta1, wl.hyper.beta2, wl.hyper.eps,
                         wl.hyper.weight_decay)
@@ -54,6 +57,7 @@ def test_full_set_sampled_parity(name):
     shapes, ks, slots, weights = bench.build_set(wl, NSLOTS, dev, layout)
     names = [mt.name for mt in wl.matrices]
     qs = [names.index(s) for s in SAMPLES]
+    light = [names.index(s) for s in LIGHT]
     w0 = {q: bits_np(logical(weights[q]).contiguous()) for q in qs}
     g_host = {(q, s): bits_np(logical(slots[s][q]).contiguous()) for q in qs
               for s in range(NSLOTS)}
@@ -67,6 +71,26 @@ def test_full_set_sampled_parity(name):
         slot = (t - 1) % NSLOTS
         print(f"# step {t} ({'refresh' if kind.refresh else 'accumulate'})", file=sys.stderr,
               flush=True)
+        for q in light:
+            if kind.refresh:
+                # exact top-k of the device's own scores
+                want = O.select_topk(f32_np(runner.norms[q]), ks[q])
+                got = runner.selection[q]
+                assert np.array_equal(got.sel_idx.cpu().numpy(), want.sel), (names[q], t)
+                assert np.array_equal(mask_np(got.mask), want.mask), (names[q], t)
+            if kind.interval_end:
+                # hand-over = fp32(1/length) * (((g_1 + g_2) + ...) + g_t) at the
+                # unselected channels, +0.0 at the selected ones (channel rows)
+                unsel = runner.selection[q].unsel_idx.long()
+                start = t - kind.step_in_interval + 1
+                acc = slots[(start - 1) % NSLOTS][q].float()[unsel]
+                for tt in range(start + 1, t + 1):
+                    acc = acc + slots[(tt - 1) % NSLOTS][q].float()[unsel]
+                want = torch.zeros_like(runner.unpacked[q])
+                want[unsel] = acc * torch.tensor(np.float32(1.0 / kind.step_in_interval),
+                                                 device=acc.device)
+                assert torch.equal(runner.unpacked[q].view(torch.int32),
+                                   want.view(torch.int32)), (names[q], t)
         if kind.refresh:
             for q, (n, m) in enumerate(shapes):
                 s = f32_np(runner.norms[q]).astype(np.float64)
