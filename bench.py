@@ -36,7 +36,7 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2505_12242_amd", "csrc", f)
                   for f in ("zf_device.hpp", "zf_internal.hpp", "zf_kernels.hip",
-                            "zf_kernels_cm.hip")]
+                            "zf_kernels_cm.hip", "zf_kernels_rv.hip", "zf_api.hip")]
 
 
 def parse_args(argv=None):
@@ -389,7 +389,9 @@ def main(argv=None) -> int:
         },
         "kernels": kernels,
         "roofline": {
-            "kernel": upd_kernel + " (fused Adam + bf16 write-back + pack)",
+            "kernel": (upd_kernel if layout == zf.CHANNEL_MAJOR else
+                       "rv_update_kernel (steps in place, hand-over) and update_kernel "
+                       "(refresh steps)") + " (fused Adam + bf16 write-back + pack)",
             "bound": "hbm",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,

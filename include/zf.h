@@ -53,6 +53,11 @@
  *           the unpack output are [m][ld >= n], P/M/V are [k][ld_state >= n]
  *           (row r = column sel_idx[r]), A is [m-k][ld_acc >= n] (row u =
  *           column unsel_idx[u]).  Results are identical in both layouts.
+ *           Row-major update steps with the states in place (and pack-only
+ *           calls) run a kernel with 16-byte accesses when G is 16-byte
+ *           aligned with ld % 8 == 0 and A, P/M/V and the hand-over output
+ *           (those the call uses) are 16-byte aligned with ld % 4 == 0;
+ *           otherwise a per-column kernel.  The results are identical.
  * Selection.  sel_idx[k] and unsel_idx[m-k] are ascending column indices;
  *           sel_mask[ceil(m/64)] has bit b of word w set iff column 64w+b is
  *           selected (bits at columns >= m are 0); sel_prefix[ceil(m/64)]

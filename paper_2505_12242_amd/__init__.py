@@ -24,6 +24,7 @@ from ._lib import (  # noqa: F401
     ZenTotals,
     ZfError,
     adam_selected,
+    alloc_stored,
     colnorm,
     colnorm_workspace_bytes,
     host_adam_unselected,

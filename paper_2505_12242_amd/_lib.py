@@ -193,6 +193,29 @@ def _stored(layout: int, rows_l: int, cols_l: int):
     return (rows_l, cols_l) if layout == ROW_MAJOR else (cols_l, rows_l)
 
 
+def alloc_stored(layout: int, rows_l: int, cols_l: int, dtype=torch.float32,
+                 device="cuda", pin_memory: bool = False) -> torch.Tensor:
+    """Uninitialised storage of a logical rows_l x cols_l matrix in `layout`.
+    Row-major rows are padded to a multiple of 16 bytes (the returned tensor
+    is a view of the first cols_l columns), which lets the row-major update
+    move packed buffers, compact states and hand-over rows 16 bytes at a
+    time; channel-major storage is dense.  pin_memory: pinned host memory."""
+    kw = dict(dtype=dtype, pin_memory=True) if pin_memory else dict(dtype=dtype, device=device)
+    if layout != ROW_MAJOR:
+        return torch.empty(*_stored(layout, rows_l, cols_l), **kw)
+    per = 16 // torch.empty(0, dtype=dtype).element_size()
+    ld = max(per, -(-cols_l // per) * per)
+    return torch.empty(rows_l, ld, **kw)[:, :cols_l]
+
+
+def padded_block(t: torch.Tensor) -> torch.Tensor:
+    """The rows of a 2-D view including their padding (a dense tensor over
+    the same memory), e.g. for one contiguous copy of a padded buffer."""
+    if t.dim() != 2 or t.shape[0] == 0 or t.stride(1) != 1:
+        return t
+    return t.as_strided((t.shape[0], t.stride(0)), (t.stride(0), 1))
+
+
 def _lmat(t, dtype, name, layout, rows_l=None, cols_l=None, **kw) -> int:
     r, c = (rows_l, cols_l) if layout == ROW_MAJOR else (cols_l, rows_l)
     return _mat(t, dtype, name, r, c, **kw)
@@ -384,7 +407,7 @@ def update_fused_handover(grad, sel: Selection, master, exp_avg, exp_avg_sq, wei
     ldw = _lmat(weight, torch.bfloat16, "weight", layout, n, m)
     lda = _lmat(acc, torch.float32, "acc", layout, n, m - sel.k)
     if out is None:
-        out = torch.empty(*_stored(layout, n, m), dtype=torch.float32, device=grad.device)
+        out = alloc_stored(layout, n, m, torch.float32, grad.device)
     ldo = _lmat(out, torch.float32, "out", layout, n, m)
     c_sel, c_hp = sel.as_c(), hp.as_c()
     c_src = src.as_c() if src is not None else None
@@ -402,7 +425,7 @@ def unpack(acc, sel: Selection, scale: float = 1.0, out: Optional[torch.Tensor] 
     n = acc.shape[0] if layout == ROW_MAJOR else acc.shape[1]
     lda = _lmat(acc, torch.float32, "acc", layout, n, m - sel.k)
     if out is None:
-        out = torch.empty(*_stored(layout, n, m), dtype=torch.float32, device=acc.device)
+        out = alloc_stored(layout, n, m, torch.float32, acc.device)
     ldo = _lmat(out, torch.float32, "out", layout, n, m)
     c_sel = sel.as_c()
     _check("zf_unpack", LIB.zf_unpack(_ptr(acc), lda, ctypes.byref(c_sel), sel.k, n, m, layout,

@@ -131,6 +131,40 @@ int pick_update_rows(const std::vector<std::pair<int64_t, int64_t>>& shapes) {
   }
 }
 
+// Row-major update with 16-byte accesses: equal-width column tiles of at
+// most kRvMaxCols columns (multiples of 8, so that 16-byte G loads and
+// hand-over stores stay aligned) and rv_rows rows per block.
+#ifndef ZF_RV_ROWS
+#define ZF_RV_ROWS 16
+#endif
+#ifndef ZF_RV_ENABLE
+#define ZF_RV_ENABLE 1
+#endif
+
+int32_t rv_width(int64_t m) {
+  const int64_t tiles = std::max<int64_t>(1, ceil_div(m, zf::kRvMaxCols));
+  return static_cast<int32_t>(8 * ceil_div(std::max<int64_t>(m, 1), 8 * tiles));
+}
+
+int64_t rv_blocks(int64_t n, int64_t m, int rows) {
+  if (n <= 0 || m <= 0) return 0;
+  return ceil_div(m, rv_width(m)) * ceil_div(n, rows);
+}
+
+int pick_rv_rows(const std::vector<std::pair<int64_t, int64_t>>& shapes) {
+  int rows = ZF_RV_ROWS;
+  for (;;) {
+    int64_t total = 0;
+    for (auto& s : shapes) total += rv_blocks(s.first, s.second, rows);
+    if (total > kMaxBlocks && rows < (1 << 20)) {
+      rows <<= 1;
+      continue;
+    }
+    if (total >= kMinBlocks || rows <= 4) return rows;
+    rows >>= 1;
+  }
+}
+
 void set_geometry(DevMat& d, int cn_rows, int up_rows) {
   d.cn_rpb = cn_rows;
   d.cn_cb = static_cast<int32_t>(ceil_div(d.m, zf::kColnormCols));
@@ -322,13 +356,38 @@ bool cm_vec_ok(const DevMat& d) {
          ok(d.st_M, d.ld_store, 4) && ok(d.st_V, d.ld_store, 4);
 }
 
-// Row-major update/unpack blocks address up_rows rows through 32-bit buffer
-// offsets: every row stride times up_rows must stay below 2^31 bytes.
-bool rm_strides_ok(const DevMat& d) {
-  const int64_t lim = (int64_t(1) << 31) / std::max<int64_t>(d.up_rows, 1);
+// Row-major 16-byte update: G rows 16-byte aligned (8 bf16), and every
+// fp32 buffer moved in slot quads or column quads (A, P/M/V, the hand-over
+// output) 16-byte aligned per row.  Other buffers are accessed by element.
+bool rv_ok(const DevMat& d) {
+  if (!ZF_RV_ENABLE || d.layout != zf::kRowMajor) return false;
+  const auto ok = [](const void* p, int64_t ld, int64_t per16) {
+    return p == nullptr || (aligned(p, 16) && ld % per16 == 0);
+  };
+  return d.grad != nullptr && aligned(d.grad, 16) && d.ld_grad % 8 == 0 &&
+         ok(d.acc, d.ld_acc, 4) && ok(d.P, d.ld_state, 4) && ok(d.M, d.ld_state, 4) &&
+         ok(d.V, d.ld_state, 4) && ok(d.out, d.ld_out, 4);
+}
+
+// Geometry of the row-major 16-byte update; used when `allow` (all matrices
+// of a plan qualify) and this matrix qualifies.
+// Row-major update/unpack blocks address `rows` rows through 32-bit buffer
+// offsets: every row stride times the rows of a block must stay below 2^31
+// bytes.
+bool strides_fit(const DevMat& d, int64_t rows) {
+  const int64_t lim = (int64_t(1) << 31) / std::max<int64_t>(rows, 1);
   return d.ld_grad * 2 < lim && d.ld_weight * 2 < lim && d.ld_state * 4 < lim &&
          d.ld_acc * 4 < lim && d.ld_out * 4 < lim && d.ld_prev * 4 < lim && d.ld_init * 4 < lim &&
          d.ld_store * 4 < lim;
+}
+
+bool rm_strides_ok(const DevMat& d) { return strides_fit(d, d.up_rows); }
+
+void set_rv(DevMat& d, int rows, bool allow) {
+  d.rv_w = rv_width(d.m);
+  d.rv_cb = d.m > 0 ? static_cast<int32_t>(ceil_div(d.m, d.rv_w)) : 0;
+  d.rv_rows = rows;
+  d.rv = (allow && rv_ok(d) && strides_fit(d, rows)) ? 1 : 0;
 }
 
 void finish_geometry(DevMat& d, int cn_rows, int up_rows) {
@@ -373,13 +432,26 @@ int64_t unpack_grid(const DevMat& d) {
   return update_blocks(d.n, d.m, d.up_rows);
 }
 
+// Row-major: the 16-byte kernel serves the steps without a refresh (states in
+// place, or no Adam); a refresh step (remap / init, whose per-column sources
+// it reads element by element) runs the per-column kernel.  Both give the
+// same bits.
+bool use_rv(const DevMat& one, int32_t mode, bool adam) {
+  return one.layout == zf::kRowMajor && one.rv && (!adam || mode == zf::kInplace);
+}
+
+int64_t rv_grid(const DevMat& d) { return rv_blocks(d.n, d.m, d.rv_rows); }
+
+// `rv` selects the row-major 16-byte kernel; t / blocks are then its table
+// and grid.
 hipError_t launch_update_any(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
                              int32_t mode, int32_t first, bool adam, bool pack, int32_t layout,
-                             hipStream_t s, bool handover = false, float scale = 1.0f) {
-  return layout == zf::kChannelMajor
-             ? zf::launch_cm_update(t, one, blocks, c, mode, first, adam, pack, nullptr, handover,
-                                    scale, s)
-             : zf::launch_update(t, one, blocks, c, mode, first, adam, pack, handover, scale, s);
+                             hipStream_t s, bool handover, float scale, bool rv) {
+  if (layout == zf::kChannelMajor)
+    return zf::launch_cm_update(t, one, blocks, c, mode, first, adam, pack, nullptr, handover,
+                                scale, s);
+  if (rv) return zf::launch_rv_update(t, one, blocks, c, mode, first, adam, pack, handover, scale, s);
+  return zf::launch_update(t, one, blocks, c, mode, first, adam, pack, handover, scale, s);
 }
 
 hipError_t launch_unpack_any(const Table& t, const DevMat& one, int64_t blocks, float scale,
@@ -446,12 +518,14 @@ zf_status run_update(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad
   }
   if (!handover && (!adam || k == 0) && (!pack || k == m)) return ZF_OK;  // no column to touch
   finish_geometry(d, 256, pick_update_rows({{n, m}}));
+  set_rv(d, pick_rv_rows({{n, m}}), true);
   if (layout == zf::kRowMajor && !rm_strides_ok(d)) return ZF_EINVAL;
-  const int64_t blocks = update_grid(d);
+  const bool rv = use_rv(d, mode, adam);
+  const int64_t blocks = rv ? rv_grid(d) : update_grid(d);
   if (blocks == 0) return ZF_OK;
   const hipError_t e = launch_update_any(single_table(), d, blocks, c, adam ? mode : 0,
                                          sii == 1 ? 1 : 0, adam, pack, layout,
-                                         as_stream(stream), handover, scale);
+                                         as_stream(stream), handover, scale, rv);
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
@@ -652,10 +726,12 @@ struct zf_plan {
   int64_t* d_off_unp = nullptr;
   int64_t* d_off_zen = nullptr;
   int64_t* d_off_zp = nullptr;  // row-major Zen-auto partial pass
+  int64_t* d_off_upv = nullptr;  // row-major 16-byte update
   double* d_ws = nullptr;
   double* d_zs = nullptr;  // Zen-auto per-wave partials
   double* d_zb = nullptr;  // Zen-auto per-finalize-block sums
-  int64_t blk_cn = 0, blk_fin = 0, blk_top = 0, blk_up = 0, blk_unp = 0, blk_zen = 0, blk_zp = 0;
+  int64_t blk_cn = 0, blk_fin = 0, blk_top = 0, blk_up = 0, blk_unp = 0, blk_zen = 0, blk_zp = 0,
+          blk_upv = 0;
   int64_t k_total = 0, u_total = 0;
   bool can_colnorm = true, can_topk = true, can_adam = true, can_remap = true, can_pack = true,
        can_unpack = true, can_zen = true, can_scatter = true, can_handover = true;
@@ -769,14 +845,24 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   }
   const int cn_rows = pick_colnorm_rows(shapes);
   const int up_rows = pick_update_rows(shapes);
+  const int rv_rows = pick_rv_rows(shapes);
+  // the row-major 16-byte update serves the plan if every matrix qualifies
+  bool all_rv = p->layout == zf::kRowMajor;
+  for (int32_t q = 0; q < nmats && all_rv; ++q) {
+    DevMat d = plan_mat(mats[q]);
+    finish_geometry(d, cn_rows, up_rows);
+    all_rv = rv_ok(d) && strides_fit(d, rv_rows);
+  }
   std::vector<int64_t> off_cn(nmats + 1), off_fin(nmats + 1), off_top(nmats + 1),
-      off_up(nmats + 1), off_unp(nmats + 1), off_zen(nmats + 1), off_zp(nmats + 1);
+      off_up(nmats + 1), off_unp(nmats + 1), off_zen(nmats + 1), off_zp(nmats + 1),
+      off_upv(nmats + 1);
   int64_t ws_doubles = 0, zs_doubles = 0;
   const bool cm = p->layout == zf::kChannelMajor;
   p->mats.resize(nmats);
   for (int32_t q = 0; q < nmats; ++q) {
     DevMat d = plan_mat(mats[q]);
     finish_geometry(d, cn_rows, up_rows);
+    set_rv(d, rv_rows, all_rv);
     if (!cm && !rm_strides_ok(d)) {
       delete p;
       return ZF_EINVAL;
@@ -799,11 +885,13 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
     off_fin[q] = p->blk_fin;
     off_top[q] = p->blk_top;
     off_up[q] = p->blk_up;
+    off_upv[q] = p->blk_upv;
     off_unp[q] = p->blk_unp;
     p->blk_cn += colnorm_grid(d);
     p->blk_fin += cm ? 0 : ceil_div(d.m, zf::kFinalizeCols);
     p->blk_top += 1;
     p->blk_up += update_grid(d);
+    if (d.rv) p->blk_upv += rv_grid(d);
     p->blk_unp += unpack_grid(d);
     p->mats[q] = d;
   }
@@ -814,8 +902,10 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   off_unp[nmats] = p->blk_unp;
   off_zen[nmats] = p->blk_zen;
   off_zp[nmats] = p->blk_zp;
+  off_upv[nmats] = p->blk_upv;
   const int64_t max_blocks = (int64_t(1) << 31) / zf::kThreads;
   if (p->blk_cn >= max_blocks || p->blk_up >= max_blocks || p->blk_unp >= max_blocks ||
+      p->blk_upv >= max_blocks ||
       p->blk_zp >= max_blocks) {
     delete p;
     return ZF_EINVAL;  // grid too large for one launch
@@ -823,7 +913,7 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
 
   const size_t mats_bytes = sizeof(DevMat) * nmats;
   const size_t off_bytes = sizeof(int64_t) * (nmats + 1);
-  const size_t head = (mats_bytes + 7 * off_bytes + 255) & ~size_t(255);
+  const size_t head = (mats_bytes + 8 * off_bytes + 255) & ~size_t(255);
   const int64_t zb_doubles = p->can_zen ? 2 * p->blk_zen : 0;
   p->dev_bytes = head + sizeof(double) * static_cast<size_t>(ws_doubles + zs_doubles + zb_doubles);
   hipError_t e = hipMalloc(&p->dev, p->dev_bytes);
@@ -841,6 +931,7 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   p->d_off_unp = p->d_off_up + (nmats + 1);
   p->d_off_zen = p->d_off_unp + (nmats + 1);
   p->d_off_zp = p->d_off_zen + (nmats + 1);
+  p->d_off_upv = p->d_off_zp + (nmats + 1);
   p->d_ws = reinterpret_cast<double*>(base + head);
   p->d_zs = p->d_ws + ws_doubles;
   p->d_zb = p->d_zs + zs_doubles;
@@ -853,6 +944,7 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   std::memcpy(host.data() + mats_bytes + 4 * off_bytes, off_unp.data(), off_bytes);
   std::memcpy(host.data() + mats_bytes + 5 * off_bytes, off_zen.data(), off_bytes);
   std::memcpy(host.data() + mats_bytes + 6 * off_bytes, off_zp.data(), off_bytes);
+  std::memcpy(host.data() + mats_bytes + 7 * off_bytes, off_upv.data(), off_bytes);
   e = hipMemcpy(p->dev, host.data(), head, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     g_last_hip_error = static_cast<int>(e);
@@ -895,6 +987,24 @@ zf_status zf_plan_topk_select(zf_plan* p, zf_stream stream) {
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
+}  // extern "C"
+
+namespace {
+
+// The plan's update launch: the row-major 16-byte kernel where it applies
+// (its own block table), else the plan's update kernel.
+hipError_t plan_update_launch(const zf_plan* p, const AdamK& c, int32_t mode, int32_t first,
+                              bool adam, bool pack, bool handover, float scale, hipStream_t s) {
+  const bool rv = use_rv(p->mats[0], mode, adam);
+  const Table t{p->d_mats, rv ? p->d_off_upv : p->d_off_up, p->nmats};
+  return launch_update_any(t, p->mats[0], rv ? p->blk_upv : p->blk_up, c, adam ? mode : 0, first,
+                           adam, pack, p->layout, s, handover, scale, rv);
+}
+
+}  // namespace
+
+extern "C" {
+
 zf_status zf_plan_update(zf_plan* p, const zf_adam_hparams* hp, int64_t step, int32_t mode,
                          int64_t step_in_interval, int64_t accum_interval, int32_t do_adam,
                          int32_t do_pack, zf_stream stream) {
@@ -911,10 +1021,9 @@ zf_status zf_plan_update(zf_plan* p, const zf_adam_hparams* hp, int64_t step, in
         step_in_interval > accum_interval)
       return ZF_EINVAL;
   }
-  const Table t{p->d_mats, p->d_off_up, p->nmats};
-  const hipError_t e = launch_update_any(t, p->mats[0], p->blk_up, c, do_adam ? mode : 0,
-                                         step_in_interval == 1 ? 1 : 0, do_adam != 0,
-                                         do_pack != 0, p->layout, as_stream(stream));
+  const hipError_t e = plan_update_launch(p, c, mode, step_in_interval == 1 ? 1 : 0,
+                                          do_adam != 0, do_pack != 0, false, 1.0f,
+                                          as_stream(stream));
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
@@ -936,10 +1045,8 @@ zf_status zf_plan_update_handover(zf_plan* p, const zf_adam_hparams* hp, int64_t
   if (accum_interval < 1 || step_in_interval < 1 || step_in_interval > accum_interval)
     return ZF_EINVAL;
   const AdamK c = adam_consts(*hp, step);
-  const Table t{p->d_mats, p->d_off_up, p->nmats};
-  const hipError_t e = launch_update_any(t, p->mats[0], p->blk_up, c, mode,
-                                         step_in_interval == 1 ? 1 : 0, true, true, p->layout,
-                                         as_stream(stream), true, scale);
+  const hipError_t e = plan_update_launch(p, c, mode, step_in_interval == 1 ? 1 : 0, true, true,
+                                          true, scale, as_stream(stream));
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
@@ -972,8 +1079,7 @@ zf_status zf_plan_update_zen(zf_plan* p, const zf_adam_hparams* hp, int64_t step
     if (e != hipSuccess) return hip_fail(e);
     e = zf::launch_zen_finalize(tz, p->mats[0], p->blk_zen, p->d_zs, p->d_zb, s);
   } else {
-    e = zf::launch_update(t, p->mats[0], p->blk_up, c, mode, step_in_interval == 1 ? 1 : 0, true,
-                          true, false, 1.0f, s);
+    e = plan_update_launch(p, c, mode, step_in_interval == 1 ? 1 : 0, true, true, false, 1.0f, s);
     if (e != hipSuccess) return hip_fail(e);
     const Table tp{p->d_mats, p->d_off_zp, p->nmats};
     e = zf::launch_rm_zen(tp, p->blk_zp, tz, p->blk_zen, p->mats[0], p->d_ws, p->d_zb, s);

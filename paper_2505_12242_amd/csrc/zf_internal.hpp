@@ -19,6 +19,10 @@ constexpr int kUpdateCols = 256;
 constexpr int kFinalizeCols = 256;
 constexpr int kTopkThreads = 1024;
 
+// Row-major update with 16-byte accesses: a block covers rv_w <= kRvMaxCols
+// columns (equal-width tiles per matrix, multiples of 8) and rv_rows rows.
+constexpr int kRvMaxCols = 1000;
+
 // Channel-major layout: an update block covers one channel and
 // cm_vpt * kThreads * 8 of its rows (cm_vpt 16-byte groups per thread, at
 // most kCmVpt, chosen per matrix to fill the lanes), an unpack block one
@@ -94,6 +98,10 @@ struct DevMat {
   int32_t cm_unch;   // channel-major: row chunks per channel (unpack)
   int32_t cm_vpt;    // channel-major: 16-byte groups per thread in the update (1 or 2)
   int32_t scat_vec;  // channel-major: 16-byte path of the weight scatter
+  int32_t rv;        // row-major: the 16-byte update kernel is used (else per-column)
+  int32_t rv_w;      // row-major 16-byte update: tile width (columns)
+  int32_t rv_cb;     // row-major 16-byte update: column tiles
+  int32_t rv_rows;   // row-major 16-byte update: rows per block
 };
 
 // Per-kernel view of a batch: a device array of matrices and the first
@@ -126,6 +134,12 @@ hipError_t launch_update(const Table& t, const DevMat& one, int64_t blocks, cons
                          float scale, hipStream_t s);
 hipError_t launch_unpack(const Table& t, const DevMat& one, int64_t blocks, float scale,
                          hipStream_t s);
+
+// Row-major update with 16-byte accesses (zf_kernels_rv.hip); same contract
+// as launch_update, geometry rv_w / rv_cb / rv_rows.
+hipError_t launch_rv_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
+                            int32_t mode, int32_t first, bool adam, bool pack, bool handover,
+                            float scale, hipStream_t s);
 
 // Channel-major kernels (zf_kernels_cm.hip).
 hipError_t launch_cm_colnorm(const Table& t, const DevMat& one, int64_t blocks, hipStream_t s);

@@ -279,6 +279,12 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(const DevMat* __rest
 #ifndef ZF_ADAM_BATCH
 #define ZF_ADAM_BATCH 8
 #endif
+#ifndef ZF_RM_AUX_RO
+#define ZF_RM_AUX_RO kCached
+#endif
+#ifndef ZF_RM_AUX_W
+#define ZF_RM_AUX_W kCached
+#endif
 constexpr int kRowBatch = ZF_PACK_BATCH;   // rows in flight per pack lane (and unpack)
 constexpr int kAdamBatch = ZF_ADAM_BATCH;  // rows in flight per Adam lane
 
@@ -313,7 +319,7 @@ __device__ __forceinline__ void pack_rows(rsrc_t rG, uint32_t vG, uint32_t sG, r
     uint16_t gb[kRowBatch];
     float a[kRowBatch];
 #pragma unroll
-    for (int b = 0; b < kRowBatch; ++b) gb[b] = buf_u16(rG, vG, (i + b) * sG);
+    for (int b = 0; b < kRowBatch; ++b) gb[b] = buf_u16<ZF_RM_AUX_RO>(rG, vG, (i + b) * sG);
     if constexpr (!FIRST) {
 #pragma unroll
       for (int b = 0; b < kRowBatch; ++b) a[b] = buf_f32(rA, vA, (i + b) * sA);
@@ -330,7 +336,7 @@ __device__ __forceinline__ void pack_rows(rsrc_t rG, uint32_t vG, uint32_t sG, r
     }
   }
   for (; i < rows; ++i) {
-    const float g = widen_bf16(buf_u16(rG, vG, i * sG));
+    const float g = widen_bf16(buf_u16<ZF_RM_AUX_RO>(rG, vG, i * sG));
     const float a = FIRST ? g : buf_f32(rA, vA, i * sA) + g;
     if constexpr (HAND) buf_put_f32(a * scale, rD, vD, i * sD);
     else buf_put_f32(a, rA, vA, i * sA);
@@ -410,7 +416,7 @@ __device__ __forceinline__ void adam_rows(const AdamSrc& a, rsrc_t rG, uint32_t 
     uint16_t gb[kAdamBatch];
     float p[kAdamBatch], mm[kAdamBatch], vv[kAdamBatch];
 #pragma unroll
-    for (int b = 0; b < kAdamBatch; ++b) gb[b] = buf_u16(rG, a.vG, (i + b) * sG);
+    for (int b = 0; b < kAdamBatch; ++b) gb[b] = buf_u16<ZF_RM_AUX_RO>(rG, a.vG, (i + b) * sG);
 #pragma unroll
     for (int b = 0; b < kAdamBatch; ++b) load_state<SRC>(a, i + b, p[b], mm[b], vv[b]);
 #pragma unroll
@@ -420,18 +426,18 @@ __device__ __forceinline__ void adam_rows(const AdamSrc& a, rsrc_t rG, uint32_t 
       buf_put_f32(p[b], a.rP, a.vS, so);
       buf_put_f32(mm[b], a.rM, a.vS, so);
       buf_put_f32(vv[b], a.rV, a.vS, so);
-      buf_put_u16(round_bf16(p[b]), a.rW, a.vG, (i + b) * a.sW);
+      buf_put_u16<ZF_RM_AUX_W>(round_bf16(p[b]), a.rW, a.vG, (i + b) * a.sW);
     }
   }
   for (; i < rows; ++i) {
     float p, mm, vv;
-    const float g = widen_bf16(buf_u16(rG, a.vG, i * sG));
+    const float g = widen_bf16(buf_u16<ZF_RM_AUX_RO>(rG, a.vG, i * sG));
     load_state<SRC>(a, i, p, mm, vv);
     adam_step(g, p, mm, vv, c);
     buf_put_f32(p, a.rP, a.vS, i * a.sS);
     buf_put_f32(mm, a.rM, a.vS, i * a.sS);
     buf_put_f32(vv, a.rV, a.vS, i * a.sS);
-    buf_put_u16(round_bf16(p), a.rW, a.vG, i * a.sW);
+    buf_put_u16<ZF_RM_AUX_W>(round_bf16(p), a.rW, a.vG, i * a.sW);
   }
 }
 

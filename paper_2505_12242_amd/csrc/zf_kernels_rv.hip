@@ -1,0 +1,348 @@
+// gfx950 row-major fused update with 16-byte accesses: selective Adam with
+// bf16 write-back, packing of the unselected columns, and the fused
+// hand-over (a3-a6 in the row-major layout).
+//
+// A lane that owns one column and walks the rows moves 2- and 4-byte
+// elements; on this chip such per-lane narrow accesses stream at about two
+// thirds of the rate of 16-byte ones.  Here a block owns a tile of up to
+// kRvMaxCols columns (equal-width tiles per matrix, multiples of 8) and
+// rv_rows rows, and works in two index spaces:
+//   column space: G is loaded with one 16-byte load per lane (8 columns,
+//     two rows per block-wide load) and staged in LDS; the fused
+//     hand-over's output rows are assembled in LDS and stored with 16-byte
+//     stores;
+//   slot space: the tile's unselected slots [us, us+cu) of the accumulation
+//     buffer and its selected slots [rs, rs+cs) of the compact states are
+//     contiguous ranges.  Lanes take one of three roles:
+//       pack quad:  the aligned quads of 4 slots inside [us, us+cu), one per
+//                   lane, A moved with one 16-byte access per row;
+//       pack edge:  the at most 6 slots of the range outside whole quads
+//                   (3 at each end), one per lane, 4-byte accesses;
+//       Adam:       the remaining lanes take the selected slots in turn
+//                   (slot rs + a + j * lanes, j < 4), so consecutive lanes
+//                   hold consecutive slots: the compact states and the bf16
+//                   write-back of W coalesce as well as the layout allows.
+//     Every lane reads its slots' column indices once per block and gets
+//     G from LDS.  With tiles of at most 1000 columns the pack roles use at
+//     most 254 lanes and an Adam lane holds at most 4 slots (checked for
+//     every tile width, slot alignment and selected count).
+// Rows are staged kRvBatch at a time, every load of a batch issued before
+// the first wait.  The kernel serves steps with the compact states in place
+// (and pack-only calls); a refresh step, whose entering and leaving columns
+// read and write their sources element by element, runs the per-column
+// kernel.
+//
+// The arithmetic per element is that of the per-column kernel (same fp32
+// operations in the same order), so both paths give identical bits.
+#include "zf_device.hpp"
+
+namespace zf {
+namespace {
+
+#ifndef ZF_RV_BATCH
+#define ZF_RV_BATCH 4
+#endif
+constexpr int kRvBatch = ZF_RV_BATCH;  // rows staged together (two per G load)
+static_assert(kRvBatch % 2 == 0 && kRvBatch >= 2, "rows are loaded in pairs");
+static_assert(kRvMaxCols % 8 == 0 && kRvMaxCols <= 1000, "lane budget of the roles");
+
+// Number of selected columns below column j (0 <= j <= m); j is the same
+// for every lane.
+__device__ __forceinline__ int64_t selected_below(const DevMat& d, int64_t j) {
+  if (j >= d.m) return d.k;
+  const int64_t w = j >> 6;
+  const uint64_t mw = uniform_u64(d.mask[w]);
+  return static_cast<int64_t>(uniform_i32(d.prefix[w])) +
+         __popcll(mw & ((uint64_t(1) << (j & 63)) - 1));
+}
+
+__device__ __forceinline__ float4 as_f4(u32x4 v) {
+  return make_float4(__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z),
+                     __uint_as_float(v.w));
+}
+__device__ __forceinline__ u32x4 as_u4(float a, float b, float c, float d) {
+  return u32x4{__float_as_uint(a), __float_as_uint(b), __float_as_uint(c), __float_as_uint(d)};
+}
+
+template <bool BATCHED, bool ADAM, bool PACK, bool HAND>
+__global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __restrict__ mats,
+                                                             const int64_t* __restrict__ off,
+                                                             int32_t nmats, DevMat one, AdamK c,
+                                                             int32_t first, float scale) {
+  __shared__ __attribute__((aligned(16))) uint16_t sg[kRvBatch][kRvMaxCols];
+  __shared__ __attribute__((aligned(16))) float sd[HAND ? kRvBatch : 1][HAND ? kRvMaxCols : 4];
+
+  int64_t local;
+  const DevMat& d = get_mat<BATCHED>(mats, off, nmats, one, local);
+  const int64_t cblk = local % d.rv_cb;
+  const int64_t rblk = local / d.rv_cb;
+  const int64_t c0 = cblk * d.rv_w;
+  const int32_t width = static_cast<int32_t>(min(static_cast<int64_t>(d.rv_w), d.m - c0));
+  const int64_t rs = selected_below(d, c0);
+  const int32_t cs = static_cast<int32_t>(selected_below(d, c0 + width) - rs);
+  const int64_t us = c0 - rs;
+  const int32_t cu = width - cs;
+  const bool do_u = PACK && cu > 0;
+
+  // Lane roles (see above).  nqf whole quads [qf0, qf0 + nqf) of the
+  // unselected range, then ne edge slots (head then tail), then Adam lanes.
+  int64_t qf0 = 0;
+  int32_t nqf = 0, nh = 0, ne = 0;
+  if (do_u) {
+    qf0 = (us + 3) >> 2;
+    const int64_t qf1 = (us + cu) >> 2;
+    if (qf1 > qf0) {
+      nqf = static_cast<int32_t>(qf1 - qf0);
+      nh = static_cast<int32_t>(4 * qf0 - us);
+      ne = nh + static_cast<int32_t>(us + cu - 4 * qf1);
+    } else {
+      nh = cu;
+      ne = cu;
+    }
+  }
+  const int32_t nA = kThreads - nqf - ne;  // >= 1 whenever cs > 0
+  const int tid = threadIdx.x;
+  const bool is_q = tid < nqf;
+  const bool is_e = !is_q && tid < nqf + ne;
+  const bool is_s = ADAM && tid >= nqf + ne && cs > 0;
+
+  // The lane's elements: slot s[e] (byte offset vs[e] in its buffer's
+  // row), column offset cj[e] in the tile, valid bit e.
+  int64_t Q = 0;
+  uint32_t valid = 0;
+  int32_t cj[4] = {0, 0, 0, 0};
+  uint32_t vs[4] = {0u, 0u, 0u, 0u};
+  if (is_q) {
+    Q = qf0 + tid;
+    valid = 0xFu;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      cj[e] = d.unsel_idx[4 * Q + e] - static_cast<int32_t>(c0);
+      vs[e] = static_cast<uint32_t>((4 * Q + e) * 4);
+    }
+  } else if (is_e) {
+    const int32_t x = tid - nqf;
+    const int64_t sl = x < nh ? us + x : us + cu - (ne - x);
+    valid = 1u;
+    cj[0] = d.unsel_idx[sl] - static_cast<int32_t>(c0);
+    vs[0] = static_cast<uint32_t>(sl * 4);
+  } else if (is_s) {
+    const int32_t a = tid - nqf - ne;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int32_t r = a + e * nA;
+      if (r < cs) {
+        valid |= 1u << e;
+        cj[e] = d.sel_idx[rs + r] - static_cast<int32_t>(c0);
+        vs[e] = static_cast<uint32_t>((rs + r) * 4);
+      }
+    }
+  }
+  // Indices come from the caller's selection; keep LDS accesses inside the
+  // tile whatever they hold.
+#pragma unroll
+  for (int e = 0; e < 4; ++e) cj[e] = min(max(cj[e], 0), width - 1);
+
+  const int64_t i0 = rblk * d.rv_rows;
+  const int64_t i1 = min(i0 + static_cast<int64_t>(d.rv_rows), d.n);
+  const int32_t rows = static_cast<int32_t>(i1 - i0);
+  const rsrc_t rG = rows_rsrc(d.grad, i0, i1, d.ld_grad, d.m);
+  const uint32_t sG = static_cast<uint32_t>(d.ld_grad * 2);
+  rsrc_t rA = rsrc_t(), rP = rsrc_t(), rM = rsrc_t(), rV = rsrc_t(), rW = rsrc_t(), rD = rsrc_t();
+  uint32_t sA = 0, sS = 0, sW = 0, sD = 0;
+  if constexpr (PACK) {
+    rA = rows_rsrc(d.acc, i0, i1, d.ld_acc, d.m - d.k);
+    sA = static_cast<uint32_t>(d.ld_acc * 4);
+  }
+  if constexpr (ADAM) {
+    rP = rows_rsrc(d.P, i0, i1, d.ld_state, d.k);
+    rM = rows_rsrc(d.M, i0, i1, d.ld_state, d.k);
+    rV = rows_rsrc(d.V, i0, i1, d.ld_state, d.k);
+    sS = static_cast<uint32_t>(d.ld_state * 4);
+    rW = rows_rsrc(d.weight, i0, i1, d.ld_weight, d.m);
+    sW = static_cast<uint32_t>(d.ld_weight * 2);
+  }
+  if constexpr (HAND) {
+    rD = rows_rsrc(d.out, i0, i1, d.ld_out, d.m);
+    sD = static_cast<uint32_t>(d.ld_out * 4);
+  }
+
+  // Column-space lane roles: G loads (row pair half h, 8-column group g8),
+  // hand-over stores (4-column group).
+  const int h = uniform_i32(tid >> 7);  // the same for the 64 lanes of a wave
+  const int32_t g8 = (tid & 127) * 8;
+  const uint32_t vQ = static_cast<uint32_t>(Q * 16);  // quad byte offset (fp32 slots)
+
+  for (int32_t i = 0; i < rows; i += kRvBatch) {
+    const int32_t nb = min(kRvBatch, rows - i);
+    if (i > 0) __syncthreads();  // the previous batch is done with the LDS rows
+
+    // 1. G rows of the batch (16-byte loads of 8 columns; ragged tail of
+    //    the last tile element by element).
+    u32x4 gv[kRvBatch / 2];
+#pragma unroll
+    for (int p = 0; p < kRvBatch / 2; ++p) {
+      const int b = 2 * p + h;
+      gv[p] = u32x4{0u, 0u, 0u, 0u};
+      if (b < nb && g8 < width) {
+        const uint32_t so = static_cast<uint32_t>(i + b) * sG;
+        const uint32_t vo = static_cast<uint32_t>((c0 + g8) * 2);
+        if (g8 + 8 <= width) {
+          gv[p] = buf_b128<kStream>(rG, vo, so);
+        } else {
+          uint32_t w[4] = {0u, 0u, 0u, 0u};
+          for (int x = 0; g8 + x < width; ++x)
+            w[x >> 1] |= static_cast<uint32_t>(buf_u16<kStream>(rG, vo + 2 * x, so))
+                         << (16 * (x & 1));
+          gv[p] = u32x4{w[0], w[1], w[2], w[3]};
+        }
+      }
+    }
+
+    // 2. Slot data of the batch: A (pack roles, after the first step of an
+    //    interval) or the Adam states.
+    float x0[kRvBatch][4], x1[kRvBatch][4], x2[kRvBatch][4];
+#pragma unroll
+    for (int b = 0; b < kRvBatch; ++b)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x0[b][e] = x1[b][e] = x2[b][e] = 0.0f;
+    if (PACK && !first) {
+      if (is_q) {
+#pragma unroll
+        for (int b = 0; b < kRvBatch; ++b) {
+          if (b < nb) {
+            const float4 v = as_f4(buf_b128(rA, vQ, static_cast<uint32_t>(i + b) * sA));
+            x0[b][0] = v.x;
+            x0[b][1] = v.y;
+            x0[b][2] = v.z;
+            x0[b][3] = v.w;
+          }
+        }
+      } else if (is_e) {
+#pragma unroll
+        for (int b = 0; b < kRvBatch; ++b)
+          if (b < nb) x0[b][0] = buf_f32(rA, vs[0], static_cast<uint32_t>(i + b) * sA);
+      }
+    }
+    if (ADAM && is_s) {
+#pragma unroll
+      for (int b = 0; b < kRvBatch; ++b) {
+        if (b < nb) {
+          const uint32_t so = static_cast<uint32_t>(i + b) * sS;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if ((valid >> e) & 1u) {
+              x0[b][e] = buf_f32(rP, vs[e], so);
+              x1[b][e] = buf_f32(rM, vs[e], so);
+              x2[b][e] = buf_f32(rV, vs[e], so);
+            }
+          }
+        }
+      }
+    }
+
+    // 3. Stage G in LDS.
+#pragma unroll
+    for (int p = 0; p < kRvBatch / 2; ++p) {
+      const int b = 2 * p + h;
+      if (b < nb && g8 < width) *reinterpret_cast<u32x4*>(&sg[b][g8]) = gv[p];
+    }
+    __syncthreads();
+
+    // 4. Slot-space arithmetic and stores.
+    if (is_q || is_e) {
+      if constexpr (PACK) {
+#pragma unroll
+        for (int b = 0; b < kRvBatch; ++b) {
+          if (b < nb) {
+            float a[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float g = widen_bf16(sg[b][cj[e]]);
+              a[e] = first ? g : x0[b][e] + g;
+            }
+            if constexpr (HAND) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                if ((valid >> e) & 1u) sd[b][cj[e]] = a[e] * scale;
+            } else {
+              const uint32_t so = static_cast<uint32_t>(i + b) * sA;
+              if (is_q) buf_put_b128(as_u4(a[0], a[1], a[2], a[3]), rA, vQ, so);
+              else buf_put_f32(a[0], rA, vs[0], so);
+            }
+          }
+        }
+      }
+    } else if (ADAM && is_s) {
+#pragma unroll
+      for (int b = 0; b < kRvBatch; ++b) {
+        if (b < nb) {
+          const uint32_t so = static_cast<uint32_t>(i + b) * sS;
+          const uint32_t sw = static_cast<uint32_t>(i + b) * sW;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if ((valid >> e) & 1u) {
+              adam_step(widen_bf16(sg[b][cj[e]]), x0[b][e], x1[b][e], x2[b][e], c);
+              buf_put_f32(x0[b][e], rP, vs[e], so);
+              buf_put_f32(x1[b][e], rM, vs[e], so);
+              buf_put_f32(x2[b][e], rV, vs[e], so);
+              buf_put_u16<kStream>(round_bf16(x0[b][e]), rW,
+                                   static_cast<uint32_t>(c0 + cj[e]) * 2u, sw);
+              if constexpr (HAND) sd[b][cj[e]] = 0.0f;  // hand-over: +0 at a selected column
+            }
+          }
+        }
+      }
+    }
+
+    // 5. Fused hand-over: the assembled output rows, 16 bytes per lane.
+    if constexpr (HAND) {
+      __syncthreads();
+      const int32_t c4 = tid * 4;
+      if (c4 < width) {
+        const uint32_t vo = static_cast<uint32_t>((c0 + c4) * 4);
+#pragma unroll
+        for (int b = 0; b < kRvBatch; ++b) {
+          if (b < nb) {
+            const uint32_t so = static_cast<uint32_t>(i + b) * sD;
+            if (c4 + 4 <= width) {
+              buf_put_b128(*reinterpret_cast<const u32x4*>(&sd[b][c4]), rD, vo, so);
+            } else {
+              for (int x = 0; c4 + x < width; ++x) buf_put_f32(sd[b][c4 + x], rD, vo + 4 * x, so);
+            }
+          }
+        }
+      }
+    }
+  }
+}
+
+template <bool ADAM, bool PACK, bool HAND>
+void launch_rv_t(const Table& t, const DevMat& one, dim3 grid, const AdamK& c, int32_t first,
+                 float scale, hipStream_t s) {
+  if (t.mats != nullptr)
+    hipLaunchKernelGGL((rv_update_kernel<true, ADAM, PACK, HAND>), grid, dim3(kThreads), 0, s,
+                       t.mats, t.off, t.nmats, one, c, first, scale);
+  else
+    hipLaunchKernelGGL((rv_update_kernel<false, ADAM, PACK, HAND>), grid, dim3(kThreads), 0, s,
+                       t.mats, t.off, t.nmats, one, c, first, scale);
+}
+
+}  // namespace
+
+hipError_t launch_rv_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
+                            int32_t mode, int32_t first, bool adam, bool pack, bool handover,
+                            float scale, hipStream_t s) {
+  (void)hipGetLastError();
+  if (blocks <= 0) return hipSuccess;
+  const dim3 grid(static_cast<uint32_t>(blocks));
+  if (handover && !(adam && pack)) return hipErrorInvalidValue;
+  if (adam && mode != kInplace) return hipErrorInvalidValue;  // refresh: per-column kernel
+  if (handover) launch_rv_t<true, true, true>(t, one, grid, c, first, scale, s);
+  else if (adam && pack) launch_rv_t<true, true, false>(t, one, grid, c, first, 1.0f, s);
+  else if (adam) launch_rv_t<true, false, false>(t, one, grid, c, first, 1.0f, s);
+  else if (pack) launch_rv_t<false, true, false>(t, one, grid, c, first, 1.0f, s);
+  return hipGetLastError();
+}
+
+}  // namespace zf

@@ -58,6 +58,7 @@ import torch
 
 from ._lib import (ROW_MAJOR, STATES_INIT, STATES_INPLACE, STATES_REMAP, ZEN_TOTALS_BYTES,
                    AdamHparams, MatrixBuffers, Plan, Selection, StateSource, ZenTotals, _stored,
+                   alloc_stored, padded_block,
                    host_adam_unselected, k_from_ratio)
 
 
@@ -147,13 +148,12 @@ class SelectiveUpdateRunner:
                 self.acc_sq.append(torch.empty(m - k, dtype=f32, device=dev))
             for p in range(2):
                 self.sels[p].append(Selection(m, k, dev))
-                self.states[p].append(tuple(torch.empty(*_stored(layout, n, k), dtype=f32,
-                                                        device=dev) for _ in range(3)))
+                self.states[p].append(tuple(alloc_stored(layout, n, k, f32, dev)
+                                            for _ in range(3)))
             for a in range(nacc):
-                self.accs[a].append(torch.empty(*_stored(layout, n, m - k), dtype=f32,
-                                                device=dev))
+                self.accs[a].append(alloc_stored(layout, n, m - k, f32, dev))
             self.norms.append(torch.empty(m, dtype=f32, device=dev))
-            self.unpacked.append(torch.empty(*_stored(layout, n, m), dtype=f32, device=dev)
+            self.unpacked.append(alloc_stored(layout, n, m, f32, dev)
                                  if self.keep_unpacked else None)
             if self.offload:
                 p0 = (self.init_master[q] if self.init_master is not None
@@ -162,7 +162,7 @@ class SelectiveUpdateRunner:
                 sp.copy_(p0)
                 self.store.append((sp, _pinned_like(p0.shape, f32).zero_(),
                                    _pinned_like(p0.shape, f32).zero_()))
-                self.host_acc.append(_pinned_like(_stored(layout, n, m - k), f32))
+                self.host_acc.append(alloc_stored(layout, n, m - k, f32, pin_memory=True))
                 self.wcols.append(_pinned_like(_stored(layout, n, m - k), torch.bfloat16))
                 self.unsel_host.append(_pinned_like((m - k,), torch.int32))
         self.acc = self.accs[0]
@@ -325,7 +325,8 @@ class SelectiveUpdateRunner:
         if not self.overlap:
             with torch.cuda.stream(st):
                 for q in range(len(self.shapes)):
-                    self.host_acc[q].copy_(self.accs[a][q], non_blocking=True)
+                    padded_block(self.host_acc[q]).copy_(padded_block(self.accs[a][q]),
+                                                         non_blocking=True)
                     self.unsel_host[q].copy_(sels[q].unsel_idx, non_blocking=True)
             st.synchronize()
             self._host_update(scale, self.th, None, None)
@@ -337,7 +338,8 @@ class SelectiveUpdateRunner:
         cs.wait_event(ev)
         with torch.cuda.stream(cs):
             for q in range(len(self.shapes)):
-                self.host_acc[q].copy_(self.accs[a][q], non_blocking=True)
+                padded_block(self.host_acc[q]).copy_(padded_block(self.accs[a][q]),
+                                                     non_blocking=True)
                 self.unsel_host[q].copy_(sels[q].unsel_idx, non_blocking=True)
         copied = torch.cuda.Event()
         copied.record(cs)

@@ -2,6 +2,7 @@
 (sanitizers on the host compilation only; no device code runs) and driven by
 tests/native/host_asan_main.cpp: the multithreaded deferred update on
 exact-size heap buffers, and the host-side argument validation."""
+import importlib.util
 import os
 import shutil
 import subprocess
@@ -10,8 +11,18 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2505_12242_amd", "csrc")
-SOURCES = ["zf_api.hip", "zf_kernels.hip", "zf_kernels_cm.hip", "zf_kernels_zen.hip",
-           "zf_kernels_offload.hip", "zf_host.cpp"]
+
+
+def _library_sources():
+    """The library's source list, as the build script compiles it."""
+    spec = importlib.util.spec_from_file_location(
+        "zf_build", os.path.join(ROOT, "paper_2505_12242_amd", "build.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return list(mod.SOURCES)
+
+
+SOURCES = _library_sources()
 
 
 @pytest.mark.timeout(600)
