@@ -284,6 +284,9 @@ def main(argv=None) -> int:
 
     # one plain streaming kernel of known size (reads and writes exactly
     # calibration_copy_gib GiB each): the calibration point for PMC counters
+    # (then timed over three more launches: a plain read+write stream on
+    # this box, reported beside the roofline as context)
+    stream_ref = None
     if args.calibration_copy_gib > 0:
         nb = int(args.calibration_copy_gib * 2**30)
         src = torch.empty(nb // 4, dtype=torch.float32, device=dev).fill_(4.0)
@@ -291,6 +294,16 @@ def main(argv=None) -> int:
         torch.cuda.synchronize()
         torch.sqrt(src, out=dst)
         torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(3):
+            torch.sqrt(src, out=dst)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / 3
+        stream_ref = {"kernel": f"torch.sqrt over {args.calibration_copy_gib:g} GiB fp32 "
+                                "(reads and writes that much)",
+                      "GB/s": round(2 * nb / (ms * 1e-3) / 1e9, 1)}
         del src, dst
 
     for _ in range(args.warmup):
@@ -400,6 +413,7 @@ def main(argv=None) -> int:
             "traffic": traffic,
             "bytes_per_launch": round(update_bytes / max(upd_launches, 1)),
             "avg_launch_ms": round(upd_avg_ms, 4),
+            "stream_reference": stream_ref,
         },
     }
     if args.offload:

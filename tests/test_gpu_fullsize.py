@@ -1,9 +1,11 @@
-"""Parity at full size, in the launch configuration bench.py times (channel-
-major, batched plans, three-slot gradient ring): the whole Llama-2-7B-shaped
-gradient set (226 matrices) for 8 steps of the R = S = 4 schedule -- first
-selection, accumulation, hand-over at step 4, refresh with state remap at
-step 5, hand-over at step 8 -- and one R = S = 8 interval of the 70B share
-(heavy-tailed scales, GQA k/v weights, 28672-channel down projections).
+"""Parity at full size, in the launch configuration bench.py times (batched
+plans, three-slot gradient ring): the whole Llama-2-7B-shaped gradient set
+(226 matrices) for 8 steps of the R = S = 4 schedule -- first selection,
+accumulation, hand-over at step 4, refresh with state remap at step 5,
+hand-over at step 8 -- in both layouts (channel-major, bench.py's default,
+and row-major with the 16-byte update), and one R = S = 8 interval of the
+70B share (heavy-tailed scales, GQA k/v weights, 28672-channel down
+projections) in the channel-major layout.
 
 * Sampled matrices (embedding, LM head and four decoder weights of three
   shapes) are run through the oracle step by step and every output is
@@ -40,20 +42,28 @@ CASES = {
 }
 
 
-def logical(t):
+RUNS = [("llama2-7b-full", "cm"), ("llama2-7b-full", "rm"), ("llama2-70b-10layers", "cm")]
+
+
+def logical_cm(t):
+    """Logical [out, in] view of a channel-major tensor."""
     return t.t()
 
 
 @pytest.mark.timeout(1200)
-@pytest.mark.parametrize("name", sorted(CASES))
-def test_full_set_sampled_parity(name):
+@pytest.mark.parametrize("name,lay", RUNS)
+def test_full_set_sampled_parity(name, lay):
     from workloads import get_workload
     SAMPLES, STEPS, NSLOTS, LIGHT = CASES[name]
     wl = get_workload(name)
     hp = zf.AdamHparams(wl.hyper.lr, wl.hyper.beta1, wl.hyper.beta2, wl.hyper.eps,
                         wl.hyper.weight_decay)
     dev = torch.device("cuda")
-    layout = zf.CHANNEL_MAJOR
+    layout = zf.CHANNEL_MAJOR if lay == "cm" else zf.ROW_MAJOR
+    assert not LIGHT or layout == zf.CHANNEL_MAJOR  # the light checks index channel rows
+
+    def logical(t):
+        return t.t() if layout == zf.CHANNEL_MAJOR else t
     shapes, ks, slots, weights = bench.build_set(wl, NSLOTS, dev, layout)
     names = [mt.name for mt in wl.matrices]
     qs = [names.index(s) for s in SAMPLES]
@@ -146,7 +156,7 @@ def test_full_set_zen_auto_statistics():
     shapes, ks, slots, weights = bench.build_set(wl, 3, dev, zf.CHANNEL_MAJOR)
     names = [mt.name for mt in wl.matrices]
     qs = [names.index("layers.5.up_proj"), names.index("lm_head")]
-    w0 = {q: bits_np(logical(weights[q]).contiguous()) for q in qs}
+    w0 = {q: bits_np(logical_cm(weights[q]).contiguous()) for q in qs}
     runner = zf.SelectiveUpdateRunner(shapes, wl.ratio, hp, wl.refresh, wl.accum, slots, weights,
                                       device=dev, layout=zf.CHANNEL_MAJOR, zen_tau=math.inf)
     orcs = {q: O.MatrixOracle(O.widen(w0[q]), w0[q], wl.ratio, hp.lr, hp.beta1, hp.beta2,
@@ -163,15 +173,15 @@ def test_full_set_zen_auto_statistics():
         assert abs(torch.sqrt(sel_all).sum().item() - tot.sum_sel) <= 1e-9 * tot.sum_sel
         assert abs(torch.sqrt(acc_all).sum().item() - tot.sum_acc) <= 1e-9 * tot.sum_acc
         for q in qs:
-            G = bits_np(logical(slots[(t - 1) % 3][q]).contiguous())
+            G = bits_np(logical_cm(slots[(t - 1) % 3][q]).contiguous())
             orcs[q].advance(G, kind.refresh, kind.step_in_interval)
             ssq, asq = O.zen_auto_stats(G, orcs[q].sel, orcs[q].A)
             ok, worst = rel_close(f32_np(runner.sel_sq[q]), ssq, 1e-5)
             assert ok, (names[q], t, worst)
             ok, worst = rel_close(f32_np(runner.acc_sq[q]), asq, 1e-5)
             assert ok, (names[q], t, worst)
-            assert same_bits(f32_np(logical(runner.acc[q])), orcs[q].A), (names[q], t)
-            P = f32_np(logical(runner.state[q][0]))
+            assert same_bits(f32_np(logical_cm(runner.acc[q])), orcs[q].A), (names[q], t)
+            P = f32_np(logical_cm(runner.state[q][0]))
             assert same_bits(P, orcs[q].P), (names[q], t)
     runner.close()
     del runner, slots, weights
