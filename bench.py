@@ -36,7 +36,7 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2505_12242_amd", "csrc", f)
                   for f in ("zf_device.hpp", "zf_internal.hpp", "zf_kernels.hip",
-                            "zf_kernels_cm.hip", "zf_kernels_rv.hip", "zf_api.hip")]
+                            "zf_kernels_cm.hip", "zf_kernels_rv.hip")]
 
 
 def parse_args(argv=None):

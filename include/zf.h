@@ -159,8 +159,9 @@ typedef enum zf_state_mode {
  * init source: in ZF_STATES_INIT and ZF_STATES_REMAP a newly selected column
  * reads (p, m, v) from its column of the store (swap-in), and in
  * ZF_STATES_REMAP a column that was selected before but no longer is writes
- * its previous compact (p, m, v) to its column of the store (swap-out).  The
- * store must not overlap any other buffer of the call. */
+ * its previous compact (p, m, v) to its column of the store (swap-out), so
+ * the prev_* states are then required even when k = 0.  The store must not
+ * overlap any other buffer of the call. */
 typedef struct zf_state_source {
   const uint64_t* prev_mask;
   const int32_t* prev_prefix;

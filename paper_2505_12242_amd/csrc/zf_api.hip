@@ -262,7 +262,9 @@ bool adam_args_ok(const DevMat& d, int32_t mode, Span g) {
     if (!vector_ok(d.prev_mask, words, 8) || !vector_ok(d.prev_prefix, words, 4)) return false;
     // The previous states hold as many slots as the previous selection has
     // columns (device data); only presence, alignment and stride are checked.
-    if (n > 0 && k > 0 &&
+    // They are read for the selected columns and, with a store, for the
+    // columns that leave the selection (swap-out), whatever k is.
+    if (n > 0 && (k > 0 || d.st_P != nullptr) &&
         (d.prev_P == nullptr || d.prev_M == nullptr || d.prev_V == nullptr ||
          !aligned(d.prev_P, 4) || !aligned(d.prev_M, 4) || !aligned(d.prev_V, 4) ||
          d.ld_prev < (L == zf::kChannelMajor ? n : 0)))
@@ -434,7 +436,8 @@ int64_t unpack_grid(const DevMat& d) {
 
 // Row-major: the 16-byte kernel serves the steps without a refresh (states in
 // place, or no Adam); a refresh step (remap / init, whose per-column sources
-// it reads element by element) runs the per-column kernel.  Both give the
+// it would read element by element behind a chain of dependent index loads)
+// runs the per-column kernel, which measured faster there.  Both give the
 // same bits.
 bool use_rv(const DevMat& one, int32_t mode, bool adam) {
   return one.layout == zf::kRowMajor && one.rv && (!adam || mode == zf::kInplace);
@@ -516,7 +519,10 @@ zf_status run_update(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad
     d.out = out;
     d.ld_out = ld_out;
   }
-  if (!handover && (!adam || k == 0) && (!pack || k == m)) return ZF_OK;  // no column to touch
+  // nothing to touch: no selected column to update, no leaving column to swap
+  // out, no unselected column to pack
+  const bool swap_out = adam && mode == zf::kRemap && d.st_P != nullptr;
+  if (!handover && (!adam || k == 0) && !swap_out && (!pack || k == m)) return ZF_OK;
   finish_geometry(d, 256, pick_update_rows({{n, m}}));
   set_rv(d, pick_rv_rows({{n, m}}), true);
   if (layout == zf::kRowMajor && !rm_strides_ok(d)) return ZF_EINVAL;

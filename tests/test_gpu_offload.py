@@ -298,3 +298,37 @@ def test_zen_auto_triggers_the_deferred_update(overlap):
     assert any(ends) and not all(ends)
     assert runner.th == za.orcs[0].th == sum(ends)
     runner.close()
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_remap_with_store_requires_previous_states(layout):
+    """With a store, a remap reads the previous compact states for the
+    columns that leave the selection even when no column is selected now
+    (k = 0): they are required, and a k = 0 remap swaps every previously
+    selected column out."""
+    n, m = 16, 40
+    rng = np.random.default_rng(7)
+    old = O.select_topk(rng.random(m).astype(np.float32), 6)
+    new = O.select_topk(rng.random(m).astype(np.float32), 0)
+    store = _store_arrays(rng, n, m)
+    sd = [place(T(x, layout), "device") for x in store]
+    P, M, V = ((rng.standard_normal((n, 6)) * s).astype(np.float32) for s in (0.02, 1e-3, 1e-5))
+    V = np.abs(V)
+    shape = (n, 0) if layout == zf.ROW_MAJOR else (0, n)
+    empty = [torch.empty(shape, device="cuda") for _ in range(3)]
+    Wd = bf16_dev(T(O.bf16_round(rng.standard_normal((n, m)).astype(np.float32)), layout))
+    G = bf16_dev(T(grad_bits(n, m, 3), layout))
+    no_prev = zf.StateSource(prev=sel_dev(old), store_master=sd[0], store_exp_avg=sd[1],
+                             store_exp_avg_sq=sd[2])
+    with pytest.raises(zf.ZfError):
+        zf.adam_selected(G, sel_dev(new), *empty, Wd, HP, 2, mode=zf.STATES_REMAP, src=no_prev,
+                         layout=layout)
+    src = zf.StateSource(prev=sel_dev(old), prev_master=f32_dev(T(P, layout)),
+                         prev_exp_avg=f32_dev(T(M, layout)), prev_exp_avg_sq=f32_dev(T(V, layout)),
+                         store_master=sd[0], store_exp_avg=sd[1], store_exp_avg_sq=sd[2])
+    zf.adam_selected(G, sel_dev(new), *empty, Wd, HP, 2, mode=zf.STATES_REMAP, src=src,
+                     layout=layout)
+    torch.cuda.synchronize()
+    _, _, _, store2 = O.swap_states(old, new, P, M, V, store)
+    for got, want in zip(sd, store2):
+        assert same_bits(T(f32_np(got), layout), want)
