@@ -24,6 +24,7 @@ from __future__ import annotations
 
 import argparse
 import contextlib
+import gc
 import hashlib
 import json
 import os
@@ -327,6 +328,10 @@ def main(argv=None) -> int:
         spans.append((name, a, b))
 
     kinds = []
+    # the garbage collector stays off in the timed region: a collection there
+    # is a host pause that a short step does not hide
+    gc.collect()
+    gc.disable()
     torch.cuda.synchronize()
     w0 = time.perf_counter()
     for _ in range(args.steps):
@@ -335,6 +340,7 @@ def main(argv=None) -> int:
         runner.sync()  # the last deferred update lands inside the timed region
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
+    gc.enable()
 
     per_kernel_ms = {}
     for name, a, b in spans:
