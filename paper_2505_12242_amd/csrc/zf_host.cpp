@@ -15,7 +15,10 @@
 //
 // Work is split over threads by whole columns (channel-major: a column is
 // one contiguous row of every buffer) or by rows (row-major); unsel must be
-// strictly ascending, so no two threads write the same element.
+// strictly ascending, so no two threads write the same element.  In the
+// row-major layout a row's unselected columns come in runs of consecutive
+// indices (the same runs in every row): each run is one contiguous stretch of
+// the states and of the accumulated row, updated by the same element loop.
 #include <algorithm>
 #include <cmath>
 #include <cstring>
@@ -124,6 +127,19 @@ zf_status zf_host_adam_unselected(const float* acc, int64_t ld_acc, const int32_
 
   const zf::AdamK c = zf::adam_consts(*hp, step);
   const int64_t units = cm ? u : n;  // columns (channel-major) or rows
+  // row-major: runs (first slot, first column, length) of consecutive columns
+  struct Run {
+    int64_t q, j, len;
+  };
+  std::vector<Run> runs;
+  if (!cm) {
+    for (int64_t q = 0; q < u;) {
+      int64_t e = q + 1;
+      while (e < u && unsel_idx[e] == unsel_idx[e - 1] + 1) ++e;
+      runs.push_back(Run{q, unsel_idx[q], e - q});
+      q = e;
+    }
+  }
   int64_t threads = nthreads > 0 ? nthreads : std::max<int64_t>(1, std::thread::hardware_concurrency());
   threads = std::max<int64_t>(1, std::min<int64_t>(threads, units));
 
@@ -141,15 +157,8 @@ zf_status zf_host_adam_unselected(const float* acc, int64_t ld_acc, const int32_
         float* mm = exp_avg + i * ld_state;
         float* vv = exp_avg_sq + i * ld_state;
         uint16_t* w = weight_cols + i * ld_wcols;
-        for (int64_t q = 0; q < u; ++q) {
-          const int64_t j = unsel_idx[q];
-          float pe = p[j], me = mm[j], ve = vv[j];
-          host_adam_elem(a[q] * scale, pe, me, ve, c);
-          p[j] = pe;
-          mm[j] = me;
-          vv[j] = ve;
-          w[q] = host_round_bf16(pe);
-        }
+        for (const Run& r : runs)
+          host_adam_run(a + r.q, scale, p + r.j, mm + r.j, vv + r.j, w + r.q, r.len, c);
       }
     }
   };
