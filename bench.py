@@ -56,7 +56,7 @@ def parse_args(argv=None):
     ap.add_argument("--accum", type=int, default=None, help="override the accumulation interval S")
     ap.add_argument("--zen-tau", type=float, default=None,
                     help="run Zen-auto (adaptive interval, at most --accum steps) with this "
-                         "threshold instead of the fixed schedule (channel-major only)")
+                         "threshold instead of the fixed schedule")
     ap.add_argument("--offload", action="store_true",
                     help="run the whole method with offloaded optimizer states: full-state "
                          "store in pinned host memory (swapped at refreshes) and the deferred "

@@ -851,7 +851,10 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   }
   const int cn_rows = pick_colnorm_rows(shapes);
   const int up_rows = pick_update_rows(shapes);
-  const int rv_rows = pick_rv_rows(shapes);
+  // a row-major plan with the Zen-auto statistics runs the 16-byte update in
+  // blocks of the column-score row blocks, so that its fused statistics are
+  // the statistics pass's partials (same row blocks, same order)
+  const int rv_rows = (p->layout == zf::kRowMajor && p->can_zen) ? cn_rows : pick_rv_rows(shapes);
   // the row-major 16-byte update serves the plan if every matrix qualifies
   bool all_rv = p->layout == zf::kRowMajor;
   for (int32_t q = 0; q < nmats && all_rv; ++q) {
@@ -1084,6 +1087,14 @@ zf_status zf_plan_update_zen(zf_plan* p, const zf_adam_hparams* hp, int64_t step
                              true, true, p->d_zs, false, 1.0f, s);
     if (e != hipSuccess) return hip_fail(e);
     e = zf::launch_zen_finalize(tz, p->mats[0], p->blk_zen, p->d_zs, p->d_zb, s);
+  } else if (use_rv(p->mats[0], mode, true)) {
+    // 16-byte update with the statistics fused: only the finalize remains
+    const Table tv{p->d_mats, p->d_off_upv, p->nmats};
+    e = zf::launch_rv_update(tv, p->mats[0], p->blk_upv, c, mode, step_in_interval == 1 ? 1 : 0,
+                             true, true, false, 1.0f, s, p->d_ws);
+    if (e != hipSuccess) return hip_fail(e);
+    const Table tp{p->d_mats, p->d_off_zp, p->nmats};
+    e = zf::launch_rm_zen(tp, 0, tz, p->blk_zen, p->mats[0], p->d_ws, p->d_zb, s);
   } else {
     e = plan_update_launch(p, c, mode, step_in_interval == 1 ? 1 : 0, true, true, false, 1.0f, s);
     if (e != hipSuccess) return hip_fail(e);

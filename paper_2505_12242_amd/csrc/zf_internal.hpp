@@ -136,10 +136,12 @@ hipError_t launch_unpack(const Table& t, const DevMat& one, int64_t blocks, floa
                          hipStream_t s);
 
 // Row-major update with 16-byte accesses (zf_kernels_rv.hip); same contract
-// as launch_update, geometry rv_w / rv_cb / rv_rows.
+// as launch_update, geometry rv_w / rv_cb / rv_rows.  zs != nullptr (fused
+// update only, rv_rows == cn_rpb): also the Zen-auto partials of the
+// row-major statistics pass, into zs at each matrix's cn_ws.
 hipError_t launch_rv_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
                             int32_t mode, int32_t first, bool adam, bool pack, bool handover,
-                            float scale, hipStream_t s);
+                            float scale, hipStream_t s, double* zs = nullptr);
 
 // Channel-major kernels (zf_kernels_cm.hip).
 hipError_t launch_cm_colnorm(const Table& t, const DevMat& one, int64_t blocks, hipStream_t s);

@@ -32,6 +32,13 @@
 // read and write their sources element by element, runs the per-column
 // kernel.
 //
+// STATS (Zen-auto, blocks of cn_rpb rows): each lane also sums, in fp64 and
+// in row order, the squares of its selected columns' gradient and of its
+// unselected slots' new accumulated values over the block's rows, and
+// writes one partial per virtual column (selected slot r, then unselected
+// slot k + u) and row block into the column-score workspace -- the partials
+// of the row-major statistics pass, in the same order, for its finalize.
+//
 // The arithmetic per element is that of the per-column kernel (same fp32
 // operations in the same order), so both paths give identical bits.
 #include "zf_device.hpp"
@@ -64,11 +71,13 @@ __device__ __forceinline__ u32x4 as_u4(float a, float b, float c, float d) {
   return u32x4{__float_as_uint(a), __float_as_uint(b), __float_as_uint(c), __float_as_uint(d)};
 }
 
-template <bool BATCHED, bool ADAM, bool PACK, bool HAND>
+template <bool BATCHED, bool ADAM, bool PACK, bool HAND, bool STATS>
 __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __restrict__ mats,
                                                              const int64_t* __restrict__ off,
                                                              int32_t nmats, DevMat one, AdamK c,
-                                                             int32_t first, float scale) {
+                                                             int32_t first, float scale,
+                                                             double* __restrict__ zs) {
+  static_assert(!STATS || (ADAM && PACK && !HAND), "statistics of the fused update");
   __shared__ __attribute__((aligned(16))) uint16_t sg[kRvBatch][kRvMaxCols];
   __shared__ __attribute__((aligned(16))) float sd[HAND ? kRvBatch : 1][HAND ? kRvMaxCols : 4];
 
@@ -172,6 +181,7 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
   const int h = uniform_i32(tid >> 7);  // the same for the 64 lanes of a wave
   const int32_t g8 = (tid & 127) * 8;
   const uint32_t vQ = static_cast<uint32_t>(Q * 16);  // quad byte offset (fp32 slots)
+  double zq[4] = {0.0, 0.0, 0.0, 0.0};  // STATS: sums of squares per element
 
   for (int32_t i = 0; i < rows; i += kRvBatch) {
     const int32_t nb = min(kRvBatch, rows - i);
@@ -260,6 +270,10 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
             for (int e = 0; e < 4; ++e) {
               const float g = widen_bf16(sg[b][cj[e]]);
               a[e] = first ? g : x0[b][e] + g;
+              if constexpr (STATS) {
+                const double x = static_cast<double>(a[e]);
+                zq[e] = __builtin_fma(x, x, zq[e]);
+              }
             }
             if constexpr (HAND) {
 #pragma unroll
@@ -282,7 +296,12 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             if ((valid >> e) & 1u) {
-              adam_step(widen_bf16(sg[b][cj[e]]), x0[b][e], x1[b][e], x2[b][e], c);
+              const float g = widen_bf16(sg[b][cj[e]]);
+              if constexpr (STATS) {
+                const double x = static_cast<double>(g);
+                zq[e] = __builtin_fma(x, x, zq[e]);
+              }
+              adam_step(g, x0[b][e], x1[b][e], x2[b][e], c);
               buf_put_f32(x0[b][e], rP, vs[e], so);
               buf_put_f32(x1[b][e], rM, vs[e], so);
               buf_put_f32(x2[b][e], rV, vs[e], so);
@@ -315,30 +334,45 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
       }
     }
   }
+
+  if constexpr (STATS) {
+    // one partial per virtual column of this row block (rv_rows = cn_rpb)
+    double* __restrict__ out = zs + d.cn_ws + rblk * d.m;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if ((valid >> e) & 1u) {
+        if (is_s) out[vs[e] >> 2] = zq[e];                      // selected slot r
+        else if (is_q || is_e) out[d.k + (vs[e] >> 2)] = zq[e];  // k + unselected slot u
+      }
+    }
+  }
 }
 
-template <bool ADAM, bool PACK, bool HAND>
+template <bool ADAM, bool PACK, bool HAND, bool STATS = false>
 void launch_rv_t(const Table& t, const DevMat& one, dim3 grid, const AdamK& c, int32_t first,
-                 float scale, hipStream_t s) {
+                 float scale, hipStream_t s, double* zs = nullptr) {
   if (t.mats != nullptr)
-    hipLaunchKernelGGL((rv_update_kernel<true, ADAM, PACK, HAND>), grid, dim3(kThreads), 0, s,
-                       t.mats, t.off, t.nmats, one, c, first, scale);
+    hipLaunchKernelGGL((rv_update_kernel<true, ADAM, PACK, HAND, STATS>), grid, dim3(kThreads), 0,
+                       s, t.mats, t.off, t.nmats, one, c, first, scale, zs);
   else
-    hipLaunchKernelGGL((rv_update_kernel<false, ADAM, PACK, HAND>), grid, dim3(kThreads), 0, s,
-                       t.mats, t.off, t.nmats, one, c, first, scale);
+    hipLaunchKernelGGL((rv_update_kernel<false, ADAM, PACK, HAND, STATS>), grid, dim3(kThreads),
+                       0, s, t.mats, t.off, t.nmats, one, c, first, scale, zs);
 }
 
 }  // namespace
 
 hipError_t launch_rv_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
                             int32_t mode, int32_t first, bool adam, bool pack, bool handover,
-                            float scale, hipStream_t s) {
+                            float scale, hipStream_t s, double* zs) {
   (void)hipGetLastError();
   if (blocks <= 0) return hipSuccess;
   const dim3 grid(static_cast<uint32_t>(blocks));
   if (handover && !(adam && pack)) return hipErrorInvalidValue;
   if (adam && mode != kInplace) return hipErrorInvalidValue;  // refresh: per-column kernel
-  if (handover) launch_rv_t<true, true, true>(t, one, grid, c, first, scale, s);
+  if (zs != nullptr) {
+    if (!(adam && pack) || handover) return hipErrorInvalidValue;
+    launch_rv_t<true, true, false, true>(t, one, grid, c, first, 1.0f, s, zs);
+  } else if (handover) launch_rv_t<true, true, true>(t, one, grid, c, first, scale, s);
   else if (adam && pack) launch_rv_t<true, true, false>(t, one, grid, c, first, 1.0f, s);
   else if (adam) launch_rv_t<true, false, false>(t, one, grid, c, first, 1.0f, s);
   else if (pack) launch_rv_t<false, true, false>(t, one, grid, c, first, 1.0f, s);
