@@ -438,11 +438,15 @@ typedef struct zf_zen_totals {
  * *totals (DEVICE).  The caller ends the interval (zf_plan_unpack with scale
  * 1/step_in_interval) when trigger is set; the next step then starts a new
  * interval (step_in_interval = 1).
- * Channel-major plans sum the squares inside the update pass; row-major
- * plans run the update and then a separate statistics pass (it reads the
- * selected gradient columns and the packed buffer again, and uses the
- * plan's column-score workspace).  Both layouts give the same statistics
- * up to the order of the fp64 sums.
+ * Channel-major plans sum the squares inside the update pass.  Row-major
+ * plans do too on steps with the states in place when their buffers take
+ * the 16-byte update (see Layouts); on refresh steps, and for other
+ * buffers, they run the update and then a separate statistics pass that
+ * reads the selected gradient columns and the packed buffer again.  Both
+ * row-major forms write the same fp64 partials (per column and
+ * column-score row block, in row order) to the plan's column-score
+ * workspace, so they give identical statistics; the two layouts agree up to
+ * the order of the fp64 sums.
  * Requirements: every descriptor of the plan provides sel_sq [k] and
  * acc_sq [m - k] (device fp32, disjoint from each other and from the
  * update's buffers), tau >= 0 (+inf allowed, never triggers when
