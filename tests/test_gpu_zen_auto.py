@@ -269,3 +269,74 @@ def test_zen_auto_rejects_bad_arguments():
     assert (tot.k_total, tot.u_total) == (10, 90)
     assert tot.sum_sel == 0.0 and tot.sum_acc == 0.0 and tot.trigger  # 0 >= tau * 0
     plan.close()
+
+
+def test_rowmajor_fused_statistics_equal_separate_pass():
+    """Row-major plans: the statistics fused into the 16-byte update (aligned,
+    padded buffers) and the separate statistics pass (the same data in
+    unaligned buffers, per-column update) write the same partials: the
+    per-channel statistics, the totals, the states and the packed buffer are
+    equal bit for bit, over an init step and two in-place steps."""
+    from tests._gpu import bf16_dev, bits_np
+    from workloads import derive_seed, gradient
+    shapes = [(40, 1009), (17, 77), (64, 2048)]
+    hp = zf.AdamHparams(lr=1e-3)
+    rng = np.random.default_rng(23)
+
+    def f32(a, aligned):
+        n, w = a.shape
+        if aligned:
+            t = zf.alloc_stored(zf.ROW_MAJOR, n, w)
+        else:
+            t = torch.empty(n * w + 1, device="cuda")[1:].view(n, w)
+        t.copy_(torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)))
+        return t
+
+    def bf16(bits, aligned):
+        m = bits.shape[1]
+        return bf16_dev(bits, ld=-(-m // 8) * 8) if aligned else bf16_dev(bits, offset=1)
+
+    grads = {}
+    sets = {True: [], False: []}
+    sels = []
+    for q, (n, m) in enumerate(shapes):
+        k = zf.k_from_ratio(0.1, m)
+        sel = O.select_topk(rng.random(m).astype(np.float32), k)
+        s = zf.Selection(m, k)
+        s.sel_idx.copy_(torch.from_numpy(sel.sel.astype(np.int32)))
+        s.unsel_idx.copy_(torch.from_numpy(sel.unsel.astype(np.int32)))
+        s.mask.copy_(torch.from_numpy(sel.mask.view(np.int64)))
+        s.prefix.copy_(torch.from_numpy(sel.prefix.astype(np.int32)))
+        sels.append(s)
+        W = O.bf16_round((rng.standard_normal((n, m)) * 0.02).astype(np.float32))
+        for t in (1, 2, 3):
+            g = torch.Generator().manual_seed(derive_seed("zen-fused", q, t))
+            sc = torch.exp(1.5 * torch.randn(m, generator=g, dtype=torch.float64))
+            grads[q, t] = bits_np(gradient(n, m, sc, seed=derive_seed("zen-fused", q, t)))
+        for al in (True, False):
+            sets[al].append(dict(
+                G=[bf16(grads[q, t], al) for t in (1, 2, 3)], W=bf16(W, al),
+                P=f32(np.zeros((n, k)), al), M=f32(np.zeros((n, k)), al),
+                V=f32(np.zeros((n, k)), al), A=f32(np.zeros((n, m - k)), al),
+                ssq=torch.empty(k, device="cuda"), asq=torch.empty(m - k, device="cuda")))
+    results = {}
+    for al in (True, False):
+        totals_seq = []
+        for t in (1, 2, 3):
+            mats = [zf.MatrixBuffers(grad=b["G"][t - 1], k=sels[q].k, sel=sels[q], weight=b["W"],
+                                     master=b["P"], exp_avg=b["M"], exp_avg_sq=b["V"], acc=b["A"],
+                                     layout=zf.ROW_MAJOR, sel_sq=b["ssq"], acc_sq=b["asq"])
+                    for q, b in enumerate(sets[al])]
+            plan = zf.Plan(mats)
+            totals = torch.zeros(5, dtype=torch.int64, device="cuda")
+            plan.update_zen(hp, t, zf.STATES_INIT if t == 1 else zf.STATES_INPLACE, t, 4,
+                            math.inf, totals)
+            torch.cuda.synchronize()
+            totals_seq.append(totals.cpu().numpy().tobytes())
+            plan.close()
+        results[al] = (totals_seq, [[x.cpu().numpy().tobytes() for x in
+                                     (b["ssq"], b["asq"], b["P"].contiguous(), b["M"].contiguous(),
+                                      b["V"].contiguous(), b["A"].contiguous())]
+                                    for b in sets[al]])
+    assert results[True][0] == results[False][0]
+    assert results[True][1] == results[False][1]
