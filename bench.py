@@ -419,7 +419,8 @@ def main(argv=None) -> int:
             "traffic": traffic,
             "bytes_per_launch": round(update_bytes / max(upd_launches, 1)),
             "avg_launch_ms": round(upd_avg_ms, 4),
-            "stream_reference": stream_ref,
+            "stream_reference": (dict(stream_ref, update_frac_of_it=round(
+                achieved / stream_ref["GB/s"], 4)) if stream_ref else None),
         },
     }
     if args.offload:
