@@ -363,10 +363,12 @@ bool cm_vec_ok(const DevMat& d) {
 // output) 16-byte aligned per row.  Other buffers are accessed by element.
 bool rv_ok(const DevMat& d) {
   if (!ZF_RV_ENABLE || d.layout != zf::kRowMajor) return false;
-  const auto ok = [](const void* p, int64_t ld, int64_t per16) {
-    return p == nullptr || (aligned(p, 16) && ld % per16 == 0);
+  // (a single row never uses its stride)
+  const bool one_row = d.n <= 1;
+  const auto ok = [one_row](const void* p, int64_t ld, int64_t per16) {
+    return p == nullptr || (aligned(p, 16) && (one_row || ld % per16 == 0));
   };
-  return d.grad != nullptr && aligned(d.grad, 16) && d.ld_grad % 8 == 0 &&
+  return d.grad != nullptr && aligned(d.grad, 16) && (one_row || d.ld_grad % 8 == 0) &&
          ok(d.acc, d.ld_acc, 4) && ok(d.P, d.ld_state, 4) && ok(d.M, d.ld_state, 4) &&
          ok(d.V, d.ld_state, 4) && ok(d.out, d.ld_out, 4);
 }

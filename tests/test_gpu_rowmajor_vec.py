@@ -302,3 +302,34 @@ def test_plan_uses_padded_buffers():
             assert same_bits(f32_np(getattr(mb, name)), f32_np(b[name])), name
         assert np.array_equal(bits_np(mb.weight), bits_np(b["weight"]))
     plan.close()
+
+
+@pytest.mark.parametrize("n,m,ratio", [(1, 77, 0.1), (2, 8, 0.5), (17, 1009, 0.1), (9, 2017, 0.0),
+                                       (5, 300, 1.0)])
+@pytest.mark.parametrize("aligned", [True, False])
+def test_handover_on_first_step(n, m, ratio, aligned):
+    """A one-step interval (warm-up, or a refresh every step) hands over on
+    its first step: the packed buffer is neither read nor written and the
+    hand-over is scale * the gradient at the unselected columns."""
+    B = Bufs(aligned)
+    rng = np.random.default_rng(derive_seed("rv-first", n, m))
+    sel = O.select_topk(rng.random(m).astype(np.float32), O.k_from_ratio(ratio, m))
+    k = sel.k
+    P = (rng.standard_normal((n, k)) * 0.02).astype(np.float32)
+    M = (rng.standard_normal((n, k)) * 1e-3).astype(np.float32)
+    V = (rng.random((n, k)) * 1e-4).astype(np.float32)
+    W = O.bf16_round((rng.standard_normal((n, m)) * 0.02).astype(np.float32))
+    Pd, Md, Vd, Wd = B.f32(P), B.f32(M), B.f32(V), B.bf16(W)
+    A = B.nan(n, m - k)
+    D = B.nan(n, m)
+    g = grad_bits(n, m, derive_seed("rv-first-g", n, m))
+    g[0, ::5] = 0x8000  # -0.0 survives
+    zf.update_fused_handover(B.bf16(g), sel_dev(sel), Pd, Md, Vd, Wd, HP, 9, A, 1, 1, 1.0,
+                             out=D)
+    torch.cuda.synchronize()
+    Pw, Mw, Vw, wsel = O.adam_selected(g, sel.sel, P, M, V, consts(9))
+    W[:, sel.sel.astype(np.int64)] = wsel
+    check(Pd, Md, Vd, Pw, Mw, Vw, "first")
+    assert np.array_equal(bits_np(Wd), W)
+    assert np.isnan(f32_np(A)).all()  # not written
+    assert same_bits(f32_np(D), O.unpack(O.pack_accumulate(g, sel.unsel, None, 1), sel, 1.0))

@@ -94,12 +94,15 @@ def test_llama2_7b_layer_four_steps(layout):
 
 
 @pytest.mark.timeout(300)
+@pytest.mark.parametrize("warmup", [0, 3])
 @pytest.mark.parametrize("fuse", [True, False], ids=["fused-handover", "separate-handover"])
 @pytest.mark.parametrize("layout", LAYOUTS)
-def test_batched_shapes_with_unaligned_schedule(layout, fuse):
+def test_batched_shapes_with_unaligned_schedule(layout, fuse, warmup):
     """Several shapes in one plan (odd sizes take the element-wise paths),
     refresh every 3 steps and accumulation interval 2, so refreshes cut
-    intervals short; every output compared with the oracle at every step."""
+    intervals short; with a warm-up, the first steps are one-step intervals
+    (hand-over on an interval's first step); every output compared with the
+    oracle at every step."""
     shapes = [(264, 300), (97, 130), (1, 64), (4104, 65), (8, 1000)]
     ratio, R, S, steps = 0.2, 3, 2, 8
     hp = zf.AdamHparams(weight_decay=0.01)
@@ -119,9 +122,9 @@ def test_batched_shapes_with_unaligned_schedule(layout, fuse):
         w0.append(bits_np(mw))
         weights.append(mw if layout == zf.ROW_MAJOR else mw.t().contiguous())
     runner = zf.SelectiveUpdateRunner(shapes, ratio, hp, R, S, slots, weights, layout=layout,
-                                      fuse_handover=fuse)
+                                      fuse_handover=fuse, warmup=warmup)
     orcs = [O.MatrixOracle(O.widen(w0[q]), w0[q], ratio, hp.lr, hp.beta1, hp.beta2, hp.eps,
-                           hp.weight_decay, R, S) for q in range(len(shapes))]
+                           hp.weight_decay, R, S, warmup=warmup) for q in range(len(shapes))]
     for t in range(1, steps + 1):
         kind = runner.step()
         torch.cuda.synchronize()
