@@ -140,3 +140,97 @@ def test_batched_shapes_with_unaligned_schedule(layout, fuse, warmup):
             if kind.interval_end:
                 assert same_bits(T(f32_np(runner.unpacked[q]), layout), out["unpacked"]), (q, t)
     runner.close()
+
+
+def _small_set(layout, shapes, steps, seed):
+    dev = torch.device("cuda")
+    slots, weights, w0 = [], [], []
+    for t in range(1, steps + 1):
+        slot = []
+        for q, (n, m) in enumerate(shapes):
+            g = torch.Generator().manual_seed(seed * 1000 + q * 100 + t)
+            s = torch.exp(1.5 * torch.randn(m, generator=g, dtype=torch.float64))
+            gd = gradient(n, m, s, derive_seed(seed, q, t), device=dev)
+            slot.append(gd if layout == zf.ROW_MAJOR else gd.t().contiguous())
+        slots.append(slot)
+    for q, (n, m) in enumerate(shapes):
+        mw = master_weights(n, m, derive_seed(seed, q), device=dev).to(torch.bfloat16)
+        w0.append(bits_np(mw))
+        weights.append(mw if layout == zf.ROW_MAJOR else mw.t().contiguous())
+    return slots, weights, w0
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_long_run_against_oracle(layout):
+    """40 steps (refresh every 5, intervals of 3, a 2-step warm-up) over a
+    ring of 7 gradient slots: every output against the oracle at every step,
+    so that selection ping-pong, state remaps and interval boundaries are
+    exercised many times."""
+    shapes = [(64, 300), (33, 1009), (8, 77)]
+    ratio, R, S, W, steps, nslots = 0.15, 5, 3, 2, 40, 7
+    hp = zf.AdamHparams(lr=1e-3, weight_decay=0.01)
+    slots, weights, w0 = _small_set(layout, shapes, nslots, seed=41)
+    runner = zf.SelectiveUpdateRunner(shapes, ratio, hp, R, S, slots, weights, layout=layout,
+                                      warmup=W)
+    orcs = [O.MatrixOracle(O.widen(w0[q]), w0[q], ratio, hp.lr, hp.beta1, hp.beta2, hp.eps,
+                           hp.weight_decay, R, S, warmup=W) for q in range(len(shapes))]
+    for t in range(1, steps + 1):
+        kind = runner.step()
+        torch.cuda.synchronize()
+        for q, orc in enumerate(orcs):
+            out = orc.step(T(bits_np(slots[(t - 1) % nslots][q]), layout))
+            if kind.refresh:
+                assert np.array_equal(runner.selection[q].sel_idx.cpu().numpy(), orc.sel.sel), (q, t)
+            P, M, V = (T(f32_np(x), layout) for x in runner.state[q])
+            assert same_bits(P, orc.P) and same_bits(M, orc.M) and same_bits(V, orc.V), (q, t)
+            assert np.array_equal(T(bits_np(weights[q]), layout), orc.W), (q, t)
+            if kind.interval_end:
+                assert same_bits(T(f32_np(runner.unpacked[q]), layout), out["unpacked"]), (q, t)
+            else:
+                assert same_bits(T(f32_np(runner.acc[q]), layout), orc.A), (q, t)
+    runner.close()
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_two_runners_on_two_streams(layout):
+    """Two independent step drivers (different sets and schedules) enqueued
+    alternately on two streams, with no synchronisation between them, end
+    with the same bits as each driver run alone."""
+    cfgs = [dict(shapes=[(64, 300), (33, 1009)], ratio=0.1, R=3, S=2, seed=5),
+            dict(shapes=[(100, 513), (8, 64)], ratio=0.3, R=2, S=4, seed=6)]
+    steps = 12
+    hp = zf.AdamHparams(lr=1e-3)
+
+    def make(c):
+        slots, weights, _ = _small_set(layout, c["shapes"], 3, c["seed"])
+        return zf.SelectiveUpdateRunner(c["shapes"], c["ratio"], hp, c["R"], c["S"], slots,
+                                        weights, layout=layout), weights
+
+    def snapshot(runner, weights):
+        out = []
+        for q in range(len(weights)):
+            out += [x.cpu().numpy().tobytes() for x in runner.state[q]]
+            out.append(runner.unpacked[q].cpu().numpy().tobytes())
+            out.append(weights[q].view(torch.int16).cpu().numpy().tobytes())
+        return out
+
+    alone = []
+    for c in cfgs:
+        r, w = make(c)
+        for _ in range(steps):
+            r.step()
+        torch.cuda.synchronize()
+        alone.append(snapshot(r, w))
+        r.close()
+    pairs = [make(c) for c in cfgs]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    for _ in range(steps):
+        for (r, _), st in zip(pairs, streams):
+            r.step(stream=st)
+    torch.cuda.synchronize()
+    for (r, w), want in zip(pairs, alone):
+        assert snapshot(r, w) == want
+        r.close()
