@@ -64,6 +64,10 @@ def parse_args(argv=None):
                          "overlapped with the following steps")
     ap.add_argument("--no-overlap", action="store_true",
                     help="with --offload: run the deferred update synchronously")
+    ap.add_argument("--model-compute-ms", type=float, default=0.0,
+                    help="with --offload: before every step, this much stand-in model compute on "
+                         "the GPU (bf16 matrix products on the step's stream), for the forward and "
+                         "backward passes that the deferred host update overlaps with")
     ap.add_argument("--host-threads", type=int, default=None,
                     help="with --offload: host threads of the deferred update (default: "
                          "min(16, cpu count))")
@@ -307,7 +311,33 @@ def main(argv=None) -> int:
                       "GB/s": round(2 * nb / (ms * 1e-3) / 1e9, 1)}
         del src, dst
 
+    # stand-in model compute (offload mode): n_mm products of two 4096 x 4096
+    # bf16 matrices, calibrated to model_compute_ms per step
+    model = None
+    if args.model_compute_ms > 0:
+        if not args.offload:
+            print(json.dumps({"error": "--model-compute-ms needs --offload"}))
+            return 2
+        ma = torch.randn(4096, 4096, device=dev, dtype=torch.bfloat16)
+        mb = torch.randn(4096, 4096, device=dev, dtype=torch.bfloat16)
+        mc = torch.empty_like(ma)
+        for _ in range(3):
+            torch.mm(ma, mb, out=mc)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(20):
+            torch.mm(ma, mb, out=mc)
+        e1.record()
+        torch.cuda.synchronize()
+        n_mm = max(1, round(args.model_compute_ms / (e0.elapsed_time(e1) / 20)))
+
+        def model():
+            for _ in range(n_mm):
+                torch.mm(ma, mb, out=mc)
+
     for _ in range(args.warmup):
+        if model is not None:
+            model()
         runner.step()
     if args.offload:
         runner.sync()
@@ -335,6 +365,9 @@ def main(argv=None) -> int:
     torch.cuda.synchronize()
     w0 = time.perf_counter()
     for _ in range(args.steps):
+        if model is not None:
+            with recorder("model_compute"):
+                model()
         kinds.append(runner.step(recorder=recorder))
     if args.offload:
         runner.sync()  # the last deferred update lands inside the timed region
@@ -399,6 +432,7 @@ def main(argv=None) -> int:
             "accum_interval": wl.accum,
             "zen_auto_tau": args.zen_tau,
             "offload": args.offload,
+            "model_compute_ms": args.model_compute_ms or None,
             "interval_ends": sum(1 for k in kinds if k.interval_end),
             "handover": "fused into the interval's last update" if fused else
                         ("device -> host copy of the packed buffer" if args.offload
@@ -443,6 +477,16 @@ def main(argv=None) -> int:
             "stall_s": round(runner.stall_s, 4),
             "stall_ms_per_step": round(runner.stall_s / args.steps * 1e3, 3),
             "store": "pinned host memory, read in place by the swap kernels",
+            # GPU time of the recorded launches (hot path, write-back and the
+            # stand-in model compute) against the wall time: what is left is
+            # the GPU waiting for the host side
+            "model_compute_ms_per_step": round(
+                sum(per_kernel_ms.get("model_compute", [])) / args.steps, 3),
+            "gpu_busy_ms_per_step": round(
+                sum(sum(v) for v in per_kernel_ms.values()) / args.steps, 3),
+            "gpu_idle_ms_per_step": round(
+                wall / args.steps * 1e3 - sum(sum(v) for v in per_kernel_ms.values()) / args.steps,
+                3),
         }
     if not args.no_cpu_baseline:
         print("# timing the CPU oracle on a sample ...", file=sys.stderr, flush=True)
