@@ -64,6 +64,9 @@ def parse_args(argv=None):
                          "overlapped with the following steps")
     ap.add_argument("--no-overlap", action="store_true",
                     help="with --offload: run the deferred update synchronously")
+    ap.add_argument("--refresh-waits", action="store_true",
+                    help="with --offload: a refresh right after an interval end waits for the "
+                         "host update (default: the device takes over the entering columns)")
     ap.add_argument("--model-compute-ms", type=float, default=0.0,
                     help="with --offload: before every step, this much stand-in model compute on "
                          "the GPU (bf16 matrix products on the step's stream), for the forward and "
@@ -280,7 +283,8 @@ def main(argv=None) -> int:
                                       weights, device=dev, layout=layout, zen_tau=args.zen_tau,
                                       offload=args.offload, overlap=not args.no_overlap,
                                       host_threads=args.host_threads,
-                                      fuse_handover=not args.separate_handover)
+                                      fuse_handover=not args.separate_handover,
+                                      refresh_pending=not args.refresh_waits)
     fused = runner.keep_unpacked and runner.fuse_handover and args.zen_tau is None
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t0
@@ -343,6 +347,7 @@ def main(argv=None) -> int:
         runner.sync()
         runner.stall_s = runner.host_update_s = 0.0
         th0 = runner.th
+        pr0 = runner.pending_refreshes
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
@@ -466,6 +471,7 @@ def main(argv=None) -> int:
         host_bytes = 30 * unsel * intervals
         result["offload"] = {
             "overlap": not args.no_overlap,
+            "pending_refreshes": runner.pending_refreshes - pr0,
             "host_threads": runner.host_threads,
             "intervals": intervals,
             "host_update_s": round(runner.host_update_s, 4),

@@ -161,7 +161,15 @@ typedef enum zf_state_mode {
  * ZF_STATES_REMAP a column that was selected before but no longer is writes
  * its previous compact (p, m, v) to its column of the store (swap-out), so
  * the prev_* states are then required even when k = 0.  The store must not
- * overlap any other buffer of the call. */
+ * overlap any other buffer of the call.
+ *
+ * Owed deferred update (read by zf_plan_update_pending only, else may be
+ * NULL): pend_acc holds the packed sums of the accumulation interval that
+ * ended just before a refresh, under the previous selection (which has k
+ * columns as well), in the layout of the packed buffer with row stride
+ * ld_pend ([n][ld_pend >= m-k],
+ * channel-major [m-k][ld_pend >= n]; slot u' = the u'-th column, in
+ * ascending order, that the previous selection left unselected). */
 typedef struct zf_state_source {
   const uint64_t* prev_mask;
   const int32_t* prev_prefix;
@@ -175,6 +183,8 @@ typedef struct zf_state_source {
   float* store_exp_avg;
   float* store_exp_avg_sq;
   int64_t ld_store;
+  const float* pend_acc;
+  int64_t ld_pend;
 } zf_state_source;
 
 /* Text for a status code (static storage). */
@@ -405,6 +415,39 @@ zf_status zf_plan_update_handover(zf_plan* plan, const zf_adam_hparams* hp, int6
 
 /* zf_scatter_weights over every matrix (weight_cols of each descriptor). */
 zf_status zf_plan_scatter_weights(zf_plan* plan, zf_stream stream);
+
+/* The refresh step of the offloaded optimizer while the host is still
+ * applying the deferred update of the interval that ended at the previous
+ * step (paper, Zero-stall Pipeline: the GPU does not wait for the CPU-side
+ * optimizer).  zf_plan_update with do_adam = do_pack = 1, mode
+ * ZF_STATES_REMAP and step_in_interval = 1 against the full-state store,
+ * except that a column entering the selection (selected now, unselected in
+ * src.prev_mask) first takes the deferred step that its store column still
+ * owes, then this step's Adam:
+ *   g' = pend_acc[i][u'] * pend_scale  (u' its slot under the previous
+ *        selection);  (p, m, v) = its store column;  the element sequence
+ *        of zf_adam_selected with the constants of pend_step and g';
+ *   then g = G[i][j] and the constants of `step` as in zf_adam_selected.
+ * The results equal, bit for bit, those of zf_host_adam_unselected (same
+ * pend_acc, pend_scale, pend_step) landing in the store before a plain
+ * refresh.  The entering columns' store columns are only read: the caller
+ * must not write them before this call has completed, and the write-back
+ * of that host update must skip the columns the refresh selected
+ * (zf_plan_scatter_weights_skip_prev).  Every descriptor needs the store,
+ * the previous selection and states, the packed buffer and pend_acc, which
+ * must not overlap any buffer the call writes.  pend_step >= 1; pend_scale
+ * finite.  Not for Zen-auto (zf_plan_update_zen). */
+zf_status zf_plan_update_pending(zf_plan* plan, const zf_adam_hparams* hp, int64_t step,
+                                 int64_t accum_interval, int64_t pend_step, float pend_scale,
+                                 zf_stream stream);
+
+/* zf_plan_scatter_weights, except that every column set in the
+ * descriptor's src.prev_mask is left untouched: the write-back of a
+ * deferred update issued after the refresh that zf_plan_update_pending
+ * ran, on a plan whose sel is the selection the update ran under and whose
+ * src.prev_mask is the refreshed selection (the columns that entered it
+ * already hold the selective optimizer's weights). */
+zf_status zf_plan_scatter_weights_skip_prev(zf_plan* plan, zf_stream stream);
 
 /* ---- Zen-auto: adaptive accumulation interval ---------------------------- */
 

@@ -43,7 +43,7 @@ class ZfStateSource(ctypes.Structure):
                 ("prev_exp_avg", c_vp), ("prev_exp_avg_sq", c_vp), ("ld_prev", c_i64),
                 ("init_master", c_vp), ("ld_init", c_i64),
                 ("store_master", c_vp), ("store_exp_avg", c_vp), ("store_exp_avg_sq", c_vp),
-                ("ld_store", c_i64)]
+                ("ld_store", c_i64), ("pend_acc", c_vp), ("ld_pend", c_i64)]
 
 
 class ZfMatrix(ctypes.Structure):
@@ -110,6 +110,9 @@ SIGNATURES = [
      [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, c_i32, c_i64, c_i64, c_flt, c_vp]),
     ("zf_plan_update_zen", ctypes.c_int,
      [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, c_i32, c_i64, c_i64, c_dbl, c_vp, c_vp]),
+    ("zf_plan_update_pending", ctypes.c_int,
+     [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, c_i64, c_i64, c_flt, c_vp]),
+    ("zf_plan_scatter_weights_skip_prev", ctypes.c_int, [c_vp, c_vp]),
 ]
 
 
@@ -314,6 +317,10 @@ class StateSource:
     store_master: Optional[torch.Tensor] = None
     store_exp_avg: Optional[torch.Tensor] = None
     store_exp_avg_sq: Optional[torch.Tensor] = None
+    # packed sums of the interval that ended just before a refresh, under the
+    # previous selection (the deferred update the store still owes; read by
+    # Plan.update_pending only)
+    pend_acc: Optional[torch.Tensor] = None
 
     def as_c(self) -> ZfStateSource:
         ld_prev = 0
@@ -332,13 +339,16 @@ class StateSource:
                     or _mat(self.store_exp_avg_sq, torch.float32, "store_exp_avg_sq",
                             device_ok=True) != ld_store):
                 raise ValueError("the store's three arrays must share one row stride")
+        ld_pend = 0
+        if self.pend_acc is not None:
+            ld_pend = _mat(self.pend_acc, torch.float32, "pend_acc", device_ok=True)
         return ZfStateSource(
             _ptr(self.prev.mask) if self.prev else None,
             _ptr(self.prev.prefix) if self.prev else None,
             _ptr(self.prev_master), _ptr(self.prev_exp_avg), _ptr(self.prev_exp_avg_sq), ld_prev,
             _ptr(self.init_master), ld_init,
             _ptr(self.store_master), _ptr(self.store_exp_avg), _ptr(self.store_exp_avg_sq),
-            ld_store)
+            ld_store, _ptr(self.pend_acc), ld_pend)
 
 
 def _states(n, k, master, exp_avg, exp_avg_sq, layout):
@@ -600,6 +610,25 @@ class Plan:
     def scatter_weights(self, stream=None) -> None:
         """W[:, unsel] = weight_cols of every matrix (zf_plan_scatter_weights)."""
         _check("zf_plan_scatter_weights", LIB.zf_plan_scatter_weights(self._h, _stream(stream)))
+
+    def update_pending(self, hp: AdamHparams, step: int, accum_interval: int, pend_step: int,
+                       pend_scale: float, stream=None) -> None:
+        """The refresh step of the offloaded optimizer while the host still
+        applies the previous interval's deferred update
+        (zf_plan_update_pending): a remap + fused update against the store
+        in which every column entering the selection first takes the owed
+        step (pend_scale x its sums in src.pend_acc, constants of
+        pend_step)."""
+        c_hp = hp.as_c()
+        _check("zf_plan_update_pending", LIB.zf_plan_update_pending(
+            self._h, ctypes.byref(c_hp), step, accum_interval, pend_step, float(pend_scale),
+            _stream(stream)))
+
+    def scatter_weights_skip_prev(self, stream=None) -> None:
+        """scatter_weights, leaving the columns of each matrix's src.prev
+        selection untouched (zf_plan_scatter_weights_skip_prev)."""
+        _check("zf_plan_scatter_weights_skip_prev",
+               LIB.zf_plan_scatter_weights_skip_prev(self._h, _stream(stream)))
 
     def update_zen(self, hp: AdamHparams, step: int, mode: int, step_in_interval: int,
                    accum_interval: int, tau: float, totals: torch.Tensor, stream=None) -> None:

@@ -342,6 +342,8 @@ void apply_source(DevMat& d, const zf_state_source* src) {
   d.st_M = src->store_exp_avg;
   d.st_V = src->store_exp_avg_sq;
   d.ld_store = src->ld_store;
+  d.pend_acc = src->pend_acc;
+  d.ld_pend = src->ld_pend;
 }
 
 // Channel-major vector path: n a multiple of 8 and every present row start
@@ -355,7 +357,7 @@ bool cm_vec_ok(const DevMat& d) {
          ok(d.M, d.ld_state, 4) && ok(d.V, d.ld_state, 4) && ok(d.acc, d.ld_acc, 4) &&
          ok(d.out, d.ld_out, 4) && ok(d.prev_P, d.ld_prev, 4) && ok(d.prev_M, d.ld_prev, 4) &&
          ok(d.prev_V, d.ld_prev, 4) && ok(d.init_P, d.ld_init, 4) && ok(d.st_P, d.ld_store, 4) &&
-         ok(d.st_M, d.ld_store, 4) && ok(d.st_V, d.ld_store, 4);
+         ok(d.st_M, d.ld_store, 4) && ok(d.st_V, d.ld_store, 4) && ok(d.pend_acc, d.ld_pend, 4);
 }
 
 // Row-major 16-byte update: G rows 16-byte aligned (8 bf16), and every
@@ -742,7 +744,8 @@ struct zf_plan {
           blk_upv = 0;
   int64_t k_total = 0, u_total = 0;
   bool can_colnorm = true, can_topk = true, can_adam = true, can_remap = true, can_pack = true,
-       can_unpack = true, can_zen = true, can_scatter = true, can_handover = true;
+       can_unpack = true, can_zen = true, can_scatter = true, can_handover = true,
+       can_pending = true, can_scatter_skip = true;
 };
 
 namespace {
@@ -810,6 +813,21 @@ zf_status check_plan_matrix(const zf_matrix& x, zf_plan& p) {
                   mat_ok(x.weight, eg, x.ld_weight, 2) &&
                   !overlaps(span(x.weight_cols, ea, x.ld_weight_cols, 2),
                             span(x.weight, eg, x.ld_weight, 2));
+  p.can_scatter_skip = p.can_scatter_skip && p.can_scatter && vector_ok(x.src.prev_mask, words, 8);
+  // refresh with the owed deferred update: the store, and the previous
+  // interval's sums, read only, disjoint from everything the update writes
+  {
+    const Span pa = span(x.src.pend_acc, ea, x.src.ld_pend, 4);
+    const Ext es = ext(L, n, k);
+    p.can_pending = p.can_pending && x.src.store_master != nullptr &&
+                    mat_ok(x.src.pend_acc, ea, x.src.ld_pend, 4) &&
+                    (n * (m - k) == 0 || device_accessible(x.src.pend_acc)) &&
+                    !overlaps(pa, span(x.acc, ea, x.ld_acc, 4)) &&
+                    !overlaps(pa, span(x.master, es, x.ld_state, 4)) &&
+                    !overlaps(pa, span(x.exp_avg, es, x.ld_state, 4)) &&
+                    !overlaps(pa, span(x.exp_avg_sq, es, x.ld_state, 4)) &&
+                    !overlaps(pa, span(x.weight, eg, x.ld_weight, 2)) && !store_overlaps(d, pa);
+  }
   // Zen-auto statistics: [k] and [m-k] fp32 outputs that overlap neither
   // each other nor any buffer the fused update touches.
   {
@@ -1065,6 +1083,34 @@ zf_status zf_plan_scatter_weights(zf_plan* p, zf_stream stream) {
   if (p == nullptr || !p->can_scatter) return ZF_EINVAL;
   const Table t{p->d_mats, p->d_off_unp, p->nmats};
   const hipError_t e = zf::launch_scatter(t, p->mats[0], p->blk_unp, p->layout, as_stream(stream));
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
+zf_status zf_plan_update_pending(zf_plan* p, const zf_adam_hparams* hp, int64_t step,
+                                 int64_t accum_interval, int64_t pend_step, float pend_scale,
+                                 zf_stream stream) {
+  if (p == nullptr || !p->can_remap || !p->can_pack || !p->can_pending) return ZF_EINVAL;
+  if (!hparams_ok(hp) || step < 1 || pend_step < 1 || !std::isfinite(pend_scale) ||
+      accum_interval < 1)
+    return ZF_EINVAL;
+  const AdamK c = adam_consts(*hp, step);
+  const zf::Pending pd{adam_consts(*hp, pend_step), pend_scale};
+  const hipStream_t s = as_stream(stream);
+  const Table t{p->d_mats, p->d_off_up, p->nmats};
+  const hipError_t e =
+      p->layout == zf::kChannelMajor
+          ? zf::launch_cm_update(t, p->mats[0], p->blk_up, c, zf::kRemap, 1, true, true, nullptr,
+                                 false, 1.0f, s, &pd)
+          : zf::launch_update(t, p->mats[0], p->blk_up, c, zf::kRemap, 1, true, true, false, 1.0f,
+                              s, &pd);
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
+zf_status zf_plan_scatter_weights_skip_prev(zf_plan* p, zf_stream stream) {
+  if (p == nullptr || !p->can_scatter_skip) return ZF_EINVAL;
+  const Table t{p->d_mats, p->d_off_unp, p->nmats};
+  const hipError_t e =
+      zf::launch_scatter(t, p->mats[0], p->blk_unp, p->layout, as_stream(stream), true);
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 

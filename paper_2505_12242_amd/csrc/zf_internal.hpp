@@ -81,6 +81,8 @@ struct DevMat {
   int64_t ld_store;
   const uint16_t* wcols;  // deferred update: bf16 weights of the unselected columns (slot order)
   int64_t ld_wcols;
+  const float* pend_acc;  // owed deferred update: packed sums under the previous selection
+  int64_t ld_pend;
   float* sel_sq;     // Zen-auto: [k] squared norms of the selected channels' gradient
   float* acc_sq;     // Zen-auto: [m-k] squared norms of the accumulated channels
   // geometry
@@ -118,6 +120,14 @@ struct AdamK {
   float b1, b2, c1, c2, lr, eps, wd, ib1, ib2;
 };
 
+// The deferred update that the full-state store still owes the columns
+// entering the selection at a refresh: each first takes gradient
+// scale * (its packed sum under the previous selection) with constants c.
+struct Pending {
+  AdamK c;
+  float scale;
+};
+
 // Hyperparameter validation and the constants of a 1-based step
 // (zf_api.hip): B1 = beta1, C1 = 1 - beta1, B2 = beta2, C2 = 1 - beta2,
 // LR = lr, EPS = eps, WD = lr * weight_decay, IB1 = 1 / (1 - beta1^t),
@@ -129,9 +139,11 @@ AdamK adam_consts(const zf_adam_hparams& hp, int64_t step);
 hipError_t launch_colnorm(const Table& t, const DevMat& one, int64_t blocks,
                           const Table& tf, int64_t fin_blocks, double* ws, hipStream_t s);
 hipError_t launch_topk(const Table& t, const DevMat& one, int64_t blocks, hipStream_t s);
+// pend != nullptr: fused Adam + pack in kRemap against the store, with the
+// owed deferred update applied to the entering columns first.
 hipError_t launch_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
                          int32_t mode, int32_t first, bool adam, bool pack, bool handover,
-                         float scale, hipStream_t s);
+                         float scale, hipStream_t s, const Pending* pend = nullptr);
 hipError_t launch_unpack(const Table& t, const DevMat& one, int64_t blocks, float scale,
                          hipStream_t s);
 
@@ -149,16 +161,19 @@ hipError_t launch_cm_colnorm(const Table& t, const DevMat& one, int64_t blocks, 
 // handover: the last step of an interval with the hand-over fused in (the
 // `out` buffer receives scale * the final sums, +0.0 for selected columns;
 // the packed buffer is not written).
+// pend: as in launch_update.
 hipError_t launch_cm_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
                             int32_t mode, int32_t first, bool adam, bool pack, double* zs,
-                            bool handover, float scale, hipStream_t s);
+                            bool handover, float scale, hipStream_t s,
+                            const Pending* pend = nullptr);
 hipError_t launch_cm_unpack(const Table& t, const DevMat& one, int64_t blocks, float scale,
                             hipStream_t s);
 
 // Deferred update write-back (zf_kernels_offload.hip): W[:, unsel[u]] =
-// wcols[:, u] in either layout (grid: unpack geometry).
+// wcols[:, u] in either layout (grid: unpack geometry); skip_prev: columns
+// set in prev_mask are left untouched.
 hipError_t launch_scatter(const Table& t, const DevMat& one, int64_t blocks, int32_t layout,
-                          hipStream_t s);
+                          hipStream_t s, bool skip_prev = false);
 
 // Zen-auto reductions (zf_kernels_zen.hip).  Totals as written to device
 // memory; the layout equals the public zf_zen_totals.

@@ -354,25 +354,34 @@ struct AdamSrc {
   uint32_t vI, sI;
   rsrc_t rTP, rTM, rTV;         // full-state store (swap-in)
   uint32_t vT, sT;
+  rsrc_t rPA;                   // owed deferred update: previous interval's sums
+  uint32_t vPA, sPA;
 };
 
 enum SrcKind {
   kSrcInplace = 0, kSrcRemapW, kSrcRemapMaster, kSrcInitW, kSrcInitMaster,
-  kSrcRemapStore, kSrcInitStore  // swap-in of new columns from the full-state store
+  kSrcRemapStore, kSrcInitStore,  // swap-in of new columns from the full-state store
+  kSrcRemapStorePend              // the same, after the owed deferred step (Pending)
 };
 
 template <int SRC>
 __device__ __forceinline__ void load_state(const AdamSrc& a, int32_t i, float& p, float& m,
-                                           float& v) {
+                                           float& v, const Pending* pd = nullptr) {
   if constexpr (SRC == kSrcInplace) {
     p = buf_f32(a.rP, a.vS, i * a.sS);
     m = buf_f32(a.rM, a.vS, i * a.sS);
     v = buf_f32(a.rV, a.vS, i * a.sS);
-  } else if constexpr (SRC == kSrcRemapStore || SRC == kSrcInitStore) {
-    const float pt = buf_f32(a.rTP, a.vT, i * a.sT);
-    const float mt = buf_f32(a.rTM, a.vT, i * a.sT);
-    const float vt = buf_f32(a.rTV, a.vT, i * a.sT);
-    if constexpr (SRC == kSrcRemapStore) {
+  } else if constexpr (SRC == kSrcRemapStore || SRC == kSrcInitStore ||
+                       SRC == kSrcRemapStorePend) {
+    float pt = buf_f32(a.rTP, a.vT, i * a.sT);
+    float mt = buf_f32(a.rTM, a.vT, i * a.sT);
+    float vt = buf_f32(a.rTV, a.vT, i * a.sT);
+    if constexpr (SRC == kSrcRemapStorePend) {
+      // every lane takes the deferred step; a lane whose column was selected
+      // before reads slot 0 (any valid slot) and keeps its previous states
+      adam_step(buf_f32(a.rPA, a.vPA, i * a.sPA) * pd->scale, pt, mt, vt, pd->c);
+    }
+    if constexpr (SRC == kSrcRemapStore || SRC == kSrcRemapStorePend) {
       // both sources are read; the lane keeps the one that applies
       const float pp = buf_f32(a.rSP, a.vPrev, i * a.sPrev);
       const float mp = buf_f32(a.rSM, a.vPrev, i * a.sPrev);
@@ -410,7 +419,8 @@ __device__ __forceinline__ void load_state(const AdamSrc& a, int32_t i, float& p
 
 template <int SRC>
 __device__ __forceinline__ void adam_rows(const AdamSrc& a, rsrc_t rG, uint32_t sG,
-                                          const AdamK& c, int32_t rows) {
+                                          const AdamK& c, int32_t rows,
+                                          const Pending* pd = nullptr) {
   int32_t i = 0;
   for (; i + kAdamBatch <= rows; i += kAdamBatch) {
     uint16_t gb[kAdamBatch];
@@ -418,7 +428,7 @@ __device__ __forceinline__ void adam_rows(const AdamSrc& a, rsrc_t rG, uint32_t 
 #pragma unroll
     for (int b = 0; b < kAdamBatch; ++b) gb[b] = buf_u16<ZF_RM_AUX_RO>(rG, a.vG, (i + b) * sG);
 #pragma unroll
-    for (int b = 0; b < kAdamBatch; ++b) load_state<SRC>(a, i + b, p[b], mm[b], vv[b]);
+    for (int b = 0; b < kAdamBatch; ++b) load_state<SRC>(a, i + b, p[b], mm[b], vv[b], pd);
 #pragma unroll
     for (int b = 0; b < kAdamBatch; ++b) {
       adam_step(widen_bf16(gb[b]), p[b], mm[b], vv[b], c);
@@ -432,7 +442,7 @@ __device__ __forceinline__ void adam_rows(const AdamSrc& a, rsrc_t rG, uint32_t 
   for (; i < rows; ++i) {
     float p, mm, vv;
     const float g = widen_bf16(buf_u16<ZF_RM_AUX_RO>(rG, a.vG, i * sG));
-    load_state<SRC>(a, i, p, mm, vv);
+    load_state<SRC>(a, i, p, mm, vv, pd);
     adam_step(g, p, mm, vv, c);
     buf_put_f32(p, a.rP, a.vS, i * a.sS);
     buf_put_f32(mm, a.rM, a.vS, i * a.sS);
@@ -441,12 +451,15 @@ __device__ __forceinline__ void adam_rows(const AdamSrc& a, rsrc_t rG, uint32_t 
   }
 }
 
-template <bool BATCHED, bool ADAM, bool PACK, bool HAND>
+// PEND (fused Adam + pack in kRemap against the store only): a column that
+// enters the selection takes the owed deferred step pd first, from its slot
+// among the previous selection's unselected columns.
+template <bool BATCHED, bool ADAM, bool PACK, bool HAND, bool PEND>
 __global__ __launch_bounds__(kThreads) void update_kernel(const DevMat* __restrict__ mats,
                                                           const int64_t* __restrict__ off,
                                                           int32_t nmats, DevMat one, AdamK c,
                                                           int32_t mode, int32_t first,
-                                                          float scale) {
+                                                          float scale, Pending pd) {
   int64_t local;
   const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, local);
   const int64_t cblk = local % d.up_cb;
@@ -526,9 +539,9 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const DevMat* __restri
     a.vI = j * 4u;
     a.sI = static_cast<uint32_t>(d.ld_init * 4);
   }
-  a.rTP = a.rTM = a.rTV = a.rP;
-  a.vT = 0;
-  a.sT = 0;
+  a.rTP = a.rTM = a.rTV = a.rPA = a.rP;
+  a.vT = a.vPA = 0;
+  a.sT = a.sPA = 0;
   if (mode != kInplace && store) {
     a.rTP = rows_rsrc(d.st_P, i0, i1, d.ld_store, d.m);
     a.rTM = rows_rsrc(d.st_M, i0, i1, d.ld_store, d.m);
@@ -548,6 +561,13 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const DevMat* __restri
     a.rSP = rows_rsrc(d.prev_P, i0, i1, d.ld_prev, d.m);
     a.rSM = rows_rsrc(d.prev_M, i0, i1, d.ld_prev, d.m);
     a.rSV = rows_rsrc(d.prev_V, i0, i1, d.ld_prev, d.m);
+    if constexpr (PEND) {
+      // (no unselected columns: an empty resource, every read returns 0)
+      a.rPA = d.m > d.k ? rows_rsrc(d.pend_acc, i0, i1, d.ld_pend, d.m - d.k)
+                        : make_rsrc(d.pend_acc, 0);
+      a.vPA = (a.was ? 0u : j - ro) * 4u;
+      a.sPA = static_cast<uint32_t>(d.ld_pend * 4);
+    }
   }
   if constexpr (HAND) {
     // the hand-over buffer is +0.0 at a selected column
@@ -557,7 +577,8 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const DevMat* __restri
   }
   if (mode == kInplace) adam_rows<kSrcInplace>(a, rG, sG, c, rows);
   else if (mode == kRemap) {
-    if (store) adam_rows<kSrcRemapStore>(a, rG, sG, c, rows);
+    if (PEND) adam_rows<kSrcRemapStorePend>(a, rG, sG, c, rows, &pd);
+    else if (store) adam_rows<kSrcRemapStore>(a, rG, sG, c, rows);
     else if (master) adam_rows<kSrcRemapMaster>(a, rG, sG, c, rows);
     else adam_rows<kSrcRemapW>(a, rG, sG, c, rows);
   } else {
@@ -650,25 +671,29 @@ hipError_t launch_topk(const Table& t, const DevMat& one, int64_t blocks, hipStr
   return hipGetLastError();
 }
 
-template <bool ADAM, bool PACK, bool HAND>
+template <bool ADAM, bool PACK, bool HAND, bool PEND = false>
 static void launch_update_t(const Table& t, const DevMat& one, dim3 grid, const AdamK& c,
-                            int32_t mode, int32_t first, float scale, hipStream_t s) {
+                            int32_t mode, int32_t first, float scale, hipStream_t s,
+                            const Pending& pd = Pending{}) {
   if (t.mats != nullptr)
-    hipLaunchKernelGGL((update_kernel<true, ADAM, PACK, HAND>), grid, dim3(kThreads), 0, s,
-                       t.mats, t.off, t.nmats, one, c, mode, first, scale);
+    hipLaunchKernelGGL((update_kernel<true, ADAM, PACK, HAND, PEND>), grid, dim3(kThreads), 0, s,
+                       t.mats, t.off, t.nmats, one, c, mode, first, scale, pd);
   else
-    hipLaunchKernelGGL((update_kernel<false, ADAM, PACK, HAND>), grid, dim3(kThreads), 0, s,
-                       t.mats, t.off, t.nmats, one, c, mode, first, scale);
+    hipLaunchKernelGGL((update_kernel<false, ADAM, PACK, HAND, PEND>), grid, dim3(kThreads), 0, s,
+                       t.mats, t.off, t.nmats, one, c, mode, first, scale, pd);
 }
 
 hipError_t launch_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
                          int32_t mode, int32_t first, bool adam, bool pack, bool handover,
-                         float scale, hipStream_t s) {
+                         float scale, hipStream_t s, const Pending* pend) {
   (void)hipGetLastError();
   if (blocks <= 0) return hipSuccess;
   const dim3 grid(static_cast<uint32_t>(blocks));
   if (handover && !(adam && pack)) return hipErrorInvalidValue;
-  if (handover) launch_update_t<true, true, true>(t, one, grid, c, mode, first, scale, s);
+  if (pend != nullptr) {
+    if (!(adam && pack) || handover || mode != kRemap) return hipErrorInvalidValue;
+    launch_update_t<true, true, false, true>(t, one, grid, c, mode, first, 1.0f, s, *pend);
+  } else if (handover) launch_update_t<true, true, true>(t, one, grid, c, mode, first, scale, s);
   else if (adam && pack) launch_update_t<true, true, false>(t, one, grid, c, mode, first, 1.0f, s);
   else if (adam) launch_update_t<true, false, false>(t, one, grid, c, mode, first, 1.0f, s);
   else if (pack) launch_update_t<false, true, false>(t, one, grid, c, mode, first, 1.0f, s);

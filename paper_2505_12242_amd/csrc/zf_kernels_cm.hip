@@ -170,14 +170,17 @@ __global__ __launch_bounds__(kThreads) void cm_colnorm_kernel(const DevMat* __re
 // a3-a5: fused Adam (selected channels) and pack (unselected channels).
 // ---------------------------------------------------------------------------
 
-enum CmSrc { kCmInplace = 0, kCmPrev, kCmInitW, kCmInitMaster };
+// kCmPend: read from the store like kCmPrev, then the owed deferred step
+// with gradient pd.scale * (row rPA of the previous interval's sums).
+enum CmSrc { kCmInplace = 0, kCmPrev, kCmInitW, kCmInitMaster, kCmPend };
 
 // Adam over one chunk of channel j (slot r), vector path.  SRC picks where
 // (p, m, v) come from; rS* are the source rows (the slot's own rows in place).
 template <int SRC, int VPT, bool STATS>
 __device__ __forceinline__ void cm_adam_vec(rsrc_t rG, rsrc_t rP, rsrc_t rM, rsrc_t rV,
                                             rsrc_t rW, rsrc_t rSP, rsrc_t rSM, rsrc_t rSV,
-                                            rsrc_t rI, const AdamK& c, double& ss) {
+                                            rsrc_t rI, const AdamK& c, double& ss,
+                                            rsrc_t rPA = rsrc_t(), const Pending* pd = nullptr) {
   const int tid = threadIdx.x;
   float g[VPT][kGroup], p[VPT][kGroup], m[VPT][kGroup], v[VPT][kGroup];
   u32x4 gv[VPT];
@@ -186,10 +189,15 @@ __device__ __forceinline__ void cm_adam_vec(rsrc_t rG, rsrc_t rP, rsrc_t rM, rsr
 #pragma unroll
   for (int q = 0; q < VPT; ++q) {
     const uint32_t e = group_elem(q, tid);
-    if constexpr (SRC == kCmInplace || SRC == kCmPrev) {
+    if constexpr (SRC == kCmInplace || SRC == kCmPrev || SRC == kCmPend) {
       f32x8_load<kAuxRMW>(rSP, e * 4, p[q]);
       f32x8_load<kAuxRMW>(rSM, e * 4, m[q]);
       f32x8_load<kAuxRMW>(rSV, e * 4, v[q]);
+      if constexpr (SRC == kCmPend) {
+        f32x8_load<kAuxRO>(rPA, e * 4, g[q]);
+#pragma unroll
+        for (int i = 0; i < kGroup; ++i) adam_step(g[q][i] * pd->scale, p[q][i], m[q][i], v[q][i], pd->c);
+      }
     } else {
       if constexpr (SRC == kCmInitMaster) f32x8_load<kAuxRO>(rI, e * 4, p[q]);
       else widen8(buf_b128<kAuxRO>(rI, e * 2, 0), p[q]);
@@ -215,16 +223,19 @@ __device__ __forceinline__ void cm_adam_vec(rsrc_t rG, rsrc_t rP, rsrc_t rM, rsr
 template <int SRC, bool STATS>
 __device__ __forceinline__ void cm_adam_elem(rsrc_t rG, rsrc_t rP, rsrc_t rM, rsrc_t rV,
                                              rsrc_t rW, rsrc_t rSP, rsrc_t rSM, rsrc_t rSV,
-                                             rsrc_t rI, const AdamK& c, int64_t len, double& ss) {
+                                             rsrc_t rI, const AdamK& c, int64_t len, double& ss,
+                                             rsrc_t rPA = rsrc_t(), const Pending* pd = nullptr) {
   for (int64_t e = threadIdx.x; e < len; e += kThreads) {
     const uint32_t o = static_cast<uint32_t>(e);
     const float g = widen_bf16(buf_u16<kAuxRO>(rG, o * 2, 0));
     if constexpr (STATS) ss = __builtin_fma(static_cast<double>(g), static_cast<double>(g), ss);
     float p, m, v;
-    if constexpr (SRC == kCmInplace || SRC == kCmPrev) {
+    if constexpr (SRC == kCmInplace || SRC == kCmPrev || SRC == kCmPend) {
       p = buf_f32<kAuxRMW>(rSP, o * 4, 0);
       m = buf_f32<kAuxRMW>(rSM, o * 4, 0);
       v = buf_f32<kAuxRMW>(rSV, o * 4, 0);
+      if constexpr (SRC == kCmPend)
+        adam_step(buf_f32<kAuxRO>(rPA, o * 4, 0) * pd->scale, p, m, v, pd->c);
     } else {
       p = (SRC == kCmInitMaster) ? buf_f32<kAuxRO>(rI, o * 4, 0) : widen_bf16(buf_u16<kAuxRO>(rI, o * 2, 0));
       m = v = 0.0f;
@@ -287,9 +298,10 @@ template <int SRC, bool STATS>
 __device__ __forceinline__ void cm_adam_vec_any(int vpt, rsrc_t rG, rsrc_t rP, rsrc_t rM,
                                                 rsrc_t rV, rsrc_t rW, rsrc_t rSP, rsrc_t rSM,
                                                 rsrc_t rSV, rsrc_t rI, const AdamK& c,
-                                                double& ss) {
-  if (vpt >= 2) cm_adam_vec<SRC, kCmVpt, STATS>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss);
-  else cm_adam_vec<SRC, 1, STATS>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss);
+                                                double& ss, rsrc_t rPA = rsrc_t(),
+                                                const Pending* pd = nullptr) {
+  if (vpt >= 2) cm_adam_vec<SRC, kCmVpt, STATS>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss, rPA, pd);
+  else cm_adam_vec<SRC, 1, STATS>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss, rPA, pd);
 }
 
 template <bool FIRST, bool STATS, bool HAND = false>
@@ -355,17 +367,23 @@ __device__ __forceinline__ void cm_swap_out(const DevMat& d, int64_t j, int64_t 
 // is written instead of the packed sums -- out row j = scale * (A + g) for an
 // unselected channel, +0.0 for a selected one -- and the packed buffer is
 // left as it was (it is overwritten when the next interval starts).
+//
+// PEND (fused Adam + pack in kRemap against the store only): a channel that
+// enters the selection takes the owed deferred step pd first (its row of
+// pend_acc is its slot among the previous selection's unselected channels:
+// j minus the previously selected channels below j).
 #ifdef ZF_CM_WAVES_PER_EU
 #define ZF_CM_UPDATE_ATTR __attribute__((amdgpu_waves_per_eu(ZF_CM_WAVES_PER_EU)))
 #else
 #define ZF_CM_UPDATE_ATTR
 #endif
-template <bool BATCHED, bool ADAM, bool PACK, bool STATS, bool HAND>
+template <bool BATCHED, bool ADAM, bool PACK, bool STATS, bool HAND, bool PEND>
 __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(const DevMat* __restrict__ mats,
                                                             const int64_t* __restrict__ off,
                                                             int32_t nmats, DevMat one, AdamK c,
                                                             int32_t mode, int32_t first,
-                                                            double* __restrict__ zs, float scale) {
+                                                            double* __restrict__ zs, float scale,
+                                                            Pending pd) {
   int64_t local;
   const DevMat& d = get_mat<BATCHED>(mats, off, nmats, one, local);
   const int64_t chunk = static_cast<int64_t>(d.cm_vpt) * kThreads * kGroup;
@@ -410,11 +428,12 @@ __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(c
     const rsrc_t rW = make_rsrc(d.weight + j * d.ld_weight + e0, len * 2);
     int src = kCmInplace;
     rsrc_t rSP = rP, rSM = rM, rSV = rV, rI = rW;
+    int64_t ro = 0;  // previously selected channels below j
     if (mode == kRemap) {
       const uint64_t pm = uniform_u64(d.prev_mask[w]);
+      ro = static_cast<int64_t>(uniform_i32(d.prev_prefix[w])) +
+           __popcll(pm & ((uint64_t(1) << (j & 63)) - 1));
       if ((pm >> (j & 63)) & 1ull) {
-        const int64_t ro = static_cast<int64_t>(uniform_i32(d.prev_prefix[w])) +
-                           __popcll(pm & ((uint64_t(1) << (j & 63)) - 1));
         rSP = make_rsrc(d.prev_P + ro * d.ld_prev + e0, len * 4);
         rSM = make_rsrc(d.prev_M + ro * d.ld_prev + e0, len * 4);
         rSV = make_rsrc(d.prev_V + ro * d.ld_prev + e0, len * 4);
@@ -430,10 +449,14 @@ __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(c
       rSP = make_rsrc(d.st_P + j * d.ld_store + e0, len * 4);
       rSM = make_rsrc(d.st_M + j * d.ld_store + e0, len * 4);
       rSV = make_rsrc(d.st_V + j * d.ld_store + e0, len * 4);
-      src = kCmPrev;
+      src = PEND ? kCmPend : kCmPrev;
     }
     if (src == kCmInitMaster) rI = make_rsrc(d.init_P + j * d.ld_init + e0, len * 4);
-    if (d.vec) {
+    if (PEND && src == kCmPend) {
+      const rsrc_t rPA = make_rsrc(d.pend_acc + (j - ro) * d.ld_pend + e0, len * 4);
+      if (d.vec) cm_adam_vec_any<kCmPend, STATS>(d.cm_vpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss, rPA, &pd);
+      else cm_adam_elem<kCmPend, STATS>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, len, ss, rPA, &pd);
+    } else if (d.vec) {
       switch (src) {
         case kCmInplace: cm_adam_vec_any<kCmInplace, STATS>(d.cm_vpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss); break;
         case kCmPrev: cm_adam_vec_any<kCmPrev, STATS>(d.cm_vpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss); break;
@@ -532,27 +555,33 @@ hipError_t launch_cm_colnorm(const Table& t, const DevMat& one, int64_t blocks, 
 #endif
 constexpr unsigned kCmUpdateLds = ZF_CM_UPDATE_LDS;
 
-template <bool ADAM, bool PACK, bool STATS, bool HAND>
+template <bool ADAM, bool PACK, bool STATS, bool HAND, bool PEND = false>
 static void launch_cm_update_t(const Table& t, const DevMat& one, dim3 grid, const AdamK& c,
                                int32_t mode, int32_t first, double* zs, float scale,
-                               hipStream_t s) {
+                               hipStream_t s, const Pending& pd = Pending{}) {
   if (t.mats != nullptr)
-    hipLaunchKernelGGL((cm_update_kernel<true, ADAM, PACK, STATS, HAND>), grid, dim3(kThreads),
-                       kCmUpdateLds, s, t.mats, t.off, t.nmats, one, c, mode, first, zs, scale);
+    hipLaunchKernelGGL((cm_update_kernel<true, ADAM, PACK, STATS, HAND, PEND>), grid,
+                       dim3(kThreads), kCmUpdateLds, s, t.mats, t.off, t.nmats, one, c, mode,
+                       first, zs, scale, pd);
   else
-    hipLaunchKernelGGL((cm_update_kernel<false, ADAM, PACK, STATS, HAND>), grid, dim3(kThreads),
-                       kCmUpdateLds, s, t.mats, t.off, t.nmats, one, c, mode, first, zs, scale);
+    hipLaunchKernelGGL((cm_update_kernel<false, ADAM, PACK, STATS, HAND, PEND>), grid,
+                       dim3(kThreads), kCmUpdateLds, s, t.mats, t.off, t.nmats, one, c, mode,
+                       first, zs, scale, pd);
 }
 
 hipError_t launch_cm_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
                             int32_t mode, int32_t first, bool adam, bool pack, double* zs,
-                            bool handover, float scale, hipStream_t s) {
+                            bool handover, float scale, hipStream_t s, const Pending* pend) {
   (void)hipGetLastError();
   if (blocks <= 0) return hipSuccess;
   const dim3 grid(static_cast<uint32_t>(blocks));
   if ((zs != nullptr || handover) && !(adam && pack)) return hipErrorInvalidValue;
   if (zs != nullptr && handover) return hipErrorInvalidValue;
-  if (zs != nullptr) {
+  if (pend != nullptr) {
+    if (!(adam && pack) || zs != nullptr || handover || mode != kRemap) return hipErrorInvalidValue;
+    launch_cm_update_t<true, true, false, false, true>(t, one, grid, c, mode, first, nullptr, 1.0f,
+                                                       s, *pend);
+  } else if (zs != nullptr) {
     launch_cm_update_t<true, true, true, false>(t, one, grid, c, mode, first, zs, 1.0f, s);
   } else if (handover) {
     launch_cm_update_t<true, true, false, true>(t, one, grid, c, mode, first, nullptr, scale, s);

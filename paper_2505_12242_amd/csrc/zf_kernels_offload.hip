@@ -4,6 +4,8 @@
 // selected columns are not touched (the selective optimizer owns them).
 // The source may be device memory or pinned host memory that the kernel
 // reads in place.  Column -> slot comes from the selection mask and prefix.
+// SKIP: columns set in prev_mask (the selection that replaced the one the
+// weights were computed under) are left as they are.
 #include "zf_device.hpp"
 
 namespace zf {
@@ -11,7 +13,7 @@ namespace {
 
 // Channel-major: block = one channel x kCmUnpackChunk of its rows (the
 // hand-over's geometry); a selected channel's block exits at once.
-template <bool BATCHED>
+template <bool BATCHED, bool SKIP>
 __global__ __launch_bounds__(kThreads) void cm_scatter_kernel(const DevMat* __restrict__ mats,
                                                              const int64_t* __restrict__ off,
                                                              int32_t nmats, DevMat one) {
@@ -23,6 +25,7 @@ __global__ __launch_bounds__(kThreads) void cm_scatter_kernel(const DevMat* __re
   const int64_t w = j >> 6;
   const uint64_t mw = uniform_u64(d.mask[w]);
   if ((mw >> (j & 63)) & 1ull) return;
+  if (SKIP && ((uniform_u64(d.prev_mask[w]) >> (j & 63)) & 1ull)) return;
   const int64_t u = j - (static_cast<int64_t>(uniform_i32(d.prefix[w])) +
                          __popcll(mw & ((uint64_t(1) << (j & 63)) - 1)));
   const uint16_t* __restrict__ src = d.wcols + u * d.ld_wcols + e0;
@@ -37,7 +40,7 @@ __global__ __launch_bounds__(kThreads) void cm_scatter_kernel(const DevMat* __re
 }
 
 // Row-major: block = 256 columns (one per thread) x up_rows rows.
-template <bool BATCHED>
+template <bool BATCHED, bool SKIP>
 __global__ __launch_bounds__(kThreads) void scatter_kernel(const DevMat* __restrict__ mats,
                                                           const int64_t* __restrict__ off,
                                                           int32_t nmats, DevMat one) {
@@ -50,6 +53,7 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(const DevMat* __restr
   const int64_t w = j >> 6;
   const uint64_t mw = d.mask[w];
   if ((mw >> (j & 63)) & 1ull) return;
+  if (SKIP && ((d.prev_mask[w] >> (j & 63)) & 1ull)) return;
   const int64_t u = j - (static_cast<int64_t>(d.prefix[w]) +
                          __popcll(mw & ((uint64_t(1) << (j & 63)) - 1)));
   const int64_t i0 = rblk * d.up_rows;
@@ -59,26 +63,33 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(const DevMat* __restr
 
 }  // namespace
 
+template <bool SKIP>
+static void launch_scatter_t(const Table& t, const DevMat& one, dim3 grid, int32_t layout,
+                             hipStream_t s) {
+  if (layout == kChannelMajor) {
+    if (t.mats != nullptr)
+      hipLaunchKernelGGL((cm_scatter_kernel<true, SKIP>), grid, dim3(kThreads), 0, s, t.mats,
+                         t.off, t.nmats, one);
+    else
+      hipLaunchKernelGGL((cm_scatter_kernel<false, SKIP>), grid, dim3(kThreads), 0, s, t.mats,
+                         t.off, t.nmats, one);
+  } else {
+    if (t.mats != nullptr)
+      hipLaunchKernelGGL((scatter_kernel<true, SKIP>), grid, dim3(kThreads), 0, s, t.mats, t.off,
+                         t.nmats, one);
+    else
+      hipLaunchKernelGGL((scatter_kernel<false, SKIP>), grid, dim3(kThreads), 0, s, t.mats,
+                         t.off, t.nmats, one);
+  }
+}
+
 hipError_t launch_scatter(const Table& t, const DevMat& one, int64_t blocks, int32_t layout,
-                          hipStream_t s) {
+                          hipStream_t s, bool skip_prev) {
   (void)hipGetLastError();
   if (blocks <= 0) return hipSuccess;
   const dim3 grid(static_cast<uint32_t>(blocks));
-  if (layout == kChannelMajor) {
-    if (t.mats != nullptr)
-      hipLaunchKernelGGL((cm_scatter_kernel<true>), grid, dim3(kThreads), 0, s, t.mats, t.off,
-                         t.nmats, one);
-    else
-      hipLaunchKernelGGL((cm_scatter_kernel<false>), grid, dim3(kThreads), 0, s, t.mats, t.off,
-                         t.nmats, one);
-  } else {
-    if (t.mats != nullptr)
-      hipLaunchKernelGGL((scatter_kernel<true>), grid, dim3(kThreads), 0, s, t.mats, t.off,
-                         t.nmats, one);
-    else
-      hipLaunchKernelGGL((scatter_kernel<false>), grid, dim3(kThreads), 0, s, t.mats, t.off,
-                         t.nmats, one);
-  }
+  if (skip_prev) launch_scatter_t<true>(t, one, grid, layout, s);
+  else launch_scatter_t<false>(t, one, grid, layout, s);
   return hipGetLastError();
 }
 

@@ -39,10 +39,18 @@ host threads, its own step counter) applies the interval's mean gradient to
 the unselected columns of the store and produces their bf16 weights, which
 zf_plan_scatter_weights writes into W.  With overlap=True the device
 buffer is double-buffered, the copy and the host update run while the GPU
-continues with the next interval, and the weights are written back at the
-first step boundary after the host finishes -- and at the latest before the
-next refresh, which is the only step that reads the store, so the results
-equal the synchronous order bit for bit.
+continues with the next interval, and the weights travel back to a device
+staging buffer on the copy stream at the first step boundary after the host
+finishes; the write-back kernel reads them there at the next boundary.
+A refresh is the only step that reads the store.  Right after an interval
+end (refresh_pending=True) it does not wait for the host: the interval's
+host update starts once the refresh has read the store, and each column
+entering the selection takes its owed step on the device first
+(zf_plan_update_pending, from the still resident packed sums); the
+write-back then leaves the refreshed selection's columns alone
+(zf_plan_scatter_weights_skip_prev).  Otherwise a refresh waits for a
+running host update.  Either way the results equal the synchronous order
+bit for bit.
 """
 
 from __future__ import annotations
@@ -112,7 +120,7 @@ class SelectiveUpdateRunner:
                  device=None, keep_unpacked: bool = True, layout: int = ROW_MAJOR,
                  zen_tau: Optional[float] = None, offload: bool = False, overlap: bool = True,
                  host_threads: Optional[int] = None, fuse_handover: bool = True,
-                 warmup: int = 0):
+                 warmup: int = 0, refresh_pending: bool = True):
         self.device = torch.device(device) if device is not None else torch.device("cuda")
         self.shapes = [(int(n), int(m)) for n, m in shapes]
         self.ratio, self.hp, self.R, self.S = ratio, hp, int(refresh), int(accum)
@@ -121,6 +129,7 @@ class SelectiveUpdateRunner:
         self.layout = layout
         self.offload = bool(offload)
         self.overlap = bool(overlap) and self.offload
+        self.refresh_pending = bool(refresh_pending) and self.overlap and zen_tau is None
         self.keep_unpacked = keep_unpacked and not self.offload
         self.fuse_handover = bool(fuse_handover)
         self.weights = list(weights)
@@ -142,6 +151,7 @@ class SelectiveUpdateRunner:
         self.accs: List[List[torch.Tensor]] = [[] for _ in range(nacc)]
         self.norms, self.unpacked, self.sel_sq, self.acc_sq = [], [], [], []
         self.store, self.host_acc, self.wcols, self.unsel_host = [], [], [], []
+        self.wcols_dev = []  # overlap: device staging of the host-produced weights
         for q, ((n, m), k) in enumerate(zip(self.shapes, self.ks)):
             if self.zen_tau is not None:
                 self.sel_sq.append(torch.empty(k, dtype=f32, device=dev))
@@ -163,7 +173,10 @@ class SelectiveUpdateRunner:
                 self.store.append((sp, _pinned_like(p0.shape, f32).zero_(),
                                    _pinned_like(p0.shape, f32).zero_()))
                 self.host_acc.append(alloc_stored(layout, n, m - k, f32, pin_memory=True))
-                self.wcols.append(_pinned_like(_stored(layout, n, m - k), torch.bfloat16))
+                self.wcols.append(alloc_stored(layout, n, m - k, torch.bfloat16,
+                                               pin_memory=True))
+                if self.overlap:
+                    self.wcols_dev.append(alloc_stored(layout, n, m - k, torch.bfloat16, dev))
                 self.unsel_host.append(_pinned_like((m - k,), torch.int32))
         self.acc = self.accs[0]
         self.grad_slots = [list(s) for s in grad_slots]
@@ -177,11 +190,16 @@ class SelectiveUpdateRunner:
         self.host_threads = host_threads if host_threads is not None else \
             min(16, os.cpu_count() or 1)
         self._job: Optional[concurrent.futures.Future] = None
+        self._job_p = 0         # selection buffer the running host update's interval used
+        self._stg_p: Optional[int] = None  # same, for weights staged but not written back
+        self._pend = None       # host update held back for the pending refresh
+        self._ev_staged: Optional[torch.cuda.Event] = None
         self._ev_scatter: Optional[torch.cuda.Event] = None
         self._acc_free: List[Optional[torch.cuda.Event]] = [None] * nacc
         self._pool = (concurrent.futures.ThreadPoolExecutor(max_workers=1)
                       if self.overlap else None)
         self._copy_stream = torch.cuda.Stream(device=dev) if self.overlap else None
+        self.pending_refreshes = 0  # refreshes that took over an unfinished host update
         self.stall_s = 0.0      # host time spent waiting for the deferred update
         self.host_update_s = 0.0  # host time inside the deferred update
         torch.cuda.synchronize(dev)  # store and host buffers ready before any kernel
@@ -196,13 +214,16 @@ class SelectiveUpdateRunner:
                               init_master=self.init_master[q] if self.init_master else None)
             if self.offload:
                 src.store_master, src.store_exp_avg, src.store_exp_avg_sq = self.store[q]
+            if self.refresh_pending:
+                src.pend_acc = self.accs[1 - a][q]  # the interval before a refresh
             q_bufs.append(MatrixBuffers(
                 grad=self.grad_slots[slot][q], k=k, sel=self.sels[p][q], weight=self.weights[q],
                 master=P, exp_avg=M, exp_avg_sq=V, acc=self.accs[a][q], norms=self.norms[q],
                 unpacked=self.unpacked[q], src=src, layout=self.layout,
                 sel_sq=self.sel_sq[q] if self.sel_sq else None,
                 acc_sq=self.acc_sq[q] if self.acc_sq else None,
-                weight_cols=self.wcols[q] if self.offload else None))
+                weight_cols=(self.wcols_dev[q] if self.overlap else self.wcols[q])
+                if self.offload else None))
         return Plan(q_bufs)
 
     @property
@@ -252,8 +273,22 @@ class SelectiveUpdateRunner:
                 with rec("update_handover"):
                     plan.update_handover(self.hp, t, mode, length, self.S, 1.0 / length, st)
                 return kind
-            with rec("update_first" if length == 1 else "update"):
-                plan.update(self.hp, t, mode, length, self.S, stream=st)
+            if refresh and self._pend is not None:
+                # the host update of the interval that just ended starts once
+                # this refresh has read the store
+                scale_p, th_p, copied, p_old = self._pend
+                self._pend = None
+                with rec("update_first"):
+                    plan.update_pending(self.hp, t, self.S, th_p, scale_p, stream=st)
+                swapped = torch.cuda.Event()
+                swapped.record(st)
+                self._job = self._pool.submit(self._host_update, scale_p, th_p, copied,
+                                              self._ev_staged, swapped)
+                self._job_p = p_old
+                self.pending_refreshes += 1
+            else:
+                with rec("update_first" if length == 1 else "update"):
+                    plan.update(self.hp, t, mode, length, self.S, stream=st)
         else:
             with rec("update_zen_first" if length == 1 else "update_zen"):
                 plan.update_zen(self.hp, t, mode, length, self.S, self.zen_tau,
@@ -277,32 +312,64 @@ class SelectiveUpdateRunner:
     # --------------------------------------------------- offloaded optimizer
 
     def _before_step(self, refresh: bool, length: int, st, rec) -> None:
-        """Writes back a finished deferred update (always before a refresh,
-        which reads the store), and makes a new interval wait until the
-        device buffer it overwrites has been copied out."""
+        """Writes back weights staged at an earlier boundary, stages a
+        finished host update (a refresh first waits for a running one: it
+        reads the store), and makes a new interval wait until the device
+        buffer it overwrites has been copied out."""
+        if self._stg_p is not None:
+            self._write_back(st, rec)
         if self._job is not None and (refresh or self._job.done()):
-            t0 = time.perf_counter()
-            self._job.result()
-            self.stall_s += time.perf_counter() - t0
-            self._job = None
-            self._scatter(st, rec)
+            self._finish_job(st, rec)
+            if refresh and self._stg_p != self.cur:
+                self._write_back(st, rec)  # its selection buffer is about to be refreshed
         if length == 1 and self._acc_free[self.cur_a] is not None:
             st.wait_event(self._acc_free[self.cur_a])
             self._acc_free[self.cur_a] = None
 
-    def _scatter(self, st, rec) -> None:
-        plan = self.plans[0][self.cur][self.cur_a]
+    def _finish_job(self, st, rec) -> None:
+        """Waits for the running host update and stages its weights: with
+        overlap, a copy to the device staging buffer on the copy stream."""
+        t0 = time.perf_counter()
+        self._job.result()
+        self.stall_s += time.perf_counter() - t0
+        self._job = None
+        if self._stg_p is not None:
+            self._write_back(st, rec)
+        if self.overlap:
+            cs = self._copy_stream
+            if self._ev_scatter is not None:
+                cs.wait_event(self._ev_scatter)  # the last write-back has read the staging buffer
+            with torch.cuda.stream(cs):
+                for q in range(len(self.shapes)):
+                    padded_block(self.wcols_dev[q]).copy_(padded_block(self.wcols[q]),
+                                                          non_blocking=True)
+            ev = torch.cuda.Event()
+            ev.record(cs)
+            self._ev_staged = ev
+        self._stg_p = self._job_p
+
+    def _write_back(self, st, rec) -> None:
+        """W[:, unsel] = the staged weights, under the selection their
+        interval used; after a refresh the refreshed selection's columns are
+        left alone (they belong to the selective optimizer)."""
+        p = self._stg_p
+        if self.overlap:
+            st.wait_event(self._ev_staged)
+        plan = self.plans[0][p][0]
         with rec("scatter_weights"):
-            plan.scatter_weights(st)
+            if p == self.cur:
+                plan.scatter_weights(st)
+            else:
+                plan.scatter_weights_skip_prev(st)
         ev = torch.cuda.Event()
         ev.record(st)
         self._ev_scatter = ev
+        self._stg_p = None
 
-    def _host_update(self, scale: float, th: int, wait_copy, wait_scatter) -> None:
-        if wait_copy is not None:
-            wait_copy.synchronize()
-        if wait_scatter is not None:
-            wait_scatter.synchronize()  # the previous write-back has read wcols
+    def _host_update(self, scale: float, th: int, *waits) -> None:
+        for ev in waits:
+            if ev is not None:
+                ev.synchronize()  # packed sums copied, staging done, store read
         t0 = time.perf_counter()
         for q, ((n, m), k) in enumerate(zip(self.shapes, self.ks)):
             P, M, V = self.store[q]
@@ -314,12 +381,6 @@ class SelectiveUpdateRunner:
     def _hand_over(self, length: int, st, rec) -> None:
         self.th += 1
         scale = float(np.float32(1.0 / length))
-        if self._job is not None:  # the host is still busy with the previous interval
-            t0 = time.perf_counter()
-            self._job.result()
-            self.stall_s += time.perf_counter() - t0
-            self._job = None
-            self._scatter(st, rec)
         a = self.cur_a
         sels = self.sels[self.cur]
         if not self.overlap:
@@ -329,9 +390,12 @@ class SelectiveUpdateRunner:
                                                          non_blocking=True)
                     self.unsel_host[q].copy_(sels[q].unsel_idx, non_blocking=True)
             st.synchronize()
-            self._host_update(scale, self.th, None, None)
-            self._scatter(st, rec)
+            self._host_update(scale, self.th)
+            self._stg_p = self.cur
+            self._write_back(st, rec)
             return
+        if self._job is not None:  # the host is still busy with the previous interval
+            self._finish_job(st, rec)
         ev = torch.cuda.Event()
         ev.record(st)
         cs = self._copy_stream
@@ -344,25 +408,36 @@ class SelectiveUpdateRunner:
         copied = torch.cuda.Event()
         copied.record(cs)
         self._acc_free[a] = copied
-        self._job = self._pool.submit(self._host_update, scale, self.th, copied,
-                                      self._ev_scatter)
+        warm = self.t <= self.warmup
+        if self.refresh_pending and not warm and self.t % self.R == 0:
+            # the next step refreshes: it takes over the columns entering its
+            # selection and then starts this host update (see step)
+            self._pend = (scale, self.th, copied, self.cur)
+        else:
+            self._job = self._pool.submit(self._host_update, scale, self.th, copied,
+                                          self._ev_staged)
+            self._job_p = self.cur
         self.cur_a = 1 - a
-        if self.t <= self.warmup:
+        if warm:
             # warm-up: synchronous, the update lands before the next step
-            t0 = time.perf_counter()
-            self._job.result()
-            self.stall_s += time.perf_counter() - t0
-            self._job = None
-            self._scatter(st, rec)
+            self._finish_job(st, rec)
+            self._write_back(st, rec)
 
     def sync(self, stream=None) -> None:
         """Finishes every outstanding deferred update and write-back and
         synchronises the device (the state the synchronous order reaches)."""
         st = stream if stream is not None else torch.cuda.current_stream(self.device)
+        if self._pend is not None:
+            # no refresh took the held-back update over: run it as usual
+            scale_p, th_p, copied, p = self._pend
+            self._pend = None
+            self._job = self._pool.submit(self._host_update, scale_p, th_p, copied,
+                                          self._ev_staged)
+            self._job_p = p
         if self._job is not None:
-            self._job.result()
-            self._job = None
-            self._scatter(st, _no_record)
+            self._finish_job(st, _no_record)
+        if self._stg_p is not None:
+            self._write_back(st, _no_record)
         torch.cuda.synchronize(self.device)
 
     @property
@@ -375,6 +450,7 @@ class SelectiveUpdateRunner:
         if self._job is not None:
             self._job.result()
             self._job = None
+        self._pend = None
         if self._pool is not None:
             self._pool.shutdown(wait=True)
         for row in self.plans:
