@@ -373,26 +373,19 @@ __device__ __forceinline__ void load_state(const AdamSrc& a, int32_t i, float& p
     v = buf_f32(a.rV, a.vS, i * a.sS);
   } else if constexpr (SRC == kSrcRemapStore || SRC == kSrcInitStore ||
                        SRC == kSrcRemapStorePend) {
-    float pt = buf_f32(a.rTP, a.vT, i * a.sT);
-    float mt = buf_f32(a.rTM, a.vT, i * a.sT);
-    float vt = buf_f32(a.rTV, a.vT, i * a.sT);
-    if constexpr (SRC == kSrcRemapStorePend) {
-      // every lane takes the deferred step; a lane whose column was selected
-      // before reads slot 0 (any valid slot) and keeps its previous states
-      adam_step(buf_f32(a.rPA, a.vPA, i * a.sPA) * pd->scale, pt, mt, vt, pd->c);
-    }
-    if constexpr (SRC == kSrcRemapStore || SRC == kSrcRemapStorePend) {
-      // both sources are read; the lane keeps the one that applies
-      const float pp = buf_f32(a.rSP, a.vPrev, i * a.sPrev);
-      const float mp = buf_f32(a.rSM, a.vPrev, i * a.sPrev);
-      const float vp = buf_f32(a.rSV, a.vPrev, i * a.sPrev);
-      p = a.was ? pp : pt;
-      m = a.was ? mp : mt;
-      v = a.was ? vp : vt;
+    // Only the lanes of entering columns read the store (it may be pinned
+    // host memory, where every lane's 4-byte read is its own PCIe request);
+    // the others read their previous compact states.
+    if (SRC != kSrcInitStore && a.was) {
+      p = buf_f32(a.rSP, a.vPrev, i * a.sPrev);
+      m = buf_f32(a.rSM, a.vPrev, i * a.sPrev);
+      v = buf_f32(a.rSV, a.vPrev, i * a.sPrev);
     } else {
-      p = pt;
-      m = mt;
-      v = vt;
+      p = buf_f32(a.rTP, a.vT, i * a.sT);
+      m = buf_f32(a.rTM, a.vT, i * a.sT);
+      v = buf_f32(a.rTV, a.vT, i * a.sT);
+      if constexpr (SRC == kSrcRemapStorePend)  // the owed deferred step first
+        adam_step(buf_f32(a.rPA, a.vPA, i * a.sPA) * pd->scale, p, m, v, pd->c);
     }
   } else {
     // init value of p for a newly selected column
