@@ -436,7 +436,7 @@ zf_status zf_plan_scatter_weights(zf_plan* plan, zf_stream stream);
  * (zf_plan_scatter_weights_skip_prev).  Every descriptor needs the store,
  * the previous selection and states, the packed buffer and pend_acc, which
  * must not overlap any buffer the call writes.  pend_step >= 1; pend_scale
- * finite.  Not for Zen-auto (zf_plan_update_zen). */
+ * finite.  Zen-auto: zf_plan_update_zen_pending. */
 zf_status zf_plan_update_pending(zf_plan* plan, const zf_adam_hparams* hp, int64_t step,
                                  int64_t accum_interval, int64_t pend_step, float pend_scale,
                                  zf_stream stream);
@@ -500,6 +500,16 @@ typedef struct zf_zen_totals {
 zf_status zf_plan_update_zen(zf_plan* plan, const zf_adam_hparams* hp, int64_t step,
                              int32_t mode, int64_t step_in_interval, int64_t accum_interval,
                              double tau, zf_zen_totals* totals, zf_stream stream);
+
+/* zf_plan_update_zen for the refresh step of the offloaded optimizer while
+ * the host is still applying the deferred update of the interval that
+ * ended at the previous step: mode ZF_STATES_REMAP and step_in_interval 1,
+ * with the entering columns' owed deferred step taken over exactly as in
+ * zf_plan_update_pending (same requirements); the statistics and totals
+ * are those of zf_plan_update_zen. */
+zf_status zf_plan_update_zen_pending(zf_plan* plan, const zf_adam_hparams* hp, int64_t step,
+                                     int64_t accum_interval, int64_t pend_step, float pend_scale,
+                                     double tau, zf_zen_totals* totals, zf_stream stream);
 
 #ifdef __cplusplus
 }

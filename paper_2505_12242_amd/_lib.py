@@ -113,6 +113,8 @@ SIGNATURES = [
     ("zf_plan_update_pending", ctypes.c_int,
      [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, c_i64, c_i64, c_flt, c_vp]),
     ("zf_plan_scatter_weights_skip_prev", ctypes.c_int, [c_vp, c_vp]),
+    ("zf_plan_update_zen_pending", ctypes.c_int,
+     [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, c_i64, c_i64, c_flt, c_dbl, c_vp, c_vp]),
 ]
 
 
@@ -642,6 +644,20 @@ class Plan:
         c_hp = hp.as_c()
         _check("zf_plan_update_zen", LIB.zf_plan_update_zen(
             self._h, ctypes.byref(c_hp), step, mode, step_in_interval, accum_interval,
+            float(tau), totals.data_ptr(), _stream(stream)))
+
+    def update_zen_pending(self, hp: AdamHparams, step: int, accum_interval: int,
+                           pend_step: int, pend_scale: float, tau: float,
+                           totals: torch.Tensor, stream=None) -> None:
+        """update_zen for the refresh step that takes over the owed deferred
+        update (zf_plan_update_zen_pending; see update_pending)."""
+        if (totals.device.type != "cuda" or not totals.is_contiguous()
+                or totals.numel() * totals.element_size() < ZEN_TOTALS_BYTES):
+            raise ValueError(f"totals: expected a contiguous GPU tensor of at least "
+                             f"{ZEN_TOTALS_BYTES} bytes")
+        c_hp = hp.as_c()
+        _check("zf_plan_update_zen_pending", LIB.zf_plan_update_zen_pending(
+            self._h, ctypes.byref(c_hp), step, accum_interval, pend_step, float(pend_scale),
             float(tau), totals.data_ptr(), _stream(stream)))
 
     def close(self) -> None:

@@ -1114,37 +1114,35 @@ zf_status zf_plan_scatter_weights_skip_prev(zf_plan* p, zf_stream stream) {
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
-zf_status zf_plan_update_zen(zf_plan* p, const zf_adam_hparams* hp, int64_t step, int32_t mode,
-                             int64_t step_in_interval, int64_t accum_interval, double tau,
-                             zf_zen_totals* totals, zf_stream stream) {
-  if (p == nullptr || !p->can_zen || !p->can_adam || !p->can_pack) return ZF_EINVAL;
-  if (!hparams_ok(hp) || step < 1) return ZF_EINVAL;
-  if (mode != zf::kInplace && mode != zf::kRemap && mode != zf::kInit) return ZF_EINVAL;
-  if (mode == zf::kRemap && !p->can_remap) return ZF_EINVAL;
-  if (accum_interval < 1 || step_in_interval < 1 || step_in_interval > accum_interval)
-    return ZF_EINVAL;
-  if (!(tau >= 0.0) || totals == nullptr || !aligned(totals, 8)) return ZF_EINVAL;
-  static_assert(sizeof(zf_zen_totals) == sizeof(zf::ZenTotals), "zen totals layout");
-  const AdamK c = adam_consts(*hp, step);
-  const hipStream_t s = as_stream(stream);
+}  // extern "C"
+
+namespace {
+
+// Zen-auto step over a plan; pd != nullptr: the refresh with the owed
+// deferred update (kRemap, first step of an interval).
+zf_status plan_update_zen(zf_plan* p, const AdamK& c, int32_t mode, int32_t first, double tau,
+                          zf_zen_totals* totals, hipStream_t s, const zf::Pending* pd) {
   const Table t{p->d_mats, p->d_off_up, p->nmats};
   const Table tz{p->d_mats, p->d_off_zen, p->nmats};
   hipError_t e;
   if (p->layout == zf::kChannelMajor) {
-    e = zf::launch_cm_update(t, p->mats[0], p->blk_up, c, mode, step_in_interval == 1 ? 1 : 0,
-                             true, true, p->d_zs, false, 1.0f, s);
+    e = zf::launch_cm_update(t, p->mats[0], p->blk_up, c, mode, first, true, true, p->d_zs, false,
+                             1.0f, s, pd);
     if (e != hipSuccess) return hip_fail(e);
     e = zf::launch_zen_finalize(tz, p->mats[0], p->blk_zen, p->d_zs, p->d_zb, s);
-  } else if (use_rv(p->mats[0], mode, true)) {
+  } else if (pd == nullptr && use_rv(p->mats[0], mode, true)) {
     // 16-byte update with the statistics fused: only the finalize remains
     const Table tv{p->d_mats, p->d_off_upv, p->nmats};
-    e = zf::launch_rv_update(tv, p->mats[0], p->blk_upv, c, mode, step_in_interval == 1 ? 1 : 0,
-                             true, true, false, 1.0f, s, p->d_ws);
+    e = zf::launch_rv_update(tv, p->mats[0], p->blk_upv, c, mode, first, true, true, false, 1.0f,
+                             s, p->d_ws);
     if (e != hipSuccess) return hip_fail(e);
     const Table tp{p->d_mats, p->d_off_zp, p->nmats};
     e = zf::launch_rm_zen(tp, 0, tz, p->blk_zen, p->mats[0], p->d_ws, p->d_zb, s);
   } else {
-    e = plan_update_launch(p, c, mode, step_in_interval == 1 ? 1 : 0, true, true, false, 1.0f, s);
+    e = pd != nullptr
+            ? zf::launch_update(t, p->mats[0], p->blk_up, c, mode, first, true, true, false, 1.0f,
+                                s, pd)
+            : plan_update_launch(p, c, mode, first, true, true, false, 1.0f, s);
     if (e != hipSuccess) return hip_fail(e);
     const Table tp{p->d_mats, p->d_off_zp, p->nmats};
     e = zf::launch_rm_zen(tp, p->blk_zp, tz, p->blk_zen, p->mats[0], p->d_ws, p->d_zb, s);
@@ -1153,6 +1151,40 @@ zf_status zf_plan_update_zen(zf_plan* p, const zf_adam_hparams* hp, int64_t step
   e = zf::launch_zen_total(p->d_zb, p->blk_zen, p->k_total, p->u_total, tau,
                            reinterpret_cast<zf::ZenTotals*>(totals), s);
   return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
+bool zen_args_ok(const zf_plan* p, const zf_adam_hparams* hp, int64_t step, double tau,
+                 const zf_zen_totals* totals) {
+  static_assert(sizeof(zf_zen_totals) == sizeof(zf::ZenTotals), "zen totals layout");
+  return p != nullptr && p->can_zen && p->can_adam && p->can_pack && hparams_ok(hp) &&
+         step >= 1 && tau >= 0.0 && totals != nullptr && aligned(totals, 8);
+}
+
+}  // namespace
+
+extern "C" {
+
+zf_status zf_plan_update_zen(zf_plan* p, const zf_adam_hparams* hp, int64_t step, int32_t mode,
+                             int64_t step_in_interval, int64_t accum_interval, double tau,
+                             zf_zen_totals* totals, zf_stream stream) {
+  if (!zen_args_ok(p, hp, step, tau, totals)) return ZF_EINVAL;
+  if (mode != zf::kInplace && mode != zf::kRemap && mode != zf::kInit) return ZF_EINVAL;
+  if (mode == zf::kRemap && !p->can_remap) return ZF_EINVAL;
+  if (accum_interval < 1 || step_in_interval < 1 || step_in_interval > accum_interval)
+    return ZF_EINVAL;
+  return plan_update_zen(p, adam_consts(*hp, step), mode, step_in_interval == 1 ? 1 : 0, tau,
+                         totals, as_stream(stream), nullptr);
+}
+
+zf_status zf_plan_update_zen_pending(zf_plan* p, const zf_adam_hparams* hp, int64_t step,
+                                     int64_t accum_interval, int64_t pend_step, float pend_scale,
+                                     double tau, zf_zen_totals* totals, zf_stream stream) {
+  if (!zen_args_ok(p, hp, step, tau, totals) || !p->can_remap || !p->can_pending)
+    return ZF_EINVAL;
+  if (pend_step < 1 || !std::isfinite(pend_scale) || accum_interval < 1) return ZF_EINVAL;
+  const zf::Pending pd{adam_consts(*hp, pend_step), pend_scale};
+  return plan_update_zen(p, adam_consts(*hp, step), zf::kRemap, 1, tau, totals,
+                         as_stream(stream), &pd);
 }
 
 }  // extern "C"

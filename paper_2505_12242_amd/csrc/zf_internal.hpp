@@ -161,7 +161,7 @@ hipError_t launch_cm_colnorm(const Table& t, const DevMat& one, int64_t blocks, 
 // handover: the last step of an interval with the hand-over fused in (the
 // `out` buffer receives scale * the final sums, +0.0 for selected columns;
 // the packed buffer is not written).
-// pend: as in launch_update.
+// pend: as in launch_update (also with zs).
 hipError_t launch_cm_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
                             int32_t mode, int32_t first, bool adam, bool pack, double* zs,
                             bool handover, float scale, hipStream_t s,

@@ -368,7 +368,8 @@ __device__ __forceinline__ void cm_swap_out(const DevMat& d, int64_t j, int64_t 
 // unselected channel, +0.0 for a selected one -- and the packed buffer is
 // left as it was (it is overwritten when the next interval starts).
 //
-// PEND (fused Adam + pack in kRemap against the store only): a channel that
+// PEND (fused Adam + pack in kRemap against the store, with or without
+// STATS): a channel that
 // enters the selection takes the owed deferred step pd first (its row of
 // pend_acc is its slot among the previous selection's unselected channels:
 // j minus the previously selected channels below j).
@@ -578,9 +579,13 @@ hipError_t launch_cm_update(const Table& t, const DevMat& one, int64_t blocks, c
   if ((zs != nullptr || handover) && !(adam && pack)) return hipErrorInvalidValue;
   if (zs != nullptr && handover) return hipErrorInvalidValue;
   if (pend != nullptr) {
-    if (!(adam && pack) || zs != nullptr || handover || mode != kRemap) return hipErrorInvalidValue;
-    launch_cm_update_t<true, true, false, false, true>(t, one, grid, c, mode, first, nullptr, 1.0f,
-                                                       s, *pend);
+    if (!(adam && pack) || handover || mode != kRemap) return hipErrorInvalidValue;
+    if (zs != nullptr)
+      launch_cm_update_t<true, true, true, false, true>(t, one, grid, c, mode, first, zs, 1.0f, s,
+                                                        *pend);
+    else
+      launch_cm_update_t<true, true, false, false, true>(t, one, grid, c, mode, first, nullptr,
+                                                         1.0f, s, *pend);
   } else if (zs != nullptr) {
     launch_cm_update_t<true, true, true, false>(t, one, grid, c, mode, first, zs, 1.0f, s);
   } else if (handover) {

@@ -129,7 +129,7 @@ class SelectiveUpdateRunner:
         self.layout = layout
         self.offload = bool(offload)
         self.overlap = bool(overlap) and self.offload
-        self.refresh_pending = bool(refresh_pending) and self.overlap and zen_tau is None
+        self.refresh_pending = bool(refresh_pending) and self.overlap
         self.keep_unpacked = keep_unpacked and not self.offload
         self.fuse_handover = bool(fuse_handover)
         self.weights = list(weights)
@@ -274,25 +274,24 @@ class SelectiveUpdateRunner:
                     plan.update_handover(self.hp, t, mode, length, self.S, 1.0 / length, st)
                 return kind
             if refresh and self._pend is not None:
-                # the host update of the interval that just ended starts once
-                # this refresh has read the store
-                scale_p, th_p, copied, p_old = self._pend
-                self._pend = None
+                scale_p, th_p = self._pend[:2]
                 with rec("update_first"):
                     plan.update_pending(self.hp, t, self.S, th_p, scale_p, stream=st)
-                swapped = torch.cuda.Event()
-                swapped.record(st)
-                self._job = self._pool.submit(self._host_update, scale_p, th_p, copied,
-                                              self._ev_staged, swapped)
-                self._job_p = p_old
-                self.pending_refreshes += 1
+                self._start_held_update(st)
             else:
                 with rec("update_first" if length == 1 else "update"):
                     plan.update(self.hp, t, mode, length, self.S, stream=st)
         else:
-            with rec("update_zen_first" if length == 1 else "update_zen"):
-                plan.update_zen(self.hp, t, mode, length, self.S, self.zen_tau,
-                                self.zen_totals, stream=st)
+            if refresh and self._pend is not None:
+                scale_p, th_p = self._pend[:2]
+                with rec("update_zen_first"):
+                    plan.update_zen_pending(self.hp, t, self.S, th_p, scale_p, self.zen_tau,
+                                            self.zen_totals, stream=st)
+                self._start_held_update(st)
+            else:
+                with rec("update_zen_first" if length == 1 else "update_zen"):
+                    plan.update_zen(self.hp, t, mode, length, self.S, self.zen_tau,
+                                    self.zen_totals, stream=st)
             with torch.cuda.stream(st):
                 self._zen_host.copy_(self.zen_totals, non_blocking=True)
             st.synchronize()
@@ -310,6 +309,19 @@ class SelectiveUpdateRunner:
         return kind
 
     # --------------------------------------------------- offloaded optimizer
+
+    def _start_held_update(self, st) -> None:
+        """After a refresh that took over the entering columns' owed step:
+        the held-back host update of the interval that just ended starts
+        once the refresh has read the store."""
+        scale_p, th_p, copied, p_old = self._pend
+        self._pend = None
+        swapped = torch.cuda.Event()
+        swapped.record(st)
+        self._job = self._pool.submit(self._host_update, scale_p, th_p, copied,
+                                      self._ev_staged, swapped)
+        self._job_p = p_old
+        self.pending_refreshes += 1
 
     def _before_step(self, refresh: bool, length: int, st, rec) -> None:
         """Writes back weights staged at an earlier boundary, stages a

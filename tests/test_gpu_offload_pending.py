@@ -151,19 +151,20 @@ def test_scatter_weights_skip_prev(n, m, layout):
 
 @pytest.mark.timeout(600)
 @pytest.mark.parametrize("pending", [True, False])
-@pytest.mark.parametrize("R,S", [(2, 2), (4, 2), (1, 1), (4, 4)])
+@pytest.mark.parametrize("R,S,W", [(2, 2, 0), (4, 2, 0), (1, 1, 0), (4, 4, 0), (4, 2, 3)])
 @pytest.mark.parametrize("layout", LAYOUTS)
-def test_pipelined_refreshes_match_oracle(layout, R, S, pending):
+def test_pipelined_refreshes_match_oracle(layout, R, S, W, pending):
+    """W > 0: the first W steps are synchronous (their refreshes wait)."""
     T_ = 13
     dev = torch.device("cuda")
     slots, host, weights, w0 = _inputs(SET, T_, 23, layout, dev)
     runner = zf.SelectiveUpdateRunner(SET, 0.1, HP, R, S, slots, weights, device=dev,
                                       layout=layout, offload=True, overlap=True,
-                                      host_threads=4, refresh_pending=pending)
+                                      host_threads=4, refresh_pending=pending, warmup=W)
     orcs = [O.OffloadOracle(O.widen(w0[q]), w0[q], 0.1, HP.lr, HP.beta1, HP.beta2, HP.eps,
-                            HP.weight_decay, R, S) for q in range(len(SET))]
+                            HP.weight_decay, R, S, warmup=W) for q in range(len(SET))]
     for t in range(1, T_ + 1):
-        print(f"# pipelined layout={layout} R={R} S={S} pending={pending} step {t}",
+        print(f"# pipelined layout={layout} R={R} S={S} W={W} pending={pending} step {t}",
               file=sys.stderr, flush=True)
         runner.step()
         for q, o in enumerate(orcs):
@@ -179,4 +180,114 @@ def test_pipelined_refreshes_match_oracle(layout, R, S, pending):
                 assert np.array_equal(logical(bits_np(runner.weights[q]), layout), o.W), (q, t)
     assert runner.th == orcs[0].th
     assert (runner.pending_refreshes > 0) == pending
+    runner.close()
+
+
+@pytest.mark.parametrize("n,m", [(33, 300), (4104, 70)])
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_update_zen_pending_equals_zen_refresh_on_the_updated_store(n, m, layout):
+    """zf_plan_update_zen_pending against zf_plan_update_zen (remap) on a
+    store that already holds the deferred update (the oracle's): compact
+    states, W, packed buffer, store, both statistics vectors and the totals
+    bit for bit."""
+    print(f"# zen pending n={n} m={m} layout={layout}", file=sys.stderr, flush=True)
+    rng = np.random.default_rng(derive_seed("zen-pend", n, m))
+    k = O.k_from_ratio(0.25, m)
+    old = O.select_topk(rng.random(m).astype(np.float32), k)
+    new = O.select_topk(rng.random(m).astype(np.float32), k)
+    bits = grad_bits(n, m, derive_seed("zen-pend-g", n, m))
+    W = O.bf16_round((rng.standard_normal((n, m)) * 0.02).astype(np.float32))
+    P, M, V = ((rng.standard_normal((n, k)) * s).astype(np.float32) for s in (0.02, 1e-3, 1e-5))
+    V = np.abs(V)
+    store = _store_arrays(rng, n, m)
+    Apend = (rng.standard_normal((n, m - k)) * 0.05).astype(np.float32)
+    pend_step, pend_scale, step, tau = 2, float(np.float32(0.5)), 7, 1.0
+    store1, _ = O.deferred_adam(Apend, old.unsel, pend_scale, store, consts(pend_step))
+    rm = layout == zf.ROW_MAJOR
+
+    def run(pending):
+        sd = [place(T(x, layout), "pinned") for x in (store if pending else store1)]
+        bufs = dict(master=_nan((n, k) if rm else (k, n)), exp_avg=_nan((n, k) if rm else (k, n)),
+                    exp_avg_sq=_nan((n, k) if rm else (k, n)),
+                    acc=_nan((n, m - k) if rm else (m - k, n)),
+                    sel_sq=torch.full((k,), np.nan, device="cuda"),
+                    acc_sq=torch.full((m - k,), np.nan, device="cuda"))
+        Wd = bf16_dev(T(W, layout))
+        src = zf.StateSource(prev=sel_dev(old), prev_master=f32_dev(T(P, layout)),
+                             prev_exp_avg=f32_dev(T(M, layout)),
+                             prev_exp_avg_sq=f32_dev(T(V, layout)),
+                             store_master=sd[0], store_exp_avg=sd[1], store_exp_avg_sq=sd[2],
+                             pend_acc=f32_dev(T(Apend, layout)) if pending else None)
+        plan = zf.Plan([zf.MatrixBuffers(grad=bf16_dev(T(bits, layout)), k=k, sel=sel_dev(new),
+                                         weight=Wd, src=src, layout=layout, **bufs)])
+        totals = torch.zeros(zf.ZEN_TOTALS_BYTES // 8, dtype=torch.int64, device="cuda")
+        if pending:
+            plan.update_zen_pending(HP, step, 4, pend_step, pend_scale, tau, totals)
+        else:
+            plan.update_zen(HP, step, zf.STATES_REMAP, 1, 4, tau, totals)
+        torch.cuda.synchronize()
+        out = [bufs[x].cpu().numpy() for x in ("master", "exp_avg", "exp_avg_sq", "acc",
+                                                "sel_sq", "acc_sq")]
+        out.append(bits_np(Wd))
+        out.append(totals.cpu().numpy())
+        plan.close()
+        return out, [host_np(x) for x in sd]
+
+    got, got_store = run(True)
+    want, want_store = run(False)
+    for g, w in zip(got, want):
+        assert g.tobytes() == w.tobytes()
+    # the pending run left the entering columns' store columns as they were;
+    # the host update applied afterwards reaches the other run's store
+    after, _ = O.deferred_adam(Apend, old.unsel, pend_scale,
+                               [logical(x, layout) for x in got_store], consts(pend_step))
+    for g, w in zip(after, want_store):
+        assert same_bits(g, logical(w, layout))
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_zen_auto_pipelined_refreshes_match_oracle(layout):
+    """Zen-auto with the offloaded optimizer, refreshes every 4 steps: the
+    forced interval end before each refresh is taken over by the refresh
+    (zf_plan_update_zen_pending); interval ends, totals, and after refresh
+    steps and at the end the compact states, the whole store and W against
+    ZenAutoOracle over OffloadOracles, bit for bit."""
+    import math
+    R, S_max, T_ = 4, 4, 13
+    dev = torch.device("cuda")
+    slots, host, weights, w0 = _inputs(SET, T_, 29, layout, dev)
+
+    def oracles(tau):
+        return O.ZenAutoOracle([O.OffloadOracle(O.widen(w0[q]), w0[q], 0.1, HP.lr, HP.beta1,
+                                                HP.beta2, HP.eps, HP.weight_decay, R, S_max)
+                                for q in range(len(SET))], R, S_max, tau)
+
+    probe = oracles(math.inf)
+    ratios = []
+    for t in range(T_):
+        tot = probe.step(host[t])["totals"]
+        ratios.append((tot.sum_acc / tot.u) / (tot.sum_sel / tot.k))
+    tau = math.sqrt(min(ratios[:2]) * max(ratios[2:S_max]))
+    za = oracles(tau)
+    runner = zf.SelectiveUpdateRunner(SET, 0.1, HP, R, S_max, slots, weights, device=dev,
+                                      layout=layout, zen_tau=tau, offload=True, overlap=True,
+                                      host_threads=4)
+    for t in range(1, T_ + 1):
+        print(f"# zen pipelined layout={layout} step {t}", file=sys.stderr, flush=True)
+        kind = runner.step()
+        ref = za.step(host[t - 1])
+        assert (kind.refresh, kind.step_in_interval, kind.interval_end) == \
+            (ref["refresh"], ref["step_in_interval"], ref["interval_end"]), t
+        assert runner.last_totals.trigger == ref["totals"].trigger
+        if t in (7, T_):
+            runner.sync()
+            for q, o in enumerate(za.orcs):
+                for g_, w_ in zip(runner.state[q], (o.P, o.M, o.V)):
+                    assert same_bits(logical(f32_np(g_), layout), w_), (q, t)
+                for g_, w_ in zip(runner.store[q], o.store):
+                    assert same_bits(logical(g_.numpy(), layout), w_), (q, t)
+                assert np.array_equal(logical(bits_np(runner.weights[q]), layout), o.W), (q, t)
+    assert runner.pending_refreshes > 0
+    assert runner.th == za.orcs[0].th
     runner.close()
