@@ -25,7 +25,7 @@ import oracle as O
 from tests._gpu import bf16_dev, bits_np, f32_dev, f32_np, same_bits
 from tests.test_gpu_offload import (HP, LAYOUTS, SET, T, _inputs, _store_arrays, consts,
                                     grad_bits, host_np, logical, place, sel_dev)
-from workloads import derive_seed
+from workloads import derive_seed, gradient
 
 pytestmark = pytest.mark.gpu
 
@@ -291,3 +291,78 @@ def test_zen_auto_pipelined_refreshes_match_oracle(layout):
     assert runner.pending_refreshes > 0
     assert runner.th == za.orcs[0].th
     runner.close()
+
+
+def _layer_inputs(T_, layout, dev):
+    """One Llama-2-7B decoder layer's gradients for T_ steps (device) and its
+    bf16 weights, in `layout`."""
+    from workloads.configs import get_workload, shapes as wl_shapes
+    shp = wl_shapes(get_workload("llama2-7b-layer").matrices)
+    slots = []
+    for t in range(1, T_ + 1):
+        row = []
+        for q, (n, m) in enumerate(shp):
+            s = torch.exp(1.5 * torch.randn(m, generator=torch.Generator().manual_seed(
+                derive_seed("layer-s", q) & 0x7fffffff), dtype=torch.float64))
+            jit = torch.exp(0.3 * torch.randn(m, generator=torch.Generator().manual_seed(
+                derive_seed("layer-j", q, t) & 0x7fffffff), dtype=torch.float64))
+            g = gradient(n, m, s * jit, derive_seed("layer-g", q, t), device=dev)
+            row.append(g if layout == zf.ROW_MAJOR else g.t().contiguous())
+        slots.append(row)
+    w = []
+    for q, (n, m) in enumerate(shp):
+        x = (0.02 * torch.randn(n, m, generator=torch.Generator().manual_seed(q))).to(torch.bfloat16)
+        w.append((x if layout == zf.ROW_MAJOR else x.t().contiguous()).to(dev))
+    return shp, slots, w
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("busy", [False, True])
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_layer_size_pipeline_equals_synchronous(layout, busy):
+    """A whole 7B decoder layer (202 M parameters): the overlapped runner with
+    pipelined refreshes against the synchronous runner over the same 10
+    steps (R = 4, S = 2: refreshes at steps 1, 5 and 9, the last two taking
+    over the interval that ends right before them), every buffer compared
+    bit for bit at the end.  At this size the host update
+    (~30 ms) outlasts several device steps: with busy=False the hand-overs
+    wait for it; with busy=True a stand-in compute of ~8 ms per step on the
+    same stream lets it finish between steps, so the staged write-backs land
+    at later boundaries."""
+    T_, R, S = 10, 4, 2
+    dev = torch.device("cuda")
+    shp, slots, w = _layer_inputs(T_, layout, dev)
+    a = torch.randn(4096, 4096, device=dev, dtype=torch.bfloat16)
+    b = torch.randn(4096, 4096, device=dev, dtype=torch.bfloat16)
+    c = torch.empty_like(a)
+    runs = []
+    for overlap in (True, False):
+        weights = [x.clone() for x in w]
+        runner = zf.SelectiveUpdateRunner(shp, 0.1, HP, R, S, slots, weights, device=dev,
+                                          layout=layout, offload=True, overlap=overlap,
+                                          host_threads=8)
+        for t in range(1, T_ + 1):
+            print(f"# layer pipeline layout={layout} busy={busy} overlap={overlap} step {t}",
+                  file=sys.stderr, flush=True)
+            if busy and overlap:
+                for _ in range(60):
+                    torch.mm(a, b, out=c)
+            runner.step()
+        runner.sync()
+        if overlap:
+            assert runner.pending_refreshes == 2  # steps 5 and 9
+        out = []
+        for q in range(len(shp)):
+            out.append(runner.selection[q].sel_idx.cpu().numpy())
+            out.extend(x.cpu().numpy() for x in runner.state[q])
+            out.extend(x.numpy().copy() for x in runner.store[q])
+            out.append(bits_np(runner.weights[q]))
+        runs.append(out)
+        runner.close()
+        del runner, weights
+        torch.cuda.synchronize()
+    assert len(runs[0]) == len(runs[1])
+    for i, (g, want) in enumerate(zip(*runs)):
+        assert g.shape == want.shape and g.dtype == want.dtype, i
+        assert np.array_equal(np.ascontiguousarray(g).view(np.uint8),
+                              np.ascontiguousarray(want).view(np.uint8)), i
