@@ -452,6 +452,61 @@ class SelectiveUpdateRunner:
             self._write_back(st, _no_record)
         torch.cuda.synchronize(self.device)
 
+    # ---------------------------------------------------- checkpoint / resume
+
+    def state_dict(self) -> dict:
+        """What a later run needs to continue bit for bit: the step
+        counters, the current selection and compact states, the current
+        interval's packed sums and, with the offloaded optimizer, the store
+        and its step counter.  Drains the pipeline first (sync).  Tensors are
+        CPU copies in the runner's layout; the weights stay the caller's."""
+        self.sync()
+        c, a = self.cur, self.cur_a
+        mats = []
+        for q in range(len(self.shapes)):
+            s = self.sels[c][q]
+            d = {"sel_idx": s.sel_idx.cpu(), "unsel_idx": s.unsel_idx.cpu(),
+                 "mask": s.mask.cpu(), "prefix": s.prefix.cpu(),
+                 "master": self.states[c][q][0].cpu(), "exp_avg": self.states[c][q][1].cpu(),
+                 "exp_avg_sq": self.states[c][q][2].cpu(), "acc": self.accs[a][q].cpu()}
+            if self.offload:
+                d["store"] = [x.clone() for x in self.store[q]]
+            mats.append(d)
+        return {"shapes": list(self.shapes), "ks": list(self.ks), "layout": self.layout,
+                "R": self.R, "S": self.S, "warmup": self.warmup, "zen_tau": self.zen_tau,
+                "offload": self.offload, "t": self.t, "th": self.th, "length": self._length,
+                "ended": self._ended, "mats": mats}
+
+    def load_state_dict(self, sd: dict) -> None:
+        """Continues from a state_dict of a runner with the same shapes,
+        ratio, layout, schedule and offload mode (the caller restores the
+        weights)."""
+        mine = {"shapes": list(self.shapes), "ks": list(self.ks), "layout": self.layout,
+                "R": self.R, "S": self.S, "warmup": self.warmup, "zen_tau": self.zen_tau,
+                "offload": self.offload}
+        for key, val in mine.items():
+            got = [tuple(x) for x in sd[key]] if key == "shapes" else sd[key]
+            want = [tuple(x) for x in val] if key == "shapes" else val
+            if got != want:
+                raise ValueError(f"state_dict {key} = {sd[key]!r}, this runner has {val!r}")
+        self.sync()
+        self.cur, self.cur_a = 0, 0
+        for q, d in enumerate(sd["mats"]):
+            s = self.sels[0][q]
+            for dst, key in ((s.sel_idx, "sel_idx"), (s.unsel_idx, "unsel_idx"),
+                             (s.mask, "mask"), (s.prefix, "prefix")):
+                dst.copy_(d[key])
+            for dst, key in zip(self.states[0][q], ("master", "exp_avg", "exp_avg_sq")):
+                dst.copy_(d[key])
+            self.accs[0][q].copy_(d["acc"])
+            if self.offload:
+                for dst, src in zip(self.store[q], d["store"]):
+                    dst.copy_(src)
+        self.t, self.th = int(sd["t"]), int(sd["th"])
+        self._length, self._ended = int(sd["length"]), bool(sd["ended"])
+        self._acc_free = [None] * len(self._acc_free)
+        torch.cuda.synchronize(self.device)
+
     @property
     def current_acc(self) -> List[torch.Tensor]:
         """The packed buffers of the current interval (double-buffered when
