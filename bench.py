@@ -64,6 +64,9 @@ def parse_args(argv=None):
                          "overlapped with the following steps")
     ap.add_argument("--no-overlap", action="store_true",
                     help="with --offload: run the deferred update synchronously")
+    ap.add_argument("--no-first-step-stage", action="store_true",
+                    help="keep an interval's first packed values in fp32 (default, channel-major "
+                         "with the fused hand-over: a bf16 stage, 2 B per value written and read)")
     ap.add_argument("--refresh-waits", action="store_true",
                     help="with --offload: a refresh right after an interval end waits for the "
                          "host update (default: the device takes over the entering columns)")
@@ -89,7 +92,7 @@ def parse_args(argv=None):
 # ---------------------------------------------------------------------------
 
 def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool = False,
-               fused_handover: bool = False) -> dict:
+               fused_handover: bool = False, second: bool = False, stage: bool = False) -> dict:
     """Algorithmic HBM bytes of one step, by kernel.
 
     colnorm  2nm (read G) + 4m (write scores)          refresh steps
@@ -105,6 +108,11 @@ def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool 
              writes the hand-over instead of A -- the same 10nu (6nu) for the
              unselected part -- plus 4nk zeros at the selected columns; A is
              neither written nor read back
+    stage    with the bf16 first-step stage of A (channel-major, fused
+             hand-over): an interval's first step writes 2 B per unselected
+             element instead of 4 (4nu instead of 6nu; 6nu when it also
+             hands over, as before) and its second step reads 2 B instead of
+             4 (8nu instead of 10nu)
     """
     out = {"colnorm": 0, "topk_select": 0, "update": 0, "unpack": 0}
     for (n, m), k in zip(shapes, ks):
@@ -112,7 +120,11 @@ def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool 
         if refresh:
             out["colnorm"] += 2 * n * m + 4 * m
             out["topk_select"] += 8 * m + 12 * ((m + 63) // 64)
-        out["update"] += 28 * n * k + (6 if first else 10) * n * u
+        if first:
+            per_u = 4 if (stage and not end) else 6
+        else:
+            per_u = 8 if (stage and second) else 10
+        out["update"] += 28 * n * k + per_u * n * u
         if end:
             if offload:
                 out["unpack"] += 4 * n * u + 2 * n * u
@@ -284,7 +296,8 @@ def main(argv=None) -> int:
                                       offload=args.offload, overlap=not args.no_overlap,
                                       host_threads=args.host_threads,
                                       fuse_handover=not args.separate_handover,
-                                      refresh_pending=not args.refresh_waits)
+                                      refresh_pending=not args.refresh_waits,
+                                      first_step_stage=not args.no_first_step_stage)
     fused = runner.keep_unpacked and runner.fuse_handover and args.zen_tau is None
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t0
@@ -386,7 +399,8 @@ def main(argv=None) -> int:
     totals = {"colnorm": 0, "topk_select": 0, "update": 0, "unpack": 0}
     for kind in kinds:
         b = step_bytes(shapes, ks, kind.refresh, kind.step_in_interval == 1, kind.interval_end,
-                       offload=args.offload, fused_handover=fused)
+                       offload=args.offload, fused_handover=fused,
+                       second=kind.step_in_interval == 2, stage=runner.use_stage)
         for key in totals:
             totals[key] += b[key]
     all_bytes = sum(totals.values())
@@ -439,6 +453,7 @@ def main(argv=None) -> int:
             "offload": args.offload,
             "model_compute_ms": args.model_compute_ms or None,
             "interval_ends": sum(1 for k in kinds if k.interval_end),
+            "first_step_stage": runner.use_stage,
             "handover": "fused into the interval's last update" if fused else
                         ("device -> host copy of the packed buffer" if args.offload
                          else "separate unpack pass"),

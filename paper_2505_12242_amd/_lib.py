@@ -57,7 +57,8 @@ class ZfMatrix(ctypes.Structure):
                 ("unpacked", c_vp), ("ld_unpacked", c_i64),
                 ("src", ZfStateSource),
                 ("sel_sq", c_vp), ("acc_sq", c_vp),
-                ("weight_cols", c_vp), ("ld_weight_cols", c_i64)]
+                ("weight_cols", c_vp), ("ld_weight_cols", c_i64),
+                ("acc_first", c_vp), ("ld_acc_first", c_i64)]
 
 
 class ZfZenTotals(ctypes.Structure):
@@ -511,6 +512,7 @@ class MatrixBuffers:
     sel_sq: Optional[torch.Tensor] = None   # Zen-auto statistics, [k] fp32
     acc_sq: Optional[torch.Tensor] = None   # Zen-auto statistics, [m-k] fp32
     weight_cols: Optional[torch.Tensor] = None  # deferred update: bf16 unselected columns
+    acc_first: Optional[torch.Tensor] = None  # channel-major: bf16 first-step stage of acc
 
     def as_c(self) -> ZfMatrix:
         L = self.layout
@@ -548,6 +550,10 @@ class MatrixBuffers:
             x.weight_cols = _ptr(self.weight_cols)
             x.ld_weight_cols = _mat(self.weight_cols, torch.bfloat16, "weight_cols", r, c,
                                     device_ok=True)
+        if self.acc_first is not None:
+            x.acc_first = _ptr(self.acc_first)
+            x.ld_acc_first = _lmat(self.acc_first, torch.bfloat16, "acc_first", L, n,
+                                   m - self.k)
         return x
 
 

@@ -357,7 +357,8 @@ bool cm_vec_ok(const DevMat& d) {
          ok(d.M, d.ld_state, 4) && ok(d.V, d.ld_state, 4) && ok(d.acc, d.ld_acc, 4) &&
          ok(d.out, d.ld_out, 4) && ok(d.prev_P, d.ld_prev, 4) && ok(d.prev_M, d.ld_prev, 4) &&
          ok(d.prev_V, d.ld_prev, 4) && ok(d.init_P, d.ld_init, 4) && ok(d.st_P, d.ld_store, 4) &&
-         ok(d.st_M, d.ld_store, 4) && ok(d.st_V, d.ld_store, 4) && ok(d.pend_acc, d.ld_pend, 4);
+         ok(d.st_M, d.ld_store, 4) && ok(d.st_V, d.ld_store, 4) && ok(d.pend_acc, d.ld_pend, 4) &&
+         ok(d.acc1, d.ld_acc1, 8);
 }
 
 // Row-major 16-byte update: G rows 16-byte aligned (8 bf16), and every
@@ -746,6 +747,7 @@ struct zf_plan {
   bool can_colnorm = true, can_topk = true, can_adam = true, can_remap = true, can_pack = true,
        can_unpack = true, can_zen = true, can_scatter = true, can_handover = true,
        can_pending = true, can_scatter_skip = true;
+  bool has_acc1 = false;  // some descriptor gives the bf16 first-step stage
 };
 
 namespace {
@@ -767,6 +769,8 @@ DevMat plan_mat(const zf_matrix& x) {
   d.acc_sq = x.acc_sq;
   d.wcols = x.weight_cols;
   d.ld_wcols = x.ld_weight_cols;
+  d.acc1 = x.acc_first;
+  d.ld_acc1 = x.ld_acc_first;
   apply_source(d, &x.src);
   return d;
 }
@@ -841,6 +845,21 @@ zf_status check_plan_matrix(const zf_matrix& x, zf_plan& p) {
               !overlaps(zsel, zacc);
     for (int a = 0; ok && a < 6; ++a) ok = !overlaps(zsel, others[a]) && !overlaps(zacc, others[a]);
     p.can_zen = p.can_zen && ok;
+  }
+  // The bf16 first-step stage (channel-major only): disjoint from everything
+  // the update reads or writes.
+  if (x.acc_first != nullptr) {
+    if (L != zf::kChannelMajor || !mat_ok(x.acc_first, ea, x.ld_acc_first, 2)) return ZF_EINVAL;
+    const Span st = span(x.acc_first, ea, x.ld_acc_first, 2);
+    const Ext es = ext(L, n, k);
+    if (overlaps(st, g) || overlaps(st, span(x.acc, ea, x.ld_acc, 4)) ||
+        overlaps(st, span(x.weight, eg, x.ld_weight, 2)) ||
+        overlaps(st, span(x.master, es, x.ld_state, 4)) ||
+        overlaps(st, span(x.exp_avg, es, x.ld_state, 4)) ||
+        overlaps(st, span(x.exp_avg_sq, es, x.ld_state, 4)) ||
+        overlaps(st, span(x.unpacked, eg, x.ld_unpacked, 4)) || store_overlaps(d, st))
+      return ZF_EINVAL;
+    p.has_acc1 = true;
   }
   // Strides must be valid whenever the buffer is given.
   if (x.weight && !mat_ok(x.weight, eg, x.ld_weight, 2)) return ZF_EINVAL;
@@ -1020,6 +1039,14 @@ zf_status zf_plan_topk_select(zf_plan* p, zf_stream stream) {
 
 namespace {
 
+// The pack phase passed to the update kernels: 1 on an interval's first
+// step, 2 on its second when the plan keeps a bf16 first-step stage (only
+// the channel-major update reads it), else 0.
+int32_t pack_phase(const zf_plan* p, int64_t step_in_interval) {
+  if (step_in_interval == 1) return 1;
+  return (step_in_interval == 2 && p->has_acc1) ? 2 : 0;
+}
+
 // The plan's update launch: the row-major 16-byte kernel where it applies
 // (its own block table), else the plan's update kernel.
 hipError_t plan_update_launch(const zf_plan* p, const AdamK& c, int32_t mode, int32_t first,
@@ -1050,14 +1077,14 @@ zf_status zf_plan_update(zf_plan* p, const zf_adam_hparams* hp, int64_t step, in
         step_in_interval > accum_interval)
       return ZF_EINVAL;
   }
-  const hipError_t e = plan_update_launch(p, c, mode, step_in_interval == 1 ? 1 : 0,
+  const hipError_t e = plan_update_launch(p, c, mode, do_pack ? pack_phase(p, step_in_interval) : 0,
                                           do_adam != 0, do_pack != 0, false, 1.0f,
                                           as_stream(stream));
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
 zf_status zf_plan_unpack(zf_plan* p, float scale, zf_stream stream) {
-  if (p == nullptr || !p->can_unpack) return ZF_EINVAL;
+  if (p == nullptr || !p->can_unpack || p->has_acc1) return ZF_EINVAL;
   const Table t{p->d_mats, p->d_off_unp, p->nmats};
   const hipError_t e =
       launch_unpack_any(t, p->mats[0], p->blk_unp, scale, p->layout, as_stream(stream));
@@ -1074,7 +1101,7 @@ zf_status zf_plan_update_handover(zf_plan* p, const zf_adam_hparams* hp, int64_t
   if (accum_interval < 1 || step_in_interval < 1 || step_in_interval > accum_interval)
     return ZF_EINVAL;
   const AdamK c = adam_consts(*hp, step);
-  const hipError_t e = plan_update_launch(p, c, mode, step_in_interval == 1 ? 1 : 0, true, true,
+  const hipError_t e = plan_update_launch(p, c, mode, pack_phase(p, step_in_interval), true, true,
                                           true, scale, as_stream(stream));
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
@@ -1089,7 +1116,8 @@ zf_status zf_plan_scatter_weights(zf_plan* p, zf_stream stream) {
 zf_status zf_plan_update_pending(zf_plan* p, const zf_adam_hparams* hp, int64_t step,
                                  int64_t accum_interval, int64_t pend_step, float pend_scale,
                                  zf_stream stream) {
-  if (p == nullptr || !p->can_remap || !p->can_pack || !p->can_pending) return ZF_EINVAL;
+  if (p == nullptr || !p->can_remap || !p->can_pack || !p->can_pending || p->has_acc1)
+    return ZF_EINVAL;
   if (!hparams_ok(hp) || step < 1 || pend_step < 1 || !std::isfinite(pend_scale) ||
       accum_interval < 1)
     return ZF_EINVAL;
@@ -1156,7 +1184,8 @@ zf_status plan_update_zen(zf_plan* p, const AdamK& c, int32_t mode, int32_t firs
 bool zen_args_ok(const zf_plan* p, const zf_adam_hparams* hp, int64_t step, double tau,
                  const zf_zen_totals* totals) {
   static_assert(sizeof(zf_zen_totals) == sizeof(zf::ZenTotals), "zen totals layout");
-  return p != nullptr && p->can_zen && p->can_adam && p->can_pack && hparams_ok(hp) &&
+  return p != nullptr && !p->has_acc1 && p->can_zen && p->can_adam && p->can_pack &&
+         hparams_ok(hp) &&
          step >= 1 && tau >= 0.0 && totals != nullptr && aligned(totals, 8);
 }
 

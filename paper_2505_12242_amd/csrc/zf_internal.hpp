@@ -83,6 +83,8 @@ struct DevMat {
   int64_t ld_wcols;
   const float* pend_acc;  // owed deferred update: packed sums under the previous selection
   int64_t ld_pend;
+  uint16_t* acc1;    // channel-major: bf16 first-step stage of the packed buffer (optional)
+  int64_t ld_acc1;
   float* sel_sq;     // Zen-auto: [k] squared norms of the selected channels' gradient
   float* acc_sq;     // Zen-auto: [m-k] squared norms of the accumulated channels
   // geometry

@@ -252,17 +252,29 @@ __device__ __forceinline__ void cm_adam_elem(rsrc_t rG, rsrc_t rP, rsrc_t rM, rs
 // stored back; scale * sum goes to the channel's row of the hand-over
 // buffer (rOut) instead -- the same two fp32 operations as accumulating and
 // then unpacking.
-template <bool FIRST, int VPT, bool STATS, bool HAND = false>
+//
+// A16 (the packed buffer's bf16 first-step stage, rA16): 1 -- the first step
+// stores its values, the widened gradient itself and so exactly a bf16, as
+// the gradient's own bits into the stage instead of fp32 into A; 2 -- the
+// second step reads the previous values from the stage (widened, the same
+// fp32 values) instead of from A.
+template <bool FIRST, int VPT, bool STATS, bool HAND = false, int A16 = 0>
 __device__ __forceinline__ void cm_pack_vec(rsrc_t rG, rsrc_t rA, double& ss,
-                                            rsrc_t rOut = rsrc_t(), float scale = 1.0f) {
+                                            rsrc_t rOut = rsrc_t(), float scale = 1.0f,
+                                            rsrc_t rA16 = rsrc_t()) {
   const int tid = threadIdx.x;
   u32x4 gv[VPT];
   float a[VPT][kGroup];
 #pragma unroll
   for (int q = 0; q < VPT; ++q) gv[q] = buf_b128<kAuxRO>(rG, group_elem(q, tid) * 2, 0);
   if constexpr (!FIRST) {
+    if constexpr (A16 == 2) {
 #pragma unroll
-    for (int q = 0; q < VPT; ++q) f32x8_load<kAuxRMW>(rA, group_elem(q, tid) * 4, a[q]);
+      for (int q = 0; q < VPT; ++q) widen8(buf_b128<kAuxRO>(rA16, group_elem(q, tid) * 2, 0), a[q]);
+    } else {
+#pragma unroll
+      for (int q = 0; q < VPT; ++q) f32x8_load<kAuxRMW>(rA, group_elem(q, tid) * 4, a[q]);
+    }
   }
 #pragma unroll
   for (int q = 0; q < VPT; ++q) {
@@ -275,21 +287,30 @@ __device__ __forceinline__ void cm_pack_vec(rsrc_t rG, rsrc_t rA, double& ss,
 #pragma unroll
       for (int i = 0; i < kGroup; ++i) a[q][i] = a[q][i] * scale;
       f32x8_store<kAuxWO>(rOut, group_elem(q, tid) * 4, a[q]);
+    } else if constexpr (FIRST && A16 == 1) {
+      buf_put_b128<kAuxAFirst>(gv[q], rA16, group_elem(q, tid) * 2, 0);
     } else {
       f32x8_store<FIRST ? kAuxAFirst : kAuxRMW>(rA, group_elem(q, tid) * 4, a[q]);
     }
   }
 }
 
-template <bool FIRST, bool STATS, bool HAND = false>
+template <bool FIRST, bool STATS, bool HAND = false, int A16 = 0>
 __device__ __forceinline__ void cm_pack_elem(rsrc_t rG, rsrc_t rA, int64_t len, double& ss,
-                                             rsrc_t rOut = rsrc_t(), float scale = 1.0f) {
+                                             rsrc_t rOut = rsrc_t(), float scale = 1.0f,
+                                             rsrc_t rA16 = rsrc_t()) {
   for (int64_t e = threadIdx.x; e < len; e += kThreads) {
     const uint32_t o = static_cast<uint32_t>(e);
-    const float g = widen_bf16(buf_u16<kAuxRO>(rG, o * 2, 0));
-    const float a = FIRST ? g : buf_f32<kAuxRMW>(rA, o * 4, 0) + g;
+    const uint16_t gb = buf_u16<kAuxRO>(rG, o * 2, 0);
+    const float g = widen_bf16(gb);
+    float a = g;
+    if constexpr (!FIRST) {
+      if constexpr (A16 == 2) a = widen_bf16(buf_u16<kAuxRO>(rA16, o * 2, 0)) + g;
+      else a = buf_f32<kAuxRMW>(rA, o * 4, 0) + g;
+    }
     if constexpr (STATS) ss = __builtin_fma(static_cast<double>(a), static_cast<double>(a), ss);
     if constexpr (HAND) buf_put_f32<kAuxWO>(a * scale, rOut, o * 4, 0);
+    else if constexpr (FIRST && A16 == 1) buf_put_u16<kAuxAFirst>(gb, rA16, o * 2, 0);
     else buf_put_f32<FIRST ? kAuxAFirst : kAuxRMW>(a, rA, o * 4, 0);
   }
 }
@@ -304,11 +325,12 @@ __device__ __forceinline__ void cm_adam_vec_any(int vpt, rsrc_t rG, rsrc_t rP, r
   else cm_adam_vec<SRC, 1, STATS>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss, rPA, pd);
 }
 
-template <bool FIRST, bool STATS, bool HAND = false>
+template <bool FIRST, bool STATS, bool HAND = false, int A16 = 0>
 __device__ __forceinline__ void cm_pack_vec_any(int vpt, rsrc_t rG, rsrc_t rA, double& ss,
-                                                rsrc_t rOut = rsrc_t(), float scale = 1.0f) {
-  if (vpt >= 2) cm_pack_vec<FIRST, kCmVpt, STATS, HAND>(rG, rA, ss, rOut, scale);
-  else cm_pack_vec<FIRST, 1, STATS, HAND>(rG, rA, ss, rOut, scale);
+                                                rsrc_t rOut = rsrc_t(), float scale = 1.0f,
+                                                rsrc_t rA16 = rsrc_t()) {
+  if (vpt >= 2) cm_pack_vec<FIRST, kCmVpt, STATS, HAND, A16>(rG, rA, ss, rOut, scale, rA16);
+  else cm_pack_vec<FIRST, 1, STATS, HAND, A16>(rG, rA, ss, rOut, scale, rA16);
 }
 
 // HAND: a selected channel's row of the hand-over buffer is +0.0.
@@ -405,21 +427,41 @@ __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(c
     if constexpr (PACK) {
       const int64_t u = j - r;
       const rsrc_t rA = make_rsrc(d.acc + u * d.ld_acc + e0, len * 4);
+      // the bf16 first-step stage: first == 1 on an interval's first step,
+      // 2 on its second (a matrix without a stage takes 2 as any later step)
+      const bool a16 = d.acc1 != nullptr;
+      const rsrc_t rA16 = a16 ? make_rsrc(d.acc1 + u * d.ld_acc1 + e0, len * 2) : rA;
       if constexpr (HAND) {
         const rsrc_t rOut = make_rsrc(d.out + j * d.ld_out + e0, len * 4);
         if (d.vec) {
-          if (first) cm_pack_vec_any<true, false, true>(d.cm_vpt, rG, rA, ss, rOut, scale);
+          if (first == 1) cm_pack_vec_any<true, false, true>(d.cm_vpt, rG, rA, ss, rOut, scale);
+          else if (a16 && first == 2)
+            cm_pack_vec_any<false, false, true, 2>(d.cm_vpt, rG, rA, ss, rOut, scale, rA16);
           else cm_pack_vec_any<false, false, true>(d.cm_vpt, rG, rA, ss, rOut, scale);
         } else {
-          if (first) cm_pack_elem<true, false, true>(rG, rA, len, ss, rOut, scale);
+          if (first == 1) cm_pack_elem<true, false, true>(rG, rA, len, ss, rOut, scale);
+          else if (a16 && first == 2)
+            cm_pack_elem<false, false, true, 2>(rG, rA, len, ss, rOut, scale, rA16);
           else cm_pack_elem<false, false, true>(rG, rA, len, ss, rOut, scale);
         }
       } else if (d.vec) {
-        if (first) cm_pack_vec_any<true, STATS>(d.cm_vpt, rG, rA, ss);
-        else cm_pack_vec_any<false, STATS>(d.cm_vpt, rG, rA, ss);
+        if (first == 1) {
+          if (a16) cm_pack_vec_any<true, STATS, false, 1>(d.cm_vpt, rG, rA, ss, rsrc_t(), 1.0f, rA16);
+          else cm_pack_vec_any<true, STATS>(d.cm_vpt, rG, rA, ss);
+        } else if (a16 && first == 2) {
+          cm_pack_vec_any<false, STATS, false, 2>(d.cm_vpt, rG, rA, ss, rsrc_t(), 1.0f, rA16);
+        } else {
+          cm_pack_vec_any<false, STATS>(d.cm_vpt, rG, rA, ss);
+        }
       } else {
-        if (first) cm_pack_elem<true, STATS>(rG, rA, len, ss);
-        else cm_pack_elem<false, STATS>(rG, rA, len, ss);
+        if (first == 1) {
+          if (a16) cm_pack_elem<true, STATS, false, 1>(rG, rA, len, ss, rsrc_t(), 1.0f, rA16);
+          else cm_pack_elem<true, STATS>(rG, rA, len, ss);
+        } else if (a16 && first == 2) {
+          cm_pack_elem<false, STATS, false, 2>(rG, rA, len, ss, rsrc_t(), 1.0f, rA16);
+        } else {
+          cm_pack_elem<false, STATS>(rG, rA, len, ss);
+        }
       }
     }
   } else if constexpr (ADAM) {

@@ -120,7 +120,7 @@ class SelectiveUpdateRunner:
                  device=None, keep_unpacked: bool = True, layout: int = ROW_MAJOR,
                  zen_tau: Optional[float] = None, offload: bool = False, overlap: bool = True,
                  host_threads: Optional[int] = None, fuse_handover: bool = True,
-                 warmup: int = 0, refresh_pending: bool = True):
+                 warmup: int = 0, refresh_pending: bool = True, first_step_stage: bool = True):
         self.device = torch.device(device) if device is not None else torch.device("cuda")
         self.shapes = [(int(n), int(m)) for n, m in shapes]
         self.ratio, self.hp, self.R, self.S = ratio, hp, int(refresh), int(accum)
@@ -132,6 +132,12 @@ class SelectiveUpdateRunner:
         self.refresh_pending = bool(refresh_pending) and self.overlap
         self.keep_unpacked = keep_unpacked and not self.offload
         self.fuse_handover = bool(fuse_handover)
+        # the bf16 first-step stage of the packed buffer (channel-major, the
+        # fixed schedule with the fused hand-over: the only consumers of the
+        # packed buffer are then the next update passes)
+        self.use_stage = (bool(first_step_stage) and layout != ROW_MAJOR and not self.offload
+                          and zen_tau is None and self.keep_unpacked and self.fuse_handover)
+        self._in_stage = False  # the current interval's sums are in the stage
         self.weights = list(weights)
         self.init_master = list(init_master) if init_master is not None else None
         dev = self.device
@@ -152,6 +158,7 @@ class SelectiveUpdateRunner:
         self.norms, self.unpacked, self.sel_sq, self.acc_sq = [], [], [], []
         self.store, self.host_acc, self.wcols, self.unsel_host = [], [], [], []
         self.wcols_dev = []  # overlap: device staging of the host-produced weights
+        self.stage = []      # bf16 first-step stage of the packed buffer
         for q, ((n, m), k) in enumerate(zip(self.shapes, self.ks)):
             if self.zen_tau is not None:
                 self.sel_sq.append(torch.empty(k, dtype=f32, device=dev))
@@ -162,6 +169,8 @@ class SelectiveUpdateRunner:
                                             for _ in range(3)))
             for a in range(nacc):
                 self.accs[a].append(alloc_stored(layout, n, m - k, f32, dev))
+            if self.use_stage:
+                self.stage.append(alloc_stored(layout, n, m - k, torch.bfloat16, dev))
             self.norms.append(torch.empty(m, dtype=f32, device=dev))
             self.unpacked.append(alloc_stored(layout, n, m, f32, dev)
                                  if self.keep_unpacked else None)
@@ -178,7 +187,6 @@ class SelectiveUpdateRunner:
                 if self.overlap:
                     self.wcols_dev.append(alloc_stored(layout, n, m - k, torch.bfloat16, dev))
                 self.unsel_host.append(_pinned_like((m - k,), torch.int32))
-        self.acc = self.accs[0]
         self.grad_slots = [list(s) for s in grad_slots]
         self.plans = [[[self._plan(slot, p, a) for a in range(nacc)] for p in range(2)]
                       for slot in range(len(self.grad_slots))]
@@ -223,7 +231,8 @@ class SelectiveUpdateRunner:
                 sel_sq=self.sel_sq[q] if self.sel_sq else None,
                 acc_sq=self.acc_sq[q] if self.acc_sq else None,
                 weight_cols=(self.wcols_dev[q] if self.overlap else self.wcols[q])
-                if self.offload else None))
+                if self.offload else None,
+                acc_first=self.stage[q] if self.use_stage else None))
         return Plan(q_bufs)
 
     @property
@@ -269,6 +278,7 @@ class SelectiveUpdateRunner:
             mode = STATES_INPLACE
         if self.zen_tau is None:
             end = kind.interval_end
+            self._in_stage = self.use_stage and length == 1 and not end
             if end and self.keep_unpacked and self.fuse_handover:
                 with rec("update_handover"):
                     plan.update_handover(self.hp, t, mode, length, self.S, 1.0 / length, st)
@@ -468,14 +478,14 @@ class SelectiveUpdateRunner:
             d = {"sel_idx": s.sel_idx.cpu(), "unsel_idx": s.unsel_idx.cpu(),
                  "mask": s.mask.cpu(), "prefix": s.prefix.cpu(),
                  "master": self.states[c][q][0].cpu(), "exp_avg": self.states[c][q][1].cpu(),
-                 "exp_avg_sq": self.states[c][q][2].cpu(), "acc": self.accs[a][q].cpu()}
+                 "exp_avg_sq": self.states[c][q][2].cpu(), "acc": self.acc[q].cpu()}
             if self.offload:
                 d["store"] = [x.clone() for x in self.store[q]]
             mats.append(d)
         return {"shapes": list(self.shapes), "ks": list(self.ks), "layout": self.layout,
                 "R": self.R, "S": self.S, "warmup": self.warmup, "zen_tau": self.zen_tau,
                 "offload": self.offload, "t": self.t, "th": self.th, "length": self._length,
-                "ended": self._ended, "mats": mats}
+                "ended": self._ended, "in_stage": self._in_stage, "mats": mats}
 
     def load_state_dict(self, sd: dict) -> None:
         """Continues from a state_dict of a runner with the same shapes,
@@ -498,19 +508,32 @@ class SelectiveUpdateRunner:
                 dst.copy_(d[key])
             for dst, key in zip(self.states[0][q], ("master", "exp_avg", "exp_avg_sq")):
                 dst.copy_(d[key])
-            self.accs[0][q].copy_(d["acc"])
+            if sd.get("in_stage") and self.use_stage:
+                self.stage[q].copy_(d["acc"])  # first-step values: exact in bf16
+            else:
+                self.accs[0][q].copy_(d["acc"])
             if self.offload:
                 for dst, src in zip(self.store[q], d["store"]):
                     dst.copy_(src)
         self.t, self.th = int(sd["t"]), int(sd["th"])
         self._length, self._ended = int(sd["length"]), bool(sd["ended"])
+        self._in_stage = bool(sd.get("in_stage")) and self.use_stage
         self._acc_free = [None] * len(self._acc_free)
         torch.cuda.synchronize(self.device)
 
     @property
+    def acc(self) -> List[torch.Tensor]:
+        """The current interval's packed sums, fp32 (after an interval's
+        first step with the bf16 stage: a widened copy of the stage, exact)."""
+        if self._in_stage:
+            return [x.float() for x in self.stage]
+        return self.accs[self.cur_a]
+
+    @property
     def current_acc(self) -> List[torch.Tensor]:
-        """The packed buffers of the current interval (double-buffered when
-        the deferred update overlaps)."""
+        """The fp32 packed buffers of the current interval (double-buffered
+        when the deferred update overlaps); after an interval's first step
+        with the bf16 stage the sums are in the stage (see acc)."""
         return self.accs[self.cur_a]
 
     def close(self) -> None:

@@ -23,7 +23,7 @@ def _snapshot(runner):
     for q in range(len(runner.shapes)):
         out.append(runner.selection[q].sel_idx.cpu().numpy())
         out.extend(x.cpu().numpy() for x in runner.state[q])
-        out.append(runner.current_acc[q].cpu().numpy())
+        out.append(runner.acc[q].cpu().numpy())
         if runner.offload:
             out.extend(x.numpy().copy() for x in runner.store[q])
         out.append(bits_np(runner.weights[q]))
