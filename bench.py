@@ -65,8 +65,9 @@ def parse_args(argv=None):
     ap.add_argument("--no-overlap", action="store_true",
                     help="with --offload: run the deferred update synchronously")
     ap.add_argument("--no-first-step-stage", action="store_true",
-                    help="keep an interval's first packed values in fp32 (default, channel-major "
-                         "with the fused hand-over: a bf16 stage, 2 B per value written and read)")
+                    help="keep an interval's first packed values in fp32 (default in the "
+                         "channel-major layout with the fused hand-over: a bf16 stage, 2 B per "
+                         "value written and read)")
     ap.add_argument("--refresh-waits", action="store_true",
                     help="with --offload: a refresh right after an interval end waits for the "
                          "host update (default: the device takes over the entering columns)")
@@ -108,8 +109,8 @@ def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool 
              writes the hand-over instead of A -- the same 10nu (6nu) for the
              unselected part -- plus 4nk zeros at the selected columns; A is
              neither written nor read back
-    stage    with the bf16 first-step stage of A (channel-major, fused
-             hand-over): an interval's first step writes 2 B per unselected
+    stage    with the bf16 first-step stage of A (fused hand-over): an
+             interval's first step writes 2 B per unselected
              element instead of 4 (4nu instead of 6nu; 6nu when it also
              hands over, as before) and its second step reads 2 B instead of
              4 (8nu instead of 10nu)
@@ -297,7 +298,8 @@ def main(argv=None) -> int:
                                       host_threads=args.host_threads,
                                       fuse_handover=not args.separate_handover,
                                       refresh_pending=not args.refresh_waits,
-                                      first_step_stage=not args.no_first_step_stage)
+                                      first_step_stage=False if args.no_first_step_stage
+                                      else None)
     fused = runner.keep_unpacked and runner.fuse_handover and args.zen_tau is None
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t0

@@ -374,13 +374,14 @@ typedef struct zf_matrix {
   float* acc_sq; /* Zen-auto only: [m - k] fp32 (else NULL) */
   const uint16_t* weight_cols; /* deferred update only: bf16 [n][m-k] / cm [m-k][n] */
   int64_t ld_weight_cols;
-  uint16_t* acc_first; /* optional, channel-major: bf16 [m-k][ld_acc_first >= n], see below */
+  uint16_t* acc_first; /* optional: bf16 in the layout of acc (row-major [n][ld >= m-k],
+                          channel-major [m-k][ld >= n]), see below */
   int64_t ld_acc_first;
 } zf_matrix;
 
 typedef struct zf_plan zf_plan;
 
-/* First-step stage of the packed buffer (acc_first; channel-major plans).
+/* First-step stage of the packed buffer (acc_first).
  * On the first step of an interval the packed values are the widened
  * gradient itself, so every one of them is exactly a bf16.  When a
  * descriptor gives acc_first, zf_plan_update (do_pack) and
@@ -392,11 +393,10 @@ typedef struct zf_plan zf_plan;
  * acc, step_in_interval == 2 reads acc_first.  Every result (acc from the
  * second step on, the hand-over, W, the states) is bit-identical to a plan
  * without it.  acc_first must be 2-byte aligned (16-byte aligned with
- * ld % 8 == 0 for the vector path) and overlap no other buffer.  A plan with
- * a stage rejects zf_plan_unpack, zf_plan_update_zen(_pending) and
+ * ld % 8 == 0 for the vector paths) and overlap no other buffer.  A plan
+ * with a stage rejects zf_plan_unpack, zf_plan_update_zen(_pending) and
  * zf_plan_update_pending (ZF_EINVAL): after a first step they would need the
- * stage.  Row-major descriptors must leave it NULL (ZF_EINVAL at plan
- * creation). */
+ * stage. */
 
 /* Validates nmats >= 1 descriptors (HOST array, copied), computes the launch
  * geometry and allocates the plan's device tables and column-score

@@ -373,7 +373,7 @@ bool rv_ok(const DevMat& d) {
   };
   return d.grad != nullptr && aligned(d.grad, 16) && (one_row || d.ld_grad % 8 == 0) &&
          ok(d.acc, d.ld_acc, 4) && ok(d.P, d.ld_state, 4) && ok(d.M, d.ld_state, 4) &&
-         ok(d.V, d.ld_state, 4) && ok(d.out, d.ld_out, 4);
+         ok(d.V, d.ld_state, 4) && ok(d.out, d.ld_out, 4) && ok(d.acc1, d.ld_acc1, 8);
 }
 
 // Geometry of the row-major 16-byte update; used when `allow` (all matrices
@@ -846,10 +846,10 @@ zf_status check_plan_matrix(const zf_matrix& x, zf_plan& p) {
     for (int a = 0; ok && a < 6; ++a) ok = !overlaps(zsel, others[a]) && !overlaps(zacc, others[a]);
     p.can_zen = p.can_zen && ok;
   }
-  // The bf16 first-step stage (channel-major only): disjoint from everything
-  // the update reads or writes.
+  // The bf16 first-step stage: disjoint from everything the update reads or
+  // writes.
   if (x.acc_first != nullptr) {
-    if (L != zf::kChannelMajor || !mat_ok(x.acc_first, ea, x.ld_acc_first, 2)) return ZF_EINVAL;
+    if (!mat_ok(x.acc_first, ea, x.ld_acc_first, 2)) return ZF_EINVAL;
     const Span st = span(x.acc_first, ea, x.ld_acc_first, 2);
     const Ext es = ext(L, n, k);
     if (overlaps(st, g) || overlaps(st, span(x.acc, ea, x.ld_acc, 4)) ||
@@ -1040,8 +1040,8 @@ zf_status zf_plan_topk_select(zf_plan* p, zf_stream stream) {
 namespace {
 
 // The pack phase passed to the update kernels: 1 on an interval's first
-// step, 2 on its second when the plan keeps a bf16 first-step stage (only
-// the channel-major update reads it), else 0.
+// step, 2 on its second when the plan keeps a bf16 first-step stage, else
+// 0.
 int32_t pack_phase(const zf_plan* p, int64_t step_in_interval) {
   if (step_in_interval == 1) return 1;
   return (step_in_interval == 2 && p->has_acc1) ? 2 : 0;

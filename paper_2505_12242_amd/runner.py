@@ -120,7 +120,8 @@ class SelectiveUpdateRunner:
                  device=None, keep_unpacked: bool = True, layout: int = ROW_MAJOR,
                  zen_tau: Optional[float] = None, offload: bool = False, overlap: bool = True,
                  host_threads: Optional[int] = None, fuse_handover: bool = True,
-                 warmup: int = 0, refresh_pending: bool = True, first_step_stage: bool = True):
+                 warmup: int = 0, refresh_pending: bool = True,
+                 first_step_stage: Optional[bool] = None):
         self.device = torch.device(device) if device is not None else torch.device("cuda")
         self.shapes = [(int(n), int(m)) for n, m in shapes]
         self.ratio, self.hp, self.R, self.S = ratio, hp, int(refresh), int(accum)
@@ -132,11 +133,16 @@ class SelectiveUpdateRunner:
         self.refresh_pending = bool(refresh_pending) and self.overlap
         self.keep_unpacked = keep_unpacked and not self.offload
         self.fuse_handover = bool(fuse_handover)
-        # the bf16 first-step stage of the packed buffer (channel-major, the
-        # fixed schedule with the fused hand-over: the only consumers of the
-        # packed buffer are then the next update passes)
-        self.use_stage = (bool(first_step_stage) and layout != ROW_MAJOR and not self.offload
-                          and zen_tau is None and self.keep_unpacked and self.fuse_handover)
+        # the bf16 first-step stage of the packed buffer, possible with the
+        # fixed schedule and the fused hand-over (the only consumers of the
+        # packed buffer are then the next update passes).  By default
+        # (first_step_stage None) channel-major only: in the row-major layout,
+        # bound by the weight write-back's partial lines, it measured no
+        # faster; True uses it in either layout, False never.
+        possible = (not self.offload and zen_tau is None and self.keep_unpacked
+                    and self.fuse_handover)
+        want = layout != ROW_MAJOR if first_step_stage is None else bool(first_step_stage)
+        self.use_stage = possible and want
         self._in_stage = False  # the current interval's sums are in the stage
         self.weights = list(weights)
         self.init_master = list(init_master) if init_master is not None else None
