@@ -109,19 +109,25 @@ def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool 
              writes the hand-over instead of A -- the same 10nu (6nu) for the
              unselected part -- plus 4nk zeros at the selected columns; A is
              neither written nor read back
-    stage    with the bf16 first-step stage of A (fused hand-over): an
-             interval's first step writes 2 B per unselected
+    stage    with the bf16 first-step stage of A (channel-major, fused
+             hand-over): an interval's first step writes 2 B per unselected
              element instead of 4 (4nu instead of 6nu; 6nu when it also
              hands over, as before) and its second step reads 2 B instead of
-             4 (8nu instead of 10nu)
+             4 (8nu instead of 10nu).  A refresh step that starts an
+             interval fills the stage from the score pass instead: colnorm
+             2nm + 2nm (every channel's row written), update 28nk (Adam
+             only)
     """
     out = {"colnorm": 0, "topk_select": 0, "update": 0, "unpack": 0}
     for (n, m), k in zip(shapes, ks):
         u = m - k
+        staged_refresh = refresh and stage and not end
         if refresh:
-            out["colnorm"] += 2 * n * m + 4 * m
+            out["colnorm"] += 2 * n * m + 4 * m + (2 * n * m if staged_refresh else 0)
             out["topk_select"] += 8 * m + 12 * ((m + 63) // 64)
-        if first:
+        if staged_refresh:
+            per_u = 0
+        elif first:
             per_u = 4 if (stage and not end) else 6
         else:
             per_u = 8 if (stage and second) else 10
@@ -298,8 +304,7 @@ def main(argv=None) -> int:
                                       host_threads=args.host_threads,
                                       fuse_handover=not args.separate_handover,
                                       refresh_pending=not args.refresh_waits,
-                                      first_step_stage=False if args.no_first_step_stage
-                                      else None)
+                                      first_step_stage=not args.no_first_step_stage)
     fused = runner.keep_unpacked and runner.fuse_handover and args.zen_tau is None
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t0

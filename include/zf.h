@@ -374,29 +374,34 @@ typedef struct zf_matrix {
   float* acc_sq; /* Zen-auto only: [m - k] fp32 (else NULL) */
   const uint16_t* weight_cols; /* deferred update only: bf16 [n][m-k] / cm [m-k][n] */
   int64_t ld_weight_cols;
-  uint16_t* acc_first; /* optional: bf16 in the layout of acc (row-major [n][ld >= m-k],
-                          channel-major [m-k][ld >= n]), see below */
+  uint16_t* acc_first; /* optional, channel-major only: bf16 [m][ld_acc_first >= n],
+                          row j = channel j, see below */
   int64_t ld_acc_first;
 } zf_matrix;
 
 typedef struct zf_plan zf_plan;
 
-/* First-step stage of the packed buffer (acc_first).
+/* First-step stage of the packed buffer (acc_first; channel-major plans).
  * On the first step of an interval the packed values are the widened
  * gradient itself, so every one of them is exactly a bf16.  When a
- * descriptor gives acc_first, zf_plan_update (do_pack) and
- * zf_plan_update_handover keep that step's values there, as the gradient's
- * bf16 bits (2 bytes per element written instead of 4), and the interval's
- * second step reads them from there instead of from acc (2 bytes read
- * instead of 4) and writes its fp32 sums to acc as usual.  The rule is
- * stateless: with acc_first, step_in_interval == 1 writes acc_first and not
- * acc, step_in_interval == 2 reads acc_first.  Every result (acc from the
- * second step on, the hand-over, W, the states) is bit-identical to a plan
- * without it.  acc_first must be 2-byte aligned (16-byte aligned with
- * ld % 8 == 0 for the vector paths) and overlap no other buffer.  A plan
- * with a stage rejects zf_plan_unpack, zf_plan_update_zen(_pending) and
- * zf_plan_update_pending (ZF_EINVAL): after a first step they would need the
- * stage. */
+ * descriptor gives acc_first (one bf16 row per channel, row j = channel j),
+ * zf_plan_update (do_pack) and zf_plan_update_handover keep that step's
+ * values there, as the gradient's bf16 bits (2 bytes per element written
+ * instead of 4), and the interval's second step reads them from there
+ * instead of from acc (2 bytes read instead of 4) and writes its fp32 sums
+ * to acc as usual.  The rule is stateless: with acc_first,
+ * step_in_interval == 1 writes the unselected channels' rows of acc_first
+ * and not acc; step_in_interval == 2 reads those rows.  A refresh step may
+ * instead run zf_plan_colnorm_stage (scores plus every channel's row of the
+ * stage, in one pass over G) and then zf_plan_update with do_pack = 0: the
+ * stage then holds what the packing would have written.  Every result (acc
+ * from the second step on, the hand-over, W, the states) is bit-identical
+ * to a plan without it.  acc_first must be 2-byte aligned (16-byte aligned
+ * with ld % 8 == 0 for the vector path) and overlap no other buffer; a
+ * row-major descriptor must leave it NULL (ZF_EINVAL at plan creation).  A
+ * plan with a stage rejects zf_plan_unpack, zf_plan_update_zen(_pending) and
+ * zf_plan_update_pending (ZF_EINVAL): after a first step they would need
+ * the stage. */
 
 /* Validates nmats >= 1 descriptors (HOST array, copied), computes the launch
  * geometry and allocates the plan's device tables and column-score
@@ -413,6 +418,15 @@ size_t zf_plan_device_bytes(const zf_plan* plan);
 /* zf_colnorm over every matrix of the plan (one workspace shared by the
  * plan: do not run two colnorm calls of one plan concurrently). */
 zf_status zf_plan_colnorm(zf_plan* plan, zf_stream stream);
+
+/* zf_plan_colnorm that also copies every channel's gradient row to its row
+ * of the descriptor's acc_first (descriptors without one: scores only), in
+ * the same pass over G: on a refresh step that starts an interval, the
+ * packing of whichever channels the selection leaves unselected, done
+ * before the selection is known (2 bytes per element written for every
+ * channel instead of 2 read + 2 written for each unselected one in the
+ * update).  Needs a plan with a stage (ZF_EINVAL otherwise). */
+zf_status zf_plan_colnorm_stage(zf_plan* plan, zf_stream stream);
 
 /* zf_topk_select over every matrix, k taken from the descriptors. */
 zf_status zf_plan_topk_select(zf_plan* plan, zf_stream stream);

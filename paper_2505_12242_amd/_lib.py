@@ -98,6 +98,7 @@ SIGNATURES = [
     ("zf_plan_device_bytes", c_sz, [c_vp]),
     ("zf_plan_colnorm", ctypes.c_int, [c_vp, c_vp]),
     ("zf_plan_topk_select", ctypes.c_int, [c_vp, c_vp]),
+    ("zf_plan_colnorm_stage", ctypes.c_int, [c_vp, c_vp]),
     ("zf_plan_update", ctypes.c_int,
      [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, c_i32, c_i64, c_i64, c_i32, c_i32, c_vp]),
     ("zf_plan_unpack", ctypes.c_int, [c_vp, c_flt, c_vp]),
@@ -512,7 +513,7 @@ class MatrixBuffers:
     sel_sq: Optional[torch.Tensor] = None   # Zen-auto statistics, [k] fp32
     acc_sq: Optional[torch.Tensor] = None   # Zen-auto statistics, [m-k] fp32
     weight_cols: Optional[torch.Tensor] = None  # deferred update: bf16 unselected columns
-    acc_first: Optional[torch.Tensor] = None  # channel-major: bf16 first-step stage of acc
+    acc_first: Optional[torch.Tensor] = None  # channel-major: bf16 first-step stage, [m, n]
 
     def as_c(self) -> ZfMatrix:
         L = self.layout
@@ -552,8 +553,7 @@ class MatrixBuffers:
                                     device_ok=True)
         if self.acc_first is not None:
             x.acc_first = _ptr(self.acc_first)
-            x.ld_acc_first = _lmat(self.acc_first, torch.bfloat16, "acc_first", L, n,
-                                   m - self.k)
+            x.ld_acc_first = _lmat(self.acc_first, torch.bfloat16, "acc_first", L, n, m)
         return x
 
 
@@ -591,6 +591,11 @@ class Plan:
 
     def colnorm(self, stream=None) -> None:
         _check("zf_plan_colnorm", LIB.zf_plan_colnorm(self._h, _stream(stream)))
+
+    def colnorm_stage(self, stream=None) -> None:
+        """Scores plus every channel's gradient row copied to its row of the
+        bf16 first-step stage (zf_plan_colnorm_stage)."""
+        _check("zf_plan_colnorm_stage", LIB.zf_plan_colnorm_stage(self._h, _stream(stream)))
 
     def topk_select(self, stream=None) -> None:
         _check("zf_plan_topk_select", LIB.zf_plan_topk_select(self._h, _stream(stream)))

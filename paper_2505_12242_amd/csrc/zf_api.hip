@@ -373,7 +373,7 @@ bool rv_ok(const DevMat& d) {
   };
   return d.grad != nullptr && aligned(d.grad, 16) && (one_row || d.ld_grad % 8 == 0) &&
          ok(d.acc, d.ld_acc, 4) && ok(d.P, d.ld_state, 4) && ok(d.M, d.ld_state, 4) &&
-         ok(d.V, d.ld_state, 4) && ok(d.out, d.ld_out, 4) && ok(d.acc1, d.ld_acc1, 8);
+         ok(d.V, d.ld_state, 4) && ok(d.out, d.ld_out, 4);
 }
 
 // Geometry of the row-major 16-byte update; used when `allow` (all matrices
@@ -738,16 +738,18 @@ struct zf_plan {
   int64_t* d_off_zen = nullptr;
   int64_t* d_off_zp = nullptr;  // row-major Zen-auto partial pass
   int64_t* d_off_upv = nullptr;  // row-major 16-byte update
+  int64_t* d_off_sel = nullptr;  // channel-major Adam over the selected channels only
   double* d_ws = nullptr;
   double* d_zs = nullptr;  // Zen-auto per-wave partials
   double* d_zb = nullptr;  // Zen-auto per-finalize-block sums
   int64_t blk_cn = 0, blk_fin = 0, blk_top = 0, blk_up = 0, blk_unp = 0, blk_zen = 0, blk_zp = 0,
-          blk_upv = 0;
+          blk_upv = 0, blk_sel = 0;
   int64_t k_total = 0, u_total = 0;
   bool can_colnorm = true, can_topk = true, can_adam = true, can_remap = true, can_pack = true,
        can_unpack = true, can_zen = true, can_scatter = true, can_handover = true,
        can_pending = true, can_scatter_skip = true;
   bool has_acc1 = false;  // some descriptor gives the bf16 first-step stage
+  bool has_store = false;  // some descriptor gives a full-state store
 };
 
 namespace {
@@ -846,11 +848,11 @@ zf_status check_plan_matrix(const zf_matrix& x, zf_plan& p) {
     for (int a = 0; ok && a < 6; ++a) ok = !overlaps(zsel, others[a]) && !overlaps(zacc, others[a]);
     p.can_zen = p.can_zen && ok;
   }
-  // The bf16 first-step stage: disjoint from everything the update reads or
-  // writes.
+  // The bf16 first-step stage (channel-major, one row per channel): disjoint
+  // from everything the update reads or writes.
   if (x.acc_first != nullptr) {
-    if (!mat_ok(x.acc_first, ea, x.ld_acc_first, 2)) return ZF_EINVAL;
-    const Span st = span(x.acc_first, ea, x.ld_acc_first, 2);
+    if (L != zf::kChannelMajor || !mat_ok(x.acc_first, eg, x.ld_acc_first, 2)) return ZF_EINVAL;
+    const Span st = span(x.acc_first, eg, x.ld_acc_first, 2);
     const Ext es = ext(L, n, k);
     if (overlaps(st, g) || overlaps(st, span(x.acc, ea, x.ld_acc, 4)) ||
         overlaps(st, span(x.weight, eg, x.ld_weight, 2)) ||
@@ -903,7 +905,7 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   }
   std::vector<int64_t> off_cn(nmats + 1), off_fin(nmats + 1), off_top(nmats + 1),
       off_up(nmats + 1), off_unp(nmats + 1), off_zen(nmats + 1), off_zp(nmats + 1),
-      off_upv(nmats + 1);
+      off_upv(nmats + 1), off_sel(nmats + 1);
   int64_t ws_doubles = 0, zs_doubles = 0;
   const bool cm = p->layout == zf::kChannelMajor;
   p->mats.resize(nmats);
@@ -934,12 +936,15 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
     off_top[q] = p->blk_top;
     off_up[q] = p->blk_up;
     off_upv[q] = p->blk_upv;
+    off_sel[q] = p->blk_sel;
     off_unp[q] = p->blk_unp;
     p->blk_cn += colnorm_grid(d);
     p->blk_fin += cm ? 0 : ceil_div(d.m, zf::kFinalizeCols);
     p->blk_top += 1;
     p->blk_up += update_grid(d);
     if (d.rv) p->blk_upv += rv_grid(d);
+    if (cm) p->blk_sel += d.k * static_cast<int64_t>(d.cm_nch);
+    p->has_store = p->has_store || d.st_P != nullptr;
     p->blk_unp += unpack_grid(d);
     p->mats[q] = d;
   }
@@ -951,9 +956,10 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   off_zen[nmats] = p->blk_zen;
   off_zp[nmats] = p->blk_zp;
   off_upv[nmats] = p->blk_upv;
+  off_sel[nmats] = p->blk_sel;
   const int64_t max_blocks = (int64_t(1) << 31) / zf::kThreads;
   if (p->blk_cn >= max_blocks || p->blk_up >= max_blocks || p->blk_unp >= max_blocks ||
-      p->blk_upv >= max_blocks ||
+      p->blk_upv >= max_blocks || p->blk_sel >= max_blocks ||
       p->blk_zp >= max_blocks) {
     delete p;
     return ZF_EINVAL;  // grid too large for one launch
@@ -961,7 +967,7 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
 
   const size_t mats_bytes = sizeof(DevMat) * nmats;
   const size_t off_bytes = sizeof(int64_t) * (nmats + 1);
-  const size_t head = (mats_bytes + 8 * off_bytes + 255) & ~size_t(255);
+  const size_t head = (mats_bytes + 9 * off_bytes + 255) & ~size_t(255);
   const int64_t zb_doubles = p->can_zen ? 2 * p->blk_zen : 0;
   p->dev_bytes = head + sizeof(double) * static_cast<size_t>(ws_doubles + zs_doubles + zb_doubles);
   hipError_t e = hipMalloc(&p->dev, p->dev_bytes);
@@ -980,6 +986,7 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   p->d_off_zen = p->d_off_unp + (nmats + 1);
   p->d_off_zp = p->d_off_zen + (nmats + 1);
   p->d_off_upv = p->d_off_zp + (nmats + 1);
+  p->d_off_sel = p->d_off_upv + (nmats + 1);
   p->d_ws = reinterpret_cast<double*>(base + head);
   p->d_zs = p->d_ws + ws_doubles;
   p->d_zb = p->d_zs + zs_doubles;
@@ -993,6 +1000,7 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   std::memcpy(host.data() + mats_bytes + 5 * off_bytes, off_zen.data(), off_bytes);
   std::memcpy(host.data() + mats_bytes + 6 * off_bytes, off_zp.data(), off_bytes);
   std::memcpy(host.data() + mats_bytes + 7 * off_bytes, off_upv.data(), off_bytes);
+  std::memcpy(host.data() + mats_bytes + 8 * off_bytes, off_sel.data(), off_bytes);
   e = hipMemcpy(p->dev, host.data(), head, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     g_last_hip_error = static_cast<int>(e);
@@ -1028,6 +1036,13 @@ zf_status zf_plan_colnorm(zf_plan* p, zf_stream stream) {
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
+zf_status zf_plan_colnorm_stage(zf_plan* p, zf_stream stream) {
+  if (p == nullptr || !p->can_colnorm || !p->has_acc1) return ZF_EINVAL;
+  const Table t{p->d_mats, p->d_off_cn, p->nmats};
+  const hipError_t e = zf::launch_cm_colnorm(t, p->mats[0], p->blk_cn, as_stream(stream), true);
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
 zf_status zf_plan_topk_select(zf_plan* p, zf_stream stream) {
   if (p == nullptr || !p->can_topk) return ZF_EINVAL;
   const Table t{p->d_mats, p->d_off_top, p->nmats};
@@ -1040,17 +1055,23 @@ zf_status zf_plan_topk_select(zf_plan* p, zf_stream stream) {
 namespace {
 
 // The pack phase passed to the update kernels: 1 on an interval's first
-// step, 2 on its second when the plan keeps a bf16 first-step stage, else
-// 0.
+// step, 2 on its second when the plan keeps a bf16 first-step stage (a
+// channel-major plan), else 0.
 int32_t pack_phase(const zf_plan* p, int64_t step_in_interval) {
   if (step_in_interval == 1) return 1;
   return (step_in_interval == 2 && p->has_acc1) ? 2 : 0;
 }
 
 // The plan's update launch: the row-major 16-byte kernel where it applies
-// (its own block table), else the plan's update kernel.
+// (its own block table); channel-major Adam alone without a store over the
+// selected channels only (its own block table); else the plan's update
+// kernel.
 hipError_t plan_update_launch(const zf_plan* p, const AdamK& c, int32_t mode, int32_t first,
                               bool adam, bool pack, bool handover, float scale, hipStream_t s) {
+  if (p->layout == zf::kChannelMajor && adam && !pack && !handover && !p->has_store) {
+    const Table ts{p->d_mats, p->d_off_sel, p->nmats};
+    return zf::launch_cm_adam_selected_grid(ts, p->mats[0], p->blk_sel, c, mode, s);
+  }
   const bool rv = use_rv(p->mats[0], mode, adam);
   const Table t{p->d_mats, rv ? p->d_off_upv : p->d_off_up, p->nmats};
   return launch_update_any(t, p->mats[0], rv ? p->blk_upv : p->blk_up, c, adam ? mode : 0, first,

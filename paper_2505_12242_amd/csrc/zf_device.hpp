@@ -125,16 +125,6 @@ __device__ __forceinline__ void buf_put_u16(uint16_t v, rsrc_t r, uint32_t voff,
 }
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
-
-template <int AUX = kCached>
-__device__ __forceinline__ u32x2 buf_b64(rsrc_t r, uint32_t voff, uint32_t soff) {
-  return __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, AUX);
-}
-template <int AUX = kCached>
-__device__ __forceinline__ void buf_put_b64(u32x2 v, rsrc_t r, uint32_t voff, uint32_t soff) {
-  __builtin_amdgcn_raw_buffer_store_b64(v, r, voff, soff, AUX);
-}
 
 template <int AUX = kCached>
 __device__ __forceinline__ u32x4 buf_b128(rsrc_t r, uint32_t voff, uint32_t soff) {

@@ -83,7 +83,8 @@ struct DevMat {
   int64_t ld_wcols;
   const float* pend_acc;  // owed deferred update: packed sums under the previous selection
   int64_t ld_pend;
-  uint16_t* acc1;    // channel-major: bf16 first-step stage of the packed buffer (optional)
+  uint16_t* acc1;    // channel-major: bf16 first-step stage of the packed buffer, row j =
+                     // channel j (optional)
   int64_t ld_acc1;
   float* sel_sq;     // Zen-auto: [k] squared norms of the selected channels' gradient
   float* acc_sq;     // Zen-auto: [m-k] squared norms of the accumulated channels
@@ -158,7 +159,10 @@ hipError_t launch_rv_update(const Table& t, const DevMat& one, int64_t blocks, c
                             float scale, hipStream_t s, double* zs = nullptr);
 
 // Channel-major kernels (zf_kernels_cm.hip).
-hipError_t launch_cm_colnorm(const Table& t, const DevMat& one, int64_t blocks, hipStream_t s);
+// stage: also copy every channel's gradient row to its row of acc1 (the
+// bf16 first-step stage), for matrices that have one.
+hipError_t launch_cm_colnorm(const Table& t, const DevMat& one, int64_t blocks, hipStream_t s,
+                             bool stage = false);
 // zs != nullptr: fused Adam + pack that also writes the Zen-auto partials.
 // handover: the last step of an interval with the hand-over fused in (the
 // `out` buffer receives scale * the final sums, +0.0 for selected columns;
@@ -170,6 +174,11 @@ hipError_t launch_cm_update(const Table& t, const DevMat& one, int64_t blocks, c
                             const Pending* pend = nullptr);
 hipError_t launch_cm_unpack(const Table& t, const DevMat& one, int64_t blocks, float scale,
                             hipStream_t s);
+// Adam only over a grid of the selected channels alone (cm_nch blocks per
+// selected channel; table offsets over sum(k * cm_nch)); for plans without
+// a full-state store (nothing to do for the unselected channels).
+hipError_t launch_cm_adam_selected_grid(const Table& t, const DevMat& one, int64_t blocks,
+                                        const AdamK& c, int32_t mode, hipStream_t s);
 
 // Deferred update write-back (zf_kernels_offload.hip): W[:, unsel[u]] =
 // wcols[:, u] in either layout (grid: unpack geometry); skip_prev: columns

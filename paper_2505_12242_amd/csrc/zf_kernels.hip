@@ -308,15 +308,12 @@ __device__ __forceinline__ TileSlots tile_slots(const DevMat& d, int64_t c0) {
 
 // Pack lane: A[i][u] (+)= G[i][j] over the block's rows.  HAND (last step
 // of an interval, fused hand-over): scale * the new sum goes to D[i][j] (rD,
-// vD, sD) and A is not written.  A16 (the bf16 first-step stage, rS/vS/sS):
-// 1 -- the first step stores the gradient's bits there instead of fp32 A;
-// 2 -- the second step reads its previous values from there instead of A.
-template <bool FIRST, bool HAND = false, int A16 = 0>
+// vD, sD) and A is not written.
+template <bool FIRST, bool HAND = false>
 __device__ __forceinline__ void pack_rows(rsrc_t rG, uint32_t vG, uint32_t sG, rsrc_t rA,
                                           uint32_t vA, uint32_t sA, int32_t rows,
                                           rsrc_t rD = rsrc_t(), uint32_t vD = 0, uint32_t sD = 0,
-                                          float scale = 1.0f, rsrc_t rS = rsrc_t(),
-                                          uint32_t vS = 0, uint32_t sS = 0) {
+                                          float scale = 1.0f) {
   int32_t i = 0;
   for (; i + kRowBatch <= rows; i += kRowBatch) {
     uint16_t gb[kRowBatch];
@@ -325,8 +322,7 @@ __device__ __forceinline__ void pack_rows(rsrc_t rG, uint32_t vG, uint32_t sG, r
     for (int b = 0; b < kRowBatch; ++b) gb[b] = buf_u16<ZF_RM_AUX_RO>(rG, vG, (i + b) * sG);
     if constexpr (!FIRST) {
 #pragma unroll
-      for (int b = 0; b < kRowBatch; ++b)
-        a[b] = A16 == 2 ? widen_bf16(buf_u16(rS, vS, (i + b) * sS)) : buf_f32(rA, vA, (i + b) * sA);
+      for (int b = 0; b < kRowBatch; ++b) a[b] = buf_f32(rA, vA, (i + b) * sA);
 #pragma unroll
       for (int b = 0; b < kRowBatch; ++b) a[b] = a[b] + widen_bf16(gb[b]);
     } else {
@@ -336,18 +332,13 @@ __device__ __forceinline__ void pack_rows(rsrc_t rG, uint32_t vG, uint32_t sG, r
 #pragma unroll
     for (int b = 0; b < kRowBatch; ++b) {
       if constexpr (HAND) buf_put_f32(a[b] * scale, rD, vD, (i + b) * sD);
-      else if constexpr (FIRST && A16 == 1) buf_put_u16(gb[b], rS, vS, (i + b) * sS);
       else buf_put_f32(a[b], rA, vA, (i + b) * sA);
     }
   }
   for (; i < rows; ++i) {
-    const uint16_t gb = buf_u16<ZF_RM_AUX_RO>(rG, vG, i * sG);
-    const float g = widen_bf16(gb);
-    float a = g;
-    if constexpr (!FIRST)
-      a = (A16 == 2 ? widen_bf16(buf_u16(rS, vS, i * sS)) : buf_f32(rA, vA, i * sA)) + g;
+    const float g = widen_bf16(buf_u16<ZF_RM_AUX_RO>(rG, vG, i * sG));
+    const float a = FIRST ? g : buf_f32(rA, vA, i * sA) + g;
     if constexpr (HAND) buf_put_f32(a * scale, rD, vD, i * sD);
-    else if constexpr (FIRST && A16 == 1) buf_put_u16(gb, rS, vS, i * sS);
     else buf_put_f32(a, rA, vA, i * sA);
   }
 }
@@ -500,32 +491,14 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const DevMat* __restri
       const uint32_t vG = j * 2u;
       const rsrc_t rA = rows_rsrc(d.acc, i0, i1, d.ld_acc, d.m - d.k);
       const uint32_t sA = static_cast<uint32_t>(d.ld_acc * 4);
-      // the bf16 first-step stage: first == 1 on an interval's first step,
-      // 2 on its second (a matrix without a stage takes 2 as any later step)
-      const bool a16 = d.acc1 != nullptr;
-      const rsrc_t rS = a16 ? rows_rsrc(d.acc1, i0, i1, d.ld_acc1, d.m - d.k) : rA;
-      const uint32_t sS = a16 ? static_cast<uint32_t>(d.ld_acc1 * 2) : 0u;
       if constexpr (HAND) {
         const rsrc_t rD = rows_rsrc(d.out, i0, i1, d.ld_out, d.m);
         const uint32_t sD = static_cast<uint32_t>(d.ld_out * 4);
-        if (first == 1)
-          pack_rows<true, true>(rG, vG, sG, rA, u * 4u, sA, rows, rD, j * 4u, sD, scale);
-        else if (a16 && first == 2)
-          pack_rows<false, true, 2>(rG, vG, sG, rA, u * 4u, sA, rows, rD, j * 4u, sD, scale, rS,
-                                    u * 2u, sS);
+        if (first) pack_rows<true, true>(rG, vG, sG, rA, u * 4u, sA, rows, rD, j * 4u, sD, scale);
         else pack_rows<false, true>(rG, vG, sG, rA, u * 4u, sA, rows, rD, j * 4u, sD, scale);
       } else {
-        if (first == 1) {
-          if (a16)
-            pack_rows<true, false, 1>(rG, vG, sG, rA, u * 4u, sA, rows, rsrc_t(), 0, 0, 1.0f, rS,
-                                      u * 2u, sS);
-          else pack_rows<true>(rG, vG, sG, rA, u * 4u, sA, rows);
-        } else if (a16 && first == 2) {
-          pack_rows<false, false, 2>(rG, vG, sG, rA, u * 4u, sA, rows, rsrc_t(), 0, 0, 1.0f, rS,
-                                     u * 2u, sS);
-        } else {
-          pack_rows<false>(rG, vG, sG, rA, u * 4u, sA, rows);
-        }
+        if (first) pack_rows<true>(rG, vG, sG, rA, u * 4u, sA, rows);
+        else pack_rows<false>(rG, vG, sG, rA, u * 4u, sA, rows);
       }
     }
     return;

@@ -115,7 +115,11 @@ __device__ __forceinline__ void sum_squares8(const float (&f)[kGroup], double& s
 // xor-butterfly across the wave.  Deterministic, no workspace.
 // ---------------------------------------------------------------------------
 
-template <bool BATCHED>
+// STAGE (refresh steps with the bf16 first-step stage): the same pass also
+// copies every channel's gradient row to its row of the stage -- the
+// refresh step's first packed values for whichever channels the selection
+// leaves unselected, so that the step's update only runs the Adam part.
+template <bool BATCHED, bool STAGE>
 __global__ __launch_bounds__(kThreads) void cm_colnorm_kernel(const DevMat* __restrict__ mats,
                                                              const int64_t* __restrict__ off,
                                                              int32_t nmats, DevMat one) {
@@ -126,6 +130,8 @@ __global__ __launch_bounds__(kThreads) void cm_colnorm_kernel(const DevMat* __re
   if (j >= d.m) return;
   const int64_t n = d.n;
   const rsrc_t r = make_rsrc(d.grad + j * d.ld_grad, n * 2);
+  const bool st = STAGE && d.acc1 != nullptr;
+  const rsrc_t rS = st ? make_rsrc(d.acc1 + j * d.ld_acc1, n * 2) : r;
   double a0 = 0.0, a1 = 0.0;
   if (d.vec) {
     constexpr int kStride = 64 * kGroup;  // elements per wave per load
@@ -134,6 +140,11 @@ __global__ __launch_bounds__(kThreads) void cm_colnorm_kernel(const DevMat* __re
       u32x4 v[4];
 #pragma unroll
       for (int b = 0; b < 4; ++b) v[b] = buf_b128<kAuxScore>(r, static_cast<uint32_t>((e + b * kStride) * 2), 0);
+      if (st) {
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+          buf_put_b128<kAuxAFirst>(v[b], rS, static_cast<uint32_t>((e + b * kStride) * 2), 0);
+      }
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
         float f[kGroup];
@@ -147,7 +158,9 @@ __global__ __launch_bounds__(kThreads) void cm_colnorm_kernel(const DevMat* __re
     }
     for (; e < n; e += kStride) {
       float f[kGroup];
-      widen8(buf_b128<kAuxScore>(r, static_cast<uint32_t>(e * 2), 0), f);
+      const u32x4 v = buf_b128<kAuxScore>(r, static_cast<uint32_t>(e * 2), 0);
+      if (st) buf_put_b128<kAuxAFirst>(v, rS, static_cast<uint32_t>(e * 2), 0);
+      widen8(v, f);
 #pragma unroll
       for (int c = 0; c < kGroup; c += 2) {
         a0 = __builtin_fma(static_cast<double>(f[c]), static_cast<double>(f[c]), a0);
@@ -156,7 +169,9 @@ __global__ __launch_bounds__(kThreads) void cm_colnorm_kernel(const DevMat* __re
     }
   } else {
     for (int64_t e = lane; e < n; e += 64) {
-      const double x = static_cast<double>(widen_bf16(buf_u16<kAuxScore>(r, static_cast<uint32_t>(e * 2), 0)));
+      const uint16_t gb = buf_u16<kAuxScore>(r, static_cast<uint32_t>(e * 2), 0);
+      if (st) buf_put_u16<kAuxAFirst>(gb, rS, static_cast<uint32_t>(e * 2), 0);
+      const double x = static_cast<double>(widen_bf16(gb));
       a0 = __builtin_fma(x, x, a0);
     }
   }
@@ -395,30 +410,43 @@ __device__ __forceinline__ void cm_swap_out(const DevMat& d, int64_t j, int64_t 
 // enters the selection takes the owed deferred step pd first (its row of
 // pend_acc is its slot among the previous selection's unselected channels:
 // j minus the previously selected channels below j).
+//
+// SELG (Adam only, no store): the grid covers the selected channels only,
+// block -> (selected slot r, row chunk), channel j = sel_idx[r]; the
+// unselected channels would have nothing to do.
 #ifdef ZF_CM_WAVES_PER_EU
 #define ZF_CM_UPDATE_ATTR __attribute__((amdgpu_waves_per_eu(ZF_CM_WAVES_PER_EU)))
 #else
 #define ZF_CM_UPDATE_ATTR
 #endif
-template <bool BATCHED, bool ADAM, bool PACK, bool STATS, bool HAND, bool PEND>
+template <bool BATCHED, bool ADAM, bool PACK, bool STATS, bool HAND, bool PEND, bool SELG>
 __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(const DevMat* __restrict__ mats,
                                                             const int64_t* __restrict__ off,
                                                             int32_t nmats, DevMat one, AdamK c,
                                                             int32_t mode, int32_t first,
                                                             double* __restrict__ zs, float scale,
                                                             Pending pd) {
+  static_assert(!SELG || (ADAM && !PACK && !STATS && !HAND && !PEND), "selected-only grid");
   int64_t local;
   const DevMat& d = get_mat<BATCHED>(mats, off, nmats, one, local);
   const int64_t chunk = static_cast<int64_t>(d.cm_vpt) * kThreads * kGroup;
-  const int64_t j = local / d.cm_nch;
+  int64_t j, r;
+  bool sel;
+  if constexpr (SELG) {
+    r = local / d.cm_nch;
+    j = static_cast<int64_t>(uniform_i32(d.sel_idx[r]));
+    sel = true;
+  } else {
+    j = local / d.cm_nch;
+    const uint64_t mj = uniform_u64(d.mask[j >> 6]);
+    sel = (mj >> (j & 63)) & 1ull;
+    r = static_cast<int64_t>(uniform_i32(d.prefix[j >> 6])) +
+        __popcll(mj & ((uint64_t(1) << (j & 63)) - 1));
+  }
   const int64_t ci = local % d.cm_nch;
   const int64_t e0 = ci * chunk;
   const int64_t len = min(chunk, d.n - e0);
   const int64_t w = j >> 6;
-  const uint64_t mw = uniform_u64(d.mask[w]);
-  const bool sel = (mw >> (j & 63)) & 1ull;
-  const int64_t r = static_cast<int64_t>(uniform_i32(d.prefix[w])) +
-                    __popcll(mw & ((uint64_t(1) << (j & 63)) - 1));
   const rsrc_t rG = make_rsrc(d.grad + j * d.ld_grad + e0, len * 2);
   double ss = 0.0;
 
@@ -427,10 +455,11 @@ __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(c
     if constexpr (PACK) {
       const int64_t u = j - r;
       const rsrc_t rA = make_rsrc(d.acc + u * d.ld_acc + e0, len * 4);
-      // the bf16 first-step stage: first == 1 on an interval's first step,
-      // 2 on its second (a matrix without a stage takes 2 as any later step)
+      // the bf16 first-step stage (row j, channel-indexed): first == 1 on an
+      // interval's first step, 2 on its second (a matrix without a stage
+      // takes 2 as any later step)
       const bool a16 = d.acc1 != nullptr;
-      const rsrc_t rA16 = a16 ? make_rsrc(d.acc1 + u * d.ld_acc1 + e0, len * 2) : rA;
+      const rsrc_t rA16 = a16 ? make_rsrc(d.acc1 + j * d.ld_acc1 + e0, len * 2) : rA;
       if constexpr (HAND) {
         const rsrc_t rOut = make_rsrc(d.out + j * d.ld_out + e0, len * 4);
         if (d.vec) {
@@ -578,15 +607,23 @@ __global__ __launch_bounds__(kThreads) void cm_unpack_kernel(const DevMat* __res
 
 }  // namespace
 
-hipError_t launch_cm_colnorm(const Table& t, const DevMat& one, int64_t blocks, hipStream_t s) {
+template <bool STAGE>
+static void launch_cm_colnorm_t(const Table& t, const DevMat& one, dim3 grid, hipStream_t s) {
+  if (t.mats != nullptr)
+    hipLaunchKernelGGL((cm_colnorm_kernel<true, STAGE>), grid, dim3(kThreads), 0, s, t.mats, t.off,
+                       t.nmats, one);
+  else
+    hipLaunchKernelGGL((cm_colnorm_kernel<false, STAGE>), grid, dim3(kThreads), 0, s, t.mats,
+                       t.off, t.nmats, one);
+}
+
+hipError_t launch_cm_colnorm(const Table& t, const DevMat& one, int64_t blocks, hipStream_t s,
+                             bool stage) {
   (void)hipGetLastError();
   if (blocks > 0) {
-    if (t.mats != nullptr)
-      hipLaunchKernelGGL((cm_colnorm_kernel<true>), dim3(static_cast<uint32_t>(blocks)),
-                         dim3(kThreads), 0, s, t.mats, t.off, t.nmats, one);
-    else
-      hipLaunchKernelGGL((cm_colnorm_kernel<false>), dim3(static_cast<uint32_t>(blocks)),
-                         dim3(kThreads), 0, s, t.mats, t.off, t.nmats, one);
+    const dim3 grid(static_cast<uint32_t>(blocks));
+    if (stage) launch_cm_colnorm_t<true>(t, one, grid, s);
+    else launch_cm_colnorm_t<false>(t, one, grid, s);
   }
   return hipGetLastError();
 }
@@ -598,18 +635,27 @@ hipError_t launch_cm_colnorm(const Table& t, const DevMat& one, int64_t blocks, 
 #endif
 constexpr unsigned kCmUpdateLds = ZF_CM_UPDATE_LDS;
 
-template <bool ADAM, bool PACK, bool STATS, bool HAND, bool PEND = false>
+template <bool ADAM, bool PACK, bool STATS, bool HAND, bool PEND = false, bool SELG = false>
 static void launch_cm_update_t(const Table& t, const DevMat& one, dim3 grid, const AdamK& c,
                                int32_t mode, int32_t first, double* zs, float scale,
                                hipStream_t s, const Pending& pd = Pending{}) {
   if (t.mats != nullptr)
-    hipLaunchKernelGGL((cm_update_kernel<true, ADAM, PACK, STATS, HAND, PEND>), grid,
+    hipLaunchKernelGGL((cm_update_kernel<true, ADAM, PACK, STATS, HAND, PEND, SELG>), grid,
                        dim3(kThreads), kCmUpdateLds, s, t.mats, t.off, t.nmats, one, c, mode,
                        first, zs, scale, pd);
   else
-    hipLaunchKernelGGL((cm_update_kernel<false, ADAM, PACK, STATS, HAND, PEND>), grid,
+    hipLaunchKernelGGL((cm_update_kernel<false, ADAM, PACK, STATS, HAND, PEND, SELG>), grid,
                        dim3(kThreads), kCmUpdateLds, s, t.mats, t.off, t.nmats, one, c, mode,
                        first, zs, scale, pd);
+}
+
+hipError_t launch_cm_adam_selected_grid(const Table& t, const DevMat& one, int64_t blocks,
+                                        const AdamK& c, int32_t mode, hipStream_t s) {
+  (void)hipGetLastError();
+  if (blocks <= 0) return hipSuccess;
+  launch_cm_update_t<true, false, false, false, false, true>(
+      t, one, dim3(static_cast<uint32_t>(blocks)), c, mode, 0, nullptr, 1.0f, s);
+  return hipGetLastError();
 }
 
 hipError_t launch_cm_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,

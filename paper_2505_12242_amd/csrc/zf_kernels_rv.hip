@@ -32,11 +32,6 @@
 // read and write their sources element by element, runs the per-column
 // kernel.
 //
-// The bf16 first-step stage of the packed buffer (acc1, optional): on an
-// interval's first step (first == 1) the pack lanes store the gradient's
-// bf16 bits there (8 bytes per quad, 2 per edge slot) instead of fp32 A; on
-// its second (first == 2) they read them back from there instead of A.
-//
 // STATS (Zen-auto, blocks of cn_rpb rows): each lane also sums, in fp64 and
 // in row order, the squares of its selected columns' gradient and of its
 // unselected slots' new accumulated values over the block's rows, and
@@ -164,16 +159,9 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
   const uint32_t sG = static_cast<uint32_t>(d.ld_grad * 2);
   rsrc_t rA = rsrc_t(), rP = rsrc_t(), rM = rsrc_t(), rV = rsrc_t(), rW = rsrc_t(), rD = rsrc_t();
   uint32_t sA = 0, sS = 0, sW = 0, sD = 0;
-  rsrc_t rA16 = rsrc_t();
-  uint32_t sA16 = 0;
-  const bool a16 = PACK && d.acc1 != nullptr;
   if constexpr (PACK) {
     rA = rows_rsrc(d.acc, i0, i1, d.ld_acc, d.m - d.k);
     sA = static_cast<uint32_t>(d.ld_acc * 4);
-    if (a16) {
-      rA16 = rows_rsrc(d.acc1, i0, i1, d.ld_acc1, d.m - d.k);
-      sA16 = static_cast<uint32_t>(d.ld_acc1 * 2);
-    }
   }
   if constexpr (ADAM) {
     rP = rows_rsrc(d.P, i0, i1, d.ld_state, d.k);
@@ -193,8 +181,6 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
   const int h = uniform_i32(tid >> 7);  // the same for the 64 lanes of a wave
   const int32_t g8 = (tid & 127) * 8;
   const uint32_t vQ = static_cast<uint32_t>(Q * 16);  // quad byte offset (fp32 slots)
-  const uint32_t vQ16 = static_cast<uint32_t>(Q * 8);  // the same quad in the bf16 stage
-  const uint32_t vE16 = vs[0] / 2;                     // an edge slot in the bf16 stage
   double zq[4] = {0.0, 0.0, 0.0, 0.0};  // STATS: sums of squares per element
 
   for (int32_t i = 0; i < rows; i += kRvBatch) {
@@ -230,26 +216,8 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
     for (int b = 0; b < kRvBatch; ++b)
 #pragma unroll
       for (int e = 0; e < 4; ++e) x0[b][e] = x1[b][e] = x2[b][e] = 0.0f;
-    if (PACK && first != 1) {
-      if (a16 && first == 2) {
-        if (is_q) {
-#pragma unroll
-          for (int b = 0; b < kRvBatch; ++b) {
-            if (b < nb) {
-              const u32x2 w = buf_b64(rA16, vQ16, static_cast<uint32_t>(i + b) * sA16);
-              x0[b][0] = widen_bf16(static_cast<uint16_t>(w.x & 0xffffu));
-              x0[b][1] = widen_bf16(static_cast<uint16_t>(w.x >> 16));
-              x0[b][2] = widen_bf16(static_cast<uint16_t>(w.y & 0xffffu));
-              x0[b][3] = widen_bf16(static_cast<uint16_t>(w.y >> 16));
-            }
-          }
-        } else if (is_e) {
-#pragma unroll
-          for (int b = 0; b < kRvBatch; ++b)
-            if (b < nb)
-              x0[b][0] = widen_bf16(buf_u16(rA16, vE16, static_cast<uint32_t>(i + b) * sA16));
-        }
-      } else if (is_q) {
+    if (PACK && !first) {
+      if (is_q) {
 #pragma unroll
         for (int b = 0; b < kRvBatch; ++b) {
           if (b < nb) {
@@ -301,7 +269,7 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
               const float g = widen_bf16(sg[b][cj[e]]);
-              a[e] = first == 1 ? g : x0[b][e] + g;
+              a[e] = first ? g : x0[b][e] + g;
               if constexpr (STATS) {
                 const double x = static_cast<double>(a[e]);
                 zq[e] = __builtin_fma(x, x, zq[e]);
@@ -311,18 +279,6 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
 #pragma unroll
               for (int e = 0; e < 4; ++e)
                 if ((valid >> e) & 1u) sd[b][cj[e]] = a[e] * scale;
-            } else if (a16 && first == 1) {
-              // the stage keeps the gradient's own bits (the values are exact)
-              const uint32_t so = static_cast<uint32_t>(i + b) * sA16;
-              if (is_q) {
-                const u32x2 w = {static_cast<uint32_t>(sg[b][cj[0]]) |
-                                     (static_cast<uint32_t>(sg[b][cj[1]]) << 16),
-                                 static_cast<uint32_t>(sg[b][cj[2]]) |
-                                     (static_cast<uint32_t>(sg[b][cj[3]]) << 16)};
-                buf_put_b64(w, rA16, vQ16, so);
-              } else {
-                buf_put_u16(sg[b][cj[0]], rA16, vE16, so);
-              }
             } else {
               const uint32_t so = static_cast<uint32_t>(i + b) * sA;
               if (is_q) buf_put_b128(as_u4(a[0], a[1], a[2], a[3]), rA, vQ, so);

@@ -120,8 +120,7 @@ class SelectiveUpdateRunner:
                  device=None, keep_unpacked: bool = True, layout: int = ROW_MAJOR,
                  zen_tau: Optional[float] = None, offload: bool = False, overlap: bool = True,
                  host_threads: Optional[int] = None, fuse_handover: bool = True,
-                 warmup: int = 0, refresh_pending: bool = True,
-                 first_step_stage: Optional[bool] = None):
+                 warmup: int = 0, refresh_pending: bool = True, first_step_stage: bool = True):
         self.device = torch.device(device) if device is not None else torch.device("cuda")
         self.shapes = [(int(n), int(m)) for n, m in shapes]
         self.ratio, self.hp, self.R, self.S = ratio, hp, int(refresh), int(accum)
@@ -133,16 +132,12 @@ class SelectiveUpdateRunner:
         self.refresh_pending = bool(refresh_pending) and self.overlap
         self.keep_unpacked = keep_unpacked and not self.offload
         self.fuse_handover = bool(fuse_handover)
-        # the bf16 first-step stage of the packed buffer, possible with the
-        # fixed schedule and the fused hand-over (the only consumers of the
-        # packed buffer are then the next update passes).  By default
-        # (first_step_stage None) channel-major only: in the row-major layout,
-        # bound by the weight write-back's partial lines, it measured no
-        # faster; True uses it in either layout, False never.
-        possible = (not self.offload and zen_tau is None and self.keep_unpacked
-                    and self.fuse_handover)
-        want = layout != ROW_MAJOR if first_step_stage is None else bool(first_step_stage)
-        self.use_stage = possible and want
+        # the bf16 first-step stage of the packed buffer (channel-major; the
+        # fixed schedule with the fused hand-over, where the only consumers
+        # of the packed buffer are the next update passes).  A refresh step
+        # that starts an interval then fills it from the score pass.
+        self.use_stage = (bool(first_step_stage) and layout != ROW_MAJOR and not self.offload
+                          and zen_tau is None and self.keep_unpacked and self.fuse_handover)
         self._in_stage = False  # the current interval's sums are in the stage
         self.weights = list(weights)
         self.init_master = list(init_master) if init_master is not None else None
@@ -176,7 +171,7 @@ class SelectiveUpdateRunner:
             for a in range(nacc):
                 self.accs[a].append(alloc_stored(layout, n, m - k, f32, dev))
             if self.use_stage:
-                self.stage.append(alloc_stored(layout, n, m - k, torch.bfloat16, dev))
+                self.stage.append(alloc_stored(layout, n, m, torch.bfloat16, dev))
             self.norms.append(torch.empty(m, dtype=f32, device=dev))
             self.unpacked.append(alloc_stored(layout, n, m, f32, dev)
                                  if self.keep_unpacked else None)
@@ -270,11 +265,17 @@ class SelectiveUpdateRunner:
         if self.offload:
             self._before_step(refresh, length, st, rec)
         slot = (t - 1) % len(self.grad_slots)
+        # a refresh that starts an interval with the stage: the score pass
+        # packs every channel into the stage, the update only runs Adam
+        staged = refresh and self.use_stage and self.zen_tau is None and not kind.interval_end
         if refresh:
             nxt = 0 if t == 1 else 1 - self.cur
             plan = self.plans[slot][nxt][self.cur_a]
             with rec("colnorm"):
-                plan.colnorm(st)
+                if staged:
+                    plan.colnorm_stage(st)
+                else:
+                    plan.colnorm(st)
             with rec("topk_select"):
                 plan.topk_select(st)
             mode = STATES_INIT if t == 1 else STATES_REMAP
@@ -296,7 +297,7 @@ class SelectiveUpdateRunner:
                 self._start_held_update(st)
             else:
                 with rec("update_first" if length == 1 else "update"):
-                    plan.update(self.hp, t, mode, length, self.S, stream=st)
+                    plan.update(self.hp, t, mode, length, self.S, pack=not staged, stream=st)
         else:
             if refresh and self._pend is not None:
                 scale_p, th_p = self._pend[:2]
@@ -515,7 +516,9 @@ class SelectiveUpdateRunner:
             for dst, key in zip(self.states[0][q], ("master", "exp_avg", "exp_avg_sq")):
                 dst.copy_(d[key])
             if sd.get("in_stage") and self.use_stage:
-                self.stage[q].copy_(d["acc"])  # first-step values: exact in bf16
+                # first-step values (exact in bf16) into the unselected rows
+                self.stage[q].index_copy_(0, s.unsel_idx.long(),
+                                          d["acc"].to(self.device, torch.bfloat16))
             else:
                 self.accs[0][q].copy_(d["acc"])
             if self.offload:
@@ -532,7 +535,8 @@ class SelectiveUpdateRunner:
         """The current interval's packed sums, fp32 (after an interval's
         first step with the bf16 stage: a widened copy of the stage, exact)."""
         if self._in_stage:
-            return [x.float() for x in self.stage]
+            return [x.index_select(0, s.unsel_idx.long()).float()
+                    for x, s in zip(self.stage, self.sels[self.cur])]
         return self.accs[self.cur_a]
 
     @property

@@ -1,17 +1,20 @@
 """The bf16 first-step stage of the packed buffer (descriptor field
-acc_first), through the C ABI, in both layouts and on the vector and
-element paths:
+acc_first: channel-major, one bf16 row per channel), through the C ABI, on
+the vector and element paths:
 
-* an interval's first step writes the unselected channels' gradient bits to
-  the stage and leaves the fp32 buffer untouched; the second step reads the
-  stage and writes f32(G1) + f32(G2) to the fp32 buffer, equal bit for bit to
-  the oracle's pack_accumulate; the fused hand-over on the second step equals
-  the oracle's unpack;
-* the runner with the stage equals the runner without it bit for bit (W,
-  compact states, packed sums, hand-over) over intervals of 1 to 4 steps,
-  with vector and element paths;
-* a stage overlapping the packed buffer is rejected at plan creation, and
-  the separate hand-over pass on a plan that has one.
+* an interval's first step writes the unselected channels' gradient rows to
+  their rows of the stage and leaves the fp32 buffer and the selected
+  channels' rows untouched; the second step reads the stage and writes
+  f32(G1) + f32(G2) to the fp32 buffer, equal bit for bit to the oracle's
+  pack_accumulate; the fused hand-over on the second step equals the
+  oracle's unpack;
+* zf_plan_colnorm_stage: the scores of zf_plan_colnorm plus every channel's
+  gradient row in the stage; an Adam-only refresh after it, then the second
+  step, equal the plain refresh's results bit for bit;
+* the runner with the stage (its refresh steps through the score pass)
+  equals the runner without it bit for bit over five R/S schedules;
+* rejected: a row-major stage, a stage overlapping the packed buffer, the
+  separate hand-over pass on a staged plan.
 """
 import sys
 
@@ -30,89 +33,127 @@ zf = pytest.importorskip("paper_2505_12242_amd")
 CM = zf.CHANNEL_MAJOR
 
 
-def _buf(layout, rows_l, cols_l, dtype, aligned, fill):
-    """Storage of a logical rows_l x cols_l matrix: 16-byte rows (the vector
-    paths) or an odd offset with unpadded rows (the element paths)."""
-    shape = (rows_l, cols_l) if layout == zf.ROW_MAJOR else (cols_l, rows_l)
+def _buf(rows, cols, dtype, aligned, fill):
+    """[rows][cols] storage: 16-byte rows (the vector paths) or an odd
+    offset with unpadded rows (the element paths)."""
     if aligned:
-        t = zf.alloc_stored(layout, rows_l, cols_l, dtype, "cuda")
+        per = 16 // torch.empty(0, dtype=dtype).element_size()
+        t = torch.empty(rows, max(per, -(-cols // per) * per), dtype=dtype, device="cuda")
+        t = t[:, :cols]
     else:
-        t = torch.empty(shape[0] * shape[1] + 1, dtype=dtype, device="cuda")[1:].view(*shape)
+        t = torch.empty(rows * cols + 1, dtype=dtype, device="cuda")[1:].view(rows, cols)
     t.fill_(fill)
     return t
 
 
-def _logical(t, layout):
-    a = t.cpu()
-    a = a if layout == zf.ROW_MAJOR else a.t()
-    return a.contiguous()
+def _setup(n, m, aligned, ratio=0.1):
+    rng = np.random.default_rng(derive_seed("stage", n, m))
+    k = O.k_from_ratio(ratio, m)
+    sel = O.select_topk(rng.random(m).astype(np.float32), k)
+    g = [grad_bits(n, m, derive_seed("stage-g", n, m, t)) for t in (1, 2)]
+    G = [bf16_dev(np.ascontiguousarray(x.T)) for x in g]
+    return k, sel, g, G
 
 
 @pytest.mark.parametrize("aligned", [True, False])
 @pytest.mark.parametrize("n,m", [(64, 300), (4104, 70), (5, 33), (48, 1000)])
-@pytest.mark.parametrize("layout", [zf.ROW_MAJOR, CM], ids=["rm", "cm"])
-def test_stage_first_and_second_step(layout, n, m, aligned):
-    print(f"# stage layout={layout} n={n} m={m} aligned={aligned}", file=sys.stderr, flush=True)
-    rng = np.random.default_rng(derive_seed("stage", n, m))
-    k = O.k_from_ratio(0.1, m)
-    sel = O.select_topk(rng.random(m).astype(np.float32), k)
+def test_stage_first_and_second_step(n, m, aligned):
+    print(f"# stage n={n} m={m} aligned={aligned}", file=sys.stderr, flush=True)
+    k, sel, (g1, g2), G = _setup(n, m, aligned)
     u = m - k
-    g1 = grad_bits(n, m, derive_seed("stage-g", n, m, 1))
-    g2 = grad_bits(n, m, derive_seed("stage-g", n, m, 2))
-    A = _buf(layout, n, u, torch.float32, aligned, np.nan)
-    stage = _buf(layout, n, u, torch.bfloat16, aligned, 0.0)
-    D = _buf(layout, n, m, torch.float32, True, np.nan)
-    T = (lambda a: a) if layout == zf.ROW_MAJOR else (lambda a: np.ascontiguousarray(a.T))
-    G = [bf16_dev(T(g)) for g in (g1, g2)]
+    A = _buf(u, n, torch.float32, aligned, np.nan)
+    stage = _buf(m, n, torch.bfloat16, aligned, 0.0)
+    D = _buf(m, n, torch.float32, True, np.nan)
 
     def plan(grad, **kw):
         return zf.Plan([zf.MatrixBuffers(grad=grad, k=k, sel=sel_dev(sel), acc=A, unpacked=D,
-                                         layout=layout, acc_first=stage, **kw)])
+                                         layout=CM, acc_first=stage, **kw)])
 
     p1, p2 = plan(G[0]), plan(G[1])
     p1.update(HP, 1, zf.STATES_INPLACE, 1, 4, adam=False, pack=True)
     torch.cuda.synchronize()
     assert torch.isnan(A).all()  # the fp32 buffer is not written on the first step
-    want_stage = np.ascontiguousarray(g1[:, sel.unsel.astype(np.int64)])
-    assert np.array_equal(bits_np(_logical(stage, layout)), want_stage)
+    st = bits_np(stage)
+    uns, sls = sel.unsel.astype(np.int64), sel.sel.astype(np.int64)
+    assert np.array_equal(st[uns], np.ascontiguousarray(g1.T)[uns])
+    assert (st[sls] == 0).all()  # selected channels' rows untouched
     p2.update(HP, 2, zf.STATES_INPLACE, 2, 4, adam=False, pack=True)
     torch.cuda.synchronize()
     A2 = O.pack_accumulate(g2, sel.unsel, O.pack_accumulate(g1, sel.unsel, None, 1), 2)
-    assert same_bits(f32_np(_logical(A, layout)), A2)
+    assert same_bits(np.ascontiguousarray(f32_np(A).T), A2)
     # a two-step interval that ends with the fused hand-over: the stage is read
     A.fill_(np.nan)
     p1.update(HP, 1, zf.STATES_INPLACE, 1, 2, adam=False, pack=True)
-    Pn = _buf(layout, n, k, torch.float32, True, 0.0)
-    Mn, Vn = _buf(layout, n, k, torch.float32, True, 0.0), _buf(layout, n, k, torch.float32,
-                                                                True, 0.0)
-    W = bf16_dev(np.zeros((n, m) if layout == zf.ROW_MAJOR else (m, n), np.uint16))
+    Pn, Mn, Vn = (_buf(k, n, torch.float32, True, 0.0) for _ in range(3))
+    W = bf16_dev(np.zeros((m, n), np.uint16))
     ph = plan(G[1], weight=W, master=Pn, exp_avg=Mn, exp_avg_sq=Vn)
     ph.update_handover(HP, 2, zf.STATES_INPLACE, 2, 2, 0.5)
     torch.cuda.synchronize()
     assert torch.isnan(A).all()  # the hand-over reads the stage, writes neither buffer
-    assert same_bits(f32_np(_logical(D, layout)), O.unpack(A2, sel, 0.5))
+    assert same_bits(np.ascontiguousarray(f32_np(D).T), O.unpack(A2, sel, 0.5))
     for x in (p1, p2, ph):
         x.close()
 
 
+@pytest.mark.parametrize("aligned", [True, False])
+@pytest.mark.parametrize("n,m", [(64, 300), (4104, 70), (5, 33)])
+def test_colnorm_stage_then_adam_only_refresh(n, m, aligned):
+    """The staged refresh (scores + stage in one pass, Adam-only update) and
+    the next step, against the plain refresh (scores, fused update with the
+    packing) and the next step: scores, compact states, W and the second
+    step's sums bit for bit; the stage holds every channel's gradient row."""
+    print(f"# colnorm stage n={n} m={m} aligned={aligned}", file=sys.stderr, flush=True)
+    k, sel, (g1, g2), G = _setup(n, m, aligned)
+    rng = np.random.default_rng(7)
+    W0 = O.bf16_round((rng.standard_normal((n, m)) * 0.02).astype(np.float32))
+    outs = []
+    for staged in (True, False):
+        A = _buf(m - k, n, torch.float32, aligned, np.nan)
+        stage = _buf(m, n, torch.bfloat16, aligned, 0.0) if staged else None
+        norms = torch.full((m,), np.nan, device="cuda")
+        Pn, Mn, Vn = (_buf(k, n, torch.float32, aligned, np.nan) for _ in range(3))
+        W = bf16_dev(np.ascontiguousarray(W0.T))
+        s = zf.Selection(m, k)
+        plans = [zf.Plan([zf.MatrixBuffers(grad=g, k=k, sel=s, weight=W, master=Pn, exp_avg=Mn,
+                                           exp_avg_sq=Vn, acc=A, norms=norms, layout=CM,
+                                           acc_first=stage)]) for g in G]
+        if staged:
+            plans[0].colnorm_stage()
+        else:
+            plans[0].colnorm()
+        plans[0].topk_select()
+        plans[0].update(HP, 1, zf.STATES_INIT, 1, 4, pack=not staged)
+        torch.cuda.synchronize()
+        if staged:
+            assert np.array_equal(bits_np(stage), np.ascontiguousarray(g1.T))
+        plans[1].update(HP, 2, zf.STATES_INPLACE, 2, 4)
+        torch.cuda.synchronize()
+        outs.append([f32_np(norms), s.sel_idx.cpu().numpy(), f32_np(Pn), f32_np(Mn), f32_np(Vn),
+                     bits_np(W), f32_np(A)])
+        for p in plans:
+            p.close()
+    for a, b in zip(*outs):
+        assert np.array_equal(np.ascontiguousarray(a).view(np.uint8),
+                              np.ascontiguousarray(b).view(np.uint8))
+
+
 @pytest.mark.timeout(600)
 @pytest.mark.parametrize("R,S", [(4, 4), (6, 3), (3, 2), (2, 1), (8, 4)])
-@pytest.mark.parametrize("layout", [zf.ROW_MAJOR, CM], ids=["rm", "cm"])
-def test_runner_with_stage_equals_runner_without(layout, R, S):
+def test_runner_with_stage_equals_runner_without(R, S):
     T_ = 10
     dev = torch.device("cuda")
     shapes = [(264, 300), (4104, 70), (43, 77), (16, 3), (40, 1500)]
-    slots, _, w, _ = _inputs(shapes, T_, 37, layout, dev)
+    slots, _, w, _ = _inputs(shapes, T_, 37, CM, dev)
     runs = []
-    for stage in (True, False):  # True: also in the row-major layout
+    for stage in (True, False):
         weights = [x.clone() for x in w]
         runner = zf.SelectiveUpdateRunner(shapes, 0.1, HP, R, S, slots, weights, device=dev,
-                                          layout=layout, first_step_stage=stage)
+                                          layout=CM, first_step_stage=stage)
         assert runner.use_stage == stage
         out = []
         for t in range(1, T_ + 1):
-            print(f"# stage runner layout={layout} R={R} S={S} stage={stage} step {t}",
-                  file=sys.stderr, flush=True)
+            print(f"# stage runner R={R} S={S} stage={stage} step {t}", file=sys.stderr,
+                  flush=True)
             kind = runner.step()
             torch.cuda.synchronize()
             for q in range(len(shapes)):
@@ -134,17 +175,31 @@ def test_plans_that_cannot_use_the_stage_reject_it():
     n, m, k = 8, 64, 6
     rng = np.random.default_rng(3)
     sel = O.select_topk(rng.random(m).astype(np.float32), k)
-    stage_cm = torch.zeros((m - k, n), dtype=torch.bfloat16, device="cuda")
+    # row-major descriptors may not give one
+    with pytest.raises(RuntimeError):
+        zf.Plan([zf.MatrixBuffers(grad=bf16_dev(np.zeros((n, m), np.uint16)), k=k,
+                                  sel=sel_dev(sel), acc=torch.zeros((n, m - k), device="cuda"),
+                                  layout=zf.ROW_MAJOR,
+                                  acc_first=torch.zeros((n, m), dtype=torch.bfloat16,
+                                                        device="cuda"))])
     # overlapping the packed buffer
-    A = torch.zeros((m - k, n), device="cuda")
+    A = torch.zeros((m, n), device="cuda")
     with pytest.raises(RuntimeError):
         zf.Plan([zf.MatrixBuffers(grad=bf16_dev(np.zeros((m, n), np.uint16)), k=k,
-                                  sel=sel_dev(sel), acc=A, layout=CM,
+                                  sel=sel_dev(sel), acc=A[: m - k], layout=CM,
                                   acc_first=A.view(torch.bfloat16)[:, :n])])
     D = torch.zeros((m, n), device="cuda")
+    stage = torch.zeros((m, n), dtype=torch.bfloat16, device="cuda")
     p = zf.Plan([zf.MatrixBuffers(grad=bf16_dev(np.zeros((m, n), np.uint16)), k=k,
-                                  sel=sel_dev(sel), acc=A, unpacked=D, layout=CM,
-                                  acc_first=stage_cm)])
+                                  sel=sel_dev(sel), acc=A[: m - k], unpacked=D, layout=CM,
+                                  acc_first=stage)])
     with pytest.raises(RuntimeError):
         p.unpack(1.0)
     p.close()
+    # colnorm_stage needs a stage
+    q = zf.Plan([zf.MatrixBuffers(grad=bf16_dev(np.zeros((m, n), np.uint16)), k=k,
+                                  sel=sel_dev(sel), norms=torch.zeros(m, device="cuda"),
+                                  layout=CM)])
+    with pytest.raises(RuntimeError):
+        q.colnorm_stage()
+    q.close()
