@@ -1,0 +1,77 @@
+"""The bench's byte model (the algorithmic bytes that GB/s and the roofline
+fraction are computed from), checked on the CPU against hand counts:
+
+* per parameter at 10% on the 4096 x 4096 matrix: refresh + first step
+  2 + 8.2 B, a middle step 11.8 B, an interval end with the fused hand-over
+  10 + 2.8 + 0.4 B;
+* the bf16 first-step stage: refresh + first step 4 + 2.8 B (the score pass
+  writes every channel's stage row, the update runs Adam alone), a plain
+  first step 2.8 + 3.6 B, the second step 2.8 + 7.2 B;
+* the 16-step R = S = 4 schedule of the 7B set: 89.63 GB per step with a
+  separate hand-over pass, 77.50 GB fused, 68.75 GB with the stage.
+"""
+import os
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+bench = pytest.importorskip("bench")
+from workloads.configs import get_workload, shapes as wl_shapes  # noqa: E402
+
+N = M = 4096
+K = 410  # round(0.1 * 4096)
+U = M - K
+
+
+def per_param(**kw):
+    b = bench.step_bytes([(N, M)], [K], **kw)
+    return sum(b.values()) / (N * M)
+
+
+def test_single_matrix_step_types():
+    refresh_first = per_param(refresh=True, first=True, end=False)
+    want = (2 * N * M + 4 * M + 8 * M + 12 * (M // 64) + 28 * N * K + 6 * N * U) / (N * M)
+    assert refresh_first == pytest.approx(want, rel=1e-12)
+    assert per_param(refresh=False, first=False, end=False) == pytest.approx(
+        (28 * N * K + 10 * N * U) / (N * M), rel=1e-12)
+    assert per_param(refresh=False, first=False, end=True, fused_handover=True) == pytest.approx(
+        (28 * N * K + 10 * N * U + 4 * N * K) / (N * M), rel=1e-12)
+    # with the stage
+    staged = per_param(refresh=True, first=True, end=False, stage=True)
+    assert staged == pytest.approx(
+        (4 * N * M + 4 * M + 8 * M + 12 * (M // 64) + 28 * N * K) / (N * M), rel=1e-12)
+    assert per_param(refresh=False, first=True, end=False, stage=True) == pytest.approx(
+        (28 * N * K + 4 * N * U) / (N * M), rel=1e-12)
+    assert per_param(refresh=False, first=False, end=False, second=True, stage=True) == \
+        pytest.approx((28 * N * K + 8 * N * U) / (N * M), rel=1e-12)
+    # a one-step interval hands over at once: the stage changes nothing
+    assert per_param(refresh=True, first=True, end=True, fused_handover=True, stage=True) == \
+        per_param(refresh=True, first=True, end=True, fused_handover=True)
+
+
+def test_7b_schedule_totals():
+    wl = get_workload("llama2-7b-full")
+    shp = wl_shapes(wl.matrices)
+    ks = [int(r) for r in (bench_k(m, wl.ratio) for _, m in shp)]
+    from paper_2505_12242_amd.runner import schedule
+
+    def avg(**kw):
+        tot = 0
+        for t in range(1, 17):
+            kd = schedule(t, 4, 4)
+            tot += sum(bench.step_bytes(shp, ks, kd.refresh, kd.step_in_interval == 1,
+                                        kd.interval_end, second=kd.step_in_interval == 2,
+                                        **kw).values())
+        return tot / 16 / 1e9
+
+    assert avg() == pytest.approx(89.63, abs=0.01)
+    assert avg(fused_handover=True) == pytest.approx(77.50, abs=0.01)
+    assert avg(fused_handover=True, stage=True) == pytest.approx(68.75, abs=0.01)
+
+
+def bench_k(m, ratio):
+    import math
+    return min(m, max(0, math.floor(ratio * m + 0.5)))
