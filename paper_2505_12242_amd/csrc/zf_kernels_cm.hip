@@ -434,7 +434,9 @@ __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(c
   bool sel;
   if constexpr (SELG) {
     r = local / d.cm_nch;
-    j = static_cast<int64_t>(uniform_i32(d.sel_idx[r]));
+    // the channel comes from the caller's selection: kept inside the matrix
+    // whatever it holds, so that every address stays in its buffer
+    j = min(max(static_cast<int64_t>(uniform_i32(d.sel_idx[r])), int64_t(0)), d.m - 1);
     sel = true;
   } else {
     j = local / d.cm_nch;
