@@ -116,16 +116,20 @@ def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool 
              4 (8nu instead of 10nu).  A refresh step that starts an
              interval fills the stage from the score pass instead: colnorm
              2nm + 2nm (every channel's row written), update 28nk (Adam
-             only)
+             only); a refresh step that is a whole (one-step) interval takes
+             its hand-over from the score pass: colnorm 2nm + 4nm, update
+             28nk + 4nk (the selected rows' zeros)
     """
     out = {"colnorm": 0, "topk_select": 0, "update": 0, "unpack": 0}
     for (n, m), k in zip(shapes, ks):
         u = m - k
         staged_refresh = refresh and stage and not end
+        scored_end = refresh and stage and end and first and fused_handover
         if refresh:
-            out["colnorm"] += 2 * n * m + 4 * m + (2 * n * m if staged_refresh else 0)
+            out["colnorm"] += (2 * n * m + 4 * m + (2 * n * m if staged_refresh else 0)
+                               + (4 * n * m if scored_end else 0))
             out["topk_select"] += 8 * m + 12 * ((m + 63) // 64)
-        if staged_refresh:
+        if staged_refresh or scored_end:
             per_u = 0
         elif first:
             per_u = 4 if (stage and not end) else 6

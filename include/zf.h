@@ -428,6 +428,18 @@ zf_status zf_plan_colnorm(zf_plan* plan, zf_stream stream);
  * update).  Needs a plan with a stage (ZF_EINVAL otherwise). */
 zf_status zf_plan_colnorm_stage(zf_plan* plan, zf_stream stream);
 
+/* zf_plan_colnorm that also writes, for every channel, scale times its
+ * widened gradient row to its row of the descriptor's `unpacked` buffer,
+ * in the same pass over G (channel-major plans): on a refresh step that is
+ * a one-step interval (handed over at once), the hand-over of whichever
+ * channels the selection leaves unselected, done before the selection is
+ * known; zf_plan_update_adam_handover then completes the step.  The
+ * results equal those of zf_plan_colnorm followed by
+ * zf_plan_update_handover with step_in_interval 1, bit for bit (4 bytes per
+ * element written for every channel instead of 2 read + 4 written for each
+ * unselected one in the update).  scale finite. */
+zf_status zf_plan_colnorm_handover(zf_plan* plan, float scale, zf_stream stream);
+
 /* zf_topk_select over every matrix, k taken from the descriptors. */
 zf_status zf_plan_topk_select(zf_plan* plan, zf_stream stream);
 
@@ -436,6 +448,14 @@ zf_status zf_plan_topk_select(zf_plan* plan, zf_stream stream);
 zf_status zf_plan_update(zf_plan* plan, const zf_adam_hparams* hp, int64_t step,
                          int32_t mode, int64_t step_in_interval, int64_t accum_interval,
                          int32_t do_adam, int32_t do_pack, zf_stream stream);
+
+/* After zf_plan_colnorm_handover and the selection: the Adam step of the
+ * selected channels (zf_adam_selected, mode as there) and +0.0 in their rows
+ * of `unpacked`; the unselected channels are not touched (their hand-over
+ * rows are already written, the packed buffer is not needed for a one-step
+ * interval).  Channel-major plans without a full-state store. */
+zf_status zf_plan_update_adam_handover(zf_plan* plan, const zf_adam_hparams* hp, int64_t step,
+                                       int32_t mode, zf_stream stream);
 
 /* zf_unpack over every matrix into its `unpacked` buffer. */
 zf_status zf_plan_unpack(zf_plan* plan, float scale, zf_stream stream);

@@ -99,6 +99,9 @@ SIGNATURES = [
     ("zf_plan_colnorm", ctypes.c_int, [c_vp, c_vp]),
     ("zf_plan_topk_select", ctypes.c_int, [c_vp, c_vp]),
     ("zf_plan_colnorm_stage", ctypes.c_int, [c_vp, c_vp]),
+    ("zf_plan_colnorm_handover", ctypes.c_int, [c_vp, c_flt, c_vp]),
+    ("zf_plan_update_adam_handover", ctypes.c_int,
+     [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, c_i32, c_vp]),
     ("zf_plan_update", ctypes.c_int,
      [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, c_i32, c_i64, c_i64, c_i32, c_i32, c_vp]),
     ("zf_plan_unpack", ctypes.c_int, [c_vp, c_flt, c_vp]),
@@ -596,6 +599,19 @@ class Plan:
         """Scores plus every channel's gradient row copied to its row of the
         bf16 first-step stage (zf_plan_colnorm_stage)."""
         _check("zf_plan_colnorm_stage", LIB.zf_plan_colnorm_stage(self._h, _stream(stream)))
+
+    def colnorm_handover(self, scale: float, stream=None) -> None:
+        """Scores plus scale x every channel's widened gradient row in its
+        row of `unpacked` (zf_plan_colnorm_handover)."""
+        _check("zf_plan_colnorm_handover",
+               LIB.zf_plan_colnorm_handover(self._h, float(scale), _stream(stream)))
+
+    def update_adam_handover(self, hp: AdamHparams, step: int, mode: int, stream=None) -> None:
+        """Adam on the selected channels and +0.0 in their hand-over rows
+        (zf_plan_update_adam_handover), after colnorm_handover."""
+        c_hp = hp.as_c()
+        _check("zf_plan_update_adam_handover", LIB.zf_plan_update_adam_handover(
+            self._h, ctypes.byref(c_hp), step, mode, _stream(stream)))
 
     def topk_select(self, stream=None) -> None:
         _check("zf_plan_topk_select", LIB.zf_plan_topk_select(self._h, _stream(stream)))

@@ -750,6 +750,7 @@ struct zf_plan {
        can_pending = true, can_scatter_skip = true;
   bool has_acc1 = false;  // some descriptor gives the bf16 first-step stage
   bool has_store = false;  // some descriptor gives a full-state store
+  bool can_colnorm_out = true;  // scores and the hand-over rows in one pass
 };
 
 namespace {
@@ -820,6 +821,9 @@ zf_status check_plan_matrix(const zf_matrix& x, zf_plan& p) {
                   !overlaps(span(x.weight_cols, ea, x.ld_weight_cols, 2),
                             span(x.weight, eg, x.ld_weight, 2));
   p.can_scatter_skip = p.can_scatter_skip && p.can_scatter && vector_ok(x.src.prev_mask, words, 8);
+  p.can_colnorm_out = p.can_colnorm_out && p.can_colnorm && p.can_handover &&
+                      !overlaps(span_of(x.norms_sq, 1, m, m, 4),
+                                span(x.unpacked, eg, x.ld_unpacked, 4));
   // refresh with the owed deferred update: the store, and the previous
   // interval's sums, read only, disjoint from everything the update writes
   {
@@ -1039,7 +1043,17 @@ zf_status zf_plan_colnorm(zf_plan* p, zf_stream stream) {
 zf_status zf_plan_colnorm_stage(zf_plan* p, zf_stream stream) {
   if (p == nullptr || !p->can_colnorm || !p->has_acc1) return ZF_EINVAL;
   const Table t{p->d_mats, p->d_off_cn, p->nmats};
-  const hipError_t e = zf::launch_cm_colnorm(t, p->mats[0], p->blk_cn, as_stream(stream), true);
+  const hipError_t e = zf::launch_cm_colnorm(t, p->mats[0], p->blk_cn, as_stream(stream), 1);
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
+zf_status zf_plan_colnorm_handover(zf_plan* p, float scale, zf_stream stream) {
+  if (p == nullptr || !p->can_colnorm_out || p->layout != zf::kChannelMajor ||
+      !std::isfinite(scale))
+    return ZF_EINVAL;
+  const Table t{p->d_mats, p->d_off_cn, p->nmats};
+  const hipError_t e =
+      zf::launch_cm_colnorm(t, p->mats[0], p->blk_cn, as_stream(stream), 2, scale);
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
@@ -1101,6 +1115,21 @@ zf_status zf_plan_update(zf_plan* p, const zf_adam_hparams* hp, int64_t step, in
   const hipError_t e = plan_update_launch(p, c, mode, do_pack ? pack_phase(p, step_in_interval) : 0,
                                           do_adam != 0, do_pack != 0, false, 1.0f,
                                           as_stream(stream));
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
+zf_status zf_plan_update_adam_handover(zf_plan* p, const zf_adam_hparams* hp, int64_t step,
+                                       int32_t mode, zf_stream stream) {
+  if (p == nullptr || !p->can_adam || !p->can_handover || p->layout != zf::kChannelMajor ||
+      p->has_store)
+    return ZF_EINVAL;
+  if (!hparams_ok(hp) || step < 1) return ZF_EINVAL;
+  if (mode != zf::kInplace && mode != zf::kRemap && mode != zf::kInit) return ZF_EINVAL;
+  if (mode == zf::kRemap && !p->can_remap) return ZF_EINVAL;
+  const Table ts{p->d_mats, p->d_off_sel, p->nmats};
+  const hipError_t e = zf::launch_cm_adam_selected_grid(ts, p->mats[0], p->blk_sel,
+                                                        adam_consts(*hp, step), mode,
+                                                        as_stream(stream), true);
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 

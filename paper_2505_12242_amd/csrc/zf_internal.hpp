@@ -159,10 +159,12 @@ hipError_t launch_rv_update(const Table& t, const DevMat& one, int64_t blocks, c
                             float scale, hipStream_t s, double* zs = nullptr);
 
 // Channel-major kernels (zf_kernels_cm.hip).
-// stage: also copy every channel's gradient row to its row of acc1 (the
-// bf16 first-step stage), for matrices that have one.
+// out == 1: also copy every channel's gradient row to its row of acc1 (the
+// bf16 first-step stage), for matrices that have one; out == 2: also write
+// scale * every channel's widened gradient row to its row of `out` (the
+// hand-over of a one-step interval).
 hipError_t launch_cm_colnorm(const Table& t, const DevMat& one, int64_t blocks, hipStream_t s,
-                             bool stage = false);
+                             int32_t out = 0, float scale = 1.0f);
 // zs != nullptr: fused Adam + pack that also writes the Zen-auto partials.
 // handover: the last step of an interval with the hand-over fused in (the
 // `out` buffer receives scale * the final sums, +0.0 for selected columns;
@@ -177,8 +179,11 @@ hipError_t launch_cm_unpack(const Table& t, const DevMat& one, int64_t blocks, f
 // Adam only over a grid of the selected channels alone (cm_nch blocks per
 // selected channel; table offsets over sum(k * cm_nch)); for plans without
 // a full-state store (nothing to do for the unselected channels).
+// zero_out: also +0.0 into the selected channels' rows of `out` (after the
+// score pass wrote the hand-over of a one-step interval).
 hipError_t launch_cm_adam_selected_grid(const Table& t, const DevMat& one, int64_t blocks,
-                                        const AdamK& c, int32_t mode, hipStream_t s);
+                                        const AdamK& c, int32_t mode, hipStream_t s,
+                                        bool zero_out = false);
 
 // Deferred update write-back (zf_kernels_offload.hip): W[:, unsel[u]] =
 // wcols[:, u] in either layout (grid: unpack geometry); skip_prev: columns

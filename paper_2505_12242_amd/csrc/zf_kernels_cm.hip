@@ -115,14 +115,19 @@ __device__ __forceinline__ void sum_squares8(const float (&f)[kGroup], double& s
 // xor-butterfly across the wave.  Deterministic, no workspace.
 // ---------------------------------------------------------------------------
 
-// STAGE (refresh steps with the bf16 first-step stage): the same pass also
-// copies every channel's gradient row to its row of the stage -- the
-// refresh step's first packed values for whichever channels the selection
-// leaves unselected, so that the step's update only runs the Adam part.
-template <bool BATCHED, bool STAGE>
+// The same pass may also do the refresh step's packing, before the
+// selection is known, for whichever channels it leaves unselected (the
+// step's update then runs the Adam part alone):
+//   OUT == 1 (an interval starts): every channel's gradient row is copied
+//     to its row of the bf16 first-step stage;
+//   OUT == 2 (a one-step interval, handed over at once): scale times every
+//     channel's widened gradient goes to its row of the hand-over buffer
+//     (the selected rows are set to +0.0 by the update).
+template <bool BATCHED, int OUT>
 __global__ __launch_bounds__(kThreads) void cm_colnorm_kernel(const DevMat* __restrict__ mats,
                                                              const int64_t* __restrict__ off,
-                                                             int32_t nmats, DevMat one) {
+                                                             int32_t nmats, DevMat one,
+                                                             float scale) {
   int64_t local;
   const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, local);
   const int lane = threadIdx.x & 63;
@@ -130,8 +135,9 @@ __global__ __launch_bounds__(kThreads) void cm_colnorm_kernel(const DevMat* __re
   if (j >= d.m) return;
   const int64_t n = d.n;
   const rsrc_t r = make_rsrc(d.grad + j * d.ld_grad, n * 2);
-  const bool st = STAGE && d.acc1 != nullptr;
+  const bool st = OUT == 1 && d.acc1 != nullptr;
   const rsrc_t rS = st ? make_rsrc(d.acc1 + j * d.ld_acc1, n * 2) : r;
+  const rsrc_t rO = OUT == 2 ? make_rsrc(d.out + j * d.ld_out, n * 4) : r;
   double a0 = 0.0, a1 = 0.0;
   if (d.vec) {
     constexpr int kStride = 64 * kGroup;  // elements per wave per load
@@ -154,6 +160,11 @@ __global__ __launch_bounds__(kThreads) void cm_colnorm_kernel(const DevMat* __re
           a0 = __builtin_fma(static_cast<double>(f[c]), static_cast<double>(f[c]), a0);
           a1 = __builtin_fma(static_cast<double>(f[c + 1]), static_cast<double>(f[c + 1]), a1);
         }
+        if constexpr (OUT == 2) {
+#pragma unroll
+          for (int c = 0; c < kGroup; ++c) f[c] = f[c] * scale;
+          f32x8_store<kAuxWO>(rO, static_cast<uint32_t>((e + b * kStride) * 4), f);
+        }
       }
     }
     for (; e < n; e += kStride) {
@@ -166,12 +177,19 @@ __global__ __launch_bounds__(kThreads) void cm_colnorm_kernel(const DevMat* __re
         a0 = __builtin_fma(static_cast<double>(f[c]), static_cast<double>(f[c]), a0);
         a1 = __builtin_fma(static_cast<double>(f[c + 1]), static_cast<double>(f[c + 1]), a1);
       }
+      if constexpr (OUT == 2) {
+#pragma unroll
+        for (int c = 0; c < kGroup; ++c) f[c] = f[c] * scale;
+        f32x8_store<kAuxWO>(rO, static_cast<uint32_t>(e * 4), f);
+      }
     }
   } else {
     for (int64_t e = lane; e < n; e += 64) {
       const uint16_t gb = buf_u16<kAuxScore>(r, static_cast<uint32_t>(e * 2), 0);
       if (st) buf_put_u16<kAuxAFirst>(gb, rS, static_cast<uint32_t>(e * 2), 0);
-      const double x = static_cast<double>(widen_bf16(gb));
+      const float g = widen_bf16(gb);
+      if constexpr (OUT == 2) buf_put_f32<kAuxWO>(g * scale, rO, static_cast<uint32_t>(e * 4), 0);
+      const double x = static_cast<double>(g);
       a0 = __builtin_fma(x, x, a0);
     }
   }
@@ -426,7 +444,7 @@ __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(c
                                                             int32_t mode, int32_t first,
                                                             double* __restrict__ zs, float scale,
                                                             Pending pd) {
-  static_assert(!SELG || (ADAM && !PACK && !STATS && !HAND && !PEND), "selected-only grid");
+  static_assert(!SELG || (ADAM && !PACK && !STATS && !PEND), "selected-only grid");
   int64_t local;
   const DevMat& d = get_mat<BATCHED>(mats, off, nmats, one, local);
   const int64_t chunk = static_cast<int64_t>(d.cm_vpt) * kThreads * kGroup;
@@ -609,23 +627,25 @@ __global__ __launch_bounds__(kThreads) void cm_unpack_kernel(const DevMat* __res
 
 }  // namespace
 
-template <bool STAGE>
-static void launch_cm_colnorm_t(const Table& t, const DevMat& one, dim3 grid, hipStream_t s) {
+template <int OUT>
+static void launch_cm_colnorm_t(const Table& t, const DevMat& one, dim3 grid, float scale,
+                                hipStream_t s) {
   if (t.mats != nullptr)
-    hipLaunchKernelGGL((cm_colnorm_kernel<true, STAGE>), grid, dim3(kThreads), 0, s, t.mats, t.off,
-                       t.nmats, one);
+    hipLaunchKernelGGL((cm_colnorm_kernel<true, OUT>), grid, dim3(kThreads), 0, s, t.mats, t.off,
+                       t.nmats, one, scale);
   else
-    hipLaunchKernelGGL((cm_colnorm_kernel<false, STAGE>), grid, dim3(kThreads), 0, s, t.mats,
-                       t.off, t.nmats, one);
+    hipLaunchKernelGGL((cm_colnorm_kernel<false, OUT>), grid, dim3(kThreads), 0, s, t.mats,
+                       t.off, t.nmats, one, scale);
 }
 
 hipError_t launch_cm_colnorm(const Table& t, const DevMat& one, int64_t blocks, hipStream_t s,
-                             bool stage) {
+                             int32_t out, float scale) {
   (void)hipGetLastError();
   if (blocks > 0) {
     const dim3 grid(static_cast<uint32_t>(blocks));
-    if (stage) launch_cm_colnorm_t<true>(t, one, grid, s);
-    else launch_cm_colnorm_t<false>(t, one, grid, s);
+    if (out == 1) launch_cm_colnorm_t<1>(t, one, grid, scale, s);
+    else if (out == 2) launch_cm_colnorm_t<2>(t, one, grid, scale, s);
+    else launch_cm_colnorm_t<0>(t, one, grid, scale, s);
   }
   return hipGetLastError();
 }
@@ -652,11 +672,17 @@ static void launch_cm_update_t(const Table& t, const DevMat& one, dim3 grid, con
 }
 
 hipError_t launch_cm_adam_selected_grid(const Table& t, const DevMat& one, int64_t blocks,
-                                        const AdamK& c, int32_t mode, hipStream_t s) {
+                                        const AdamK& c, int32_t mode, hipStream_t s,
+                                        bool zero_out) {
   (void)hipGetLastError();
   if (blocks <= 0) return hipSuccess;
-  launch_cm_update_t<true, false, false, false, false, true>(
-      t, one, dim3(static_cast<uint32_t>(blocks)), c, mode, 0, nullptr, 1.0f, s);
+  const dim3 grid(static_cast<uint32_t>(blocks));
+  if (zero_out)
+    launch_cm_update_t<true, false, false, true, false, true>(t, one, grid, c, mode, 0, nullptr,
+                                                              1.0f, s);
+  else
+    launch_cm_update_t<true, false, false, false, false, true>(t, one, grid, c, mode, 0, nullptr,
+                                                               1.0f, s);
   return hipGetLastError();
 }
 

@@ -138,6 +138,8 @@ class SelectiveUpdateRunner:
         # that starts an interval then fills it from the score pass.
         self.use_stage = (bool(first_step_stage) and layout != ROW_MAJOR and not self.offload
                           and zen_tau is None and self.keep_unpacked and self.fuse_handover)
+        # under the same conditions a refresh step that is a one-step
+        # interval takes its hand-over from the score pass as well
         self._in_stage = False  # the current interval's sums are in the stage
         self.weights = list(weights)
         self.init_master = list(init_master) if init_master is not None else None
@@ -265,15 +267,20 @@ class SelectiveUpdateRunner:
         if self.offload:
             self._before_step(refresh, length, st, rec)
         slot = (t - 1) % len(self.grad_slots)
-        # a refresh that starts an interval with the stage: the score pass
-        # packs every channel into the stage, the update only runs Adam
+        # a refresh with the stage: the score pass packs every channel (into
+        # the stage when an interval starts; into the hand-over buffer when
+        # the step is a whole interval) and the update only runs Adam
         staged = refresh and self.use_stage and self.zen_tau is None and not kind.interval_end
+        scored_end = (refresh and self.use_stage and self.zen_tau is None and kind.interval_end
+                      and length == 1)
         if refresh:
             nxt = 0 if t == 1 else 1 - self.cur
             plan = self.plans[slot][nxt][self.cur_a]
             with rec("colnorm"):
                 if staged:
                     plan.colnorm_stage(st)
+                elif scored_end:
+                    plan.colnorm_handover(1.0, st)
                 else:
                     plan.colnorm(st)
             with rec("topk_select"):
@@ -286,6 +293,10 @@ class SelectiveUpdateRunner:
         if self.zen_tau is None:
             end = kind.interval_end
             self._in_stage = self.use_stage and length == 1 and not end
+            if scored_end:
+                with rec("update_handover"):
+                    plan.update_adam_handover(self.hp, t, mode, st)
+                return kind
             if end and self.keep_unpacked and self.fuse_handover:
                 with rec("update_handover"):
                     plan.update_handover(self.hp, t, mode, length, self.S, 1.0 / length, st)

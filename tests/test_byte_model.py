@@ -6,7 +6,8 @@ fraction are computed from), checked on the CPU against hand counts:
   10 + 2.8 + 0.4 B;
 * the bf16 first-step stage: refresh + first step 4 + 2.8 B (the score pass
   writes every channel's stage row, the update runs Adam alone), a plain
-  first step 2.8 + 3.6 B, the second step 2.8 + 7.2 B;
+  first step 2.8 + 3.6 B, the second step 2.8 + 7.2 B; a refresh step that
+  is a whole interval 6 + 3.2 B (the score pass writes the hand-over);
 * the 16-step R = S = 4 schedule of the 7B set: 89.63 GB per step with a
   separate hand-over pass, 77.50 GB fused, 68.75 GB with the stage.
 """
@@ -47,9 +48,13 @@ def test_single_matrix_step_types():
         (28 * N * K + 4 * N * U) / (N * M), rel=1e-12)
     assert per_param(refresh=False, first=False, end=False, second=True, stage=True) == \
         pytest.approx((28 * N * K + 8 * N * U) / (N * M), rel=1e-12)
-    # a one-step interval hands over at once: the stage changes nothing
+    # a refresh step that is a one-step interval: hand-over from the score pass
+    assert per_param(refresh=True, first=True, end=True, fused_handover=True) == pytest.approx(
+        (2 * N * M + 4 * M + 8 * M + 12 * (M // 64) + 28 * N * K + 6 * N * U + 4 * N * K)
+        / (N * M), rel=1e-12)
     assert per_param(refresh=True, first=True, end=True, fused_handover=True, stage=True) == \
-        per_param(refresh=True, first=True, end=True, fused_handover=True)
+        pytest.approx((6 * N * M + 4 * M + 8 * M + 12 * (M // 64) + 28 * N * K + 4 * N * K)
+                      / (N * M), rel=1e-12)
 
 
 def test_7b_schedule_totals():

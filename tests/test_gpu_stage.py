@@ -11,8 +11,11 @@ the vector and element paths:
 * zf_plan_colnorm_stage: the scores of zf_plan_colnorm plus every channel's
   gradient row in the stage; an Adam-only refresh after it, then the second
   step, equal the plain refresh's results bit for bit;
+* zf_plan_colnorm_handover then zf_plan_update_adam_handover (a refresh
+  step that is a one-step interval) equal zf_plan_colnorm then
+  zf_plan_update_handover bit for bit, from an initial and a remapped state;
 * the runner with the stage (its refresh steps through the score pass)
-  equals the runner without it bit for bit over five R/S schedules;
+  equals the runner without it bit for bit over six R/S schedules;
 * rejected: a row-major stage, a stage overlapping the packed buffer, the
   separate hand-over pass on a staged plan.
 """
@@ -137,8 +140,58 @@ def test_colnorm_stage_then_adam_only_refresh(n, m, aligned):
                               np.ascontiguousarray(b).view(np.uint8))
 
 
+@pytest.mark.parametrize("mode", ["init", "remap"])
+@pytest.mark.parametrize("aligned", [True, False])
+@pytest.mark.parametrize("n,m", [(64, 300), (4104, 70), (5, 33)])
+def test_colnorm_handover_then_adam_handover(n, m, aligned, mode):
+    """A refresh step that is a one-step interval, the hand-over taken from
+    the score pass (zf_plan_colnorm_handover, selection, then
+    zf_plan_update_adam_handover), against the plain path (scores,
+    selection, zf_plan_update_handover with step_in_interval 1): scores,
+    selection, compact states, W and the hand-over bit for bit."""
+    print(f"# colnorm handover n={n} m={m} aligned={aligned} {mode}", file=sys.stderr,
+          flush=True)
+    k, sel, (g1, g2), G = _setup(n, m, aligned)
+    rng = np.random.default_rng(11)
+    W0 = O.bf16_round((rng.standard_normal((n, m)) * 0.02).astype(np.float32))
+    prev = O.select_topk(rng.random(m).astype(np.float32), k)
+    P0 = (rng.standard_normal((k, n)) * 0.02).astype(np.float32)
+    outs = []
+    for scored in (True, False):
+        A = _buf(m - k, n, torch.float32, aligned, np.nan)
+        D = _buf(m, n, torch.float32, aligned, np.nan)
+        norms = torch.full((m,), np.nan, device="cuda")
+        Pn, Mn, Vn = (_buf(k, n, torch.float32, aligned, np.nan) for _ in range(3))
+        W = bf16_dev(np.ascontiguousarray(W0.T))
+        s = zf.Selection(m, k)
+        src = None
+        if mode == "remap":
+            Pp = torch.from_numpy(P0).cuda()
+            src = zf.StateSource(prev=sel_dev(prev), prev_master=Pp, prev_exp_avg=Pp * 0.01,
+                                 prev_exp_avg_sq=(Pp * 0.001).abs())
+        plan = zf.Plan([zf.MatrixBuffers(grad=G[0], k=k, sel=s, weight=W, master=Pn,
+                                         exp_avg=Mn, exp_avg_sq=Vn, acc=A, norms=norms,
+                                         unpacked=D, src=src, layout=CM)])
+        md = zf.STATES_INIT if mode == "init" else zf.STATES_REMAP
+        if scored:
+            plan.colnorm_handover(1.0)
+            plan.topk_select()
+            plan.update_adam_handover(HP, 5, md)
+        else:
+            plan.colnorm()
+            plan.topk_select()
+            plan.update_handover(HP, 5, md, 1, 1, 1.0)
+        torch.cuda.synchronize()
+        outs.append([f32_np(norms), s.sel_idx.cpu().numpy(), f32_np(Pn), f32_np(Mn), f32_np(Vn),
+                     bits_np(W), f32_np(D)])
+        plan.close()
+    for a, b in zip(*outs):
+        assert np.array_equal(np.ascontiguousarray(a).view(np.uint8),
+                              np.ascontiguousarray(b).view(np.uint8))
+
+
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("R,S", [(4, 4), (6, 3), (3, 2), (2, 1), (8, 4)])
+@pytest.mark.parametrize("R,S", [(4, 4), (6, 3), (3, 2), (2, 1), (8, 4), (1, 1)])
 def test_runner_with_stage_equals_runner_without(R, S):
     T_ = 10
     dev = torch.device("cuda")
