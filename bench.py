@@ -109,11 +109,13 @@ def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool 
              writes the hand-over instead of A -- the same 10nu (6nu) for the
              unselected part -- plus 4nk zeros at the selected columns; A is
              neither written nor read back
-    stage    with the bf16 first-step stage of A (channel-major, fused
-             hand-over): an interval's first step writes 2 B per unselected
-             element instead of 4 (4nu instead of 6nu; 6nu when it also
-             hands over, as before) and its second step reads 2 B instead of
-             4 (8nu instead of 10nu).  A refresh step that starts an
+    stage    with the bf16 first-step stage of A (channel-major): an
+             interval's first step writes 2 B per unselected element
+             instead of 4 (4nu instead of 6nu; 6nu when it also hands over
+             in the same pass, as before) and its second step reads 2 B
+             instead of 4 (8nu instead of 10nu); a separate hand-over pass
+             after a one-step interval reads the stage (2nu instead of 4nu).
+             With the fused hand-over a refresh step that starts an
              interval fills the stage from the score pass instead: colnorm
              2nm + 2nm (every channel's row written), update 28nk (Adam
              only); a refresh step that is a whole (one-step) interval takes
@@ -123,8 +125,8 @@ def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool 
     out = {"colnorm": 0, "topk_select": 0, "update": 0, "unpack": 0}
     for (n, m), k in zip(shapes, ks):
         u = m - k
-        staged_refresh = refresh and stage and not end
-        scored_end = refresh and stage and end and first and fused_handover
+        staged_refresh = refresh and stage and fused_handover and not end
+        scored_end = refresh and stage and fused_handover and end and first
         if refresh:
             out["colnorm"] += (2 * n * m + 4 * m + (2 * n * m if staged_refresh else 0)
                                + (4 * n * m if scored_end else 0))
@@ -132,7 +134,8 @@ def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool 
         if staged_refresh or scored_end:
             per_u = 0
         elif first:
-            per_u = 4 if (stage and not end) else 6
+            # the fused hand-over of a one-step interval writes no packed values
+            per_u = 4 if (stage and not (end and fused_handover)) else 6
         else:
             per_u = 8 if (stage and second) else 10
         out["update"] += 28 * n * k + per_u * n * u
@@ -142,7 +145,8 @@ def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool 
             elif fused_handover:
                 out["update"] += 4 * n * k
             else:
-                out["unpack"] += 4 * n * u + 4 * n * m
+                # the separate pass reads the stage after a one-step interval
+                out["unpack"] += (2 if (stage and first) else 4) * n * u + 4 * n * m
     return out
 
 

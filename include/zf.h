@@ -398,10 +398,12 @@ typedef struct zf_plan zf_plan;
  * from the second step on, the hand-over, W, the states) is bit-identical
  * to a plan without it.  acc_first must be 2-byte aligned (16-byte aligned
  * with ld % 8 == 0 for the vector path) and overlap no other buffer; a
- * row-major descriptor must leave it NULL (ZF_EINVAL at plan creation).  A
- * plan with a stage rejects zf_plan_unpack, zf_plan_update_zen(_pending) and
- * zf_plan_update_pending (ZF_EINVAL): after a first step they would need
- * the stage. */
+ * row-major descriptor must leave it NULL (ZF_EINVAL at plan creation).
+ * zf_plan_update_zen follows the same rule.  The separate hand-over of an
+ * interval that ended after its first step reads the stage:
+ * zf_plan_unpack_first instead of zf_plan_unpack.  The offloaded
+ * optimizer's calls (zf_plan_update_pending, zf_plan_update_zen_pending)
+ * reject a plan with a stage (ZF_EINVAL). */
 
 /* Validates nmats >= 1 descriptors (HOST array, copied), computes the launch
  * geometry and allocates the plan's device tables and column-score
@@ -456,6 +458,12 @@ zf_status zf_plan_update(zf_plan* plan, const zf_adam_hparams* hp, int64_t step,
  * interval).  Channel-major plans without a full-state store. */
 zf_status zf_plan_update_adam_handover(zf_plan* plan, const zf_adam_hparams* hp, int64_t step,
                                        int32_t mode, zf_stream stream);
+
+/* zf_plan_unpack for an interval that ended after its first step on a plan
+ * whose every descriptor gives acc_first: the unselected channels' rows
+ * are scale times their widened stage rows (the first step's values),
+ * selected rows +0.0.  ZF_EINVAL when a descriptor has no stage. */
+zf_status zf_plan_unpack_first(zf_plan* plan, float scale, zf_stream stream);
 
 /* zf_unpack over every matrix into its `unpacked` buffer. */
 zf_status zf_plan_unpack(zf_plan* plan, float scale, zf_stream stream);

@@ -99,6 +99,7 @@ SIGNATURES = [
     ("zf_plan_colnorm", ctypes.c_int, [c_vp, c_vp]),
     ("zf_plan_topk_select", ctypes.c_int, [c_vp, c_vp]),
     ("zf_plan_colnorm_stage", ctypes.c_int, [c_vp, c_vp]),
+    ("zf_plan_unpack_first", ctypes.c_int, [c_vp, c_flt, c_vp]),
     ("zf_plan_colnorm_handover", ctypes.c_int, [c_vp, c_flt, c_vp]),
     ("zf_plan_update_adam_handover", ctypes.c_int,
      [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, c_i32, c_vp]),
@@ -625,6 +626,12 @@ class Plan:
 
     def unpack(self, scale: float, stream=None) -> None:
         _check("zf_plan_unpack", LIB.zf_plan_unpack(self._h, float(scale), _stream(stream)))
+
+    def unpack_first(self, scale: float, stream=None) -> None:
+        """The hand-over of a one-step interval from the bf16 stage
+        (zf_plan_unpack_first)."""
+        _check("zf_plan_unpack_first",
+               LIB.zf_plan_unpack_first(self._h, float(scale), _stream(stream)))
 
     def update_handover(self, hp: AdamHparams, step: int, mode: int, step_in_interval: int,
                         accum_interval: int, scale: float, stream=None) -> None:

@@ -749,6 +749,7 @@ struct zf_plan {
        can_unpack = true, can_zen = true, can_scatter = true, can_handover = true,
        can_pending = true, can_scatter_skip = true;
   bool has_acc1 = false;  // some descriptor gives the bf16 first-step stage
+  bool all_acc1 = true;   // every descriptor does
   bool has_store = false;  // some descriptor gives a full-state store
   bool can_colnorm_out = true;  // scores and the hand-over rows in one pass
 };
@@ -866,6 +867,8 @@ zf_status check_plan_matrix(const zf_matrix& x, zf_plan& p) {
         overlaps(st, span(x.unpacked, eg, x.ld_unpacked, 4)) || store_overlaps(d, st))
       return ZF_EINVAL;
     p.has_acc1 = true;
+  } else {
+    p.all_acc1 = false;
   }
   // Strides must be valid whenever the buffer is given.
   if (x.weight && !mat_ok(x.weight, eg, x.ld_weight, 2)) return ZF_EINVAL;
@@ -1133,8 +1136,16 @@ zf_status zf_plan_update_adam_handover(zf_plan* p, const zf_adam_hparams* hp, in
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
+zf_status zf_plan_unpack_first(zf_plan* p, float scale, zf_stream stream) {
+  if (p == nullptr || !p->can_unpack || !p->all_acc1) return ZF_EINVAL;
+  const Table t{p->d_mats, p->d_off_unp, p->nmats};
+  const hipError_t e =
+      zf::launch_cm_unpack(t, p->mats[0], p->blk_unp, scale, as_stream(stream), true);
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
 zf_status zf_plan_unpack(zf_plan* p, float scale, zf_stream stream) {
-  if (p == nullptr || !p->can_unpack || p->has_acc1) return ZF_EINVAL;
+  if (p == nullptr || !p->can_unpack) return ZF_EINVAL;
   const Table t{p->d_mats, p->d_off_unp, p->nmats};
   const hipError_t e =
       launch_unpack_any(t, p->mats[0], p->blk_unp, scale, p->layout, as_stream(stream));
@@ -1234,8 +1245,7 @@ zf_status plan_update_zen(zf_plan* p, const AdamK& c, int32_t mode, int32_t firs
 bool zen_args_ok(const zf_plan* p, const zf_adam_hparams* hp, int64_t step, double tau,
                  const zf_zen_totals* totals) {
   static_assert(sizeof(zf_zen_totals) == sizeof(zf::ZenTotals), "zen totals layout");
-  return p != nullptr && !p->has_acc1 && p->can_zen && p->can_adam && p->can_pack &&
-         hparams_ok(hp) &&
+  return p != nullptr && p->can_zen && p->can_adam && p->can_pack && hparams_ok(hp) &&
          step >= 1 && tau >= 0.0 && totals != nullptr && aligned(totals, 8);
 }
 
@@ -1251,14 +1261,14 @@ zf_status zf_plan_update_zen(zf_plan* p, const zf_adam_hparams* hp, int64_t step
   if (mode == zf::kRemap && !p->can_remap) return ZF_EINVAL;
   if (accum_interval < 1 || step_in_interval < 1 || step_in_interval > accum_interval)
     return ZF_EINVAL;
-  return plan_update_zen(p, adam_consts(*hp, step), mode, step_in_interval == 1 ? 1 : 0, tau,
+  return plan_update_zen(p, adam_consts(*hp, step), mode, pack_phase(p, step_in_interval), tau,
                          totals, as_stream(stream), nullptr);
 }
 
 zf_status zf_plan_update_zen_pending(zf_plan* p, const zf_adam_hparams* hp, int64_t step,
                                      int64_t accum_interval, int64_t pend_step, float pend_scale,
                                      double tau, zf_zen_totals* totals, zf_stream stream) {
-  if (!zen_args_ok(p, hp, step, tau, totals) || !p->can_remap || !p->can_pending)
+  if (!zen_args_ok(p, hp, step, tau, totals) || !p->can_remap || !p->can_pending || p->has_acc1)
     return ZF_EINVAL;
   if (pend_step < 1 || !std::isfinite(pend_scale) || accum_interval < 1) return ZF_EINVAL;
   const zf::Pending pd{adam_consts(*hp, pend_step), pend_scale};

@@ -174,8 +174,10 @@ hipError_t launch_cm_update(const Table& t, const DevMat& one, int64_t blocks, c
                             int32_t mode, int32_t first, bool adam, bool pack, double* zs,
                             bool handover, float scale, hipStream_t s,
                             const Pending* pend = nullptr);
+// from_stage: the source is the bf16 first-step stage (a one-step interval;
+// every matrix of the table has one).
 hipError_t launch_cm_unpack(const Table& t, const DevMat& one, int64_t blocks, float scale,
-                            hipStream_t s);
+                            hipStream_t s, bool from_stage = false);
 // Adam only over a grid of the selected channels alone (cm_nch blocks per
 // selected channel; table offsets over sum(k * cm_nch)); for plans without
 // a full-state store (nothing to do for the unselected channels).

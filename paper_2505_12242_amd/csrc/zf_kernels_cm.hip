@@ -575,10 +575,11 @@ __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(c
 
 // ---------------------------------------------------------------------------
 // a6: hand-over.  Channel j of the dense buffer is +0.0 when selected, else
-// scale times its packed row.
+// scale times its packed row -- or, STAGE (a one-step interval on a plan with
+// the bf16 first-step stage), scale times its widened row of the stage.
 // ---------------------------------------------------------------------------
 
-template <bool BATCHED>
+template <bool BATCHED, bool STAGE>
 __global__ __launch_bounds__(kThreads) void cm_unpack_kernel(const DevMat* __restrict__ mats,
                                                             const int64_t* __restrict__ off,
                                                             int32_t nmats, DevMat one,
@@ -607,10 +608,14 @@ __global__ __launch_bounds__(kThreads) void cm_unpack_kernel(const DevMat* __res
   const int64_t u = j - (static_cast<int64_t>(uniform_i32(d.prefix[w])) +
                          __popcll(mw & ((uint64_t(1) << (j & 63)) - 1)));
   const rsrc_t rA = make_rsrc(d.acc + u * d.ld_acc + e0, len * 4);
+  const rsrc_t rS = STAGE ? make_rsrc(d.acc1 + j * d.ld_acc1 + e0, len * 2) : rA;
   if (d.vec) {
     float a[kCmUnpackVpt][kGroup];
 #pragma unroll
-    for (int q = 0; q < kCmUnpackVpt; ++q) f32x8_load<kAuxRO>(rA, group_elem(q, tid) * 4, a[q]);
+    for (int q = 0; q < kCmUnpackVpt; ++q) {
+      if constexpr (STAGE) widen8(buf_b128<kAuxRO>(rS, group_elem(q, tid) * 2, 0), a[q]);
+      else f32x8_load<kAuxRO>(rA, group_elem(q, tid) * 4, a[q]);
+    }
 #pragma unroll
     for (int q = 0; q < kCmUnpackVpt; ++q) {
 #pragma unroll
@@ -620,7 +625,9 @@ __global__ __launch_bounds__(kThreads) void cm_unpack_kernel(const DevMat* __res
   } else {
     for (int64_t e = tid; e < len; e += kThreads) {
       const uint32_t o = static_cast<uint32_t>(e) * 4;
-      buf_put_f32<kAuxWO>(buf_f32<kAuxRO>(rA, o, 0) * scale, rD, o, 0);
+      const float a = STAGE ? widen_bf16(buf_u16<kAuxRO>(rS, static_cast<uint32_t>(e) * 2, 0))
+                            : buf_f32<kAuxRO>(rA, o, 0);
+      buf_put_f32<kAuxWO>(a * scale, rD, o, 0);
     }
   }
 }
@@ -716,16 +723,24 @@ hipError_t launch_cm_update(const Table& t, const DevMat& one, int64_t blocks, c
   return hipGetLastError();
 }
 
+template <bool STAGE>
+static void launch_cm_unpack_t(const Table& t, const DevMat& one, dim3 grid, float scale,
+                               hipStream_t s) {
+  if (t.mats != nullptr)
+    hipLaunchKernelGGL((cm_unpack_kernel<true, STAGE>), grid, dim3(kThreads), 0, s, t.mats, t.off,
+                       t.nmats, one, scale);
+  else
+    hipLaunchKernelGGL((cm_unpack_kernel<false, STAGE>), grid, dim3(kThreads), 0, s, t.mats,
+                       t.off, t.nmats, one, scale);
+}
+
 hipError_t launch_cm_unpack(const Table& t, const DevMat& one, int64_t blocks, float scale,
-                            hipStream_t s) {
+                            hipStream_t s, bool from_stage) {
   (void)hipGetLastError();
   if (blocks > 0) {
-    if (t.mats != nullptr)
-      hipLaunchKernelGGL((cm_unpack_kernel<true>), dim3(static_cast<uint32_t>(blocks)),
-                         dim3(kThreads), 0, s, t.mats, t.off, t.nmats, one, scale);
-    else
-      hipLaunchKernelGGL((cm_unpack_kernel<false>), dim3(static_cast<uint32_t>(blocks)),
-                         dim3(kThreads), 0, s, t.mats, t.off, t.nmats, one, scale);
+    const dim3 grid(static_cast<uint32_t>(blocks));
+    if (from_stage) launch_cm_unpack_t<true>(t, one, grid, scale, s);
+    else launch_cm_unpack_t<false>(t, one, grid, scale, s);
   }
   return hipGetLastError();
 }

@@ -137,9 +137,11 @@ class SelectiveUpdateRunner:
         # of the packed buffer are the next update passes).  A refresh step
         # that starts an interval then fills it from the score pass.
         self.use_stage = (bool(first_step_stage) and layout != ROW_MAJOR and not self.offload
-                          and zen_tau is None and self.keep_unpacked and self.fuse_handover)
-        # under the same conditions a refresh step that is a one-step
-        # interval takes its hand-over from the score pass as well
+                          and self.keep_unpacked)
+        # with the fixed schedule and the fused hand-over a refresh step also
+        # packs from the score pass: into the stage when an interval starts,
+        # into the hand-over buffer when the step is a whole interval
+        self.score_pack = self.use_stage and zen_tau is None and self.fuse_handover
         self._in_stage = False  # the current interval's sums are in the stage
         self.weights = list(weights)
         self.init_master = list(init_master) if init_master is not None else None
@@ -270,9 +272,8 @@ class SelectiveUpdateRunner:
         # a refresh with the stage: the score pass packs every channel (into
         # the stage when an interval starts; into the hand-over buffer when
         # the step is a whole interval) and the update only runs Adam
-        staged = refresh and self.use_stage and self.zen_tau is None and not kind.interval_end
-        scored_end = (refresh and self.use_stage and self.zen_tau is None and kind.interval_end
-                      and length == 1)
+        staged = refresh and self.score_pack and not kind.interval_end
+        scored_end = refresh and self.score_pack and kind.interval_end and length == 1
         if refresh:
             nxt = 0 if t == 1 else 1 - self.cur
             plan = self.plans[slot][nxt][self.cur_a]
@@ -292,7 +293,10 @@ class SelectiveUpdateRunner:
             mode = STATES_INPLACE
         if self.zen_tau is None:
             end = kind.interval_end
-            self._in_stage = self.use_stage and length == 1 and not end
+            # an interval's first packed values sit in the stage, unless the
+            # step handed over in the same pass (nothing packed then)
+            self._in_stage = (self.use_stage and length == 1
+                              and not (end and self.fuse_handover))
             if scored_end:
                 with rec("update_handover"):
                     plan.update_adam_handover(self.hp, t, mode, st)
@@ -327,13 +331,17 @@ class SelectiveUpdateRunner:
             end = (self.last_totals.trigger or length >= self.S or t % self.R == 0
                    or t <= self.warmup)
             self._ended = end
+            self._in_stage = self.use_stage and length == 1
             kind = StepKind(refresh=refresh, step_in_interval=length, interval_end=end)
         if end:
             if self.offload:
                 self._hand_over(length, st, rec)
             elif self.keep_unpacked:
                 with rec("unpack"):
-                    plan.unpack(1.0 / length, st)
+                    if self.use_stage and length == 1:
+                        plan.unpack_first(1.0, st)  # the sums are the stage's values
+                    else:
+                        plan.unpack(1.0 / length, st)
         return kind
 
     # --------------------------------------------------- offloaded optimizer
@@ -543,8 +551,8 @@ class SelectiveUpdateRunner:
 
     @property
     def acc(self) -> List[torch.Tensor]:
-        """The current interval's packed sums, fp32 (after an interval's
-        first step with the bf16 stage: a widened copy of the stage, exact)."""
+        """The last interval's packed sums, fp32 (after an interval's first
+        step with the bf16 stage: a widened copy of the stage, exact)."""
         if self._in_stage:
             return [x.index_select(0, s.unsel_idx.long()).float()
                     for x, s in zip(self.stage, self.sels[self.cur])]

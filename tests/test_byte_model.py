@@ -41,13 +41,20 @@ def test_single_matrix_step_types():
     assert per_param(refresh=False, first=False, end=True, fused_handover=True) == pytest.approx(
         (28 * N * K + 10 * N * U + 4 * N * K) / (N * M), rel=1e-12)
     # with the stage
-    staged = per_param(refresh=True, first=True, end=False, stage=True)
+    staged = per_param(refresh=True, first=True, end=False, stage=True, fused_handover=True)
     assert staged == pytest.approx(
         (4 * N * M + 4 * M + 8 * M + 12 * (M // 64) + 28 * N * K) / (N * M), rel=1e-12)
     assert per_param(refresh=False, first=True, end=False, stage=True) == pytest.approx(
         (28 * N * K + 4 * N * U) / (N * M), rel=1e-12)
     assert per_param(refresh=False, first=False, end=False, second=True, stage=True) == \
         pytest.approx((28 * N * K + 8 * N * U) / (N * M), rel=1e-12)
+    # the stage with a separate hand-over pass (Zen-auto): the refresh packs
+    # into the stage in the update, a one-step interval's pass reads it
+    assert per_param(refresh=True, first=True, end=False, stage=True) == pytest.approx(
+        (2 * N * M + 4 * M + 8 * M + 12 * (M // 64) + 28 * N * K + 4 * N * U) / (N * M),
+        rel=1e-12)
+    assert per_param(refresh=False, first=True, end=True, stage=True) == pytest.approx(
+        (28 * N * K + 4 * N * U + 2 * N * U + 4 * N * M) / (N * M), rel=1e-12)
     # a refresh step that is a one-step interval: hand-over from the score pass
     assert per_param(refresh=True, first=True, end=True, fused_handover=True) == pytest.approx(
         (2 * N * M + 4 * M + 8 * M + 12 * (M // 64) + 28 * N * K + 6 * N * U + 4 * N * K)

@@ -16,8 +16,11 @@ the vector and element paths:
   zf_plan_update_handover bit for bit, from an initial and a remapped state;
 * the runner with the stage (its refresh steps through the score pass)
   equals the runner without it bit for bit over six R/S schedules;
-* rejected: a row-major stage, a stage overlapping the packed buffer, the
-  separate hand-over pass on a staged plan.
+* Zen-auto and the separate hand-over pass with the stage equal the same
+  runs without it (one-step intervals hand over from the stage,
+  zf_plan_unpack_first);
+* rejected: a row-major stage, a stage overlapping the packed buffer,
+  colnorm_stage and unpack_first without a stage.
 """
 import sys
 
@@ -241,14 +244,6 @@ def test_plans_that_cannot_use_the_stage_reject_it():
         zf.Plan([zf.MatrixBuffers(grad=bf16_dev(np.zeros((m, n), np.uint16)), k=k,
                                   sel=sel_dev(sel), acc=A[: m - k], layout=CM,
                                   acc_first=A.view(torch.bfloat16)[:, :n])])
-    D = torch.zeros((m, n), device="cuda")
-    stage = torch.zeros((m, n), dtype=torch.bfloat16, device="cuda")
-    p = zf.Plan([zf.MatrixBuffers(grad=bf16_dev(np.zeros((m, n), np.uint16)), k=k,
-                                  sel=sel_dev(sel), acc=A[: m - k], unpacked=D, layout=CM,
-                                  acc_first=stage)])
-    with pytest.raises(RuntimeError):
-        p.unpack(1.0)
-    p.close()
     # colnorm_stage needs a stage
     q = zf.Plan([zf.MatrixBuffers(grad=bf16_dev(np.zeros((m, n), np.uint16)), k=k,
                                   sel=sel_dev(sel), norms=torch.zeros(m, device="cuda"),
@@ -256,3 +251,96 @@ def test_plans_that_cannot_use_the_stage_reject_it():
     with pytest.raises(RuntimeError):
         q.colnorm_stage()
     q.close()
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("tau", [0.05, 0.8, float("inf")])
+def test_zen_auto_with_stage_equals_without(tau):
+    """Zen-auto (statistics fused into the update, separate hand-over pass)
+    with the bf16 stage against the same runs without it: interval ends,
+    totals, compact states, W, the packed sums and every hand-over bit for
+    bit; a small tau ends intervals after one step (the hand-over then reads
+    the stage, zf_plan_unpack_first)."""
+    T_, R, S = 12, 4, 4
+    dev = torch.device("cuda")
+    shapes = [(264, 300), (4104, 70), (43, 77), (40, 1500)]
+    slots, _, w, _ = _inputs(shapes, T_, 41, CM, dev)
+    runs, ends = [], []
+    for stage in (True, False):
+        weights = [x.clone() for x in w]
+        runner = zf.SelectiveUpdateRunner(shapes, 0.1, HP, R, S, slots, weights, device=dev,
+                                          layout=CM, zen_tau=tau, first_step_stage=stage)
+        assert runner.use_stage == stage and not runner.score_pack
+        out, e = [], []
+        for t in range(1, T_ + 1):
+            print(f"# zen stage tau={tau} stage={stage} step {t}", file=sys.stderr, flush=True)
+            kind = runner.step()
+            e.append((kind.step_in_interval, kind.interval_end, runner.last_totals.sum_acc,
+                      runner.last_totals.sum_sel))
+            for q in range(len(shapes)):
+                out.append(bits_np(runner.weights[q]))
+                out.extend(f32_np(x) for x in runner.state[q])
+                out.append(f32_np(runner.unpacked[q]) if kind.interval_end
+                           else f32_np(runner.acc[q]))
+        runs.append(out)
+        ends.append(e)
+        runner.close()
+    assert ends[0] == ends[1]
+    if tau == 0.05:
+        assert any(sii == 1 and end for sii, end, _, _ in ends[0][1:])  # one-step intervals
+    for i, (a, b) in enumerate(zip(*runs)):
+        assert a.shape == b.shape and np.array_equal(np.ascontiguousarray(a).view(np.uint8),
+                                                     np.ascontiguousarray(b).view(np.uint8)), i
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("R,S", [(4, 4), (2, 1), (6, 3)])
+def test_separate_handover_with_stage_equals_without(R, S):
+    """The fixed schedule with the separate hand-over pass: with the stage,
+    one-step intervals hand over from it (zf_plan_unpack_first)."""
+    T_ = 9
+    dev = torch.device("cuda")
+    shapes = [(264, 300), (43, 77), (16, 3)]
+    slots, _, w, _ = _inputs(shapes, T_, 43, CM, dev)
+    runs = []
+    for stage in (True, False):
+        weights = [x.clone() for x in w]
+        runner = zf.SelectiveUpdateRunner(shapes, 0.1, HP, R, S, slots, weights, device=dev,
+                                          layout=CM, fuse_handover=False, first_step_stage=stage)
+        out = []
+        for t in range(1, T_ + 1):
+            kind = runner.step()
+            torch.cuda.synchronize()
+            for q in range(len(shapes)):
+                out.append(bits_np(runner.weights[q]))
+                out.extend(f32_np(x) for x in runner.state[q])
+                out.append(f32_np(runner.unpacked[q]) if kind.interval_end
+                           else f32_np(runner.acc[q]))
+        runs.append(out)
+        runner.close()
+    for i, (a, b) in enumerate(zip(*runs)):
+        assert a.shape == b.shape and np.array_equal(np.ascontiguousarray(a).view(np.uint8),
+                                                     np.ascontiguousarray(b).view(np.uint8)), i
+
+
+@pytest.mark.parametrize("aligned", [True, False])
+def test_unpack_first_reads_the_stage(aligned):
+    n, m = 40, 300
+    k, sel, (g1, _), G = _setup(n, m, aligned)
+    A = _buf(m - k, n, torch.float32, aligned, np.nan)
+    stage = _buf(m, n, torch.bfloat16, aligned, 0.0)
+    D = _buf(m, n, torch.float32, aligned, np.nan)
+    plan = zf.Plan([zf.MatrixBuffers(grad=G[0], k=k, sel=sel_dev(sel), acc=A, unpacked=D,
+                                     layout=CM, acc_first=stage)])
+    plan.update(HP, 1, zf.STATES_INPLACE, 1, 4, adam=False, pack=True)
+    plan.unpack_first(0.25)
+    torch.cuda.synchronize()
+    want = O.unpack(O.pack_accumulate(g1, sel.unsel, None, 1), sel, 0.25)
+    assert same_bits(np.ascontiguousarray(f32_np(D).T), want)
+    plan.close()
+    # a plan without a stage has nothing to read
+    p2 = zf.Plan([zf.MatrixBuffers(grad=G[0], k=k, sel=sel_dev(sel), acc=A, unpacked=D,
+                                   layout=CM)])
+    with pytest.raises(RuntimeError):
+        p2.unpack_first(1.0)
+    p2.close()
