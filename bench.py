@@ -65,9 +65,8 @@ def parse_args(argv=None):
     ap.add_argument("--no-overlap", action="store_true",
                     help="with --offload: run the deferred update synchronously")
     ap.add_argument("--no-first-step-stage", action="store_true",
-                    help="keep an interval's first packed values in fp32 (default in the "
-                         "channel-major layout with the fused hand-over: a bf16 stage, 2 B per "
-                         "value written and read)")
+                    help="keep an interval's first packed values in fp32 (default: a bf16 "
+                         "stage, 2 B per value written and read)")
     ap.add_argument("--refresh-waits", action="store_true",
                     help="with --offload: a refresh right after an interval end waits for the "
                          "host update (default: the device takes over the entering columns)")
@@ -93,7 +92,8 @@ def parse_args(argv=None):
 # ---------------------------------------------------------------------------
 
 def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool = False,
-               fused_handover: bool = False, second: bool = False, stage: bool = False) -> dict:
+               fused_handover: bool = False, second: bool = False, stage: bool = False,
+               scored_handover: bool = None) -> dict:
     """Algorithmic HBM bytes of one step, by kernel.
 
     colnorm  2nm (read G) + 4m (write scores)          refresh steps
@@ -119,14 +119,17 @@ def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool 
              interval fills the stage from the score pass instead: colnorm
              2nm + 2nm (every channel's row written), update 28nk (Adam
              only); a refresh step that is a whole (one-step) interval takes
-             its hand-over from the score pass: colnorm 2nm + 4nm, update
+             its hand-over from the score pass (scored_handover, channel-
+             major; default: with the stage): colnorm 2nm + 4nm, update
              28nk + 4nk (the selected rows' zeros)
     """
+    if scored_handover is None:
+        scored_handover = stage
     out = {"colnorm": 0, "topk_select": 0, "update": 0, "unpack": 0}
     for (n, m), k in zip(shapes, ks):
         u = m - k
         staged_refresh = refresh and stage and fused_handover and not end
-        scored_end = refresh and stage and fused_handover and end and first
+        scored_end = refresh and stage and scored_handover and fused_handover and end and first
         if refresh:
             out["colnorm"] += (2 * n * m + 4 * m + (2 * n * m if staged_refresh else 0)
                                + (4 * n * m if scored_end else 0))
@@ -415,7 +418,8 @@ def main(argv=None) -> int:
     for kind in kinds:
         b = step_bytes(shapes, ks, kind.refresh, kind.step_in_interval == 1, kind.interval_end,
                        offload=args.offload, fused_handover=fused,
-                       second=kind.step_in_interval == 2, stage=runner.use_stage)
+                       second=kind.step_in_interval == 2, stage=runner.use_stage,
+                       scored_handover=runner.score_handover)
         for key in totals:
             totals[key] += b[key]
     all_bytes = sum(totals.values())

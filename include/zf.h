@@ -374,17 +374,18 @@ typedef struct zf_matrix {
   float* acc_sq; /* Zen-auto only: [m - k] fp32 (else NULL) */
   const uint16_t* weight_cols; /* deferred update only: bf16 [n][m-k] / cm [m-k][n] */
   int64_t ld_weight_cols;
-  uint16_t* acc_first; /* optional, channel-major only: bf16 [m][ld_acc_first >= n],
-                          row j = channel j, see below */
+  uint16_t* acc_first; /* optional: bf16 in the gradient's shape (channel-major
+                          [m][ld >= n], row j = channel j; row-major [n][ld >= m]) */
   int64_t ld_acc_first;
 } zf_matrix;
 
 typedef struct zf_plan zf_plan;
 
-/* First-step stage of the packed buffer (acc_first; channel-major plans).
+/* First-step stage of the packed buffer (acc_first).
  * On the first step of an interval the packed values are the widened
  * gradient itself, so every one of them is exactly a bf16.  When a
- * descriptor gives acc_first (one bf16 row per channel, row j = channel j),
+ * descriptor gives acc_first (a bf16 array in the gradient's shape: element
+ * (i, j) at the place of G's element (i, j)),
  * zf_plan_update (do_pack) and zf_plan_update_handover keep that step's
  * values there, as the gradient's bf16 bits (2 bytes per element written
  * instead of 4), and the interval's second step reads them from there
@@ -396,14 +397,16 @@ typedef struct zf_plan zf_plan;
  * stage, in one pass over G) and then zf_plan_update with do_pack = 0: the
  * stage then holds what the packing would have written.  Every result (acc
  * from the second step on, the hand-over, W, the states) is bit-identical
- * to a plan without it.  acc_first must be 2-byte aligned (16-byte aligned
- * with ld % 8 == 0 for the vector path) and overlap no other buffer; a
- * row-major descriptor must leave it NULL (ZF_EINVAL at plan creation).
- * zf_plan_update_zen follows the same rule.  The separate hand-over of an
- * interval that ended after its first step reads the stage:
- * zf_plan_unpack_first instead of zf_plan_unpack.  The offloaded
- * optimizer's calls (zf_plan_update_pending, zf_plan_update_zen_pending)
- * reject a plan with a stage (ZF_EINVAL). */
+ * to a plan without it.  acc_first must overlap no other buffer and be
+ * 2-byte aligned (channel-major: 16-byte aligned with ld % 8 == 0 for the
+ * vector path; row-major: always 16-byte aligned with ld % 8 == 0).  In the
+ * channel-major layout zf_plan_update_zen follows the same rule, and the
+ * separate hand-over of an interval that ended after its first step reads
+ * the stage: zf_plan_unpack_first instead of zf_plan_unpack.  Row-major
+ * plans with a stage reject zf_plan_update_zen (its refresh statistics
+ * read the packed buffer); the offloaded optimizer's calls
+ * (zf_plan_update_pending, zf_plan_update_zen_pending) reject any plan with
+ * a stage (ZF_EINVAL). */
 
 /* Validates nmats >= 1 descriptors (HOST array, copied), computes the launch
  * geometry and allocates the plan's device tables and column-score
@@ -421,9 +424,9 @@ size_t zf_plan_device_bytes(const zf_plan* plan);
  * plan: do not run two colnorm calls of one plan concurrently). */
 zf_status zf_plan_colnorm(zf_plan* plan, zf_stream stream);
 
-/* zf_plan_colnorm that also copies every channel's gradient row to its row
- * of the descriptor's acc_first (descriptors without one: scores only), in
- * the same pass over G: on a refresh step that starts an interval, the
+/* zf_plan_colnorm that also copies the gradient to the descriptor's
+ * acc_first (descriptors without one: scores only), in the same pass over
+ * G: on a refresh step that starts an interval, the
  * packing of whichever channels the selection leaves unselected, done
  * before the selection is known (2 bytes per element written for every
  * channel instead of 2 read + 2 written for each unselected one in the

@@ -853,10 +853,13 @@ zf_status check_plan_matrix(const zf_matrix& x, zf_plan& p) {
     for (int a = 0; ok && a < 6; ++a) ok = !overlaps(zsel, others[a]) && !overlaps(zacc, others[a]);
     p.can_zen = p.can_zen && ok;
   }
-  // The bf16 first-step stage (channel-major, one row per channel): disjoint
-  // from everything the update reads or writes.
+  // The bf16 first-step stage (the gradient's shape: channel-major one row
+  // per channel, row-major [n][ld >= m] with 16-byte rows): disjoint from
+  // everything the update reads or writes.
   if (x.acc_first != nullptr) {
-    if (L != zf::kChannelMajor || !mat_ok(x.acc_first, eg, x.ld_acc_first, 2)) return ZF_EINVAL;
+    if (!mat_ok(x.acc_first, eg, x.ld_acc_first, 2)) return ZF_EINVAL;
+    if (L == zf::kRowMajor && (!aligned(x.acc_first, 16) || x.ld_acc_first % 8 != 0))
+      return ZF_EINVAL;
     const Span st = span(x.acc_first, eg, x.ld_acc_first, 2);
     const Ext es = ext(L, n, k);
     if (overlaps(st, g) || overlaps(st, span(x.acc, ea, x.ld_acc, 4)) ||
@@ -1046,7 +1049,14 @@ zf_status zf_plan_colnorm(zf_plan* p, zf_stream stream) {
 zf_status zf_plan_colnorm_stage(zf_plan* p, zf_stream stream) {
   if (p == nullptr || !p->can_colnorm || !p->has_acc1) return ZF_EINVAL;
   const Table t{p->d_mats, p->d_off_cn, p->nmats};
-  const hipError_t e = zf::launch_cm_colnorm(t, p->mats[0], p->blk_cn, as_stream(stream), 1);
+  hipError_t e;
+  if (p->layout == zf::kChannelMajor) {
+    e = zf::launch_cm_colnorm(t, p->mats[0], p->blk_cn, as_stream(stream), 1);
+  } else {
+    const Table tf{p->d_mats, p->d_off_fin, p->nmats};
+    e = zf::launch_colnorm(t, p->mats[0], p->blk_cn, tf, p->blk_fin, p->d_ws, as_stream(stream),
+                           true);
+  }
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
@@ -1072,8 +1082,8 @@ zf_status zf_plan_topk_select(zf_plan* p, zf_stream stream) {
 namespace {
 
 // The pack phase passed to the update kernels: 1 on an interval's first
-// step, 2 on its second when the plan keeps a bf16 first-step stage (a
-// channel-major plan), else 0.
+// step, 2 on its second when the plan keeps a bf16 first-step stage, else
+// 0.
 int32_t pack_phase(const zf_plan* p, int64_t step_in_interval) {
   if (step_in_interval == 1) return 1;
   return (step_in_interval == 2 && p->has_acc1) ? 2 : 0;
@@ -1137,7 +1147,8 @@ zf_status zf_plan_update_adam_handover(zf_plan* p, const zf_adam_hparams* hp, in
 }
 
 zf_status zf_plan_unpack_first(zf_plan* p, float scale, zf_stream stream) {
-  if (p == nullptr || !p->can_unpack || !p->all_acc1) return ZF_EINVAL;
+  if (p == nullptr || !p->can_unpack || !p->all_acc1 || p->layout != zf::kChannelMajor)
+    return ZF_EINVAL;
   const Table t{p->d_mats, p->d_off_unp, p->nmats};
   const hipError_t e =
       zf::launch_cm_unpack(t, p->mats[0], p->blk_unp, scale, as_stream(stream), true);
@@ -1245,7 +1256,10 @@ zf_status plan_update_zen(zf_plan* p, const AdamK& c, int32_t mode, int32_t firs
 bool zen_args_ok(const zf_plan* p, const zf_adam_hparams* hp, int64_t step, double tau,
                  const zf_zen_totals* totals) {
   static_assert(sizeof(zf_zen_totals) == sizeof(zf::ZenTotals), "zen totals layout");
+  // (row-major Zen-auto statistics of refresh steps read the packed buffer
+  // in a separate pass: no stage there)
   return p != nullptr && p->can_zen && p->can_adam && p->can_pack && hparams_ok(hp) &&
+         !(p->has_acc1 && p->layout == zf::kRowMajor) &&
          step >= 1 && tau >= 0.0 && totals != nullptr && aligned(totals, 8);
 }
 

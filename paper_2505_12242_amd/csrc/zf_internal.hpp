@@ -83,8 +83,8 @@ struct DevMat {
   int64_t ld_wcols;
   const float* pend_acc;  // owed deferred update: packed sums under the previous selection
   int64_t ld_pend;
-  uint16_t* acc1;    // channel-major: bf16 first-step stage of the packed buffer, row j =
-                     // channel j (optional)
+  uint16_t* acc1;    // bf16 first-step stage of the packed buffer, in the gradient's shape
+                     // (channel-major row j = channel j; row-major [n][ld >= m]) (optional)
   int64_t ld_acc1;
   float* sel_sq;     // Zen-auto: [k] squared norms of the selected channels' gradient
   float* acc_sq;     // Zen-auto: [m-k] squared norms of the accumulated channels
@@ -139,8 +139,11 @@ bool hparams_ok(const zf_adam_hparams* hp);
 AdamK adam_consts(const zf_adam_hparams& hp, int64_t step);
 
 // Kernel launchers (zf_kernels.hip).  `blocks` is the grid size.
+// stage: also copy every element read to the same place of acc1 (the
+// bf16 first-step stage; row-major plans that have one).
 hipError_t launch_colnorm(const Table& t, const DevMat& one, int64_t blocks,
-                          const Table& tf, int64_t fin_blocks, double* ws, hipStream_t s);
+                          const Table& tf, int64_t fin_blocks, double* ws, hipStream_t s,
+                          bool stage = false);
 hipError_t launch_topk(const Table& t, const DevMat& one, int64_t blocks, hipStream_t s);
 // pend != nullptr: fused Adam + pack in kRemap against the store, with the
 // owed deferred update applied to the entering columns first.

@@ -32,11 +32,17 @@ __device__ __forceinline__ void accum8(double (&acc)[8], uint4 v) {
   }
 }
 
-template <bool BATCHED>
+// STAGE (a refresh step that starts an interval, plans with the bf16
+// first-step stage): the pass also copies every element it reads to the
+// same place of the stage (one bf16 row per gradient row), the packing of
+// whichever columns the selection leaves unselected, so that the step's
+// update runs the Adam part alone.
+template <bool BATCHED, bool STAGE>
 __global__ __launch_bounds__(kThreads) void colnorm_partial_kernel(const DevMat* __restrict__ mats, const int64_t* __restrict__ off, int32_t nmats, DevMat one,
                                                                    double* __restrict__ ws) {
   int64_t local;
   const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, local);
+  const bool st = STAGE && d.acc1 != nullptr;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int64_t cblk = local % d.cn_cb;
@@ -52,6 +58,8 @@ __global__ __launch_bounds__(kThreads) void colnorm_partial_kernel(const DevMat*
   if (c0 < d.m) {
     const uint16_t* __restrict__ base = d.grad + c0;
     const int64_t ld = d.ld_grad;
+    uint16_t* __restrict__ sbase = st ? d.acc1 + c0 : nullptr;
+    const int64_t sld = d.ld_acc1;
     if (d.vec && c0 + 8 <= d.m) {
       int64_t i = r0 + wave;
       for (; i + 12 < r1; i += 16) {
@@ -59,12 +67,22 @@ __global__ __launch_bounds__(kThreads) void colnorm_partial_kernel(const DevMat*
         const uint4 v1 = *reinterpret_cast<const uint4*>(base + (i + 4) * ld);
         const uint4 v2 = *reinterpret_cast<const uint4*>(base + (i + 8) * ld);
         const uint4 v3 = *reinterpret_cast<const uint4*>(base + (i + 12) * ld);
+        if (st) {
+          *reinterpret_cast<uint4*>(sbase + i * sld) = v0;
+          *reinterpret_cast<uint4*>(sbase + (i + 4) * sld) = v1;
+          *reinterpret_cast<uint4*>(sbase + (i + 8) * sld) = v2;
+          *reinterpret_cast<uint4*>(sbase + (i + 12) * sld) = v3;
+        }
         accum8(acc, v0);
         accum8(acc, v1);
         accum8(acc, v2);
         accum8(acc, v3);
       }
-      for (; i < r1; i += 4) accum8(acc, *reinterpret_cast<const uint4*>(base + i * ld));
+      for (; i < r1; i += 4) {
+        const uint4 v = *reinterpret_cast<const uint4*>(base + i * ld);
+        if (st) *reinterpret_cast<uint4*>(sbase + i * sld) = v;
+        accum8(acc, v);
+      }
     } else {
       const int64_t nc = min(static_cast<int64_t>(8), d.m - c0);
       for (int64_t i = r0 + wave; i < r1; i += 4) {
@@ -72,6 +90,7 @@ __global__ __launch_bounds__(kThreads) void colnorm_partial_kernel(const DevMat*
 #pragma unroll
         for (int c = 0; c < 8; ++c) {
           if (c < nc) {
+            if (st) sbase[i * sld + c] = row[c];
             const double x = static_cast<double>(widen_bf16(row[c]));
             acc[c] = __builtin_fma(x, x, acc[c]);
           }
@@ -308,12 +327,15 @@ __device__ __forceinline__ TileSlots tile_slots(const DevMat& d, int64_t c0) {
 
 // Pack lane: A[i][u] (+)= G[i][j] over the block's rows.  HAND (last step
 // of an interval, fused hand-over): scale * the new sum goes to D[i][j] (rD,
-// vD, sD) and A is not written.
-template <bool FIRST, bool HAND = false>
+// vD, sD) and A is not written.  A16 (the bf16 first-step stage, element
+// (i, j) at rS/vS/sS): 1 -- the first step stores the gradient's bits there
+// instead of fp32 A; 2 -- the second step reads its previous values there.
+template <bool FIRST, bool HAND = false, int A16 = 0>
 __device__ __forceinline__ void pack_rows(rsrc_t rG, uint32_t vG, uint32_t sG, rsrc_t rA,
                                           uint32_t vA, uint32_t sA, int32_t rows,
                                           rsrc_t rD = rsrc_t(), uint32_t vD = 0, uint32_t sD = 0,
-                                          float scale = 1.0f) {
+                                          float scale = 1.0f, rsrc_t rS = rsrc_t(),
+                                          uint32_t vS = 0, uint32_t sS = 0) {
   int32_t i = 0;
   for (; i + kRowBatch <= rows; i += kRowBatch) {
     uint16_t gb[kRowBatch];
@@ -322,7 +344,8 @@ __device__ __forceinline__ void pack_rows(rsrc_t rG, uint32_t vG, uint32_t sG, r
     for (int b = 0; b < kRowBatch; ++b) gb[b] = buf_u16<ZF_RM_AUX_RO>(rG, vG, (i + b) * sG);
     if constexpr (!FIRST) {
 #pragma unroll
-      for (int b = 0; b < kRowBatch; ++b) a[b] = buf_f32(rA, vA, (i + b) * sA);
+      for (int b = 0; b < kRowBatch; ++b)
+        a[b] = A16 == 2 ? widen_bf16(buf_u16(rS, vS, (i + b) * sS)) : buf_f32(rA, vA, (i + b) * sA);
 #pragma unroll
       for (int b = 0; b < kRowBatch; ++b) a[b] = a[b] + widen_bf16(gb[b]);
     } else {
@@ -332,13 +355,18 @@ __device__ __forceinline__ void pack_rows(rsrc_t rG, uint32_t vG, uint32_t sG, r
 #pragma unroll
     for (int b = 0; b < kRowBatch; ++b) {
       if constexpr (HAND) buf_put_f32(a[b] * scale, rD, vD, (i + b) * sD);
+      else if constexpr (FIRST && A16 == 1) buf_put_u16(gb[b], rS, vS, (i + b) * sS);
       else buf_put_f32(a[b], rA, vA, (i + b) * sA);
     }
   }
   for (; i < rows; ++i) {
-    const float g = widen_bf16(buf_u16<ZF_RM_AUX_RO>(rG, vG, i * sG));
-    const float a = FIRST ? g : buf_f32(rA, vA, i * sA) + g;
+    const uint16_t gb = buf_u16<ZF_RM_AUX_RO>(rG, vG, i * sG);
+    const float g = widen_bf16(gb);
+    float a = g;
+    if constexpr (!FIRST)
+      a = (A16 == 2 ? widen_bf16(buf_u16(rS, vS, i * sS)) : buf_f32(rA, vA, i * sA)) + g;
     if constexpr (HAND) buf_put_f32(a * scale, rD, vD, i * sD);
+    else if constexpr (FIRST && A16 == 1) buf_put_u16(gb, rS, vS, i * sS);
     else buf_put_f32(a, rA, vA, i * sA);
   }
 }
@@ -491,14 +519,33 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const DevMat* __restri
       const uint32_t vG = j * 2u;
       const rsrc_t rA = rows_rsrc(d.acc, i0, i1, d.ld_acc, d.m - d.k);
       const uint32_t sA = static_cast<uint32_t>(d.ld_acc * 4);
+      // the bf16 first-step stage at element (i, j): first == 1 on an
+      // interval's first step, 2 on its second (a matrix without a stage
+      // takes 2 as any later step)
+      const bool a16 = d.acc1 != nullptr;
+      const rsrc_t rS = a16 ? rows_rsrc(d.acc1, i0, i1, d.ld_acc1, d.m) : rA;
+      const uint32_t sS = a16 ? static_cast<uint32_t>(d.ld_acc1 * 2) : 0u;
       if constexpr (HAND) {
         const rsrc_t rD = rows_rsrc(d.out, i0, i1, d.ld_out, d.m);
         const uint32_t sD = static_cast<uint32_t>(d.ld_out * 4);
-        if (first) pack_rows<true, true>(rG, vG, sG, rA, u * 4u, sA, rows, rD, j * 4u, sD, scale);
+        if (first == 1)
+          pack_rows<true, true>(rG, vG, sG, rA, u * 4u, sA, rows, rD, j * 4u, sD, scale);
+        else if (a16 && first == 2)
+          pack_rows<false, true, 2>(rG, vG, sG, rA, u * 4u, sA, rows, rD, j * 4u, sD, scale, rS,
+                                    vG, sS);
         else pack_rows<false, true>(rG, vG, sG, rA, u * 4u, sA, rows, rD, j * 4u, sD, scale);
       } else {
-        if (first) pack_rows<true>(rG, vG, sG, rA, u * 4u, sA, rows);
-        else pack_rows<false>(rG, vG, sG, rA, u * 4u, sA, rows);
+        if (first == 1) {
+          if (a16)
+            pack_rows<true, false, 1>(rG, vG, sG, rA, u * 4u, sA, rows, rsrc_t(), 0, 0, 1.0f, rS,
+                                      vG, sS);
+          else pack_rows<true>(rG, vG, sG, rA, u * 4u, sA, rows);
+        } else if (a16 && first == 2) {
+          pack_rows<false, false, 2>(rG, vG, sG, rA, u * 4u, sA, rows, rsrc_t(), 0, 0, 1.0f, rS,
+                                     vG, sS);
+        } else {
+          pack_rows<false>(rG, vG, sG, rA, u * 4u, sA, rows);
+        }
       }
     }
     return;
@@ -646,11 +693,26 @@ __global__ __launch_bounds__(kThreads) void unpack_kernel(const DevMat* __restri
   } while (0)
 
 hipError_t launch_colnorm(const Table& t, const DevMat& one, int64_t blocks, const Table& tf,
-                          int64_t fin_blocks, double* ws, hipStream_t s) {
+                          int64_t fin_blocks, double* ws, hipStream_t s, bool stage) {
   (void)hipGetLastError();
-  if (blocks > 0)
-    ZF_LAUNCH(colnorm_partial_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), s, t,
-              one, ws);
+  if (blocks > 0) {
+    const dim3 grid(static_cast<uint32_t>(blocks));
+    if (stage) {
+      if (t.mats != nullptr)
+        hipLaunchKernelGGL((colnorm_partial_kernel<true, true>), grid, dim3(kThreads), 0, s,
+                           t.mats, t.off, t.nmats, one, ws);
+      else
+        hipLaunchKernelGGL((colnorm_partial_kernel<false, true>), grid, dim3(kThreads), 0, s,
+                           t.mats, t.off, t.nmats, one, ws);
+    } else {
+      if (t.mats != nullptr)
+        hipLaunchKernelGGL((colnorm_partial_kernel<true, false>), grid, dim3(kThreads), 0, s,
+                           t.mats, t.off, t.nmats, one, ws);
+      else
+        hipLaunchKernelGGL((colnorm_partial_kernel<false, false>), grid, dim3(kThreads), 0, s,
+                           t.mats, t.off, t.nmats, one, ws);
+    }
+  }
   if (fin_blocks > 0)
     ZF_LAUNCH(colnorm_finalize_kernel, dim3(static_cast<uint32_t>(fin_blocks)),
               dim3(kFinalizeCols), s, tf, one, static_cast<const double*>(ws));

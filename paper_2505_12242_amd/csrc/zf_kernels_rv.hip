@@ -32,6 +32,13 @@
 // read and write their sources element by element, runs the per-column
 // kernel.
 //
+// The bf16 first-step stage (acc1, optional; one bf16 row per gradient row):
+// on an interval's first step (first == 1) the block stores the G rows it
+// loads into the stage as they are (every column, 16 bytes per lane) and
+// the pack lanes write nothing; on its second (first == 2) the stage rows
+// are loaded and staged in LDS like G, and the pack lanes take their
+// previous values from there instead of from A.
+//
 // STATS (Zen-auto, blocks of cn_rpb rows): each lane also sums, in fp64 and
 // in row order, the squares of its selected columns' gradient and of its
 // unselected slots' new accumulated values over the block's rows, and
@@ -79,6 +86,7 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
                                                              double* __restrict__ zs) {
   static_assert(!STATS || (ADAM && PACK && !HAND), "statistics of the fused update");
   __shared__ __attribute__((aligned(16))) uint16_t sg[kRvBatch][kRvMaxCols];
+  __shared__ __attribute__((aligned(16))) uint16_t sa[PACK ? kRvBatch : 1][PACK ? kRvMaxCols : 8];
   __shared__ __attribute__((aligned(16))) float sd[HAND ? kRvBatch : 1][HAND ? kRvMaxCols : 4];
 
   int64_t local;
@@ -159,9 +167,18 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
   const uint32_t sG = static_cast<uint32_t>(d.ld_grad * 2);
   rsrc_t rA = rsrc_t(), rP = rsrc_t(), rM = rsrc_t(), rV = rsrc_t(), rW = rsrc_t(), rD = rsrc_t();
   uint32_t sA = 0, sS = 0, sW = 0, sD = 0;
+  rsrc_t rT = rsrc_t();
+  uint32_t sT = 0;
+  const bool a16 = PACK && d.acc1 != nullptr;
+  const bool put16 = a16 && first == 1 && !HAND;  // store G rows to the stage
+  const bool get16 = a16 && first == 2;           // read the stage rows
   if constexpr (PACK) {
     rA = rows_rsrc(d.acc, i0, i1, d.ld_acc, d.m - d.k);
     sA = static_cast<uint32_t>(d.ld_acc * 4);
+    if (a16) {
+      rT = rows_rsrc(d.acc1, i0, i1, d.ld_acc1, d.m);
+      sT = static_cast<uint32_t>(d.ld_acc1 * 2);
+    }
   }
   if constexpr (ADAM) {
     rP = rows_rsrc(d.P, i0, i1, d.ld_state, d.k);
@@ -189,22 +206,49 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
 
     // 1. G rows of the batch (16-byte loads of 8 columns; ragged tail of
     //    the last tile element by element).
-    u32x4 gv[kRvBatch / 2];
+    u32x4 gv[kRvBatch / 2], av[kRvBatch / 2];
 #pragma unroll
     for (int p = 0; p < kRvBatch / 2; ++p) {
       const int b = 2 * p + h;
       gv[p] = u32x4{0u, 0u, 0u, 0u};
+      av[p] = u32x4{0u, 0u, 0u, 0u};
       if (b < nb && g8 < width) {
         const uint32_t so = static_cast<uint32_t>(i + b) * sG;
         const uint32_t vo = static_cast<uint32_t>((c0 + g8) * 2);
+        const uint32_t to = static_cast<uint32_t>(i + b) * sT;
         if (g8 + 8 <= width) {
           gv[p] = buf_b128<kStream>(rG, vo, so);
+          if (get16) av[p] = buf_b128<kStream>(rT, vo, to);
         } else {
-          uint32_t w[4] = {0u, 0u, 0u, 0u};
-          for (int x = 0; g8 + x < width; ++x)
+          uint32_t w[4] = {0u, 0u, 0u, 0u}, x4[4] = {0u, 0u, 0u, 0u};
+          for (int x = 0; g8 + x < width; ++x) {
             w[x >> 1] |= static_cast<uint32_t>(buf_u16<kStream>(rG, vo + 2 * x, so))
                          << (16 * (x & 1));
+            if (get16)
+              x4[x >> 1] |= static_cast<uint32_t>(buf_u16<kStream>(rT, vo + 2 * x, to))
+                            << (16 * (x & 1));
+          }
           gv[p] = u32x4{w[0], w[1], w[2], w[3]};
+          av[p] = u32x4{x4[0], x4[1], x4[2], x4[3]};
+        }
+      }
+    }
+    if (put16) {
+      // the first step's packed values: the gradient rows themselves
+#pragma unroll
+      for (int p = 0; p < kRvBatch / 2; ++p) {
+        const int b = 2 * p + h;
+        if (b < nb && g8 < width) {
+          const uint32_t to = static_cast<uint32_t>(i + b) * sT;
+          const uint32_t vo = static_cast<uint32_t>((c0 + g8) * 2);
+          if (g8 + 8 <= width) {
+            buf_put_b128<kStream>(gv[p], rT, vo, to);
+          } else {
+            const uint32_t w[4] = {gv[p].x, gv[p].y, gv[p].z, gv[p].w};
+            for (int x = 0; g8 + x < width; ++x)
+              buf_put_u16<kStream>(static_cast<uint16_t>(w[x >> 1] >> (16 * (x & 1))), rT,
+                                   vo + 2 * x, to);
+          }
         }
       }
     }
@@ -216,7 +260,7 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
     for (int b = 0; b < kRvBatch; ++b)
 #pragma unroll
       for (int e = 0; e < 4; ++e) x0[b][e] = x1[b][e] = x2[b][e] = 0.0f;
-    if (PACK && !first) {
+    if (PACK && first != 1 && !get16) {
       if (is_q) {
 #pragma unroll
         for (int b = 0; b < kRvBatch; ++b) {
@@ -255,7 +299,10 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
 #pragma unroll
     for (int p = 0; p < kRvBatch / 2; ++p) {
       const int b = 2 * p + h;
-      if (b < nb && g8 < width) *reinterpret_cast<u32x4*>(&sg[b][g8]) = gv[p];
+      if (b < nb && g8 < width) {
+        *reinterpret_cast<u32x4*>(&sg[b][g8]) = gv[p];
+        if (get16) *reinterpret_cast<u32x4*>(&sa[b][g8]) = av[p];
+      }
     }
     __syncthreads();
 
@@ -269,7 +316,8 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
               const float g = widen_bf16(sg[b][cj[e]]);
-              a[e] = first ? g : x0[b][e] + g;
+              const float prev = get16 ? widen_bf16(sa[b][cj[e]]) : x0[b][e];
+              a[e] = first == 1 ? g : prev + g;
               if constexpr (STATS) {
                 const double x = static_cast<double>(a[e]);
                 zq[e] = __builtin_fma(x, x, zq[e]);
@@ -279,7 +327,7 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
 #pragma unroll
               for (int e = 0; e < 4; ++e)
                 if ((valid >> e) & 1u) sd[b][cj[e]] = a[e] * scale;
-            } else {
+            } else if (!put16) {
               const uint32_t so = static_cast<uint32_t>(i + b) * sA;
               if (is_q) buf_put_b128(as_u4(a[0], a[1], a[2], a[3]), rA, vQ, so);
               else buf_put_f32(a[0], rA, vs[0], so);

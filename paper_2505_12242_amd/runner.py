@@ -136,12 +136,15 @@ class SelectiveUpdateRunner:
         # fixed schedule with the fused hand-over, where the only consumers
         # of the packed buffer are the next update passes).  A refresh step
         # that starts an interval then fills it from the score pass.
-        self.use_stage = (bool(first_step_stage) and layout != ROW_MAJOR and not self.offload
-                          and self.keep_unpacked)
+        # (row-major: the fixed schedule with the fused hand-over only)
+        self.use_stage = (bool(first_step_stage) and not self.offload and self.keep_unpacked
+                          and (layout != ROW_MAJOR or (zen_tau is None and self.fuse_handover)))
         # with the fixed schedule and the fused hand-over a refresh step also
         # packs from the score pass: into the stage when an interval starts,
-        # into the hand-over buffer when the step is a whole interval
+        # and (channel-major) into the hand-over buffer when the step is a
+        # whole interval
         self.score_pack = self.use_stage and zen_tau is None and self.fuse_handover
+        self.score_handover = self.score_pack and layout != ROW_MAJOR
         self._in_stage = False  # the current interval's sums are in the stage
         self.weights = list(weights)
         self.init_master = list(init_master) if init_master is not None else None
@@ -273,7 +276,7 @@ class SelectiveUpdateRunner:
         # the stage when an interval starts; into the hand-over buffer when
         # the step is a whole interval) and the update only runs Adam
         staged = refresh and self.score_pack and not kind.interval_end
-        scored_end = refresh and self.score_pack and kind.interval_end and length == 1
+        scored_end = refresh and self.score_handover and kind.interval_end and length == 1
         if refresh:
             nxt = 0 if t == 1 else 1 - self.cur
             plan = self.plans[slot][nxt][self.cur_a]
@@ -536,7 +539,8 @@ class SelectiveUpdateRunner:
                 dst.copy_(d[key])
             if sd.get("in_stage") and self.use_stage:
                 # first-step values (exact in bf16) into the unselected rows
-                self.stage[q].index_copy_(0, s.unsel_idx.long(),
+                self.stage[q].index_copy_(1 if self.layout == ROW_MAJOR else 0,
+                                          s.unsel_idx.long(),
                                           d["acc"].to(self.device, torch.bfloat16))
             else:
                 self.accs[0][q].copy_(d["acc"])
@@ -554,7 +558,8 @@ class SelectiveUpdateRunner:
         """The last interval's packed sums, fp32 (after an interval's first
         step with the bf16 stage: a widened copy of the stage, exact)."""
         if self._in_stage:
-            return [x.index_select(0, s.unsel_idx.long()).float()
+            dim = 1 if self.layout == ROW_MAJOR else 0
+            return [x.index_select(dim, s.unsel_idx.long()).float()
                     for x, s in zip(self.stage, self.sels[self.cur])]
         return self.accs[self.cur_a]
 

@@ -19,8 +19,12 @@ the vector and element paths:
 * Zen-auto and the separate hand-over pass with the stage equal the same
   runs without it (one-step intervals hand over from the stage,
   zf_plan_unpack_first);
-* rejected: a row-major stage, a stage overlapping the packed buffer,
-  colnorm_stage and unpack_first without a stage.
+* the row-major stage (one bf16 row per gradient row): first and second
+  steps on the 16-byte and per-column kernels, the staged refresh and the
+  runner, bit for bit against the runs without it;
+* rejected: a stage overlapping the packed buffer, a row-major stage
+  without 16-byte rows, Zen-auto on a row-major staged plan, colnorm_stage
+  and unpack_first without a stage.
 """
 import sys
 
@@ -231,13 +235,6 @@ def test_plans_that_cannot_use_the_stage_reject_it():
     n, m, k = 8, 64, 6
     rng = np.random.default_rng(3)
     sel = O.select_topk(rng.random(m).astype(np.float32), k)
-    # row-major descriptors may not give one
-    with pytest.raises(RuntimeError):
-        zf.Plan([zf.MatrixBuffers(grad=bf16_dev(np.zeros((n, m), np.uint16)), k=k,
-                                  sel=sel_dev(sel), acc=torch.zeros((n, m - k), device="cuda"),
-                                  layout=zf.ROW_MAJOR,
-                                  acc_first=torch.zeros((n, m), dtype=torch.bfloat16,
-                                                        device="cuda"))])
     # overlapping the packed buffer
     A = torch.zeros((m, n), device="cuda")
     with pytest.raises(RuntimeError):
@@ -344,3 +341,153 @@ def test_unpack_first_reads_the_stage(aligned):
     with pytest.raises(RuntimeError):
         p2.unpack_first(1.0)
     p2.close()
+
+
+# ------------------------------------------------------------ row-major stage
+
+RM = zf.ROW_MAJOR
+
+
+@pytest.mark.parametrize("vec", [True, False])
+@pytest.mark.parametrize("n,m", [(64, 300), (4104, 70), (5, 33), (48, 1000), (16, 2049)])
+def test_row_major_stage_first_and_second_step(n, m, vec):
+    """Row-major: the first step stores the gradient rows in the stage (the
+    16-byte kernel: whole rows; the per-column kernel, taken when the fp32
+    buffer is not 16-byte aligned: the unselected columns), the second step
+    reads it; sums and the second-step hand-over bit for bit."""
+    print(f"# rm stage n={n} m={m} vec={vec}", file=sys.stderr, flush=True)
+    rng = np.random.default_rng(derive_seed("rm-stage", n, m))
+    k = O.k_from_ratio(0.1, m)
+    sel = O.select_topk(rng.random(m).astype(np.float32), k)
+    g1 = grad_bits(n, m, derive_seed("rm-stage-g", n, m, 1))
+    g2 = grad_bits(n, m, derive_seed("rm-stage-g", n, m, 2))
+    G = [bf16_dev(g, ld=-(-m // 8) * 8) for g in (g1, g2)]
+    A = _buf(n, m - k, torch.float32, vec, np.nan)
+    stage = _buf(n, m, torch.bfloat16, True, 0.0)
+    D = _buf(n, m, torch.float32, vec, np.nan)
+
+    def plan(grad, **kw):
+        return zf.Plan([zf.MatrixBuffers(grad=grad, k=k, sel=sel_dev(sel), acc=A, unpacked=D,
+                                         layout=RM, acc_first=stage, **kw)])
+
+    p1, p2 = plan(G[0]), plan(G[1])
+    p1.update(HP, 1, zf.STATES_INPLACE, 1, 4, adam=False, pack=True)
+    torch.cuda.synchronize()
+    assert torch.isnan(A).all()
+    st = bits_np(stage)
+    uns = sel.unsel.astype(np.int64)
+    assert np.array_equal(st[:, uns], g1[:, uns])
+    p2.update(HP, 2, zf.STATES_INPLACE, 2, 4, adam=False, pack=True)
+    torch.cuda.synchronize()
+    A2 = O.pack_accumulate(g2, sel.unsel, O.pack_accumulate(g1, sel.unsel, None, 1), 2)
+    assert same_bits(f32_np(A), A2)
+    A.fill_(np.nan)
+    p1.update(HP, 1, zf.STATES_INPLACE, 1, 2, adam=False, pack=True)
+    Pn, Mn, Vn = (_buf(n, k, torch.float32, vec, 0.0) for _ in range(3))
+    W = bf16_dev(np.zeros((n, m), np.uint16), ld=-(-m // 8) * 8)
+    ph = plan(G[1], weight=W, master=Pn, exp_avg=Mn, exp_avg_sq=Vn)
+    ph.update_handover(HP, 2, zf.STATES_INPLACE, 2, 2, 0.5)
+    torch.cuda.synchronize()
+    assert torch.isnan(A).all()
+    assert same_bits(f32_np(D), O.unpack(A2, sel, 0.5))
+    for x in (p1, p2, ph):
+        x.close()
+
+
+@pytest.mark.parametrize("n,m", [(64, 300), (4104, 70), (5, 33)])
+def test_row_major_colnorm_stage_then_adam_only_refresh(n, m):
+    print(f"# rm colnorm stage n={n} m={m}", file=sys.stderr, flush=True)
+    rng = np.random.default_rng(derive_seed("rm-cs", n, m))
+    k = O.k_from_ratio(0.1, m)
+    g = [grad_bits(n, m, derive_seed("rm-cs-g", n, m, t)) for t in (1, 2)]
+    W0 = O.bf16_round((rng.standard_normal((n, m)) * 0.02).astype(np.float32))
+    outs = []
+    for staged in (True, False):
+        G = [bf16_dev(x, ld=-(-m // 8) * 8) for x in g]
+        A = _buf(n, m - k, torch.float32, True, np.nan)
+        stage = _buf(n, m, torch.bfloat16, True, 0.0) if staged else None
+        norms = torch.full((m,), np.nan, device="cuda")
+        Pn, Mn, Vn = (_buf(n, k, torch.float32, True, np.nan) for _ in range(3))
+        W = bf16_dev(W0, ld=-(-m // 8) * 8)
+        s = zf.Selection(m, k)
+        plans = [zf.Plan([zf.MatrixBuffers(grad=x, k=k, sel=s, weight=W, master=Pn, exp_avg=Mn,
+                                           exp_avg_sq=Vn, acc=A, norms=norms, layout=RM,
+                                           acc_first=stage)]) for x in G]
+        if staged:
+            plans[0].colnorm_stage()
+        else:
+            plans[0].colnorm()
+        plans[0].topk_select()
+        plans[0].update(HP, 1, zf.STATES_INIT, 1, 4, pack=not staged)
+        torch.cuda.synchronize()
+        if staged:
+            assert np.array_equal(bits_np(stage), g[0])
+        plans[1].update(HP, 2, zf.STATES_INPLACE, 2, 4)
+        torch.cuda.synchronize()
+        outs.append([f32_np(norms), s.sel_idx.cpu().numpy(), f32_np(Pn), f32_np(Mn), f32_np(Vn),
+                     bits_np(W), f32_np(A)])
+        for p in plans:
+            p.close()
+    for a, b in zip(*outs):
+        assert np.array_equal(np.ascontiguousarray(a).view(np.uint8),
+                              np.ascontiguousarray(b).view(np.uint8))
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("vec", [True, False])
+@pytest.mark.parametrize("R,S", [(4, 4), (6, 3), (3, 2), (2, 1)])
+def test_row_major_runner_with_stage_equals_runner_without(R, S, vec):
+    """vec: every gradient row 16-byte aligned (the plans take the 16-byte
+    kernel); else the per-column kernel throughout."""
+    T_ = 10
+    dev = torch.device("cuda")
+    shapes = ([(264, 304), (4104, 72), (40, 1504), (16, 8)] if vec else
+              [(264, 300), (4104, 70), (43, 77), (16, 3), (40, 1500)])
+    slots, _, w, _ = _inputs(shapes, T_, 47, RM, dev)
+    runs = []
+    for stage in (True, False):
+        weights = [x.clone() for x in w]
+        runner = zf.SelectiveUpdateRunner(shapes, 0.1, HP, R, S, slots, weights, device=dev,
+                                          layout=RM, first_step_stage=stage)
+        assert runner.use_stage == stage and not runner.score_handover
+        out = []
+        for t in range(1, T_ + 1):
+            print(f"# rm stage runner R={R} S={S} vec={vec} stage={stage} step {t}", file=sys.stderr,
+                  flush=True)
+            kind = runner.step()
+            torch.cuda.synchronize()
+            for q in range(len(shapes)):
+                out.append(bits_np(runner.weights[q]))
+                out.extend(f32_np(x) for x in runner.state[q])
+                out.append(f32_np(runner.unpacked[q]) if kind.interval_end
+                           else f32_np(runner.acc[q]))
+        runs.append(out)
+        runner.close()
+    for i, (a, b) in enumerate(zip(*runs)):
+        assert a.shape == b.shape and np.array_equal(np.ascontiguousarray(a).view(np.uint8),
+                                                     np.ascontiguousarray(b).view(np.uint8)), i
+
+
+def test_row_major_stage_rules():
+    n, m, k = 8, 64, 6
+    rng = np.random.default_rng(3)
+    sel = O.select_topk(rng.random(m).astype(np.float32), k)
+    base = dict(grad=bf16_dev(np.zeros((n, m), np.uint16)), k=k, sel=sel_dev(sel),
+                acc=torch.zeros((n, m - k), device="cuda"), layout=RM)
+    # the row-major stage must have 16-byte rows
+    odd = torch.zeros(n * m + 1, dtype=torch.bfloat16, device="cuda")[1:].view(n, m)
+    with pytest.raises(RuntimeError):
+        zf.Plan([zf.MatrixBuffers(acc_first=odd, **base)])
+    # Zen-auto rejects a row-major plan with a stage
+    z = zf.Plan([zf.MatrixBuffers(acc_first=torch.zeros((n, m), dtype=torch.bfloat16,
+                                                        device="cuda"),
+                                  weight=bf16_dev(np.zeros((n, m), np.uint16)),
+                                  master=torch.zeros((n, k), device="cuda"),
+                                  exp_avg=torch.zeros((n, k), device="cuda"),
+                                  exp_avg_sq=torch.zeros((n, k), device="cuda"),
+                                  sel_sq=torch.zeros(k, device="cuda"),
+                                  acc_sq=torch.zeros(m - k, device="cuda"), **base)])
+    totals = torch.zeros(zf.ZEN_TOTALS_BYTES // 8, dtype=torch.int64, device="cuda")
+    with pytest.raises(RuntimeError):
+        z.update_zen(HP, 1, zf.STATES_INPLACE, 1, 4, 1.0, totals)
+    z.close()
