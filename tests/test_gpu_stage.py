@@ -491,3 +491,53 @@ def test_row_major_stage_rules():
     with pytest.raises(RuntimeError):
         z.update_zen(HP, 1, zf.STATES_INPLACE, 1, 4, 1.0, totals)
     z.close()
+
+
+@pytest.mark.parametrize("master", [False, True])
+@pytest.mark.parametrize("mode", ["init", "remap"])
+def test_row_major_adam_only_selected_grid(mode, master):
+    """Row-major Adam alone (the staged refresh's update): states and W equal
+    the fused per-column pass's bit for bit, over a batched plan whose
+    matrices span one to many column tiles and ragged row blocks (0 selected
+    columns included)."""
+    shapes = [(300, 2900), (17, 77), (4104, 70), (9, 5000), (6, 40)]
+    ratios = [0.1, 0.1, 0.1, 0.2, 0.0]
+    print(f"# rm selected grid mode={mode} master={master}", file=sys.stderr, flush=True)
+    rng = np.random.default_rng(derive_seed("rm-selg", mode, master))
+    res = []
+    for pack in (False, True):
+        bufs = []
+        for (n, m), ratio in zip(shapes, ratios):
+            k = O.k_from_ratio(ratio, m)
+            r2 = np.random.default_rng(derive_seed("rm-selg-q", n, m))
+            old = O.select_topk(r2.random(m).astype(np.float32), k)
+            new = O.select_topk(r2.random(m).astype(np.float32), k)
+            g = grad_bits(n, m, derive_seed("rm-selg-g", n, m))
+            W = O.bf16_round((r2.standard_normal((n, m)) * 0.02).astype(np.float32))
+            prev = [(r2.standard_normal((n, k)) * s).astype(np.float32) for s in (0.02, 1e-3, 1e-3)]
+            prev[2] = np.abs(prev[2])
+            ld_m = -(-m // 8) * 8
+            dev = lambda x: _buf(n, x.shape[1], torch.float32, True, 0.0).copy_(torch.from_numpy(x))
+            P, M, V = (_buf(n, k, torch.float32, True, np.nan) for _ in range(3))
+            src = None
+            if mode == "remap" or master:
+                src = zf.StateSource(
+                    prev=sel_dev(old) if mode == "remap" else None,
+                    prev_master=dev(prev[0]) if mode == "remap" else None,
+                    prev_exp_avg=dev(prev[1]) if mode == "remap" else None,
+                    prev_exp_avg_sq=dev(prev[2]) if mode == "remap" else None,
+                    init_master=dev(W + np.float32(1e-3)) if master else None)
+            bufs.append(zf.MatrixBuffers(
+                grad=bf16_dev(g, ld=ld_m), k=k, sel=sel_dev(new), weight=bf16_dev(W, ld=ld_m),
+                master=P, exp_avg=M, exp_avg_sq=V, src=src, layout=RM,
+                acc=_buf(n, m - k, torch.float32, False, 0.0)))
+        plan = zf.Plan(bufs)
+        plan.update(HP, 3, zf.STATES_INIT if mode == "init" else zf.STATES_REMAP, 1, 4,
+                    pack=pack)
+        torch.cuda.synchronize()
+        res.append([x for b in bufs for x in (f32_np(b.master), f32_np(b.exp_avg),
+                                              f32_np(b.exp_avg_sq), bits_np(b.weight))])
+        plan.close()
+    for i, (a, b) in enumerate(zip(*res)):
+        assert np.array_equal(np.ascontiguousarray(a).view(np.uint8),
+                              np.ascontiguousarray(b).view(np.uint8)), i
