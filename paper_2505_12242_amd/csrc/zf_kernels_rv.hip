@@ -78,7 +78,7 @@ __device__ __forceinline__ u32x4 as_u4(float a, float b, float c, float d) {
   return u32x4{__float_as_uint(a), __float_as_uint(b), __float_as_uint(c), __float_as_uint(d)};
 }
 
-template <bool BATCHED, bool ADAM, bool PACK, bool HAND, bool STATS>
+template <bool BATCHED, bool ADAM, bool PACK, bool HAND, bool STATS, bool A16>
 __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __restrict__ mats,
                                                              const int64_t* __restrict__ off,
                                                              int32_t nmats, DevMat one, AdamK c,
@@ -86,7 +86,7 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
                                                              double* __restrict__ zs) {
   static_assert(!STATS || (ADAM && PACK && !HAND), "statistics of the fused update");
   __shared__ __attribute__((aligned(16))) uint16_t sg[kRvBatch][kRvMaxCols];
-  __shared__ __attribute__((aligned(16))) uint16_t sa[PACK ? kRvBatch : 1][PACK ? kRvMaxCols : 8];
+  __shared__ __attribute__((aligned(16))) uint16_t sa[A16 ? kRvBatch : 1][A16 ? kRvMaxCols : 8];
   __shared__ __attribute__((aligned(16))) float sd[HAND ? kRvBatch : 1][HAND ? kRvMaxCols : 4];
 
   int64_t local;
@@ -169,7 +169,7 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
   uint32_t sA = 0, sS = 0, sW = 0, sD = 0;
   rsrc_t rT = rsrc_t();
   uint32_t sT = 0;
-  const bool a16 = PACK && d.acc1 != nullptr;
+  const bool a16 = A16 && PACK && d.acc1 != nullptr;
   const bool put16 = a16 && first == 1 && !HAND;  // store G rows to the stage
   const bool get16 = a16 && first == 2;           // read the stage rows
   if constexpr (PACK) {
@@ -396,15 +396,30 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
   }
 }
 
+template <bool ADAM, bool PACK, bool HAND, bool STATS, bool A16>
+void launch_rv_a(const Table& t, const DevMat& one, dim3 grid, const AdamK& c, int32_t first,
+                 float scale, hipStream_t s, double* zs) {
+  if (t.mats != nullptr)
+    hipLaunchKernelGGL((rv_update_kernel<true, ADAM, PACK, HAND, STATS, A16>), grid,
+                       dim3(kThreads), 0, s, t.mats, t.off, t.nmats, one, c, first, scale, zs);
+  else
+    hipLaunchKernelGGL((rv_update_kernel<false, ADAM, PACK, HAND, STATS, A16>), grid,
+                       dim3(kThreads), 0, s, t.mats, t.off, t.nmats, one, c, first, scale, zs);
+}
+
+// The stage's code (and its registers and LDS) only in the launches of the
+// phases that use it: an interval's first step without the hand-over, and
+// its second step.  (Zen-auto statistics never run with a row-major stage.)
 template <bool ADAM, bool PACK, bool HAND, bool STATS = false>
 void launch_rv_t(const Table& t, const DevMat& one, dim3 grid, const AdamK& c, int32_t first,
                  float scale, hipStream_t s, double* zs = nullptr) {
-  if (t.mats != nullptr)
-    hipLaunchKernelGGL((rv_update_kernel<true, ADAM, PACK, HAND, STATS>), grid, dim3(kThreads), 0,
-                       s, t.mats, t.off, t.nmats, one, c, first, scale, zs);
-  else
-    hipLaunchKernelGGL((rv_update_kernel<false, ADAM, PACK, HAND, STATS>), grid, dim3(kThreads),
-                       0, s, t.mats, t.off, t.nmats, one, c, first, scale, zs);
+  if constexpr (PACK && !STATS) {
+    if (first == 2 || (first == 1 && !HAND)) {
+      launch_rv_a<ADAM, PACK, HAND, STATS, true>(t, one, grid, c, first, scale, s, zs);
+      return;
+    }
+  }
+  launch_rv_a<ADAM, PACK, HAND, STATS, false>(t, one, grid, c, first, scale, s, zs);
 }
 
 }  // namespace
