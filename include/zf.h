@@ -465,7 +465,8 @@ zf_status zf_plan_update_adam_handover(zf_plan* plan, const zf_adam_hparams* hp,
 /* zf_plan_unpack for an interval that ended after its first step on a plan
  * whose every descriptor gives acc_first: the unselected channels' rows
  * are scale times their widened stage rows (the first step's values),
- * selected rows +0.0.  ZF_EINVAL when a descriptor has no stage. */
+ * selected rows +0.0.  Channel-major plans; ZF_EINVAL for a row-major plan
+ * or when a descriptor has no stage. */
 zf_status zf_plan_unpack_first(zf_plan* plan, float scale, zf_stream stream);
 
 /* zf_unpack over every matrix into its `unpacked` buffer. */
