@@ -530,6 +530,15 @@ class SelectiveUpdateRunner:
                 raise ValueError(f"state_dict {key} = {sd[key]!r}, this runner has {val!r}")
         self.sync()
         self.cur, self.cur_a = 0, 0
+        # the next step is an interval's second: with the stage it reads the
+        # first step's values there, whichever runner saved them
+        t_saved = int(sd["t"])
+        if self.zen_tau is None:
+            k = schedule(t_saved, self.R, self.S, self.warmup) if t_saved >= 1 else None
+            first_only = k is not None and k.step_in_interval == 1 and not k.interval_end
+        else:
+            first_only = int(sd["length"]) == 1 and not bool(sd["ended"])
+        to_stage = self.use_stage and (bool(sd.get("in_stage")) or first_only)
         for q, d in enumerate(sd["mats"]):
             s = self.sels[0][q]
             for dst, key in ((s.sel_idx, "sel_idx"), (s.unsel_idx, "unsel_idx"),
@@ -537,19 +546,18 @@ class SelectiveUpdateRunner:
                 dst.copy_(d[key])
             for dst, key in zip(self.states[0][q], ("master", "exp_avg", "exp_avg_sq")):
                 dst.copy_(d[key])
-            if sd.get("in_stage") and self.use_stage:
+            if to_stage:
                 # first-step values (exact in bf16) into the unselected rows
                 self.stage[q].index_copy_(1 if self.layout == ROW_MAJOR else 0,
                                           s.unsel_idx.long(),
                                           d["acc"].to(self.device, torch.bfloat16))
-            else:
-                self.accs[0][q].copy_(d["acc"])
+            self.accs[0][q].copy_(d["acc"])
             if self.offload:
                 for dst, src in zip(self.store[q], d["store"]):
                     dst.copy_(src)
         self.t, self.th = int(sd["t"]), int(sd["th"])
         self._length, self._ended = int(sd["length"]), bool(sd["ended"])
-        self._in_stage = bool(sd.get("in_stage")) and self.use_stage
+        self._in_stage = to_stage
         self._acc_free = [None] * len(self._acc_free)
         torch.cuda.synchronize(self.device)
 
