@@ -15,6 +15,7 @@ from .configs import (  # noqa: F401
     get_workload,
     llama_layer_shapes,
 )
+from .edges import edge_bf16, edge_f32, sprinkle_nonfinite  # noqa: F401
 from .synth import (  # noqa: F401
     base_scales,
     derive_seed,
