@@ -34,8 +34,12 @@
  * Conventions shared by every entry point
  * ---------------------------------------
  * Memory.   Every pointer argument is a DEVICE pointer unless marked HOST.
- *           The caller owns all memory.  Only zf_plan_create allocates
- *           (its device tables and workspace, freed by zf_plan_destroy).
+ *           The caller owns all memory; the library allocates no device
+ *           memory.  Workspaces and a plan's device tables live in buffers
+ *           the caller provides, sized by the *_workspace_bytes and
+ *           zf_plan_query calls.  The only allocation the library makes is
+ *           the host-side plan handle (zf_plan_create, freed by
+ *           zf_plan_destroy).
  * Streams.  Work is enqueued on `stream` (a hipStream_t; NULL = the null
  *           stream); calls return without synchronising.  Device-side
  *           faults surface at the caller's next synchronisation.
@@ -70,7 +74,8 @@
  *           [1, accum_interval], invalid hyperparameters, or the gradient
  *           overlapping an output.  ZF_EWORKSPACE: workspace too small.
  *           ZF_EHIP: a HIP call failed (zf_last_hip_error() gives its code,
- *           per thread).  ZF_ENOMEM: a plan's device allocation failed.
+ *           per thread).  ZF_ENOMEM: the plan's host handle could not be
+ *           allocated.
  *           Sizes n = 0 or m = 0 are valid and enqueue no work, except that
  *           zf_colnorm with n = 0 writes zeros to its m scores.  Limits:
  *           n, m < 2^30; in the row-major layout the update and unpack
@@ -408,16 +413,31 @@ typedef struct zf_plan zf_plan;
  * (zf_plan_update_pending, zf_plan_update_zen_pending) reject any plan with
  * a stage (ZF_EINVAL). */
 
-/* Validates nmats >= 1 descriptors (HOST array, copied), computes the launch
- * geometry and allocates the plan's device tables and column-score
- * workspace (synchronous upload on the null stream).  *out receives the plan
- * (HOST handle). */
-zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out);
+/* Device bytes a plan over these descriptors needs (its descriptor tables
+ * and its workspaces: column-score partials of row-major matrices,
+ * Zen-auto partials).  Validates the descriptors as zf_plan_create does;
+ * no device work.  mats: HOST array of nmats >= 1 descriptors;
+ * device_bytes: HOST, receives the size. */
+zf_status zf_plan_query(const zf_matrix* mats, int32_t nmats, size_t* device_bytes);
 
-/* Frees a plan and its device memory (synchronises the device first). */
+/* Builds a plan in caller-provided device memory: validates nmats >= 1
+ * descriptors (HOST array, copied into the plan), computes the launch
+ * geometry and enqueues, on `stream`, the upload of the descriptor tables
+ * to the start of device_mem (the rest is the plan's workspace).  The
+ * upload is stream-ordered: launches of the plan on `stream`, or on a
+ * stream ordered after it, see the tables.  device_mem: at least
+ * zf_plan_query's bytes, 256-byte aligned, owned by the caller, not
+ * touched by anything else while the plan is used.  *out receives the plan
+ * (a HOST handle, the only memory the library allocates).  ZF_EWORKSPACE
+ * when device_bytes is too small; nothing is enqueued on any error. */
+zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, void* device_mem,
+                         size_t device_bytes, zf_stream stream, zf_plan** out);
+
+/* Frees the plan's host handle.  No device call and no synchronisation:
+ * the caller frees device_mem once the plan's launches have completed. */
 void zf_plan_destroy(zf_plan* plan);
 
-/* Device bytes a plan holds (tables + workspace). */
+/* Device bytes the plan uses of its device_mem (tables + workspace). */
 size_t zf_plan_device_bytes(const zf_plan* plan);
 
 /* zf_colnorm over every matrix of the plan (one workspace shared by the

@@ -93,7 +93,9 @@ SIGNATURES = [
     ("zf_unpack", ctypes.c_int,
      [c_vp, c_i64, ctypes.POINTER(ZfSelection), c_i64, c_i64, c_i64, c_i32, c_flt, c_vp, c_i64,
       c_vp]),
-    ("zf_plan_create", ctypes.c_int, [ctypes.POINTER(ZfMatrix), c_i32, ctypes.POINTER(c_vp)]),
+    ("zf_plan_query", ctypes.c_int, [ctypes.POINTER(ZfMatrix), c_i32, ctypes.POINTER(c_sz)]),
+    ("zf_plan_create", ctypes.c_int,
+     [ctypes.POINTER(ZfMatrix), c_i32, c_vp, c_sz, c_vp, ctypes.POINTER(c_vp)]),
     ("zf_plan_destroy", None, [c_vp]),
     ("zf_plan_device_bytes", c_sz, [c_vp]),
     ("zf_plan_colnorm", ctypes.c_int, [c_vp, c_vp]),
@@ -127,7 +129,7 @@ SIGNATURES = [
 def load(path: str = LIB_PATH) -> ctypes.CDLL:
     if not os.path.exists(path):
         raise RuntimeError(
-            f"libzf.so is not built ({path} missing); run `python -m paper_2505_12242_amd.build`")
+            f"libzf.so is not built ({path} missing); run `python paper_2505_12242_amd/build.py`")
     lib = ctypes.CDLL(path)
     for name, res, args in SIGNATURES:
         fn = getattr(lib, name)
@@ -580,14 +582,34 @@ class ZenTotals:
 
 
 class Plan:
-    """A batch of matrices run by one launch per kernel (zf_plan_*)."""
+    """A batch of matrices run by one launch per kernel (zf_plan_*).
 
-    def __init__(self, mats: Sequence[MatrixBuffers]):
+    The plan's device tables and workspace live in a torch buffer owned by
+    this object (sized by zf_plan_query).  The tables are uploaded on
+    `stream` (default: the current stream), which is then synchronised, so
+    the plan can be launched on any stream.  close() synchronises the
+    device before the buffer is released (kernels in flight may still read
+    the tables)."""
+
+    def __init__(self, mats: Sequence[MatrixBuffers], stream=None):
         self.mats: List[MatrixBuffers] = list(mats)  # keeps the tensors alive
         arr = (ZfMatrix * len(self.mats))(*[b.as_c() for b in self.mats])
+        nbytes = c_sz()
+        _check("zf_plan_query", LIB.zf_plan_query(arr, len(self.mats), ctypes.byref(nbytes)))
+        dev = self.mats[0].grad.device if self.mats[0].grad is not None else None
+        if dev is None or dev.type != "cuda":
+            dev = torch.device("cuda", torch.cuda.current_device())
+        self.device = dev
+        # 256-byte aligned start inside the buffer
+        self._mem = torch.empty(nbytes.value + 256, dtype=torch.uint8, device=dev)
+        base = self._mem.data_ptr()
+        aligned = (base + 255) & ~255
+        st = stream if stream is not None else torch.cuda.current_stream(dev)
         h = c_vp()
-        _check("zf_plan_create", LIB.zf_plan_create(arr, len(self.mats), ctypes.byref(h)))
+        _check("zf_plan_create", LIB.zf_plan_create(arr, len(self.mats), aligned, nbytes.value,
+                                                   st.cuda_stream, ctypes.byref(h)))
         self._h = h
+        st.synchronize()
 
     @property
     def device_bytes(self) -> int:
@@ -696,8 +718,10 @@ class Plan:
 
     def close(self) -> None:
         if getattr(self, "_h", None):
+            torch.cuda.synchronize(self.device)  # launches may still read the tables
             LIB.zf_plan_destroy(self._h)
             self._h = None
+            self._mem = None
 
     def __del__(self):
         try:

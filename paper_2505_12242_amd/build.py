@@ -1,6 +1,10 @@
 """Builds libzf.so (the HIP library behind include/zf.h) in-tree for gfx950.
 
-    python -m paper_2505_12242_amd.build
+    python paper_2505_12242_amd/build.py
+
+(run as a script: importing the package loads the library it is about to
+rebuild).  Each source is compiled to an object file in parallel, then
+linked.
 
 Flags: -ffp-contract=off and correctly rounded fp32 division / square root
 keep every arithmetic line of the kernels a single IEEE operation; packed
@@ -10,6 +14,7 @@ import os
 import shutil
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
@@ -35,20 +40,37 @@ def hipcc() -> str:
     return path
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp"
-    cmd = [hipcc(), *FLAGS, "-I", INCLUDE, "-I", CSRC, "-o", tmp,
-           *[os.path.join(CSRC, s) for s in SOURCES]]
+OBJ_DIR = os.path.join(ROOT, "_build")
+
+
+def _run(cmd, verbose, what):
     if verbose:
         print(" ".join(cmd), flush=True)
     proc = subprocess.run(cmd, capture_output=True, text=True)
     if proc.returncode != 0:
         sys.stderr.write(proc.stdout + proc.stderr)
-        raise RuntimeError(f"hipcc failed with exit code {proc.returncode}")
+        raise RuntimeError(f"hipcc failed on {what} (exit code {proc.returncode})")
     noise = [ln for ln in (proc.stdout + proc.stderr).splitlines()
              if ln.strip() and "packed-fp32-ops" not in ln]
     if verbose and noise:
         sys.stderr.write("\n".join(noise) + "\n")
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(OBJ_DIR, exist_ok=True)
+    compile_flags = [f for f in FLAGS if f != "-shared"]
+    objs = [os.path.join(OBJ_DIR, os.path.splitext(src)[0] + ".o") for src in SOURCES]
+
+    def compile_one(i):
+        _run([hipcc(), *compile_flags, "-I", INCLUDE, "-I", CSRC, "-c",
+              os.path.join(CSRC, SOURCES[i]), "-o", objs[i]], verbose, SOURCES[i])
+
+    jobs = max(1, min(len(SOURCES), os.cpu_count() or 1))
+    with ThreadPoolExecutor(jobs) as ex:
+        list(ex.map(compile_one, range(len(SOURCES))))
+    tmp = LIB + ".tmp"
+    _run([hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-pthread", "-o", tmp, *objs],
+         verbose, "the link of libzf.so")
     os.replace(tmp, LIB)
     build_abi_smoke(verbose)
     return LIB

@@ -554,7 +554,7 @@ const char* zf_status_string(int status) {
     case ZF_EINVAL: return "ZF_EINVAL: invalid argument";
     case ZF_EWORKSPACE: return "ZF_EWORKSPACE: workspace too small";
     case ZF_EHIP: return "ZF_EHIP: HIP call failed";
-    case ZF_ENOMEM: return "ZF_ENOMEM: device allocation failed";
+    case ZF_ENOMEM: return "ZF_ENOMEM: host allocation failed";
     default: return "unknown zf status";
   }
 }
@@ -727,8 +727,11 @@ struct zf_plan {
   int32_t nmats = 0;
   int32_t layout = 0;
   std::vector<DevMat> mats;
-  void* dev = nullptr;
-  size_t dev_bytes = 0;
+  void* dev = nullptr;     // caller-provided device memory (tables, then workspaces)
+  size_t dev_bytes = 0;    // bytes of it the plan uses
+  size_t head_bytes = 0;   // descriptor tables at the start of dev
+  std::vector<char> image;  // host image of the tables, the source of the upload
+  int64_t ws_doubles = 0, zs_doubles = 0, zb_doubles = 0;
   DevMat* d_mats = nullptr;
   int64_t* d_off_cn = nullptr;
   int64_t* d_off_fin = nullptr;
@@ -881,23 +884,17 @@ zf_status check_plan_matrix(const zf_matrix& x, zf_plan& p) {
   return ZF_OK;
 }
 
-}  // namespace
-
-extern "C" {
-
-zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
-  if (mats == nullptr || nmats < 1 || out == nullptr) return ZF_EINVAL;
-  zf_plan* p = new (std::nothrow) zf_plan();
-  if (p == nullptr) return ZF_ENOMEM;
+// Validates the descriptors and computes everything a plan holds on the
+// host: geometry, grids, the host image of its device tables and the size
+// of its workspaces.  No device work.
+zf_status build_plan_impl(const zf_matrix* mats, int32_t nmats, zf_plan* p) {
+  if (mats == nullptr || nmats < 1) return ZF_EINVAL;
   p->nmats = nmats;
   p->layout = mats[0].layout;
   std::vector<std::pair<int64_t, int64_t>> shapes;
   for (int32_t q = 0; q < nmats; ++q) {
     const zf_status st = check_plan_matrix(mats[q], *p);
-    if (st != ZF_OK) {
-      delete p;
-      return st;
-    }
+    if (st != ZF_OK) return st;
     shapes.emplace_back(mats[q].n, mats[q].m);
   }
   const int cn_rows = pick_colnorm_rows(shapes);
@@ -923,10 +920,7 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
     DevMat d = plan_mat(mats[q]);
     finish_geometry(d, cn_rows, up_rows);
     set_rv(d, rv_rows, all_rv);
-    if (!cm && !rm_strides_ok(d)) {
-      delete p;
-      return ZF_EINVAL;
-    }
+    if (!cm && !rm_strides_ok(d)) return ZF_EINVAL;
     d.cn_ws = ws_doubles;
     if (!cm) ws_doubles += static_cast<int64_t>(d.cn_rb) * d.m;
     d.zs_off = zs_doubles;
@@ -970,23 +964,45 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   const int64_t max_blocks = (int64_t(1) << 31) / zf::kThreads;
   if (p->blk_cn >= max_blocks || p->blk_up >= max_blocks || p->blk_unp >= max_blocks ||
       p->blk_upv >= max_blocks || p->blk_sel >= max_blocks ||
-      p->blk_zp >= max_blocks) {
-    delete p;
+      p->blk_zp >= max_blocks)
     return ZF_EINVAL;  // grid too large for one launch
-  }
 
   const size_t mats_bytes = sizeof(DevMat) * nmats;
   const size_t off_bytes = sizeof(int64_t) * (nmats + 1);
   const size_t head = (mats_bytes + 9 * off_bytes + 255) & ~size_t(255);
-  const int64_t zb_doubles = p->can_zen ? 2 * p->blk_zen : 0;
-  p->dev_bytes = head + sizeof(double) * static_cast<size_t>(ws_doubles + zs_doubles + zb_doubles);
-  hipError_t e = hipMalloc(&p->dev, p->dev_bytes);
-  if (e != hipSuccess) {
-    g_last_hip_error = static_cast<int>(e);
-    delete p;
+  p->ws_doubles = ws_doubles;
+  p->zs_doubles = zs_doubles;
+  p->zb_doubles = p->can_zen ? 2 * p->blk_zen : 0;
+  p->head_bytes = head;
+  p->dev_bytes =
+      head + sizeof(double) * static_cast<size_t>(ws_doubles + zs_doubles + p->zb_doubles);
+  p->image.assign(head, 0);
+  char* img = p->image.data();
+  std::memcpy(img, p->mats.data(), mats_bytes);
+  const std::vector<int64_t>* offs[9] = {&off_cn, &off_fin, &off_top, &off_up, &off_unp,
+                                         &off_zen, &off_zp, &off_upv, &off_sel};
+  for (int a = 0; a < 9; ++a)
+    std::memcpy(img + mats_bytes + a * off_bytes, offs[a]->data(), off_bytes);
+  return ZF_OK;
+}
+
+// build_plan_impl with host allocation failures (std::bad_alloc from its
+// vectors) turned into a status: no exception crosses the C ABI.
+zf_status build_plan(const zf_matrix* mats, int32_t nmats, zf_plan* p) {
+  try {
+    return build_plan_impl(mats, nmats, p);
+  } catch (...) {
     return ZF_ENOMEM;
   }
-  char* base = static_cast<char*>(p->dev);
+}
+
+// Points the plan's tables and workspaces into `dev` (the table layout of
+// build_plan's image).
+void place_plan(zf_plan* p, void* dev) {
+  const int32_t nmats = p->nmats;
+  const size_t mats_bytes = sizeof(DevMat) * nmats;
+  char* base = static_cast<char*>(dev);
+  p->dev = dev;
   p->d_mats = reinterpret_cast<DevMat*>(base);
   p->d_off_cn = reinterpret_cast<int64_t*>(base + mats_bytes);
   p->d_off_fin = p->d_off_cn + (nmats + 1);
@@ -997,24 +1013,42 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   p->d_off_zp = p->d_off_zen + (nmats + 1);
   p->d_off_upv = p->d_off_zp + (nmats + 1);
   p->d_off_sel = p->d_off_upv + (nmats + 1);
-  p->d_ws = reinterpret_cast<double*>(base + head);
-  p->d_zs = p->d_ws + ws_doubles;
-  p->d_zb = p->d_zs + zs_doubles;
-  std::vector<char> host(head, 0);
-  std::memcpy(host.data(), p->mats.data(), mats_bytes);
-  std::memcpy(host.data() + mats_bytes, off_cn.data(), off_bytes);
-  std::memcpy(host.data() + mats_bytes + off_bytes, off_fin.data(), off_bytes);
-  std::memcpy(host.data() + mats_bytes + 2 * off_bytes, off_top.data(), off_bytes);
-  std::memcpy(host.data() + mats_bytes + 3 * off_bytes, off_up.data(), off_bytes);
-  std::memcpy(host.data() + mats_bytes + 4 * off_bytes, off_unp.data(), off_bytes);
-  std::memcpy(host.data() + mats_bytes + 5 * off_bytes, off_zen.data(), off_bytes);
-  std::memcpy(host.data() + mats_bytes + 6 * off_bytes, off_zp.data(), off_bytes);
-  std::memcpy(host.data() + mats_bytes + 7 * off_bytes, off_upv.data(), off_bytes);
-  std::memcpy(host.data() + mats_bytes + 8 * off_bytes, off_sel.data(), off_bytes);
-  e = hipMemcpy(p->dev, host.data(), head, hipMemcpyHostToDevice);
+  p->d_ws = reinterpret_cast<double*>(base + p->head_bytes);
+  p->d_zs = p->d_ws + p->ws_doubles;
+  p->d_zb = p->d_zs + p->zs_doubles;
+}
+
+}  // namespace
+
+extern "C" {
+
+zf_status zf_plan_query(const zf_matrix* mats, int32_t nmats, size_t* device_bytes) {
+  if (device_bytes == nullptr) return ZF_EINVAL;
+  zf_plan* p = new (std::nothrow) zf_plan();
+  if (p == nullptr) return ZF_ENOMEM;
+  const zf_status st = build_plan(mats, nmats, p);
+  if (st == ZF_OK) *device_bytes = p->dev_bytes;
+  delete p;
+  return st;
+}
+
+zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, void* device_mem,
+                         size_t device_bytes, zf_stream stream, zf_plan** out) {
+  if (out == nullptr || device_mem == nullptr || !aligned(device_mem, 256)) return ZF_EINVAL;
+  zf_plan* p = new (std::nothrow) zf_plan();
+  if (p == nullptr) return ZF_ENOMEM;
+  zf_status st = build_plan(mats, nmats, p);
+  if (st == ZF_OK && device_bytes < p->dev_bytes) st = ZF_EWORKSPACE;
+  if (st != ZF_OK) {
+    delete p;
+    return st;
+  }
+  place_plan(p, device_mem);
+  // stream-ordered upload of the tables; the host image stays with the plan
+  const hipError_t e = hipMemcpyAsync(p->dev, p->image.data(), p->head_bytes,
+                                      hipMemcpyHostToDevice, as_stream(stream));
   if (e != hipSuccess) {
     g_last_hip_error = static_cast<int>(e);
-    (void)hipFree(p->dev);
     delete p;
     return ZF_EHIP;
   }
@@ -1022,14 +1056,7 @@ zf_status zf_plan_create(const zf_matrix* mats, int32_t nmats, zf_plan** out) {
   return ZF_OK;
 }
 
-void zf_plan_destroy(zf_plan* plan) {
-  if (plan == nullptr) return;
-  if (plan->dev != nullptr) {
-    (void)hipDeviceSynchronize();
-    (void)hipFree(plan->dev);
-  }
-  delete plan;
-}
+void zf_plan_destroy(zf_plan* plan) { delete plan; }
 
 size_t zf_plan_device_bytes(const zf_plan* plan) { return plan ? plan->dev_bytes : 0; }
 

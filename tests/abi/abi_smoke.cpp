@@ -277,12 +277,21 @@ int main() {
       d.unpacked = x.D;
       d.ld_unpacked = x.ld_g();
     }
+    // the plans' tables and workspaces in memory this program allocates
+    size_t bytes1 = 0, bytes2 = 0;
+    ZF_OK_(zf_plan_query(desc, 2, &bytes1));
+    void* mem1 = nullptr;
+    HIP_OK(hipMalloc(&mem1, bytes1));
     zf_plan* plan1 = nullptr;
-    ZF_OK_(zf_plan_create(desc, 2, &plan1));
+    ZF_OK_(zf_plan_create(desc, 2, mem1, bytes1, s, &plan1));
+    CHECK(zf_plan_device_bytes(plan1) == bytes1);
     desc[0].grad = pa.G2;
     desc[1].grad = pb.G2;
+    ZF_OK_(zf_plan_query(desc, 2, &bytes2));
+    void* mem2 = nullptr;
+    HIP_OK(hipMalloc(&mem2, bytes2));
     zf_plan* plan2 = nullptr;
-    ZF_OK_(zf_plan_create(desc, 2, &plan2));
+    ZF_OK_(zf_plan_create(desc, 2, mem2, bytes2, s, &plan2));
     ZF_OK_(zf_plan_colnorm(plan1, s));
     ZF_OK_(zf_plan_topk_select(plan1, s));
     ZF_OK_(zf_plan_update(plan1, &kHp, 1, ZF_STATES_INIT, 1, 2, 1, 1, s));
@@ -292,6 +301,8 @@ int main() {
     CHECK(same_bits(down(pa.W, pa.n * pa.m), Wa) && same_bits(down(pb.W, pb.n * pb.m), Wb));
     zf_plan_destroy(plan1);
     zf_plan_destroy(plan2);
+    HIP_OK(hipFree(mem1));  // the stream was synchronised above
+    HIP_OK(hipFree(mem2));
     for (Mat* x : {&a, &b, &pa, &pb}) release(*x);
   }
   HIP_OK(hipStreamDestroy(s));

@@ -140,7 +140,23 @@ int main() {
   CHECK(zf_colnorm(nullptr, 4, 4, 4, 0, nullptr, nullptr, 0, nullptr) == ZF_EINVAL);
   CHECK(zf_topk_select(nullptr, 4, 0.5, nullptr, nullptr, nullptr) == ZF_EINVAL);
   zf_plan* plan = nullptr;
-  CHECK(zf_plan_create(nullptr, 1, &plan) == ZF_EINVAL);
+  size_t plan_bytes = 0;
+  CHECK(zf_plan_query(nullptr, 1, &plan_bytes) == ZF_EINVAL);
+  CHECK(zf_plan_create(nullptr, 1, nullptr, 0, nullptr, &plan) == ZF_EINVAL);
+  {
+    // valid (empty) descriptors: sized on the host; create rejects too
+    // little memory before any device call
+    zf_matrix d[2];
+    std::memset(d, 0, sizeof(d));
+    d[0].m = 4;
+    d[0].k = 1;
+    d[1].m = 9;
+    d[1].k = 2;
+    CHECK(zf_plan_query(d, 2, &plan_bytes) == ZF_OK && plan_bytes >= 256);
+    void* fake = reinterpret_cast<void*>(uintptr_t(1) << 40);
+    CHECK(zf_plan_create(d, 2, fake, plan_bytes - 1, nullptr, &plan) == ZF_EWORKSPACE);
+    CHECK(plan == nullptr);
+  }
   CHECK(zf_plan_update(nullptr, &hp, 1, 0, 1, 1, 1, 1, nullptr) == ZF_EINVAL);
   CHECK(zf_plan_update_zen(nullptr, &hp, 1, 0, 1, 4, 1.0, nullptr, nullptr) == ZF_EINVAL);
   CHECK(zf_plan_update_handover(nullptr, &hp, 1, 0, 1, 4, 1.0f, nullptr) == ZF_EINVAL);

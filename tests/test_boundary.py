@@ -184,15 +184,33 @@ def test_update_fused_validation():
 
 def test_plan_validation():
     h = ctypes.c_void_p()
-    assert LIB.zf_plan_create(None, 1, ctypes.byref(h)) == EINVAL
+    nb = ctypes.c_size_t()
+    mem = 1 << 20  # a 256-aligned stand-in address: never reached, the descriptors fail first
+    assert LIB.zf_plan_query(None, 1, ctypes.byref(nb)) == EINVAL
+    assert LIB.zf_plan_create(None, 1, mem, 1 << 20, None, ctypes.byref(h)) == EINVAL
     arr = (_lib.ZfMatrix * 1)()
-    assert LIB.zf_plan_create(arr, 0, ctypes.byref(h)) == EINVAL
+    assert LIB.zf_plan_query(arr, 0, ctypes.byref(nb)) == EINVAL
+    assert LIB.zf_plan_create(arr, 0, mem, 1 << 20, None, ctypes.byref(h)) == EINVAL
     arr[0].n, arr[0].m, arr[0].k = 4, 4, 5          # k > m
-    assert LIB.zf_plan_create(arr, 1, ctypes.byref(h)) == EINVAL
+    assert LIB.zf_plan_query(arr, 1, ctypes.byref(nb)) == EINVAL
+    assert LIB.zf_plan_create(arr, 1, mem, 1 << 20, None, ctypes.byref(h)) == EINVAL
     arr2 = (_lib.ZfMatrix * 2)()
     arr2[0].n, arr2[0].m, arr2[0].k, arr2[0].layout = 0, 4, 1, RM
     arr2[1].n, arr2[1].m, arr2[1].k, arr2[1].layout = 0, 4, 1, CM   # mixed layouts
-    assert LIB.zf_plan_create(arr2, 2, ctypes.byref(h)) == EINVAL
+    assert LIB.zf_plan_query(arr2, 2, ctypes.byref(nb)) == EINVAL
+    assert LIB.zf_plan_create(arr2, 2, mem, 1 << 20, None, ctypes.byref(h)) == EINVAL
+    # valid descriptors (empty matrices): the size query succeeds on the host,
+    # and create rejects missing, misaligned or too small device memory
+    # before enqueueing anything
+    ok = (_lib.ZfMatrix * 2)()
+    ok[0].n, ok[0].m, ok[0].k, ok[0].layout = 0, 4, 1, RM
+    ok[1].n, ok[1].m, ok[1].k, ok[1].layout = 0, 9, 2, RM
+    assert LIB.zf_plan_query(ok, 2, ctypes.byref(nb)) == 0 and nb.value >= 256
+    assert LIB.zf_plan_query(ok, 2, None) == EINVAL
+    assert LIB.zf_plan_create(ok, 2, None, nb.value, None, ctypes.byref(h)) == EINVAL
+    assert LIB.zf_plan_create(ok, 2, mem + 8, nb.value, None, ctypes.byref(h)) == EINVAL
+    assert LIB.zf_plan_create(ok, 2, mem, nb.value - 1, None, ctypes.byref(h)) == EWS
+    assert LIB.zf_plan_create(ok, 2, mem, nb.value, None, None) == EINVAL
     assert LIB.zf_plan_colnorm(None, None) == EINVAL
     assert LIB.zf_plan_update(None, None, 1, 0, 1, 1, 1, 1, None) == EINVAL
     hp = _lib.ZfAdamHparams(1e-5, 0.9, 0.999, 1e-8, 0.0)
