@@ -218,6 +218,24 @@ zf_status zf_colnorm(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad
                      int32_t layout, float* norms_sq, void* ws, size_t ws_bytes,
                      zf_stream stream);
 
+/* For callers that cannot allocate device memory or pass a workspace (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): zf_colnorm with its workspace in an array of
+ * ZF_STATIC_SCRATCH_BYTES that the library holds on each GPU it runs on,
+ * from the first call on that GPU until the process ends.  Arguments and
+ * results as in zf_colnorm.  Allocates nothing: the first call on a GPU
+ * only looks up that array's device address.  ZF_EWORKSPACE (nothing
+ * enqueued) when zf_colnorm_workspace_bytes(n, m, layout) exceeds
+ * ZF_STATIC_SCRATCH_BYTES (row-major: ceil(n / rows per block) * m * 8
+ * bytes, 4-15 MiB for the Llama-2 shapes; channel-major needs none).  Every
+ * call on one GPU shares that GPU's array: calls that may overlap on one
+ * GPU (other streams, other host threads) race and must be ordered by the
+ * caller.  Nothing in the array needs to start at zero; each call writes
+ * every part it reads. */
+#define ZF_STATIC_SCRATCH_BYTES (32u << 20)
+zf_status zf_colnorm_noalloc(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
+                             int32_t layout, float* norms_sq, zf_stream stream);
+
 /* ---- a2: selection ------------------------------------------------------ */
 
 /* Selects the k = zf_k_from_ratio(ratio, m) columns with the largest score.

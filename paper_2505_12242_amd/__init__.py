@@ -12,6 +12,7 @@ from ._lib import (  # noqa: F401
     LIB,
     LIB_PATH,
     ROW_MAJOR,
+    STATIC_SCRATCH_BYTES,
     STATES_INIT,
     STATES_INPLACE,
     STATES_REMAP,
@@ -26,6 +27,7 @@ from ._lib import (  # noqa: F401
     adam_selected,
     alloc_stored,
     colnorm,
+    colnorm_noalloc,
     colnorm_workspace_bytes,
     host_adam_unselected,
     k_from_ratio,

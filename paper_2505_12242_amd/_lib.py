@@ -73,6 +73,7 @@ SIGNATURES = [
     ("zf_k_from_ratio", c_i64, [c_dbl, c_i64]),
     ("zf_colnorm_workspace_bytes", c_sz, [c_i64, c_i64, c_i32]),
     ("zf_colnorm", ctypes.c_int, [c_vp, c_i64, c_i64, c_i64, c_i32, c_vp, c_vp, c_sz, c_vp]),
+    ("zf_colnorm_noalloc", ctypes.c_int, [c_vp, c_i64, c_i64, c_i64, c_i32, c_vp, c_vp]),
     ("zf_topk_select", ctypes.c_int,
      [c_vp, c_i64, c_dbl, ctypes.POINTER(ZfSelection), ctypes.POINTER(c_i64), c_vp]),
     ("zf_adam_selected", ctypes.c_int,
@@ -295,6 +296,22 @@ def colnorm(grad: torch.Tensor, out: Optional[torch.Tensor] = None,
         workspace = torch.empty(max(need, 8), dtype=torch.uint8, device=grad.device)
     _check("zf_colnorm", LIB.zf_colnorm(_ptr(grad), n, m, ld, layout, _ptr(out),
                                         _ptr(workspace), workspace.numel(), _stream(stream)))
+    return out
+
+
+STATIC_SCRATCH_BYTES = 32 << 20  # ZF_STATIC_SCRATCH_BYTES
+
+
+def colnorm_noalloc(grad: torch.Tensor, out: torch.Tensor, layout: int = ROW_MAJOR,
+                    stream=None) -> torch.Tensor:
+    """zf_colnorm_noalloc: the column scores with the library's static
+    per-GPU workspace; `out` ([m] fp32 on the GPU) is caller-provided, so
+    the call allocates nothing."""
+    n, m = _logical(grad, layout)
+    ld = _mat(grad, torch.bfloat16, "grad")
+    _vec(out, torch.float32, "out", m)
+    _check("zf_colnorm_noalloc", LIB.zf_colnorm_noalloc(_ptr(grad), n, m, ld, layout, _ptr(out),
+                                                        _stream(stream)))
     return out
 
 

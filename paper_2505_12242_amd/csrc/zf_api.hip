@@ -2,8 +2,10 @@
 // constants and the batched plan.  Every check runs before the first HIP
 // call, so invalid arguments enqueue nothing (and never touch a device).
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -600,6 +602,68 @@ zf_status zf_colnorm(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad
                            ceil_div(m, zf::kFinalizeCols), static_cast<double*>(ws),
                            as_stream(stream));
   return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
+}  // extern "C"
+
+// ---- allocation-free column scores -----------------------------------------
+// The workspace of zf_colnorm_noalloc: one array per GPU, part of this
+// library's device code object (it lives as long as the process).  In host
+// code `scratch` only names the symbol; its device address comes from
+// hipGetSymbolAddress, once per device.
+static __device__ __align__(256) double scratch[ZF_STATIC_SCRATCH_BYTES / sizeof(double)];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_ptr[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// Device address of `scratch` on the device `stream` belongs to (the
+// current device for the null stream).  The first call for a device looks
+// it up with that device current.
+zf_status scratch_for(hipStream_t stream, void** out) {
+  int dev = 0;
+  hipError_t e = stream != nullptr ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e);
+  if (dev < 0 || dev >= kMaxDevices) return ZF_EINVAL;
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (p == nullptr) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+    if (p == nullptr) {
+      int cur = 0;
+      e = hipGetDevice(&cur);
+      if (e == hipSuccess && cur != dev) e = hipSetDevice(dev);
+      if (e == hipSuccess) e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      if (cur != dev) (void)hipSetDevice(cur);
+      if (e != hipSuccess) return hip_fail(e);
+      if (p == nullptr) return hip_fail(hipErrorInvalidSymbol);
+      g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return ZF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+zf_status zf_colnorm_noalloc(const uint16_t* grad, int64_t n, int64_t m, int64_t ld_grad,
+                             int32_t layout, float* norms_sq, zf_stream stream) {
+  // the same host validation as zf_colnorm, before the scratch is looked up
+  if (!layout_ok(layout) || !shape_ok(n, m, 0) ||
+      !mat_ok(grad, ext(layout, n, m), ld_grad, 2) || !vector_ok(norms_sq, m, 4))
+    return ZF_EINVAL;
+  const size_t need = zf_colnorm_workspace_bytes(n, m, layout);
+  if (need > ZF_STATIC_SCRATCH_BYTES) return ZF_EWORKSPACE;
+  void* ws = nullptr;
+  if (need > 0) {
+    const zf_status st = scratch_for(as_stream(stream), &ws);
+    if (st != ZF_OK) return st;
+  }
+  return zf_colnorm(grad, n, m, ld_grad, layout, norms_sq, ws, need, stream);
 }
 
 zf_status zf_topk_select(const float* norms_sq, int64_t m, double ratio, const zf_selection* out,

@@ -182,6 +182,21 @@ def test_update_fused_validation():
                                None) == EINVAL
 
 
+def test_colnorm_noalloc_validation():
+    """The allocation-free column scores reject on the host, before the
+    static workspace is looked up: invalid arguments, and sizes whose
+    workspace exceeds the static array."""
+    n, m = 16384, 65536
+    assert LIB.zf_colnorm_workspace_bytes(n, m, RM) == _lib.STATIC_SCRATCH_BYTES
+    assert LIB.zf_colnorm_noalloc(A, n, m + 1, m + 8, RM, B, None) == EWS
+    assert LIB.zf_colnorm_noalloc(A, 1 << 20, 4096, 4096, RM, B, None) == EWS  # 128 MiB
+    assert LIB.zf_colnorm_noalloc(None, 4, 8, 8, RM, B, None) == EINVAL
+    assert LIB.zf_colnorm_noalloc(A, 4, 8, 7, RM, B, None) == EINVAL  # ld < width
+    assert LIB.zf_colnorm_noalloc(A, 4, 8, 8, 5, B, None) == EINVAL   # layout
+    assert LIB.zf_colnorm_noalloc(A, 4, 8, 8, RM, None, None) == EINVAL
+    assert LIB.zf_colnorm_noalloc(A, -1, 8, 8, RM, B, None) == EINVAL
+
+
 def test_plan_validation():
     h = ctypes.c_void_p()
     nb = ctypes.c_size_t()
