@@ -37,7 +37,7 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2505_12242_amd", "csrc", f)
                   for f in ("zf_device.hpp", "zf_internal.hpp", "zf_kernels.hip",
-                            "zf_kernels_cm.hip", "zf_kernels_rv.hip")]
+                            "zf_kernels_cm.hip", "zf_kernels_rv.hip", "zf_kernels_stream.hip")]
 
 
 def parse_args(argv=None):
@@ -81,9 +81,14 @@ def parse_args(argv=None):
                     help="hand over with a separate unpack pass after the last update of an "
                          "interval instead of fusing it into that update")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample", choices=["set", "layer"], default="set",
+                    help="matrices the all-core oracle timing covers: the whole set, or the "
+                         "first decoder layer (the one-thread timing always covers that layer)")
     ap.add_argument("--cpu-sample-steps", type=int, default=4)
-    ap.add_argument("--calibration-copy-gib", type=float, default=1.0,
-                    help="size of the plain copy launched once for PMC calibration (0: skip)")
+    ap.add_argument("--calibration-gib", type=float, default=8.0,
+                    help="size of the reference streams (read, copy, read-modify-write) timed "
+                         "before the workload; the copy is also the PMC calibration point "
+                         "(0: skip)")
     return ap.parse_args(argv)
 
 
@@ -91,10 +96,10 @@ def parse_args(argv=None):
 # byte model: the bytes each kernel must move, per matrix
 # ---------------------------------------------------------------------------
 
-def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool = False,
-               fused_handover: bool = False, second: bool = False, stage: bool = False,
-               scored_handover: bool = None) -> dict:
-    """Algorithmic HBM bytes of one step, by kernel.
+def step_traffic(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool = False,
+                 fused_handover: bool = False, second: bool = False, stage: bool = False,
+                 scored_handover: bool = None) -> dict:
+    """Algorithmic HBM bytes of one step, by kernel, as [read, written].
 
     colnorm  2nm (read G) + 4m (write scores)          refresh steps
     topk     4m (read scores) + 4m (write indices)
@@ -125,32 +130,49 @@ def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool 
     """
     if scored_handover is None:
         scored_handover = stage
-    out = {"colnorm": 0, "topk_select": 0, "update": 0, "unpack": 0}
+    out = {"colnorm": [0, 0], "topk_select": [0, 0], "update": [0, 0], "unpack": [0, 0]}
+
+    def add(cls, r, w):
+        out[cls][0] += r
+        out[cls][1] += w
+
     for (n, m), k in zip(shapes, ks):
         u = m - k
         staged_refresh = refresh and stage and fused_handover and not end
         scored_end = refresh and stage and scored_handover and fused_handover and end and first
         if refresh:
-            out["colnorm"] += (2 * n * m + 4 * m + (2 * n * m if staged_refresh else 0)
-                               + (4 * n * m if scored_end else 0))
-            out["topk_select"] += 8 * m + 12 * ((m + 63) // 64)
+            add("colnorm", 2 * n * m, 4 * m + (2 * n * m if staged_refresh else 0)
+                + (4 * n * m if scored_end else 0))
+            add("topk_select", 4 * m, 4 * m + 12 * ((m + 63) // 64))
+        # selected: G 2 + P/M/V 12 read, P/M/V 12 + W 2 written
+        add("update", 14 * n * k, 14 * n * k)
         if staged_refresh or scored_end:
-            per_u = 0
+            pass  # the score pass did the packing
         elif first:
-            # the fused hand-over of a one-step interval writes no packed values
-            per_u = 4 if (stage and not (end and fused_handover)) else 6
+            # G read; the fused hand-over of a one-step interval writes no
+            # packed values (it writes the hand-over: 4)
+            add("update", 2 * n * u, (2 if (stage and not (end and fused_handover)) else 4) * n * u)
         else:
-            per_u = 8 if (stage and second) else 10
-        out["update"] += 28 * n * k + per_u * n * u
+            # G and the previous sums (the stage's 2 B on the second step) read, 4 written
+            add("update", (4 if (stage and second) else 6) * n * u, 4 * n * u)
         if end:
             if offload:
-                out["unpack"] += 4 * n * u + 2 * n * u
+                add("unpack", 4 * n * u, 2 * n * u)
             elif fused_handover:
-                out["update"] += 4 * n * k
+                add("update", 0, 4 * n * k)
             else:
                 # the separate pass reads the stage after a one-step interval
-                out["unpack"] += (2 if (stage and first) else 4) * n * u + 4 * n * m
+                add("unpack", (2 if (stage and first) else 4) * n * u, 4 * n * m)
     return out
+
+
+def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool = False,
+               fused_handover: bool = False, second: bool = False, stage: bool = False,
+               scored_handover: bool = None) -> dict:
+    """step_traffic's bytes read + written, by kernel."""
+    t = step_traffic(shapes, ks, refresh, first, end, offload, fused_handover, second, stage,
+                     scored_handover)
+    return {cls: r + w for cls, (r, w) in t.items()}
 
 
 # ---------------------------------------------------------------------------
@@ -191,56 +213,247 @@ def build_set(wl, slots: int, device, layout: int = 0):
 # CPU oracle baseline on a bounded sample
 # ---------------------------------------------------------------------------
 
-def cpu_baseline(wl, shapes, ks, grad_slots, weights0, steps: int, layout: int = 0) -> dict:
-    """Times the oracle (as it stands) over the first decoder layer's seven
-    matrices for `steps` steps of the workload's schedule, on the host.
-    Inputs are copied to the host in the logical [out, in] layout before
-    timing."""
+def host_info() -> dict:
+    """The host the oracle is timed on: usable cores, CPU model, sockets /
+    NUMA nodes, memory."""
+    info = {"nproc": len(os.sched_getaffinity(0)), "cpu_count": os.cpu_count()}
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    info["model"] = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        import subprocess
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            key, _, val = line.partition(":")
+            if key.strip() in ("Socket(s)", "NUMA node(s)", "Thread(s) per core",
+                               "Core(s) per socket"):
+                info[key.strip()] = val.strip()
+    except Exception:
+        pass
+    try:
+        with open("/proc/meminfo") as f:
+            info["mem_GB"] = round(int(f.readline().split()[1]) * 1024 / 1e9, 1)
+    except (OSError, ValueError, IndexError):
+        pass
+    return info
+
+
+def _oracle_worker(conn) -> None:
+    """One process of the all-core oracle timing (spawned: no torch, no GPU).
+    Receives its matrices' jobs (shared-memory names of the initial bf16
+    weight and of the gradients, the step -> gradient map, the workload's
+    hyperparameters), builds one oracle per matrix, reports ready, and on
+    "go" runs the steps, timing them with the system-wide monotonic clock."""
+    import hashlib as _hl
+    from multiprocessing import shared_memory
+
     import numpy as np
-    import torch
     import oracle as O
 
-    def logical(t):
-        return t if layout == 0 else t.t()
+    jobs = conn.recv()
+    held, work = [], []
+    for job in jobs:
+        n, m = job["shape"]
 
-    qs = [q for q, mt in enumerate(wl.matrices) if mt.name.startswith("layers.0.")]
-    if not qs:
-        qs = [0]
+        def view(name):
+            shm = shared_memory.SharedMemory(name=name)
+            held.append(shm)
+            return np.ndarray((n, m), dtype=np.uint16, buffer=shm.buf)
+
+        W = view(job["w"])
+        G = [view(x) for x in job["g"]]
+        orc = O.MatrixOracle(O.widen(W), W, job["ratio"], *job["hyper"], job["R"], job["S"])
+        work.append((orc, G, job["slots"]))
+    conn.send("ready")
+    conn.recv()
+    t0 = time.monotonic()
+    for t in range(len(work[0][2]) if work else 0):
+        for orc, G, slots in work:
+            orc.step(G[slots[t]])
+    t1 = time.monotonic()
+    digests = [_hl.sha256(orc.P.tobytes() + orc.W.tobytes() + orc.A.tobytes()).hexdigest()[:16]
+               for orc, _, _ in work]
+    del work
+    for shm in held:
+        shm.close()
+    conn.send({"start": t0, "end": t1, "digests": digests})
+
+
+class HostSample:
+    """The oracle's inputs for the CPU baseline in shared memory (logical
+    [out, in] bf16 bits): every sampled matrix's initial weight, copied
+    before the GPU run changes it, and the gradients its steps read."""
+
+    def __init__(self, wl, qs, weights, layout: int):
+        from multiprocessing import shared_memory
+
+        import numpy as np
+        import torch
+        self.qs = list(qs)
+        self.shm = {}
+        self.layout = layout
+        self._np = np
+        self._shared_memory = shared_memory
+        for q in self.qs:
+            self.shm[("w", q)] = self._put(weights[q], torch)
+
+    def _put(self, t, torch):
+        x = t if self.layout == 0 else t.t()
+        n, m = x.shape
+        shm = self._shared_memory.SharedMemory(create=True, size=max(1, n * m * 2))
+        host = torch.from_numpy(self._np.ndarray((n, m), dtype=self._np.int16, buffer=shm.buf))
+        host.copy_(x.view(torch.int16))
+        return shm
+
+    def add_grads(self, grad_slots, steps: int):
+        """The gradients steps 1..steps read (step t reads ring slot
+        (t-1) mod len(grad_slots), as on the device)."""
+        import torch
+        ring = len(grad_slots)
+        self.steps = steps
+        self.used = sorted({(t - 1) % ring for t in range(1, steps + 1)})
+        self.step_slot = [self.used.index((t - 1) % ring) for t in range(1, steps + 1)]
+        for q in self.qs:
+            for s in self.used:
+                self.shm[("g", q, s)] = self._put(grad_slots[s][q], torch)
+
+    def array(self, key, shape):
+        return self._np.ndarray(shape, dtype=self._np.uint16, buffer=self.shm[key].buf)
+
+    def close(self):
+        for shm in self.shm.values():
+            shm.close()
+            shm.unlink()
+        self.shm = {}
+
+
+def cpu_baseline(wl, shapes, ks, sample: "HostSample", one_thread_qs, workers: int) -> dict:
+    """Times the oracle (as it stands) on the host over the sample's steps
+    1..steps of the workload's schedule:
+      one thread -- the matrices one_thread_qs in this process;
+      all cores  -- every sampled matrix, one process per core (matrices
+                    assigned longest first), all starting together; the
+                    wall time runs from the first start to the last end.
+    Each matrix's oracle is independent and deterministic, so the all-core
+    run gives the same results as one thread; the digests of the
+    one-thread matrices' final states are compared to show it."""
+    import hashlib as _hl
+
+    import oracle as O
     hp = wl.hyper
-    host_g = {}
-    for q in qs:
-        for t in range(1, steps + 1):
-            s = (t - 1) % len(grad_slots)
-            if (q, s) not in host_g:
-                host_g[(q, s)] = np.ascontiguousarray(
-                    logical(grad_slots[s][q]).contiguous().view(torch.int16).cpu().numpy()
-                    .view(np.uint16))
+    hyper = (hp.lr, hp.beta1, hp.beta2, hp.eps, hp.weight_decay)
+    steps = sample.steps
+    slots = sample.step_slot  # step t (0-based) -> index into sample.used
+
+    def sample_bytes(qs):
+        total = 0
+        for q in qs:
+            for t in range(1, steps + 1):
+                kind = O.schedule(t, wl.refresh, wl.accum)
+                total += sum(step_bytes([shapes[q]], [ks[q]], kind.refresh,
+                                        kind.step_in_interval == 1, kind.interval_end).values())
+        return total
+
+    # one thread, in this process
     elapsed = 0.0
-    nbytes = 0
-    for q in qs:
-        W = weights0[q]
-        orc = O.MatrixOracle(O.widen(W), W, wl.ratio, hp.lr, hp.beta1, hp.beta2, hp.eps,
-                             hp.weight_decay, wl.refresh, wl.accum)
-        for t in range(1, steps + 1):
-            G = host_g[(q, (t - 1) % len(grad_slots))]
+    digests1 = {}
+    for q in one_thread_qs:
+        n, m = shapes[q]
+        W = sample.array(("w", q), (n, m))
+        orc = O.MatrixOracle(O.widen(W), W, wl.ratio, *hyper, wl.refresh, wl.accum)
+        G = [sample.array(("g", q, s), (n, m)) for s in sample.used]
+        for t in range(steps):
             t0 = time.perf_counter()
-            out = orc.step(G)
+            orc.step(G[slots[t]])
             elapsed += time.perf_counter() - t0
-            kind = out["kind"]
-            b = step_bytes([shapes[q]], [ks[q]], kind.refresh, kind.step_in_interval == 1,
-                           kind.interval_end)
-            nbytes += sum(b.values())
-    params = sum(shapes[q][0] * shapes[q][1] for q in qs)
+        digests1[q] = _hl.sha256(orc.P.tobytes() + orc.W.tobytes() + orc.A.tobytes()).hexdigest()[:16]
+        del orc, G, W
+    b1 = sample_bytes(one_thread_qs)
+    p1 = sum(shapes[q][0] * shapes[q][1] for q in one_thread_qs)
+    out = {
+        "one_thread": {"GB/s": round(b1 / elapsed / 1e9, 4),
+                       "params_per_s": round(p1 * steps / elapsed, 1),
+                       "seconds": round(elapsed, 3),
+                       "sample": f"{len(one_thread_qs)} matrices ({p1:,} params), steps 1-{steps}"},
+    }
+
+    try:
+        out["all_cores"] = _all_cores(wl, shapes, ks, sample, workers, hyper, slots,
+                                      sample_bytes, digests1)
+    except Exception as e:  # the one-thread figure stands; say why
+        out["all_cores_error"] = f"{type(e).__name__}: {e}"
+    return out
+
+
+def _all_cores(wl, shapes, ks, sample, workers, hyper, slots, sample_bytes, digests1) -> dict:
+    """The all-core leg of cpu_baseline: one spawned process per core."""
+    import multiprocessing as mp
+    steps = sample.steps
+    qs = sorted(sample.qs, key=lambda q: -shapes[q][0] * shapes[q][1])
+    nw = max(1, min(workers, len(qs)))
+    assign = [[] for _ in range(nw)]
+    load = [0] * nw
+    for q in qs:
+        w = load.index(min(load))
+        assign[w].append(q)
+        load[w] += shapes[q][0] * shapes[q][1]
+    ctx = mp.get_context("spawn")
+    saved = {k: os.environ.get(k) for k in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS",
+                                            "MKL_NUM_THREADS")}
+    for k in saved:
+        os.environ[k] = "1"
+    procs, conns = [], []
+    try:
+        for w in range(nw):
+            a, b = ctx.Pipe()
+            p = ctx.Process(target=_oracle_worker, args=(b,), daemon=True)
+            p.start()
+            procs.append(p)
+            conns.append(a)
+    finally:
+        for k, v in saved.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+    for w in range(nw):
+        conns[w].send([{"shape": shapes[q], "w": sample.shm[("w", q)].name,
+                        "g": [sample.shm[("g", q, s)].name for s in sample.used],
+                        "slots": slots, "ratio": wl.ratio, "hyper": hyper, "R": wl.refresh,
+                        "S": wl.accum} for q in assign[w]])
+    def receive(c, timeout):
+        if not c.poll(timeout):
+            raise TimeoutError("an oracle process did not answer")
+        return c.recv()
+
+    try:
+        for c in conns:
+            if receive(c, 600) != "ready":
+                raise RuntimeError("an oracle process failed to start")
+        for c in conns:
+            c.send("go")
+        res = [receive(c, 1800) for c in conns]
+    finally:
+        for p in procs:
+            p.join(timeout=60)
+            if p.is_alive():
+                p.kill()
+    wall = max(r["end"] for r in res) - min(r["start"] for r in res)
+    digests = {q: d for w, r in enumerate(res) for q, d in zip(assign[w], r["digests"])}
+    ball = sample_bytes(sample.qs)
+    pall = sum(shapes[q][0] * shapes[q][1] for q in sample.qs)
     return {
-        "value": round(nbytes / elapsed / 1e9, 4),
-        "unit": "GB/s",
-        "params_per_s": round(params * steps / elapsed, 1),
-        "seconds": round(elapsed, 3),
-        "cores": 1,
-        "kind": "oracle",
-        "sample": (f"{len(qs)} matrices of the first decoder layer "
-                   f"({params:,} params), steps 1-{steps} of the R={wl.refresh}, "
-                   f"S={wl.accum} schedule, numpy oracle on one host thread"),
+        "GB/s": round(ball / wall / 1e9, 4),
+        "params_per_s": round(pall * steps / wall, 1),
+        "seconds": round(wall, 3),
+        "processes": nw,
+        "sample": f"{len(sample.qs)} matrices ({pall:,} params), steps 1-{steps}",
+        "same_results_as_one_thread": all(digests.get(q) == d for q, d in digests1.items()),
     }
 
 
@@ -256,22 +469,67 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def recorded_traffic(kernel: str, workload: str):
-    """Bytes per launch of the fused update kernel measured with rocprofv3
-    PMC counters (scaled by a plain streaming kernel's counter reading), if
-    recorded for this workload and the current kernel source."""
-    path = os.path.join(PROFILES, f"{kernel}_{workload}_traffic.md")
+def recorded_traffic(launch_kind: str, workload: str, layout: str):
+    """HBM bytes per launch of one update launch kind, from rocprofv3 PMC
+    counters (FETCH_SIZE and WRITE_SIZE runs, scaled by the reference copy
+    stream's reading), if recorded for this workload, layout and the current
+    kernel sources."""
+    path = os.path.join(PROFILES, f"traffic_{workload}_{layout}.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
     h = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
-    v = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    v = re.search(r"traffic_bytes_per_launch\[" + re.escape(launch_kind) +
+                  r"\]:\s*([0-9.eE+]+)", text)
     if not h or not v or h.group(1) != kernel_source_hash():
         return None
     return float(v.group(1))
 
 
-# ---------------------------------------------------------------------------
+def calibrate_streams(dev, gib: float, reps: int = 5) -> dict:
+    """The reference streams of zf_measure.h (the update pass's access
+    pattern with no arithmetic) over `gib` GiB: read-only, copy and
+    read-modify-write in place, each one untimed launch then `reps` timed
+    ones (HIP events on the launch stream)."""
+    import torch
+    import paper_2505_12242_amd as zf
+    nb = int(gib * 2**30) // 16 * 16
+    src = torch.empty(nb, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty(nb, dtype=torch.uint8, device=dev).fill_(2)
+    sink = torch.zeros(1, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    out = {"kernel": "stream_probe_kernel<0|1|2> (zf_stream_probe)", "GiB": gib}
+    for kind, name, moved in ((zf.PROBE_READ, "read", nb), (zf.PROBE_COPY, "copy", 2 * nb),
+                              (zf.PROBE_RMW, "rmw", 2 * nb)):
+        args = ((src, sink) if kind == zf.PROBE_READ else (src, dst) if kind == zf.PROBE_COPY
+                else (None, dst))
+        zf.stream_probe(kind, *args, nb, key=0x9E3779B9, stream=stream)
+        torch.cuda.synchronize(dev)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            zf.stream_probe(kind, *args, nb, key=0x9E3779B9, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize(dev)
+        ms = e0.elapsed_time(e1) / reps
+        out[f"{name}_GB/s"] = round(moved / (ms * 1e-3) / 1e9, 1)
+    del src, dst, sink
+    torch.cuda.empty_cache()
+    return out
+
+
+UPDATE_NAMES = ("update", "update_first", "update_second", "update_handover", "update_adam",
+                "update_adam_handover", "update_zen", "update_zen_first")
+
+
+def kernel_class(name: str):
+    """Which entry of step_bytes a recorded launch belongs to."""
+    if name in ("colnorm", "topk_select", "unpack"):
+        return name
+    if name in UPDATE_NAMES:
+        return "update"
+    return None
+
 
 def main(argv=None) -> int:
     args = parse_args(argv)
@@ -281,7 +539,6 @@ def main(argv=None) -> int:
                                    "share of the work); --gpus must be 1"}), flush=True)
         return 2
 
-    import numpy as np
     import torch
     import paper_2505_12242_amd as zf
     from workloads import get_workload
@@ -300,15 +557,27 @@ def main(argv=None) -> int:
     hp = zf.AdamHparams(wl.hyper.lr, wl.hyper.beta1, wl.hyper.beta2, wl.hyper.eps,
                         wl.hyper.weight_decay)
 
+    # reference streams first, while HBM is free
+    calib = None
+    if args.calibration_gib > 0:
+        calib = calibrate_streams(dev, args.calibration_gib)
+        print(f"# reference streams over {args.calibration_gib:g} GiB: read "
+              f"{calib['read_GB/s']}, copy {calib['copy_GB/s']}, read-modify-write "
+              f"{calib['rmw_GB/s']} GB/s", file=sys.stderr, flush=True)
+
     t0 = time.perf_counter()
     shapes, ks, grad_slots, weights = build_set(wl, args.slots, dev, layout)
-    weights0 = None
+    sample = None
+    one_thread_qs = []
     if not args.no_cpu_baseline:
-        qs0 = [q for q, mt in enumerate(wl.matrices) if mt.name.startswith("layers.0.")] or [0]
-        weights0 = {}
-        for q in qs0:
-            w = weights[q] if layout == zf.ROW_MAJOR else weights[q].t()
-            weights0[q] = w.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+        names = [mt.name for mt in wl.matrices]
+        one_thread_qs = [q for q, nm in enumerate(names) if nm.startswith("layers.0.")] or [0]
+        if args.cpu_sample == "layer":
+            qs = one_thread_qs
+        else:
+            qs = list(range(len(shapes)))
+        # the initial weights, before the GPU run updates them
+        sample = HostSample(wl, qs, weights, layout)
     runner = zf.SelectiveUpdateRunner(shapes, wl.ratio, hp, wl.refresh, wl.accum, grad_slots,
                                       weights, device=dev, layout=layout, zen_tau=args.zen_tau,
                                       offload=args.offload, overlap=not args.no_overlap,
@@ -321,30 +590,6 @@ def main(argv=None) -> int:
     setup_s = time.perf_counter() - t0
     print(f"# setup {setup_s:.1f}s: {len(shapes)} matrices, {wl.params:,} params, "
           f"{torch.cuda.memory_allocated() / 2**30:.1f} GiB allocated", file=sys.stderr, flush=True)
-
-    # one plain streaming kernel of known size (reads and writes exactly
-    # calibration_copy_gib GiB each): the calibration point for PMC counters
-    # (then timed over three more launches: a plain read+write stream on
-    # this box, reported beside the roofline as context)
-    stream_ref = None
-    if args.calibration_copy_gib > 0:
-        nb = int(args.calibration_copy_gib * 2**30)
-        src = torch.empty(nb // 4, dtype=torch.float32, device=dev).fill_(4.0)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        torch.sqrt(src, out=dst)
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(3):
-            torch.sqrt(src, out=dst)
-        e1.record()
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / 3
-        stream_ref = {"kernel": f"torch.sqrt over {args.calibration_copy_gib:g} GiB fp32 "
-                                "(reads and writes that much)",
-                      "GB/s": round(2 * nb / (ms * 1e-3) / 1e9, 1)}
-        del src, dst
 
     # stand-in model compute (offload mode): n_mm products of two 4096 x 4096
     # bf16 matrices, calibrated to model_compute_ms per step
@@ -382,7 +627,8 @@ def main(argv=None) -> int:
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
-    spans = []  # (name, start event, end event)
+    spans = []  # (name, timed step index, start event, end event)
+    cur = [0]
 
     @contextlib.contextmanager
     def recorder(name):
@@ -391,7 +637,7 @@ def main(argv=None) -> int:
         a.record(stream)
         yield
         b.record(stream)
-        spans.append((name, a, b))
+        spans.append((name, cur[0], a, b))
 
     kinds = []
     # the garbage collector stays off in the timed region: a collection there
@@ -400,7 +646,8 @@ def main(argv=None) -> int:
     gc.disable()
     torch.cuda.synchronize()
     w0 = time.perf_counter()
-    for _ in range(args.steps):
+    for i in range(args.steps):
+        cur[0] = i
         if model is not None:
             with recorder("model_compute"):
                 model()
@@ -411,38 +658,95 @@ def main(argv=None) -> int:
     wall = time.perf_counter() - w0
     gc.enable()
 
-    per_kernel_ms = {}
-    for name, a, b in spans:
-        per_kernel_ms.setdefault(name, []).append(a.elapsed_time(b))
-    totals = {"colnorm": 0, "topk_select": 0, "update": 0, "unpack": 0}
-    for kind in kinds:
-        b = step_bytes(shapes, ks, kind.refresh, kind.step_in_interval == 1, kind.interval_end,
-                       offload=args.offload, fused_handover=fused,
-                       second=kind.step_in_interval == 2, stage=runner.use_stage,
-                       scored_handover=runner.score_handover)
-        for key in totals:
-            totals[key] += b[key]
-    all_bytes = sum(totals.values())
-    update_bytes = totals["update"]  # both update kinds
-    upd_ms = [ms for name, lst in per_kernel_ms.items() if name.startswith("update")
-              for ms in lst]
-    upd_launches = len(upd_ms)
-    upd_avg_ms = sum(upd_ms) / max(upd_launches, 1)
-    achieved = update_bytes / upd_launches / (upd_avg_ms * 1e-3) / 1e9 if upd_launches else 0.0
+    def model_bytes(kind, survey=False):
+        first, second = kind.step_in_interval == 1, kind.step_in_interval == 2
+        if survey:  # the unfused method: separate hand-over, fp32 first-step packing
+            return step_bytes(shapes, ks, kind.refresh, first, kind.interval_end,
+                              offload=args.offload)
+        return step_bytes(shapes, ks, kind.refresh, first, kind.interval_end,
+                          offload=args.offload, fused_handover=fused, second=second,
+                          stage=runner.use_stage, scored_handover=runner.score_handover)
 
-    value = all_bytes / wall / 1e9
+    def model_traffic(kind):
+        first, second = kind.step_in_interval == 1, kind.step_in_interval == 2
+        return step_traffic(shapes, ks, kind.refresh, first, kind.interval_end,
+                            offload=args.offload, fused_handover=fused, second=second,
+                            stage=runner.use_stage, scored_handover=runner.score_handover)
+
+    build_total = sum(sum(model_bytes(k).values()) for k in kinds)
+    survey_total = sum(sum(model_bytes(k, True).values()) for k in kinds)
+    value = build_total / wall / 1e9
+    # what the reference streams predict for a pass that reads r and writes w
+    # bytes: r / (read rate) + w / (write rate), the write rate inferred from
+    # the copy stream (half reads, half writes)
+    stream_rates = None
+    if calib:
+        rr = calib["read_GB/s"] * 1e9
+        wr = 0.5 / (1.0 / (calib["copy_GB/s"] * 1e9) - 0.5 / rr)
+        stream_rates = (rr, wr)
+        calib["write_GB/s_inferred"] = round(wr / 1e9, 1)
+
+    per = {}
+    for name, i, a, b in spans:
+        e = per.setdefault(name, {"ms": [], "bytes": 0, "survey": 0, "rw": [0, 0]})
+        e["ms"].append(a.elapsed_time(b))
+        cls = kernel_class(name)
+        if cls is not None:
+            r, w = model_traffic(kinds[i])[cls]
+            e["bytes"] += r + w
+            e["rw"][0] += r
+            e["rw"][1] += w
+            e["survey"] += model_bytes(kinds[i], True)[cls]
     kernels = {}
-    for name, lst in per_kernel_ms.items():
-        kernels[name] = {"launches": len(lst), "avg_ms": round(sum(lst) / len(lst), 4)}
-    for name in ("colnorm", "topk_select", "unpack"):
-        if name in per_kernel_ms and totals[name]:
-            tot_ms = sum(per_kernel_ms[name])
-            kernels[name]["GB/s"] = round(totals[name] / (tot_ms * 1e-3) / 1e9, 1)
+    for name, e in per.items():
+        n = len(e["ms"])
+        avg = sum(e["ms"]) / n
+        k = {"launches": n, "avg_ms": round(avg, 4), "total_ms": round(sum(e["ms"]), 3)}
+        if e["bytes"]:
+            rate = e["bytes"] / n / (avg * 1e-3) / 1e9
+            k.update({"GB_per_launch": round(e["bytes"] / n / 1e9, 3), "GB/s": round(rate, 1),
+                      "frac_of_peak": round(rate / HBM_PEAK_GBS, 4)})
+            if stream_rates:
+                model_ms = (e["rw"][0] / stream_rates[0] + e["rw"][1] / stream_rates[1]) / n * 1e3
+                k["read_fraction"] = round(e["rw"][0] / e["bytes"], 3)
+                k["reference_stream_ms"] = round(model_ms, 4)
+                k["frac_of_reference_stream"] = round(model_ms / avg, 4)
+        kernels[name] = k
 
-    upd_kernel = "cm_update_kernel" if layout == zf.CHANNEL_MAJOR else "update_kernel"
-    if args.zen_tau is not None:
-        upd_kernel += " (with Zen-auto statistics)"
-    traffic = recorded_traffic(upd_kernel, wl.name)
+    # the dominant kernel: the fused Adam + pack pass in its middle-step form
+    # (states in place, accumulation; no hand-over): its bytes per launch are
+    # the survey's per-unit figures, 28 per selected and 10 per unselected
+    # element; else the update launch kind with the most time
+    upd = [nm for nm in per if kernel_class(nm) == "update"]
+    dom = "update" if "update" in per else (max(upd, key=lambda nm: sum(per[nm]["ms"]))
+                                            if upd else None)
+    roof = None
+    if dom is not None:
+        e = per[dom]
+        n = len(e["ms"])
+        avg = sum(e["ms"]) / n
+        nbytes = (e["survey"] if dom == "update" else e["bytes"]) / n
+        achieved = nbytes / (avg * 1e-3) / 1e9
+        if layout == zf.CHANNEL_MAJOR:
+            kname = ("cm_update_kernel<true, true, true, false, false, false, false, 3>"
+                     if dom == "update" else f"cm_update_kernel ({dom})")
+        else:
+            kname = f"rv_update_kernel / update_kernel ({dom})"
+        roof = {
+            "kernel": kname + " (fused Adam + bf16 write-back + pack)",
+            "launch_kind": dom,
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": recorded_traffic(dom, wl.name, args.layout),
+            "bytes_per_launch": round(nbytes),
+            "byte_model": "survey per-unit figures" if dom == "update" else "build",
+            "avg_launch_ms": round(avg, 4),
+            "frac_of_reference_stream": kernels[dom].get("frac_of_reference_stream"),
+        }
+
     result = {
         "metric": "GB/s and fraction of HBM peak per full step; params/s",
         "value": round(value, 2),
@@ -477,24 +781,20 @@ def main(argv=None) -> int:
                         ("device -> host copy of the packed buffer" if args.offload
                          else "separate unpack pass"),
             "grad_slots": args.slots,
-            "algorithmic_GB_per_step": round(all_bytes / args.steps / 1e9, 3),
+        },
+        "byte_models": {
+            "build": {"GB_per_step": round(build_total / args.steps / 1e9, 3),
+                      "GB/s": round(value, 1), "frac_of_peak": round(value / HBM_PEAK_GBS, 4),
+                      "what": "bytes this build's kernels move (value)"},
+            "survey": {"GB_per_step": round(survey_total / args.steps / 1e9, 3),
+                       "GB/s": round(survey_total / wall / 1e9, 1),
+                       "frac_of_peak": round(survey_total / wall / 1e9 / HBM_PEAK_GBS, 4),
+                       "what": "the unfused method's bytes: separate hand-over pass, fp32 "
+                               "first-step packing"},
         },
         "kernels": kernels,
-        "roofline": {
-            "kernel": (upd_kernel if layout == zf.CHANNEL_MAJOR else
-                       "rv_update_kernel (steps in place, hand-over) and update_kernel "
-                       "(refresh steps)") + " (fused Adam + bf16 write-back + pack)",
-            "bound": "hbm",
-            "achieved": round(achieved, 1),
-            "peak": HBM_PEAK_GBS,
-            "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": traffic,
-            "bytes_per_launch": round(update_bytes / max(upd_launches, 1)),
-            "avg_launch_ms": round(upd_avg_ms, 4),
-            "stream_reference": (dict(stream_ref, update_frac_of_it=round(
-                achieved / stream_ref["GB/s"], 4)) if stream_ref else None),
-        },
+        "reference_streams": calib,
+        "roofline": roof,
     }
     if args.offload:
         # host side of the deferred update: per unselected element it reads
@@ -521,18 +821,38 @@ def main(argv=None) -> int:
             # stand-in model compute) against the wall time: what is left is
             # the GPU waiting for the host side
             "model_compute_ms_per_step": round(
-                sum(per_kernel_ms.get("model_compute", [])) / args.steps, 3),
+                sum(per.get("model_compute", {"ms": []})["ms"]) / args.steps, 3),
             "gpu_busy_ms_per_step": round(
-                sum(sum(v) for v in per_kernel_ms.values()) / args.steps, 3),
+                sum(sum(v["ms"]) for v in per.values()) / args.steps, 3),
             "gpu_idle_ms_per_step": round(
-                wall / args.steps * 1e3 - sum(sum(v) for v in per_kernel_ms.values()) / args.steps,
+                wall / args.steps * 1e3 - sum(sum(v["ms"]) for v in per.values()) / args.steps,
                 3),
         }
-    if not args.no_cpu_baseline:
-        print("# timing the CPU oracle on a sample ...", file=sys.stderr, flush=True)
-        result["cpu_baseline"] = cpu_baseline(wl, shapes, ks, grad_slots, weights0,
-                                              args.cpu_sample_steps, layout)
     runner.close()
+    if sample is not None:
+        try:
+            print("# timing the CPU oracle on a sample ...", file=sys.stderr, flush=True)
+            sample.add_grads(grad_slots, args.cpu_sample_steps)
+            del grad_slots, weights
+            torch.cuda.empty_cache()
+            info = host_info()
+            workers = min(16, info["nproc"])
+            cb = cpu_baseline(wl, shapes, ks, sample, one_thread_qs, workers)
+            best = cb.get("all_cores") or dict(cb["one_thread"], processes=1)
+            result["cpu_baseline"] = {
+                "value": best["GB/s"],
+                "unit": "GB/s",
+                "params_per_s": best["params_per_s"],
+                "cores": best["processes"],
+                "kind": "oracle",
+                "sample": (best["sample"] + f" of the R={wl.refresh}, S={wl.accum} schedule, "
+                           f"numpy oracle, one process per core"),
+                "one_thread": cb["one_thread"],
+                "all_cores": best,
+                "host": info,
+            }
+        finally:
+            sample.close()
     print(json.dumps(result), flush=True)
     return 0
 

@@ -34,6 +34,10 @@ from ._lib import (  # noqa: F401
     pack_accumulate,
     scatter_weights,
     topk_select,
+    stream_probe,
+    PROBE_READ,
+    PROBE_COPY,
+    PROBE_RMW,
     unpack,
     update_fused,
     update_fused_handover,

@@ -74,6 +74,7 @@ SIGNATURES = [
     ("zf_colnorm_workspace_bytes", c_sz, [c_i64, c_i64, c_i32]),
     ("zf_colnorm", ctypes.c_int, [c_vp, c_i64, c_i64, c_i64, c_i32, c_vp, c_vp, c_sz, c_vp]),
     ("zf_colnorm_noalloc", ctypes.c_int, [c_vp, c_i64, c_i64, c_i64, c_i32, c_vp, c_vp]),
+    ("zf_stream_probe", ctypes.c_int, [c_i32, c_vp, c_vp, c_sz, ctypes.c_uint32, c_vp]),
     ("zf_topk_select", ctypes.c_int,
      [c_vp, c_i64, c_dbl, ctypes.POINTER(ZfSelection), ctypes.POINTER(c_i64), c_vp]),
     ("zf_adam_selected", ctypes.c_int,
@@ -313,6 +314,24 @@ def colnorm_noalloc(grad: torch.Tensor, out: torch.Tensor, layout: int = ROW_MAJ
     _check("zf_colnorm_noalloc", LIB.zf_colnorm_noalloc(_ptr(grad), n, m, ld, layout, _ptr(out),
                                                         _stream(stream)))
     return out
+
+
+PROBE_READ, PROBE_COPY, PROBE_RMW = 0, 1, 2
+
+
+def stream_probe(kind: int, src: Optional[torch.Tensor], dst: torch.Tensor, nbytes: int,
+                 key: int = 0, stream=None) -> None:
+    """One reference streaming pass of zf_measure.h (zf_stream_probe) over
+    the first `nbytes` of src / dst (GPU tensors)."""
+    for t, name in ((src, "src"), (dst, "dst")):
+        if t is not None and (not t.is_cuda or not t.is_contiguous()):
+            raise ValueError(f"{name}: expected a contiguous GPU tensor")
+    if src is not None and src.numel() * src.element_size() < nbytes and kind != PROBE_RMW:
+        raise ValueError("src smaller than nbytes")
+    if kind != PROBE_READ and dst.numel() * dst.element_size() < nbytes:
+        raise ValueError("dst smaller than nbytes")
+    _check("zf_stream_probe", LIB.zf_stream_probe(int(kind), _ptr(src), _ptr(dst), int(nbytes),
+                                                  int(key) & 0xFFFFFFFF, _stream(stream)))
 
 
 def topk_select(norms: torch.Tensor, ratio: float, out: Optional[Selection] = None,

@@ -24,7 +24,7 @@ LIB = os.path.join(PKG, "libzf.so")
 ARCH = "gfx950"
 
 SOURCES = ["zf_api.hip", "zf_kernels.hip", "zf_kernels_cm.hip", "zf_kernels_zen.hip",
-           "zf_kernels_offload.hip", "zf_kernels_rv.hip", "zf_host.cpp"]
+           "zf_kernels_offload.hip", "zf_kernels_rv.hip", "zf_kernels_stream.hip", "zf_host.cpp"]
 
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared", "-Wall", "-pthread",

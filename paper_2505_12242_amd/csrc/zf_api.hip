@@ -11,6 +11,7 @@
 
 #include "zf.h"
 #include "zf_internal.hpp"
+#include "zf_measure.h"
 
 namespace zf {
 
@@ -664,6 +665,22 @@ zf_status zf_colnorm_noalloc(const uint16_t* grad, int64_t n, int64_t m, int64_t
     if (st != ZF_OK) return st;
   }
   return zf_colnorm(grad, n, m, ld_grad, layout, norms_sq, ws, need, stream);
+}
+
+zf_status zf_stream_probe(int32_t kind, const void* src, void* dst, size_t bytes, uint32_t key,
+                          zf_stream stream) {
+  if (kind < 0 || kind > 2 || bytes == 0 || bytes % 16 != 0 ||
+      bytes > static_cast<size_t>(INT64_MAX / 2) || dst == nullptr)
+    return ZF_EINVAL;
+  const int64_t nb = static_cast<int64_t>(bytes);
+  if (zf::stream_probe_blocks(nb) >= (int64_t(1) << 31)) return ZF_EINVAL;
+  if (kind == 0 && !aligned(dst, 4)) return ZF_EINVAL;
+  if (kind != 0 && !aligned(dst, 16)) return ZF_EINVAL;
+  if (kind != 2 && (src == nullptr || !aligned(src, 16))) return ZF_EINVAL;
+  if (kind == 1 && overlaps(span_of(src, 1, nb, nb, 1), span_of(dst, 1, nb, nb, 1)))
+    return ZF_EINVAL;
+  const hipError_t e = zf::launch_stream_probe(kind, src, dst, nb, key, as_stream(stream));
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
 zf_status zf_topk_select(const float* norms_sq, int64_t m, double ratio, const zf_selection* out,

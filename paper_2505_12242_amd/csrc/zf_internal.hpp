@@ -218,6 +218,12 @@ hipError_t launch_rm_zen(const Table& tp, int64_t partial_blocks, const Table& t
                          int64_t finalize_blocks, const DevMat& one, double* zs, double* zb,
                          hipStream_t s);
 // One block: sums zb in a fixed order and evaluates the trigger.
+// Streaming reference passes (zf_measure.h): kind 0 read, 1 copy, 2
+// read-modify-write in place.
+int64_t stream_probe_blocks(int64_t bytes);
+hipError_t launch_stream_probe(int32_t kind, const void* src, void* dst, int64_t bytes,
+                               uint32_t key, hipStream_t s);
+
 hipError_t launch_zen_total(const double* zb, int64_t blocks, int64_t k_total, int64_t u_total,
                             double tau, ZenTotals* out, hipStream_t s);
 

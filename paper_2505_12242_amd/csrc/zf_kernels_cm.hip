@@ -437,7 +437,13 @@ __device__ __forceinline__ void cm_swap_out(const DevMat& d, int64_t j, int64_t 
 #else
 #define ZF_CM_UPDATE_ATTR
 #endif
-template <bool BATCHED, bool ADAM, bool PACK, bool STATS, bool HAND, bool PEND, bool SELG>
+//
+// PH: the interval phase as a compile-time constant (1: an interval's first
+// step, 2: its second, 3: a later step), or 0 to take it from `first`.  The
+// fused launches of the fixed schedule pass it, so that each phase is a
+// kernel of its own (its own code, its own name in a profile).
+template <bool BATCHED, bool ADAM, bool PACK, bool STATS, bool HAND, bool PEND, bool SELG,
+          int PH = 0>
 __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(const DevMat* __restrict__ mats,
                                                             const int64_t* __restrict__ off,
                                                             int32_t nmats, DevMat one, AdamK c,
@@ -445,6 +451,7 @@ __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(c
                                                             double* __restrict__ zs, float scale,
                                                             Pending pd) {
   static_assert(!SELG || (ADAM && !PACK && !STATS && !PEND), "selected-only grid");
+  const int32_t ph = PH != 0 ? PH : first;
   int64_t local;
   const DevMat& d = get_mat<BATCHED>(mats, off, nmats, one, local);
   const int64_t chunk = static_cast<int64_t>(d.cm_vpt) * kThreads * kGroup;
@@ -475,7 +482,7 @@ __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(c
     if constexpr (PACK) {
       const int64_t u = j - r;
       const rsrc_t rA = make_rsrc(d.acc + u * d.ld_acc + e0, len * 4);
-      // the bf16 first-step stage (row j, channel-indexed): first == 1 on an
+      // the bf16 first-step stage (row j, channel-indexed): ph == 1 on an
       // interval's first step, 2 on its second (a matrix without a stage
       // takes 2 as any later step)
       const bool a16 = d.acc1 != nullptr;
@@ -483,30 +490,30 @@ __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(c
       if constexpr (HAND) {
         const rsrc_t rOut = make_rsrc(d.out + j * d.ld_out + e0, len * 4);
         if (d.vec) {
-          if (first == 1) cm_pack_vec_any<true, false, true>(d.cm_vpt, rG, rA, ss, rOut, scale);
-          else if (a16 && first == 2)
+          if (ph == 1) cm_pack_vec_any<true, false, true>(d.cm_vpt, rG, rA, ss, rOut, scale);
+          else if (a16 && ph == 2)
             cm_pack_vec_any<false, false, true, 2>(d.cm_vpt, rG, rA, ss, rOut, scale, rA16);
           else cm_pack_vec_any<false, false, true>(d.cm_vpt, rG, rA, ss, rOut, scale);
         } else {
-          if (first == 1) cm_pack_elem<true, false, true>(rG, rA, len, ss, rOut, scale);
-          else if (a16 && first == 2)
+          if (ph == 1) cm_pack_elem<true, false, true>(rG, rA, len, ss, rOut, scale);
+          else if (a16 && ph == 2)
             cm_pack_elem<false, false, true, 2>(rG, rA, len, ss, rOut, scale, rA16);
           else cm_pack_elem<false, false, true>(rG, rA, len, ss, rOut, scale);
         }
       } else if (d.vec) {
-        if (first == 1) {
+        if (ph == 1) {
           if (a16) cm_pack_vec_any<true, STATS, false, 1>(d.cm_vpt, rG, rA, ss, rsrc_t(), 1.0f, rA16);
           else cm_pack_vec_any<true, STATS>(d.cm_vpt, rG, rA, ss);
-        } else if (a16 && first == 2) {
+        } else if (a16 && ph == 2) {
           cm_pack_vec_any<false, STATS, false, 2>(d.cm_vpt, rG, rA, ss, rsrc_t(), 1.0f, rA16);
         } else {
           cm_pack_vec_any<false, STATS>(d.cm_vpt, rG, rA, ss);
         }
       } else {
-        if (first == 1) {
+        if (ph == 1) {
           if (a16) cm_pack_elem<true, STATS, false, 1>(rG, rA, len, ss, rsrc_t(), 1.0f, rA16);
           else cm_pack_elem<true, STATS>(rG, rA, len, ss);
-        } else if (a16 && first == 2) {
+        } else if (a16 && ph == 2) {
           cm_pack_elem<false, STATS, false, 2>(rG, rA, len, ss, rsrc_t(), 1.0f, rA16);
         } else {
           cm_pack_elem<false, STATS>(rG, rA, len, ss);
@@ -664,18 +671,35 @@ hipError_t launch_cm_colnorm(const Table& t, const DevMat& one, int64_t blocks, 
 #endif
 constexpr unsigned kCmUpdateLds = ZF_CM_UPDATE_LDS;
 
-template <bool ADAM, bool PACK, bool STATS, bool HAND, bool PEND = false, bool SELG = false>
+template <bool ADAM, bool PACK, bool STATS, bool HAND, bool PEND = false, bool SELG = false,
+          int PH = 0>
 static void launch_cm_update_t(const Table& t, const DevMat& one, dim3 grid, const AdamK& c,
                                int32_t mode, int32_t first, double* zs, float scale,
                                hipStream_t s, const Pending& pd = Pending{}) {
   if (t.mats != nullptr)
-    hipLaunchKernelGGL((cm_update_kernel<true, ADAM, PACK, STATS, HAND, PEND, SELG>), grid,
+    hipLaunchKernelGGL((cm_update_kernel<true, ADAM, PACK, STATS, HAND, PEND, SELG, PH>), grid,
                        dim3(kThreads), kCmUpdateLds, s, t.mats, t.off, t.nmats, one, c, mode,
                        first, zs, scale, pd);
   else
-    hipLaunchKernelGGL((cm_update_kernel<false, ADAM, PACK, STATS, HAND, PEND, SELG>), grid,
+    hipLaunchKernelGGL((cm_update_kernel<false, ADAM, PACK, STATS, HAND, PEND, SELG, PH>), grid,
                        dim3(kThreads), kCmUpdateLds, s, t.mats, t.off, t.nmats, one, c, mode,
                        first, zs, scale, pd);
+}
+
+// The fused update (HAND: with the hand-over) with its interval phase as a
+// compile-time constant.
+template <bool HAND>
+static void launch_cm_fused_phase(const Table& t, const DevMat& one, dim3 grid, const AdamK& c,
+                                  int32_t mode, int32_t first, float scale, hipStream_t s) {
+  if (first == 1)
+    launch_cm_update_t<true, true, false, HAND, false, false, 1>(t, one, grid, c, mode, first,
+                                                                 nullptr, scale, s);
+  else if (first == 2)
+    launch_cm_update_t<true, true, false, HAND, false, false, 2>(t, one, grid, c, mode, first,
+                                                                 nullptr, scale, s);
+  else
+    launch_cm_update_t<true, true, false, HAND, false, false, 3>(t, one, grid, c, mode, first,
+                                                                 nullptr, scale, s);
 }
 
 hipError_t launch_cm_adam_selected_grid(const Table& t, const DevMat& one, int64_t blocks,
@@ -712,9 +736,9 @@ hipError_t launch_cm_update(const Table& t, const DevMat& one, int64_t blocks, c
   } else if (zs != nullptr) {
     launch_cm_update_t<true, true, true, false>(t, one, grid, c, mode, first, zs, 1.0f, s);
   } else if (handover) {
-    launch_cm_update_t<true, true, false, true>(t, one, grid, c, mode, first, nullptr, scale, s);
+    launch_cm_fused_phase<true>(t, one, grid, c, mode, first, scale, s);
   } else if (adam && pack) {
-    launch_cm_update_t<true, true, false, false>(t, one, grid, c, mode, first, nullptr, 1.0f, s);
+    launch_cm_fused_phase<false>(t, one, grid, c, mode, first, 1.0f, s);
   } else if (adam) {
     launch_cm_update_t<true, false, false, false>(t, one, grid, c, mode, first, nullptr, 1.0f, s);
   } else if (pack) {

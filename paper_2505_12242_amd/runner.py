@@ -301,7 +301,7 @@ class SelectiveUpdateRunner:
             self._in_stage = (self.use_stage and length == 1
                               and not (end and self.fuse_handover))
             if scored_end:
-                with rec("update_handover"):
+                with rec("update_adam_handover"):
                     plan.update_adam_handover(self.hp, t, mode, st)
                 return kind
             if end and self.keep_unpacked and self.fuse_handover:
@@ -314,7 +314,9 @@ class SelectiveUpdateRunner:
                     plan.update_pending(self.hp, t, self.S, th_p, scale_p, stream=st)
                 self._start_held_update(st)
             else:
-                with rec("update_first" if length == 1 else "update"):
+                name = ("update_adam" if staged else "update_first" if length == 1
+                        else "update_second" if length == 2 else "update")
+                with rec(name):
                     plan.update(self.hp, t, mode, length, self.S, pack=not staged, stream=st)
         else:
             if refresh and self._pend is not None:

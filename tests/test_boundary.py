@@ -24,9 +24,14 @@ E = A + (4 << 30)
 
 
 def header_functions():
-    text = open(os.path.join(ROOT, "include", "zf.h")).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(zf_[a-z0-9_]+)\s*\(", text)))
+    """Every function declared in include/*.h."""
+    names = set()
+    inc = os.path.join(ROOT, "include")
+    for h in sorted(os.listdir(inc)):
+        if h.endswith(".h"):
+            text = re.sub(r"/\*.*?\*/", "", open(os.path.join(inc, h)).read(), flags=re.S)
+            names |= set(re.findall(r"\b(zf_[a-z0-9_]+)\s*\(", text))
+    return sorted(names)
 
 
 def test_every_declared_function_is_exported_and_bound():
@@ -195,6 +200,21 @@ def test_colnorm_noalloc_validation():
     assert LIB.zf_colnorm_noalloc(A, 4, 8, 8, 5, B, None) == EINVAL   # layout
     assert LIB.zf_colnorm_noalloc(A, 4, 8, 8, RM, None, None) == EINVAL
     assert LIB.zf_colnorm_noalloc(A, -1, 8, 8, RM, B, None) == EINVAL
+
+
+def test_stream_probe_validation():
+    """The measurement streams validate on the host before any launch."""
+    P = LIB.zf_stream_probe
+    assert "zf_stream_probe" in header_functions()
+    assert P(3, A, B, 4096, 0, None) == EINVAL           # kind
+    assert P(1, A, B, 0, 0, None) == EINVAL              # no bytes
+    assert P(1, A, B, 4100, 0, None) == EINVAL           # not a multiple of 16
+    assert P(1, A + 8, B, 4096, 0, None) == EINVAL       # src alignment
+    assert P(1, A, B + 4, 4096, 0, None) == EINVAL       # dst alignment
+    assert P(1, A, A + 1024, 4096, 0, None) == EINVAL    # overlapping copy
+    assert P(0, None, B, 4096, 0, None) == EINVAL        # read without a source
+    assert P(2, None, None, 4096, 0, None) == EINVAL     # rmw without a buffer
+    assert P(1, A, B, 1 << 62, 0, None) == EINVAL        # too many blocks
 
 
 def test_plan_validation():

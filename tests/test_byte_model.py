@@ -87,3 +87,22 @@ def test_7b_schedule_totals():
 def bench_k(m, ratio):
     import math
     return min(m, max(0, math.floor(ratio * m + 0.5)))
+
+
+def test_read_write_split():
+    """step_traffic splits each kernel's bytes into reads and writes; their
+    sums are step_bytes.  A middle step of the fused update reads G and the
+    selected states (2 + 12 B) and the previous sums (4 B), and writes the
+    states and the weight (12 + 2 B) and the new sums (4 B)."""
+    shapes, ks = [(64, 100), (7, 33)], [10, 3]
+    for args in [(True, True, False), (False, False, False), (False, False, True),
+                 (True, True, True)]:
+        for kw in ({}, {"fused_handover": True, "stage": True}, {"offload": True},
+                   {"fused_handover": True, "stage": True, "second": True}):
+            t = bench.step_traffic(shapes, ks, *args, **kw)
+            b = bench.step_bytes(shapes, ks, *args, **kw)
+            assert {c: r + w for c, (r, w) in t.items()} == b
+    t = bench.step_traffic(shapes, ks, False, False, False)
+    nk = 64 * 10 + 7 * 3
+    nu = 64 * 90 + 7 * 30
+    assert t["update"] == [14 * nk + 6 * nu, 14 * nk + 4 * nu]
