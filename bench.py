@@ -57,6 +57,9 @@ def parse_args(argv=None):
     ap.add_argument("--zen-tau", type=float, default=None,
                     help="run Zen-auto (adaptive interval, at most --accum steps) with this "
                          "threshold instead of the fixed schedule")
+    ap.add_argument("--zen-on-host", action="store_true",
+                    help="with --zen-tau: decide each interval end on the host (one stream "
+                         "synchronisation per step) instead of on the device")
     ap.add_argument("--offload", action="store_true",
                     help="run the whole method with offloaded optimizer states: full-state "
                          "store in pinned host memory (swapped at refreshes) and the deferred "
@@ -526,6 +529,8 @@ def kernel_class(name: str):
     """Which entry of step_bytes a recorded launch belongs to."""
     if name in ("colnorm", "topk_select", "unpack"):
         return name
+    if name == "handover_zen":
+        return "unpack"
     if name in UPDATE_NAMES:
         return "update"
     return None
@@ -584,7 +589,8 @@ def main(argv=None) -> int:
                                       host_threads=args.host_threads,
                                       fuse_handover=not args.separate_handover,
                                       refresh_pending=not args.refresh_waits,
-                                      first_step_stage=not args.no_first_step_stage)
+                                      first_step_stage=not args.no_first_step_stage,
+                                      zen_on_device=not args.zen_on_host)
     fused = runner.keep_unpacked and runner.fuse_handover and args.zen_tau is None
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t0
@@ -773,6 +779,8 @@ def main(argv=None) -> int:
             "refresh_interval": wl.refresh,
             "accum_interval": wl.accum,
             "zen_auto_tau": args.zen_tau,
+            "zen_interval_decided_on": (None if args.zen_tau is None else
+                                        "device" if runner.zen_device else "host"),
             "offload": args.offload,
             "model_compute_ms": args.model_compute_ms or None,
             "interval_ends": sum(1 for k in kinds if k.interval_end),

@@ -615,6 +615,44 @@ zf_status zf_plan_update_zen_pending(zf_plan* plan, const zf_adam_hparams* hp, i
                                      int64_t accum_interval, int64_t pend_step, float pend_scale,
                                      double tau, zf_zen_totals* totals, zf_stream stream);
 
+/* Zen-auto's interval driven on the device, so that a step needs no host
+ * round trip (paper, Zero-stall Pipeline, "Hyperparameter Auto-tuning": the
+ * deferred update is triggered as soon as the accumulated part becomes
+ * comparable; the decision stays on the GPU).  The interval state lives in
+ * DEVICE memory (8 bytes, 4-byte aligned), initialised by the caller to
+ * {0, 1} (nothing accumulated; the first step starts an interval) and then
+ * owned by the calls below, in stream order. */
+typedef struct zf_zen_state {
+  int32_t length; /* steps of the current interval so far               */
+  int32_t ended;  /* 1: the last step ended its interval (handed over)  */
+} zf_zen_state;
+
+/* zf_plan_update_zen whose position in the interval is read from *state
+ * instead of passed: 1 on a refresh (mode ZF_STATES_REMAP or
+ * ZF_STATES_INIT) or after an ended interval, else state->length + 1 (so
+ * the accumulation overwrites or adds, and with the bf16 stage writes or
+ * reads the stage, as zf_plan_update_zen with that step_in_interval).
+ * After the statistics and totals, the same launch sequence updates the
+ * state: length = that position; ended = trigger || position >=
+ * accum_interval (S_max) || force_end.  force_end: the caller's own end of
+ * the interval (the next step refreshes the selection, or a warm-up step).
+ * Channel-major plans without a full-state store; the requirements of
+ * zf_plan_update_zen otherwise.  Follow it with zf_plan_handover_zen. */
+zf_status zf_plan_update_zen_device(zf_plan* plan, const zf_adam_hparams* hp, int64_t step,
+                                    int32_t mode, int64_t accum_interval, int32_t force_end,
+                                    double tau, zf_zen_totals* totals, zf_zen_state* state,
+                                    zf_stream stream);
+
+/* The hand-over of the step zf_plan_update_zen_device just ran: if
+ * state->ended, every matrix's `unpacked` buffer receives the hand-over of
+ * the interval (scale = fp32(1 / state->length); from the bf16 stage after
+ * a one-step interval on a plan with one; +0.0 in the selected channels'
+ * rows), bit for bit as zf_plan_unpack / zf_plan_unpack_first with that
+ * scale; else nothing is written.  A fixed grid that loops over the work:
+ * a step that does not end its interval costs one short launch.  Plans
+ * whose descriptors all have the stage or none has it. */
+zf_status zf_plan_handover_zen(zf_plan* plan, const zf_zen_state* state, zf_stream stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -123,6 +123,9 @@ SIGNATURES = [
     ("zf_plan_update_pending", ctypes.c_int,
      [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, c_i64, c_i64, c_flt, c_vp]),
     ("zf_plan_scatter_weights_skip_prev", ctypes.c_int, [c_vp, c_vp]),
+    ("zf_plan_update_zen_device", ctypes.c_int,
+     [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, c_i32, c_i64, c_i32, c_dbl, c_vp, c_vp, c_vp]),
+    ("zf_plan_handover_zen", ctypes.c_int, [c_vp, c_vp, c_vp]),
     ("zf_plan_update_zen_pending", ctypes.c_int,
      [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, c_i64, c_i64, c_flt, c_dbl, c_vp, c_vp]),
 ]
@@ -600,6 +603,13 @@ class MatrixBuffers:
 
 
 ZEN_TOTALS_BYTES = ctypes.sizeof(ZfZenTotals)
+ZEN_STATE_BYTES = 8  # zf_zen_state: int32 length, int32 ended
+
+
+def _check_dev_bytes(t: torch.Tensor, nbytes: int, name: str) -> None:
+    if (t.device.type != "cuda" or not t.is_contiguous()
+            or t.numel() * t.element_size() < nbytes):
+        raise ValueError(f"{name}: expected a contiguous GPU tensor of at least {nbytes} bytes")
 
 
 @dataclass(frozen=True)
@@ -737,6 +747,26 @@ class Plan:
         _check("zf_plan_update_zen", LIB.zf_plan_update_zen(
             self._h, ctypes.byref(c_hp), step, mode, step_in_interval, accum_interval,
             float(tau), totals.data_ptr(), _stream(stream)))
+
+    def update_zen_device(self, hp: AdamHparams, step: int, mode: int, accum_interval: int,
+                          force_end: bool, tau: float, totals: torch.Tensor,
+                          state: torch.Tensor, stream=None) -> None:
+        """update_zen with the interval's position read from, and the end
+        decision written to, the device interval state `state` (a GPU tensor
+        of ZEN_STATE_BYTES bytes; zf_plan_update_zen_device)."""
+        _check_dev_bytes(totals, ZEN_TOTALS_BYTES, "totals")
+        _check_dev_bytes(state, ZEN_STATE_BYTES, "state")
+        c_hp = hp.as_c()
+        _check("zf_plan_update_zen_device", LIB.zf_plan_update_zen_device(
+            self._h, ctypes.byref(c_hp), step, mode, accum_interval, int(bool(force_end)),
+            float(tau), totals.data_ptr(), state.data_ptr(), _stream(stream)))
+
+    def handover_zen(self, state: torch.Tensor, stream=None) -> None:
+        """The hand-over of the step update_zen_device ran, if the device
+        ended the interval (zf_plan_handover_zen)."""
+        _check_dev_bytes(state, ZEN_STATE_BYTES, "state")
+        _check("zf_plan_handover_zen", LIB.zf_plan_handover_zen(self._h, state.data_ptr(),
+                                                                _stream(stream)))
 
     def update_zen_pending(self, hp: AdamHparams, step: int, accum_interval: int,
                            pend_step: int, pend_scale: float, tau: float,

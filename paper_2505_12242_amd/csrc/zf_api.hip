@@ -1329,13 +1329,14 @@ namespace {
 // Zen-auto step over a plan; pd != nullptr: the refresh with the owed
 // deferred update (kRemap, first step of an interval).
 zf_status plan_update_zen(zf_plan* p, const AdamK& c, int32_t mode, int32_t first, double tau,
-                          zf_zen_totals* totals, hipStream_t s, const zf::Pending* pd) {
+                          zf_zen_totals* totals, hipStream_t s, const zf::Pending* pd,
+                          zf::ZenState* zst = nullptr, int32_t S_max = 1, int32_t force_end = 0) {
   const Table t{p->d_mats, p->d_off_up, p->nmats};
   const Table tz{p->d_mats, p->d_off_zen, p->nmats};
   hipError_t e;
   if (p->layout == zf::kChannelMajor) {
     e = zf::launch_cm_update(t, p->mats[0], p->blk_up, c, mode, first, true, true, p->d_zs, false,
-                             1.0f, s, pd);
+                             1.0f, s, pd, zst);
     if (e != hipSuccess) return hip_fail(e);
     e = zf::launch_zen_finalize(tz, p->mats[0], p->blk_zen, p->d_zs, p->d_zb, s);
   } else if (pd == nullptr && use_rv(p->mats[0], mode, true)) {
@@ -1357,7 +1358,8 @@ zf_status plan_update_zen(zf_plan* p, const AdamK& c, int32_t mode, int32_t firs
   }
   if (e != hipSuccess) return hip_fail(e);
   e = zf::launch_zen_total(p->d_zb, p->blk_zen, p->k_total, p->u_total, tau,
-                           reinterpret_cast<zf::ZenTotals*>(totals), s);
+                           reinterpret_cast<zf::ZenTotals*>(totals), s, zst,
+                           mode != zf::kInplace ? 1 : 0, S_max, force_end);
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
@@ -1385,6 +1387,35 @@ zf_status zf_plan_update_zen(zf_plan* p, const zf_adam_hparams* hp, int64_t step
     return ZF_EINVAL;
   return plan_update_zen(p, adam_consts(*hp, step), mode, pack_phase(p, step_in_interval), tau,
                          totals, as_stream(stream), nullptr);
+}
+
+zf_status zf_plan_update_zen_device(zf_plan* p, const zf_adam_hparams* hp, int64_t step,
+                                    int32_t mode, int64_t accum_interval, int32_t force_end,
+                                    double tau, zf_zen_totals* totals, zf_zen_state* state,
+                                    zf_stream stream) {
+  static_assert(sizeof(zf_zen_state) == sizeof(zf::ZenState), "zen state layout");
+  if (!zen_args_ok(p, hp, step, tau, totals) || p->layout != zf::kChannelMajor || p->has_store)
+    return ZF_EINVAL;
+  if (mode != zf::kInplace && mode != zf::kRemap && mode != zf::kInit) return ZF_EINVAL;
+  if (mode == zf::kRemap && !p->can_remap) return ZF_EINVAL;
+  if (accum_interval < 1 || accum_interval > INT32_MAX || state == nullptr ||
+      !aligned(state, 4))
+    return ZF_EINVAL;
+  return plan_update_zen(p, adam_consts(*hp, step), mode, 0, tau, totals, as_stream(stream),
+                         nullptr, reinterpret_cast<zf::ZenState*>(state),
+                         static_cast<int32_t>(accum_interval), force_end ? 1 : 0);
+}
+
+zf_status zf_plan_handover_zen(zf_plan* p, const zf_zen_state* state, zf_stream stream) {
+  if (p == nullptr || !p->can_unpack || p->layout != zf::kChannelMajor || state == nullptr ||
+      !aligned(state, 4) || (p->has_acc1 && !p->all_acc1))
+    return ZF_EINVAL;
+  const Table t{p->d_mats, p->d_off_unp, p->nmats};
+  const hipError_t e =
+      zf::launch_cm_unpack_zen(t, p->mats[0], p->blk_unp,
+                               reinterpret_cast<const zf::ZenState*>(state), p->all_acc1,
+                               as_stream(stream));
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
 zf_status zf_plan_update_zen_pending(zf_plan* p, const zf_adam_hparams* hp, int64_t step,

@@ -131,6 +131,14 @@ struct Pending {
   float scale;
 };
 
+// Zen-auto's interval state when the device drives the interval
+// (zf_zen_state): steps of the current interval so far, and whether the
+// last step ended it.
+struct ZenState {
+  int32_t length;
+  int32_t ended;
+};
+
 // Hyperparameter validation and the constants of a 1-based step
 // (zf_api.hip): B1 = beta1, C1 = 1 - beta1, B2 = beta2, C2 = 1 - beta2,
 // LR = lr, EPS = eps, WD = lr * weight_decay, IB1 = 1 / (1 - beta1^t),
@@ -176,7 +184,14 @@ hipError_t launch_cm_colnorm(const Table& t, const DevMat& one, int64_t blocks, 
 hipError_t launch_cm_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
                             int32_t mode, int32_t first, bool adam, bool pack, double* zs,
                             bool handover, float scale, hipStream_t s,
-                            const Pending* pend = nullptr);
+                            const Pending* pend = nullptr, const ZenState* zst = nullptr);
+// The hand-over of an interval that Zen-auto ended on the device: when
+// zst->ended, every matrix's `out` receives scale * its sums with scale =
+// fp32(1 / zst->length) (from the stage when stage and the interval was one
+// step), +0.0 for selected channels; else nothing.  A grid of at most
+// `grid` blocks loops over the `units` unpack blocks of the table.
+hipError_t launch_cm_unpack_zen(const Table& t, const DevMat& one, int64_t units,
+                                const ZenState* zst, bool stage, hipStream_t s);
 // from_stage: the source is the bf16 first-step stage (a one-step interval;
 // every matrix of the table has one).
 hipError_t launch_cm_unpack(const Table& t, const DevMat& one, int64_t blocks, float scale,
@@ -224,7 +239,12 @@ int64_t stream_probe_blocks(int64_t bytes);
 hipError_t launch_stream_probe(int32_t kind, const void* src, void* dst, int64_t bytes,
                                uint32_t key, hipStream_t s);
 
+// zst != nullptr (the interval driven on the device): the step's position
+// is 1 after a refresh or an ended interval, else zst->length + 1; the
+// kernel stores it in zst->length and ends the interval when the trigger
+// fires, the position reaches S_max, or force_end.
 hipError_t launch_zen_total(const double* zb, int64_t blocks, int64_t k_total, int64_t u_total,
-                            double tau, ZenTotals* out, hipStream_t s);
+                            double tau, ZenTotals* out, hipStream_t s, ZenState* zst = nullptr,
+                            int32_t refresh = 0, int32_t S_max = 1, int32_t force_end = 0);
 
 }  // namespace zf

@@ -449,9 +449,17 @@ __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(c
                                                             int32_t nmats, DevMat one, AdamK c,
                                                             int32_t mode, int32_t first,
                                                             double* __restrict__ zs, float scale,
-                                                            Pending pd) {
+                                                            Pending pd,
+                                                            const ZenState* __restrict__ zst) {
   static_assert(!SELG || (ADAM && !PACK && !STATS && !PEND), "selected-only grid");
-  const int32_t ph = PH != 0 ? PH : first;
+  // the phase: a compile-time constant, the caller's, or (Zen-auto with the
+  // interval driven on the device) 1 after a refresh or an ended interval,
+  // else the interval's length so far + 1
+  int32_t ph = PH != 0 ? PH : first;
+  if (PH == 0 && zst != nullptr) {
+    const int32_t pos = (mode != kInplace || zst->ended) ? 1 : zst->length + 1;
+    ph = pos < 3 ? pos : 3;
+  }
   int64_t local;
   const DevMat& d = get_mat<BATCHED>(mats, off, nmats, one, local);
   const int64_t chunk = static_cast<int64_t>(d.cm_vpt) * kThreads * kGroup;
@@ -586,16 +594,11 @@ __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(c
 // the bf16 first-step stage), scale times its widened row of the stage.
 // ---------------------------------------------------------------------------
 
-template <bool BATCHED, bool STAGE>
-__global__ __launch_bounds__(kThreads) void cm_unpack_kernel(const DevMat* __restrict__ mats,
-                                                            const int64_t* __restrict__ off,
-                                                            int32_t nmats, DevMat one,
-                                                            float scale) {
-  int64_t local;
-  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, local);
-  const int64_t j = local / d.cm_unch;
-  const int64_t e0 = (local % d.cm_unch) * kCmUnpackChunk;
-  const int64_t len = min(static_cast<int64_t>(kCmUnpackChunk), d.n - e0);
+// The hand-over of rows [e0, e0 + len) of channel j, len <= VPT * 256 * 8
+// (VPT 16-byte groups per lane on the vector path).
+template <bool STAGE, int VPT>
+__device__ __forceinline__ void cm_unpack_rows(const DevMat& d, int64_t j, int64_t e0,
+                                               int64_t len, float scale) {
   const int64_t w = j >> 6;
   const uint64_t mw = uniform_u64(d.mask[w]);
   const bool sel = (mw >> (j & 63)) & 1ull;
@@ -605,7 +608,7 @@ __global__ __launch_bounds__(kThreads) void cm_unpack_kernel(const DevMat* __res
     const float z[kGroup] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     if (d.vec) {
 #pragma unroll
-      for (int q = 0; q < kCmUnpackVpt; ++q) f32x8_store<kAuxWO>(rD, group_elem(q, tid) * 4, z);
+      for (int q = 0; q < VPT; ++q) f32x8_store<kAuxWO>(rD, group_elem(q, tid) * 4, z);
     } else {
       for (int64_t e = tid; e < len; e += kThreads)
         buf_put_f32<kAuxWO>(0.0f, rD, static_cast<uint32_t>(e) * 4, 0);
@@ -617,14 +620,14 @@ __global__ __launch_bounds__(kThreads) void cm_unpack_kernel(const DevMat* __res
   const rsrc_t rA = make_rsrc(d.acc + u * d.ld_acc + e0, len * 4);
   const rsrc_t rS = STAGE ? make_rsrc(d.acc1 + j * d.ld_acc1 + e0, len * 2) : rA;
   if (d.vec) {
-    float a[kCmUnpackVpt][kGroup];
+    float a[VPT][kGroup];
 #pragma unroll
-    for (int q = 0; q < kCmUnpackVpt; ++q) {
+    for (int q = 0; q < VPT; ++q) {
       if constexpr (STAGE) widen8(buf_b128<kAuxRO>(rS, group_elem(q, tid) * 2, 0), a[q]);
       else f32x8_load<kAuxRO>(rA, group_elem(q, tid) * 4, a[q]);
     }
 #pragma unroll
-    for (int q = 0; q < kCmUnpackVpt; ++q) {
+    for (int q = 0; q < VPT; ++q) {
 #pragma unroll
       for (int i = 0; i < kGroup; ++i) a[q][i] = a[q][i] * scale;
       f32x8_store<kAuxWO>(rD, group_elem(q, tid) * 4, a[q]);
@@ -635,6 +638,76 @@ __global__ __launch_bounds__(kThreads) void cm_unpack_kernel(const DevMat* __res
       const float a = STAGE ? widen_bf16(buf_u16<kAuxRO>(rS, static_cast<uint32_t>(e) * 2, 0))
                             : buf_f32<kAuxRO>(rA, o, 0);
       buf_put_f32<kAuxWO>(a * scale, rD, o, 0);
+    }
+  }
+}
+
+// One unpack block's work: channel local / cm_unch, its chunk local %
+// cm_unch of kCmUnpackChunk rows.
+template <bool STAGE>
+__device__ __forceinline__ void cm_unpack_unit(const DevMat& d, int64_t local, float scale) {
+  const int64_t j = local / d.cm_unch;
+  const int64_t e0 = (local % d.cm_unch) * kCmUnpackChunk;
+  const int64_t len = min(static_cast<int64_t>(kCmUnpackChunk), d.n - e0);
+  cm_unpack_rows<STAGE, kCmUnpackVpt>(d, j, e0, len, scale);
+}
+
+template <bool BATCHED, bool STAGE>
+__global__ __launch_bounds__(kThreads) void cm_unpack_kernel(const DevMat* __restrict__ mats,
+                                                            const int64_t* __restrict__ off,
+                                                            int32_t nmats, DevMat one,
+                                                            float scale) {
+  int64_t local;
+  const DevMat& d = get_mat<BATCHED>(mats, off, nmats, one, local);
+  cm_unpack_unit<STAGE>(d, local, scale);
+}
+
+// The hand-over of an interval that Zen-auto ended on the device: nothing
+// unless zst->ended; then scale = fp32(1 / length) (a correctly rounded
+// fp32 division, the value the host passes as fp32(1.0 / length)), from the
+// stage after a one-step interval when the plan keeps one.  A fixed grid
+// loops over the table's unpack blocks, so that a step that does not end
+// its interval costs one short launch.
+__global__ __launch_bounds__(kThreads) void cm_unpack_zen_kernel(const DevMat* __restrict__ mats,
+                                                                const int64_t* __restrict__ off,
+                                                                int32_t nmats, int64_t units,
+                                                                const ZenState* __restrict__ zst,
+                                                                int32_t stage) {
+  if (!zst->ended) return;
+  const int32_t length = zst->length;
+  const float scale = 1.0f / static_cast<float>(length);
+  const bool from_stage = stage != 0 && length == 1;
+  // each block walks one contiguous run of units, the runs in the
+  // XCD-aware block order (XCD x covers one contiguous range, as the
+  // full-grid passes do)
+  const int64_t b = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t per = (units + gridDim.x - 1) / gridDim.x;
+  const int64_t u0 = b * per;
+  const int64_t u1 = min(units, u0 + per);
+  if (u0 >= u1) return;
+  int lo = 0, hi = nmats - 1;
+  while (lo < hi) {  // largest q with off[q] <= u0
+    const int mid = (lo + hi + 1) >> 1;
+    if (off[mid] <= u0) lo = mid; else hi = mid - 1;
+  }
+  // two consecutive chunks of one channel in one pass (twice the bytes in
+  // flight per lane); a lone chunk on its own
+  for (int64_t u = u0; u < u1;) {
+    while (lo + 1 < nmats && off[lo + 1] <= u) ++lo;
+    const DevMat& d = mats[lo];
+    const int64_t local = u - off[lo];
+    const int64_t j = local / d.cm_unch;
+    const int64_t e0 = (local % d.cm_unch) * kCmUnpackChunk;
+    const bool pair = u + 1 < u1 && (local + 1) / d.cm_unch == j;
+    const int64_t len = min(static_cast<int64_t>(pair ? 2 : 1) * kCmUnpackChunk, d.n - e0);
+    if (pair) {
+      if (from_stage) cm_unpack_rows<true, 2 * kCmUnpackVpt>(d, j, e0, len, scale);
+      else cm_unpack_rows<false, 2 * kCmUnpackVpt>(d, j, e0, len, scale);
+      u += 2;
+    } else {
+      if (from_stage) cm_unpack_rows<true, kCmUnpackVpt>(d, j, e0, len, scale);
+      else cm_unpack_rows<false, kCmUnpackVpt>(d, j, e0, len, scale);
+      u += 1;
     }
   }
 }
@@ -675,15 +748,16 @@ template <bool ADAM, bool PACK, bool STATS, bool HAND, bool PEND = false, bool S
           int PH = 0>
 static void launch_cm_update_t(const Table& t, const DevMat& one, dim3 grid, const AdamK& c,
                                int32_t mode, int32_t first, double* zs, float scale,
-                               hipStream_t s, const Pending& pd = Pending{}) {
+                               hipStream_t s, const Pending& pd = Pending{},
+                               const ZenState* zst = nullptr) {
   if (t.mats != nullptr)
     hipLaunchKernelGGL((cm_update_kernel<true, ADAM, PACK, STATS, HAND, PEND, SELG, PH>), grid,
                        dim3(kThreads), kCmUpdateLds, s, t.mats, t.off, t.nmats, one, c, mode,
-                       first, zs, scale, pd);
+                       first, zs, scale, pd, zst);
   else
     hipLaunchKernelGGL((cm_update_kernel<false, ADAM, PACK, STATS, HAND, PEND, SELG, PH>), grid,
                        dim3(kThreads), kCmUpdateLds, s, t.mats, t.off, t.nmats, one, c, mode,
-                       first, zs, scale, pd);
+                       first, zs, scale, pd, zst);
 }
 
 // The fused update (HAND: with the hand-over) with its interval phase as a
@@ -719,12 +793,14 @@ hipError_t launch_cm_adam_selected_grid(const Table& t, const DevMat& one, int64
 
 hipError_t launch_cm_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
                             int32_t mode, int32_t first, bool adam, bool pack, double* zs,
-                            bool handover, float scale, hipStream_t s, const Pending* pend) {
+                            bool handover, float scale, hipStream_t s, const Pending* pend,
+                            const ZenState* zst) {
   (void)hipGetLastError();
   if (blocks <= 0) return hipSuccess;
   const dim3 grid(static_cast<uint32_t>(blocks));
   if ((zs != nullptr || handover) && !(adam && pack)) return hipErrorInvalidValue;
   if (zs != nullptr && handover) return hipErrorInvalidValue;
+  if (zst != nullptr && (zs == nullptr || pend != nullptr)) return hipErrorInvalidValue;
   if (pend != nullptr) {
     if (!(adam && pack) || handover || mode != kRemap) return hipErrorInvalidValue;
     if (zs != nullptr)
@@ -734,7 +810,8 @@ hipError_t launch_cm_update(const Table& t, const DevMat& one, int64_t blocks, c
       launch_cm_update_t<true, true, false, false, true>(t, one, grid, c, mode, first, nullptr,
                                                          1.0f, s, *pend);
   } else if (zs != nullptr) {
-    launch_cm_update_t<true, true, true, false>(t, one, grid, c, mode, first, zs, 1.0f, s);
+    launch_cm_update_t<true, true, true, false>(t, one, grid, c, mode, first, zs, 1.0f, s,
+                                                Pending{}, zst);
   } else if (handover) {
     launch_cm_fused_phase<true>(t, one, grid, c, mode, first, scale, s);
   } else if (adam && pack) {
@@ -756,6 +833,19 @@ static void launch_cm_unpack_t(const Table& t, const DevMat& one, dim3 grid, flo
   else
     hipLaunchKernelGGL((cm_unpack_kernel<false, STAGE>), grid, dim3(kThreads), 0, s, t.mats,
                        t.off, t.nmats, one, scale);
+}
+
+constexpr int64_t kCmUnpackZenGrid = 4096;  // 16 blocks per CU
+
+hipError_t launch_cm_unpack_zen(const Table& t, const DevMat& one, int64_t units,
+                                const ZenState* zst, bool stage, hipStream_t s) {
+  (void)hipGetLastError();
+  (void)one;
+  if (units <= 0 || t.mats == nullptr) return hipSuccess;
+  const dim3 grid(static_cast<uint32_t>(units < kCmUnpackZenGrid ? units : kCmUnpackZenGrid));
+  hipLaunchKernelGGL(cm_unpack_zen_kernel, grid, dim3(kThreads), 0, s, t.mats, t.off, t.nmats,
+                     units, zst, stage ? 1 : 0);
+  return hipGetLastError();
 }
 
 hipError_t launch_cm_unpack(const Table& t, const DevMat& one, int64_t blocks, float scale,

@@ -153,7 +153,10 @@ __global__ __launch_bounds__(kZenTotalThreads) void zen_total_kernel(const doubl
                                                                     int64_t blocks,
                                                                     int64_t k_total,
                                                                     int64_t u_total, double tau,
-                                                                    ZenTotals* __restrict__ out) {
+                                                                    ZenTotals* __restrict__ out,
+                                                                    ZenState* __restrict__ zst,
+                                                                    int32_t refresh, int32_t S_max,
+                                                                    int32_t force_end) {
   const int tid = threadIdx.x;
   double a = 0.0, c = 0.0;
   for (int64_t i = tid; i < blocks; i += kZenTotalThreads) {
@@ -181,8 +184,15 @@ __global__ __launch_bounds__(kZenTotalThreads) void zen_total_kernel(const doubl
     out->sum_acc = sum_acc;
     out->k_total = k_total;
     out->u_total = u_total;
-    out->trigger = (k_total > 0 && u_total > 0 && lhs >= rhs) ? 1 : 0;
+    const int32_t trigger = (k_total > 0 && u_total > 0 && lhs >= rhs) ? 1 : 0;
+    out->trigger = trigger;
     out->pad_ = 0;
+    if (zst != nullptr) {
+      // the position the update of this step took (it read the same state)
+      const int32_t pos = (refresh || zst->ended) ? 1 : zst->length + 1;
+      zst->length = pos;
+      zst->ended = (trigger || pos >= S_max || force_end) ? 1 : 0;
+    }
   }
 }
 
@@ -217,10 +227,11 @@ hipError_t launch_rm_zen(const Table& tp, int64_t partial_blocks, const Table& t
 }
 
 hipError_t launch_zen_total(const double* zb, int64_t blocks, int64_t k_total, int64_t u_total,
-                            double tau, ZenTotals* out, hipStream_t s) {
+                            double tau, ZenTotals* out, hipStream_t s, ZenState* zst,
+                            int32_t refresh, int32_t S_max, int32_t force_end) {
   (void)hipGetLastError();
   hipLaunchKernelGGL(zen_total_kernel, dim3(1), dim3(kZenTotalThreads), 0, s, zb, blocks,
-                     k_total, u_total, tau, out);
+                     k_total, u_total, tau, out, zst, refresh, S_max, force_end);
   return hipGetLastError();
 }
 

@@ -24,9 +24,17 @@ Pipeline, "Hyperparameter Auto-tuning"): every update is zf_plan_update_zen,
 which also measures the selected channels' gradient norms and the
 accumulated channels' norms; the interval ends after the step whose pooled
 mean accumulated norm reaches zen_tau times the pooled mean selected norm,
-after `accum` (= S_max) steps, or before a refresh.  The decision is taken
-on the host from the 40-byte totals copied back after each update (one
-stream synchronisation per step).
+after `accum` (= S_max) steps, or before a refresh.  In the channel-major
+layout without the offloaded optimizer the decision stays on the device
+(zen_on_device, the default there): the update reads the interval's
+position from a device state word, the totals kernel writes the end
+decision into it, and a hand-over pass acts on it
+(zf_plan_update_zen_device, zf_plan_handover_zen), so a step issues no
+host synchronisation; the state and totals of each step are copied to
+pinned host memory behind it and read only when the caller asks (the
+returned step kind resolves lazily).  Otherwise the decision is taken on
+the host from the 40-byte totals copied back after each update (one stream
+synchronisation per step).
 
 Offloaded optimizer (offload=True; Asynchronous Offloading Workflow and
 Zero-stall Pipeline): every column's fp32 (p, m, v) lives in a full-state
@@ -64,7 +72,8 @@ from typing import List, Optional, Sequence, Tuple
 import numpy as np
 import torch
 
-from ._lib import (ROW_MAJOR, STATES_INIT, STATES_INPLACE, STATES_REMAP, ZEN_TOTALS_BYTES,
+from ._lib import (ROW_MAJOR, STATES_INIT, STATES_INPLACE, STATES_REMAP, ZEN_STATE_BYTES,
+                   ZEN_TOTALS_BYTES,
                    AdamHparams, MatrixBuffers, Plan, Selection, StateSource, ZenTotals, _stored,
                    alloc_stored, padded_block,
                    host_adam_unselected, k_from_ratio)
@@ -96,6 +105,38 @@ def schedule(t: int, R: int, S: int, warmup: int = 0) -> StepKind:
     return StepKind(refresh=(t - 1) % R == 0, step_in_interval=t - start + 1, interval_end=end)
 
 
+class DeviceZenStep:
+    """The kind of a Zen-auto step whose interval the device decided: refresh
+    is known on the host; the step's position in the interval, whether it
+    ended the interval and the totals are read back from pinned host memory
+    (after waiting for the step) the first time one of them is asked for."""
+
+    def __init__(self, refresh: bool, host: torch.Tensor, event: torch.cuda.Event):
+        self.refresh = refresh
+        self._host = host
+        self._event = event
+        self._vals = None
+
+    def resolve(self):
+        if self._vals is None:
+            self._event.synchronize()
+            raw = self._host.numpy()
+            self._vals = (int(raw[0]), bool(raw[1]), ZenTotals.from_bytes(raw[2:].tobytes()))
+        return self._vals
+
+    @property
+    def step_in_interval(self) -> int:
+        return self.resolve()[0]
+
+    @property
+    def interval_end(self) -> bool:
+        return self.resolve()[1]
+
+    @property
+    def totals(self) -> ZenTotals:
+        return self.resolve()[2]
+
+
 class _NoRecord:
     def __enter__(self):
         return self
@@ -120,7 +161,8 @@ class SelectiveUpdateRunner:
                  device=None, keep_unpacked: bool = True, layout: int = ROW_MAJOR,
                  zen_tau: Optional[float] = None, offload: bool = False, overlap: bool = True,
                  host_threads: Optional[int] = None, fuse_handover: bool = True,
-                 warmup: int = 0, refresh_pending: bool = True, first_step_stage: bool = True):
+                 warmup: int = 0, refresh_pending: bool = True, first_step_stage: bool = True,
+                 zen_on_device: bool = True):
         self.device = torch.device(device) if device is not None else torch.device("cuda")
         self.shapes = [(int(n), int(m)) for n, m in shapes]
         self.ratio, self.hp, self.R, self.S = ratio, hp, int(refresh), int(accum)
@@ -151,11 +193,18 @@ class SelectiveUpdateRunner:
         dev = self.device
         f32 = torch.float32
         self.zen_tau = None if zen_tau is None else float(zen_tau)
+        # the interval decided on the device (channel-major, no offload)
+        self.zen_device = (self.zen_tau is not None and bool(zen_on_device)
+                           and layout != ROW_MAJOR and not self.offload)
         if self.zen_tau is not None:
             self.zen_totals = torch.zeros(ZEN_TOTALS_BYTES // 8, dtype=torch.int64, device=dev)
             self._zen_host = torch.zeros(ZEN_TOTALS_BYTES // 8, dtype=torch.int64,
                                          pin_memory=True)
-        self.last_totals: Optional[ZenTotals] = None
+            # device interval state {length, ended}: nothing accumulated yet
+            self.zen_state = torch.tensor([0, 1], dtype=torch.int32, device=dev)
+            assert self.zen_state.numel() * 4 == ZEN_STATE_BYTES
+        self._last_totals: Optional[ZenTotals] = None
+        self._zen_pending: Optional[DeviceZenStep] = None
         self._length = 0
         self._ended = True
 
@@ -243,6 +292,22 @@ class SelectiveUpdateRunner:
                 acc_first=self.stage[q] if self.use_stage else None))
         return Plan(q_bufs)
 
+    def _resolve_zen(self) -> None:
+        """Zen-auto on the device: the host-side interval fields of the
+        last step (position, end, whether its sums are in the stage, totals),
+        read back now."""
+        k = self._zen_pending
+        if k is not None:
+            length, end, tot = k.resolve()
+            self._length, self._ended, self._last_totals = length, end, tot
+            self._in_stage = self.use_stage and length == 1
+            self._zen_pending = None
+
+    @property
+    def last_totals(self) -> Optional[ZenTotals]:
+        self._resolve_zen()
+        return self._last_totals
+
     @property
     def selection(self) -> List[Selection]:
         return self.sels[self.cur]
@@ -265,6 +330,9 @@ class SelectiveUpdateRunner:
         if self.zen_tau is None:
             kind = schedule(t, self.R, self.S, self.warmup)
             refresh, length = kind.refresh, kind.step_in_interval
+        elif self.zen_device:
+            refresh = (t - 1) % self.R == 0
+            length = None  # decided on the device
         else:
             refresh = (t - 1) % self.R == 0
             length = 1 if (refresh or self._ended or t <= self.warmup) else self._length + 1
@@ -318,6 +386,25 @@ class SelectiveUpdateRunner:
                         else "update_second" if length == 2 else "update")
                 with rec(name):
                     plan.update(self.hp, t, mode, length, self.S, pack=not staged, stream=st)
+        elif self.zen_device:
+            # the interval ends on the device (trigger, S_max) or by the
+            # caller's rule (before a refresh, warm-up steps)
+            force_end = (t % self.R == 0) or t <= self.warmup
+            with rec("update_zen"):
+                plan.update_zen_device(self.hp, t, mode, self.S, force_end, self.zen_tau,
+                                       self.zen_totals, self.zen_state, stream=st)
+            if self.keep_unpacked:
+                with rec("handover_zen"):
+                    plan.handover_zen(self.zen_state, st)
+            host = torch.empty(2 + ZEN_TOTALS_BYTES // 4, dtype=torch.int32, pin_memory=True)
+            with torch.cuda.stream(st):
+                host[:2].copy_(self.zen_state, non_blocking=True)
+                host[2:].copy_(self.zen_totals.view(torch.int32), non_blocking=True)
+            ev = torch.cuda.Event()
+            ev.record(st)
+            kind = DeviceZenStep(refresh, host, ev)
+            self._zen_pending = kind
+            return kind
         else:
             if refresh and self._pend is not None:
                 scale_p, th_p = self._pend[:2]
@@ -332,8 +419,8 @@ class SelectiveUpdateRunner:
             with torch.cuda.stream(st):
                 self._zen_host.copy_(self.zen_totals, non_blocking=True)
             st.synchronize()
-            self.last_totals = ZenTotals.from_bytes(self._zen_host.numpy().tobytes())
-            end = (self.last_totals.trigger or length >= self.S or t % self.R == 0
+            self._last_totals = ZenTotals.from_bytes(self._zen_host.numpy().tobytes())
+            end = (self._last_totals.trigger or length >= self.S or t % self.R == 0
                    or t <= self.warmup)
             self._ended = end
             self._in_stage = self.use_stage and length == 1
@@ -502,6 +589,7 @@ class SelectiveUpdateRunner:
         and its step counter.  Drains the pipeline first (sync).  Tensors are
         CPU copies in the runner's layout; the weights stay the caller's."""
         self.sync()
+        self._resolve_zen()
         c, a = self.cur, self.cur_a
         mats = []
         for q in range(len(self.shapes)):
@@ -560,6 +648,9 @@ class SelectiveUpdateRunner:
         self.t, self.th = int(sd["t"]), int(sd["th"])
         self._length, self._ended = int(sd["length"]), bool(sd["ended"])
         self._in_stage = to_stage
+        self._zen_pending = None
+        if self.zen_tau is not None:
+            self.zen_state.copy_(torch.tensor([self._length, int(self._ended)], dtype=torch.int32))
         self._acc_free = [None] * len(self._acc_free)
         torch.cuda.synchronize(self.device)
 
@@ -567,6 +658,7 @@ class SelectiveUpdateRunner:
     def acc(self) -> List[torch.Tensor]:
         """The last interval's packed sums, fp32 (after an interval's first
         step with the bf16 stage: a widened copy of the stage, exact)."""
+        self._resolve_zen()
         if self._in_stage:
             dim = 1 if self.layout == ROW_MAJOR else 0
             return [x.index_select(dim, s.unsel_idx.long()).float()

@@ -97,13 +97,15 @@ def fixed_ends(T, R, S_max):
     return ends
 
 
-def run_zen(shapes, ratio, R, S_max, tau, T, seed, host_in=None, layout=None):
+def run_zen(shapes, ratio, R, S_max, tau, T, seed, host_in=None, layout=None, on_device=True):
     layout = zf.CHANNEL_MAJOR if layout is None else layout
     dev = torch.device("cuda")
     hp = zf.AdamHparams(lr=1e-3)
     slots, host, weights, w0 = host_in or _inputs(shapes, ratio, T, seed, dev, layout)
     runner = zf.SelectiveUpdateRunner(shapes, ratio, hp, R, S_max, slots, weights, device=dev,
-                                      layout=layout, zen_tau=tau)
+                                      layout=layout, zen_tau=tau, zen_on_device=on_device)
+    # channel-major: the interval decided on the device unless asked otherwise
+    assert runner.zen_device == (on_device and layout == zf.CHANNEL_MAJOR)
     za = _oracle(shapes, w0, ratio, hp, R, S_max, tau)
     ends = []
     exact_stats = total_stats = 0
@@ -148,14 +150,19 @@ def run_zen(shapes, ratio, R, S_max, tau, T, seed, host_in=None, layout=None):
 
 
 LAYOUTS = [pytest.param(zf.ROW_MAJOR, id="rm"), pytest.param(zf.CHANNEL_MAJOR, id="cm")]
+# the channel-major interval decided on the device (the default) and on the host
+LAYOUT_MODES = [pytest.param(zf.ROW_MAJOR, True, id="rm"),
+                pytest.param(zf.CHANNEL_MAJOR, True, id="cm-device"),
+                pytest.param(zf.CHANNEL_MAJOR, False, id="cm-host")]
 
 
 @pytest.mark.timeout(600)
 @pytest.mark.parametrize("tau", [0.0, math.inf])
-@pytest.mark.parametrize("layout", LAYOUTS)
-def test_zen_auto_extreme_thresholds(tau, layout):
+@pytest.mark.parametrize("layout,on_device", LAYOUT_MODES)
+def test_zen_auto_extreme_thresholds(tau, layout, on_device):
     T, R, S_max = 9, 4, 3
-    ends, exact, total = run_zen(SHAPES, 0.1, R, S_max, tau, T, seed=11, layout=layout)
+    ends, exact, total = run_zen(SHAPES, 0.1, R, S_max, tau, T, seed=11, layout=layout,
+                                 on_device=on_device)
     if tau == 0.0:
         assert all(ends)
     else:
@@ -166,8 +173,8 @@ def test_zen_auto_extreme_thresholds(tau, layout):
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("layout", LAYOUTS)
-def test_zen_auto_threshold_between_observed_ratios(layout):
+@pytest.mark.parametrize("layout,on_device", LAYOUT_MODES)
+def test_zen_auto_threshold_between_observed_ratios(layout, on_device):
     """tau between the ratios the fixed schedule produces after one and after
     several accumulated steps: the trigger fires mid-interval."""
     T, R, S_max, ratio = 10, 16, 6, 0.1
@@ -177,7 +184,8 @@ def test_zen_auto_threshold_between_observed_ratios(layout):
     lo, hi = min(r[:2]), max(r[2:S_max])
     assert hi > lo
     tau = math.sqrt(lo * hi)
-    ends, _, _ = run_zen(SHAPES, ratio, R, S_max, tau, T, seed=12, host_in=inputs, layout=layout)
+    ends, _, _ = run_zen(SHAPES, ratio, R, S_max, tau, T, seed=12, host_in=inputs, layout=layout,
+                         on_device=on_device)
     assert any(ends) and not all(ends)
     # at least one interval ended by the trigger before reaching S_max
     lengths, cur = [], 0
@@ -217,6 +225,58 @@ def test_zen_auto_deterministic(layout):
         outs.append((tots, [f32_np(x).tobytes() for x in runner.acc_sq + runner.sel_sq]))
         runner.close()
     assert outs[0] == outs[1]
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("case", ["early-end", "warmup"])
+def test_zen_auto_on_device_needs_no_host_round_trip(case):
+    """The device-decided interval: steps are enqueued without reading
+    anything back (each returned step kind is unresolved until asked), and
+    resolving them afterwards gives the host-decided run's positions, ends,
+    hand-overs and states bit for bit -- with a threshold between the
+    observed ratios (intervals ended by the trigger before S_max), and with
+    a two-step warm-up."""
+    dev = torch.device("cuda")
+    if case == "early-end":
+        T, R, S_max, warmup = 10, 16, 6, 0
+        inputs = _inputs(SHAPES, 0.1, T, 12, dev, zf.CHANNEL_MAJOR)
+        r = _ratios(SHAPES, inputs[1], inputs[3], 0.1, zf.AdamHparams(lr=1e-3), R, S_max)
+        tau = math.sqrt(min(r[:2]) * max(r[2:S_max]))
+    else:
+        T, R, S_max, warmup, tau = 8, 4, 3, 2, 1.0
+        inputs = _inputs(SHAPES, 0.1, T, 16, dev, zf.CHANNEL_MAJOR)
+    results = []
+    for on_device in (True, False):
+        slots, _, weights, _ = inputs
+        ws = [w.clone() for w in weights]
+        runner = zf.SelectiveUpdateRunner(SHAPES, 0.1, zf.AdamHparams(lr=1e-3), R, S_max, slots,
+                                          ws, device=dev, layout=zf.CHANNEL_MAJOR, zen_tau=tau,
+                                          warmup=warmup, zen_on_device=on_device)
+        assert runner.zen_device == on_device
+        kinds, hand = [], []
+        for t in range(T):
+            kinds.append(runner.step())
+            if on_device:
+                assert kinds[-1]._vals is None  # nothing read back by the step
+            hand.append([x.clone() for x in runner.unpacked])
+        torch.cuda.synchronize()
+        seq = [(k.refresh, k.step_in_interval, k.interval_end) for k in kinds]
+        results.append((seq, [[f32_np(x) for x in h] for h, k in zip(hand, kinds)
+                              if k.interval_end],
+                        [f32_np(x) for q in range(len(SHAPES)) for x in runner.state[q]]))
+        runner.close()
+    (seq_d, hand_d, st_d), (seq_h, hand_h, st_h) = results
+    assert seq_d == seq_h
+    if case == "early-end":
+        assert any(e and sii < S_max for _, sii, e in seq_d)
+    else:
+        assert all(e and sii == 1 for _, sii, e in seq_d[:warmup])
+    assert len(hand_d) == len(hand_h)
+    for a, b in zip(hand_d, hand_h):
+        for x, y in zip(a, b):
+            assert same_bits(x, y)
+    for x, y in zip(st_d, st_h):
+        assert same_bits(x, y)
 
 
 def _plan_buffers(layout, with_stats=True):
