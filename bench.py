@@ -51,6 +51,10 @@ def parse_args(argv=None):
                     help="storage of every matrix: channel-major (each input channel one "
                          "contiguous row, the paper's column-major gradient storage) or "
                          "PyTorch's row-major [out, in]")
+    ap.add_argument("--layers", type=int, default=None,
+                    help="keep only the first N decoder layers of the workload (with its "
+                         "embedding and LM head), e.g. the part of a set whose offloaded "
+                         "optimizer fits the pinned host memory")
     ap.add_argument("--ratio", type=float, default=None, help="override the top-k ratio")
     ap.add_argument("--refresh", type=int, default=None, help="override the refresh interval R")
     ap.add_argument("--accum", type=int, default=None, help="override the accumulation interval S")
@@ -558,6 +562,10 @@ def main(argv=None) -> int:
                               ("accum", args.accum)) if v is not None}
     if over:
         wl = wl.with_(**over)
+    if args.layers is not None:
+        keep = tuple(mt for mt in wl.matrices if not mt.name.startswith("layers.")
+                     or int(mt.name.split(".")[1]) < args.layers)
+        wl = wl.with_(name=f"{wl.name}-first{args.layers}layers", matrices=keep)
     layout = zf.CHANNEL_MAJOR if args.layout == "channel-major" else zf.ROW_MAJOR
     hp = zf.AdamHparams(wl.hyper.lr, wl.hyper.beta1, wl.hyper.beta2, wl.hyper.eps,
                         wl.hyper.weight_decay)
@@ -658,10 +666,12 @@ def main(argv=None) -> int:
             with recorder("model_compute"):
                 model()
         kinds.append(runner.step(recorder=recorder))
+    t_drain = time.perf_counter()
     if args.offload:
         runner.sync()  # the last deferred update lands inside the timed region
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
+    drain = time.perf_counter() - t_drain
     gc.enable()
 
     def model_bytes(kind, survey=False):
@@ -835,6 +845,13 @@ def main(argv=None) -> int:
             "gpu_idle_ms_per_step": round(
                 wall / args.steps * 1e3 - sum(sum(v["ms"]) for v in per.values()) / args.steps,
                 3),
+            # the last interval's copy, host update and write-back finish after
+            # the last step (the drain): the idle time without it is what a
+            # longer run approaches
+            "drain_s": round(drain, 4),
+            "gpu_idle_ms_per_step_without_drain": round(
+                (wall - drain) / args.steps * 1e3
+                - sum(sum(v["ms"]) for v in per.values()) / args.steps, 3),
         }
     runner.close()
     if sample is not None:

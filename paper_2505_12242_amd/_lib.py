@@ -226,6 +226,111 @@ def alloc_stored(layout: int, rows_l: int, cols_l: int, dtype=torch.float32,
     return torch.empty(rows_l, ld, **kw)[:, :cols_l]
 
 
+_HIP = None
+
+
+def _hip():
+    """The HIP runtime, for the few calls the binding makes itself (pinned
+    host allocation, asynchronous copies of it)."""
+    global _HIP
+    if _HIP is None:
+        lib = ctypes.CDLL("libamdhip64.so")
+        lib.hipHostMalloc.restype = ctypes.c_int
+        lib.hipHostMalloc.argtypes = [ctypes.POINTER(c_vp), c_sz, ctypes.c_uint]
+        lib.hipHostFree.restype = ctypes.c_int
+        lib.hipHostFree.argtypes = [c_vp]
+        lib.hipMemcpyAsync.restype = ctypes.c_int
+        lib.hipMemcpyAsync.argtypes = [c_vp, c_vp, c_sz, ctypes.c_int, c_vp]
+        _HIP = lib
+    return _HIP
+
+
+def copy_async(dst: torch.Tensor, src: torch.Tensor, stream) -> None:
+    """dst <- src as one hipMemcpyAsync on `stream` (a torch stream): both
+    dense, the same size in bytes, either on the GPU or in pinned host
+    memory.  Used for PinnedArena tensors, which torch does not recognise as
+    pinned (its own non_blocking copies would turn synchronous)."""
+    n = dst.numel() * dst.element_size()
+    if src.numel() * src.element_size() != n or not (dst.is_contiguous() and src.is_contiguous()):
+        raise ValueError("copy_async: dense tensors of the same size expected")
+    if n == 0:
+        return
+    err = _hip().hipMemcpyAsync(dst.data_ptr(), src.data_ptr(), n, 4,  # hipMemcpyDefault
+                                stream.cuda_stream)
+    if err != 0:
+        raise RuntimeError(f"hipMemcpyAsync failed (hipError {err})")
+
+
+class PinnedArena:
+    """Pinned host memory of exactly the size asked for, handed out as CPU
+    tensors.  torch's pinned allocator rounds every allocation up to a
+    power of two, which for the offloaded optimizer's store and staging of a
+    whole gradient set (tens of GB each) wastes up to half of the pinned
+    memory a process is granted.  The arena allocates hipHostMalloc chunks
+    of at most CHUNK bytes (a single pinned allocation is limited well below
+    the total a process may pin) and places tensors in them back to back.
+    torch does not see these tensors as pinned: copy them with copy_async.
+    The caller frees the arena (free()) once no GPU work and no host thread
+    uses its tensors."""
+
+    CHUNK = 32 << 30
+
+    def __init__(self, nbytes: int):
+        self.total = int(nbytes)
+        self.allocated = 0
+        self.chunks = []  # (pointer, size, base tensor)
+        self.used = 0     # bytes used in the last chunk
+
+    @staticmethod
+    def bytes_for(shape, dtype) -> int:
+        n = 1
+        for x in shape:
+            n *= int(x)
+        return n * torch.empty(0, dtype=dtype).element_size() + 256
+
+    @staticmethod
+    def stored_shape(layout: int, rows_l: int, cols_l: int, dtype):
+        """Dense shape alloc_stored uses for a logical matrix (row-major rows
+        padded to 16 bytes)."""
+        if layout != ROW_MAJOR:
+            return _stored(layout, rows_l, cols_l)
+        per = 16 // torch.empty(0, dtype=dtype).element_size()
+        return (rows_l, max(per, -(-cols_l // per) * per))
+
+    def _new_chunk(self, need: int) -> None:
+        size = max(need, min(self.CHUNK, max(self.total - self.allocated, need)), 256)
+        ptr = c_vp()
+        err = _hip().hipHostMalloc(ctypes.byref(ptr), size, 0)
+        if err != 0 or not ptr.value:
+            raise MemoryError(f"hipHostMalloc of {size / 1e9:.1f} GB failed after "
+                              f"{self.allocated / 1e9:.1f} GB (hipError {err})")
+        base = torch.frombuffer((ctypes.c_char * size).from_address(ptr.value), dtype=torch.uint8)
+        self.chunks.append((ptr.value, size, base))
+        self.allocated += size
+        self.used = 0
+
+    def take(self, shape, dtype) -> torch.Tensor:
+        """A tensor of `shape` in the arena (256-byte aligned)."""
+        n = self.bytes_for(shape, dtype) - 256
+        off = (self.used + 255) & ~255
+        if not self.chunks or off + n > self.chunks[-1][1]:
+            self._new_chunk(n)
+            off = 0
+        self.used = off + n
+        return self.chunks[-1][2][off: off + n].view(dtype).view(*shape)
+
+    def take_stored(self, layout: int, rows_l: int, cols_l: int, dtype) -> torch.Tensor:
+        """alloc_stored(..., pin_memory=True) in the arena."""
+        t = self.take(self.stored_shape(layout, rows_l, cols_l, dtype), dtype)
+        return t if layout != ROW_MAJOR else t[:, :cols_l]
+
+    def free(self) -> None:
+        for ptr, _, _ in self.chunks:
+            _hip().hipHostFree(ptr)
+        self.chunks = []
+        self.allocated = 0
+
+
 def padded_block(t: torch.Tensor) -> torch.Tensor:
     """The rows of a 2-D view including their padding (a dense tensor over
     the same memory), e.g. for one contiguous copy of a padded buffer."""

@@ -73,7 +73,7 @@ import numpy as np
 import torch
 
 from ._lib import (ROW_MAJOR, STATES_INIT, STATES_INPLACE, STATES_REMAP, ZEN_STATE_BYTES,
-                   ZEN_TOTALS_BYTES,
+                   ZEN_TOTALS_BYTES, PinnedArena, copy_async,
                    AdamHparams, MatrixBuffers, Plan, Selection, StateSource, ZenTotals, _stored,
                    alloc_stored, padded_block,
                    host_adam_unselected, k_from_ratio)
@@ -149,10 +149,6 @@ def _no_record(name):
     return _NoRecord()
 
 
-def _pinned_like(shape, dtype):
-    return torch.empty(*shape, dtype=dtype, pin_memory=True)
-
-
 class SelectiveUpdateRunner:
     def __init__(self, shapes: Sequence[Tuple[int, int]], ratio: float, hp: AdamHparams,
                  refresh: int, accum: int, grad_slots: Sequence[Sequence[torch.Tensor]],
@@ -214,6 +210,18 @@ class SelectiveUpdateRunner:
         self.accs: List[List[torch.Tensor]] = [[] for _ in range(nacc)]
         self.norms, self.unpacked, self.sel_sq, self.acc_sq = [], [], [], []
         self.store, self.host_acc, self.wcols, self.unsel_host = [], [], [], []
+        # the offloaded optimizer's pinned host buffers: one exact-size arena
+        self.arena = None
+        if self.offload:
+            total = 0
+            for (n, m), k in zip(self.shapes, self.ks):
+                full = (n, m) if layout == ROW_MAJOR else (m, n)
+                total += 3 * PinnedArena.bytes_for(full, f32)
+                total += PinnedArena.bytes_for(PinnedArena.stored_shape(layout, n, m - k, f32), f32)
+                total += PinnedArena.bytes_for(
+                    PinnedArena.stored_shape(layout, n, m - k, torch.bfloat16), torch.bfloat16)
+                total += PinnedArena.bytes_for((m - k,), torch.int32)
+            self.arena = PinnedArena(total)
         self.wcols_dev = []  # overlap: device staging of the host-produced weights
         self.stage = []      # bf16 first-step stage of the packed buffer
         for q, ((n, m), k) in enumerate(zip(self.shapes, self.ks)):
@@ -234,16 +242,16 @@ class SelectiveUpdateRunner:
             if self.offload:
                 p0 = (self.init_master[q] if self.init_master is not None
                       else self.weights[q].float())
-                sp = _pinned_like(p0.shape, f32)
+                ar = self.arena
+                sp = ar.take(p0.shape, f32)
                 sp.copy_(p0)
-                self.store.append((sp, _pinned_like(p0.shape, f32).zero_(),
-                                   _pinned_like(p0.shape, f32).zero_()))
-                self.host_acc.append(alloc_stored(layout, n, m - k, f32, pin_memory=True))
-                self.wcols.append(alloc_stored(layout, n, m - k, torch.bfloat16,
-                                               pin_memory=True))
+                self.store.append((sp, ar.take(p0.shape, f32).zero_(),
+                                   ar.take(p0.shape, f32).zero_()))
+                self.host_acc.append(ar.take_stored(layout, n, m - k, f32))
+                self.wcols.append(ar.take_stored(layout, n, m - k, torch.bfloat16))
                 if self.overlap:
                     self.wcols_dev.append(alloc_stored(layout, n, m - k, torch.bfloat16, dev))
-                self.unsel_host.append(_pinned_like((m - k,), torch.int32))
+                self.unsel_host.append(self.arena.take((m - k,), torch.int32))
         self.grad_slots = [list(s) for s in grad_slots]
         self.plans = [[[self._plan(slot, p, a) for a in range(nacc)] for p in range(2)]
                       for slot in range(len(self.grad_slots))]
@@ -252,8 +260,12 @@ class SelectiveUpdateRunner:
         self.cur_a = 0
         # offloaded optimizer
         self.th = 0
-        self.host_threads = host_threads if host_threads is not None else \
-            min(16, os.cpu_count() or 1)
+        # default: the process's cores up to 16, one of them left to the
+        # thread that keeps feeding the GPU while an overlapped update runs
+        cores = min(16, len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity")
+                    else (os.cpu_count() or 1))
+        self.host_threads = (host_threads if host_threads is not None else
+                             max(1, cores - 1) if self.overlap else cores)
         self._job: Optional[concurrent.futures.Future] = None
         self._job_p = 0         # selection buffer the running host update's interval used
         self._stg_p: Optional[int] = None  # same, for weights staged but not written back
@@ -479,10 +491,8 @@ class SelectiveUpdateRunner:
             cs = self._copy_stream
             if self._ev_scatter is not None:
                 cs.wait_event(self._ev_scatter)  # the last write-back has read the staging buffer
-            with torch.cuda.stream(cs):
-                for q in range(len(self.shapes)):
-                    padded_block(self.wcols_dev[q]).copy_(padded_block(self.wcols[q]),
-                                                          non_blocking=True)
+            for q in range(len(self.shapes)):
+                copy_async(padded_block(self.wcols_dev[q]), padded_block(self.wcols[q]), cs)
             ev = torch.cuda.Event()
             ev.record(cs)
             self._ev_staged = ev
@@ -506,12 +516,19 @@ class SelectiveUpdateRunner:
         self._ev_scatter = ev
         self._stg_p = None
 
-    def _host_update(self, scale: float, th: int, *waits) -> None:
+    def _host_update(self, scale: float, th: int, copied, *waits) -> None:
+        """The deferred update of every matrix on the host threads.  copied:
+        one event (or one per matrix) after which the packed sums are on the
+        host; waits: the previous staging copy has read the weight columns,
+        the refresh has read the store."""
         for ev in waits:
             if ev is not None:
-                ev.synchronize()  # packed sums copied, staging done, store read
+                ev.synchronize()
+        per = copied if isinstance(copied, list) else [copied] * len(self.shapes)
         t0 = time.perf_counter()
         for q, ((n, m), k) in enumerate(zip(self.shapes, self.ks)):
+            if per[q] is not None:
+                per[q].synchronize()
             P, M, V = self.store[q]
             host_adam_unselected(self.host_acc[q], self.unsel_host[q], n, m, k, scale, P, M, V,
                                  self.wcols[q], self.hp, th, layout=self.layout,
@@ -524,13 +541,11 @@ class SelectiveUpdateRunner:
         a = self.cur_a
         sels = self.sels[self.cur]
         if not self.overlap:
-            with torch.cuda.stream(st):
-                for q in range(len(self.shapes)):
-                    padded_block(self.host_acc[q]).copy_(padded_block(self.accs[a][q]),
-                                                         non_blocking=True)
-                    self.unsel_host[q].copy_(sels[q].unsel_idx, non_blocking=True)
+            for q in range(len(self.shapes)):
+                copy_async(padded_block(self.host_acc[q]), padded_block(self.accs[a][q]), st)
+                copy_async(self.unsel_host[q], sels[q].unsel_idx, st)
             st.synchronize()
-            self._host_update(scale, self.th)
+            self._host_update(scale, self.th, None)
             self._stg_p = self.cur
             self._write_back(st, rec)
             return
@@ -540,14 +555,16 @@ class SelectiveUpdateRunner:
         ev.record(st)
         cs = self._copy_stream
         cs.wait_event(ev)
-        with torch.cuda.stream(cs):
-            for q in range(len(self.shapes)):
-                padded_block(self.host_acc[q]).copy_(padded_block(self.accs[a][q]),
-                                                     non_blocking=True)
-                self.unsel_host[q].copy_(sels[q].unsel_idx, non_blocking=True)
-        copied = torch.cuda.Event()
-        copied.record(cs)
-        self._acc_free[a] = copied
+        # one event per matrix: the host update starts on a matrix as soon as
+        # its sums have arrived, while the later ones still copy
+        copied = []
+        for q in range(len(self.shapes)):
+            copy_async(self.unsel_host[q], sels[q].unsel_idx, cs)
+            copy_async(padded_block(self.host_acc[q]), padded_block(self.accs[a][q]), cs)
+            e = torch.cuda.Event()
+            e.record(cs)
+            copied.append(e)
+        self._acc_free[a] = copied[-1] if copied else None
         warm = self.t <= self.warmup
         if self.refresh_pending and not warm and self.t % self.R == 0:
             # the next step refreshes: it takes over the columns entering its
@@ -682,4 +699,9 @@ class SelectiveUpdateRunner:
         for row in self.plans:
             for pp in row:
                 for plan in pp:
-                    plan.close()
+                    plan.close()  # (synchronises the device)
+        if self.arena is not None:
+            # the store and staging tensors live in the arena: invalid from here on
+            self.store, self.host_acc, self.wcols, self.unsel_host = [], [], [], []
+            self.arena.free()
+            self.arena = None
