@@ -84,6 +84,12 @@ def parse_args(argv=None):
     ap.add_argument("--host-threads", type=int, default=None,
                     help="with --offload: host threads of the deferred update (default: "
                          "min(16, cpu count))")
+    ap.add_argument("--packing", choices=["deferred", "every-step"], default="deferred",
+                    help="deferred (default where it applies: channel-major, fixed schedule, no "
+                         "offload): every gradient of an interval stays in its slot and the "
+                         "interval's last step sums them into the hand-over, with no packed "
+                         "buffer (the ring gets at least min(S, R) slots); every-step: the "
+                         "unselected part is accumulated into the packed buffer at every step")
     ap.add_argument("--separate-handover", action="store_true",
                     help="hand over with a separate unpack pass after the last update of an "
                          "interval instead of fusing it into that update")
@@ -105,7 +111,7 @@ def parse_args(argv=None):
 
 def step_traffic(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool = False,
                  fused_handover: bool = False, second: bool = False, stage: bool = False,
-                 scored_handover: bool = None) -> dict:
+                 scored_handover: bool = None, deferred: bool = False, length: int = 1) -> dict:
     """Algorithmic HBM bytes of one step, by kernel, as [read, written].
 
     colnorm  2nm (read G) + 4m (write scores)          refresh steps
@@ -134,9 +140,15 @@ def step_traffic(shapes, ks, refresh: bool, first: bool, end: bool, offload: boo
              its hand-over from the score pass (scored_handover, channel-
              major; default: with the stage): colnorm 2nm + 4nm, update
              28nk + 4nk (the selected rows' zeros)
+    deferred packing (deferred; fused hand-over): no packed buffer.  Every
+             step but an interval's last updates the selected part only
+             (28nk); the last, of `length` >= 2 steps, reads each step's
+             gradient once at the unselected elements and writes the
+             hand-over: 28nk + 4nk + (2 length + 4) nu.  One-step intervals
+             as with the stage (the score pass hands over on a refresh)
     """
     if scored_handover is None:
-        scored_handover = stage
+        scored_handover = stage or deferred
     out = {"colnorm": [0, 0], "topk_select": [0, 0], "update": [0, 0], "unpack": [0, 0]}
 
     def add(cls, r, w):
@@ -146,13 +158,17 @@ def step_traffic(shapes, ks, refresh: bool, first: bool, end: bool, offload: boo
     for (n, m), k in zip(shapes, ks):
         u = m - k
         staged_refresh = refresh and stage and fused_handover and not end
-        scored_end = refresh and stage and scored_handover and fused_handover and end and first
+        scored_end = refresh and scored_handover and fused_handover and end and first
         if refresh:
             add("colnorm", 2 * n * m, 4 * m + (2 * n * m if staged_refresh else 0)
                 + (4 * n * m if scored_end else 0))
             add("topk_select", 4 * m, 4 * m + 12 * ((m + 63) // 64))
         # selected: G 2 + P/M/V 12 read, P/M/V 12 + W 2 written
         add("update", 14 * n * k, 14 * n * k)
+        if deferred and not scored_end and not (end and first):
+            if end:  # each step's gradient read once, the hand-over written
+                add("update", 2 * length * n * u, 4 * n * u + 4 * n * k)
+            continue
         if staged_refresh or scored_end:
             pass  # the score pass did the packing
         elif first:
@@ -175,10 +191,10 @@ def step_traffic(shapes, ks, refresh: bool, first: bool, end: bool, offload: boo
 
 def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool = False,
                fused_handover: bool = False, second: bool = False, stage: bool = False,
-               scored_handover: bool = None) -> dict:
+               scored_handover: bool = None, deferred: bool = False, length: int = 1) -> dict:
     """step_traffic's bytes read + written, by kernel."""
     t = step_traffic(shapes, ks, refresh, first, end, offload, fused_handover, second, stage,
-                     scored_handover)
+                     scored_handover, deferred, length)
     return {cls: r + w for cls, (r, w) in t.items()}
 
 
@@ -578,6 +594,10 @@ def main(argv=None) -> int:
               f"{calib['read_GB/s']}, copy {calib['copy_GB/s']}, read-modify-write "
               f"{calib['rmw_GB/s']} GB/s", file=sys.stderr, flush=True)
 
+    deferred = (args.packing == "deferred" and layout == zf.CHANNEL_MAJOR and args.zen_tau is None
+                and not args.offload and not args.separate_handover)
+    if deferred:
+        args.slots = max(args.slots, min(wl.accum, wl.refresh))
     t0 = time.perf_counter()
     shapes, ks, grad_slots, weights = build_set(wl, args.slots, dev, layout)
     sample = None
@@ -598,7 +618,8 @@ def main(argv=None) -> int:
                                       fuse_handover=not args.separate_handover,
                                       refresh_pending=not args.refresh_waits,
                                       first_step_stage=not args.no_first_step_stage,
-                                      zen_on_device=not args.zen_on_host)
+                                      zen_on_device=not args.zen_on_host,
+                                      deferred_pack=deferred)
     fused = runner.keep_unpacked and runner.fuse_handover and args.zen_tau is None
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t0
@@ -681,13 +702,15 @@ def main(argv=None) -> int:
                               offload=args.offload)
         return step_bytes(shapes, ks, kind.refresh, first, kind.interval_end,
                           offload=args.offload, fused_handover=fused, second=second,
-                          stage=runner.use_stage, scored_handover=runner.score_handover)
+                          stage=runner.use_stage, scored_handover=runner.score_handover,
+                          deferred=runner.deferred, length=kind.step_in_interval)
 
     def model_traffic(kind):
         first, second = kind.step_in_interval == 1, kind.step_in_interval == 2
         return step_traffic(shapes, ks, kind.refresh, first, kind.interval_end,
                             offload=args.offload, fused_handover=fused, second=second,
-                            stage=runner.use_stage, scored_handover=runner.score_handover)
+                            stage=runner.use_stage, scored_handover=runner.score_handover,
+                            deferred=runner.deferred, length=kind.step_in_interval)
 
     build_total = sum(sum(model_bytes(k).values()) for k in kinds)
     survey_total = sum(sum(model_bytes(k, True).values()) for k in kinds)
@@ -743,13 +766,17 @@ def main(argv=None) -> int:
         avg = sum(e["ms"]) / n
         nbytes = (e["survey"] if dom == "update" else e["bytes"]) / n
         achieved = nbytes / (avg * 1e-3) / 1e9
-        if layout == zf.CHANNEL_MAJOR:
+        if layout == zf.CHANNEL_MAJOR and runner.deferred and dom == "update_handover":
+            kname = "cm_handover_deferred_kernel (the interval's last step: Adam + the sum of " \
+                    "the interval's gradients into the hand-over)"
+        elif layout == zf.CHANNEL_MAJOR:
             kname = ("cm_update_kernel<true, true, true, false, false, false, false, 3>"
-                     if dom == "update" else f"cm_update_kernel ({dom})")
+                     if dom == "update" else f"cm_update_kernel ({dom})") + \
+                " (fused Adam + bf16 write-back + pack)"
         else:
-            kname = f"rv_update_kernel / update_kernel ({dom})"
+            kname = f"rv_update_kernel / update_kernel ({dom}) (fused Adam + bf16 write-back + pack)"
         roof = {
-            "kernel": kname + " (fused Adam + bf16 write-back + pack)",
+            "kernel": kname,
             "launch_kind": dom,
             "bound": "hbm",
             "achieved": round(achieved, 1),
@@ -795,6 +822,8 @@ def main(argv=None) -> int:
             "model_compute_ms": args.model_compute_ms or None,
             "interval_ends": sum(1 for k in kinds if k.interval_end),
             "first_step_stage": runner.use_stage,
+            "packing": "deferred to the interval's last step" if runner.deferred else
+                       "every step",
             "handover": "fused into the interval's last update" if fused else
                         ("device -> host copy of the packed buffer" if args.offload
                          else "separate unpack pass"),

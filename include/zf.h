@@ -512,10 +512,37 @@ zf_status zf_plan_unpack(zf_plan* plan, float scale, zf_stream stream);
 
 /* zf_update_fused_handover over every matrix (out = its `unpacked` buffer):
  * the last step of an interval in one pass, Adam + final accumulation +
- * hand-over. */
+ * hand-over.  With step_in_interval == 1 the packed buffer is not used
+ * (out = scale * G at the unselected columns), so descriptors may then
+ * leave it NULL. */
 zf_status zf_plan_update_handover(zf_plan* plan, const zf_adam_hparams* hp, int64_t step,
                                   int32_t mode, int64_t step_in_interval, int64_t accum_interval,
                                   float scale, zf_stream stream);
+
+/* Deferred packing: the unselected part of each step's gradient is left
+ * where it was written (the caller keeps the gradients of the interval's
+ * steps resident and unchanged until the interval ends: S buffers per
+ * matrix), the interval's earlier steps run the Adam part alone
+ * (zf_plan_update with do_pack = 0), and its last step, with
+ * length = n_earlier + 1 >= 2, runs this call: the Adam step of the
+ * selected channels (states in place, zf_adam_selected) and, in every
+ * matrix's `unpacked` buffer,
+ *   out[i][j] = scale * (((g_1[i][j] + g_2[i][j]) + ...) + g[i][j])
+ * at the unselected channels (g_s the gradient of the interval's s-th step,
+ * g this step's; the additions in step order, each one fp32 operation),
+ * +0.0 at the selected ones: bit for bit what zf_pack_accumulate over the
+ * interval followed by zf_unpack (or zf_plan_update_handover on the last
+ * step) gives, with the packed buffer never written.  Each step's gradient
+ * is read once, at its unselected channels, when the interval ends (2 bytes
+ * per element per step, instead of the packed buffer's 8 per step).
+ * earlier: HOST array of n_earlier (1..15) plans over the same matrices in
+ * the same order (same n, m, k and access path), in step order, whose
+ * descriptors' grad is the gradient of that step; only those gradients are
+ * read.  They must not overlap what this step writes.  Channel-major plans
+ * without a full-state store; `unpacked` required; scale finite. */
+zf_status zf_plan_update_handover_deferred(zf_plan* plan, const zf_adam_hparams* hp, int64_t step,
+                                           const zf_plan* const* earlier, int32_t n_earlier,
+                                           float scale, zf_stream stream);
 
 /* zf_scatter_weights over every matrix (weight_cols of each descriptor). */
 zf_status zf_plan_scatter_weights(zf_plan* plan, zf_stream stream);

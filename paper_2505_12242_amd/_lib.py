@@ -123,6 +123,8 @@ SIGNATURES = [
     ("zf_plan_update_pending", ctypes.c_int,
      [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, c_i64, c_i64, c_flt, c_vp]),
     ("zf_plan_scatter_weights_skip_prev", ctypes.c_int, [c_vp, c_vp]),
+    ("zf_plan_update_handover_deferred", ctypes.c_int,
+     [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, ctypes.POINTER(c_vp), c_i32, c_flt, c_vp]),
     ("zf_plan_update_zen_device", ctypes.c_int,
      [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, c_i32, c_i64, c_i32, c_dbl, c_vp, c_vp, c_vp]),
     ("zf_plan_handover_zen", ctypes.c_int, [c_vp, c_vp, c_vp]),
@@ -815,6 +817,17 @@ class Plan:
         _check("zf_plan_update_handover", LIB.zf_plan_update_handover(
             self._h, ctypes.byref(c_hp), step, mode, step_in_interval, accum_interval,
             float(scale), _stream(stream)))
+
+    def update_handover_deferred(self, hp: AdamHparams, step: int, earlier: Sequence["Plan"],
+                                 scale: float, stream=None) -> None:
+        """The last step of an interval with deferred packing
+        (zf_plan_update_handover_deferred): Adam on the selected channels and
+        the hand-over of scale x the sum, in step order, of the gradients of
+        the plans `earlier` (the interval's earlier steps) and this plan's."""
+        hs = (c_vp * len(earlier))(*[e._h.value for e in earlier])
+        c_hp = hp.as_c()
+        _check("zf_plan_update_handover_deferred", LIB.zf_plan_update_handover_deferred(
+            self._h, ctypes.byref(c_hp), step, hs, len(earlier), float(scale), _stream(stream)))
 
     def scatter_weights(self, stream=None) -> None:
         """W[:, unsel] = weight_cols of every matrix (zf_plan_scatter_weights)."""

@@ -1274,7 +1274,10 @@ zf_status zf_plan_unpack(zf_plan* p, float scale, zf_stream stream) {
 zf_status zf_plan_update_handover(zf_plan* p, const zf_adam_hparams* hp, int64_t step,
                                   int32_t mode, int64_t step_in_interval, int64_t accum_interval,
                                   float scale, zf_stream stream) {
-  if (p == nullptr || !p->can_adam || !p->can_pack || !p->can_handover) return ZF_EINVAL;
+  // (an interval's first step hands over scale * G: the packed buffer is
+  // neither read nor written, so a plan without one may run it)
+  if (p == nullptr || !p->can_adam || !p->can_handover) return ZF_EINVAL;
+  if (!p->can_pack && step_in_interval != 1) return ZF_EINVAL;
   if (!hparams_ok(hp) || step < 1) return ZF_EINVAL;
   if (mode != zf::kInplace && mode != zf::kRemap && mode != zf::kInit) return ZF_EINVAL;
   if (mode == zf::kRemap && !p->can_remap) return ZF_EINVAL;
@@ -1283,6 +1286,44 @@ zf_status zf_plan_update_handover(zf_plan* p, const zf_adam_hparams* hp, int64_t
   const AdamK c = adam_consts(*hp, step);
   const hipError_t e = plan_update_launch(p, c, mode, pack_phase(p, step_in_interval), true, true,
                                           true, scale, as_stream(stream));
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
+zf_status zf_plan_update_handover_deferred(zf_plan* p, const zf_adam_hparams* hp, int64_t step,
+                                           const zf_plan* const* earlier, int32_t n_earlier,
+                                           float scale, zf_stream stream) {
+  if (p == nullptr || p->layout != zf::kChannelMajor || !p->can_adam || !p->can_handover ||
+      p->has_store)
+    return ZF_EINVAL;
+  if (!hparams_ok(hp) || step < 1 || !std::isfinite(scale)) return ZF_EINVAL;
+  if (earlier == nullptr || n_earlier < 1 || n_earlier > zf::kMaxDeferred) return ZF_EINVAL;
+  zf::HistTable h{};
+  h.n = n_earlier;
+  for (int32_t s = 0; s < n_earlier; ++s) {
+    const zf_plan* e = earlier[s];
+    if (e == nullptr || e->nmats != p->nmats || e->layout != p->layout) return ZF_EINVAL;
+    for (int32_t q = 0; q < p->nmats; ++q) {
+      const DevMat& a = e->mats[q];
+      const DevMat& b = p->mats[q];
+      if (a.n != b.n || a.m != b.m || a.k != b.k || a.vec != b.vec || a.cm_vpt != b.cm_vpt ||
+          a.cm_nch != b.cm_nch)
+        return ZF_EINVAL;
+      if (b.n * (b.m - b.k) > 0 && a.grad == nullptr) return ZF_EINVAL;
+      // an earlier gradient is only read: disjoint from everything the step writes
+      const Span g = span(a.grad, ext(zf::kChannelMajor, a.n, a.m), a.ld_grad, 2);
+      const Ext es = ext(zf::kChannelMajor, b.n, b.k);
+      if (overlaps(g, span(b.out, ext(zf::kChannelMajor, b.n, b.m), b.ld_out, 4)) ||
+          overlaps(g, span(b.P, es, b.ld_state, 4)) || overlaps(g, span(b.M, es, b.ld_state, 4)) ||
+          overlaps(g, span(b.V, es, b.ld_state, 4)) ||
+          overlaps(g, span(b.weight, ext(zf::kChannelMajor, b.n, b.m), b.ld_weight, 2)))
+        return ZF_EINVAL;
+    }
+    h.mats[s] = e->d_mats;
+  }
+  const Table t{p->d_mats, p->d_off_up, p->nmats};
+  const hipError_t e = zf::launch_cm_handover_deferred(t, p->mats[0], p->blk_up,
+                                                       adam_consts(*hp, step), scale, h,
+                                                       as_stream(stream));
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 

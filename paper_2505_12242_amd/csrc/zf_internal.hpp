@@ -131,6 +131,14 @@ struct Pending {
   float scale;
 };
 
+// Deferred packing: the device tables of the plans of an interval's earlier
+// steps (the same matrices; their descriptors' grad = that step's gradient).
+constexpr int kMaxDeferred = 15;
+struct HistTable {
+  const DevMat* mats[kMaxDeferred];
+  int32_t n;
+};
+
 // Zen-auto's interval state when the device drives the interval
 // (zf_zen_state): steps of the current interval so far, and whether the
 // last step ended it.
@@ -192,6 +200,14 @@ hipError_t launch_cm_update(const Table& t, const DevMat& one, int64_t blocks, c
 // `grid` blocks loops over the `units` unpack blocks of the table.
 hipError_t launch_cm_unpack_zen(const Table& t, const DevMat& one, int64_t units,
                                 const ZenState* zst, bool stage, hipStream_t s);
+// The last step of an interval with deferred packing (batched plans only):
+// Adam on the selected channels (states in place) and +0.0 in their rows of
+// `out`; at the unselected channels out = scale * (((g_1 + g_2) + ...) + g),
+// g_s the channel's row of the gradient of earlier step s (h.mats[s - 1]),
+// g this step's.
+hipError_t launch_cm_handover_deferred(const Table& t, const DevMat& one, int64_t blocks,
+                                       const AdamK& c, float scale, const HistTable& h,
+                                       hipStream_t s);
 // from_stage: the source is the bf16 first-step stage (a one-step interval;
 // every matrix of the table has one).
 hipError_t launch_cm_unpack(const Table& t, const DevMat& one, int64_t blocks, float scale,

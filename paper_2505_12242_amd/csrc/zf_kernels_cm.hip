@@ -589,6 +589,120 @@ __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(c
 }
 
 // ---------------------------------------------------------------------------
+// a3-a6 with deferred packing: the interval's last step.  The unselected
+// part of each step's gradient stayed where it was written; here it is
+// summed, in step order and in fp32 (the accumulation's own sequence), and
+// scaled into the hand-over.  A block owns one channel and one chunk of its
+// rows, as in the update.
+// ---------------------------------------------------------------------------
+
+template <int VPT>
+__device__ __forceinline__ void cm_deferred_sum_vec(const HistTable& h, int32_t q, int64_t j,
+                                                    int64_t e0, int64_t len, rsrc_t rG,
+                                                    rsrc_t rOut, float scale) {
+  const int tid = threadIdx.x;
+  constexpr int kBatch = 4;  // steps whose rows are loaded before they are added
+  float a[VPT][kGroup];
+  const int32_t steps = h.n + 1;  // the earlier steps, then this one
+  for (int32_t s0 = 0; s0 < steps; s0 += kBatch) {
+    u32x4 gv[kBatch][VPT];
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      const int32_t s = s0 + b;
+      if (s < steps) {
+        rsrc_t r = rG;
+        if (s < h.n) {
+          const DevMat& hd = h.mats[s][q];
+          r = make_rsrc(hd.grad + j * hd.ld_grad + e0, len * 2);
+        }
+#pragma unroll
+        for (int p = 0; p < VPT; ++p) gv[b][p] = buf_b128<kAuxRO>(r, group_elem(p, tid) * 2, 0);
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      const int32_t s = s0 + b;
+      if (s < steps) {
+#pragma unroll
+        for (int p = 0; p < VPT; ++p) {
+          float g[kGroup];
+          widen8(gv[b][p], g);
+#pragma unroll
+          for (int i = 0; i < kGroup; ++i) a[p][i] = s == 0 ? g[i] : a[p][i] + g[i];
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < VPT; ++p) {
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) a[p][i] = a[p][i] * scale;
+    f32x8_store<kAuxWO>(rOut, group_elem(p, tid) * 4, a[p]);
+  }
+}
+
+__device__ __forceinline__ void cm_deferred_sum_elem(const HistTable& h, int32_t q, int64_t j,
+                                                     int64_t e0, int64_t len, rsrc_t rG,
+                                                     rsrc_t rOut, float scale) {
+  for (int64_t e = threadIdx.x; e < len; e += kThreads) {
+    const uint32_t o = static_cast<uint32_t>(e);
+    float a = 0.0f;
+    for (int32_t s = 0; s <= h.n; ++s) {
+      rsrc_t r = rG;
+      if (s < h.n) {
+        const DevMat& hd = h.mats[s][q];
+        r = make_rsrc(hd.grad + j * hd.ld_grad + e0, len * 2);
+      }
+      const float g = widen_bf16(buf_u16<kAuxRO>(r, o * 2, 0));
+      a = s == 0 ? g : a + g;
+    }
+    buf_put_f32<kAuxWO>(a * scale, rOut, o * 4, 0);
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void cm_handover_deferred_kernel(
+    const DevMat* __restrict__ mats, const int64_t* __restrict__ off, int32_t nmats, AdamK c,
+    float scale, HistTable h) {
+  const int64_t b = xcd_remap(blockIdx.x, gridDim.x);
+  int32_t lo = 0, hi = nmats - 1;
+  while (lo < hi) {  // the matrix: largest q with off[q] <= b
+    const int32_t mid = (lo + hi + 1) >> 1;
+    if (off[mid] <= b) lo = mid; else hi = mid - 1;
+  }
+  const int32_t q = lo;
+  const DevMat& d = mats[q];
+  const int64_t local = b - off[q];
+  const int64_t chunk = static_cast<int64_t>(d.cm_vpt) * kThreads * kGroup;
+  const int64_t j = local / d.cm_nch;
+  const int64_t ci = local % d.cm_nch;
+  const int64_t e0 = ci * chunk;
+  const int64_t len = min(chunk, d.n - e0);
+  const uint64_t mj = uniform_u64(d.mask[j >> 6]);
+  const bool sel = (mj >> (j & 63)) & 1ull;
+  const rsrc_t rG = make_rsrc(d.grad + j * d.ld_grad + e0, len * 2);
+  const rsrc_t rOut = make_rsrc(d.out + j * d.ld_out + e0, len * 4);
+  double ss = 0.0;
+  if (sel) {
+    const int64_t r = static_cast<int64_t>(uniform_i32(d.prefix[j >> 6])) +
+                      __popcll(mj & ((uint64_t(1) << (j & 63)) - 1));
+    const rsrc_t rP = make_rsrc(d.P + r * d.ld_state + e0, len * 4);
+    const rsrc_t rM = make_rsrc(d.M + r * d.ld_state + e0, len * 4);
+    const rsrc_t rV = make_rsrc(d.V + r * d.ld_state + e0, len * 4);
+    const rsrc_t rW = make_rsrc(d.weight + j * d.ld_weight + e0, len * 2);
+    if (d.vec)
+      cm_adam_vec_any<kCmInplace, false>(d.cm_vpt, rG, rP, rM, rV, rW, rP, rM, rV, rW, c, ss);
+    else
+      cm_adam_elem<kCmInplace, false>(rG, rP, rM, rV, rW, rP, rM, rV, rW, c, len, ss);
+    cm_zero_rows(d, rOut, len);
+  } else if (d.vec) {
+    if (d.cm_vpt >= 2) cm_deferred_sum_vec<kCmVpt>(h, q, j, e0, len, rG, rOut, scale);
+    else cm_deferred_sum_vec<1>(h, q, j, e0, len, rG, rOut, scale);
+  } else {
+    cm_deferred_sum_elem(h, q, j, e0, len, rG, rOut, scale);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // a6: hand-over.  Channel j of the dense buffer is +0.0 when selected, else
 // scale times its packed row -- or, STAGE (a one-step interval on a plan with
 // the bf16 first-step stage), scale times its widened row of the stage.
@@ -833,6 +947,17 @@ static void launch_cm_unpack_t(const Table& t, const DevMat& one, dim3 grid, flo
   else
     hipLaunchKernelGGL((cm_unpack_kernel<false, STAGE>), grid, dim3(kThreads), 0, s, t.mats,
                        t.off, t.nmats, one, scale);
+}
+
+hipError_t launch_cm_handover_deferred(const Table& t, const DevMat& one, int64_t blocks,
+                                       const AdamK& c, float scale, const HistTable& h,
+                                       hipStream_t s) {
+  (void)hipGetLastError();
+  (void)one;
+  if (blocks <= 0 || t.mats == nullptr) return hipSuccess;
+  hipLaunchKernelGGL(cm_handover_deferred_kernel, dim3(static_cast<uint32_t>(blocks)),
+                     dim3(kThreads), 0, s, t.mats, t.off, t.nmats, c, scale, h);
+  return hipGetLastError();
 }
 
 constexpr int64_t kCmUnpackZenGrid = 4096;  // 16 blocks per CU

@@ -12,6 +12,14 @@ issues one batched launch per kernel per step:
                    the packed buffer is only read), or zf_plan_update then
                    zf_plan_unpack when fuse_handover is False
 
+Deferred packing (deferred_pack=True; channel-major, fixed schedule, fused
+hand-over): no packed buffer.  The unselected part of each step's gradient
+stays in its gradient slot, every step but an interval's last runs the
+Adam part alone, and the last step sums the interval's gradients (in step
+order, the accumulation's own fp32 sequence) straight into the hand-over
+(zf_plan_update_handover_deferred).  The slots must hold every gradient of
+an interval: at least min(S, R) of them.
+
 Compact states and selections are double-buffered: a refresh writes the new
 selection and new states into the other buffer while reading the previous
 ones (ZF_STATES_REMAP), so a column that stays selected carries its moments
@@ -158,7 +166,7 @@ class SelectiveUpdateRunner:
                  zen_tau: Optional[float] = None, offload: bool = False, overlap: bool = True,
                  host_threads: Optional[int] = None, fuse_handover: bool = True,
                  warmup: int = 0, refresh_pending: bool = True, first_step_stage: bool = True,
-                 zen_on_device: bool = True):
+                 zen_on_device: bool = True, deferred_pack: bool = False):
         self.device = torch.device(device) if device is not None else torch.device("cuda")
         self.shapes = [(int(n), int(m)) for n, m in shapes]
         self.ratio, self.hp, self.R, self.S = ratio, hp, int(refresh), int(accum)
@@ -175,14 +183,27 @@ class SelectiveUpdateRunner:
         # of the packed buffer are the next update passes).  A refresh step
         # that starts an interval then fills it from the score pass.
         # (row-major: the fixed schedule with the fused hand-over only)
+        # deferred packing (channel-major, fixed schedule, hand-over fused, no
+        # offload): the unselected part of every step's gradient stays in its
+        # slot until the interval ends; the interval's last step sums them
+        self.deferred = bool(deferred_pack)
+        if self.deferred:
+            if (layout == ROW_MAJOR or zen_tau is not None or self.offload
+                    or not self.keep_unpacked or not self.fuse_handover):
+                raise ValueError("deferred packing runs in the channel-major layout on the fixed "
+                                 "schedule with the fused hand-over, without offload")
+            if len(grad_slots) < min(self.S, self.R):
+                raise ValueError("deferred packing keeps every gradient of an interval: it needs "
+                                 f"at least min(S, R) = {min(self.S, self.R)} gradient slots")
         self.use_stage = (bool(first_step_stage) and not self.offload and self.keep_unpacked
+                          and not self.deferred
                           and (layout != ROW_MAJOR or (zen_tau is None and self.fuse_handover)))
         # with the fixed schedule and the fused hand-over a refresh step also
         # packs from the score pass: into the stage when an interval starts,
         # and (channel-major) into the hand-over buffer when the step is a
         # whole interval
         self.score_pack = self.use_stage and zen_tau is None and self.fuse_handover
-        self.score_handover = self.score_pack and layout != ROW_MAJOR
+        self.score_handover = (self.score_pack or self.deferred) and layout != ROW_MAJOR
         self._in_stage = False  # the current interval's sums are in the stage
         self.weights = list(weights)
         self.init_master = list(init_master) if init_master is not None else None
@@ -233,7 +254,8 @@ class SelectiveUpdateRunner:
                 self.states[p].append(tuple(alloc_stored(layout, n, k, f32, dev)
                                             for _ in range(3)))
             for a in range(nacc):
-                self.accs[a].append(alloc_stored(layout, n, m - k, f32, dev))
+                self.accs[a].append(None if self.deferred
+                                    else alloc_stored(layout, n, m - k, f32, dev))
             if self.use_stage:
                 self.stage.append(alloc_stored(layout, n, m, torch.bfloat16, dev))
             self.norms.append(torch.empty(m, dtype=f32, device=dev))
@@ -385,8 +407,16 @@ class SelectiveUpdateRunner:
                     plan.update_adam_handover(self.hp, t, mode, st)
                 return kind
             if end and self.keep_unpacked and self.fuse_handover:
-                with rec("update_handover"):
-                    plan.update_handover(self.hp, t, mode, length, self.S, 1.0 / length, st)
+                if self.deferred and length > 1:
+                    # the interval's earlier gradients, still in their slots
+                    nsl = len(self.grad_slots)
+                    earlier = [self.plans[(tt - 1) % nsl][self.cur][self.cur_a]
+                               for tt in range(t - length + 1, t)]
+                    with rec("update_handover"):
+                        plan.update_handover_deferred(self.hp, t, earlier, 1.0 / length, st)
+                else:
+                    with rec("update_handover"):
+                        plan.update_handover(self.hp, t, mode, length, self.S, 1.0 / length, st)
                 return kind
             if refresh and self._pend is not None:
                 scale_p, th_p = self._pend[:2]
@@ -394,10 +424,11 @@ class SelectiveUpdateRunner:
                     plan.update_pending(self.hp, t, self.S, th_p, scale_p, stream=st)
                 self._start_held_update(st)
             else:
-                name = ("update_adam" if staged else "update_first" if length == 1
+                adam_only = staged or self.deferred
+                name = ("update_adam" if adam_only else "update_first" if length == 1
                         else "update_second" if length == 2 else "update")
                 with rec(name):
-                    plan.update(self.hp, t, mode, length, self.S, pack=not staged, stream=st)
+                    plan.update(self.hp, t, mode, length, self.S, pack=not adam_only, stream=st)
         elif self.zen_device:
             # the interval ends on the device (trigger, S_max) or by the
             # caller's rule (before a refresh, warm-up steps)
@@ -605,6 +636,9 @@ class SelectiveUpdateRunner:
         interval's packed sums and, with the offloaded optimizer, the store
         and its step counter.  Drains the pipeline first (sync).  Tensors are
         CPU copies in the runner's layout; the weights stay the caller's."""
+        if self.deferred:
+            raise NotImplementedError("deferred packing keeps an interval's sums in the "
+                                      "gradient slots: no checkpoint of them")
         self.sync()
         self._resolve_zen()
         c, a = self.cur, self.cur_a
@@ -627,6 +661,9 @@ class SelectiveUpdateRunner:
         """Continues from a state_dict of a runner with the same shapes,
         ratio, layout, schedule and offload mode (the caller restores the
         weights)."""
+        if self.deferred:
+            raise NotImplementedError("deferred packing keeps an interval's sums in the "
+                                      "gradient slots: no checkpoint of them")
         mine = {"shapes": list(self.shapes), "ks": list(self.ks), "layout": self.layout,
                 "R": self.R, "S": self.S, "warmup": self.warmup, "zen_tau": self.zen_tau,
                 "offload": self.offload}
@@ -675,6 +712,8 @@ class SelectiveUpdateRunner:
     def acc(self) -> List[torch.Tensor]:
         """The last interval's packed sums, fp32 (after an interval's first
         step with the bf16 stage: a widened copy of the stage, exact)."""
+        if self.deferred:
+            raise AttributeError("deferred packing materialises no packed buffer")
         self._resolve_zen()
         if self._in_stage:
             dim = 1 if self.layout == ROW_MAJOR else 0

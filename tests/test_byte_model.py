@@ -106,3 +106,24 @@ def test_read_write_split():
     nk = 64 * 10 + 7 * 3
     nu = 64 * 90 + 7 * 30
     assert t["update"] == [14 * nk + 6 * nu, 14 * nk + 4 * nu]
+
+
+def test_deferred_packing_bytes():
+    """Deferred packing: steps before an interval's last move the selected
+    part only (28 B per selected element); the last step of L steps reads
+    each step's gradient once at the unselected elements (2 B each) and
+    writes the hand-over (4 B per element, zeros at the selected)."""
+    n, m, k = 4096, 4096, 410
+    u = m - k
+    sh, ks = [(n, m)], [k]
+    kw = dict(fused_handover=True, deferred=True)
+    assert bench.step_bytes(sh, ks, True, True, False, length=1, **kw) == {
+        "colnorm": 2 * n * m + 4 * m, "topk_select": 8 * m + 12 * 64, "update": 28 * n * k,
+        "unpack": 0}
+    assert bench.step_bytes(sh, ks, False, False, False, length=3, **kw)["update"] == 28 * n * k
+    for L in (2, 4, 8):
+        assert bench.step_bytes(sh, ks, False, False, True, length=L, **kw)["update"] == \
+            28 * n * k + 4 * n * k + (2 * L + 4) * n * u
+    # a refresh step that is a whole interval hands over from the score pass
+    b = bench.step_bytes(sh, ks, True, True, True, length=1, **kw)
+    assert b["colnorm"] == 6 * n * m + 4 * m and b["update"] == 32 * n * k
