@@ -492,12 +492,13 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def recorded_traffic(launch_kind: str, workload: str, layout: str):
+def recorded_traffic(launch_kind: str, workload: str, variant: str):
     """HBM bytes per launch of one update launch kind, from rocprofv3 PMC
     counters (FETCH_SIZE and WRITE_SIZE runs, scaled by the reference copy
-    stream's reading), if recorded for this workload, layout and the current
-    kernel sources."""
-    path = os.path.join(PROFILES, f"traffic_{workload}_{layout}.md")
+    stream's reading), if recorded for this workload, variant (layout, and
+    for the channel-major eager path "-every-step") and the current kernel
+    sources."""
+    path = os.path.join(PROFILES, f"traffic_{workload}_{variant}.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
@@ -783,7 +784,8 @@ def main(argv=None) -> int:
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": recorded_traffic(dom, wl.name, args.layout),
+            "traffic": recorded_traffic(dom, wl.name, args.layout + (
+                "-every-step" if layout == zf.CHANNEL_MAJOR and not runner.deferred else "")),
             "bytes_per_launch": round(nbytes),
             "byte_model": "survey per-unit figures" if dom == "update" else "build",
             "avg_launch_ms": round(avg, 4),
