@@ -3,18 +3,21 @@ the paper's 13B model (Evaluation, Table "Experimental environments") and
 its sweep of the top-k ratio and the selection refresh interval
 (Evaluation, "Sensitivity of Hyperparameters"), in bench.py's launch
 configuration: batched plans over the whole set, a ring of gradient slots,
-the channel-major layout with the bf16 first-step stage, and the hand-over
-fused into each interval's last update (one-step intervals take it from
-the score pass).
+the channel-major layout, and the hand-over fused into each interval's last
+update (one-step intervals take it from the score pass).
 
 * test_13b_full_set: all 282 matrices (13.0 G parameters) for 8 steps of
   the R = S = 4 schedule at ratio 10% -- first selection, accumulation,
-  hand-over at 4, refresh with state remap at 5, hand-over at 8.
+  hand-over at 4, refresh with state remap at 5, hand-over at 8 -- in both
+  packing modes: deferred (bench.py's default: the interval's gradients
+  stay in a four-slot ring and its last step sums them,
+  zf_plan_update_handover_deferred) and every step (the bf16 stage, then
+  fp32 packed sums).
 * test_13b_sweep: the 13B shapes (embedding, one decoder layer: 5120^2,
   13824 x 5120, 5120 x 13824, LM head) at ratios 1%, 5% and 25% with R = 1
   (every step refreshes and hands over at once: zf_plan_colnorm_handover,
-  then zf_plan_update_adam_handover) and R = 16 (four S = 4 intervals, then
-  a refresh with state remap), S = 4.
+  then zf_plan_update_adam_handover) and R = 16 (four S = 4 intervals with
+  deferred packing, then a refresh with state remap), S = 4.
 
 Checks, every matrix, every step:
 * on refresh steps the selection (indices, mask, prefix) is the exact
@@ -23,8 +26,8 @@ Checks, every matrix, every step:
   columns (the k-th and (k+1)-th ranked among them) match the oracle's
   colnorm within 1e-5 (scores are per column, so a column subset is exact);
 * sampled rows of every output -- compact states P/M/V, the bf16 weight,
-  the packed sums (or the bf16 stage after an interval's first step) and
-  the hand-over -- equal, bit for bit, the oracle's composition run on those
+  the packed sums (or the bf16 stage after an interval's first step; with
+  deferred packing there are none) and the hand-over -- equal, bit for bit, the oracle's composition run on those
   rows under the device's selection (every step but the scores is
   row-wise, so the rows of the outputs follow from the rows of the inputs).
 Sampled matrices are in addition run through the oracle in full
@@ -100,7 +103,7 @@ class RowReplay:
         return O.unpack(self.A, self.sel, float(np.float32(1.0 / steps)))
 
 
-def run_and_check(wl, nslots, steps, full_names, tag):
+def run_and_check(wl, nslots, steps, full_names, tag, deferred=False):
     hp = zf.AdamHparams(wl.hyper.lr, wl.hyper.beta1, wl.hyper.beta2, wl.hyper.eps,
                         wl.hyper.weight_decay)
     hyper = (hp.lr, hp.beta1, hp.beta2, hp.eps, hp.weight_decay)
@@ -117,8 +120,8 @@ def run_and_check(wl, nslots, steps, full_names, tag):
             for q in full}
     del w0
     runner = zf.SelectiveUpdateRunner(shapes, wl.ratio, hp, wl.refresh, wl.accum, slots, weights,
-                                      device=dev, layout=layout)
-    assert runner.use_stage and runner.fuse_handover
+                                      device=dev, layout=layout, deferred_pack=deferred)
+    assert runner.fuse_handover and runner.use_stage != deferred
     pool = ThreadPoolExecutor(max(1, len(full)))
     try:
         for t in range(1, steps + 1):
@@ -162,7 +165,10 @@ def run_and_check(wl, nslots, steps, full_names, tag):
                 assert same_bits(P, rp.P) and same_bits(M, rp.M) and same_bits(V, rp.V), \
                     (names[q], t)
                 assert np.array_equal(rows_of(weights[q], r), rp.W), (names[q], t)
-                if not end:
+                if end:
+                    assert same_bits(rows_of(runner.unpacked[q], r), rp.hand_over(sii)), \
+                        (names[q], t)
+                elif not deferred:  # deferred packing keeps no sums between steps
                     if runner._in_stage:
                         stage_rows = runner.stage[q].index_select(1, r.to(dev))
                         a = O.widen(np.ascontiguousarray(bits_np(
@@ -170,9 +176,6 @@ def run_and_check(wl, nslots, steps, full_names, tag):
                     else:
                         a = rows_of(runner.current_acc[q], r)
                     assert same_bits(a, rp.A), (names[q], t)
-                else:
-                    assert same_bits(rows_of(runner.unpacked[q], r), rp.hand_over(sii)), \
-                        (names[q], t)
             # scores are per column: one oracle colnorm over the sampled
             # columns of all matrices with the same row count
             for n, items in col_checks.items():
@@ -207,12 +210,16 @@ def run_and_check(wl, nslots, steps, full_names, tag):
 
 
 @pytest.mark.timeout(1200)
-def test_13b_full_set():
+@pytest.mark.parametrize("packing", ["deferred", "every-step"])
+def test_13b_full_set(packing):
     from workloads import get_workload
     wl = get_workload("llama2-13b-full")
     assert len(wl.matrices) == 282 and wl.params == 13_015_449_600
-    run_and_check(wl, 2, 8, ["layers.0.q_proj", "layers.0.gate_proj", "layers.39.down_proj",
-                             "lm_head"], "13b-full")
+    deferred = packing == "deferred"
+    # deferred packing keeps the interval's S = 4 gradients in the ring
+    run_and_check(wl, 4 if deferred else 2, 8,
+                  ["layers.0.q_proj", "layers.0.gate_proj", "layers.39.down_proj", "lm_head"],
+                  f"13b-full {packing}", deferred=deferred)
 
 
 SWEEP = [(0.01, 1, 3, "layers.0.gate_proj"), (0.05, 1, 3, "layers.0.down_proj"),
@@ -232,4 +239,9 @@ def test_13b_sweep(ratio, R, steps, full):
     assert sorted({(mt.n, mt.m) for mt in keep}) == [(5120, 5120), (5120, 13824),
                                                      (13824, 5120), (32000, 5120)]
     wl = wl.with_(matrices=tuple(keep), ratio=ratio, refresh=R, accum=4)
-    run_and_check(wl, 3, steps, [full], f"13b ratio {ratio} R {R}")
+    # R = 16 runs with deferred packing (four slots for the S = 4 intervals);
+    # R = 1 hands over every step from the score pass, the same launches in
+    # both packing modes
+    deferred = R > 1
+    run_and_check(wl, 4 if deferred else 3, steps, [full], f"13b ratio {ratio} R {R}",
+                  deferred=deferred)
