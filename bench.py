@@ -85,8 +85,8 @@ def parse_args(argv=None):
                     help="with --offload: host threads of the deferred update (default: "
                          "min(16, cpu count))")
     ap.add_argument("--packing", choices=["deferred", "every-step"], default="deferred",
-                    help="deferred (default where it applies: channel-major, fixed schedule, no "
-                         "offload): every gradient of an interval stays in its slot and the "
+                    help="deferred (default where it applies: fixed schedule, fused hand-over, "
+                         "no offload): every gradient of an interval stays in its slot and the "
                          "interval's last step sums them into the hand-over, with no packed "
                          "buffer (the ring gets at least min(S, R) slots); every-step: the "
                          "unselected part is accumulated into the packed buffer at every step")
@@ -492,12 +492,33 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
+def launch_kernels(kind: str, channel_major: bool, deferred: bool) -> str:
+    """The kernels behind one update launch kind of the runner."""
+    if channel_major:
+        if deferred and kind == "update_handover":
+            return ("cm_handover_deferred_kernel (the interval's last step: Adam + the sum of "
+                    "the interval's gradients into the hand-over)")
+        if kind == "update_adam":
+            return "cm_update_kernel, selected-only grid (Adam + bf16 write-back)"
+        if kind == "update":
+            return ("cm_update_kernel<true, true, true, false, false, false, false, 3> "
+                    "(fused Adam + bf16 write-back + pack)")
+        return f"cm_update_kernel ({kind}) (fused Adam + bf16 write-back + pack)"
+    if deferred and kind == "update_handover":
+        return ("rv_update_kernel Adam-only pass, then rv_update_kernel<true, false, false, false, "
+                "false, false, true> (the interval's last step: Adam, then the sum of the "
+                "interval's gradients into the hand-over)")
+    if kind == "update_adam":
+        return ("update_kernel (refresh steps) / rv_update_kernel (steps in place): Adam + bf16 "
+                "write-back")
+    return f"rv_update_kernel / update_kernel ({kind}) (fused Adam + bf16 write-back + pack)"
+
+
 def recorded_traffic(launch_kind: str, workload: str, variant: str):
     """HBM bytes per launch of one update launch kind, from rocprofv3 PMC
     counters (FETCH_SIZE and WRITE_SIZE runs, scaled by the reference copy
     stream's reading), if recorded for this workload, variant (layout, and
-    for the channel-major eager path "-every-step") and the current kernel
-    sources."""
+    for the eager path "-every-step") and the current kernel sources."""
     path = os.path.join(PROFILES, f"traffic_{workload}_{variant}.md")
     if not os.path.exists(path):
         return None
@@ -595,8 +616,8 @@ def main(argv=None) -> int:
               f"{calib['read_GB/s']}, copy {calib['copy_GB/s']}, read-modify-write "
               f"{calib['rmw_GB/s']} GB/s", file=sys.stderr, flush=True)
 
-    deferred = (args.packing == "deferred" and layout == zf.CHANNEL_MAJOR and args.zen_tau is None
-                and not args.offload and not args.separate_handover)
+    deferred = (args.packing == "deferred" and args.zen_tau is None and not args.offload
+                and not args.separate_handover)
     if deferred:
         args.slots = max(args.slots, min(wl.accum, wl.refresh))
     t0 = time.perf_counter()
@@ -767,15 +788,7 @@ def main(argv=None) -> int:
         avg = sum(e["ms"]) / n
         nbytes = (e["survey"] if dom == "update" else e["bytes"]) / n
         achieved = nbytes / (avg * 1e-3) / 1e9
-        if layout == zf.CHANNEL_MAJOR and runner.deferred and dom == "update_handover":
-            kname = "cm_handover_deferred_kernel (the interval's last step: Adam + the sum of " \
-                    "the interval's gradients into the hand-over)"
-        elif layout == zf.CHANNEL_MAJOR:
-            kname = ("cm_update_kernel<true, true, true, false, false, false, false, 3>"
-                     if dom == "update" else f"cm_update_kernel ({dom})") + \
-                " (fused Adam + bf16 write-back + pack)"
-        else:
-            kname = f"rv_update_kernel / update_kernel ({dom}) (fused Adam + bf16 write-back + pack)"
+        kname = launch_kernels(dom, layout == zf.CHANNEL_MAJOR, runner.deferred)
         roof = {
             "kernel": kname,
             "launch_kind": dom,
@@ -785,7 +798,7 @@ def main(argv=None) -> int:
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": recorded_traffic(dom, wl.name, args.layout + (
-                "-every-step" if layout == zf.CHANNEL_MAJOR and not runner.deferred else "")),
+                "" if runner.deferred else "-every-step")),
             "bytes_per_launch": round(nbytes),
             "byte_model": "survey per-unit figures" if dom == "update" else "build",
             "avg_launch_ms": round(avg, 4),

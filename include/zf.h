@@ -536,10 +536,17 @@ zf_status zf_plan_update_handover(zf_plan* plan, const zf_adam_hparams* hp, int6
  * is read once, at its unselected channels, when the interval ends (2 bytes
  * per element per step, instead of the packed buffer's 8 per step).
  * earlier: HOST array of n_earlier (1..15) plans over the same matrices in
- * the same order (same n, m, k and access path), in step order, whose
- * descriptors' grad is the gradient of that step; only those gradients are
- * read.  They must not overlap what this step writes.  Channel-major plans
- * without a full-state store; `unpacked` required; scale finite. */
+ * the same order (same n, m, k; channel-major: the same access path), in
+ * step order, whose descriptors' grad is the gradient of that step; only
+ * those gradients are read.  They must not overlap what this step writes.
+ * Both layouts, plans without a full-state store; `unpacked` required;
+ * scale finite.  Row-major: two launches, the Adam-only pass and a
+ * hand-over pass (the 16-byte kernels when the plan runs the 16-byte update
+ * and every earlier gradient has 16-byte rows, else the per-column ones);
+ * the hand-over pass reads every element of each step's gradient, since
+ * the selected columns share their cache lines.  ZF_EINVAL (nothing
+ * enqueued) on a mismatch or when an earlier gradient's row stride does
+ * not fit the plan's row blocks. */
 zf_status zf_plan_update_handover_deferred(zf_plan* plan, const zf_adam_hparams* hp, int64_t step,
                                            const zf_plan* const* earlier, int32_t n_earlier,
                                            float scale, zf_stream stream);

@@ -1292,38 +1292,62 @@ zf_status zf_plan_update_handover(zf_plan* p, const zf_adam_hparams* hp, int64_t
 zf_status zf_plan_update_handover_deferred(zf_plan* p, const zf_adam_hparams* hp, int64_t step,
                                            const zf_plan* const* earlier, int32_t n_earlier,
                                            float scale, zf_stream stream) {
-  if (p == nullptr || p->layout != zf::kChannelMajor || !p->can_adam || !p->can_handover ||
-      p->has_store)
-    return ZF_EINVAL;
+  if (p == nullptr || !p->can_adam || !p->can_handover || p->has_store) return ZF_EINVAL;
   if (!hparams_ok(hp) || step < 1 || !std::isfinite(scale)) return ZF_EINVAL;
   if (earlier == nullptr || n_earlier < 1 || n_earlier > zf::kMaxDeferred) return ZF_EINVAL;
+  const int32_t L = p->layout;
+  const bool cm = L == zf::kChannelMajor;
+  // row-major: the 16-byte kernel reads the earlier gradients as it reads
+  // this step's (16-byte rows, strides within its 32-bit row offsets)
+  bool rv = !cm && p->mats[0].rv;
   zf::HistTable h{};
   h.n = n_earlier;
   for (int32_t s = 0; s < n_earlier; ++s) {
     const zf_plan* e = earlier[s];
-    if (e == nullptr || e->nmats != p->nmats || e->layout != p->layout) return ZF_EINVAL;
+    if (e == nullptr || e->nmats != p->nmats || e->layout != L) return ZF_EINVAL;
     for (int32_t q = 0; q < p->nmats; ++q) {
       const DevMat& a = e->mats[q];
       const DevMat& b = p->mats[q];
-      if (a.n != b.n || a.m != b.m || a.k != b.k || a.vec != b.vec || a.cm_vpt != b.cm_vpt ||
-          a.cm_nch != b.cm_nch)
+      if (a.n != b.n || a.m != b.m || a.k != b.k) return ZF_EINVAL;
+      if (cm && (a.vec != b.vec || a.cm_vpt != b.cm_vpt || a.cm_nch != b.cm_nch))
         return ZF_EINVAL;
       if (b.n * (b.m - b.k) > 0 && a.grad == nullptr) return ZF_EINVAL;
+      if (!cm) {
+        // the row blocks of this plan's kernels address the earlier rows
+        // through the same 32-bit offsets
+        const int64_t lim = int64_t(1) << 31;
+        if (b.n > 1 && a.ld_grad * 2 >= lim / std::max<int64_t>(b.up_rows, 1)) return ZF_EINVAL;
+        if (rv && !(aligned(a.grad, 16) && (b.n <= 1 || (a.ld_grad % 8 == 0 &&
+                                                          a.ld_grad * 2 < lim / b.rv_rows))))
+          rv = false;
+      }
       // an earlier gradient is only read: disjoint from everything the step writes
-      const Span g = span(a.grad, ext(zf::kChannelMajor, a.n, a.m), a.ld_grad, 2);
-      const Ext es = ext(zf::kChannelMajor, b.n, b.k);
-      if (overlaps(g, span(b.out, ext(zf::kChannelMajor, b.n, b.m), b.ld_out, 4)) ||
+      const Span g = span(a.grad, ext(L, a.n, a.m), a.ld_grad, 2);
+      const Ext es = ext(L, b.n, b.k);
+      if (overlaps(g, span(b.out, ext(L, b.n, b.m), b.ld_out, 4)) ||
           overlaps(g, span(b.P, es, b.ld_state, 4)) || overlaps(g, span(b.M, es, b.ld_state, 4)) ||
           overlaps(g, span(b.V, es, b.ld_state, 4)) ||
-          overlaps(g, span(b.weight, ext(zf::kChannelMajor, b.n, b.m), b.ld_weight, 2)))
+          overlaps(g, span(b.weight, ext(L, b.n, b.m), b.ld_weight, 2)))
         return ZF_EINVAL;
     }
     h.mats[s] = e->d_mats;
   }
-  const Table t{p->d_mats, p->d_off_up, p->nmats};
-  const hipError_t e = zf::launch_cm_handover_deferred(t, p->mats[0], p->blk_up,
-                                                       adam_consts(*hp, step), scale, h,
-                                                       as_stream(stream));
+  const AdamK c = adam_consts(*hp, step);
+  const hipStream_t st = as_stream(stream);
+  hipError_t e;
+  if (cm) {
+    e = zf::launch_cm_handover_deferred(Table{p->d_mats, p->d_off_up, p->nmats}, p->mats[0],
+                                        p->blk_up, c, scale, h, st);
+  } else if (rv) {
+    e = zf::launch_rv_handover_deferred(Table{p->d_mats, p->d_off_upv, p->nmats}, p->mats[0],
+                                        p->blk_upv, c, scale, h, st);
+  } else {
+    e = zf::launch_update(Table{p->d_mats, p->d_off_up, p->nmats}, p->mats[0], p->blk_up, c,
+                          zf::kInplace, 0, true, false, false, 1.0f, st);
+    if (e == hipSuccess)
+      e = zf::launch_rm_handover_deferred(Table{p->d_mats, p->d_off_unp, p->nmats}, p->blk_unp,
+                                          scale, h, st);
+  }
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 

@@ -176,6 +176,18 @@ hipError_t launch_unpack(const Table& t, const DevMat& one, int64_t blocks, floa
 hipError_t launch_rv_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
                             int32_t mode, int32_t first, bool adam, bool pack, bool handover,
                             float scale, hipStream_t s, double* zs = nullptr);
+// Deferred packing, row-major, the interval's last step (states in place):
+// Adam on the selected columns and the hand-over of the unselected ones,
+// g_1 + ... + g_t summed in step order from h's plans (the earlier steps)
+// and this plan (step t), times scale.  The 16-byte kernel over the plan's
+// 16-byte update grid, as two passes (Adam-only, then the hand-over) ...
+hipError_t launch_rv_handover_deferred(const Table& t, const DevMat& one, int64_t blocks,
+                                       const AdamK& c, float scale, const HistTable& h,
+                                       hipStream_t s);
+// ... or, off the 16-byte path, the hand-over alone over the unpack grid
+// (Adam then runs as the per-column update's Adam-only pass).
+hipError_t launch_rm_handover_deferred(const Table& t, int64_t blocks, float scale,
+                                       const HistTable& h, hipStream_t s);
 
 // Channel-major kernels (zf_kernels_cm.hip).
 // out == 1: also copy every channel's gradient row to its row of acc1 (the

@@ -680,6 +680,49 @@ __global__ __launch_bounds__(kThreads) void unpack_kernel(const DevMat* __restri
   }
 }
 
+// a3-a6 with deferred packing, row-major buffers off the 16-byte path: the
+// interval's hand-over from the gradients it kept (the earlier steps' plans,
+// then this step's), summed in step order in fp32 and scaled, +0.0 at a
+// selected column.  Same column mapping as the hand-over above; the Adam
+// part of the step is the per-column update's.
+__global__ __launch_bounds__(kThreads) void rm_handover_deferred_kernel(
+    const DevMat* __restrict__ mats, const int64_t* __restrict__ off, int32_t nmats, float scale,
+    HistTable hist) {
+  int64_t local;
+  const DevMat& d = get_mat<true>(mats, off, nmats, mats[0], local);
+  const int32_t q = static_cast<int32_t>(&d - mats);
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int64_t cblk = local % d.up_cb;
+  const int64_t rblk = local / d.up_cb;
+  const int64_t word = cblk * (kUpdateCols / 64) + wave;
+  const int64_t j = word * 64 + lane;
+  if (j >= d.m) return;
+  const bool sel = (d.mask[word] >> lane) & 1ull;
+  const int64_t i0 = rblk * d.up_rows;
+  const int64_t i1 = min(i0 + static_cast<int64_t>(d.up_rows), d.n);
+  const int32_t rows = static_cast<int32_t>(i1 - i0);
+  const rsrc_t rG = rows_rsrc(d.grad, i0, i1, d.ld_grad, d.m);
+  const rsrc_t rD = rows_rsrc(d.out, i0, i1, d.ld_out, d.m);
+  const uint32_t sG = static_cast<uint32_t>(d.ld_grad * 2);
+  const uint32_t sD = static_cast<uint32_t>(d.ld_out * 4);
+  const uint32_t vG = static_cast<uint32_t>(j) * 2u;
+  const uint32_t vD = static_cast<uint32_t>(j) * 4u;
+  for (int32_t i = 0; i < rows; ++i) {
+    float a = 0.0f;
+    for (int32_t st = 0; st < hist.n; ++st) {
+      const DevMat& hd = hist.mats[st][q];
+      const rsrc_t rE = rows_rsrc(hd.grad, i0, i1, hd.ld_grad, d.m);
+      const float g = widen_bf16(buf_u16<kStream>(
+          rE, vG, static_cast<uint32_t>(i) * static_cast<uint32_t>(hd.ld_grad * 2)));
+      a = st == 0 ? g : a + g;
+    }
+    const float g = widen_bf16(buf_u16<kStream>(rG, vG, static_cast<uint32_t>(i) * sG));
+    a = hist.n > 0 ? a + g : g;
+    buf_put_f32(sel ? 0.0f : a * scale, rD, vD, static_cast<uint32_t>(i) * sD);
+  }
+}
+
 }  // namespace
 
 #define ZF_LAUNCH(KERNEL, GRID, BLOCK, STREAM, T, ...)                                      \
@@ -761,6 +804,15 @@ hipError_t launch_unpack(const Table& t, const DevMat& one, int64_t blocks, floa
   if (blocks > 0)
     ZF_LAUNCH(unpack_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), s, t, one,
               scale);
+  return hipGetLastError();
+}
+
+hipError_t launch_rm_handover_deferred(const Table& t, int64_t blocks, float scale,
+                                       const HistTable& h, hipStream_t s) {
+  (void)hipGetLastError();
+  if (blocks <= 0 || t.mats == nullptr) return hipSuccess;
+  hipLaunchKernelGGL(rm_handover_deferred_kernel, dim3(static_cast<uint32_t>(blocks)),
+                     dim3(kThreads), 0, s, t.mats, t.off, t.nmats, scale, h);
   return hipGetLastError();
 }
 

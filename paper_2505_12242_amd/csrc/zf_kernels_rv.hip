@@ -46,6 +46,16 @@
 // slot k + u) and row block into the column-score workspace -- the partials
 // of the row-major statistics pass, in the same order, for its finalize.
 //
+// DEF (deferred packing, the hand-over of the interval's last step; no
+// Adam, no packed buffer): the column-space lanes load, for their 8 columns
+// of each row, that row of every earlier gradient of the interval (the same
+// matrix in the earlier steps' plans) and of this step's, add them in step
+// order in fp32 with this step's last, and store the hand-over -- +0.0 at a
+// selected column, else the sum times `scale` -- with two 16-byte stores.
+// The step's Adam runs before it as the Adam-only instantiation over the
+// same tiles.  (Fused into one pass with the Adam lanes the kernel needs
+// registers for both and ran slower than the two passes.)
+//
 // The arithmetic per element is that of the per-column kernel (same fp32
 // operations in the same order), so both paths give identical bits.
 #include "zf_device.hpp"
@@ -70,6 +80,30 @@ __device__ __forceinline__ int64_t selected_below(const DevMat& d, int64_t j) {
          __popcll(mw & ((uint64_t(1) << (j & 63)) - 1));
 }
 
+// The 8 bf16 of a 16-byte group, widened (element x in half x & 1 of word
+// x >> 1).
+__device__ __forceinline__ void widen_group(u32x4 v, float (&f)[8]) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int x = 0; x < 8; ++x)
+    f[x] = widen_bf16(static_cast<uint16_t>(w[x >> 1] >> (16 * (x & 1))));
+}
+
+// Row b of a batch, 8 columns at byte offset vo: one 16-byte load, or the
+// ragged tail of a tile element by element (zeros past the tile).
+template <int AUX>
+__device__ __forceinline__ u32x4 load_group(rsrc_t r, uint32_t vo, uint32_t so, int32_t cols) {
+  if (cols >= 8) return buf_b128<AUX>(r, vo, so);
+  uint32_t w[4] = {0u, 0u, 0u, 0u};
+  for (int x = 0; x < cols; ++x)
+    w[x >> 1] |= static_cast<uint32_t>(buf_u16<AUX>(r, vo + 2 * x, so)) << (16 * (x & 1));
+  return u32x4{w[0], w[1], w[2], w[3]};
+}
+
+// earlier steps whose rows are loaded before they are added (more costs
+// the pass its occupancy)
+constexpr int kDefBatch = 2;
+
 __device__ __forceinline__ float4 as_f4(u32x4 v) {
   return make_float4(__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z),
                      __uint_as_float(v.w));
@@ -78,19 +112,23 @@ __device__ __forceinline__ u32x4 as_u4(float a, float b, float c, float d) {
   return u32x4{__float_as_uint(a), __float_as_uint(b), __float_as_uint(c), __float_as_uint(d)};
 }
 
-template <bool BATCHED, bool ADAM, bool PACK, bool HAND, bool STATS, bool A16>
+template <bool BATCHED, bool ADAM, bool PACK, bool HAND, bool STATS, bool A16, bool DEF>
 __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __restrict__ mats,
                                                              const int64_t* __restrict__ off,
                                                              int32_t nmats, DevMat one, AdamK c,
                                                              int32_t first, float scale,
-                                                             double* __restrict__ zs) {
+                                                             double* __restrict__ zs,
+                                                             HistTable hist) {
   static_assert(!STATS || (ADAM && PACK && !HAND), "statistics of the fused update");
+  static_assert(!DEF || (BATCHED && !ADAM && !PACK && !HAND && !STATS && !A16),
+                "the deferred hand-over pass");
   __shared__ __attribute__((aligned(16))) uint16_t sg[kRvBatch][kRvMaxCols];
   __shared__ __attribute__((aligned(16))) uint16_t sa[A16 ? kRvBatch : 1][A16 ? kRvMaxCols : 8];
   __shared__ __attribute__((aligned(16))) float sd[HAND ? kRvBatch : 1][HAND ? kRvMaxCols : 4];
 
   int64_t local;
   const DevMat& d = get_mat<BATCHED>(mats, off, nmats, one, local);
+  const int32_t q = BATCHED ? static_cast<int32_t>(&d - mats) : 0;
   const int64_t cblk = local % d.rv_cb;
   const int64_t rblk = local / d.rv_cb;
   const int64_t c0 = cblk * d.rv_w;
@@ -188,15 +226,24 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
     rW = rows_rsrc(d.weight, i0, i1, d.ld_weight, d.m);
     sW = static_cast<uint32_t>(d.ld_weight * 2);
   }
-  if constexpr (HAND) {
+  if constexpr (HAND || DEF) {
     rD = rows_rsrc(d.out, i0, i1, d.ld_out, d.m);
     sD = static_cast<uint32_t>(d.ld_out * 4);
   }
+  // DEF: which of the lane's 8 columns are selected (c0 and g8 are
+  // multiples of 8, so the 8 bits sit in one mask word)
+  uint32_t sel8 = 0;
 
   // Column-space lane roles: G loads (row pair half h, 8-column group g8),
   // hand-over stores (4-column group).
   const int h = uniform_i32(tid >> 7);  // the same for the 64 lanes of a wave
   const int32_t g8 = (tid & 127) * 8;
+  if constexpr (DEF) {
+    if (g8 < width) {
+      const int64_t cg = c0 + g8;
+      sel8 = static_cast<uint32_t>(d.mask[cg >> 6] >> (cg & 63)) & 0xFFu;
+    }
+  }
   const uint32_t vQ = static_cast<uint32_t>(Q * 16);  // quad byte offset (fp32 slots)
   double zq[4] = {0.0, 0.0, 0.0, 0.0};  // STATS: sums of squares per element
 
@@ -253,6 +300,66 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
       }
     }
 
+    if constexpr (DEF) {
+      // the hand-over of the lane's 8 columns in rows 2p + h of the batch
+      const int32_t cols = width - g8;
+      const uint32_t vo = static_cast<uint32_t>((c0 + g8) * 2);
+      float a[kRvBatch / 2][8];
+      for (int32_t s0 = 0; s0 < hist.n; s0 += kDefBatch) {
+        u32x4 ev[kDefBatch][kRvBatch / 2];
+#pragma unroll
+        for (int e = 0; e < kDefBatch; ++e) {
+          const int32_t st = s0 + e;
+          if (st < hist.n) {
+            const DevMat& hd = hist.mats[st][q];
+            const rsrc_t rE = rows_rsrc(hd.grad, i0, i1, hd.ld_grad, d.m);
+            const uint32_t sE = static_cast<uint32_t>(hd.ld_grad * 2);
+#pragma unroll
+            for (int p = 0; p < kRvBatch / 2; ++p) {
+              const int b = 2 * p + h;
+              ev[e][p] = u32x4{0u, 0u, 0u, 0u};
+              if (b < nb && cols > 0)
+                ev[e][p] = load_group<kStream>(rE, vo, static_cast<uint32_t>(i + b) * sE, cols);
+            }
+          }
+        }
+#pragma unroll
+        for (int e = 0; e < kDefBatch; ++e) {
+          const int32_t st = s0 + e;
+          if (st < hist.n) {
+#pragma unroll
+            for (int p = 0; p < kRvBatch / 2; ++p) {
+              float g[8];
+              widen_group(ev[e][p], g);
+#pragma unroll
+              for (int x = 0; x < 8; ++x) a[p][x] = st == 0 ? g[x] : a[p][x] + g[x];
+            }
+          }
+        }
+      }
+#pragma unroll
+      for (int p = 0; p < kRvBatch / 2; ++p) {
+        const int b = 2 * p + h;
+        if (b < nb && cols > 0) {
+          float g[8];
+          widen_group(gv[p], g);
+#pragma unroll
+          for (int x = 0; x < 8; ++x) {
+            const float sum = hist.n > 0 ? a[p][x] + g[x] : g[x];
+            a[p][x] = ((sel8 >> x) & 1u) ? 0.0f : sum * scale;
+          }
+          const uint32_t so = static_cast<uint32_t>(i + b) * sD;
+          const uint32_t vd = static_cast<uint32_t>((c0 + g8) * 4);
+          if (cols >= 8) {
+            buf_put_b128(as_u4(a[p][0], a[p][1], a[p][2], a[p][3]), rD, vd, so);
+            buf_put_b128(as_u4(a[p][4], a[p][5], a[p][6], a[p][7]), rD, vd + 16, so);
+          } else {
+            for (int x = 0; x < cols; ++x) buf_put_f32(a[p][x], rD, vd + 4 * x, so);
+          }
+        }
+      }
+    }
+
     // 2. Slot data of the batch: A (pack roles, after the first step of an
     //    interval) or the Adam states.
     float x0[kRvBatch][4], x1[kRvBatch][4], x2[kRvBatch][4];
@@ -294,6 +401,8 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
         }
       }
     }
+
+    if constexpr (!ADAM && !PACK) continue;  // the hand-over alone
 
     // 3. Stage G in LDS.
 #pragma unroll
@@ -399,12 +508,15 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
 template <bool ADAM, bool PACK, bool HAND, bool STATS, bool A16>
 void launch_rv_a(const Table& t, const DevMat& one, dim3 grid, const AdamK& c, int32_t first,
                  float scale, hipStream_t s, double* zs) {
+  const HistTable none{};
   if (t.mats != nullptr)
-    hipLaunchKernelGGL((rv_update_kernel<true, ADAM, PACK, HAND, STATS, A16>), grid,
-                       dim3(kThreads), 0, s, t.mats, t.off, t.nmats, one, c, first, scale, zs);
+    hipLaunchKernelGGL((rv_update_kernel<true, ADAM, PACK, HAND, STATS, A16, false>), grid,
+                       dim3(kThreads), 0, s, t.mats, t.off, t.nmats, one, c, first, scale, zs,
+                       none);
   else
-    hipLaunchKernelGGL((rv_update_kernel<false, ADAM, PACK, HAND, STATS, A16>), grid,
-                       dim3(kThreads), 0, s, t.mats, t.off, t.nmats, one, c, first, scale, zs);
+    hipLaunchKernelGGL((rv_update_kernel<false, ADAM, PACK, HAND, STATS, A16, false>), grid,
+                       dim3(kThreads), 0, s, t.mats, t.off, t.nmats, one, c, first, scale, zs,
+                       none);
 }
 
 // The stage's code (and its registers and LDS) only in the launches of the
@@ -439,6 +551,19 @@ hipError_t launch_rv_update(const Table& t, const DevMat& one, int64_t blocks, c
   else if (adam && pack) launch_rv_t<true, true, false>(t, one, grid, c, first, 1.0f, s);
   else if (adam) launch_rv_t<true, false, false>(t, one, grid, c, first, 1.0f, s);
   else if (pack) launch_rv_t<false, true, false>(t, one, grid, c, first, 1.0f, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_rv_handover_deferred(const Table& t, const DevMat& one, int64_t blocks,
+                                       const AdamK& c, float scale, const HistTable& h,
+                                       hipStream_t s) {
+  (void)hipGetLastError();
+  if (blocks <= 0 || t.mats == nullptr) return hipSuccess;
+  launch_rv_a<true, false, false, false, false>(t, one, dim3(static_cast<uint32_t>(blocks)), c, 0,
+                                                1.0f, s, nullptr);
+  hipLaunchKernelGGL((rv_update_kernel<true, false, false, false, false, false, true>),
+                     dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0, s, t.mats, t.off,
+                     t.nmats, one, c, 0, scale, nullptr, h);
   return hipGetLastError();
 }
 

@@ -12,7 +12,7 @@ issues one batched launch per kernel per step:
                    the packed buffer is only read), or zf_plan_update then
                    zf_plan_unpack when fuse_handover is False
 
-Deferred packing (deferred_pack=True; channel-major, fixed schedule, fused
+Deferred packing (deferred_pack=True; either layout, fixed schedule, fused
 hand-over): no packed buffer.  The unselected part of each step's gradient
 stays in its gradient slot, every step but an interval's last runs the
 Adam part alone, and the last step sums the interval's gradients (in step
@@ -183,15 +183,15 @@ class SelectiveUpdateRunner:
         # of the packed buffer are the next update passes).  A refresh step
         # that starts an interval then fills it from the score pass.
         # (row-major: the fixed schedule with the fused hand-over only)
-        # deferred packing (channel-major, fixed schedule, hand-over fused, no
-        # offload): the unselected part of every step's gradient stays in its
-        # slot until the interval ends; the interval's last step sums them
+        # deferred packing (fixed schedule, hand-over fused, no offload): the
+        # unselected part of every step's gradient stays in its slot until
+        # the interval ends; the interval's last step sums them
         self.deferred = bool(deferred_pack)
         if self.deferred:
-            if (layout == ROW_MAJOR or zen_tau is not None or self.offload
-                    or not self.keep_unpacked or not self.fuse_handover):
-                raise ValueError("deferred packing runs in the channel-major layout on the fixed "
-                                 "schedule with the fused hand-over, without offload")
+            if (zen_tau is not None or self.offload or not self.keep_unpacked
+                    or not self.fuse_handover):
+                raise ValueError("deferred packing runs on the fixed schedule with the fused "
+                                 "hand-over, without offload")
             if len(grad_slots) < min(self.S, self.R):
                 raise ValueError("deferred packing keeps every gradient of an interval: it needs "
                                  f"at least min(S, R) = {min(self.S, self.R)} gradient slots")

@@ -176,3 +176,78 @@ def test_no_write_outside_store_and_statistics(layout):
         assert g.intact()
     assert ssq.fully_written() and asq.fully_written()
     plan.close()
+
+
+@pytest.mark.parametrize("n,m", [(3, 7), (43, 77), (64, 130), (4104, 70), (16, 1000)])
+@pytest.mark.parametrize("padded", [True, False], ids=["earlier-16B", "earlier-ld-eq-width"])
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_no_write_outside_deferred_handover(n, m, padded, layout):
+    """zf_plan_update_handover_deferred (the interval's last step with
+    deferred packing; three earlier gradients) writes nothing outside the
+    compact states, W and the hand-over, fills the hand-over, leaves the
+    earlier gradients alone, and equals the oracle: Adam in place on the
+    selected columns, the hand-over of pack_accumulate over the four
+    gradients times fp32(1/4).  Earlier gradients with 16-byte rows keep
+    the row-major 16-byte kernel; unpadded ones (ld = width) take the
+    per-column passes."""
+    ratio = 0.1
+    k = zf.k_from_ratio(ratio, m)
+    rng = np.random.default_rng(n * 1000 + m)
+    sel_h = O.select_topk(rng.random(m).astype(np.float32), k)
+    sel = zf.Selection(m, k)
+    sel.sel_idx.copy_(torch.from_numpy(sel_h.sel.astype(np.int32)))
+    sel.unsel_idx.copy_(torch.from_numpy(sel_h.unsel.astype(np.int32)))
+    sel.mask.copy_(torch.from_numpy(sel_h.mask.view(np.int64)))
+    sel.prefix.copy_(torch.from_numpy(sel_h.prefix.astype(np.int32)))
+    bits = [grad_bits(n, m, derive_seed("canary-deferred", n, m, s)) for s in range(4)]
+    G = Guarded(*storage(layout, n, m), torch.bfloat16).fill(to_layout(bits[3], layout))
+    if padded:
+        E = [Guarded(*storage(layout, n, m), torch.bfloat16).fill(to_layout(b, layout))
+             for b in bits[:3]]
+        earlier_t = [e.t for e in E]
+    else:
+        E = []
+        earlier_t = [torch.from_numpy(to_layout(b, layout).view(np.int16)).view(torch.bfloat16)
+                     .cuda() for b in bits[:3]]
+    before = [e.clone() for e in earlier_t]
+    P0, M0 = (rng.standard_normal((n, k)).astype(np.float32) * 0.02 for _ in range(2))
+    V0 = np.abs(rng.standard_normal((n, k)).astype(np.float32)) * 1e-4
+    W0 = O.bf16_round((rng.standard_normal((n, m)) * 0.02).astype(np.float32))
+    P, M, V = (Guarded(*storage(layout, n, k), torch.float32).fill(to_layout(x, layout))
+               for x in (P0, M0, V0))
+    W = Guarded(*storage(layout, n, m), torch.bfloat16).fill(to_layout(W0, layout))
+    D = Guarded(*storage(layout, n, m), torch.float32)
+
+    def buffers(grad):
+        return zf.MatrixBuffers(grad=grad, k=k, sel=sel, weight=W.t, master=P.t, exp_avg=M.t,
+                                exp_avg_sq=V.t, unpacked=D.t, layout=layout)
+    plan = zf.Plan([buffers(G.t)])
+    earlier = [zf.Plan([buffers(e)]) for e in earlier_t]
+    step = 7
+    plan.update_handover_deferred(HP, step, earlier, 0.25)
+    torch.cuda.synchronize()
+    for g in [P, M, V, W, D, G] + E:
+        assert g.intact()
+    assert D.fully_written()
+    for a, b in zip(before, earlier_t):
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    # against the oracle
+    c = O.AdamConsts.at_step(HP.lr, HP.beta1, HP.beta2, HP.eps, HP.weight_decay, step)
+    Pw, Mw, Vw, wsel = O.adam_selected(bits[3], sel_h.sel, P0, M0, V0, c)
+    Ww = W0.copy()
+    Ww[:, sel_h.sel.astype(np.int64)] = wsel
+    A = None
+    for s in range(4):
+        A = O.pack_accumulate(bits[s], sel_h.unsel, A, s + 1)
+    Dw = O.unpack(A, sel_h, float(np.float32(0.25)))
+
+    def logical(t):
+        x = t.t() if layout == zf.CHANNEL_MAJOR else t
+        return x.contiguous().cpu()
+    for got, want in ((P, Pw), (M, Mw), (V, Vw), (D, Dw)):
+        assert np.array_equal(logical(got.t).view(torch.int32).numpy(),
+                              np.ascontiguousarray(want, np.float32).view(np.int32))
+    assert np.array_equal(logical(W.t).view(torch.int16).numpy().view(np.uint16), Ww)
+    for e in earlier:
+        e.close()
+    plan.close()

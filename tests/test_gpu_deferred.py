@@ -1,7 +1,11 @@
-"""Deferred packing (channel-major): the unselected part of each step's
-gradient stays in its gradient slot and the interval's last step sums the
-interval's gradients, in step order, into the hand-over
-(zf_plan_update_handover_deferred); the other steps run Adam alone.
+"""Deferred packing: the unselected part of each step's gradient stays in
+its gradient slot and the interval's last step sums the interval's
+gradients, in step order, into the hand-over
+(zf_plan_update_handover_deferred); the other steps run Adam alone.  Three
+storage variants: channel-major; row-major with 16-byte gradient rows (the
+16-byte update kernel with the sum fused in, ragged tile ends included);
+row-major with unpadded rows whose widths are not multiples of 8 (the
+per-column Adam pass and the per-column hand-over pass).
 
 * the runner in this mode against the oracle (MatrixOracle), every step:
   compact states and W bit for bit, selections bit-exact, the hand-over bit
@@ -27,12 +31,27 @@ pytestmark = pytest.mark.gpu
 
 zf = pytest.importorskip("paper_2505_12242_amd")
 CM = zf.CHANNEL_MAJOR
+RM = zf.ROW_MAJOR
 HP = zf.AdamHparams(lr=1e-3)
-# n % 8 != 0 (43 x 77, 16 x 3 has 16 rows but 3 channels) takes the element path
+# channel-major: n % 8 != 0 (43 x 77, 16 x 3 has 16 rows but 3 channels)
+# takes the element path; row-major: every width but none a multiple of 8
 SHAPES = [(264, 300), (4104, 70), (43, 77), (40, 1500), (16, 3)]
+# storage variant -> layout
+VARIANTS = {"cm": CM, "rm-vec": RM, "rm-col": RM}
 
 
-def inputs(shapes, nslots, seed, ratio=0.1):
+def store(G, variant):
+    """A logical [n, m] tensor in the variant's storage: channel-major
+    transposed; rm-vec with rows padded to 16 bytes; rm-col contiguous."""
+    if variant == "cm":
+        return G.t().contiguous()
+    if variant == "rm-vec":
+        n, m = G.shape
+        return zf.alloc_stored(RM, n, m, G.dtype, G.device).copy_(G)
+    return G.contiguous()
+
+
+def inputs(shapes, nslots, seed, ratio=0.1, variant="cm"):
     dev = torch.device("cuda")
     slots, host = [], []
     for s in range(nslots):
@@ -43,36 +62,42 @@ def inputs(shapes, nslots, seed, ratio=0.1):
             sc = space_boundary(sc * (1.0 + 0.01 * s), O.k_from_ratio(ratio, m))
             G = gradient(n, m, sc, derive_seed(seed, q, "g", s), device=dev)
             hb.append(bits_np(G))
-            buf.append(G.t().contiguous())
+            buf.append(store(G, variant))
         slots.append(buf)
         host.append(hb)
     weights, w0 = [], []
     for q, (n, m) in enumerate(shapes):
         w = master_weights(n, m, derive_seed(seed, q, "w"), device=dev).to(torch.bfloat16)
         w0.append(bits_np(w))
-        weights.append(w.t().contiguous())
+        weights.append(w.t().contiguous() if variant == "cm" else w.contiguous())
     return slots, host, weights, w0
 
 
-def logical(t):
-    return t.t().contiguous()
+def logical_of(variant):
+    if variant == "cm":
+        return lambda t: t.t().contiguous()
+    return lambda t: t.contiguous()
 
 
 SCHEDULES = [(4, 4, 0), (6, 4, 0), (1, 4, 0), (8, 3, 0), (2, 1, 0), (16, 6, 0), (4, 4, 2)]
 
 
 @pytest.mark.timeout(600)
+@pytest.mark.parametrize("variant", list(VARIANTS))
 @pytest.mark.parametrize("R,S,warmup", SCHEDULES, ids=[f"R{r}S{s}w{w}" for r, s, w in SCHEDULES])
-def test_deferred_runner_equals_oracle_and_eager(R, S, warmup):
+def test_deferred_runner_equals_oracle_and_eager(R, S, warmup, variant):
     T = 14
     nslots = max(3, min(S, R))
-    slots, host, weights, w0 = inputs(SHAPES, nslots, derive_seed("deferred", R, S))
+    slots, host, weights, w0 = inputs(SHAPES, nslots, derive_seed("deferred", R, S),
+                                      variant=variant)
+    logical = logical_of(variant)
     dev = torch.device("cuda")
     runs = {}
     for mode in ("deferred", "eager"):
         ws = [w.clone() for w in weights]
-        runner = zf.SelectiveUpdateRunner(SHAPES, 0.1, HP, R, S, slots, ws, device=dev, layout=CM,
-                                          warmup=warmup, deferred_pack=(mode == "deferred"))
+        runner = zf.SelectiveUpdateRunner(SHAPES, 0.1, HP, R, S, slots, ws, device=dev,
+                                          layout=VARIANTS[variant], warmup=warmup,
+                                          deferred_pack=(mode == "deferred"))
         assert runner.deferred == (mode == "deferred")
         orcs = [O.MatrixOracle(O.widen(w0[q]), w0[q], 0.1, HP.lr, HP.beta1, HP.beta2, HP.eps,
                                HP.weight_decay, R, S, warmup) for q in range(len(SHAPES))]
@@ -80,7 +105,8 @@ def test_deferred_runner_equals_oracle_and_eager(R, S, warmup):
         for t in range(1, T + 1):
             kind = runner.step()
             torch.cuda.synchronize()
-            print(f"# deferred R={R} S={S} {mode} step {t} {kind}", file=sys.stderr, flush=True)
+            print(f"# deferred {variant} R={R} S={S} {mode} step {t} {kind}", file=sys.stderr,
+                  flush=True)
             slot = (t - 1) % nslots
             for q in range(len(SHAPES)):
                 ref = orcs[q].step(host[slot][q])
@@ -113,25 +139,27 @@ def test_deferred_needs_the_interval_in_the_ring():
     with pytest.raises(ValueError, match="gradient slots"):
         zf.SelectiveUpdateRunner(SHAPES[:2], 0.1, HP, 4, 4, slots, weights, layout=CM,
                                  deferred_pack=True)
-    with pytest.raises(ValueError, match="channel-major"):
-        zf.SelectiveUpdateRunner(SHAPES[:2], 0.1, HP, 4, 4, slots, weights,
-                                 layout=zf.ROW_MAJOR, deferred_pack=True)
+    with pytest.raises(ValueError, match="fixed schedule"):
+        zf.SelectiveUpdateRunner(SHAPES[:2], 0.1, HP, 4, 4, slots, weights, layout=CM,
+                                 zen_tau=1.0, deferred_pack=True)
 
 
-def test_deferred_entry_point_checks():
+@pytest.mark.parametrize("variant", list(VARIANTS))
+def test_deferred_entry_point_checks(variant):
     """Host-side checks of zf_plan_update_handover_deferred: the earlier
-    plans must cover the same matrices (count, shapes, k, access path), at
-    most 15 of them; nothing is enqueued otherwise."""
+    plans must cover the same matrices (count, shapes, k; channel-major:
+    access path), at most 15 of them; nothing is enqueued otherwise."""
     dev = torch.device("cuda")
-    slots, _, weights, _ = inputs(SHAPES[:2], 4, 6)
+    lay = VARIANTS[variant]
+    slots, _, weights, _ = inputs(SHAPES[:2], 4, 6, variant=variant)
     runner = zf.SelectiveUpdateRunner(SHAPES[:2], 0.1, HP, 4, 4, slots, weights, device=dev,
-                                      layout=CM, deferred_pack=True)
+                                      layout=lay, deferred_pack=True)
     runner.step()
     plan = runner.plans[1][runner.cur][0]
     earlier = [runner.plans[0][runner.cur][0]]
     before = [x.clone() for x in runner.unpacked]
     other = zf.SelectiveUpdateRunner(SHAPES[:1], 0.1, HP, 4, 4, [s[:1] for s in slots],
-                                     [w.clone() for w in weights[:1]], device=dev, layout=CM,
+                                     [w.clone() for w in weights[:1]], device=dev, layout=lay,
                                      deferred_pack=True)
     for bad in ([other.plans[0][0][0]],            # another matrix count
                 earlier * 16):                      # more than 15 earlier steps

@@ -5,10 +5,10 @@ accumulation, hand-over at step 4, refresh with state remap at step 5,
 hand-over at step 8 -- in both layouts (channel-major, bench.py's default,
 and row-major with the 16-byte update), and one R = S = 8 interval of the
 70B share (heavy-tailed scales, GQA k/v weights, 28672-channel down
-projections) in the channel-major layout.  Channel-major runs take both
-packing modes: every step (packed sums updated by each step) and deferred
-(bench.py's default: the interval's gradients stay in a ring of min(S, R)
-slots and its last step sums them).
+projections) in the channel-major layout.  Both packing modes run: every
+step (packed sums updated by each step) and deferred (bench.py's default:
+the interval's gradients stay in a ring of min(S, R) slots and its last
+step sums them), the 7B set in both layouts.
 
 * Sampled matrices (embedding, LM head and four decoder weights of three
   shapes) are run through the oracle step by step and every output is
@@ -46,7 +46,8 @@ CASES = {
 
 
 RUNS = [("llama2-7b-full", "cm"), ("llama2-7b-full", "cm-deferred"), ("llama2-7b-full", "rm"),
-        ("llama2-70b-10layers", "cm"), ("llama2-70b-10layers", "cm-deferred")]
+        ("llama2-7b-full", "rm-deferred"), ("llama2-70b-10layers", "cm"),
+        ("llama2-70b-10layers", "cm-deferred")]
 # the row-major run compares the three decoder shapes in full (the 32000-row
 # embedding and head, the slowest oracle work, are compared in the
 # channel-major run; every matrix gets the property checks in both)
@@ -63,16 +64,16 @@ def logical_cm(t):
 def test_full_set_sampled_parity(name, lay):
     from workloads import get_workload
     SAMPLES, STEPS, NSLOTS, LIGHT = CASES[name]
-    if lay == "rm":
+    if lay.startswith("rm"):
         SAMPLES = RM_SAMPLES
-    deferred = lay == "cm-deferred"  # bench.py's default packing: the interval in the ring
+    deferred = lay.endswith("-deferred")  # bench.py's default packing: the interval in the ring
     wl = get_workload(name)
     if deferred:
         NSLOTS = min(wl.accum, wl.refresh)
     hp = zf.AdamHparams(wl.hyper.lr, wl.hyper.beta1, wl.hyper.beta2, wl.hyper.eps,
                         wl.hyper.weight_decay)
     dev = torch.device("cuda")
-    layout = zf.ROW_MAJOR if lay == "rm" else zf.CHANNEL_MAJOR
+    layout = zf.ROW_MAJOR if lay.startswith("rm") else zf.CHANNEL_MAJOR
     assert not LIGHT or layout == zf.CHANNEL_MAJOR  # the light checks index channel rows
 
     def logical(t):
