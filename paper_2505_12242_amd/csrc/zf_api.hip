@@ -942,7 +942,8 @@ zf_status check_plan_matrix(const zf_matrix& x, zf_plan& p) {
   // everything the update reads or writes.
   if (x.acc_first != nullptr) {
     if (!mat_ok(x.acc_first, eg, x.ld_acc_first, 2)) return ZF_EINVAL;
-    if (L == zf::kRowMajor && (!aligned(x.acc_first, 16) || x.ld_acc_first % 8 != 0))
+    // (16-byte rows; a single row never uses its stride)
+    if (L == zf::kRowMajor && (!aligned(x.acc_first, 16) || (n > 1 && x.ld_acc_first % 8 != 0)))
       return ZF_EINVAL;
     const Span st = span(x.acc_first, eg, x.ld_acc_first, 2);
     const Ext es = ext(L, n, k);

@@ -100,8 +100,8 @@ __device__ __forceinline__ u32x4 load_group(rsrc_t r, uint32_t vo, uint32_t so, 
   return u32x4{w[0], w[1], w[2], w[3]};
 }
 
-// earlier steps whose rows are loaded before they are added (more costs
-// the pass its occupancy)
+// earlier steps whose rows are loaded before they are added (2, 3 and 4
+// measured alike)
 constexpr int kDefBatch = 2;
 
 __device__ __forceinline__ float4 as_f4(u32x4 v) {
@@ -249,7 +249,8 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
 
   for (int32_t i = 0; i < rows; i += kRvBatch) {
     const int32_t nb = min(kRvBatch, rows - i);
-    if (i > 0) __syncthreads();  // the previous batch is done with the LDS rows
+    // the previous batch is done with the LDS rows (the hand-over pass uses none)
+    if (i > 0 && (ADAM || PACK)) __syncthreads();
 
     // 1. G rows of the batch (16-byte loads of 8 columns; ragged tail of
     //    the last tile element by element).

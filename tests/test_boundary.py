@@ -255,6 +255,25 @@ def test_plan_validation():
     LIB.zf_plan_destroy(None)
 
 
+def test_rowmajor_stage_stride_rule():
+    """The row-major bf16 first-step stage needs 16-byte rows: a stride that
+    is a multiple of 8 elements and a 16-byte aligned base.  A single row
+    never uses its stride (the binding passes its width), so a one-row
+    matrix of any width is accepted."""
+    nb = ctypes.c_size_t()
+
+    def query(n, m, ld_stage, stage=0x200000):
+        arr = (_lib.ZfMatrix * 1)()
+        x = arr[0]
+        x.n, x.m, x.k, x.layout = n, m, 1, RM
+        x.grad, x.ld_grad = 0x100000, 16
+        x.acc_first, x.ld_acc_first = stage, ld_stage
+        return LIB.zf_plan_query(arr, 1, ctypes.byref(nb))
+    assert query(1, 9, 9) == 0 and query(1, 1, 1) == 0
+    assert query(2, 9, 9) == EINVAL and query(2, 9, 16) == 0
+    assert query(1, 9, 9, stage=0x200008) == EINVAL   # base alignment
+
+
 def test_offload_and_handover_entry_points_validate_on_the_host():
     hp = _lib.ZfAdamHparams(1e-5, 0.9, 0.999, 1e-8, 0.0)
     s = _lib.ZfSelection()

@@ -15,6 +15,8 @@ per-column Adam pass and the per-column hand-over pass).
   the vector and the element path;
 * the same runs equal the eager runner (the packed buffer accumulated every
   step, bf16 first-step stage) bit for bit;
+* degenerate selections (k = 0, k = m) on one-element, one-row and
+  one-column matrices;
 * the entry point's host-side checks.
 """
 import sys
@@ -130,6 +132,63 @@ def test_deferred_runner_equals_oracle_and_eager(R, S, warmup, variant):
         runner.close()
         runs[mode] = out
     assert len(runs["deferred"]) == len(runs["eager"])
+    for a, b in zip(runs["deferred"], runs["eager"]):
+        assert same_bits(a, b)
+
+
+# one element, one row, one column, a whole mask word, a square of 8, and
+# 3 channels of 16 rows (channel-major element path)
+EDGE_SHAPES = [(1, 1), (1, 9), (5, 1), (9, 64), (8, 8), (16, 3)]
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("variant", list(VARIANTS))
+@pytest.mark.parametrize("ratio", [0.0, 1.0, 0.5])
+def test_deferred_degenerate_selections(ratio, variant):
+    """k = 0 (the hand-over is the whole interval's sum, no Adam), k = m
+    (the hand-over is all +0.0 and no gradient is summed) and k = m / 2, on
+    one-element, one-row and one-column matrices, over R = 6, S = 4 (an
+    interval cut short by a refresh): the deferred runner equals the oracle
+    and the eager runner bit for bit at every step."""
+    R, S, T = 6, 4, 9
+    nslots = 4
+    slots, host, weights, w0 = inputs(EDGE_SHAPES, nslots, derive_seed("deferred-edge", ratio),
+                                      ratio=ratio, variant=variant)
+    logical = logical_of(variant)
+    dev = torch.device("cuda")
+    runs = {}
+    for mode in ("deferred", "eager"):
+        ws = [w.clone() for w in weights]
+        runner = zf.SelectiveUpdateRunner(EDGE_SHAPES, ratio, HP, R, S, slots, ws, device=dev,
+                                          layout=VARIANTS[variant],
+                                          deferred_pack=(mode == "deferred"))
+        orcs = [O.MatrixOracle(O.widen(w0[q]), w0[q], ratio, HP.lr, HP.beta1, HP.beta2, HP.eps,
+                               HP.weight_decay, R, S) for q in range(len(EDGE_SHAPES))]
+        out = []
+        for t in range(1, T + 1):
+            kind = runner.step()
+            torch.cuda.synchronize()
+            print(f"# deferred edges {variant} ratio={ratio} {mode} step {t} {kind}",
+                  file=sys.stderr, flush=True)
+            slot = (t - 1) % nslots
+            for q in range(len(EDGE_SHAPES)):
+                ref = orcs[q].step(host[slot][q])
+                sel = runner.selection[q]
+                assert np.array_equal(sel.sel_idx.cpu().numpy(), orcs[q].sel.sel), (q, t)
+                P, M, V = (f32_np(logical(x)) for x in runner.state[q])
+                assert same_bits(P, orcs[q].P) and same_bits(M, orcs[q].M) and \
+                    same_bits(V, orcs[q].V), (mode, q, t)
+                W = bits_np(logical(ws[q]))
+                assert np.array_equal(W, orcs[q].W), (mode, q, t)
+                out.extend([W, P, M, V])
+                if kind.interval_end:
+                    D = f32_np(logical(runner.unpacked[q]))
+                    assert same_bits(D, ref["unpacked"]), (mode, q, t)
+                    if ratio == 1.0:
+                        assert not np.any(D.view(np.uint32)), (mode, q, t)  # all +0.0
+                    out.append(D)
+        runner.close()
+        runs[mode] = out
     for a, b in zip(runs["deferred"], runs["eager"]):
         assert same_bits(a, b)
 
