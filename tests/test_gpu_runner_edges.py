@@ -1,0 +1,156 @@
+"""Degenerate shapes through every mode of the runner, against the oracle.
+
+The matrices:
+* one element (1 x 1);
+* one row (1 x 9, 1 x 64);
+* one column (5 x 1);
+* a whole 64-channel mask word (9 x 64);
+* a square of 8 (8 x 8);
+* 3 channels of 16 rows (16 x 3).
+
+The selections: nothing selected (ratio 0, the hand-over is the whole
+interval's sum), everything selected (ratio 1, the hand-over is +0.0) and
+half.
+
+The storage variants:
+* channel-major;
+* row-major with 16-byte gradient rows (the 16-byte kernels);
+* row-major with unpadded rows (the per-column kernels).
+
+The modes:
+* packing every step: with the bf16 first-step stage, without it, and with
+  the separate hand-over pass;
+* deferred packing;
+* Zen-auto, decided on the device (channel-major) and on the host;
+* the offloaded optimizer, synchronous and overlapped.
+
+Schedule: R = 6, S = 4 (an interval cut short by a refresh).  Every step is
+compared with MatrixOracle, ZenAutoOracle or OffloadOracle: selections,
+compact states, W, the hand-over and the store, bit for bit.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from tests._gpu import bits_np, f32_np, same_bits
+from workloads import derive_seed, gradient, space_boundary
+
+pytestmark = pytest.mark.gpu
+
+zf = pytest.importorskip("paper_2505_12242_amd")
+CM, RM = zf.CHANNEL_MAJOR, zf.ROW_MAJOR
+HP = zf.AdamHparams(lr=1e-3, weight_decay=0.01)
+EDGE_SHAPES = [(1, 1), (1, 9), (5, 1), (9, 64), (8, 8), (16, 3), (1, 64)]
+VARIANTS = {"cm": CM, "rm-vec": RM, "rm-col": RM}
+MODES = {
+    "stage": {},
+    "no-stage": {"first_step_stage": False},
+    "separate-handover": {"fuse_handover": False},
+    "deferred": {"deferred_pack": True},
+    "zen-device": {"zen_tau": 1.0},
+    "zen-host": {"zen_tau": 1.0, "zen_on_device": False},
+    "offload-sync": {"offload": True, "overlap": False, "host_threads": 2},
+    "offload-overlap": {"offload": True, "overlap": True, "host_threads": 2},
+}
+R, S, T = 6, 4, 9
+
+
+def store_as(G, variant):
+    """A logical [n, m] tensor in the variant's storage."""
+    if variant == "cm":
+        return G.t().contiguous()
+    if variant == "rm-vec":
+        n, m = G.shape
+        return zf.alloc_stored(RM, n, m, G.dtype, G.device).copy_(G)
+    return G.contiguous()
+
+
+def logical(t, variant):
+    return (t.t() if variant == "cm" else t).contiguous()
+
+
+def make_inputs(ratio, variant, seed):
+    dev = torch.device("cuda")
+    slots, host = [], []
+    for t in range(1, T + 1):
+        ds, hs = [], []
+        for q, (n, m) in enumerate(EDGE_SHAPES):
+            g = torch.Generator().manual_seed(derive_seed(seed, q, "s") & 0x7fffffff)
+            base = torch.exp(1.5 * torch.randn(m, generator=g, dtype=torch.float64))
+            jit = torch.exp(0.3 * torch.randn(m, generator=torch.Generator().manual_seed(
+                derive_seed(seed, q, "j", t) & 0x7fffffff), dtype=torch.float64))
+            sc = space_boundary(base * jit, O.k_from_ratio(ratio, m))
+            G = gradient(n, m, sc, derive_seed(seed, q, "g", t), device=dev)
+            hs.append(bits_np(G))
+            ds.append(store_as(G, variant))
+        slots.append(ds)
+        host.append(hs)
+    weights, w0 = [], []
+    for q, (n, m) in enumerate(EDGE_SHAPES):
+        g = torch.Generator().manual_seed(derive_seed(seed, q, "w") & 0x7fffffff)
+        w = (0.02 * torch.randn(n, m, generator=g)).to(torch.bfloat16).to(dev)
+        w0.append(bits_np(w))
+        weights.append(w.t().contiguous() if variant == "cm" else w.contiguous())
+    return slots, host, weights, w0
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("ratio", [0.0, 0.5, 1.0])
+@pytest.mark.parametrize("variant", list(VARIANTS))
+@pytest.mark.parametrize("mode", list(MODES))
+def test_runner_modes_on_degenerate_shapes(mode, variant, ratio):
+    opts = MODES[mode]
+    zen = "zen_tau" in opts
+    offload = opts.get("offload", False)
+    slots, host, weights, w0 = make_inputs(ratio, variant, derive_seed("runner-edges", ratio))
+    dev = torch.device("cuda")
+    runner = zf.SelectiveUpdateRunner(EDGE_SHAPES, ratio, HP, R, S, slots, weights, device=dev,
+                                      layout=VARIANTS[variant], **opts)
+    hyper = (HP.lr, HP.beta1, HP.beta2, HP.eps, HP.weight_decay)
+    if offload:
+        orcs = [O.OffloadOracle(O.widen(w0[q]), w0[q], ratio, *hyper, R, S)
+                for q in range(len(EDGE_SHAPES))]
+    else:
+        orcs = [O.MatrixOracle(O.widen(w0[q]), w0[q], ratio, *hyper, R, S)
+                for q in range(len(EDGE_SHAPES))]
+    za = O.ZenAutoOracle(orcs, R, S, opts["zen_tau"]) if zen else None
+    try:
+        for t in range(1, T + 1):
+            kind = runner.step()
+            torch.cuda.synchronize()
+            print(f"# runner edges {mode} {variant} ratio={ratio} step {t}", file=sys.stderr,
+                  flush=True)
+            if zen:
+                ref = za.step(host[t - 1])
+                want = (ref["refresh"], ref["step_in_interval"], ref["interval_end"])
+                hand = ref.get("unpacked")
+            else:
+                outs = [o.step(host[t - 1][q]) for q, o in enumerate(orcs)]
+                k0 = outs[0]["kind"]
+                want = (k0.refresh, k0.step_in_interval, k0.interval_end)
+                hand = [o.get("unpacked") for o in outs]
+            assert (kind.refresh, kind.step_in_interval, kind.interval_end) == want, t
+            if offload:
+                runner.sync()
+            for q, o in enumerate(orcs):
+                assert np.array_equal(runner.selection[q].sel_idx.cpu().numpy(), o.sel.sel), \
+                    (q, t)
+                for got, ref_v in zip(runner.state[q], (o.P, o.M, o.V)):
+                    assert same_bits(f32_np(logical(got, variant)), ref_v), (q, t)
+                assert np.array_equal(bits_np(logical(runner.weights[q], variant)), o.W), (q, t)
+                if offload:
+                    for got, ref_v in zip(runner.store[q], o.store):
+                        assert same_bits(logical(got, variant).numpy(), ref_v), (q, t)
+                elif kind.interval_end:
+                    D = f32_np(logical(runner.unpacked[q], variant))
+                    assert same_bits(D, hand[q]), (q, t)
+                    if ratio == 1.0:
+                        assert not np.any(D.view(np.uint32)), (q, t)  # all +0.0
+        if offload:
+            assert runner.th == orcs[0].th
+    finally:
+        runner.close()
