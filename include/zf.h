@@ -546,7 +546,9 @@ zf_status zf_plan_update_handover(zf_plan* plan, const zf_adam_hparams* hp, int6
  * the hand-over pass reads every element of each step's gradient, since
  * the selected columns share their cache lines.  ZF_EINVAL (nothing
  * enqueued) on a mismatch or when an earlier gradient's row stride does
- * not fit the plan's row blocks. */
+ * not fit the plan's row blocks.  The kernels read the earlier plans'
+ * device tables when they run: those plans' device memory (and their
+ * gradients) must stay valid until this call's work on `stream` is done. */
 zf_status zf_plan_update_handover_deferred(zf_plan* plan, const zf_adam_hparams* hp, int64_t step,
                                            const zf_plan* const* earlier, int32_t n_earlier,
                                            float scale, zf_stream stream);

@@ -303,13 +303,56 @@ int main() {
     zf_plan_destroy(plan2);
     HIP_OK(hipFree(mem1));  // the stream was synchronised above
     HIP_OK(hipFree(mem2));
-    for (Mat* x : {&a, &b, &pa, &pb}) release(*x);
+    // deferred packing: no packed buffer; step 1 runs Adam alone, step 2
+    // sums both steps' gradients into the hand-over -- the same bits
+    Mat da = make(264, 300, 0.1, layout, 11), db = make(43, 77, 0.2, layout, 12);
+    Mat* dm[2] = {&da, &db};
+    for (int q = 0; q < 2; ++q) {
+      desc[q].grad = dm[q]->G1;
+      desc[q].weight = dm[q]->W;
+      desc[q].master = dm[q]->P;
+      desc[q].exp_avg = dm[q]->M;
+      desc[q].exp_avg_sq = dm[q]->V;
+      desc[q].acc = nullptr;
+      desc[q].ld_acc = 0;
+      desc[q].norms_sq = dm[q]->norms;
+      desc[q].sel = dm[q]->sel;
+      desc[q].unpacked = dm[q]->D;
+    }
+    size_t bytes3 = 0, bytes4 = 0;
+    ZF_OK_(zf_plan_query(desc, 2, &bytes3));
+    void* mem3 = nullptr;
+    HIP_OK(hipMalloc(&mem3, bytes3));
+    zf_plan* plan3 = nullptr;
+    ZF_OK_(zf_plan_create(desc, 2, mem3, bytes3, s, &plan3));
+    desc[0].grad = da.G2;
+    desc[1].grad = db.G2;
+    ZF_OK_(zf_plan_query(desc, 2, &bytes4));
+    void* mem4 = nullptr;
+    HIP_OK(hipMalloc(&mem4, bytes4));
+    zf_plan* plan4 = nullptr;
+    ZF_OK_(zf_plan_create(desc, 2, mem4, bytes4, s, &plan4));
+    ZF_OK_(zf_plan_colnorm(plan3, s));
+    ZF_OK_(zf_plan_topk_select(plan3, s));
+    ZF_OK_(zf_plan_update(plan3, &kHp, 1, ZF_STATES_INIT, 1, 2, 1, 0, s));
+    // packing every step needs the packed buffer these plans do not have
+    CHECK(zf_plan_update(plan3, &kHp, 1, ZF_STATES_INPLACE, 2, 2, 1, 1, s) == ZF_EINVAL);
+    const zf_plan* earlier[1] = {plan3};
+    ZF_OK_(zf_plan_update_handover_deferred(plan4, &kHp, 2, earlier, 1, 0.5f, s));
+    HIP_OK(hipStreamSynchronize(s));
+    CHECK(same_bits(down(da.D, da.n * da.m), Da) && same_bits(down(db.D, db.n * db.m), Db));
+    CHECK(same_bits(down(da.W, da.n * da.m), Wa) && same_bits(down(db.W, db.n * db.m), Wb));
+    zf_plan_destroy(plan3);
+    zf_plan_destroy(plan4);
+    HIP_OK(hipFree(mem3));
+    HIP_OK(hipFree(mem4));
+    for (Mat* x : {&a, &b, &pa, &pb, &da, &db}) release(*x);
   }
   HIP_OK(hipStreamDestroy(s));
   if (failures) {
     std::fprintf(stderr, "%d failures\n", failures);
     return 1;
   }
-  std::printf("abi smoke ok: both layouts, single calls and plans\n");
+  std::printf("abi smoke ok: both layouts, single calls, plans, deferred packing\n");
   return 0;
 }
