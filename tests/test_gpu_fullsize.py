@@ -200,3 +200,46 @@ def test_full_set_zen_auto_statistics():
     runner.close()
     del runner, slots, weights
     torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("lay", ["cm", "rm"])
+def test_full_set_deferred_equals_every_step_over_48_steps(lay):
+    """The whole 7B set for 48 steps of the R = S = 4 schedule (12
+    refreshes, 12 interval ends), once with deferred packing (bench.py's
+    default) and once packing every step: every matrix's W, compact states,
+    selection and final hand-over are equal bit for bit (torch.equal on the
+    device, all 226 matrices)."""
+    from workloads import get_workload
+    wl = get_workload("llama2-7b-full")
+    hp = zf.AdamHparams(wl.hyper.lr, wl.hyper.beta1, wl.hyper.beta2, wl.hyper.eps,
+                        wl.hyper.weight_decay)
+    dev = torch.device("cuda")
+    layout = zf.ROW_MAJOR if lay == "rm" else zf.CHANNEL_MAJOR
+    steps, nslots = 48, 4
+    kept = None
+    for deferred in (True, False):
+        torch.cuda.empty_cache()
+        shapes, ks, slots, weights = bench.build_set(wl, nslots, dev, layout)
+        runner = zf.SelectiveUpdateRunner(shapes, wl.ratio, hp, wl.refresh, wl.accum, slots,
+                                          weights, device=dev, layout=layout,
+                                          deferred_pack=deferred)
+        for t in range(1, steps + 1):
+            kind = runner.step()
+        torch.cuda.synchronize()
+        assert kind.interval_end
+        print(f"# {lay} deferred={deferred}: {steps} steps done", file=sys.stderr, flush=True)
+        out = [(weights[q], *runner.state[q], runner.unpacked[q],
+                runner.selection[q].sel_idx) for q in range(len(shapes))]
+        if kept is None:
+            kept = [tuple(x.clone() for x in o) for o in out]
+        else:
+            bits = {torch.float32: torch.int32, torch.bfloat16: torch.int16}
+            for q, (a, b) in enumerate(zip(kept, out)):
+                for x, y in zip(a, b):
+                    assert torch.equal(x.view(bits.get(x.dtype, x.dtype)),
+                                       y.view(bits.get(y.dtype, y.dtype))), q
+        runner.close()
+        del runner, slots, weights, out
+    del kept
+    torch.cuda.empty_cache()
