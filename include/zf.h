@@ -652,9 +652,9 @@ zf_status zf_plan_update_zen_pending(zf_plan* plan, const zf_adam_hparams* hp, i
                                      double tau, zf_zen_totals* totals, zf_stream stream);
 
 /* Zen-auto's interval driven on the device, so that a step needs no host
- * round trip (paper, Zero-stall Pipeline, "Hyperparameter Auto-tuning": the
- * deferred update is triggered as soon as the accumulated part becomes
- * comparable; the decision stays on the GPU).  The interval state lives in
+ * round trip (paper §3.2, "Hyperparameter Auto-tuning": the deferred update
+ * is triggered once the accumulated part becomes comparable; keeping that
+ * decision on the GPU is this library's choice).  The interval state lives in
  * DEVICE memory (8 bytes, 4-byte aligned), initialised by the caller to
  * {0, 1} (nothing accumulated; the first step starts an interval) and then
  * owned by the calls below, in stream order. */
@@ -672,8 +672,9 @@ typedef struct zf_zen_state {
  * state: length = that position; ended = trigger || position >=
  * accum_interval (S_max) || force_end.  force_end: the caller's own end of
  * the interval (the next step refreshes the selection, or a warm-up step).
- * Channel-major plans without a full-state store; the requirements of
- * zf_plan_update_zen otherwise.  Follow it with zf_plan_handover_zen. */
+ * Both layouts, plans without a full-state store; a row-major plan without
+ * the bf16 stage; the requirements of zf_plan_update_zen otherwise.  Follow
+ * it with zf_plan_handover_zen. */
 zf_status zf_plan_update_zen_device(zf_plan* plan, const zf_adam_hparams* hp, int64_t step,
                                     int32_t mode, int64_t accum_interval, int32_t force_end,
                                     double tau, zf_zen_totals* totals, zf_zen_state* state,
@@ -685,8 +686,9 @@ zf_status zf_plan_update_zen_device(zf_plan* plan, const zf_adam_hparams* hp, in
  * a one-step interval on a plan with one; +0.0 in the selected channels'
  * rows), bit for bit as zf_plan_unpack / zf_plan_unpack_first with that
  * scale; else nothing is written.  A fixed grid that loops over the work:
- * a step that does not end its interval costs one short launch.  Plans
- * whose descriptors all have the stage or none has it. */
+ * a step that does not end its interval costs one short launch.  Both
+ * layouts; channel-major plans whose descriptors all have the stage or none
+ * has it, row-major plans without it. */
 zf_status zf_plan_handover_zen(zf_plan* plan, const zf_zen_state* state, zf_stream stream);
 
 #ifdef __cplusplus

@@ -1409,15 +1409,15 @@ zf_status plan_update_zen(zf_plan* p, const AdamK& c, int32_t mode, int32_t firs
     // 16-byte update with the statistics fused: only the finalize remains
     const Table tv{p->d_mats, p->d_off_upv, p->nmats};
     e = zf::launch_rv_update(tv, p->mats[0], p->blk_upv, c, mode, first, true, true, false, 1.0f,
-                             s, p->d_ws);
+                             s, p->d_ws, zst);
     if (e != hipSuccess) return hip_fail(e);
     const Table tp{p->d_mats, p->d_off_zp, p->nmats};
     e = zf::launch_rm_zen(tp, 0, tz, p->blk_zen, p->mats[0], p->d_ws, p->d_zb, s);
   } else {
-    e = pd != nullptr
-            ? zf::launch_update(t, p->mats[0], p->blk_up, c, mode, first, true, true, false, 1.0f,
-                                s, pd)
-            : plan_update_launch(p, c, mode, first, true, true, false, 1.0f, s);
+    // the per-column update (with zst the kernel derives the phase: 1 on a
+    // refresh or after an ended interval, else the interval's length + 1)
+    e = zf::launch_update(t, p->mats[0], p->blk_up, c, mode, first, true, true, false, 1.0f, s,
+                          pd, zst);
     if (e != hipSuccess) return hip_fail(e);
     const Table tp{p->d_mats, p->d_off_zp, p->nmats};
     e = zf::launch_rm_zen(tp, p->blk_zp, tz, p->blk_zen, p->mats[0], p->d_ws, p->d_zb, s);
@@ -1460,8 +1460,10 @@ zf_status zf_plan_update_zen_device(zf_plan* p, const zf_adam_hparams* hp, int64
                                     double tau, zf_zen_totals* totals, zf_zen_state* state,
                                     zf_stream stream) {
   static_assert(sizeof(zf_zen_state) == sizeof(zf::ZenState), "zen state layout");
-  if (!zen_args_ok(p, hp, step, tau, totals) || p->layout != zf::kChannelMajor || p->has_store)
-    return ZF_EINVAL;
+  if (!zen_args_ok(p, hp, step, tau, totals) || p->has_store) return ZF_EINVAL;
+  // (row-major: the phase comes from the state, so the bf16 stage, which
+  // the row-major kernels select on the host, is not supported)
+  if (p->layout == zf::kRowMajor && p->has_acc1) return ZF_EINVAL;
   if (mode != zf::kInplace && mode != zf::kRemap && mode != zf::kInit) return ZF_EINVAL;
   if (mode == zf::kRemap && !p->can_remap) return ZF_EINVAL;
   if (accum_interval < 1 || accum_interval > INT32_MAX || state == nullptr ||
@@ -1473,14 +1475,16 @@ zf_status zf_plan_update_zen_device(zf_plan* p, const zf_adam_hparams* hp, int64
 }
 
 zf_status zf_plan_handover_zen(zf_plan* p, const zf_zen_state* state, zf_stream stream) {
-  if (p == nullptr || !p->can_unpack || p->layout != zf::kChannelMajor || state == nullptr ||
-      !aligned(state, 4) || (p->has_acc1 && !p->all_acc1))
+  if (p == nullptr || !p->can_unpack || state == nullptr || !aligned(state, 4) ||
+      (p->has_acc1 && (!p->all_acc1 || p->layout == zf::kRowMajor)))
     return ZF_EINVAL;
   const Table t{p->d_mats, p->d_off_unp, p->nmats};
+  const auto* zst = reinterpret_cast<const zf::ZenState*>(state);
   const hipError_t e =
-      zf::launch_cm_unpack_zen(t, p->mats[0], p->blk_unp,
-                               reinterpret_cast<const zf::ZenState*>(state), p->all_acc1,
-                               as_stream(stream));
+      p->layout == zf::kChannelMajor
+          ? zf::launch_cm_unpack_zen(t, p->mats[0], p->blk_unp, zst, p->all_acc1,
+                                     as_stream(stream))
+          : zf::launch_unpack_zen(t, p->blk_unp, zst, as_stream(stream));
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 

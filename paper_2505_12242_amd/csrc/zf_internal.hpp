@@ -163,11 +163,17 @@ hipError_t launch_colnorm(const Table& t, const DevMat& one, int64_t blocks,
 hipError_t launch_topk(const Table& t, const DevMat& one, int64_t blocks, hipStream_t s);
 // pend != nullptr: fused Adam + pack in kRemap against the store, with the
 // owed deferred update applied to the entering columns first.
+// zst (Zen-auto with the interval driven on the device; packing passes
+// only): an in-place step takes its phase from the interval state
 hipError_t launch_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
                          int32_t mode, int32_t first, bool adam, bool pack, bool handover,
-                         float scale, hipStream_t s, const Pending* pend = nullptr);
+                         float scale, hipStream_t s, const Pending* pend = nullptr,
+                         const ZenState* zst = nullptr);
 hipError_t launch_unpack(const Table& t, const DevMat& one, int64_t blocks, float scale,
                          hipStream_t s);
+// The hand-over of an interval Zen-auto ended on the device (row-major):
+// nothing unless zst->ended; `units` = the table's unpack blocks.
+hipError_t launch_unpack_zen(const Table& t, int64_t units, const ZenState* zst, hipStream_t s);
 
 // Row-major update with 16-byte accesses (zf_kernels_rv.hip); same contract
 // as launch_update, geometry rv_w / rv_cb / rv_rows.  zs != nullptr (fused
@@ -175,7 +181,8 @@ hipError_t launch_unpack(const Table& t, const DevMat& one, int64_t blocks, floa
 // row-major statistics pass, into zs at each matrix's cn_ws.
 hipError_t launch_rv_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
                             int32_t mode, int32_t first, bool adam, bool pack, bool handover,
-                            float scale, hipStream_t s, double* zs = nullptr);
+                            float scale, hipStream_t s, double* zs = nullptr,
+                            const ZenState* zst = nullptr);
 // Deferred packing, row-major, the interval's last step (states in place):
 // Adam on the selected columns and the hand-over of the unselected ones,
 // g_1 + ... + g_t summed in step order from h's plans (the earlier steps)

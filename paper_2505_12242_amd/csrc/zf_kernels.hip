@@ -480,7 +480,12 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const DevMat* __restri
                                                           const int64_t* __restrict__ off,
                                                           int32_t nmats, DevMat one, AdamK c,
                                                           int32_t mode, int32_t first,
-                                                          float scale, Pending pd) {
+                                                          float scale, Pending pd,
+                                                          const ZenState* __restrict__ zst) {
+  // Zen-auto with the interval driven on the device: a refresh step, or
+  // any step after an ended interval, overwrites; else it accumulates
+  if (zst != nullptr)
+    first = (mode != kInplace || uniform_i32(zst->ended)) ? 1 : uniform_i32(zst->length) + 1;
   int64_t local;
   const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, local);
   const int64_t cblk = local % d.up_cb;
@@ -632,13 +637,9 @@ __global__ __launch_bounds__(kThreads) void update_kernel(const DevMat* __restri
 // a6: hand-over.  Same column mapping as the update pass.
 // ---------------------------------------------------------------------------
 
-template <bool BATCHED>
-__global__ __launch_bounds__(kThreads) void unpack_kernel(const DevMat* __restrict__ mats,
-                                                          const int64_t* __restrict__ off,
-                                                          int32_t nmats, DevMat one,
-                                                          float scale) {
-  int64_t local;
-  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, local);
+// One block's share of the hand-over: the block-th tile (rows x 256
+// columns) of matrix d.
+__device__ __forceinline__ void unpack_unit(const DevMat& d, int64_t local, float scale) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int64_t cblk = local % d.up_cb;
@@ -677,6 +678,39 @@ __global__ __launch_bounds__(kThreads) void unpack_kernel(const DevMat* __restri
   for (; i < rows; ++i) {
     const float a = buf_f32(rA, vA, i * sA);
     buf_put_f32(sel ? 0.0f : a * scale, rD, vD, i * sD);
+  }
+}
+
+template <bool BATCHED>
+__global__ __launch_bounds__(kThreads) void unpack_kernel(const DevMat* __restrict__ mats,
+                                                          const int64_t* __restrict__ off,
+                                                          int32_t nmats, DevMat one,
+                                                          float scale) {
+  int64_t local;
+  const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, local);
+  unpack_unit(d, local, scale);
+}
+
+// The hand-over of an interval that Zen-auto ended on the device: nothing
+// unless zst->ended; then scale = fp32(1 / length) (a correctly rounded
+// fp32 division, the value the host passes as fp32(1.0 / length)).  A fixed
+// grid walks the table's unpack tiles, so that a step that does not end its
+// interval costs one short launch.
+__global__ __launch_bounds__(kThreads) void unpack_zen_kernel(const DevMat* __restrict__ mats,
+                                                             const int64_t* __restrict__ off,
+                                                             int32_t nmats, int64_t units,
+                                                             const ZenState* __restrict__ zst) {
+  if (!uniform_i32(zst->ended)) return;
+  const float scale = 1.0f / static_cast<float>(uniform_i32(zst->length));
+  const int64_t b = xcd_remap(blockIdx.x, gridDim.x);
+  int lo = 0;
+  for (int64_t u = b; u < units; u += gridDim.x) {
+    int hi = nmats - 1;
+    while (lo < hi) {  // largest q with off[q] <= u (u only grows)
+      const int mid = (lo + hi + 1) >> 1;
+      if (off[mid] <= u) lo = mid; else hi = mid - 1;
+    }
+    unpack_unit(mats[lo], u - off[lo], scale);
   }
 }
 
@@ -772,29 +806,32 @@ hipError_t launch_topk(const Table& t, const DevMat& one, int64_t blocks, hipStr
 template <bool ADAM, bool PACK, bool HAND, bool PEND = false>
 static void launch_update_t(const Table& t, const DevMat& one, dim3 grid, const AdamK& c,
                             int32_t mode, int32_t first, float scale, hipStream_t s,
-                            const Pending& pd = Pending{}) {
+                            const Pending& pd = Pending{}, const ZenState* zst = nullptr) {
   if (t.mats != nullptr)
     hipLaunchKernelGGL((update_kernel<true, ADAM, PACK, HAND, PEND>), grid, dim3(kThreads), 0, s,
-                       t.mats, t.off, t.nmats, one, c, mode, first, scale, pd);
+                       t.mats, t.off, t.nmats, one, c, mode, first, scale, pd, zst);
   else
     hipLaunchKernelGGL((update_kernel<false, ADAM, PACK, HAND, PEND>), grid, dim3(kThreads), 0, s,
-                       t.mats, t.off, t.nmats, one, c, mode, first, scale, pd);
+                       t.mats, t.off, t.nmats, one, c, mode, first, scale, pd, zst);
 }
 
 hipError_t launch_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
                          int32_t mode, int32_t first, bool adam, bool pack, bool handover,
-                         float scale, hipStream_t s, const Pending* pend) {
+                         float scale, hipStream_t s, const Pending* pend, const ZenState* zst) {
   (void)hipGetLastError();
   if (blocks <= 0) return hipSuccess;
   const dim3 grid(static_cast<uint32_t>(blocks));
   if (handover && !(adam && pack)) return hipErrorInvalidValue;
+  if (zst != nullptr && (pend != nullptr || handover || !pack)) return hipErrorInvalidValue;
   if (pend != nullptr) {
     if (!(adam && pack) || handover || mode != kRemap) return hipErrorInvalidValue;
     launch_update_t<true, true, false, true>(t, one, grid, c, mode, first, 1.0f, s, *pend);
   } else if (handover) launch_update_t<true, true, true>(t, one, grid, c, mode, first, scale, s);
-  else if (adam && pack) launch_update_t<true, true, false>(t, one, grid, c, mode, first, 1.0f, s);
+  else if (adam && pack)
+    launch_update_t<true, true, false>(t, one, grid, c, mode, first, 1.0f, s, Pending{}, zst);
   else if (adam) launch_update_t<true, false, false>(t, one, grid, c, mode, first, 1.0f, s);
-  else if (pack) launch_update_t<false, true, false>(t, one, grid, c, mode, first, 1.0f, s);
+  else if (pack)
+    launch_update_t<false, true, false>(t, one, grid, c, mode, first, 1.0f, s, Pending{}, zst);
   return hipGetLastError();
 }
 
@@ -804,6 +841,20 @@ hipError_t launch_unpack(const Table& t, const DevMat& one, int64_t blocks, floa
   if (blocks > 0)
     ZF_LAUNCH(unpack_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), s, t, one,
               scale);
+  return hipGetLastError();
+}
+
+// 256 blocks per CU: a step that does not end its interval exits in a
+// short launch, one that does keeps enough tiles in flight (4096 and a full
+// grid measured slower)
+constexpr int64_t kUnpackZenGrid = 65536;
+
+hipError_t launch_unpack_zen(const Table& t, int64_t units, const ZenState* zst, hipStream_t s) {
+  (void)hipGetLastError();
+  if (units <= 0 || t.mats == nullptr) return hipSuccess;
+  const dim3 grid(static_cast<uint32_t>(units < kUnpackZenGrid ? units : kUnpackZenGrid));
+  hipLaunchKernelGGL(unpack_zen_kernel, grid, dim3(kThreads), 0, s, t.mats, t.off, t.nmats, units,
+                     zst);
   return hipGetLastError();
 }
 

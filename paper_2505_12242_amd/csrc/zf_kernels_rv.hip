@@ -118,10 +118,14 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
                                                              int32_t nmats, DevMat one, AdamK c,
                                                              int32_t first, float scale,
                                                              double* __restrict__ zs,
-                                                             HistTable hist) {
+                                                             HistTable hist,
+                                                             const ZenState* __restrict__ zst) {
   static_assert(!STATS || (ADAM && PACK && !HAND), "statistics of the fused update");
   static_assert(!DEF || (BATCHED && !ADAM && !PACK && !HAND && !STATS && !A16),
                 "the deferred hand-over pass");
+  // Zen-auto with the interval driven on the device (steps in place):
+  // overwrite after an ended interval, else accumulate
+  if (zst != nullptr) first = uniform_i32(zst->ended) ? 1 : uniform_i32(zst->length) + 1;
   __shared__ __attribute__((aligned(16))) uint16_t sg[kRvBatch][kRvMaxCols];
   __shared__ __attribute__((aligned(16))) uint16_t sa[A16 ? kRvBatch : 1][A16 ? kRvMaxCols : 8];
   __shared__ __attribute__((aligned(16))) float sd[HAND ? kRvBatch : 1][HAND ? kRvMaxCols : 4];
@@ -508,16 +512,16 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
 
 template <bool ADAM, bool PACK, bool HAND, bool STATS, bool A16>
 void launch_rv_a(const Table& t, const DevMat& one, dim3 grid, const AdamK& c, int32_t first,
-                 float scale, hipStream_t s, double* zs) {
+                 float scale, hipStream_t s, double* zs, const ZenState* zst = nullptr) {
   const HistTable none{};
   if (t.mats != nullptr)
     hipLaunchKernelGGL((rv_update_kernel<true, ADAM, PACK, HAND, STATS, A16, false>), grid,
                        dim3(kThreads), 0, s, t.mats, t.off, t.nmats, one, c, first, scale, zs,
-                       none);
+                       none, zst);
   else
     hipLaunchKernelGGL((rv_update_kernel<false, ADAM, PACK, HAND, STATS, A16, false>), grid,
                        dim3(kThreads), 0, s, t.mats, t.off, t.nmats, one, c, first, scale, zs,
-                       none);
+                       none, zst);
 }
 
 // The stage's code (and its registers and LDS) only in the launches of the
@@ -525,29 +529,30 @@ void launch_rv_a(const Table& t, const DevMat& one, dim3 grid, const AdamK& c, i
 // its second step.  (Zen-auto statistics never run with a row-major stage.)
 template <bool ADAM, bool PACK, bool HAND, bool STATS = false>
 void launch_rv_t(const Table& t, const DevMat& one, dim3 grid, const AdamK& c, int32_t first,
-                 float scale, hipStream_t s, double* zs = nullptr) {
+                 float scale, hipStream_t s, double* zs = nullptr, const ZenState* zst = nullptr) {
   if constexpr (PACK && !STATS) {
-    if (first == 2 || (first == 1 && !HAND)) {
+    if (zst == nullptr && (first == 2 || (first == 1 && !HAND))) {
       launch_rv_a<ADAM, PACK, HAND, STATS, true>(t, one, grid, c, first, scale, s, zs);
       return;
     }
   }
-  launch_rv_a<ADAM, PACK, HAND, STATS, false>(t, one, grid, c, first, scale, s, zs);
+  launch_rv_a<ADAM, PACK, HAND, STATS, false>(t, one, grid, c, first, scale, s, zs, zst);
 }
 
 }  // namespace
 
 hipError_t launch_rv_update(const Table& t, const DevMat& one, int64_t blocks, const AdamK& c,
                             int32_t mode, int32_t first, bool adam, bool pack, bool handover,
-                            float scale, hipStream_t s, double* zs) {
+                            float scale, hipStream_t s, double* zs, const ZenState* zst) {
   (void)hipGetLastError();
   if (blocks <= 0) return hipSuccess;
   const dim3 grid(static_cast<uint32_t>(blocks));
   if (handover && !(adam && pack)) return hipErrorInvalidValue;
   if (adam && mode != kInplace) return hipErrorInvalidValue;  // refresh: per-column kernel
+  if (zst != nullptr && zs == nullptr) return hipErrorInvalidValue;  // Zen-auto steps only
   if (zs != nullptr) {
     if (!(adam && pack) || handover) return hipErrorInvalidValue;
-    launch_rv_t<true, true, false, true>(t, one, grid, c, first, 1.0f, s, zs);
+    launch_rv_t<true, true, false, true>(t, one, grid, c, first, 1.0f, s, zs, zst);
   } else if (handover) launch_rv_t<true, true, true>(t, one, grid, c, first, scale, s);
   else if (adam && pack) launch_rv_t<true, true, false>(t, one, grid, c, first, 1.0f, s);
   else if (adam) launch_rv_t<true, false, false>(t, one, grid, c, first, 1.0f, s);
@@ -564,7 +569,7 @@ hipError_t launch_rv_handover_deferred(const Table& t, const DevMat& one, int64_
                                                 1.0f, s, nullptr);
   hipLaunchKernelGGL((rv_update_kernel<true, false, false, false, false, false, true>),
                      dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0, s, t.mats, t.off,
-                     t.nmats, one, c, 0, scale, nullptr, h);
+                     t.nmats, one, c, 0, scale, nullptr, h, nullptr);
   return hipGetLastError();
 }
 

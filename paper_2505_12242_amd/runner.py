@@ -32,9 +32,9 @@ Pipeline, "Hyperparameter Auto-tuning"): every update is zf_plan_update_zen,
 which also measures the selected channels' gradient norms and the
 accumulated channels' norms; the interval ends after the step whose pooled
 mean accumulated norm reaches zen_tau times the pooled mean selected norm,
-after `accum` (= S_max) steps, or before a refresh.  In the channel-major
-layout without the offloaded optimizer the decision stays on the device
-(zen_on_device, the default there): the update reads the interval's
+after `accum` (= S_max) steps, or before a refresh.  Without the offloaded
+optimizer the decision stays on the device (zen_on_device, the default
+there; both layouts): the update reads the interval's
 position from a device state word, the totals kernel writes the end
 decision into it, and a hand-over pass acts on it
 (zf_plan_update_zen_device, zf_plan_handover_zen), so a step issues no
@@ -210,9 +210,9 @@ class SelectiveUpdateRunner:
         dev = self.device
         f32 = torch.float32
         self.zen_tau = None if zen_tau is None else float(zen_tau)
-        # the interval decided on the device (channel-major, no offload)
+        # the interval decided on the device (no offload)
         self.zen_device = (self.zen_tau is not None and bool(zen_on_device)
-                           and layout != ROW_MAJOR and not self.offload)
+                           and not self.offload)
         if self.zen_tau is not None:
             self.zen_totals = torch.zeros(ZEN_TOTALS_BYTES // 8, dtype=torch.int64, device=dev)
             self._zen_host = torch.zeros(ZEN_TOTALS_BYTES // 8, dtype=torch.int64,

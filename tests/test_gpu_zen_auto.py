@@ -38,9 +38,11 @@ zf = pytest.importorskip("paper_2505_12242_amd")
 SHAPES = [(264, 300), (4104, 70), (43, 77), (8192, 65), (16, 3), (128, 1000)]
 
 
-def _inputs(shapes, ratio, T, seed, dev, layout=None):
+def _inputs(shapes, ratio, T, seed, dev, layout=None, padded=False):
     """Device gradients per step and bf16 weights in `layout` (default
-    channel-major), plus the logical host bit patterns the oracle takes."""
+    channel-major), plus the logical host bit patterns the oracle takes.
+    padded (row-major): gradient rows padded to 16 bytes, so that the plans
+    run the 16-byte update."""
     cm = layout is None or layout == zf.CHANNEL_MAJOR
     slots, host = [], []
     for t in range(1, T + 1):
@@ -51,7 +53,12 @@ def _inputs(shapes, ratio, T, seed, dev, layout=None):
             s = space_boundary(jittered_scales(base, 0.05, derive_seed(seed, q, "jit", t)), k)
             g = gradient(n, m, s, derive_seed(seed, q, "grad", t), device=dev)
             hslot.append(bits_np(g))
-            dslot.append(g.t().contiguous() if cm else g)
+            if cm:
+                dslot.append(g.t().contiguous())
+            elif padded:
+                dslot.append(zf.alloc_stored(zf.ROW_MAJOR, n, m, torch.bfloat16, dev).copy_(g))
+            else:
+                dslot.append(g)
         slots.append(dslot)
         host.append(hslot)
     weights, w0 = [], []
@@ -104,8 +111,8 @@ def run_zen(shapes, ratio, R, S_max, tau, T, seed, host_in=None, layout=None, on
     slots, host, weights, w0 = host_in or _inputs(shapes, ratio, T, seed, dev, layout)
     runner = zf.SelectiveUpdateRunner(shapes, ratio, hp, R, S_max, slots, weights, device=dev,
                                       layout=layout, zen_tau=tau, zen_on_device=on_device)
-    # channel-major: the interval decided on the device unless asked otherwise
-    assert runner.zen_device == (on_device and layout == zf.CHANNEL_MAJOR)
+    # the interval decided on the device unless asked otherwise
+    assert runner.zen_device == on_device
     za = _oracle(shapes, w0, ratio, hp, R, S_max, tau)
     ends = []
     exact_stats = total_stats = 0
@@ -150,8 +157,9 @@ def run_zen(shapes, ratio, R, S_max, tau, T, seed, host_in=None, layout=None, on
 
 
 LAYOUTS = [pytest.param(zf.ROW_MAJOR, id="rm"), pytest.param(zf.CHANNEL_MAJOR, id="cm")]
-# the channel-major interval decided on the device (the default) and on the host
-LAYOUT_MODES = [pytest.param(zf.ROW_MAJOR, True, id="rm"),
+# the interval decided on the device (the default) and on the host
+LAYOUT_MODES = [pytest.param(zf.ROW_MAJOR, True, id="rm-device"),
+                pytest.param(zf.ROW_MAJOR, False, id="rm-host"),
                 pytest.param(zf.CHANNEL_MAJOR, True, id="cm-device"),
                 pytest.param(zf.CHANNEL_MAJOR, False, id="cm-host")]
 
@@ -228,29 +236,33 @@ def test_zen_auto_deterministic(layout):
 
 
 @pytest.mark.timeout(300)
+@pytest.mark.parametrize("storage", ["cm", "rm", "rm-16B"])
 @pytest.mark.parametrize("case", ["early-end", "warmup"])
-def test_zen_auto_on_device_needs_no_host_round_trip(case):
+def test_zen_auto_on_device_needs_no_host_round_trip(case, storage):
     """The device-decided interval: steps are enqueued without reading
     anything back (each returned step kind is unresolved until asked), and
     resolving them afterwards gives the host-decided run's positions, ends,
     hand-overs and states bit for bit -- with a threshold between the
     observed ratios (intervals ended by the trigger before S_max), and with
-    a two-step warm-up."""
+    a two-step warm-up.  Channel-major, and row-major on the per-column
+    update (unpadded rows) and on the 16-byte update (16-byte rows)."""
     dev = torch.device("cuda")
+    layout = zf.CHANNEL_MAJOR if storage == "cm" else zf.ROW_MAJOR
+    padded = storage == "rm-16B"
     if case == "early-end":
         T, R, S_max, warmup = 10, 16, 6, 0
-        inputs = _inputs(SHAPES, 0.1, T, 12, dev, zf.CHANNEL_MAJOR)
+        inputs = _inputs(SHAPES, 0.1, T, 12, dev, layout, padded)
         r = _ratios(SHAPES, inputs[1], inputs[3], 0.1, zf.AdamHparams(lr=1e-3), R, S_max)
         tau = math.sqrt(min(r[:2]) * max(r[2:S_max]))
     else:
         T, R, S_max, warmup, tau = 8, 4, 3, 2, 1.0
-        inputs = _inputs(SHAPES, 0.1, T, 16, dev, zf.CHANNEL_MAJOR)
+        inputs = _inputs(SHAPES, 0.1, T, 16, dev, layout, padded)
     results = []
     for on_device in (True, False):
         slots, _, weights, _ = inputs
         ws = [w.clone() for w in weights]
         runner = zf.SelectiveUpdateRunner(SHAPES, 0.1, zf.AdamHparams(lr=1e-3), R, S_max, slots,
-                                          ws, device=dev, layout=zf.CHANNEL_MAJOR, zen_tau=tau,
+                                          ws, device=dev, layout=layout, zen_tau=tau,
                                           warmup=warmup, zen_on_device=on_device)
         assert runner.zen_device == on_device
         kinds, hand = [], []
