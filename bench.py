@@ -717,9 +717,9 @@ def main(argv=None) -> int:
     drain = time.perf_counter() - t_drain
     gc.enable()
 
-    def model_bytes(kind, survey=False):
+    def model_bytes(kind, unfused=False):
         first, second = kind.step_in_interval == 1, kind.step_in_interval == 2
-        if survey:  # the unfused method: separate hand-over, fp32 first-step packing
+        if unfused:  # the unfused method: separate hand-over, fp32 first-step packing
             return step_bytes(shapes, ks, kind.refresh, first, kind.interval_end,
                               offload=args.offload)
         return step_bytes(shapes, ks, kind.refresh, first, kind.interval_end,
@@ -735,7 +735,7 @@ def main(argv=None) -> int:
                             deferred=runner.deferred, length=kind.step_in_interval)
 
     build_total = sum(sum(model_bytes(k).values()) for k in kinds)
-    survey_total = sum(sum(model_bytes(k, True).values()) for k in kinds)
+    unfused_total = sum(sum(model_bytes(k, True).values()) for k in kinds)
     value = build_total / wall / 1e9
     # what the reference streams predict for a pass that reads r and writes w
     # bytes: r / (read rate) + w / (write rate), the write rate inferred from
@@ -749,7 +749,7 @@ def main(argv=None) -> int:
 
     per = {}
     for name, i, a, b in spans:
-        e = per.setdefault(name, {"ms": [], "bytes": 0, "survey": 0, "rw": [0, 0]})
+        e = per.setdefault(name, {"ms": [], "bytes": 0, "unfused": 0, "rw": [0, 0]})
         e["ms"].append(a.elapsed_time(b))
         cls = kernel_class(name)
         if cls is not None:
@@ -757,7 +757,7 @@ def main(argv=None) -> int:
             e["bytes"] += r + w
             e["rw"][0] += r
             e["rw"][1] += w
-            e["survey"] += model_bytes(kinds[i], True)[cls]
+            e["unfused"] += model_bytes(kinds[i], True)[cls]
     kernels = {}
     for name, e in per.items():
         n = len(e["ms"])
@@ -776,7 +776,7 @@ def main(argv=None) -> int:
 
     # the dominant kernel: the fused Adam + pack pass in its middle-step form
     # (states in place, accumulation; no hand-over): its bytes per launch are
-    # the survey's per-unit figures, 28 per selected and 10 per unselected
+    # the unfused method's per-unit figures, 28 per selected and 10 per unselected
     # element; else the update launch kind with the most time
     upd = [nm for nm in per if kernel_class(nm) == "update"]
     dom = "update" if "update" in per else (max(upd, key=lambda nm: sum(per[nm]["ms"]))
@@ -786,7 +786,7 @@ def main(argv=None) -> int:
         e = per[dom]
         n = len(e["ms"])
         avg = sum(e["ms"]) / n
-        nbytes = (e["survey"] if dom == "update" else e["bytes"]) / n
+        nbytes = (e["unfused"] if dom == "update" else e["bytes"]) / n
         achieved = nbytes / (avg * 1e-3) / 1e9
         kname = launch_kernels(dom, layout == zf.CHANNEL_MAJOR, runner.deferred)
         roof = {
@@ -800,7 +800,7 @@ def main(argv=None) -> int:
             "traffic": recorded_traffic(dom, wl.name, args.layout + (
                 "" if runner.deferred else "-every-step")),
             "bytes_per_launch": round(nbytes),
-            "byte_model": "survey per-unit figures" if dom == "update" else "build",
+            "byte_model": "unfused per-unit figures" if dom == "update" else "build",
             "avg_launch_ms": round(avg, 4),
             "frac_of_reference_stream": kernels[dom].get("frac_of_reference_stream"),
         }
@@ -848,11 +848,11 @@ def main(argv=None) -> int:
             "build": {"GB_per_step": round(build_total / args.steps / 1e9, 3),
                       "GB/s": round(value, 1), "frac_of_peak": round(value / HBM_PEAK_GBS, 4),
                       "what": "bytes this build's kernels move (value)"},
-            "survey": {"GB_per_step": round(survey_total / args.steps / 1e9, 3),
-                       "GB/s": round(survey_total / wall / 1e9, 1),
-                       "frac_of_peak": round(survey_total / wall / 1e9 / HBM_PEAK_GBS, 4),
-                       "what": "the unfused method's bytes: separate hand-over pass, fp32 "
-                               "first-step packing"},
+            "unfused": {"GB_per_step": round(unfused_total / args.steps / 1e9, 3),
+                        "GB/s": round(unfused_total / wall / 1e9, 1),
+                        "frac_of_peak": round(unfused_total / wall / 1e9 / HBM_PEAK_GBS, 4),
+                        "what": "the unfused method's bytes: packing every step in fp32, a "
+                                "separate hand-over pass"},
         },
         "kernels": kernels,
         "reference_streams": calib,
