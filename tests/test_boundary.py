@@ -255,6 +255,25 @@ def test_plan_validation():
     LIB.zf_plan_destroy(None)
 
 
+def test_plan_entry_points_reject_a_missing_plan():
+    """The deferred hand-over and the device-driven Zen-auto calls validate
+    on the host: no plan, no state, a bad count or scale give ZF_EINVAL and
+    nothing is enqueued (no GPU is touched)."""
+    hp = _lib.ZfAdamHparams(1e-5, 0.9, 0.999, 1e-8, 0.0)
+    hs = (ctypes.c_void_p * 16)()
+    for n_earlier in (0, 1, 15, 16):
+        assert LIB.zf_plan_update_handover_deferred(None, ctypes.byref(hp), 2, hs, n_earlier,
+                                                    0.5, None) == EINVAL
+    assert LIB.zf_plan_update_handover_deferred(None, None, 2, None, 1, float("nan"),
+                                                None) == EINVAL
+    assert LIB.zf_plan_update_zen_device(None, ctypes.byref(hp), 1, 0, 4, 0, 1.0, None, None,
+                                         None) == EINVAL
+    assert LIB.zf_plan_handover_zen(None, None, None) == EINVAL
+    for name in ("zf_plan_update_handover_deferred", "zf_plan_update_zen_device",
+                 "zf_plan_handover_zen"):
+        assert name in header_functions()
+
+
 def test_rowmajor_stage_stride_rule():
     """The row-major bf16 first-step stage needs 16-byte rows: a stride that
     is a multiple of 8 elements and a 16-byte aligned base.  A single row
