@@ -722,15 +722,19 @@ def main(argv=None) -> int:
         if unfused:  # the unfused method: separate hand-over, fp32 first-step packing
             return step_bytes(shapes, ks, kind.refresh, first, kind.interval_end,
                               offload=args.offload)
+        # (Zen-auto on the device: an end the caller forces is handed over
+        # by the update itself)
+        fh = fused or getattr(kind, "fused", False)
         return step_bytes(shapes, ks, kind.refresh, first, kind.interval_end,
-                          offload=args.offload, fused_handover=fused, second=second,
+                          offload=args.offload, fused_handover=fh, second=second,
                           stage=runner.use_stage, scored_handover=runner.score_handover,
                           deferred=runner.deferred, length=kind.step_in_interval)
 
     def model_traffic(kind):
         first, second = kind.step_in_interval == 1, kind.step_in_interval == 2
+        fh = fused or getattr(kind, "fused", False)
         return step_traffic(shapes, ks, kind.refresh, first, kind.interval_end,
-                            offload=args.offload, fused_handover=fused, second=second,
+                            offload=args.offload, fused_handover=fh, second=second,
                             stage=runner.use_stage, scored_handover=runner.score_handover,
                             deferred=runner.deferred, length=kind.step_in_interval)
 

@@ -659,8 +659,9 @@ zf_status zf_plan_update_zen_pending(zf_plan* plan, const zf_adam_hparams* hp, i
  * {0, 1} (nothing accumulated; the first step starts an interval) and then
  * owned by the calls below, in stream order. */
 typedef struct zf_zen_state {
-  int32_t length; /* steps of the current interval so far               */
-  int32_t ended;  /* 1: the last step ended its interval (handed over)  */
+  int32_t length; /* steps of the current interval so far                     */
+  int32_t ended;  /* nonzero: the last step ended its interval; 1: its hand-
+                   * over is zf_plan_handover_zen's, 2: the update wrote it  */
 } zf_zen_state;
 
 /* zf_plan_update_zen whose position in the interval is read from *state
@@ -671,7 +672,13 @@ typedef struct zf_zen_state {
  * After the statistics and totals, the same launch sequence updates the
  * state: length = that position; ended = trigger || position >=
  * accum_interval (S_max) || force_end.  force_end: the caller's own end of
- * the interval (the next step refreshes the selection, or a warm-up step).
+ * the interval (the next step refreshes the selection, or a warm-up step):
+ * 1 -- the hand-over is left to zf_plan_handover_zen; 2 (channel-major,
+ * `unpacked` required) -- the update writes it itself, scale = fp32(1 /
+ * position), bit for bit what zf_plan_handover_zen would write, and sets
+ * ended = 2 so that zf_plan_handover_zen writes nothing (the packed buffer
+ * is then left as it was, as in zf_plan_update_handover).  Other values:
+ * ZF_EINVAL.
  * Both layouts, plans without a full-state store; a row-major plan without
  * the bf16 stage; the requirements of zf_plan_update_zen otherwise.  Follow
  * it with zf_plan_handover_zen. */
@@ -681,7 +688,7 @@ zf_status zf_plan_update_zen_device(zf_plan* plan, const zf_adam_hparams* hp, in
                                     zf_stream stream);
 
 /* The hand-over of the step zf_plan_update_zen_device just ran: if
- * state->ended, every matrix's `unpacked` buffer receives the hand-over of
+ * state->ended == 1, every matrix's `unpacked` buffer receives the hand-over of
  * the interval (scale = fp32(1 / state->length); from the bf16 stage after
  * a one-step interval on a plan with one; +0.0 in the selected channels'
  * rows), bit for bit as zf_plan_unpack / zf_plan_unpack_first with that

@@ -867,16 +867,18 @@ class Plan:
             float(tau), totals.data_ptr(), _stream(stream)))
 
     def update_zen_device(self, hp: AdamHparams, step: int, mode: int, accum_interval: int,
-                          force_end: bool, tau: float, totals: torch.Tensor,
+                          force_end: int, tau: float, totals: torch.Tensor,
                           state: torch.Tensor, stream=None) -> None:
         """update_zen with the interval's position read from, and the end
         decision written to, the device interval state `state` (a GPU tensor
-        of ZEN_STATE_BYTES bytes; zf_plan_update_zen_device)."""
+        of ZEN_STATE_BYTES bytes; zf_plan_update_zen_device).  force_end: 0,
+        1 (the caller ends the interval; handover_zen hands over) or 2
+        (channel-major: the update writes the hand-over itself)."""
         _check_dev_bytes(totals, ZEN_TOTALS_BYTES, "totals")
         _check_dev_bytes(state, ZEN_STATE_BYTES, "state")
         c_hp = hp.as_c()
         _check("zf_plan_update_zen_device", LIB.zf_plan_update_zen_device(
-            self._h, ctypes.byref(c_hp), step, mode, accum_interval, int(bool(force_end)),
+            self._h, ctypes.byref(c_hp), step, mode, accum_interval, int(force_end),
             float(tau), totals.data_ptr(), state.data_ptr(), _stream(stream)))
 
     def handover_zen(self, state: torch.Tensor, stream=None) -> None:

@@ -1401,8 +1401,9 @@ zf_status plan_update_zen(zf_plan* p, const AdamK& c, int32_t mode, int32_t firs
   const Table tz{p->d_mats, p->d_off_zen, p->nmats};
   hipError_t e;
   if (p->layout == zf::kChannelMajor) {
-    e = zf::launch_cm_update(t, p->mats[0], p->blk_up, c, mode, first, true, true, p->d_zs, false,
-                             1.0f, s, pd, zst);
+    // force_end 2: the interval ends here and the update writes the hand-over
+    e = zf::launch_cm_update(t, p->mats[0], p->blk_up, c, mode, first, true, true, p->d_zs,
+                             force_end == 2, 1.0f, s, pd, zst);
     if (e != hipSuccess) return hip_fail(e);
     e = zf::launch_zen_finalize(tz, p->mats[0], p->blk_zen, p->d_zs, p->d_zb, s);
   } else if (pd == nullptr && use_rv(p->mats[0], mode, true)) {
@@ -1469,9 +1470,12 @@ zf_status zf_plan_update_zen_device(zf_plan* p, const zf_adam_hparams* hp, int64
   if (accum_interval < 1 || accum_interval > INT32_MAX || state == nullptr ||
       !aligned(state, 4))
     return ZF_EINVAL;
+  // 2: end here with the hand-over fused into the update (channel-major)
+  if (force_end < 0 || force_end > 2) return ZF_EINVAL;
+  if (force_end == 2 && (p->layout != zf::kChannelMajor || !p->can_handover)) return ZF_EINVAL;
   return plan_update_zen(p, adam_consts(*hp, step), mode, 0, tau, totals, as_stream(stream),
                          nullptr, reinterpret_cast<zf::ZenState*>(state),
-                         static_cast<int32_t>(accum_interval), force_end ? 1 : 0);
+                         static_cast<int32_t>(accum_interval), force_end);
 }
 
 zf_status zf_plan_handover_zen(zf_plan* p, const zf_zen_state* state, zf_stream stream) {

@@ -692,7 +692,7 @@ __global__ __launch_bounds__(kThreads) void unpack_kernel(const DevMat* __restri
 }
 
 // The hand-over of an interval that Zen-auto ended on the device: nothing
-// unless zst->ended; then scale = fp32(1 / length) (a correctly rounded
+// unless zst->ended == 1; then scale = fp32(1 / length) (a correctly rounded
 // fp32 division, the value the host passes as fp32(1.0 / length)).  A fixed
 // grid walks the table's unpack tiles, so that a step that does not end its
 // interval costs one short launch.
@@ -700,7 +700,7 @@ __global__ __launch_bounds__(kThreads) void unpack_zen_kernel(const DevMat* __re
                                                              const int64_t* __restrict__ off,
                                                              int32_t nmats, int64_t units,
                                                              const ZenState* __restrict__ zst) {
-  if (!uniform_i32(zst->ended)) return;
+  if (uniform_i32(zst->ended) != 1) return;  // (2: already handed over)
   const float scale = 1.0f / static_cast<float>(uniform_i32(zst->length));
   const int64_t b = xcd_remap(blockIdx.x, gridDim.x);
   int lo = 0;

@@ -421,7 +421,9 @@ __device__ __forceinline__ void cm_swap_out(const DevMat& d, int64_t j, int64_t 
 // HAND (fused Adam + pack only, the last step of an interval): the hand-over
 // is written instead of the packed sums -- out row j = scale * (A + g) for an
 // unselected channel, +0.0 for a selected one -- and the packed buffer is
-// left as it was (it is overwritten when the next interval starts).
+// left as it was (it is overwritten when the next interval starts).  With
+// STATS (Zen-auto, an interval the caller ends at this step) the statistics
+// are those of the new sums, before the scale.
 //
 // PEND (fused Adam + pack in kRemap against the store, with or without
 // STATS): a channel that
@@ -459,6 +461,9 @@ __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(c
   if (PH == 0 && zst != nullptr) {
     const int32_t pos = (mode != kInplace || zst->ended) ? 1 : zst->length + 1;
     ph = pos < 3 ? pos : 3;
+    // HAND (an interval the caller ends at this step): scale = fp32(1 /
+    // length), a correctly rounded fp32 division
+    if constexpr (HAND) scale = 1.0f / static_cast<float>(pos);
   }
   int64_t local;
   const DevMat& d = get_mat<BATCHED>(mats, off, nmats, one, local);
@@ -498,15 +503,15 @@ __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(c
       if constexpr (HAND) {
         const rsrc_t rOut = make_rsrc(d.out + j * d.ld_out + e0, len * 4);
         if (d.vec) {
-          if (ph == 1) cm_pack_vec_any<true, false, true>(d.cm_vpt, rG, rA, ss, rOut, scale);
+          if (ph == 1) cm_pack_vec_any<true, STATS, true>(d.cm_vpt, rG, rA, ss, rOut, scale);
           else if (a16 && ph == 2)
-            cm_pack_vec_any<false, false, true, 2>(d.cm_vpt, rG, rA, ss, rOut, scale, rA16);
-          else cm_pack_vec_any<false, false, true>(d.cm_vpt, rG, rA, ss, rOut, scale);
+            cm_pack_vec_any<false, STATS, true, 2>(d.cm_vpt, rG, rA, ss, rOut, scale, rA16);
+          else cm_pack_vec_any<false, STATS, true>(d.cm_vpt, rG, rA, ss, rOut, scale);
         } else {
-          if (ph == 1) cm_pack_elem<true, false, true>(rG, rA, len, ss, rOut, scale);
+          if (ph == 1) cm_pack_elem<true, STATS, true>(rG, rA, len, ss, rOut, scale);
           else if (a16 && ph == 2)
-            cm_pack_elem<false, false, true, 2>(rG, rA, len, ss, rOut, scale, rA16);
-          else cm_pack_elem<false, false, true>(rG, rA, len, ss, rOut, scale);
+            cm_pack_elem<false, STATS, true, 2>(rG, rA, len, ss, rOut, scale, rA16);
+          else cm_pack_elem<false, STATS, true>(rG, rA, len, ss, rOut, scale);
         }
       } else if (d.vec) {
         if (ph == 1) {
@@ -777,7 +782,8 @@ __global__ __launch_bounds__(kThreads) void cm_unpack_kernel(const DevMat* __res
 }
 
 // The hand-over of an interval that Zen-auto ended on the device: nothing
-// unless zst->ended; then scale = fp32(1 / length) (a correctly rounded
+// unless zst->ended == 1 (ended, not yet handed over: 2 means the update
+// wrote the hand-over itself); then scale = fp32(1 / length) (a correctly rounded
 // fp32 division, the value the host passes as fp32(1.0 / length)), from the
 // stage after a one-step interval when the plan keeps one.  A fixed grid
 // loops over the table's unpack blocks, so that a step that does not end
@@ -787,7 +793,7 @@ __global__ __launch_bounds__(kThreads) void cm_unpack_zen_kernel(const DevMat* _
                                                                 int32_t nmats, int64_t units,
                                                                 const ZenState* __restrict__ zst,
                                                                 int32_t stage) {
-  if (!zst->ended) return;
+  if (zst->ended != 1) return;
   const int32_t length = zst->length;
   const float scale = 1.0f / static_cast<float>(length);
   const bool from_stage = stage != 0 && length == 1;
@@ -913,7 +919,7 @@ hipError_t launch_cm_update(const Table& t, const DevMat& one, int64_t blocks, c
   if (blocks <= 0) return hipSuccess;
   const dim3 grid(static_cast<uint32_t>(blocks));
   if ((zs != nullptr || handover) && !(adam && pack)) return hipErrorInvalidValue;
-  if (zs != nullptr && handover) return hipErrorInvalidValue;
+  if (zs != nullptr && handover && zst == nullptr) return hipErrorInvalidValue;
   if (zst != nullptr && (zs == nullptr || pend != nullptr)) return hipErrorInvalidValue;
   if (pend != nullptr) {
     if (!(adam && pack) || handover || mode != kRemap) return hipErrorInvalidValue;
@@ -923,6 +929,11 @@ hipError_t launch_cm_update(const Table& t, const DevMat& one, int64_t blocks, c
     else
       launch_cm_update_t<true, true, false, false, true>(t, one, grid, c, mode, first, nullptr,
                                                          1.0f, s, *pend);
+  } else if (zs != nullptr && handover) {
+    // Zen-auto on the device, an interval the caller ends here: the
+    // hand-over fused, its scale from the interval's length
+    launch_cm_update_t<true, true, true, true>(t, one, grid, c, mode, first, zs, 1.0f, s,
+                                               Pending{}, zst);
   } else if (zs != nullptr) {
     launch_cm_update_t<true, true, true, false>(t, one, grid, c, mode, first, zs, 1.0f, s,
                                                 Pending{}, zst);

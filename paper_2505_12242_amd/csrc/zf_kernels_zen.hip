@@ -191,7 +191,9 @@ __global__ __launch_bounds__(kZenTotalThreads) void zen_total_kernel(const doubl
       // the position the update of this step took (it read the same state)
       const int32_t pos = (refresh || zst->ended) ? 1 : zst->length + 1;
       zst->length = pos;
-      zst->ended = (trigger || pos >= S_max || force_end) ? 1 : 0;
+      // 2: the update of this step already wrote the hand-over (fused);
+      // 1: the interval ended and waits for the hand-over pass
+      zst->ended = force_end == 2 ? 2 : (trigger || pos >= S_max || force_end) ? 1 : 0;
     }
   }
 }

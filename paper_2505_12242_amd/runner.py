@@ -119,8 +119,10 @@ class DeviceZenStep:
     ended the interval and the totals are read back from pinned host memory
     (after waiting for the step) the first time one of them is asked for."""
 
-    def __init__(self, refresh: bool, host: torch.Tensor, event: torch.cuda.Event):
+    def __init__(self, refresh: bool, host: torch.Tensor, event: torch.cuda.Event,
+                 fused: bool = False):
         self.refresh = refresh
+        self.fused = fused  # the update wrote the hand-over itself (a caller-known end)
         self._host = host
         self._event = event
         self._vals = None
@@ -334,7 +336,8 @@ class SelectiveUpdateRunner:
         if k is not None:
             length, end, tot = k.resolve()
             self._length, self._ended, self._last_totals = length, end, tot
-            self._in_stage = self.use_stage and length == 1
+            # (a fused end writes the hand-over, not the stage)
+            self._in_stage = self.use_stage and length == 1 and not k.fused
             self._zen_pending = None
 
     @property
@@ -431,12 +434,16 @@ class SelectiveUpdateRunner:
                     plan.update(self.hp, t, mode, length, self.S, pack=not adam_only, stream=st)
         elif self.zen_device:
             # the interval ends on the device (trigger, S_max) or by the
-            # caller's rule (before a refresh, warm-up steps)
+            # caller's rule (before a refresh, warm-up steps); an end the
+            # caller knows of is handed over by the update itself
+            # (channel-major, force_end 2)
             force_end = (t % self.R == 0) or t <= self.warmup
+            fused = (force_end and self.keep_unpacked and self.layout != ROW_MAJOR
+                     and self.fuse_handover)
             with rec("update_zen"):
-                plan.update_zen_device(self.hp, t, mode, self.S, force_end, self.zen_tau,
-                                       self.zen_totals, self.zen_state, stream=st)
-            if self.keep_unpacked:
+                plan.update_zen_device(self.hp, t, mode, self.S, 2 if fused else int(force_end),
+                                       self.zen_tau, self.zen_totals, self.zen_state, stream=st)
+            if self.keep_unpacked and not fused:
                 with rec("handover_zen"):
                     plan.handover_zen(self.zen_state, st)
             host = torch.empty(2 + ZEN_TOTALS_BYTES // 4, dtype=torch.int32, pin_memory=True)
@@ -445,7 +452,7 @@ class SelectiveUpdateRunner:
                 host[2:].copy_(self.zen_totals.view(torch.int32), non_blocking=True)
             ev = torch.cuda.Event()
             ev.record(st)
-            kind = DeviceZenStep(refresh, host, ev)
+            kind = DeviceZenStep(refresh, host, ev, fused)
             self._zen_pending = kind
             return kind
         else:

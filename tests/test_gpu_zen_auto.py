@@ -145,7 +145,11 @@ def run_zen(shapes, ratio, R, S_max, tau, T, seed, host_in=None, layout=None, on
             for a, b, name in ((P, orc.P, "master"), (M, orc.M, "exp_avg"),
                                (V, orc.V, "exp_avg_sq")):
                 assert same_bits(a, b), (name, q, t)
-            assert same_bits(_host(runner.acc[q], layout).numpy(), orc.A), ("acc", q, t)
+            # (an end the caller forces is handed over by the update itself,
+            # which leaves the packed buffer as it was; the hand-over below
+            # carries the sums)
+            if not (kind.interval_end and getattr(kind, "fused", False)):
+                assert same_bits(_host(runner.acc[q], layout).numpy(), orc.A), ("acc", q, t)
             wl = runner.weights[q] if layout == zf.ROW_MAJOR else runner.weights[q].t()
             assert same_bits(bits_np(wl), orc.W), ("weight", q, t)
             if kind.interval_end:
