@@ -673,11 +673,13 @@ typedef struct zf_zen_state {
  * state: length = that position; ended = trigger || position >=
  * accum_interval (S_max) || force_end.  force_end: the caller's own end of
  * the interval (the next step refreshes the selection, or a warm-up step):
- * 1 -- the hand-over is left to zf_plan_handover_zen; 2 (channel-major,
- * `unpacked` required) -- the update writes it itself, scale = fp32(1 /
+ * 1 -- the hand-over is left to zf_plan_handover_zen; 2 -- where the plan
+ * can (channel-major; row-major steps in place on the 16-byte update; every
+ * descriptor with `unpacked`) the update writes it itself, scale = fp32(1 /
  * position), bit for bit what zf_plan_handover_zen would write, and sets
  * ended = 2 so that zf_plan_handover_zen writes nothing (the packed buffer
- * is then left as it was, as in zf_plan_update_handover).  Other values:
+ * is then left as it was, as in zf_plan_update_handover); elsewhere as 1.
+ * Call zf_plan_handover_zen after every step either way.  Other values:
  * ZF_EINVAL.
  * Both layouts, plans without a full-state store; a row-major plan without
  * the bf16 stage; the requirements of zf_plan_update_zen otherwise.  Follow

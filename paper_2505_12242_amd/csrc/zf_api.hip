@@ -1400,16 +1400,22 @@ zf_status plan_update_zen(zf_plan* p, const AdamK& c, int32_t mode, int32_t firs
   const Table t{p->d_mats, p->d_off_up, p->nmats};
   const Table tz{p->d_mats, p->d_off_zen, p->nmats};
   hipError_t e;
+  // force_end 2: the interval ends here and the update writes the hand-over
+  // where it can (channel-major; row-major steps in place on the 16-byte
+  // update); elsewhere a plain end, the hand-over left to the gated pass
+  const bool rv = p->layout == zf::kRowMajor && pd == nullptr && use_rv(p->mats[0], mode, true);
+  const bool fuse = force_end == 2 && p->can_handover && zst != nullptr &&
+                    (p->layout == zf::kChannelMajor || rv);
+  if (force_end == 2 && !fuse) force_end = 1;
   if (p->layout == zf::kChannelMajor) {
-    // force_end 2: the interval ends here and the update writes the hand-over
     e = zf::launch_cm_update(t, p->mats[0], p->blk_up, c, mode, first, true, true, p->d_zs,
-                             force_end == 2, 1.0f, s, pd, zst);
+                             fuse, 1.0f, s, pd, zst);
     if (e != hipSuccess) return hip_fail(e);
     e = zf::launch_zen_finalize(tz, p->mats[0], p->blk_zen, p->d_zs, p->d_zb, s);
-  } else if (pd == nullptr && use_rv(p->mats[0], mode, true)) {
+  } else if (rv) {
     // 16-byte update with the statistics fused: only the finalize remains
     const Table tv{p->d_mats, p->d_off_upv, p->nmats};
-    e = zf::launch_rv_update(tv, p->mats[0], p->blk_upv, c, mode, first, true, true, false, 1.0f,
+    e = zf::launch_rv_update(tv, p->mats[0], p->blk_upv, c, mode, first, true, true, fuse, 1.0f,
                              s, p->d_ws, zst);
     if (e != hipSuccess) return hip_fail(e);
     const Table tp{p->d_mats, p->d_off_zp, p->nmats};
@@ -1470,9 +1476,8 @@ zf_status zf_plan_update_zen_device(zf_plan* p, const zf_adam_hparams* hp, int64
   if (accum_interval < 1 || accum_interval > INT32_MAX || state == nullptr ||
       !aligned(state, 4))
     return ZF_EINVAL;
-  // 2: end here with the hand-over fused into the update (channel-major)
+  // 2: end here with the hand-over fused into the update where the plan can
   if (force_end < 0 || force_end > 2) return ZF_EINVAL;
-  if (force_end == 2 && (p->layout != zf::kChannelMajor || !p->can_handover)) return ZF_EINVAL;
   return plan_update_zen(p, adam_consts(*hp, step), mode, 0, tau, totals, as_stream(stream),
                          nullptr, reinterpret_cast<zf::ZenState*>(state),
                          static_cast<int32_t>(accum_interval), force_end);

@@ -39,7 +39,8 @@
 // are loaded and staged in LDS like G, and the pack lanes take their
 // previous values from there instead of from A.
 //
-// STATS (Zen-auto, blocks of cn_rpb rows): each lane also sums, in fp64 and
+// STATS (Zen-auto, blocks of cn_rpb rows; with HAND on an end the caller
+// forces, the sums before the scale): each lane also sums, in fp64 and
 // in row order, the squares of its selected columns' gradient and of its
 // unselected slots' new accumulated values over the block's rows, and
 // writes one partial per virtual column (selected slot r, then unselected
@@ -120,12 +121,16 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
                                                              double* __restrict__ zs,
                                                              HistTable hist,
                                                              const ZenState* __restrict__ zst) {
-  static_assert(!STATS || (ADAM && PACK && !HAND), "statistics of the fused update");
+  static_assert(!STATS || (ADAM && PACK), "statistics of the fused update");
   static_assert(!DEF || (BATCHED && !ADAM && !PACK && !HAND && !STATS && !A16),
                 "the deferred hand-over pass");
   // Zen-auto with the interval driven on the device (steps in place):
-  // overwrite after an ended interval, else accumulate
-  if (zst != nullptr) first = uniform_i32(zst->ended) ? 1 : uniform_i32(zst->length) + 1;
+  // overwrite after an ended interval, else accumulate; HAND (an end the
+  // caller forces) hands over with scale = fp32(1 / length)
+  if (zst != nullptr) {
+    first = uniform_i32(zst->ended) ? 1 : uniform_i32(zst->length) + 1;
+    if constexpr (HAND) scale = 1.0f / static_cast<float>(first);
+  }
   __shared__ __attribute__((aligned(16))) uint16_t sg[kRvBatch][kRvMaxCols];
   __shared__ __attribute__((aligned(16))) uint16_t sa[A16 ? kRvBatch : 1][A16 ? kRvMaxCols : 8];
   __shared__ __attribute__((aligned(16))) float sd[HAND ? kRvBatch : 1][HAND ? kRvMaxCols : 4];
@@ -551,8 +556,9 @@ hipError_t launch_rv_update(const Table& t, const DevMat& one, int64_t blocks, c
   if (adam && mode != kInplace) return hipErrorInvalidValue;  // refresh: per-column kernel
   if (zst != nullptr && zs == nullptr) return hipErrorInvalidValue;  // Zen-auto steps only
   if (zs != nullptr) {
-    if (!(adam && pack) || handover) return hipErrorInvalidValue;
-    launch_rv_t<true, true, false, true>(t, one, grid, c, first, 1.0f, s, zs, zst);
+    if (!(adam && pack) || (handover && zst == nullptr)) return hipErrorInvalidValue;
+    if (handover) launch_rv_t<true, true, true, true>(t, one, grid, c, first, 1.0f, s, zs, zst);
+    else launch_rv_t<true, true, false, true>(t, one, grid, c, first, 1.0f, s, zs, zst);
   } else if (handover) launch_rv_t<true, true, true>(t, one, grid, c, first, scale, s);
   else if (adam && pack) launch_rv_t<true, true, false>(t, one, grid, c, first, 1.0f, s);
   else if (adam) launch_rv_t<true, false, false>(t, one, grid, c, first, 1.0f, s);

@@ -119,10 +119,8 @@ class DeviceZenStep:
     ended the interval and the totals are read back from pinned host memory
     (after waiting for the step) the first time one of them is asked for."""
 
-    def __init__(self, refresh: bool, host: torch.Tensor, event: torch.cuda.Event,
-                 fused: bool = False):
+    def __init__(self, refresh: bool, host: torch.Tensor, event: torch.cuda.Event):
         self.refresh = refresh
-        self.fused = fused  # the update wrote the hand-over itself (a caller-known end)
         self._host = host
         self._event = event
         self._vals = None
@@ -131,8 +129,14 @@ class DeviceZenStep:
         if self._vals is None:
             self._event.synchronize()
             raw = self._host.numpy()
-            self._vals = (int(raw[0]), bool(raw[1]), ZenTotals.from_bytes(raw[2:].tobytes()))
+            # ended: 0, 1, or 2 when the update wrote the hand-over itself
+            self._vals = (int(raw[0]), int(raw[1]), ZenTotals.from_bytes(raw[2:].tobytes()))
         return self._vals
+
+    @property
+    def fused(self) -> bool:
+        """The step ended its interval and its update wrote the hand-over."""
+        return self.resolve()[1] == 2
 
     @property
     def step_in_interval(self) -> int:
@@ -140,7 +144,7 @@ class DeviceZenStep:
 
     @property
     def interval_end(self) -> bool:
-        return self.resolve()[1]
+        return self.resolve()[1] != 0
 
     @property
     def totals(self) -> ZenTotals:
@@ -335,9 +339,9 @@ class SelectiveUpdateRunner:
         k = self._zen_pending
         if k is not None:
             length, end, tot = k.resolve()
-            self._length, self._ended, self._last_totals = length, end, tot
+            self._length, self._ended, self._last_totals = length, bool(end), tot
             # (a fused end writes the hand-over, not the stage)
-            self._in_stage = self.use_stage and length == 1 and not k.fused
+            self._in_stage = self.use_stage and length == 1 and end != 2
             self._zen_pending = None
 
     @property
@@ -435,15 +439,15 @@ class SelectiveUpdateRunner:
         elif self.zen_device:
             # the interval ends on the device (trigger, S_max) or by the
             # caller's rule (before a refresh, warm-up steps); an end the
-            # caller knows of is handed over by the update itself
-            # (channel-major, force_end 2)
+            # caller knows of is handed over by the update itself where the
+            # plan can (force_end 2; the word then says ended = 2 and the
+            # gated hand-over does nothing)
             force_end = (t % self.R == 0) or t <= self.warmup
-            fused = (force_end and self.keep_unpacked and self.layout != ROW_MAJOR
-                     and self.fuse_handover)
+            fuse = force_end and self.keep_unpacked and self.fuse_handover
             with rec("update_zen"):
-                plan.update_zen_device(self.hp, t, mode, self.S, 2 if fused else int(force_end),
+                plan.update_zen_device(self.hp, t, mode, self.S, 2 if fuse else int(force_end),
                                        self.zen_tau, self.zen_totals, self.zen_state, stream=st)
-            if self.keep_unpacked and not fused:
+            if self.keep_unpacked:
                 with rec("handover_zen"):
                     plan.handover_zen(self.zen_state, st)
             host = torch.empty(2 + ZEN_TOTALS_BYTES // 4, dtype=torch.int32, pin_memory=True)
@@ -452,7 +456,7 @@ class SelectiveUpdateRunner:
                 host[2:].copy_(self.zen_totals.view(torch.int32), non_blocking=True)
             ev = torch.cuda.Event()
             ev.record(st)
-            kind = DeviceZenStep(refresh, host, ev, fused)
+            kind = DeviceZenStep(refresh, host, ev)
             self._zen_pending = kind
             return kind
         else:
