@@ -403,21 +403,19 @@ void set_rv(DevMat& d, int rows, bool allow) {
 void finish_geometry(DevMat& d, int cn_rows, int up_rows) {
   set_geometry(d, cn_rows, up_rows);
   if (d.layout == zf::kChannelMajor) {
-    // groups per thread: the larger of 1..kCmVpt that fills at least as many
-    // lanes of the last chunk (fewer, fuller blocks)
-    int best = 1;
-    double best_fill = 0.0;
-    for (int v = 1; v <= zf::kCmVpt; ++v) {
-      const int64_t chunk = static_cast<int64_t>(v) * zf::kThreads * 8;
+    // quads per thread in the full-grid passes: kCmQpt when it fills at
+    // least as many lanes of the last chunk as kCmQpt / 2 does (fewer,
+    // fuller blocks), else kCmQpt / 2; the selected-only Adam grid takes one
+    // quad per thread
+    const auto fill = [&](int v) {
+      const int64_t chunk = static_cast<int64_t>(v) * zf::kThreads * 4;
       const int64_t nch = std::max<int64_t>(1, ceil_div(d.n, chunk));
-      const double fill = static_cast<double>(d.n) / static_cast<double>(nch * chunk);
-      if (fill >= best_fill - 1e-12) {
-        best = v;
-        best_fill = fill;
-      }
-    }
-    d.cm_vpt = best;
-    d.cm_nch = d.n > 0 ? static_cast<int32_t>(ceil_div(d.n, int64_t(best) * zf::kThreads * 8)) : 0;
+      return static_cast<double>(d.n) / static_cast<double>(nch * chunk);
+    };
+    const int best = fill(zf::kCmQpt) >= fill(zf::kCmQpt / 2) - 1e-12 ? zf::kCmQpt : zf::kCmQpt / 2;
+    d.cm_qpt = best;
+    d.cm_nch = d.n > 0 ? static_cast<int32_t>(ceil_div(d.n, int64_t(best) * zf::kThreads * 4)) : 0;
+    d.cm_snch = d.n > 0 ? static_cast<int32_t>(ceil_div(d.n, int64_t(zf::kCmSelChunk))) : 0;
     d.cm_unch = d.n > 0 ? static_cast<int32_t>(ceil_div(d.n, zf::kCmUnpackChunk)) : 0;
     d.vec = cm_vec_ok(d) ? 1 : 0;
     const auto al16 = [](const void* p, int64_t ld) {
@@ -1029,7 +1027,7 @@ zf_status build_plan_impl(const zf_matrix* mats, int32_t nmats, zf_plan* p) {
     p->blk_top += 1;
     p->blk_up += update_grid(d);
     if (d.rv) p->blk_upv += rv_grid(d);
-    if (cm) p->blk_sel += d.k * static_cast<int64_t>(d.cm_nch);
+    if (cm) p->blk_sel += d.k * static_cast<int64_t>(d.cm_snch);
     p->has_store = p->has_store || d.st_P != nullptr;
     p->blk_unp += unpack_grid(d);
     p->mats[q] = d;
@@ -1043,10 +1041,12 @@ zf_status build_plan_impl(const zf_matrix* mats, int32_t nmats, zf_plan* p) {
   off_zp[nmats] = p->blk_zp;
   off_upv[nmats] = p->blk_upv;
   off_sel[nmats] = p->blk_sel;
-  const int64_t max_blocks = (int64_t(1) << 31) / zf::kThreads;
-  if (p->blk_cn >= max_blocks || p->blk_up >= max_blocks || p->blk_unp >= max_blocks ||
-      p->blk_upv >= max_blocks || p->blk_sel >= max_blocks ||
-      p->blk_zp >= max_blocks)
+  // one launch holds at most 2^32 - 1 work-items in x (the dispatch
+  // packet's grid size is a 32-bit count of work-items)
+  const int64_t max_blocks = ((int64_t(1) << 32) - 1) / zf::kThreads;
+  if (p->blk_cn > max_blocks || p->blk_up > max_blocks || p->blk_unp > max_blocks ||
+      p->blk_upv > max_blocks || p->blk_sel > max_blocks ||
+      p->blk_zp > max_blocks)
     return ZF_EINVAL;  // grid too large for one launch
 
   const size_t mats_bytes = sizeof(DevMat) * nmats;
@@ -1310,7 +1310,7 @@ zf_status zf_plan_update_handover_deferred(zf_plan* p, const zf_adam_hparams* hp
       const DevMat& a = e->mats[q];
       const DevMat& b = p->mats[q];
       if (a.n != b.n || a.m != b.m || a.k != b.k) return ZF_EINVAL;
-      if (cm && (a.vec != b.vec || a.cm_vpt != b.cm_vpt || a.cm_nch != b.cm_nch))
+      if (cm && (a.vec != b.vec || a.cm_qpt != b.cm_qpt || a.cm_nch != b.cm_nch || a.cm_snch != b.cm_snch))
         return ZF_EINVAL;
       if (b.n * (b.m - b.k) > 0 && a.grad == nullptr) return ZF_EINVAL;
       if (!cm) {

@@ -32,6 +32,16 @@ __device__ __forceinline__ int32_t uniform_i32(int32_t x) {
   return __builtin_amdgcn_readfirstlane(x);
 }
 
+// A plan's device tables (matrix descriptors, block offsets) are written by
+// the host before a launch and only read by the kernels.  Reading one
+// through the constant address space lets the compiler use scalar loads:
+// the values land in scalar registers without waiting for the vector loads
+// in flight, and buffer resources built from them need no per-lane loop.
+template <typename T>
+__device__ __forceinline__ const __attribute__((address_space(4))) T* const_table(const T* p) {
+  return (const __attribute__((address_space(4))) T*)(p);
+}
+
 // Number of set bits of `mask` at lane positions below the calling lane.
 __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
   return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
@@ -133,6 +143,17 @@ __device__ __forceinline__ u32x4 buf_b128(rsrc_t r, uint32_t voff, uint32_t soff
 template <int AUX = kCached>
 __device__ __forceinline__ void buf_put_b128(u32x4 v, rsrc_t r, uint32_t voff, uint32_t soff) {
   __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, soff, AUX);
+}
+
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+template <int AUX = kCached>
+__device__ __forceinline__ u32x2 buf_b64(rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, AUX);
+}
+template <int AUX = kCached>
+__device__ __forceinline__ void buf_put_b64(u32x2 v, rsrc_t r, uint32_t voff, uint32_t soff) {
+  __builtin_amdgcn_raw_buffer_store_b64(v, r, voff, soff, AUX);
 }
 
 // One Adam/AdamW element update; each line is one fp32 operation (the

@@ -24,19 +24,26 @@ constexpr int kTopkThreads = 1024;
 constexpr int kRvMaxCols = 1000;
 
 // Channel-major layout: an update block covers one channel and
-// cm_vpt * kThreads * 8 of its rows (cm_vpt 16-byte groups per thread, at
-// most kCmVpt, chosen per matrix to fill the lanes), an unpack block one
+// cm_qpt * kThreads * 4 of its rows (cm_qpt quads of 4 elements per thread,
+// kCmQpt / 2 or kCmQpt, chosen per matrix to fill the lanes); a block of the
+// Adam grid over the selected channels alone one channel and kThreads * 4
+// rows (one quad per thread; cm_snch chunks per channel); an unpack block one
 // channel and kCmUnpackChunk rows; a colnorm block covers kThreads / 64
-// channels, one per wave.
-#ifndef ZF_CM_VPT
-#define ZF_CM_VPT 2
+// channels, one per wave.  Measured on MI355X: the Adam-only pass is fastest
+// with one quad per thread, the passes that pack or sum the unselected
+// channels (two or three streams of 8 or 16 bytes per quad) need two to four
+// quads per thread in flight.
+#ifndef ZF_CM_QPT
+#define ZF_CM_QPT 4
 #endif
-#ifndef ZF_CM_UNPACK_VPT
-#define ZF_CM_UNPACK_VPT 1
+#ifndef ZF_CM_UNPACK_QPT
+#define ZF_CM_UNPACK_QPT 2
 #endif
-constexpr int kCmVpt = ZF_CM_VPT;
-constexpr int kCmUnpackVpt = ZF_CM_UNPACK_VPT;
-constexpr int kCmUnpackChunk = kThreads * 8 * kCmUnpackVpt;
+constexpr int kCmQpt = ZF_CM_QPT;
+static_assert(kCmQpt >= 2 && kCmQpt % 2 == 0, "two quad counts per thread: kCmQpt / 2 and kCmQpt");
+constexpr int kCmUnpackQpt = ZF_CM_UNPACK_QPT;
+constexpr int kCmUnpackChunk = kThreads * 4 * kCmUnpackQpt;
+constexpr int kCmSelChunk = kThreads * 4;  // rows per block of the selected-only Adam grid
 constexpr int kCmColnormCols = kThreads / 64;
 constexpr int kCmWaves = kThreads / 64;  // waves per update block (one statistics partial each)
 
@@ -101,7 +108,8 @@ struct DevMat {
   int32_t layout;    // Layout
   int32_t cm_nch;    // channel-major: row chunks per channel (update)
   int32_t cm_unch;   // channel-major: row chunks per channel (unpack)
-  int32_t cm_vpt;    // channel-major: 16-byte groups per thread in the update (1 or 2)
+  int32_t cm_qpt;    // channel-major: quads (4 elements) per thread in the update (kCmQpt / 2 or kCmQpt)
+  int32_t cm_snch;   // channel-major: row chunks per channel of the selected-only Adam grid
   int32_t scat_vec;  // channel-major: 16-byte path of the weight scatter
   int32_t rv;        // row-major: the 16-byte update kernel is used (else per-column)
   int32_t rv_w;      // row-major 16-byte update: tile width (columns)
@@ -231,8 +239,8 @@ hipError_t launch_cm_handover_deferred(const Table& t, const DevMat& one, int64_
 // every matrix of the table has one).
 hipError_t launch_cm_unpack(const Table& t, const DevMat& one, int64_t blocks, float scale,
                             hipStream_t s, bool from_stage = false);
-// Adam only over a grid of the selected channels alone (cm_nch blocks per
-// selected channel; table offsets over sum(k * cm_nch)); for plans without
+// Adam only over a grid of the selected channels alone (cm_snch blocks per
+// selected channel; table offsets over sum(k * cm_snch)); for plans without
 // a full-state store (nothing to do for the unselected channels).
 // zero_out: also +0.0 into the selected channels' rows of `out` (after the
 // score pass wrote the hand-over of a one-step interval).

@@ -745,7 +745,7 @@ __global__ __launch_bounds__(kThreads) void rm_handover_deferred_kernel(
   for (int32_t i = 0; i < rows; ++i) {
     float a = 0.0f;
     for (int32_t st = 0; st < hist.n; ++st) {
-      const DevMat& hd = hist.mats[st][q];
+      const auto& hd = const_table(hist.mats[st])[q];
       const rsrc_t rE = rows_rsrc(hd.grad, i0, i1, hd.ld_grad, d.m);
       const float g = widen_bf16(buf_u16<kStream>(
           rE, vG, static_cast<uint32_t>(i) * static_cast<uint32_t>(hd.ld_grad * 2)));

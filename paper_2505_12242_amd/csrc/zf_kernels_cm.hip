@@ -7,17 +7,17 @@
 // values.  The compact states are [k][ld_state >= n] (slot r = channel
 // sel_idx[r]), the packed buffer [m-k][ld_acc >= n] (slot u = channel
 // unsel_idx[u]) and the hand-over buffer [m][ld_out >= n].  Every access of
-// the hot path is then a contiguous 16-byte-per-lane stream, and the bf16
-// write-back writes whole cache lines.
+// the hot path is then a contiguous stream, and the bf16 write-back writes
+// whole cache lines.
 //
 // Work unit of update / unpack: one channel x one chunk of its rows.
 // Whether the channel is selected, and its slot, are uniform per block, so
 // a block is either an Adam block or a pack block.  A block's buffer
-// resources cover exactly its chunk, so 16-byte groups past the end of a
-// channel (the last chunk) read zeros and their stores are dropped by the
-// hardware range check; the loops carry no per-group conditions.  The vector
-// path requires n % 8 == 0 and 16-byte aligned rows (DevMat::vec); other
-// shapes take an element-wise path.
+// resources cover exactly its chunk, so quads past the end of a channel (the
+// last chunk) read zeros and their stores are dropped by the hardware range
+// check; the loops carry no per-quad conditions.  The vector path requires
+// n % 8 == 0 and 16-byte aligned rows (DevMat::vec); other shapes take an
+// element-wise path.
 #include "zf_device.hpp"
 
 namespace zf {
@@ -66,25 +66,6 @@ __device__ __forceinline__ void widen8(u32x4 v, float (&f)[kGroup]) {
   }
 }
 
-__device__ __forceinline__ u32x4 narrow8(const float (&f)[kGroup]) {
-  u32x4 v;
-  v.x = static_cast<uint32_t>(round_bf16(f[0])) | (static_cast<uint32_t>(round_bf16(f[1])) << 16);
-  v.y = static_cast<uint32_t>(round_bf16(f[2])) | (static_cast<uint32_t>(round_bf16(f[3])) << 16);
-  v.z = static_cast<uint32_t>(round_bf16(f[4])) | (static_cast<uint32_t>(round_bf16(f[5])) << 16);
-  v.w = static_cast<uint32_t>(round_bf16(f[6])) | (static_cast<uint32_t>(round_bf16(f[7])) << 16);
-  return v;
-}
-
-template <int AUX>
-__device__ __forceinline__ void f32x8_load(rsrc_t r, uint32_t byte_off, float (&f)[kGroup]) {
-  const u32x4 a = buf_b128<AUX>(r, byte_off, 0);
-  const u32x4 b = buf_b128<AUX>(r, byte_off + 16, 0);
-  f[0] = __uint_as_float(a.x); f[1] = __uint_as_float(a.y);
-  f[2] = __uint_as_float(a.z); f[3] = __uint_as_float(a.w);
-  f[4] = __uint_as_float(b.x); f[5] = __uint_as_float(b.y);
-  f[6] = __uint_as_float(b.z); f[7] = __uint_as_float(b.w);
-}
-
 template <int AUX>
 __device__ __forceinline__ void f32x8_store(rsrc_t r, uint32_t byte_off, const float (&f)[kGroup]) {
   u32x4 a, b;
@@ -96,16 +77,56 @@ __device__ __forceinline__ void f32x8_store(rsrc_t r, uint32_t byte_off, const f
   buf_put_b128<AUX>(b, r, byte_off + 16, 0);
 }
 
-// Byte offset, within the block's chunk, of group g of thread tid.
-__device__ __forceinline__ uint32_t group_elem(int g, int tid) {
-  return static_cast<uint32_t>((g * kThreads + tid) * kGroup);
+// The vector paths of the update, the deferred hand-over and the unpack
+// work in quads: 4 consecutive elements per lane access (8 bytes of bf16,
+// 16 of fp32), quad q of thread tid at elements (q * kThreads + tid) * 4 of
+// the block's chunk.  The 64 lanes of a wave then touch 256 consecutive
+// elements with every load and store, whole cache lines of each stream.  (A
+// lane holding 8 consecutive fp32 values splits them over two accesses that
+// each fill half of every line they touch; the quads measured 5-10% faster
+// on MI355X, together with chunks of one quad per lane.)
+constexpr int kQuad = 4;
+
+__device__ __forceinline__ uint32_t quad_elem(int q, int tid) {
+  return static_cast<uint32_t>((q * kThreads + tid) * kQuad);
 }
 
-// ss += x^2 over eight fp32 values, in fp64 (squares of fp32 values are
-// exact in fp64).
-__device__ __forceinline__ void sum_squares8(const float (&f)[kGroup], double& ss) {
+// bf16 x 4 (two dwords) -> fp32 x 4
+__device__ __forceinline__ void widen4(u32x2 v, float (&f)[kQuad]) {
+  f[0] = __uint_as_float(v.x << 16);
+  f[1] = __uint_as_float(v.x & 0xffff0000u);
+  f[2] = __uint_as_float(v.y << 16);
+  f[3] = __uint_as_float(v.y & 0xffff0000u);
+}
+
+__device__ __forceinline__ u32x2 narrow4(const float (&f)[kQuad]) {
+  u32x2 v;
+  v.x = static_cast<uint32_t>(round_bf16(f[0])) | (static_cast<uint32_t>(round_bf16(f[1])) << 16);
+  v.y = static_cast<uint32_t>(round_bf16(f[2])) | (static_cast<uint32_t>(round_bf16(f[3])) << 16);
+  return v;
+}
+
+template <int AUX>
+__device__ __forceinline__ void f32x4_load(rsrc_t r, uint32_t byte_off, float (&f)[kQuad]) {
+  const u32x4 a = buf_b128<AUX>(r, byte_off, 0);
+  f[0] = __uint_as_float(a.x); f[1] = __uint_as_float(a.y);
+  f[2] = __uint_as_float(a.z); f[3] = __uint_as_float(a.w);
+}
+
+template <int AUX>
+__device__ __forceinline__ void f32x4_store(rsrc_t r, uint32_t byte_off, const float (&f)[kQuad]) {
+  u32x4 a;
+  a.x = __float_as_uint(f[0]); a.y = __float_as_uint(f[1]);
+  a.z = __float_as_uint(f[2]); a.w = __float_as_uint(f[3]);
+  buf_put_b128<AUX>(a, r, byte_off, 0);
+}
+
+// ss += x^2 over fp32 values, in fp64 (squares of fp32 values are exact in
+// fp64).
+template <int N>
+__device__ __forceinline__ void sum_squares(const float (&f)[N], double& ss) {
 #pragma unroll
-  for (int i = 0; i < kGroup; ++i)
+  for (int i = 0; i < N; ++i)
     ss = __builtin_fma(static_cast<double>(f[i]), static_cast<double>(f[i]), ss);
 }
 
@@ -131,7 +152,10 @@ __global__ __launch_bounds__(kThreads) void cm_colnorm_kernel(const DevMat* __re
   int64_t local;
   const DevMat d = get_mat<BATCHED>(mats, off, nmats, one, local);
   const int lane = threadIdx.x & 63;
-  const int64_t j = local * (kThreads / 64) + (threadIdx.x >> 6);
+  // the wave's channel, moved to scalar registers (it is wave-uniform, which
+  // the compiler cannot tell from threadIdx.x; without this every buffer
+  // access of the wave sits in a per-lane loop)
+  const int64_t j = local * (kThreads / 64) + uniform_i32(threadIdx.x >> 6);
   if (j >= d.m) return;
   const int64_t n = d.n;
   const rsrc_t r = make_rsrc(d.grad + j * d.ld_grad, n * 2);
@@ -140,16 +164,21 @@ __global__ __launch_bounds__(kThreads) void cm_colnorm_kernel(const DevMat* __re
   const rsrc_t rO = OUT == 2 ? make_rsrc(d.out + j * d.ld_out, n * 4) : r;
   double a0 = 0.0, a1 = 0.0;
   if (d.vec) {
+    // A pass covers 4 loads of kStride rows; its base is wave-uniform, so
+    // the loop is too.  Groups past n read zeros (resource range), add +0.0
+    // to the sums and their stores are dropped: each lane adds its groups in
+    // row order, as a loop over its own groups would.
     constexpr int kStride = 64 * kGroup;  // elements per wave per load
-    int64_t e = static_cast<int64_t>(lane) * kGroup;
-    for (; e + 3 * kStride < n; e += 4 * kStride) {
+    const int64_t lo = static_cast<int64_t>(lane) * kGroup;
+    for (int64_t e0 = 0; e0 < n; e0 += 4 * kStride) {
       u32x4 v[4];
 #pragma unroll
-      for (int b = 0; b < 4; ++b) v[b] = buf_b128<kAuxScore>(r, static_cast<uint32_t>((e + b * kStride) * 2), 0);
+      for (int b = 0; b < 4; ++b)
+        v[b] = buf_b128<kAuxScore>(r, static_cast<uint32_t>((e0 + b * kStride + lo) * 2), 0);
       if (st) {
 #pragma unroll
         for (int b = 0; b < 4; ++b)
-          buf_put_b128<kAuxAFirst>(v[b], rS, static_cast<uint32_t>((e + b * kStride) * 2), 0);
+          buf_put_b128<kAuxAFirst>(v[b], rS, static_cast<uint32_t>((e0 + b * kStride + lo) * 2), 0);
       }
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
@@ -163,24 +192,8 @@ __global__ __launch_bounds__(kThreads) void cm_colnorm_kernel(const DevMat* __re
         if constexpr (OUT == 2) {
 #pragma unroll
           for (int c = 0; c < kGroup; ++c) f[c] = f[c] * scale;
-          f32x8_store<kAuxWO>(rO, static_cast<uint32_t>((e + b * kStride) * 4), f);
+          f32x8_store<kAuxWO>(rO, static_cast<uint32_t>((e0 + b * kStride + lo) * 4), f);
         }
-      }
-    }
-    for (; e < n; e += kStride) {
-      float f[kGroup];
-      const u32x4 v = buf_b128<kAuxScore>(r, static_cast<uint32_t>(e * 2), 0);
-      if (st) buf_put_b128<kAuxAFirst>(v, rS, static_cast<uint32_t>(e * 2), 0);
-      widen8(v, f);
-#pragma unroll
-      for (int c = 0; c < kGroup; c += 2) {
-        a0 = __builtin_fma(static_cast<double>(f[c]), static_cast<double>(f[c]), a0);
-        a1 = __builtin_fma(static_cast<double>(f[c + 1]), static_cast<double>(f[c + 1]), a1);
-      }
-      if constexpr (OUT == 2) {
-#pragma unroll
-        for (int c = 0; c < kGroup; ++c) f[c] = f[c] * scale;
-        f32x8_store<kAuxWO>(rO, static_cast<uint32_t>(e * 4), f);
       }
     }
   } else {
@@ -207,48 +220,49 @@ __global__ __launch_bounds__(kThreads) void cm_colnorm_kernel(const DevMat* __re
 // with gradient pd.scale * (row rPA of the previous interval's sums).
 enum CmSrc { kCmInplace = 0, kCmPrev, kCmInitW, kCmInitMaster, kCmPend };
 
-// Adam over one chunk of channel j (slot r), vector path.  SRC picks where
-// (p, m, v) come from; rS* are the source rows (the slot's own rows in place).
-template <int SRC, int VPT, bool STATS>
+// Adam over one chunk of channel j (slot r), vector path (QPT quads per
+// lane).  SRC picks where (p, m, v) come from; rS* are the source rows (the
+// slot's own rows in place).
+template <int SRC, int QPT, bool STATS>
 __device__ __forceinline__ void cm_adam_vec(rsrc_t rG, rsrc_t rP, rsrc_t rM, rsrc_t rV,
                                             rsrc_t rW, rsrc_t rSP, rsrc_t rSM, rsrc_t rSV,
                                             rsrc_t rI, const AdamK& c, double& ss,
                                             rsrc_t rPA = rsrc_t(), const Pending* pd = nullptr) {
   const int tid = threadIdx.x;
-  float g[VPT][kGroup], p[VPT][kGroup], m[VPT][kGroup], v[VPT][kGroup];
-  u32x4 gv[VPT];
+  float g[QPT][kQuad], p[QPT][kQuad], m[QPT][kQuad], v[QPT][kQuad];
+  u32x2 gv[QPT];
 #pragma unroll
-  for (int q = 0; q < VPT; ++q) gv[q] = buf_b128<kAuxRO>(rG, group_elem(q, tid) * 2, 0);
+  for (int q = 0; q < QPT; ++q) gv[q] = buf_b64<kAuxRO>(rG, quad_elem(q, tid) * 2, 0);
 #pragma unroll
-  for (int q = 0; q < VPT; ++q) {
-    const uint32_t e = group_elem(q, tid);
+  for (int q = 0; q < QPT; ++q) {
+    const uint32_t e = quad_elem(q, tid);
     if constexpr (SRC == kCmInplace || SRC == kCmPrev || SRC == kCmPend) {
-      f32x8_load<kAuxRMW>(rSP, e * 4, p[q]);
-      f32x8_load<kAuxRMW>(rSM, e * 4, m[q]);
-      f32x8_load<kAuxRMW>(rSV, e * 4, v[q]);
+      f32x4_load<kAuxRMW>(rSP, e * 4, p[q]);
+      f32x4_load<kAuxRMW>(rSM, e * 4, m[q]);
+      f32x4_load<kAuxRMW>(rSV, e * 4, v[q]);
       if constexpr (SRC == kCmPend) {
-        f32x8_load<kAuxRO>(rPA, e * 4, g[q]);
+        f32x4_load<kAuxRO>(rPA, e * 4, g[q]);
 #pragma unroll
-        for (int i = 0; i < kGroup; ++i) adam_step(g[q][i] * pd->scale, p[q][i], m[q][i], v[q][i], pd->c);
+        for (int i = 0; i < kQuad; ++i) adam_step(g[q][i] * pd->scale, p[q][i], m[q][i], v[q][i], pd->c);
       }
     } else {
-      if constexpr (SRC == kCmInitMaster) f32x8_load<kAuxRO>(rI, e * 4, p[q]);
-      else widen8(buf_b128<kAuxRO>(rI, e * 2, 0), p[q]);
+      if constexpr (SRC == kCmInitMaster) f32x4_load<kAuxRO>(rI, e * 4, p[q]);
+      else widen4(buf_b64<kAuxRO>(rI, e * 2, 0), p[q]);
 #pragma unroll
-      for (int i = 0; i < kGroup; ++i) m[q][i] = v[q][i] = 0.0f;
+      for (int i = 0; i < kQuad; ++i) m[q][i] = v[q][i] = 0.0f;
     }
   }
 #pragma unroll
-  for (int q = 0; q < VPT; ++q) {
-    widen8(gv[q], g[q]);
-    if constexpr (STATS) sum_squares8(g[q], ss);
+  for (int q = 0; q < QPT; ++q) {
+    widen4(gv[q], g[q]);
+    if constexpr (STATS) sum_squares(g[q], ss);
 #pragma unroll
-    for (int i = 0; i < kGroup; ++i) adam_step(g[q][i], p[q][i], m[q][i], v[q][i], c);
-    const uint32_t e = group_elem(q, tid);
-    f32x8_store<kAuxRMW>(rP, e * 4, p[q]);
-    f32x8_store<kAuxRMW>(rM, e * 4, m[q]);
-    f32x8_store<kAuxRMW>(rV, e * 4, v[q]);
-    buf_put_b128<kAuxW>(narrow8(p[q]), rW, e * 2, 0);
+    for (int i = 0; i < kQuad; ++i) adam_step(g[q][i], p[q][i], m[q][i], v[q][i], c);
+    const uint32_t e = quad_elem(q, tid);
+    f32x4_store<kAuxRMW>(rP, e * 4, p[q]);
+    f32x4_store<kAuxRMW>(rM, e * 4, m[q]);
+    f32x4_store<kAuxRMW>(rV, e * 4, v[q]);
+    buf_put_b64<kAuxW>(narrow4(p[q]), rW, e * 2, 0);
   }
 }
 
@@ -291,39 +305,39 @@ __device__ __forceinline__ void cm_adam_elem(rsrc_t rG, rsrc_t rP, rsrc_t rM, rs
 // the gradient's own bits into the stage instead of fp32 into A; 2 -- the
 // second step reads the previous values from the stage (widened, the same
 // fp32 values) instead of from A.
-template <bool FIRST, int VPT, bool STATS, bool HAND = false, int A16 = 0>
+template <bool FIRST, int QPT, bool STATS, bool HAND = false, int A16 = 0>
 __device__ __forceinline__ void cm_pack_vec(rsrc_t rG, rsrc_t rA, double& ss,
                                             rsrc_t rOut = rsrc_t(), float scale = 1.0f,
                                             rsrc_t rA16 = rsrc_t()) {
   const int tid = threadIdx.x;
-  u32x4 gv[VPT];
-  float a[VPT][kGroup];
+  u32x2 gv[QPT];
+  float a[QPT][kQuad];
 #pragma unroll
-  for (int q = 0; q < VPT; ++q) gv[q] = buf_b128<kAuxRO>(rG, group_elem(q, tid) * 2, 0);
+  for (int q = 0; q < QPT; ++q) gv[q] = buf_b64<kAuxRO>(rG, quad_elem(q, tid) * 2, 0);
   if constexpr (!FIRST) {
     if constexpr (A16 == 2) {
 #pragma unroll
-      for (int q = 0; q < VPT; ++q) widen8(buf_b128<kAuxRO>(rA16, group_elem(q, tid) * 2, 0), a[q]);
+      for (int q = 0; q < QPT; ++q) widen4(buf_b64<kAuxRO>(rA16, quad_elem(q, tid) * 2, 0), a[q]);
     } else {
 #pragma unroll
-      for (int q = 0; q < VPT; ++q) f32x8_load<kAuxRMW>(rA, group_elem(q, tid) * 4, a[q]);
+      for (int q = 0; q < QPT; ++q) f32x4_load<kAuxRMW>(rA, quad_elem(q, tid) * 4, a[q]);
     }
   }
 #pragma unroll
-  for (int q = 0; q < VPT; ++q) {
-    float g[kGroup];
-    widen8(gv[q], g);
+  for (int q = 0; q < QPT; ++q) {
+    float g[kQuad];
+    widen4(gv[q], g);
 #pragma unroll
-    for (int i = 0; i < kGroup; ++i) a[q][i] = FIRST ? g[i] : a[q][i] + g[i];
-    if constexpr (STATS) sum_squares8(a[q], ss);
+    for (int i = 0; i < kQuad; ++i) a[q][i] = FIRST ? g[i] : a[q][i] + g[i];
+    if constexpr (STATS) sum_squares(a[q], ss);
     if constexpr (HAND) {
 #pragma unroll
-      for (int i = 0; i < kGroup; ++i) a[q][i] = a[q][i] * scale;
-      f32x8_store<kAuxWO>(rOut, group_elem(q, tid) * 4, a[q]);
+      for (int i = 0; i < kQuad; ++i) a[q][i] = a[q][i] * scale;
+      f32x4_store<kAuxWO>(rOut, quad_elem(q, tid) * 4, a[q]);
     } else if constexpr (FIRST && A16 == 1) {
-      buf_put_b128<kAuxAFirst>(gv[q], rA16, group_elem(q, tid) * 2, 0);
+      buf_put_b64<kAuxAFirst>(gv[q], rA16, quad_elem(q, tid) * 2, 0);
     } else {
-      f32x8_store<FIRST ? kAuxAFirst : kAuxRMW>(rA, group_elem(q, tid) * 4, a[q]);
+      f32x4_store<FIRST ? kAuxAFirst : kAuxRMW>(rA, quad_elem(q, tid) * 4, a[q]);
     }
   }
 }
@@ -348,30 +362,39 @@ __device__ __forceinline__ void cm_pack_elem(rsrc_t rG, rsrc_t rA, int64_t len, 
   }
 }
 
-template <int SRC, bool STATS>
-__device__ __forceinline__ void cm_adam_vec_any(int vpt, rsrc_t rG, rsrc_t rP, rsrc_t rM,
+// The vector paths at a matrix's quads per lane: cm_qpt (kCmQpt / 2 or
+// kCmQpt) in the full-grid passes; ONE: one quad (the selected-only Adam
+// grid).
+template <int SRC, bool STATS, bool ONE = false>
+__device__ __forceinline__ void cm_adam_vec_any(int qpt, rsrc_t rG, rsrc_t rP, rsrc_t rM,
                                                 rsrc_t rV, rsrc_t rW, rsrc_t rSP, rsrc_t rSM,
                                                 rsrc_t rSV, rsrc_t rI, const AdamK& c,
                                                 double& ss, rsrc_t rPA = rsrc_t(),
                                                 const Pending* pd = nullptr) {
-  if (vpt >= 2) cm_adam_vec<SRC, kCmVpt, STATS>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss, rPA, pd);
-  else cm_adam_vec<SRC, 1, STATS>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss, rPA, pd);
+  if constexpr (ONE)
+    cm_adam_vec<SRC, 1, STATS>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss, rPA, pd);
+  else if (qpt >= kCmQpt)
+    cm_adam_vec<SRC, kCmQpt, STATS>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss, rPA, pd);
+  else
+    cm_adam_vec<SRC, kCmQpt / 2, STATS>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss, rPA, pd);
 }
 
 template <bool FIRST, bool STATS, bool HAND = false, int A16 = 0>
-__device__ __forceinline__ void cm_pack_vec_any(int vpt, rsrc_t rG, rsrc_t rA, double& ss,
+__device__ __forceinline__ void cm_pack_vec_any(int qpt, rsrc_t rG, rsrc_t rA, double& ss,
                                                 rsrc_t rOut = rsrc_t(), float scale = 1.0f,
                                                 rsrc_t rA16 = rsrc_t()) {
-  if (vpt >= 2) cm_pack_vec<FIRST, kCmVpt, STATS, HAND, A16>(rG, rA, ss, rOut, scale, rA16);
-  else cm_pack_vec<FIRST, 1, STATS, HAND, A16>(rG, rA, ss, rOut, scale, rA16);
+  if (qpt >= kCmQpt)
+    cm_pack_vec<FIRST, kCmQpt, STATS, HAND, A16>(rG, rA, ss, rOut, scale, rA16);
+  else
+    cm_pack_vec<FIRST, kCmQpt / 2, STATS, HAND, A16>(rG, rA, ss, rOut, scale, rA16);
 }
 
 // HAND: a selected channel's row of the hand-over buffer is +0.0.
 __device__ __forceinline__ void cm_zero_rows(const DevMat& d, rsrc_t rOut, int64_t len) {
   if (d.vec) {
-    const float z[kGroup] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int64_t g = threadIdx.x; g * kGroup < len; g += kThreads)
-      f32x8_store<kAuxWO>(rOut, static_cast<uint32_t>(g * kGroup * 4), z);
+    const float z[kQuad] = {0.f, 0.f, 0.f, 0.f};
+    for (int64_t g = threadIdx.x; g * kQuad < len; g += kThreads)
+      f32x4_store<kAuxWO>(rOut, static_cast<uint32_t>(g * kQuad * 4), z);
   } else {
     for (int64_t e = threadIdx.x; e < len; e += kThreads)
       buf_put_f32<kAuxWO>(0.0f, rOut, static_cast<uint32_t>(e) * 4, 0);
@@ -393,13 +416,13 @@ __device__ __forceinline__ void cm_swap_out(const DevMat& d, int64_t j, int64_t 
                          make_rsrc(d.st_M + j * d.ld_store + e0, len * 4),
                          make_rsrc(d.st_V + j * d.ld_store + e0, len * 4)};
   if (d.vec) {
-    for (int64_t g = threadIdx.x; g * kGroup < len; g += kThreads) {
-      const uint32_t o = static_cast<uint32_t>(g * kGroup * 4);
+    for (int64_t g = threadIdx.x; g * kQuad < len; g += kThreads) {
+      const uint32_t o = static_cast<uint32_t>(g * kQuad * 4);
 #pragma unroll
       for (int a = 0; a < 3; ++a) {
-        float f[kGroup];
-        f32x8_load<kAuxRO>(src[a], o, f);
-        f32x8_store<kAuxWO>(dst[a], o, f);
+        float f[kQuad];
+        f32x4_load<kAuxRO>(src[a], o, f);
+        f32x4_store<kAuxWO>(dst[a], o, f);
       }
     }
   } else {
@@ -467,23 +490,26 @@ __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(c
   }
   int64_t local;
   const DevMat& d = get_mat<BATCHED>(mats, off, nmats, one, local);
-  const int64_t chunk = static_cast<int64_t>(d.cm_vpt) * kThreads * kGroup;
+  // SELG: one quad per lane, cm_snch chunks per channel; else cm_qpt quads
+  const int32_t qpt = SELG ? 1 : d.cm_qpt;
+  const int64_t nch = SELG ? d.cm_snch : d.cm_nch;
+  const int64_t chunk = static_cast<int64_t>(qpt) * kThreads * kQuad;
   int64_t j, r;
   bool sel;
   if constexpr (SELG) {
-    r = local / d.cm_nch;
+    r = local / nch;
     // the channel comes from the caller's selection: kept inside the matrix
     // whatever it holds, so that every address stays in its buffer
     j = min(max(static_cast<int64_t>(uniform_i32(d.sel_idx[r])), int64_t(0)), d.m - 1);
     sel = true;
   } else {
-    j = local / d.cm_nch;
+    j = local / nch;
     const uint64_t mj = uniform_u64(d.mask[j >> 6]);
     sel = (mj >> (j & 63)) & 1ull;
     r = static_cast<int64_t>(uniform_i32(d.prefix[j >> 6])) +
         __popcll(mj & ((uint64_t(1) << (j & 63)) - 1));
   }
-  const int64_t ci = local % d.cm_nch;
+  const int64_t ci = local % nch;
   const int64_t e0 = ci * chunk;
   const int64_t len = min(chunk, d.n - e0);
   const int64_t w = j >> 6;
@@ -503,10 +529,10 @@ __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(c
       if constexpr (HAND) {
         const rsrc_t rOut = make_rsrc(d.out + j * d.ld_out + e0, len * 4);
         if (d.vec) {
-          if (ph == 1) cm_pack_vec_any<true, STATS, true>(d.cm_vpt, rG, rA, ss, rOut, scale);
+          if (ph == 1) cm_pack_vec_any<true, STATS, true>(d.cm_qpt, rG, rA, ss, rOut, scale);
           else if (a16 && ph == 2)
-            cm_pack_vec_any<false, STATS, true, 2>(d.cm_vpt, rG, rA, ss, rOut, scale, rA16);
-          else cm_pack_vec_any<false, STATS, true>(d.cm_vpt, rG, rA, ss, rOut, scale);
+            cm_pack_vec_any<false, STATS, true, 2>(d.cm_qpt, rG, rA, ss, rOut, scale, rA16);
+          else cm_pack_vec_any<false, STATS, true>(d.cm_qpt, rG, rA, ss, rOut, scale);
         } else {
           if (ph == 1) cm_pack_elem<true, STATS, true>(rG, rA, len, ss, rOut, scale);
           else if (a16 && ph == 2)
@@ -515,12 +541,12 @@ __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(c
         }
       } else if (d.vec) {
         if (ph == 1) {
-          if (a16) cm_pack_vec_any<true, STATS, false, 1>(d.cm_vpt, rG, rA, ss, rsrc_t(), 1.0f, rA16);
-          else cm_pack_vec_any<true, STATS>(d.cm_vpt, rG, rA, ss);
+          if (a16) cm_pack_vec_any<true, STATS, false, 1>(d.cm_qpt, rG, rA, ss, rsrc_t(), 1.0f, rA16);
+          else cm_pack_vec_any<true, STATS>(d.cm_qpt, rG, rA, ss);
         } else if (a16 && ph == 2) {
-          cm_pack_vec_any<false, STATS, false, 2>(d.cm_vpt, rG, rA, ss, rsrc_t(), 1.0f, rA16);
+          cm_pack_vec_any<false, STATS, false, 2>(d.cm_qpt, rG, rA, ss, rsrc_t(), 1.0f, rA16);
         } else {
-          cm_pack_vec_any<false, STATS>(d.cm_vpt, rG, rA, ss);
+          cm_pack_vec_any<false, STATS>(d.cm_qpt, rG, rA, ss);
         }
       } else {
         if (ph == 1) {
@@ -566,14 +592,14 @@ __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(c
     if (src == kCmInitMaster) rI = make_rsrc(d.init_P + j * d.ld_init + e0, len * 4);
     if (PEND && src == kCmPend) {
       const rsrc_t rPA = make_rsrc(d.pend_acc + (j - ro) * d.ld_pend + e0, len * 4);
-      if (d.vec) cm_adam_vec_any<kCmPend, STATS>(d.cm_vpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss, rPA, &pd);
+      if (d.vec) cm_adam_vec_any<kCmPend, STATS, SELG>(qpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss, rPA, &pd);
       else cm_adam_elem<kCmPend, STATS>(rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, len, ss, rPA, &pd);
     } else if (d.vec) {
       switch (src) {
-        case kCmInplace: cm_adam_vec_any<kCmInplace, STATS>(d.cm_vpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss); break;
-        case kCmPrev: cm_adam_vec_any<kCmPrev, STATS>(d.cm_vpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss); break;
-        case kCmInitW: cm_adam_vec_any<kCmInitW, STATS>(d.cm_vpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss); break;
-        default: cm_adam_vec_any<kCmInitMaster, STATS>(d.cm_vpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss); break;
+        case kCmInplace: cm_adam_vec_any<kCmInplace, STATS, SELG>(qpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss); break;
+        case kCmPrev: cm_adam_vec_any<kCmPrev, STATS, SELG>(qpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss); break;
+        case kCmInitW: cm_adam_vec_any<kCmInitW, STATS, SELG>(qpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss); break;
+        default: cm_adam_vec_any<kCmInitMaster, STATS, SELG>(qpt, rG, rP, rM, rV, rW, rSP, rSM, rSV, rI, c, ss); break;
       }
     } else {
       switch (src) {
@@ -601,27 +627,27 @@ __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(c
 // rows, as in the update.
 // ---------------------------------------------------------------------------
 
-template <int VPT>
+template <int QPT>
 __device__ __forceinline__ void cm_deferred_sum_vec(const HistTable& h, int32_t q, int64_t j,
                                                     int64_t e0, int64_t len, rsrc_t rG,
                                                     rsrc_t rOut, float scale) {
   const int tid = threadIdx.x;
   constexpr int kBatch = 4;  // steps whose rows are loaded before they are added
-  float a[VPT][kGroup];
+  float a[QPT][kQuad];
   const int32_t steps = h.n + 1;  // the earlier steps, then this one
   for (int32_t s0 = 0; s0 < steps; s0 += kBatch) {
-    u32x4 gv[kBatch][VPT];
+    u32x2 gv[kBatch][QPT];
 #pragma unroll
     for (int b = 0; b < kBatch; ++b) {
       const int32_t s = s0 + b;
       if (s < steps) {
         rsrc_t r = rG;
         if (s < h.n) {
-          const DevMat& hd = h.mats[s][q];
+          const auto& hd = const_table(h.mats[s])[q];
           r = make_rsrc(hd.grad + j * hd.ld_grad + e0, len * 2);
         }
 #pragma unroll
-        for (int p = 0; p < VPT; ++p) gv[b][p] = buf_b128<kAuxRO>(r, group_elem(p, tid) * 2, 0);
+        for (int p = 0; p < QPT; ++p) gv[b][p] = buf_b64<kAuxRO>(r, quad_elem(p, tid) * 2, 0);
       }
     }
 #pragma unroll
@@ -629,20 +655,20 @@ __device__ __forceinline__ void cm_deferred_sum_vec(const HistTable& h, int32_t 
       const int32_t s = s0 + b;
       if (s < steps) {
 #pragma unroll
-        for (int p = 0; p < VPT; ++p) {
-          float g[kGroup];
-          widen8(gv[b][p], g);
+        for (int p = 0; p < QPT; ++p) {
+          float g[kQuad];
+          widen4(gv[b][p], g);
 #pragma unroll
-          for (int i = 0; i < kGroup; ++i) a[p][i] = s == 0 ? g[i] : a[p][i] + g[i];
+          for (int i = 0; i < kQuad; ++i) a[p][i] = s == 0 ? g[i] : a[p][i] + g[i];
         }
       }
     }
   }
 #pragma unroll
-  for (int p = 0; p < VPT; ++p) {
+  for (int p = 0; p < QPT; ++p) {
 #pragma unroll
-    for (int i = 0; i < kGroup; ++i) a[p][i] = a[p][i] * scale;
-    f32x8_store<kAuxWO>(rOut, group_elem(p, tid) * 4, a[p]);
+    for (int i = 0; i < kQuad; ++i) a[p][i] = a[p][i] * scale;
+    f32x4_store<kAuxWO>(rOut, quad_elem(p, tid) * 4, a[p]);
   }
 }
 
@@ -655,7 +681,7 @@ __device__ __forceinline__ void cm_deferred_sum_elem(const HistTable& h, int32_t
     for (int32_t s = 0; s <= h.n; ++s) {
       rsrc_t r = rG;
       if (s < h.n) {
-        const DevMat& hd = h.mats[s][q];
+        const auto& hd = const_table(h.mats[s])[q];
         r = make_rsrc(hd.grad + j * hd.ld_grad + e0, len * 2);
       }
       const float g = widen_bf16(buf_u16<kAuxRO>(r, o * 2, 0));
@@ -677,7 +703,7 @@ __global__ __launch_bounds__(kThreads) void cm_handover_deferred_kernel(
   const int32_t q = lo;
   const DevMat& d = mats[q];
   const int64_t local = b - off[q];
-  const int64_t chunk = static_cast<int64_t>(d.cm_vpt) * kThreads * kGroup;
+  const int64_t chunk = static_cast<int64_t>(d.cm_qpt) * kThreads * kQuad;
   const int64_t j = local / d.cm_nch;
   const int64_t ci = local % d.cm_nch;
   const int64_t e0 = ci * chunk;
@@ -695,13 +721,13 @@ __global__ __launch_bounds__(kThreads) void cm_handover_deferred_kernel(
     const rsrc_t rV = make_rsrc(d.V + r * d.ld_state + e0, len * 4);
     const rsrc_t rW = make_rsrc(d.weight + j * d.ld_weight + e0, len * 2);
     if (d.vec)
-      cm_adam_vec_any<kCmInplace, false>(d.cm_vpt, rG, rP, rM, rV, rW, rP, rM, rV, rW, c, ss);
+      cm_adam_vec_any<kCmInplace, false>(d.cm_qpt, rG, rP, rM, rV, rW, rP, rM, rV, rW, c, ss);
     else
       cm_adam_elem<kCmInplace, false>(rG, rP, rM, rV, rW, rP, rM, rV, rW, c, len, ss);
     cm_zero_rows(d, rOut, len);
   } else if (d.vec) {
-    if (d.cm_vpt >= 2) cm_deferred_sum_vec<kCmVpt>(h, q, j, e0, len, rG, rOut, scale);
-    else cm_deferred_sum_vec<1>(h, q, j, e0, len, rG, rOut, scale);
+    if (d.cm_qpt >= kCmQpt) cm_deferred_sum_vec<kCmQpt>(h, q, j, e0, len, rG, rOut, scale);
+    else cm_deferred_sum_vec<kCmQpt / 2>(h, q, j, e0, len, rG, rOut, scale);
   } else {
     cm_deferred_sum_elem(h, q, j, e0, len, rG, rOut, scale);
   }
@@ -713,9 +739,9 @@ __global__ __launch_bounds__(kThreads) void cm_handover_deferred_kernel(
 // the bf16 first-step stage), scale times its widened row of the stage.
 // ---------------------------------------------------------------------------
 
-// The hand-over of rows [e0, e0 + len) of channel j, len <= VPT * 256 * 8
-// (VPT 16-byte groups per lane on the vector path).
-template <bool STAGE, int VPT>
+// The hand-over of rows [e0, e0 + len) of channel j, len <= QPT * 256 * 4
+// (QPT quads per lane on the vector path).
+template <bool STAGE, int QPT>
 __device__ __forceinline__ void cm_unpack_rows(const DevMat& d, int64_t j, int64_t e0,
                                                int64_t len, float scale) {
   const int64_t w = j >> 6;
@@ -724,10 +750,10 @@ __device__ __forceinline__ void cm_unpack_rows(const DevMat& d, int64_t j, int64
   const rsrc_t rD = make_rsrc(d.out + j * d.ld_out + e0, len * 4);
   const int tid = threadIdx.x;
   if (sel) {
-    const float z[kGroup] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    const float z[kQuad] = {0.f, 0.f, 0.f, 0.f};
     if (d.vec) {
 #pragma unroll
-      for (int q = 0; q < VPT; ++q) f32x8_store<kAuxWO>(rD, group_elem(q, tid) * 4, z);
+      for (int q = 0; q < QPT; ++q) f32x4_store<kAuxWO>(rD, quad_elem(q, tid) * 4, z);
     } else {
       for (int64_t e = tid; e < len; e += kThreads)
         buf_put_f32<kAuxWO>(0.0f, rD, static_cast<uint32_t>(e) * 4, 0);
@@ -739,17 +765,17 @@ __device__ __forceinline__ void cm_unpack_rows(const DevMat& d, int64_t j, int64
   const rsrc_t rA = make_rsrc(d.acc + u * d.ld_acc + e0, len * 4);
   const rsrc_t rS = STAGE ? make_rsrc(d.acc1 + j * d.ld_acc1 + e0, len * 2) : rA;
   if (d.vec) {
-    float a[VPT][kGroup];
+    float a[QPT][kQuad];
 #pragma unroll
-    for (int q = 0; q < VPT; ++q) {
-      if constexpr (STAGE) widen8(buf_b128<kAuxRO>(rS, group_elem(q, tid) * 2, 0), a[q]);
-      else f32x8_load<kAuxRO>(rA, group_elem(q, tid) * 4, a[q]);
+    for (int q = 0; q < QPT; ++q) {
+      if constexpr (STAGE) widen4(buf_b64<kAuxRO>(rS, quad_elem(q, tid) * 2, 0), a[q]);
+      else f32x4_load<kAuxRO>(rA, quad_elem(q, tid) * 4, a[q]);
     }
 #pragma unroll
-    for (int q = 0; q < VPT; ++q) {
+    for (int q = 0; q < QPT; ++q) {
 #pragma unroll
-      for (int i = 0; i < kGroup; ++i) a[q][i] = a[q][i] * scale;
-      f32x8_store<kAuxWO>(rD, group_elem(q, tid) * 4, a[q]);
+      for (int i = 0; i < kQuad; ++i) a[q][i] = a[q][i] * scale;
+      f32x4_store<kAuxWO>(rD, quad_elem(q, tid) * 4, a[q]);
     }
   } else {
     for (int64_t e = tid; e < len; e += kThreads) {
@@ -768,7 +794,7 @@ __device__ __forceinline__ void cm_unpack_unit(const DevMat& d, int64_t local, f
   const int64_t j = local / d.cm_unch;
   const int64_t e0 = (local % d.cm_unch) * kCmUnpackChunk;
   const int64_t len = min(static_cast<int64_t>(kCmUnpackChunk), d.n - e0);
-  cm_unpack_rows<STAGE, kCmUnpackVpt>(d, j, e0, len, scale);
+  cm_unpack_rows<STAGE, kCmUnpackQpt>(d, j, e0, len, scale);
 }
 
 template <bool BATCHED, bool STAGE>
@@ -821,12 +847,12 @@ __global__ __launch_bounds__(kThreads) void cm_unpack_zen_kernel(const DevMat* _
     const bool pair = u + 1 < u1 && (local + 1) / d.cm_unch == j;
     const int64_t len = min(static_cast<int64_t>(pair ? 2 : 1) * kCmUnpackChunk, d.n - e0);
     if (pair) {
-      if (from_stage) cm_unpack_rows<true, 2 * kCmUnpackVpt>(d, j, e0, len, scale);
-      else cm_unpack_rows<false, 2 * kCmUnpackVpt>(d, j, e0, len, scale);
+      if (from_stage) cm_unpack_rows<true, 2 * kCmUnpackQpt>(d, j, e0, len, scale);
+      else cm_unpack_rows<false, 2 * kCmUnpackQpt>(d, j, e0, len, scale);
       u += 2;
     } else {
-      if (from_stage) cm_unpack_rows<true, kCmUnpackVpt>(d, j, e0, len, scale);
-      else cm_unpack_rows<false, kCmUnpackVpt>(d, j, e0, len, scale);
+      if (from_stage) cm_unpack_rows<true, kCmUnpackQpt>(d, j, e0, len, scale);
+      else cm_unpack_rows<false, kCmUnpackQpt>(d, j, e0, len, scale);
       u += 1;
     }
   }

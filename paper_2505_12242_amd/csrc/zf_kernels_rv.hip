@@ -321,7 +321,7 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
         for (int e = 0; e < kDefBatch; ++e) {
           const int32_t st = s0 + e;
           if (st < hist.n) {
-            const DevMat& hd = hist.mats[st][q];
+            const auto& hd = const_table(hist.mats[st])[q];
             const rsrc_t rE = rows_rsrc(hd.grad, i0, i1, hd.ld_grad, d.m);
             const uint32_t sE = static_cast<uint32_t>(hd.ld_grad * 2);
 #pragma unroll
