@@ -531,11 +531,13 @@ def recorded_traffic(launch_kind: str, workload: str, variant: str):
     return float(v.group(1))
 
 
-def calibrate_streams(dev, gib: float, reps: int = 5) -> dict:
+def calibrate_streams(dev, gib: float, reps: int = 10) -> dict:
     """The reference streams of zf_measure.h (the update pass's access
     pattern with no arithmetic) over `gib` GiB: read-only, copy and
     read-modify-write in place, each one untimed launch then `reps` timed
-    ones (HIP events on the launch stream)."""
+    ones (HIP events on the launch stream).  They are the process's first
+    GPU work, so about 0.1 s of copies runs first: on a GPU that has just
+    left idle the first milliseconds stream slower."""
     import torch
     import paper_2505_12242_amd as zf
     nb = int(gib * 2**30) // 16 * 16
@@ -544,6 +546,14 @@ def calibrate_streams(dev, gib: float, reps: int = 5) -> dict:
     sink = torch.zeros(1, dtype=torch.int32, device=dev)
     stream = torch.cuda.current_stream(dev)
     out = {"kernel": "stream_probe_kernel<0|1|2> (zf_stream_probe)", "GiB": gib}
+    warm_ms, t_warm = 0.0, time.perf_counter()
+    while warm_ms < 100.0 and time.perf_counter() - t_warm < 5.0:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        zf.stream_probe(zf.PROBE_COPY, src, dst, nb, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize(dev)
+        warm_ms += e0.elapsed_time(e1)
     for kind, name, moved in ((zf.PROBE_READ, "read", nb), (zf.PROBE_COPY, "copy", 2 * nb),
                               (zf.PROBE_RMW, "rmw", 2 * nb)):
         args = ((src, sink) if kind == zf.PROBE_READ else (src, dst) if kind == zf.PROBE_COPY

@@ -5,7 +5,7 @@
  * streams its operands once).  To state how close each pass comes to what
  * the chip can stream with the same access pattern, the library exports
  * reference streams built from the update pass's own building blocks (one
- * contiguous 8 KiB chunk per 256-thread block, 16-byte raw buffer accesses,
+ * contiguous 4 KiB chunk per 256-thread block, 16-byte raw buffer accesses,
  * the XCD-aware block order, the update's cache policies) with no
  * arithmetic.  Conventions (device pointers, caller-owned memory, stream
  * ordering, status codes) are those of zf.h.
@@ -31,7 +31,7 @@ typedef enum zf_stream_probe_kind {
 } zf_stream_probe_kind;
 
 /* Enqueues one streaming pass of `kind` over `bytes` on `stream`.
- * bytes: > 0, a multiple of 16, at most 2^31 - 1 blocks of 8 KiB; src and
+ * bytes: > 0, a multiple of 16, at most (2^32 - 1) / 256 blocks of 4 KiB; src and
  * dst 16-byte aligned (dst 4-byte aligned for ZF_PROBE_READ).  ZF_EINVAL
  * (nothing enqueued) otherwise, or when src and dst overlap for
  * ZF_PROBE_COPY.  Bytes moved: `bytes` for READ, 2 * `bytes` for COPY and

@@ -671,7 +671,8 @@ zf_status zf_stream_probe(int32_t kind, const void* src, void* dst, size_t bytes
       bytes > static_cast<size_t>(INT64_MAX / 2) || dst == nullptr)
     return ZF_EINVAL;
   const int64_t nb = static_cast<int64_t>(bytes);
-  if (zf::stream_probe_blocks(nb) >= (int64_t(1) << 31)) return ZF_EINVAL;
+  // one launch: at most 2^32 - 1 work-items
+  if (zf::stream_probe_blocks(nb) > ((int64_t(1) << 32) - 1) / zf::kThreads) return ZF_EINVAL;
   if (kind == 0 && !aligned(dst, 4)) return ZF_EINVAL;
   if (kind != 0 && !aligned(dst, 16)) return ZF_EINVAL;
   if (kind != 2 && (src == nullptr || !aligned(src, 16))) return ZF_EINVAL;

@@ -25,12 +25,14 @@ namespace {
 
 constexpr int kGroup = 8;  // bf16 elements in 16 bytes
 
-// Cache policy per stream, chosen by measurement on MI355X (7B set, three
-// alternating runs per variant): streams read once by a pass -- G in every
-// pass, the init sources -- and the bf16 weight write-back are non-temporal
-// (2% faster steps than the default policy everywhere); the hand-over output
-// and read-modify-write streams keep the default policy (non-temporal stores
-// of the hand-over cost 2-3% there).
+// Cache policy per stream, chosen by measurement on MI355X (7B and 13B
+// sets, alternating runs per variant): streams read once by a pass -- G in
+// every pass, the init sources --, streams only written by a pass (the
+// hand-over output, the packed buffer on an interval's first step) and the
+// bf16 weight write-back are non-temporal; read-modify-write streams keep
+// the default policy (non-temporal there made the Adam pass 10-17% slower).
+// Default-policy loads of the read-only streams cost 1-2% per step;
+// non-temporal stores of the write-only ones gain about 1%.
 #ifndef ZF_AUX_SCORE
 #define ZF_AUX_SCORE kStream
 #endif
@@ -38,7 +40,7 @@ constexpr int kGroup = 8;  // bf16 elements in 16 bytes
 #define ZF_AUX_RO kStream
 #endif
 #ifndef ZF_AUX_WO
-#define ZF_AUX_WO kCached
+#define ZF_AUX_WO kStream
 #endif
 #ifndef ZF_AUX_RMW
 #define ZF_AUX_RMW kCached

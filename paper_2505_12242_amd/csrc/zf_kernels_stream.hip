@@ -1,16 +1,20 @@
 // Streaming reference kernels for measurement: the memory access pattern of
-// the channel-major update pass with no arithmetic, so that what one MI355X
+// the channel-major passes with no arithmetic, so that what one MI355X
 // reaches with it (read-only, copy, read-modify-write) can be measured in
-// the same run as the hot path.  Same building blocks as the update: a
-// block owns one contiguous chunk of kProbeVpt x 256 lanes x 16 bytes, raw
-// buffer resources over exactly that chunk, 16-byte accesses, the XCD-aware
-// block order, non-temporal loads of streams the pass only reads and the
-// default policy for written and read-modify-write streams.
+// the same run as the hot path.  Same building blocks as the passes: raw
+// buffer resources over exactly a block's chunk, 16-byte accesses that a
+// wave issues over 1 KiB of consecutive bytes, the XCD-aware block order,
+// non-temporal loads and stores of streams only read or only written and
+// the default policy for read-modify-write streams.  A block owns one chunk
+// of 256 lanes x 16 bytes: of the chunk sizes measured on MI355X (4, 8 and
+// 16 KiB per 256-thread block) the fastest for each of the three streams
+// (read 7.6, copy 6.5, read-modify-write 6.3 TB/s against 6.9, 5.9 and 5.8
+// with 8 KiB).
 #include "zf_device.hpp"
 
 namespace zf {
 
-constexpr int kProbeVpt = 2;  // 16-byte groups per lane, as the update
+constexpr int kProbeVpt = 1;  // 16-byte groups per lane
 constexpr int64_t kProbeChunk = int64_t(kProbeVpt) * kThreads * 16;
 
 // KIND 0: read src; KIND 1: copy src to dst; KIND 2: dst ^= key in place.
@@ -49,7 +53,8 @@ __global__ __launch_bounds__(kThreads) void stream_probe_kernel(const uint8_t* _
         w.z ^= key;
         w.w ^= key;
       }
-      buf_put_b128<kCached>(w, rd, o, 0);
+      if constexpr (KIND == 2) buf_put_b128<kCached>(w, rd, o, 0);
+      else buf_put_b128<kStream>(w, rd, o, 0);
     }
   }
 }

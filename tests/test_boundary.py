@@ -215,6 +215,7 @@ def test_stream_probe_validation():
     assert P(0, None, B, 4096, 0, None) == EINVAL        # read without a source
     assert P(2, None, None, 4096, 0, None) == EINVAL     # rmw without a buffer
     assert P(1, A, B, 1 << 62, 0, None) == EINVAL        # too many blocks
+    assert P(2, None, B, 4096 * (1 << 24), 0, None) == EINVAL   # 2^32 work-items: one too many
 
 
 def test_plan_validation():

@@ -1,7 +1,7 @@
 """The reference streams of zf_measure.h (measurement only): the copy
 leaves dst equal to src, the read-modify-write pass leaves every 32-bit word
 xor key, and the read pass writes nothing unless its folded data equal the
-key -- on sizes with a ragged last block (not a multiple of the 8 KiB block
+key -- on sizes with a ragged last block (not a multiple of the 4 KiB block
 chunk) and buffers padded with sentinels that must stay intact."""
 import pytest
 import torch
@@ -10,7 +10,7 @@ pytestmark = pytest.mark.gpu
 
 zf = pytest.importorskip("paper_2505_12242_amd")
 
-SIZES = [16, 8192, 8192 + 16, 3 * 2**20 + 48, 64 * 2**20]
+SIZES = [16, 4096, 4096 + 16, 8192 + 16, 3 * 2**20 + 48, 64 * 2**20]
 PAD = 4096
 
 
