@@ -194,7 +194,11 @@ __global__ __launch_bounds__(kThreads) void cm_colnorm_kernel(const DevMat* __re
         if constexpr (OUT == 2) {
 #pragma unroll
           for (int c = 0; c < kGroup; ++c) f[c] = f[c] * scale;
-          f32x8_store<kAuxWO>(rO, static_cast<uint32_t>((e0 + b * kStride + lo) * 4), f);
+          // a lane's 8 values go out as two 16-byte stores, each filling
+          // half of every line it touches: the default policy merges the
+          // halves in L2 (non-temporal, each half reaches HBM on its own and
+          // the pass ran at half speed)
+          f32x8_store<kCached>(rO, static_cast<uint32_t>((e0 + b * kStride + lo) * 4), f);
         }
       }
     }
