@@ -435,7 +435,11 @@ typedef struct zf_plan zf_plan;
  * and its workspaces: column-score partials of row-major matrices,
  * Zen-auto partials).  Validates the descriptors as zf_plan_create does;
  * no device work.  mats: HOST array of nmats >= 1 descriptors;
- * device_bytes: HOST, receives the size. */
+ * device_bytes: HOST, receives the size.  ZF_EINVAL also when one of the
+ * plan's launches would need more than 2^32 - 1 work-items, the limit of a
+ * dispatch (channel-major: a set of more than about 34 G parameters, whose
+ * update grid covers 2048 or 4096 rows of a channel per 256-thread block);
+ * such a set is split over several plans. */
 zf_status zf_plan_query(const zf_matrix* mats, int32_t nmats, size_t* device_bytes);
 
 /* Builds a plan in caller-provided device memory: validates nmats >= 1
