@@ -5,8 +5,8 @@ import pytest
 import torch
 
 from oracle import colnorm, k_from_ratio, select_topk
-from workloads import (WORKLOADS, derive_seed, get_workload, gradient, master_weights,
-                       space_all_pairs, space_boundary, step_scales)
+from workloads import (WORKLOADS, derive_seed, get_workload, gradient, gradient_iid,
+                       master_weights, space_all_pairs, space_boundary, step_scales)
 
 
 def bits(t):
@@ -30,6 +30,25 @@ def test_determinism():
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
     assert not torch.equal(a.view(torch.int16), c.view(torch.int16))
     assert torch.equal(master_weights(8, 8, 3), master_weights(8, 8, 3))
+
+
+def test_independent_draws():
+    """gradient_iid: the same seed gives the same bits; each column's energy
+    divided by s_j^2 varies from column to column (its own noise), where the
+    shifted-copy generator gives the same ratio for every column up to bf16
+    rounding; the mean of those ratios is about 1 (elements N(0, 1) * s_j)."""
+    n, m = 512, 200
+    sc = torch.exp(torch.randn(m, generator=torch.Generator().manual_seed(3),
+                               dtype=torch.float64))
+    a = gradient_iid(n, m, sc, seed=9)
+    assert torch.equal(a.view(torch.int16), gradient_iid(n, m, sc, seed=9).view(torch.int16))
+    assert not torch.equal(a.view(torch.int16), gradient_iid(n, m, sc, seed=10).view(torch.int16))
+    s2 = sc.numpy() ** 2
+    ratio_iid = colnorm(bits(a)).astype(np.float64) / s2 / n
+    ratio_shift = colnorm(bits(gradient(n, m, sc, seed=9))).astype(np.float64) / s2 / n
+    assert np.std(ratio_shift) < 2e-3                       # one noise energy for all
+    assert 0.03 < np.std(ratio_iid) < 0.12                  # sqrt(2 / n) = 0.0625
+    assert abs(np.mean(ratio_iid) - 1.0) < 0.03
 
 
 def test_all_pairs_spacing_of_realised_scores():

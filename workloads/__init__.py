@@ -20,6 +20,7 @@ from .synth import (  # noqa: F401
     base_scales,
     derive_seed,
     gradient,
+    gradient_iid,
     jittered_scales,
     master_weights,
     score_vector,

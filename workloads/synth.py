@@ -18,6 +18,8 @@ What is drawn (all seeded, all reproducible on the device they are drawn on):
   norm of G.
 * Master weights N(0, std^2) in fp32, bf16 weights = their bf16 rounding
   (torch's cast).
+* `gradient_iid`: the same scales with every element its own N(0, 1) draw,
+  for tests of selection on columns whose noise energies differ.
 
 Nothing here computes column norms, selections, optimizer steps or packed
 buffers.
@@ -150,6 +152,25 @@ def gradient(n: int, m: int, scales: torch.Tensor, seed: int,
         z = torch.where(sign.bool(), -z, z)
         out[r0:r1] = (z * s32[None, :]).to(torch.bfloat16)
     return out
+
+
+def gradient_iid(n: int, m: int, scales: torch.Tensor, seed: int,
+                 device="cpu") -> torch.Tensor:
+    """bf16 gradient [n, m] with independent elements: bf16(z_ij * s_j), z_ij ~
+    N(0, 1) each its own draw (torch's CPU generator, then moved to
+    `device`, so that the same seed gives the same bits wherever the test
+    runs).  Unlike `gradient`, each column carries its own noise energy, so
+    column energies only approximately follow s_j^2 and no spacing can be
+    imposed through the scales."""
+    out = torch.empty(n, m, dtype=torch.bfloat16)
+    if n > 0 and m > 0:
+        g = _gen(seed, "cpu")
+        s32 = scales.to(torch.float32).cpu()
+        for r0 in range(0, n, _CHUNK_ROWS):
+            r1 = min(n, r0 + _CHUNK_ROWS)
+            z = torch.randn(r1 - r0, m, generator=g, dtype=torch.float32)
+            out[r0:r1] = (z * s32[None, :]).to(torch.bfloat16)
+    return out.to(torch.device(device))
 
 
 def master_weights(n: int, m: int, seed: int, std: float = 0.02,
