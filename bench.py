@@ -85,11 +85,13 @@ def parse_args(argv=None):
                     help="with --offload: host threads of the deferred update (default: "
                          "min(16, cpu count))")
     ap.add_argument("--packing", choices=["deferred", "every-step"], default="deferred",
-                    help="deferred (default where it applies: fixed schedule, fused hand-over, "
+                    help="deferred (default where it applies: fixed schedule or Zen-auto "
+                         "decided on the device in the channel-major layout, fused hand-over, "
                          "no offload): every gradient of an interval stays in its slot and the "
-                         "interval's last step sums them into the hand-over, with no packed "
-                         "buffer (the ring gets at least min(S, R) slots); every-step: the "
-                         "unselected part is accumulated into the packed buffer at every step")
+                         "interval's last step sums them into the hand-over (Zen-auto: every "
+                         "step sums them for its statistics), with no packed buffer (the ring "
+                         "gets at least min(S, R) slots); every-step: the unselected part is "
+                         "accumulated into the packed buffer at every step")
     ap.add_argument("--separate-handover", action="store_true",
                     help="hand over with a separate unpack pass after the last update of an "
                          "interval instead of fusing it into that update")
@@ -111,7 +113,8 @@ def parse_args(argv=None):
 
 def step_traffic(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool = False,
                  fused_handover: bool = False, second: bool = False, stage: bool = False,
-                 scored_handover: bool = None, deferred: bool = False, length: int = 1) -> dict:
+                 scored_handover: bool = None, deferred: bool = False, length: int = 1,
+                 zen: bool = False) -> dict:
     """Algorithmic HBM bytes of one step, by kernel, as [read, written].
 
     colnorm  2nm (read G) + 4m (write scores)          refresh steps
@@ -146,6 +149,12 @@ def step_traffic(shapes, ks, refresh: bool, first: bool, end: bool, offload: boo
              gradient once at the unselected elements and writes the
              hand-over: 28nk + 4nk + (2 length + 4) nu.  One-step intervals
              as with the stage (the score pass hands over on a refresh)
+    Zen-auto with deferred packing (deferred and zen): every step, at
+             position `length` in its interval, reads the interval's kept
+             gradients at the unselected elements for the statistics
+             (28nk + 2 length nu); an end the caller forces writes the
+             hand-over from the update (+ 4nu + 4nk), any other end from the
+             gated hand-over pass (unpack: 2 length nu + 4nm)
     """
     if scored_handover is None:
         scored_handover = stage or deferred
@@ -165,6 +174,14 @@ def step_traffic(shapes, ks, refresh: bool, first: bool, end: bool, offload: boo
             add("topk_select", 4 * m, 4 * m + 12 * ((m + 63) // 64))
         # selected: G 2 + P/M/V 12 read, P/M/V 12 + W 2 written
         add("update", 14 * n * k, 14 * n * k)
+        if deferred and zen:
+            add("update", 2 * length * n * u, 0)
+            if end:
+                if fused_handover:
+                    add("update", 0, 4 * n * u + 4 * n * k)
+                else:
+                    add("unpack", 2 * length * n * u, 4 * n * m)
+            continue
         if deferred and not scored_end and not (end and first):
             if end:  # each step's gradient read once, the hand-over written
                 add("update", 2 * length * n * u, 4 * n * u + 4 * n * k)
@@ -191,10 +208,11 @@ def step_traffic(shapes, ks, refresh: bool, first: bool, end: bool, offload: boo
 
 def step_bytes(shapes, ks, refresh: bool, first: bool, end: bool, offload: bool = False,
                fused_handover: bool = False, second: bool = False, stage: bool = False,
-               scored_handover: bool = None, deferred: bool = False, length: int = 1) -> dict:
+               scored_handover: bool = None, deferred: bool = False, length: int = 1,
+               zen: bool = False) -> dict:
     """step_traffic's bytes read + written, by kernel."""
     t = step_traffic(shapes, ks, refresh, first, end, offload, fused_handover, second, stage,
-                     scored_handover, deferred, length)
+                     scored_handover, deferred, length, zen)
     return {cls: r + w for cls, (r, w) in t.items()}
 
 
@@ -495,6 +513,9 @@ def kernel_source_hash() -> str:
 def launch_kernels(kind: str, channel_major: bool, deferred: bool) -> str:
     """The kernels behind one update launch kind of the runner."""
     if channel_major:
+        if deferred and kind == "update_zen":
+            return ("cm_update_kernel, Zen-auto with deferred packing (Adam + statistics of the "
+                    "interval's running sum, summed from the kept gradients)")
         if deferred and kind == "update_handover":
             return ("cm_handover_deferred_kernel (the interval's last step: Adam + the sum of "
                     "the interval's gradients into the hand-over)")
@@ -626,8 +647,10 @@ def main(argv=None) -> int:
               f"{calib['read_GB/s']}, copy {calib['copy_GB/s']}, read-modify-write "
               f"{calib['rmw_GB/s']} GB/s", file=sys.stderr, flush=True)
 
-    deferred = (args.packing == "deferred" and args.zen_tau is None and not args.offload
-                and not args.separate_handover)
+    # (Zen-auto: with deferred packing when decided on the device, channel-major)
+    deferred = (args.packing == "deferred" and not args.offload and not args.separate_handover
+                and (args.zen_tau is None
+                     or (not args.zen_on_host and args.layout == "channel-major")))
     if deferred:
         args.slots = max(args.slots, min(wl.accum, wl.refresh))
     t0 = time.perf_counter()
@@ -738,7 +761,8 @@ def main(argv=None) -> int:
         return step_bytes(shapes, ks, kind.refresh, first, kind.interval_end,
                           offload=args.offload, fused_handover=fh, second=second,
                           stage=runner.use_stage, scored_handover=runner.score_handover,
-                          deferred=runner.deferred, length=kind.step_in_interval)
+                          deferred=runner.deferred, length=kind.step_in_interval,
+                          zen=args.zen_tau is not None)
 
     def model_traffic(kind):
         first, second = kind.step_in_interval == 1, kind.step_in_interval == 2
@@ -746,7 +770,8 @@ def main(argv=None) -> int:
         return step_traffic(shapes, ks, kind.refresh, first, kind.interval_end,
                             offload=args.offload, fused_handover=fh, second=second,
                             stage=runner.use_stage, scored_handover=runner.score_handover,
-                            deferred=runner.deferred, length=kind.step_in_interval)
+                            deferred=runner.deferred, length=kind.step_in_interval,
+                            zen=args.zen_tau is not None)
 
     build_total = sum(sum(model_bytes(k).values()) for k in kinds)
     unfused_total = sum(sum(model_bytes(k, True).values()) for k in kinds)
@@ -851,11 +876,14 @@ def main(argv=None) -> int:
             "model_compute_ms": args.model_compute_ms or None,
             "interval_ends": sum(1 for k in kinds if k.interval_end),
             "first_step_stage": runner.use_stage,
-            "packing": "deferred to the interval's last step" if runner.deferred else
-                       "every step",
+            "packing": ("deferred: the kept gradients summed again at every step for the "
+                        "Zen-auto statistics" if runner.deferred and args.zen_tau is not None
+                        else "deferred to the interval's last step" if runner.deferred else
+                        "every step"),
             "handover": "fused into the interval's last update" if fused else
                         ("device -> host copy of the packed buffer" if args.offload
-                         else "separate unpack pass"),
+                         else "fused into the update at forced ends, else the gated pass"
+                         if runner.zen_device else "separate unpack pass"),
             "grad_slots": args.slots,
         },
         "byte_models": {

@@ -704,6 +704,55 @@ zf_status zf_plan_update_zen_device(zf_plan* plan, const zf_adam_hparams* hp, in
  * has it, row-major plans without it. */
 zf_status zf_plan_handover_zen(zf_plan* plan, const zf_zen_state* state, zf_stream stream);
 
+/* Zen-auto on the device with deferred packing (channel-major): the
+ * interval's sums are never written step by step.  The unselected part of
+ * each step's gradient stays where it was written, and the caller keeps the
+ * gradients of the last accum_interval (S_max) steps resident and unchanged.
+ * Zen-auto's statistic of an unselected channel is the squared norm of the
+ * interval's running sum (paper §3.2, "Hyperparameter Auto-tuning"), so
+ * each step sums the interval's kept gradients again, in step order in fp32
+ * (the accumulation's own sequence, hence the same bits), for the
+ * statistics; the selected channels take the Adam step as in
+ * zf_plan_update_zen_device.  At a position p the unselected channels cost
+ * 2p bytes per element read, against 8-10 read and written per step when
+ * packing every step: fewer bytes while the intervals are short (S_max up to
+ * about 6).
+ * zf_plan_update_zen_device's semantics otherwise: position from *state, the
+ * statistics, totals and trigger, the new state; force_end 2 writes the
+ * hand-over, scale = fp32(1 / position) times the running sum (+0.0 at the
+ * selected channels), and sets ended = 2; 1 leaves it to
+ * zf_plan_handover_zen_deferred; 0 no forced end.
+ * earlier: HOST array of n_earlier (0..15) plans over the same matrices in
+ * the same order (same n, m, k and channel-major geometry), the plans of the
+ * steps before this one, oldest first, whose descriptors' grad is that
+ * step's gradient: at least the last min(S_max, steps since the first) - 1
+ * of them.  The update reads the last position - 1 of them, the position
+ * read from *state on the device; only their gradients are read, and they
+ * must not overlap what the step writes.  Channel-major plans with
+ * `unpacked`, the Zen-auto statistics buffers, without a full-state store;
+ * the packed buffer (acc) and the bf16 stage are not used.  ZF_EINVAL
+ * (nothing enqueued) otherwise.  The earlier plans' device memory and
+ * gradients must stay valid until the work on `stream` is done.  Follow it
+ * with zf_plan_handover_zen_deferred with the same earlier plans. */
+zf_status zf_plan_update_zen_deferred(zf_plan* plan, const zf_adam_hparams* hp, int64_t step,
+                                      int32_t mode, int64_t accum_interval,
+                                      const zf_plan* const* earlier, int32_t n_earlier,
+                                      int32_t force_end, double tau, zf_zen_totals* totals,
+                                      zf_zen_state* state, zf_stream stream);
+
+/* The hand-over of the step zf_plan_update_zen_deferred just ran: if
+ * state->ended == 1, every matrix's `unpacked` buffer receives scale =
+ * fp32(1 / state->length) times the interval's sums, summed from the last
+ * length - 1 earlier plans' gradients and this plan's, in step order in
+ * fp32, +0.0 at the selected channels: bit for bit what packing every step
+ * and zf_plan_handover_zen give.  Else nothing is written; a fixed grid, so
+ * that a step that does not end its interval costs one short launch.
+ * earlier as in zf_plan_update_zen_deferred; channel-major plans with
+ * `unpacked`; ZF_EINVAL otherwise. */
+zf_status zf_plan_handover_zen_deferred(zf_plan* plan, const zf_plan* const* earlier,
+                                        int32_t n_earlier, const zf_zen_state* state,
+                                        zf_stream stream);
+
 #ifdef __cplusplus
 }
 #endif

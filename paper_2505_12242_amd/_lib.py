@@ -128,6 +128,11 @@ SIGNATURES = [
     ("zf_plan_update_zen_device", ctypes.c_int,
      [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, c_i32, c_i64, c_i32, c_dbl, c_vp, c_vp, c_vp]),
     ("zf_plan_handover_zen", ctypes.c_int, [c_vp, c_vp, c_vp]),
+    ("zf_plan_update_zen_deferred", ctypes.c_int,
+     [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, c_i32, c_i64, ctypes.POINTER(c_vp), c_i32,
+      c_i32, c_dbl, c_vp, c_vp, c_vp]),
+    ("zf_plan_handover_zen_deferred", ctypes.c_int,
+     [c_vp, ctypes.POINTER(c_vp), c_i32, c_vp, c_vp]),
     ("zf_plan_update_zen_pending", ctypes.c_int,
      [c_vp, ctypes.POINTER(ZfAdamHparams), c_i64, c_i64, c_i64, c_flt, c_dbl, c_vp, c_vp]),
 ]
@@ -887,6 +892,32 @@ class Plan:
         _check_dev_bytes(state, ZEN_STATE_BYTES, "state")
         _check("zf_plan_handover_zen", LIB.zf_plan_handover_zen(self._h, state.data_ptr(),
                                                                 _stream(stream)))
+
+    def update_zen_deferred(self, hp: AdamHparams, step: int, mode: int, accum_interval: int,
+                            earlier: Sequence["Plan"], force_end: int, tau: float,
+                            totals: torch.Tensor, state: torch.Tensor, stream=None) -> None:
+        """update_zen_device with deferred packing (channel-major;
+        zf_plan_update_zen_deferred): the unselected channels' statistics
+        are taken on the interval's running sum, summed from the gradients of
+        the last position - 1 plans of `earlier` (the steps before this one,
+        oldest first) and this plan's; nothing is packed.  force_end 2
+        writes the hand-over."""
+        _check_dev_bytes(totals, ZEN_TOTALS_BYTES, "totals")
+        _check_dev_bytes(state, ZEN_STATE_BYTES, "state")
+        hs = (c_vp * max(1, len(earlier)))(*[e._h.value for e in earlier])
+        c_hp = hp.as_c()
+        _check("zf_plan_update_zen_deferred", LIB.zf_plan_update_zen_deferred(
+            self._h, ctypes.byref(c_hp), step, mode, accum_interval, hs, len(earlier),
+            int(force_end), float(tau), totals.data_ptr(), state.data_ptr(), _stream(stream)))
+
+    def handover_zen_deferred(self, earlier: Sequence["Plan"], state: torch.Tensor,
+                              stream=None) -> None:
+        """The hand-over of the step update_zen_deferred ran, if the device
+        ended the interval (zf_plan_handover_zen_deferred)."""
+        _check_dev_bytes(state, ZEN_STATE_BYTES, "state")
+        hs = (c_vp * max(1, len(earlier)))(*[e._h.value for e in earlier])
+        _check("zf_plan_handover_zen_deferred", LIB.zf_plan_handover_zen_deferred(
+            self._h, hs, len(earlier), state.data_ptr(), _stream(stream)))
 
     def update_zen_pending(self, hp: AdamHparams, step: int, accum_interval: int,
                            pend_step: int, pend_scale: float, tau: float,

@@ -1291,18 +1291,21 @@ zf_status zf_plan_update_handover(zf_plan* p, const zf_adam_hparams* hp, int64_t
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 
-zf_status zf_plan_update_handover_deferred(zf_plan* p, const zf_adam_hparams* hp, int64_t step,
-                                           const zf_plan* const* earlier, int32_t n_earlier,
-                                           float scale, zf_stream stream) {
-  if (p == nullptr || !p->can_adam || !p->can_handover || p->has_store) return ZF_EINVAL;
-  if (!hparams_ok(hp) || step < 1 || !std::isfinite(scale)) return ZF_EINVAL;
-  if (earlier == nullptr || n_earlier < 1 || n_earlier > zf::kMaxDeferred) return ZF_EINVAL;
+}  // extern "C"
+
+namespace {
+
+// The earlier steps' plans of a call with deferred packing (oldest first):
+// the same matrices as p (count, shapes, k; channel-major: access path and
+// geometry), each with its gradient, read only and disjoint from every
+// buffer the step writes.  rv (row-major): cleared when an earlier gradient
+// does not fit the 16-byte kernel's addressing.
+zf_status gather_earlier(const zf_plan* p, const zf_plan* const* earlier, int32_t n_earlier,
+                         zf::HistTable& h, bool& rv) {
+  if (n_earlier < 0 || n_earlier > zf::kMaxDeferred || (n_earlier > 0 && earlier == nullptr))
+    return ZF_EINVAL;
   const int32_t L = p->layout;
   const bool cm = L == zf::kChannelMajor;
-  // row-major: the 16-byte kernel reads the earlier gradients as it reads
-  // this step's (16-byte rows, strides within its 32-bit row offsets)
-  bool rv = !cm && p->mats[0].rv;
-  zf::HistTable h{};
   h.n = n_earlier;
   for (int32_t s = 0; s < n_earlier; ++s) {
     const zf_plan* e = earlier[s];
@@ -1311,7 +1314,8 @@ zf_status zf_plan_update_handover_deferred(zf_plan* p, const zf_adam_hparams* hp
       const DevMat& a = e->mats[q];
       const DevMat& b = p->mats[q];
       if (a.n != b.n || a.m != b.m || a.k != b.k) return ZF_EINVAL;
-      if (cm && (a.vec != b.vec || a.cm_qpt != b.cm_qpt || a.cm_nch != b.cm_nch || a.cm_snch != b.cm_snch))
+      if (cm && (a.vec != b.vec || a.cm_qpt != b.cm_qpt || a.cm_nch != b.cm_nch ||
+                 a.cm_snch != b.cm_snch || a.cm_unch != b.cm_unch))
         return ZF_EINVAL;
       if (b.n * (b.m - b.k) > 0 && a.grad == nullptr) return ZF_EINVAL;
       if (!cm) {
@@ -1334,21 +1338,41 @@ zf_status zf_plan_update_handover_deferred(zf_plan* p, const zf_adam_hparams* hp
     }
     h.mats[s] = e->d_mats;
   }
+  return ZF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+zf_status zf_plan_update_handover_deferred(zf_plan* p, const zf_adam_hparams* hp, int64_t step,
+                                           const zf_plan* const* earlier, int32_t n_earlier,
+                                           float scale, zf_stream stream) {
+  if (p == nullptr || !p->can_adam || !p->can_handover || p->has_store) return ZF_EINVAL;
+  if (!hparams_ok(hp) || step < 1 || !std::isfinite(scale)) return ZF_EINVAL;
+  if (earlier == nullptr || n_earlier < 1) return ZF_EINVAL;
+  const bool cm = p->layout == zf::kChannelMajor;
+  // row-major: the 16-byte kernel reads the earlier gradients as it reads
+  // this step's (16-byte rows, strides within its 32-bit row offsets)
+  bool rv = !cm && p->mats[0].rv;
+  zf::HistTable h{};
+  const zf_status st = gather_earlier(p, earlier, n_earlier, h, rv);
+  if (st != ZF_OK) return st;
   const AdamK c = adam_consts(*hp, step);
-  const hipStream_t st = as_stream(stream);
+  const hipStream_t stm = as_stream(stream);
   hipError_t e;
   if (cm) {
     e = zf::launch_cm_handover_deferred(Table{p->d_mats, p->d_off_up, p->nmats}, p->mats[0],
-                                        p->blk_up, c, scale, h, st);
+                                        p->blk_up, c, scale, h, stm);
   } else if (rv) {
     e = zf::launch_rv_handover_deferred(Table{p->d_mats, p->d_off_upv, p->nmats}, p->mats[0],
-                                        p->blk_upv, c, scale, h, st);
+                                        p->blk_upv, c, scale, h, stm);
   } else {
     e = zf::launch_update(Table{p->d_mats, p->d_off_up, p->nmats}, p->mats[0], p->blk_up, c,
-                          zf::kInplace, 0, true, false, false, 1.0f, st);
+                          zf::kInplace, 0, true, false, false, 1.0f, stm);
     if (e == hipSuccess)
       e = zf::launch_rm_handover_deferred(Table{p->d_mats, p->d_off_unp, p->nmats}, p->blk_unp,
-                                          scale, h, st);
+                                          scale, h, stm);
   }
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
@@ -1495,6 +1519,56 @@ zf_status zf_plan_handover_zen(zf_plan* p, const zf_zen_state* state, zf_stream 
           ? zf::launch_cm_unpack_zen(t, p->mats[0], p->blk_unp, zst, p->all_acc1,
                                      as_stream(stream))
           : zf::launch_unpack_zen(t, p->blk_unp, zst, as_stream(stream));
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
+zf_status zf_plan_update_zen_deferred(zf_plan* p, const zf_adam_hparams* hp, int64_t step,
+                                      int32_t mode, int64_t accum_interval,
+                                      const zf_plan* const* earlier, int32_t n_earlier,
+                                      int32_t force_end, double tau, zf_zen_totals* totals,
+                                      zf_zen_state* state, zf_stream stream) {
+  if (p == nullptr || p->layout != zf::kChannelMajor || !p->can_zen || !p->can_adam ||
+      !p->can_handover || p->has_store || !hparams_ok(hp) || step < 1 || !(tau >= 0.0) ||
+      totals == nullptr || !aligned(totals, 8))
+    return ZF_EINVAL;
+  if (mode != zf::kInplace && mode != zf::kRemap && mode != zf::kInit) return ZF_EINVAL;
+  if (mode == zf::kRemap && !p->can_remap) return ZF_EINVAL;
+  if (accum_interval < 1 || accum_interval > INT32_MAX || state == nullptr ||
+      !aligned(state, 4) || force_end < 0 || force_end > 2)
+    return ZF_EINVAL;
+  zf::HistTable h{};
+  bool rv = false;
+  const zf_status st = gather_earlier(p, earlier, n_earlier, h, rv);
+  if (st != ZF_OK) return st;
+  auto* zst = reinterpret_cast<zf::ZenState*>(state);
+  const hipStream_t s = as_stream(stream);
+  const Table t{p->d_mats, p->d_off_up, p->nmats};
+  const Table tz{p->d_mats, p->d_off_zen, p->nmats};
+  hipError_t e = zf::launch_cm_update_zen_deferred(t, p->mats[0], p->blk_up,
+                                                   adam_consts(*hp, step), mode, p->d_zs,
+                                                   force_end == 2, h, zst, s);
+  if (e == hipSuccess) e = zf::launch_zen_finalize(tz, p->mats[0], p->blk_zen, p->d_zs, p->d_zb, s);
+  if (e == hipSuccess)
+    e = zf::launch_zen_total(p->d_zb, p->blk_zen, p->k_total, p->u_total, tau,
+                             reinterpret_cast<zf::ZenTotals*>(totals), s, zst,
+                             mode != zf::kInplace ? 1 : 0, static_cast<int32_t>(accum_interval),
+                             force_end);
+  return e == hipSuccess ? ZF_OK : hip_fail(e);
+}
+
+zf_status zf_plan_handover_zen_deferred(zf_plan* p, const zf_plan* const* earlier,
+                                        int32_t n_earlier, const zf_zen_state* state,
+                                        zf_stream stream) {
+  if (p == nullptr || p->layout != zf::kChannelMajor || !p->can_handover || state == nullptr ||
+      !aligned(state, 4))
+    return ZF_EINVAL;
+  zf::HistTable h{};
+  bool rv = false;
+  const zf_status st = gather_earlier(p, earlier, n_earlier, h, rv);
+  if (st != ZF_OK) return st;
+  const hipError_t e = zf::launch_cm_unpack_zen_deferred(
+      Table{p->d_mats, p->d_off_unp, p->nmats}, p->blk_unp, h,
+      reinterpret_cast<const zf::ZenState*>(state), as_stream(stream));
   return e == hipSuccess ? ZF_OK : hip_fail(e);
 }
 

@@ -72,10 +72,12 @@ __device__ __forceinline__ int64_t xcd_remap(int64_t b, int64_t B) {
 template <bool BATCHED>
 __device__ __forceinline__ const DevMat& get_mat(const DevMat* __restrict__ mats,
                                                  const int64_t* __restrict__ off, int32_t nmats,
-                                                 const DevMat& one, int64_t& local) {
+                                                 const DevMat& one, int64_t& local,
+                                                 int32_t& index) {
   const int64_t b = xcd_remap(blockIdx.x, gridDim.x);
   if constexpr (!BATCHED) {
     local = b;
+    index = 0;
     return one;
   } else {
     int lo = 0, hi = nmats - 1;
@@ -84,8 +86,17 @@ __device__ __forceinline__ const DevMat& get_mat(const DevMat* __restrict__ mats
       if (off[mid] <= b) lo = mid; else hi = mid - 1;
     }
     local = b - off[lo];
+    index = lo;
     return mats[lo];
   }
+}
+
+template <bool BATCHED>
+__device__ __forceinline__ const DevMat& get_mat(const DevMat* __restrict__ mats,
+                                                 const int64_t* __restrict__ off, int32_t nmats,
+                                                 const DevMat& one, int64_t& local) {
+  int32_t index;
+  return get_mat<BATCHED>(mats, off, nmats, one, local, index);
 }
 
 // Raw buffer resources (gfx9 family word 3).  A resource is based at the

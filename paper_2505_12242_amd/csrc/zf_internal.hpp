@@ -235,6 +235,17 @@ hipError_t launch_cm_unpack_zen(const Table& t, const DevMat& one, int64_t units
 hipError_t launch_cm_handover_deferred(const Table& t, const DevMat& one, int64_t blocks,
                                        const AdamK& c, float scale, const HistTable& h,
                                        hipStream_t s);
+// Zen-auto on the device with deferred packing (channel-major): the update
+// with the statistics of the interval's running sum taken from the kept
+// gradients (the last position - 1 entries of h); handover: an end the
+// caller forces, scale times that sum written to the hand-over.
+hipError_t launch_cm_update_zen_deferred(const Table& t, const DevMat& one, int64_t blocks,
+                                         const AdamK& c, int32_t mode, double* zs, bool handover,
+                                         const HistTable& h, const ZenState* zst, hipStream_t s);
+// Its gated hand-over (ended == 1): the interval's sums from the kept
+// gradients and the plan's own (unpack table and units).
+hipError_t launch_cm_unpack_zen_deferred(const Table& t, int64_t units, const HistTable& h,
+                                         const ZenState* zst, hipStream_t s);
 // from_stage: the source is the bf16 first-step stage (a one-step interval;
 // every matrix of the table has one).
 hipError_t launch_cm_unpack(const Table& t, const DevMat& one, int64_t blocks, float scale,

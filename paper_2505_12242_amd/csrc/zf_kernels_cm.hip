@@ -440,6 +440,84 @@ __device__ __forceinline__ void cm_swap_out(const DevMat& d, int64_t j, int64_t 
   }
 }
 
+// The sum over steps of an interval whose unselected gradients stayed in
+// their slots: rows [e0, e0 + len) of channel j of the kept gradients of
+// entries s_first .. h.n - 1 of h (oldest first), then of this step's (rG),
+// added in step order in fp32 (the accumulation's own sequence, so the
+// same bits as packing every step).  STATS: ss += the squares of the sums,
+// in fp64; WRITE: scale times the sums to rOut.
+template <int QPT, bool STATS, bool WRITE>
+__device__ __forceinline__ void cm_interval_sum_vec(const HistTable& h, int32_t s_first, int32_t q,
+                                                    int64_t j, int64_t e0, int64_t len,
+                                                    rsrc_t rG, rsrc_t rOut, float scale,
+                                                    double& ss) {
+  const int tid = threadIdx.x;
+  constexpr int kBatch = 4;  // steps whose rows are loaded before they are added
+  float a[QPT][kQuad];
+  const int32_t steps = h.n - s_first + 1;  // the kept steps, then this one
+  for (int32_t s0 = 0; s0 < steps; s0 += kBatch) {
+    u32x2 gv[kBatch][QPT];
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      const int32_t s = s0 + b;
+      if (s < steps) {
+        rsrc_t r = rG;
+        if (s < steps - 1) {
+          const auto& hd = const_table(h.mats[s_first + s])[q];
+          r = make_rsrc(hd.grad + j * hd.ld_grad + e0, len * 2);
+        }
+#pragma unroll
+        for (int p = 0; p < QPT; ++p) gv[b][p] = buf_b64<kAuxRO>(r, quad_elem(p, tid) * 2, 0);
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < kBatch; ++b) {
+      const int32_t s = s0 + b;
+      if (s < steps) {
+#pragma unroll
+        for (int p = 0; p < QPT; ++p) {
+          float g[kQuad];
+          widen4(gv[b][p], g);
+#pragma unroll
+          for (int i = 0; i < kQuad; ++i) a[p][i] = s == 0 ? g[i] : a[p][i] + g[i];
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < QPT; ++p) {
+    if constexpr (STATS) sum_squares(a[p], ss);
+    if constexpr (WRITE) {
+#pragma unroll
+      for (int i = 0; i < kQuad; ++i) a[p][i] = a[p][i] * scale;
+      f32x4_store<kAuxWO>(rOut, quad_elem(p, tid) * 4, a[p]);
+    }
+  }
+}
+
+template <bool STATS, bool WRITE>
+__device__ __forceinline__ void cm_interval_sum_elem(const HistTable& h, int32_t s_first,
+                                                     int32_t q, int64_t j, int64_t e0,
+                                                     int64_t len, rsrc_t rG, rsrc_t rOut,
+                                                     float scale, double& ss) {
+  const int32_t steps = h.n - s_first + 1;
+  for (int64_t e = threadIdx.x; e < len; e += kThreads) {
+    const uint32_t o = static_cast<uint32_t>(e);
+    float a = 0.0f;
+    for (int32_t s = 0; s < steps; ++s) {
+      rsrc_t r = rG;
+      if (s < steps - 1) {
+        const auto& hd = const_table(h.mats[s_first + s])[q];
+        r = make_rsrc(hd.grad + j * hd.ld_grad + e0, len * 2);
+      }
+      const float g = widen_bf16(buf_u16<kAuxRO>(r, o * 2, 0));
+      a = s == 0 ? g : a + g;
+    }
+    if constexpr (STATS) ss = __builtin_fma(static_cast<double>(a), static_cast<double>(a), ss);
+    if constexpr (WRITE) buf_put_f32<kAuxWO>(a * scale, rOut, o * 4, 0);
+  }
+}
+
 // STATS (fused Adam + pack only): every wave also sums, in fp64, the squares
 // of the values its lanes handled -- the gradient of a selected channel, the
 // new accumulated value of an unselected one -- after a fixed xor butterfly,
@@ -474,28 +552,33 @@ __device__ __forceinline__ void cm_swap_out(const DevMat& d, int64_t j, int64_t 
 // fused launches of the fixed schedule pass it, so that each phase is a
 // kernel of its own (its own code, its own name in a profile).
 template <bool BATCHED, bool ADAM, bool PACK, bool STATS, bool HAND, bool PEND, bool SELG,
-          int PH = 0>
+          int PH = 0, bool DEFP = false>
 __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(const DevMat* __restrict__ mats,
                                                             const int64_t* __restrict__ off,
                                                             int32_t nmats, DevMat one, AdamK c,
                                                             int32_t mode, int32_t first,
                                                             double* __restrict__ zs, float scale,
                                                             Pending pd,
-                                                            const ZenState* __restrict__ zst) {
+                                                            const ZenState* __restrict__ zst,
+                                                            HistTable h) {
   static_assert(!SELG || (ADAM && !PACK && !STATS && !PEND), "selected-only grid");
+  static_assert(!DEFP || (BATCHED && ADAM && PACK && STATS && !PEND && !SELG && PH == 0),
+                "deferred packing under Zen-auto on the device");
   // the phase: a compile-time constant, the caller's, or (Zen-auto with the
   // interval driven on the device) 1 after a refresh or an ended interval,
   // else the interval's length so far + 1
   int32_t ph = PH != 0 ? PH : first;
+  int32_t pos = ph;
   if (PH == 0 && zst != nullptr) {
-    const int32_t pos = (mode != kInplace || zst->ended) ? 1 : zst->length + 1;
+    pos = (mode != kInplace || zst->ended) ? 1 : zst->length + 1;
     ph = pos < 3 ? pos : 3;
     // HAND (an interval the caller ends at this step): scale = fp32(1 /
     // length), a correctly rounded fp32 division
     if constexpr (HAND) scale = 1.0f / static_cast<float>(pos);
   }
   int64_t local;
-  const DevMat& d = get_mat<BATCHED>(mats, off, nmats, one, local);
+  int32_t q;
+  const DevMat& d = get_mat<BATCHED>(mats, off, nmats, one, local, q);
   // SELG: one quad per lane, cm_snch chunks per channel; else cm_qpt quads
   const int32_t qpt = SELG ? 1 : d.cm_qpt;
   const int64_t nch = SELG ? d.cm_snch : d.cm_nch;
@@ -524,7 +607,24 @@ __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(c
 
   if (!sel) {
     if (mode == kRemap && d.st_P != nullptr) cm_swap_out(d, j, w, e0, len);
-    if constexpr (PACK) {
+    if constexpr (DEFP) {
+      // deferred packing: the gradient stays in its slot.  The statistics
+      // are taken on the interval's running sum, the sum of its kept steps
+      // (the last pos - 1 entries of h) and this one's; HAND writes scale
+      // times that sum to the hand-over.  Nothing else is written.
+      const int32_t kept = min(max(pos - 1, 0), h.n);
+      const rsrc_t rOut = HAND ? make_rsrc(d.out + j * d.ld_out + e0, len * 4) : rG;
+      if (d.vec) {
+        if (d.cm_qpt >= kCmQpt)
+          cm_interval_sum_vec<kCmQpt, true, HAND>(h, h.n - kept, q, j, e0, len, rG, rOut, scale,
+                                                   ss);
+        else
+          cm_interval_sum_vec<kCmQpt / 2, true, HAND>(h, h.n - kept, q, j, e0, len, rG, rOut,
+                                                       scale, ss);
+      } else {
+        cm_interval_sum_elem<true, HAND>(h, h.n - kept, q, j, e0, len, rG, rOut, scale, ss);
+      }
+    } else if constexpr (PACK) {
       const int64_t u = j - r;
       const rsrc_t rA = make_rsrc(d.acc + u * d.ld_acc + e0, len * 4);
       // the bf16 first-step stage (row j, channel-indexed): ph == 1 on an
@@ -633,70 +733,6 @@ __global__ __launch_bounds__(kThreads) ZF_CM_UPDATE_ATTR void cm_update_kernel(c
 // rows, as in the update.
 // ---------------------------------------------------------------------------
 
-template <int QPT>
-__device__ __forceinline__ void cm_deferred_sum_vec(const HistTable& h, int32_t q, int64_t j,
-                                                    int64_t e0, int64_t len, rsrc_t rG,
-                                                    rsrc_t rOut, float scale) {
-  const int tid = threadIdx.x;
-  constexpr int kBatch = 4;  // steps whose rows are loaded before they are added
-  float a[QPT][kQuad];
-  const int32_t steps = h.n + 1;  // the earlier steps, then this one
-  for (int32_t s0 = 0; s0 < steps; s0 += kBatch) {
-    u32x2 gv[kBatch][QPT];
-#pragma unroll
-    for (int b = 0; b < kBatch; ++b) {
-      const int32_t s = s0 + b;
-      if (s < steps) {
-        rsrc_t r = rG;
-        if (s < h.n) {
-          const auto& hd = const_table(h.mats[s])[q];
-          r = make_rsrc(hd.grad + j * hd.ld_grad + e0, len * 2);
-        }
-#pragma unroll
-        for (int p = 0; p < QPT; ++p) gv[b][p] = buf_b64<kAuxRO>(r, quad_elem(p, tid) * 2, 0);
-      }
-    }
-#pragma unroll
-    for (int b = 0; b < kBatch; ++b) {
-      const int32_t s = s0 + b;
-      if (s < steps) {
-#pragma unroll
-        for (int p = 0; p < QPT; ++p) {
-          float g[kQuad];
-          widen4(gv[b][p], g);
-#pragma unroll
-          for (int i = 0; i < kQuad; ++i) a[p][i] = s == 0 ? g[i] : a[p][i] + g[i];
-        }
-      }
-    }
-  }
-#pragma unroll
-  for (int p = 0; p < QPT; ++p) {
-#pragma unroll
-    for (int i = 0; i < kQuad; ++i) a[p][i] = a[p][i] * scale;
-    f32x4_store<kAuxWO>(rOut, quad_elem(p, tid) * 4, a[p]);
-  }
-}
-
-__device__ __forceinline__ void cm_deferred_sum_elem(const HistTable& h, int32_t q, int64_t j,
-                                                     int64_t e0, int64_t len, rsrc_t rG,
-                                                     rsrc_t rOut, float scale) {
-  for (int64_t e = threadIdx.x; e < len; e += kThreads) {
-    const uint32_t o = static_cast<uint32_t>(e);
-    float a = 0.0f;
-    for (int32_t s = 0; s <= h.n; ++s) {
-      rsrc_t r = rG;
-      if (s < h.n) {
-        const auto& hd = const_table(h.mats[s])[q];
-        r = make_rsrc(hd.grad + j * hd.ld_grad + e0, len * 2);
-      }
-      const float g = widen_bf16(buf_u16<kAuxRO>(r, o * 2, 0));
-      a = s == 0 ? g : a + g;
-    }
-    buf_put_f32<kAuxWO>(a * scale, rOut, o * 4, 0);
-  }
-}
-
 __global__ __launch_bounds__(kThreads) void cm_handover_deferred_kernel(
     const DevMat* __restrict__ mats, const int64_t* __restrict__ off, int32_t nmats, AdamK c,
     float scale, HistTable h) {
@@ -732,10 +768,12 @@ __global__ __launch_bounds__(kThreads) void cm_handover_deferred_kernel(
       cm_adam_elem<kCmInplace, false>(rG, rP, rM, rV, rW, rP, rM, rV, rW, c, len, ss);
     cm_zero_rows(d, rOut, len);
   } else if (d.vec) {
-    if (d.cm_qpt >= kCmQpt) cm_deferred_sum_vec<kCmQpt>(h, q, j, e0, len, rG, rOut, scale);
-    else cm_deferred_sum_vec<kCmQpt / 2>(h, q, j, e0, len, rG, rOut, scale);
+    if (d.cm_qpt >= kCmQpt)
+      cm_interval_sum_vec<kCmQpt, false, true>(h, 0, q, j, e0, len, rG, rOut, scale, ss);
+    else
+      cm_interval_sum_vec<kCmQpt / 2, false, true>(h, 0, q, j, e0, len, rG, rOut, scale, ss);
   } else {
-    cm_deferred_sum_elem(h, q, j, e0, len, rG, rOut, scale);
+    cm_interval_sum_elem<false, true>(h, 0, q, j, e0, len, rG, rOut, scale, ss);
   }
 }
 
@@ -793,6 +831,35 @@ __device__ __forceinline__ void cm_unpack_rows(const DevMat& d, int64_t j, int64
   }
 }
 
+// The same with deferred packing: rows [e0, e0 + len) of channel j of the
+// hand-over are scale times the interval's sum, its kept steps (the last
+// `kept` entries of h) and this plan's gradient, or +0.0 when selected.
+template <int QPT>
+__device__ __forceinline__ void cm_handover_rows_deferred(const DevMat& d, int32_t q, int64_t j,
+                                                          int64_t e0, int64_t len, float scale,
+                                                          const HistTable& h, int32_t kept) {
+  const uint64_t mw = uniform_u64(d.mask[j >> 6]);
+  const rsrc_t rD = make_rsrc(d.out + j * d.ld_out + e0, len * 4);
+  const int tid = threadIdx.x;
+  if ((mw >> (j & 63)) & 1ull) {
+    const float z[kQuad] = {0.f, 0.f, 0.f, 0.f};
+    if (d.vec) {
+#pragma unroll
+      for (int p = 0; p < QPT; ++p) f32x4_store<kAuxWO>(rD, quad_elem(p, tid) * 4, z);
+    } else {
+      for (int64_t e = tid; e < len; e += kThreads)
+        buf_put_f32<kAuxWO>(0.0f, rD, static_cast<uint32_t>(e) * 4, 0);
+    }
+    return;
+  }
+  const rsrc_t rG = make_rsrc(d.grad + j * d.ld_grad + e0, len * 2);
+  double ss = 0.0;  // (no statistics)
+  if (d.vec)
+    cm_interval_sum_vec<QPT, false, true>(h, h.n - kept, q, j, e0, len, rG, rD, scale, ss);
+  else
+    cm_interval_sum_elem<false, true>(h, h.n - kept, q, j, e0, len, rG, rD, scale, ss);
+}
+
 // One unpack block's work: channel local / cm_unch, its chunk local %
 // cm_unch of kCmUnpackChunk rows.
 template <bool STAGE>
@@ -820,15 +887,21 @@ __global__ __launch_bounds__(kThreads) void cm_unpack_kernel(const DevMat* __res
 // stage after a one-step interval when the plan keeps one.  A fixed grid
 // loops over the table's unpack blocks, so that a step that does not end
 // its interval costs one short launch.
+//
+// DEFP (deferred packing): the interval's sums are taken from the kept
+// gradients of its earlier steps (the last length - 1 entries of h) and this
+// plan's gradient, as the deferred update would have written them.
+template <bool DEFP>
 __global__ __launch_bounds__(kThreads) void cm_unpack_zen_kernel(const DevMat* __restrict__ mats,
                                                                 const int64_t* __restrict__ off,
                                                                 int32_t nmats, int64_t units,
                                                                 const ZenState* __restrict__ zst,
-                                                                int32_t stage) {
+                                                                int32_t stage, HistTable h) {
   if (zst->ended != 1) return;
   const int32_t length = zst->length;
   const float scale = 1.0f / static_cast<float>(length);
-  const bool from_stage = stage != 0 && length == 1;
+  const bool from_stage = !DEFP && stage != 0 && length == 1;
+  const int32_t kept = DEFP ? min(max(length - 1, 0), h.n) : 0;
   // each block walks one contiguous run of units, the runs in the
   // XCD-aware block order (XCD x covers one contiguous range, as the
   // full-grid passes do)
@@ -853,11 +926,13 @@ __global__ __launch_bounds__(kThreads) void cm_unpack_zen_kernel(const DevMat* _
     const bool pair = u + 1 < u1 && (local + 1) / d.cm_unch == j;
     const int64_t len = min(static_cast<int64_t>(pair ? 2 : 1) * kCmUnpackChunk, d.n - e0);
     if (pair) {
-      if (from_stage) cm_unpack_rows<true, 2 * kCmUnpackQpt>(d, j, e0, len, scale);
+      if constexpr (DEFP) cm_handover_rows_deferred<2 * kCmUnpackQpt>(d, lo, j, e0, len, scale, h, kept);
+      else if (from_stage) cm_unpack_rows<true, 2 * kCmUnpackQpt>(d, j, e0, len, scale);
       else cm_unpack_rows<false, 2 * kCmUnpackQpt>(d, j, e0, len, scale);
       u += 2;
     } else {
-      if (from_stage) cm_unpack_rows<true, kCmUnpackQpt>(d, j, e0, len, scale);
+      if constexpr (DEFP) cm_handover_rows_deferred<kCmUnpackQpt>(d, lo, j, e0, len, scale, h, kept);
+      else if (from_stage) cm_unpack_rows<true, kCmUnpackQpt>(d, j, e0, len, scale);
       else cm_unpack_rows<false, kCmUnpackQpt>(d, j, e0, len, scale);
       u += 1;
     }
@@ -905,11 +980,11 @@ static void launch_cm_update_t(const Table& t, const DevMat& one, dim3 grid, con
   if (t.mats != nullptr)
     hipLaunchKernelGGL((cm_update_kernel<true, ADAM, PACK, STATS, HAND, PEND, SELG, PH>), grid,
                        dim3(kThreads), kCmUpdateLds, s, t.mats, t.off, t.nmats, one, c, mode,
-                       first, zs, scale, pd, zst);
+                       first, zs, scale, pd, zst, HistTable{});
   else
     hipLaunchKernelGGL((cm_update_kernel<false, ADAM, PACK, STATS, HAND, PEND, SELG, PH>), grid,
                        dim3(kThreads), kCmUpdateLds, s, t.mats, t.off, t.nmats, one, c, mode,
-                       first, zs, scale, pd, zst);
+                       first, zs, scale, pd, zst, HistTable{});
 }
 
 // The fused update (HAND: with the hand-over) with its interval phase as a
@@ -1003,6 +1078,25 @@ hipError_t launch_cm_handover_deferred(const Table& t, const DevMat& one, int64_
   return hipGetLastError();
 }
 
+hipError_t launch_cm_update_zen_deferred(const Table& t, const DevMat& one, int64_t blocks,
+                                         const AdamK& c, int32_t mode, double* zs, bool handover,
+                                         const HistTable& h, const ZenState* zst,
+                                         hipStream_t s) {
+  (void)hipGetLastError();
+  if (blocks <= 0 || t.mats == nullptr) return hipSuccess;
+  if (zs == nullptr || zst == nullptr) return hipErrorInvalidValue;
+  const dim3 grid(static_cast<uint32_t>(blocks));
+  if (handover)
+    hipLaunchKernelGGL((cm_update_kernel<true, true, true, true, true, false, false, 0, true>),
+                       grid, dim3(kThreads), kCmUpdateLds, s, t.mats, t.off, t.nmats, one, c,
+                       mode, 1, zs, 1.0f, Pending{}, zst, h);
+  else
+    hipLaunchKernelGGL((cm_update_kernel<true, true, true, true, false, false, false, 0, true>),
+                       grid, dim3(kThreads), kCmUpdateLds, s, t.mats, t.off, t.nmats, one, c,
+                       mode, 1, zs, 1.0f, Pending{}, zst, h);
+  return hipGetLastError();
+}
+
 constexpr int64_t kCmUnpackZenGrid = 4096;  // 16 blocks per CU
 
 hipError_t launch_cm_unpack_zen(const Table& t, const DevMat& one, int64_t units,
@@ -1011,8 +1105,18 @@ hipError_t launch_cm_unpack_zen(const Table& t, const DevMat& one, int64_t units
   (void)one;
   if (units <= 0 || t.mats == nullptr) return hipSuccess;
   const dim3 grid(static_cast<uint32_t>(units < kCmUnpackZenGrid ? units : kCmUnpackZenGrid));
-  hipLaunchKernelGGL(cm_unpack_zen_kernel, grid, dim3(kThreads), 0, s, t.mats, t.off, t.nmats,
-                     units, zst, stage ? 1 : 0);
+  hipLaunchKernelGGL(cm_unpack_zen_kernel<false>, grid, dim3(kThreads), 0, s, t.mats, t.off,
+                     t.nmats, units, zst, stage ? 1 : 0, HistTable{});
+  return hipGetLastError();
+}
+
+hipError_t launch_cm_unpack_zen_deferred(const Table& t, int64_t units, const HistTable& h,
+                                         const ZenState* zst, hipStream_t s) {
+  (void)hipGetLastError();
+  if (units <= 0 || t.mats == nullptr) return hipSuccess;
+  const dim3 grid(static_cast<uint32_t>(units < kCmUnpackZenGrid ? units : kCmUnpackZenGrid));
+  hipLaunchKernelGGL(cm_unpack_zen_kernel<true>, grid, dim3(kThreads), 0, s, t.mats, t.off,
+                     t.nmats, units, zst, 0, h);
   return hipGetLastError();
 }
 

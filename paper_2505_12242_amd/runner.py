@@ -18,7 +18,10 @@ stays in its gradient slot, every step but an interval's last runs the
 Adam part alone, and the last step sums the interval's gradients (in step
 order, the accumulation's own fp32 sequence) straight into the hand-over
 (zf_plan_update_handover_deferred).  The slots must hold every gradient of
-an interval: at least min(S, R) of them.
+an interval: at least min(S, R) of them.  With Zen-auto decided on the
+device (channel-major), every step sums the interval's kept gradients again
+for the statistics and nothing is packed (zf_plan_update_zen_deferred,
+zf_plan_handover_zen_deferred).
 
 Compact states and selections are double-buffered: a refresh writes the new
 selection and new states into the other buffer while reading the previous
@@ -192,12 +195,15 @@ class SelectiveUpdateRunner:
         # deferred packing (fixed schedule, hand-over fused, no offload): the
         # unselected part of every step's gradient stays in its slot until
         # the interval ends; the interval's last step sums them
+        # (Zen-auto: decided on the device, channel-major; each step sums the
+        # interval's kept gradients again for the statistics)
         self.deferred = bool(deferred_pack)
         if self.deferred:
-            if (zen_tau is not None or self.offload or not self.keep_unpacked
-                    or not self.fuse_handover):
-                raise ValueError("deferred packing runs on the fixed schedule with the fused "
-                                 "hand-over, without offload")
+            zen_ok = (zen_tau is None or (bool(zen_on_device) and layout != ROW_MAJOR))
+            if not zen_ok or self.offload or not self.keep_unpacked or not self.fuse_handover:
+                raise ValueError("deferred packing runs on the fixed schedule, or with Zen-auto "
+                                 "decided on the device in the channel-major layout, with the "
+                                 "fused hand-over, without offload")
             if len(grad_slots) < min(self.S, self.R):
                 raise ValueError("deferred packing keeps every gradient of an interval: it needs "
                                  f"at least min(S, R) = {min(self.S, self.R)} gradient slots")
@@ -209,7 +215,8 @@ class SelectiveUpdateRunner:
         # and (channel-major) into the hand-over buffer when the step is a
         # whole interval
         self.score_pack = self.use_stage and zen_tau is None and self.fuse_handover
-        self.score_handover = (self.score_pack or self.deferred) and layout != ROW_MAJOR
+        self.score_handover = ((self.score_pack or self.deferred) and layout != ROW_MAJOR
+                               and zen_tau is None)
         self._in_stage = False  # the current interval's sums are in the stage
         self.weights = list(weights)
         self.init_master = list(init_master) if init_master is not None else None
@@ -444,12 +451,27 @@ class SelectiveUpdateRunner:
             # gated hand-over does nothing)
             force_end = (t % self.R == 0) or t <= self.warmup
             fuse = force_end and self.keep_unpacked and self.fuse_handover
-            with rec("update_zen"):
-                plan.update_zen_device(self.hp, t, mode, self.S, 2 if fuse else int(force_end),
-                                       self.zen_tau, self.zen_totals, self.zen_state, stream=st)
-            if self.keep_unpacked:
+            if self.deferred:
+                # the plans of the steps an interval can still reach back to
+                # (the device reads the last position - 1 of them)
+                nsl = len(self.grad_slots)
+                first = max(1, t - (min(self.S, self.R) - 1))
+                earlier = [self.plans[(tt - 1) % nsl][self.cur][self.cur_a]
+                           for tt in range(first, t)]
+                with rec("update_zen"):
+                    plan.update_zen_deferred(self.hp, t, mode, self.S, earlier,
+                                             2 if fuse else int(force_end), self.zen_tau,
+                                             self.zen_totals, self.zen_state, stream=st)
                 with rec("handover_zen"):
-                    plan.handover_zen(self.zen_state, st)
+                    plan.handover_zen_deferred(earlier, self.zen_state, st)
+            else:
+                with rec("update_zen"):
+                    plan.update_zen_device(self.hp, t, mode, self.S,
+                                           2 if fuse else int(force_end), self.zen_tau,
+                                           self.zen_totals, self.zen_state, stream=st)
+                if self.keep_unpacked:
+                    with rec("handover_zen"):
+                        plan.handover_zen(self.zen_state, st)
             host = torch.empty(2 + ZEN_TOTALS_BYTES // 4, dtype=torch.int32, pin_memory=True)
             with torch.cuda.stream(st):
                 host[:2].copy_(self.zen_state, non_blocking=True)

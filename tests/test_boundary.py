@@ -257,9 +257,10 @@ def test_plan_validation():
 
 
 def test_plan_entry_points_reject_a_missing_plan():
-    """The deferred hand-over and the device-driven Zen-auto calls validate
-    on the host: no plan, no state, a bad count or scale give ZF_EINVAL and
-    nothing is enqueued (no GPU is touched)."""
+    """The deferred hand-over and the device-driven Zen-auto calls (with and
+    without deferred packing) validate on the host: no plan, no state, a bad
+    count or scale give ZF_EINVAL and nothing is enqueued (no GPU is
+    touched)."""
     hp = _lib.ZfAdamHparams(1e-5, 0.9, 0.999, 1e-8, 0.0)
     hs = (ctypes.c_void_p * 16)()
     for n_earlier in (0, 1, 15, 16):
@@ -270,8 +271,13 @@ def test_plan_entry_points_reject_a_missing_plan():
     assert LIB.zf_plan_update_zen_device(None, ctypes.byref(hp), 1, 0, 4, 0, 1.0, None, None,
                                          None) == EINVAL
     assert LIB.zf_plan_handover_zen(None, None, None) == EINVAL
+    for n_earlier in (0, 1, 15, 16, -1):
+        assert LIB.zf_plan_update_zen_deferred(None, ctypes.byref(hp), 1, 0, 4, hs, n_earlier,
+                                               2, 1.0, None, None, None) == EINVAL
+        assert LIB.zf_plan_handover_zen_deferred(None, hs, n_earlier, None, None) == EINVAL
     for name in ("zf_plan_update_handover_deferred", "zf_plan_update_zen_device",
-                 "zf_plan_handover_zen"):
+                 "zf_plan_handover_zen", "zf_plan_update_zen_deferred",
+                 "zf_plan_handover_zen_deferred"):
         assert name in header_functions()
 
 

@@ -127,3 +127,32 @@ def test_deferred_packing_bytes():
     # a refresh step that is a whole interval hands over from the score pass
     b = bench.step_bytes(sh, ks, True, True, True, length=1, **kw)
     assert b["colnorm"] == 6 * n * m + 4 * m and b["update"] == 32 * n * k
+
+
+def test_zen_deferred_packing_bytes():
+    """Zen-auto with deferred packing: a step at position p of its interval
+    reads the kept gradients at the unselected elements (2p B each) for the
+    statistics and writes nothing for them; an end the caller forces writes
+    the hand-over from the update (4 B per element, zeros at the selected),
+    any other end from the gated pass, which reads the p gradients again.
+    Over an interval of 4 steps ended by force that is 24 B per unselected
+    element, against 32 when packing every step with the stage."""
+    n, m, k = 4096, 4096, 410
+    u = m - k
+    sh, ks = [(n, m)], [k]
+    kw = dict(deferred=True, zen=True)
+    b = bench.step_bytes(sh, ks, True, True, False, length=1, **kw)
+    assert b == {"colnorm": 2 * n * m + 4 * m, "topk_select": 8 * m + 12 * 64,
+                 "update": 28 * n * k + 2 * n * u, "unpack": 0}
+    for p in (2, 3, 6):
+        assert bench.step_bytes(sh, ks, False, False, False, length=p, **kw)["update"] == \
+            28 * n * k + 2 * p * n * u
+        forced = bench.step_bytes(sh, ks, False, False, True, length=p, fused_handover=True, **kw)
+        assert forced["update"] == 28 * n * k + 4 * n * k + (2 * p + 4) * n * u
+        assert forced["unpack"] == 0
+        trig = bench.step_bytes(sh, ks, False, False, True, length=p, **kw)
+        assert trig["update"] == 28 * n * k + 2 * p * n * u
+        assert trig["unpack"] == 2 * p * n * u + 4 * n * m
+    per_u = sum(bench.step_bytes([(1, 1000)], [0], False, p == 1, p == 4, length=p,
+                                 fused_handover=p == 4, **kw)["update"] for p in (1, 2, 3, 4))
+    assert per_u == 24 * 1000

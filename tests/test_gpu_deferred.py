@@ -198,8 +198,13 @@ def test_deferred_needs_the_interval_in_the_ring():
     with pytest.raises(ValueError, match="gradient slots"):
         zf.SelectiveUpdateRunner(SHAPES[:2], 0.1, HP, 4, 4, slots, weights, layout=CM,
                                  deferred_pack=True)
+    # Zen-auto with deferred packing: decided on the device, channel-major only
     with pytest.raises(ValueError, match="fixed schedule"):
         zf.SelectiveUpdateRunner(SHAPES[:2], 0.1, HP, 4, 4, slots, weights, layout=CM,
+                                 zen_tau=1.0, zen_on_device=False, deferred_pack=True)
+    rslots, _, rweights, _ = inputs(SHAPES[:2], 4, 5, variant="rm-col")
+    with pytest.raises(ValueError, match="fixed schedule"):
+        zf.SelectiveUpdateRunner(SHAPES[:2], 0.1, HP, 4, 4, rslots, rweights, layout=RM,
                                  zen_tau=1.0, deferred_pack=True)
 
 

@@ -12,7 +12,10 @@ row-major layout):
   wherever the oracle's comparison is not within 1e-9 of a tie;
 * the schedule it drives (interval lengths, ends, hand-over scale) and every
   state, packed buffer, weight and hand-over bit for bit, as in the fixed
-  schedule.
+  schedule;
+* channel-major with deferred packing (zf_plan_update_zen_deferred): the
+  unselected channels' statistics from the interval's kept gradients summed
+  again at every step; the same checks, nothing packed.
 
 Shapes mix the vector path (n % 8 == 0, one and several row chunks per
 channel) with the element-wise path (n % 8 != 0), k = 0 matrices (m < 5 at
@@ -104,13 +107,15 @@ def fixed_ends(T, R, S_max):
     return ends
 
 
-def run_zen(shapes, ratio, R, S_max, tau, T, seed, host_in=None, layout=None, on_device=True):
+def run_zen(shapes, ratio, R, S_max, tau, T, seed, host_in=None, layout=None, on_device=True,
+            deferred=False):
     layout = zf.CHANNEL_MAJOR if layout is None else layout
     dev = torch.device("cuda")
     hp = zf.AdamHparams(lr=1e-3)
     slots, host, weights, w0 = host_in or _inputs(shapes, ratio, T, seed, dev, layout)
     runner = zf.SelectiveUpdateRunner(shapes, ratio, hp, R, S_max, slots, weights, device=dev,
-                                      layout=layout, zen_tau=tau, zen_on_device=on_device)
+                                      layout=layout, zen_tau=tau, zen_on_device=on_device,
+                                      deferred_pack=deferred)
     # the interval decided on the device unless asked otherwise
     assert runner.zen_device == on_device
     za = _oracle(shapes, w0, ratio, hp, R, S_max, tau)
@@ -148,7 +153,8 @@ def run_zen(shapes, ratio, R, S_max, tau, T, seed, host_in=None, layout=None, on
             # (an end the caller forces is handed over by the update itself,
             # which leaves the packed buffer as it was; the hand-over below
             # carries the sums)
-            if not (kind.interval_end and getattr(kind, "fused", False)):
+            # (deferred packing writes no packed buffer)
+            if not deferred and not (kind.interval_end and getattr(kind, "fused", False)):
                 assert same_bits(_host(runner.acc[q], layout).numpy(), orc.A), ("acc", q, t)
             wl = runner.weights[q] if layout == zf.ROW_MAJOR else runner.weights[q].t()
             assert same_bits(bits_np(wl), orc.W), ("weight", q, t)
@@ -162,19 +168,20 @@ def run_zen(shapes, ratio, R, S_max, tau, T, seed, host_in=None, layout=None, on
 
 LAYOUTS = [pytest.param(zf.ROW_MAJOR, id="rm"), pytest.param(zf.CHANNEL_MAJOR, id="cm")]
 # the interval decided on the device (the default) and on the host
-LAYOUT_MODES = [pytest.param(zf.ROW_MAJOR, True, id="rm-device"),
-                pytest.param(zf.ROW_MAJOR, False, id="rm-host"),
-                pytest.param(zf.CHANNEL_MAJOR, True, id="cm-device"),
-                pytest.param(zf.CHANNEL_MAJOR, False, id="cm-host")]
+LAYOUT_MODES = [pytest.param(zf.ROW_MAJOR, True, False, id="rm-device"),
+                pytest.param(zf.ROW_MAJOR, False, False, id="rm-host"),
+                pytest.param(zf.CHANNEL_MAJOR, True, False, id="cm-device"),
+                pytest.param(zf.CHANNEL_MAJOR, False, False, id="cm-host"),
+                pytest.param(zf.CHANNEL_MAJOR, True, True, id="cm-device-deferred")]
 
 
 @pytest.mark.timeout(600)
 @pytest.mark.parametrize("tau", [0.0, math.inf])
-@pytest.mark.parametrize("layout,on_device", LAYOUT_MODES)
-def test_zen_auto_extreme_thresholds(tau, layout, on_device):
+@pytest.mark.parametrize("layout,on_device,deferred", LAYOUT_MODES)
+def test_zen_auto_extreme_thresholds(tau, layout, on_device, deferred):
     T, R, S_max = 9, 4, 3
     ends, exact, total = run_zen(SHAPES, 0.1, R, S_max, tau, T, seed=11, layout=layout,
-                                 on_device=on_device)
+                                 on_device=on_device, deferred=deferred)
     if tau == 0.0:
         assert all(ends)
     else:
@@ -185,8 +192,8 @@ def test_zen_auto_extreme_thresholds(tau, layout, on_device):
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("layout,on_device", LAYOUT_MODES)
-def test_zen_auto_threshold_between_observed_ratios(layout, on_device):
+@pytest.mark.parametrize("layout,on_device,deferred", LAYOUT_MODES)
+def test_zen_auto_threshold_between_observed_ratios(layout, on_device, deferred):
     """tau between the ratios the fixed schedule produces after one and after
     several accumulated steps: the trigger fires mid-interval."""
     T, R, S_max, ratio = 10, 16, 6, 0.1
@@ -197,7 +204,7 @@ def test_zen_auto_threshold_between_observed_ratios(layout, on_device):
     assert hi > lo
     tau = math.sqrt(lo * hi)
     ends, _, _ = run_zen(SHAPES, ratio, R, S_max, tau, T, seed=12, host_in=inputs, layout=layout,
-                         on_device=on_device)
+                         on_device=on_device, deferred=deferred)
     assert any(ends) and not all(ends)
     # at least one interval ended by the trigger before reaching S_max
     lengths, cur = [], 0
@@ -211,11 +218,14 @@ def test_zen_auto_threshold_between_observed_ratios(layout, on_device):
 
 @pytest.mark.timeout(300)
 @pytest.mark.parametrize("ratio", [0.0, 1.0])
-@pytest.mark.parametrize("layout", LAYOUTS)
-def test_zen_auto_one_part_empty(ratio, layout):
+@pytest.mark.parametrize("layout,deferred", [(zf.ROW_MAJOR, False), (zf.CHANNEL_MAJOR, False),
+                                             (zf.CHANNEL_MAJOR, True)],
+                         ids=["rm", "cm", "cm-deferred"])
+def test_zen_auto_one_part_empty(ratio, layout, deferred):
     """k = 0 (nothing selected) or k = m (nothing accumulated): the trigger
     never fires and the schedule is the fixed one."""
-    ends, _, _ = run_zen(SHAPES[:3], ratio, 4, 2, 0.0, 5, seed=13, layout=layout)
+    ends, _, _ = run_zen(SHAPES[:3], ratio, 4, 2, 0.0, 5, seed=13, layout=layout,
+                         deferred=deferred)
     assert ends == fixed_ends(5, 4, 2) == [False, True, False, True, False]
 
 
@@ -240,7 +250,7 @@ def test_zen_auto_deterministic(layout):
 
 
 @pytest.mark.timeout(300)
-@pytest.mark.parametrize("storage", ["cm", "rm", "rm-16B"])
+@pytest.mark.parametrize("storage", ["cm", "cm-deferred", "rm", "rm-16B"])
 @pytest.mark.parametrize("case", ["early-end", "warmup"])
 def test_zen_auto_on_device_needs_no_host_round_trip(case, storage):
     """The device-decided interval: steps are enqueued without reading
@@ -248,11 +258,14 @@ def test_zen_auto_on_device_needs_no_host_round_trip(case, storage):
     resolving them afterwards gives the host-decided run's positions, ends,
     hand-overs and states bit for bit -- with a threshold between the
     observed ratios (intervals ended by the trigger before S_max), and with
-    a two-step warm-up.  Channel-major, and row-major on the per-column
+    a two-step warm-up.  Channel-major (packing every step, and deferred
+    packing: the device run keeps the interval's gradients in their slots
+    and sums them for the statistics), and row-major on the per-column
     update (unpadded rows) and on the 16-byte update (16-byte rows)."""
     dev = torch.device("cuda")
-    layout = zf.CHANNEL_MAJOR if storage == "cm" else zf.ROW_MAJOR
+    layout = zf.CHANNEL_MAJOR if storage.startswith("cm") else zf.ROW_MAJOR
     padded = storage == "rm-16B"
+    deferred = storage == "cm-deferred"
     if case == "early-end":
         T, R, S_max, warmup = 10, 16, 6, 0
         inputs = _inputs(SHAPES, 0.1, T, 12, dev, layout, padded)
@@ -267,7 +280,8 @@ def test_zen_auto_on_device_needs_no_host_round_trip(case, storage):
         ws = [w.clone() for w in weights]
         runner = zf.SelectiveUpdateRunner(SHAPES, 0.1, zf.AdamHparams(lr=1e-3), R, S_max, slots,
                                           ws, device=dev, layout=layout, zen_tau=tau,
-                                          warmup=warmup, zen_on_device=on_device)
+                                          warmup=warmup, zen_on_device=on_device,
+                                          deferred_pack=deferred and on_device)
         assert runner.zen_device == on_device
         kinds, hand = [], []
         for t in range(T):
@@ -345,6 +359,48 @@ def test_zen_auto_rejects_bad_arguments():
     assert (tot.k_total, tot.u_total) == (10, 90)
     assert tot.sum_sel == 0.0 and tot.sum_acc == 0.0 and tot.trigger  # 0 >= tau * 0
     plan.close()
+
+
+def test_zen_deferred_rejects_bad_arguments():
+    """zf_plan_update_zen_deferred / zf_plan_handover_zen_deferred validate on
+    the host, with nothing enqueued: a plan without `unpacked` or a row-major
+    plan, more than 15 earlier plans, an earlier plan over other matrices, a
+    bad force_end or tau, a missing state."""
+    dev = torch.device("cuda")
+    totals = torch.zeros(5, dtype=torch.int64, device=dev)
+    state = torch.tensor([0, 1], dtype=torch.int32, device=dev)
+    hp = zf.AdamHparams()
+
+    def with_out(layout):
+        b = _plan_buffers(layout)
+        n, m = 64, 100
+        b.unpacked = torch.zeros(*((n, m) if layout == zf.ROW_MAJOR else (m, n)),
+                                 dtype=torch.float32, device=dev)
+        return b
+
+    plan = zf.Plan([with_out(zf.CHANNEL_MAJOR)])
+    other = zf.Plan([with_out(zf.CHANNEL_MAJOR), with_out(zf.CHANNEL_MAJOR)])
+    rm = zf.Plan([with_out(zf.ROW_MAJOR)])
+    no_out = zf.Plan([_plan_buffers(zf.CHANNEL_MAJOR)])
+    before = state.clone()
+    bad = [
+        (rm, [], 2, 1.0, state),              # row-major
+        (no_out, [], 2, 1.0, state),          # no hand-over buffer
+        (plan, [plan] * 16, 2, 1.0, state),   # more than 15 earlier plans
+        (plan, [other], 2, 1.0, state),       # other matrices
+        (plan, [], 3, 1.0, state),            # force_end
+        (plan, [], 2, -1.0, state),           # tau
+    ]
+    for pl, earlier, fe, tau, st in bad:
+        with pytest.raises(zf.ZfError, match="invalid argument"):
+            pl.update_zen_deferred(hp, 1, zf.STATES_INIT, 4, earlier, fe, tau, totals, st)
+    for pl, earlier in ((rm, []), (no_out, []), (plan, [plan] * 16), (plan, [other])):
+        with pytest.raises(zf.ZfError, match="invalid argument"):
+            pl.handover_zen_deferred(earlier, state)
+    torch.cuda.synchronize()
+    assert torch.equal(state, before)
+    for pl in (plan, other, rm, no_out):
+        pl.close()
 
 
 def test_rowmajor_fused_statistics_equal_separate_pass():
