@@ -243,3 +243,53 @@ def test_full_set_deferred_equals_every_step_over_48_steps(lay):
         del runner, slots, weights, out
     del kept
     torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(900)
+def test_full_set_zen_deferred_equals_every_step():
+    """Zen-auto over the whole 7B set in bench.py's launch configuration for
+    it (channel-major, decided on the device, tau = 1, R = S = 4, a four-slot
+    ring), 16 steps, once with deferred packing (bench.py's default there)
+    and once packing every step: the same interval positions and ends and
+    the same 40-byte totals at every step, and at the end every matrix's W,
+    compact states, selection and hand-over equal bit for bit (torch.equal
+    on the device, all 226 matrices)."""
+    from workloads import get_workload
+    wl = get_workload("llama2-7b-full")
+    hp = zf.AdamHparams(wl.hyper.lr, wl.hyper.beta1, wl.hyper.beta2, wl.hyper.eps,
+                        wl.hyper.weight_decay)
+    dev = torch.device("cuda")
+    steps, nslots = 16, 4
+    kept = None
+    for deferred in (True, False):
+        torch.cuda.empty_cache()
+        shapes, ks, slots, weights = bench.build_set(wl, nslots, dev, zf.CHANNEL_MAJOR)
+        runner = zf.SelectiveUpdateRunner(shapes, wl.ratio, hp, wl.refresh, wl.accum, slots,
+                                          weights, device=dev, layout=zf.CHANNEL_MAJOR,
+                                          zen_tau=1.0, deferred_pack=deferred)
+        assert runner.zen_device and runner.deferred == deferred
+        seq = []
+        for t in range(1, steps + 1):
+            kind = runner.step()
+            tot = runner.last_totals  # resolves the step (a read-back after it)
+            seq.append((kind.refresh, kind.step_in_interval, kind.interval_end,
+                        tot.k_total, tot.u_total, tot.sum_sel, tot.sum_acc, tot.trigger))
+        torch.cuda.synchronize()
+        assert seq[-1][2]  # the last step ends an interval (a refresh follows)
+        print(f"# zen full set deferred={deferred}: {steps} steps, ends at "
+              f"{[t + 1 for t, s in enumerate(seq) if s[2]]}", file=sys.stderr, flush=True)
+        out = [(weights[q], *runner.state[q], runner.unpacked[q],
+                runner.selection[q].sel_idx) for q in range(len(shapes))]
+        if kept is None:
+            kept = (seq, [tuple(x.clone() for x in o) for o in out])
+        else:
+            assert seq == kept[0]
+            bits = {torch.float32: torch.int32, torch.bfloat16: torch.int16}
+            for q, (a, b) in enumerate(zip(kept[1], out)):
+                for x, y in zip(a, b):
+                    assert torch.equal(x.view(bits.get(x.dtype, x.dtype)),
+                                       y.view(bits.get(y.dtype, y.dtype))), q
+        runner.close()
+        del runner, slots, weights, out
+    del kept
+    torch.cuda.empty_cache()
