@@ -522,7 +522,7 @@ def launch_kernels(kind: str, channel_major: bool, deferred: bool) -> str:
         if kind == "update_adam":
             return "cm_update_kernel, selected-only grid (Adam + bf16 write-back)"
         if kind == "update":
-            return ("cm_update_kernel<true, true, true, false, false, false, false, 3> "
+            return ("cm_update_kernel<true, true, true, false, false, false, false, 3, false> "
                     "(fused Adam + bf16 write-back + pack)")
         return f"cm_update_kernel ({kind}) (fused Adam + bf16 write-back + pack)"
     if deferred and kind == "update_handover":
