@@ -11,7 +11,11 @@
 //     interval with the fused hand-over (scale 0.5): the hand-over is +0.0
 //     at selected channels and 0.5 * (g1 + g2) at the others (exact fp32
 //     operations), the packed buffer keeps g1;
-//   * the plan over two matrices gives the same bits as the single calls.
+//   * the plan over two matrices gives the same bits as the single calls;
+//   * so do plans with deferred packing (zf_plan_update_handover_deferred)
+//     and, channel-major, Zen-auto on the device with deferred packing
+//     (zf_plan_update_zen_deferred ending the interval by force at step 2,
+//     zf_plan_handover_zen_deferred then writing nothing).
 // Built by __graft_entry__.build() next to this file; run by
 // tests/test_gpu_abi_native.py.
 #include <hip/hip_runtime.h>
@@ -20,6 +24,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <limits>
 #include <random>
 #include <vector>
 
@@ -346,6 +351,72 @@ int main() {
     zf_plan_destroy(plan4);
     HIP_OK(hipFree(mem3));
     HIP_OK(hipFree(mem4));
+    if (layout == ZF_LAYOUT_CHANNEL_MAJOR) {
+      // Zen-auto on the device with deferred packing: step 1 refreshes (no
+      // end: tau = inf never triggers), step 2 ends the interval by force
+      // with the hand-over fused -- again the single calls' bits; the gated
+      // hand-over then writes nothing
+      Mat za = make(264, 300, 0.1, layout, 11), zb = make(43, 77, 0.2, layout, 12);
+      Mat* zm[2] = {&za, &zb};
+      std::vector<float*> stats;
+      for (int q = 0; q < 2; ++q) {
+        desc[q].grad = zm[q]->G1;
+        desc[q].weight = zm[q]->W;
+        desc[q].master = zm[q]->P;
+        desc[q].exp_avg = zm[q]->M;
+        desc[q].exp_avg_sq = zm[q]->V;
+        desc[q].norms_sq = zm[q]->norms;
+        desc[q].sel = zm[q]->sel;
+        desc[q].unpacked = zm[q]->D;
+        desc[q].sel_sq = dev_alloc<float>(zm[q]->k);
+        desc[q].acc_sq = dev_alloc<float>(zm[q]->m - zm[q]->k);
+        stats.push_back(desc[q].sel_sq);
+        stats.push_back(desc[q].acc_sq);
+      }
+      size_t bytes5 = 0, bytes6 = 0;
+      ZF_OK_(zf_plan_query(desc, 2, &bytes5));
+      void* mem5 = nullptr;
+      HIP_OK(hipMalloc(&mem5, bytes5));
+      zf_plan* plan5 = nullptr;
+      ZF_OK_(zf_plan_create(desc, 2, mem5, bytes5, s, &plan5));
+      desc[0].grad = za.G2;
+      desc[1].grad = zb.G2;
+      ZF_OK_(zf_plan_query(desc, 2, &bytes6));
+      void* mem6 = nullptr;
+      HIP_OK(hipMalloc(&mem6, bytes6));
+      zf_plan* plan6 = nullptr;
+      ZF_OK_(zf_plan_create(desc, 2, mem6, bytes6, s, &plan6));
+      zf_zen_totals* tot = dev_alloc<zf_zen_totals>(1);
+      zf_zen_state* st = dev_alloc<zf_zen_state>(1);
+      const zf_zen_state st0{0, 1};
+      HIP_OK(hipMemcpy(st, &st0, sizeof st0, hipMemcpyHostToDevice));
+      const double inf = std::numeric_limits<double>::infinity();
+      ZF_OK_(zf_plan_colnorm(plan5, s));
+      ZF_OK_(zf_plan_topk_select(plan5, s));
+      ZF_OK_(zf_plan_update_zen_deferred(plan5, &kHp, 1, ZF_STATES_INIT, 4, nullptr, 0, 0, inf,
+                                         tot, st, s));
+      ZF_OK_(zf_plan_handover_zen_deferred(plan5, nullptr, 0, st, s));
+      const zf_plan* zearlier[1] = {plan5};
+      ZF_OK_(zf_plan_update_zen_deferred(plan6, &kHp, 2, ZF_STATES_INPLACE, 4, zearlier, 1, 2,
+                                         inf, tot, st, s));
+      ZF_OK_(zf_plan_handover_zen_deferred(plan6, zearlier, 1, st, s));
+      HIP_OK(hipStreamSynchronize(s));
+      zf_zen_state st2{};
+      HIP_OK(hipMemcpy(&st2, st, sizeof st2, hipMemcpyDeviceToHost));
+      CHECK(st2.length == 2 && st2.ended == 2);
+      CHECK(same_bits(down(za.D, za.n * za.m), Da) && same_bits(down(zb.D, zb.n * zb.m), Db));
+      CHECK(same_bits(down(za.W, za.n * za.m), Wa) && same_bits(down(zb.W, zb.n * zb.m), Wb));
+      zf_plan_destroy(plan5);
+      zf_plan_destroy(plan6);
+      HIP_OK(hipFree(mem5));
+      HIP_OK(hipFree(mem6));
+      HIP_OK(hipFree(tot));
+      HIP_OK(hipFree(st));
+      for (float* p : stats) HIP_OK(hipFree(p));
+      for (int q = 0; q < 2; ++q) desc[q].sel_sq = desc[q].acc_sq = nullptr;
+      release(za);
+      release(zb);
+    }
     for (Mat* x : {&a, &b, &pa, &pb, &da, &db}) release(*x);
   }
   HIP_OK(hipStreamDestroy(s));
@@ -353,6 +424,7 @@ int main() {
     std::fprintf(stderr, "%d failures\n", failures);
     return 1;
   }
-  std::printf("abi smoke ok: both layouts, single calls, plans, deferred packing\n");
+  std::printf("abi smoke ok: both layouts, single calls, plans, deferred packing, "
+              "Zen-auto with deferred packing\n");
   return 0;
 }
