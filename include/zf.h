@@ -747,8 +747,9 @@ zf_status zf_plan_update_zen_deferred(zf_plan* plan, const zf_adam_hparams* hp, 
  * fp32, +0.0 at the selected channels: bit for bit what packing every step
  * and zf_plan_handover_zen give.  Else nothing is written; a fixed grid, so
  * that a step that does not end its interval costs one short launch.
- * earlier as in zf_plan_update_zen_deferred; channel-major plans with
- * `unpacked`; ZF_EINVAL otherwise. */
+ * earlier as in zf_plan_update_zen_deferred; channel-major plans that
+ * zf_plan_update_zen_deferred accepts (gradient, selection, states,
+ * `unpacked`); ZF_EINVAL otherwise. */
 zf_status zf_plan_handover_zen_deferred(zf_plan* plan, const zf_plan* const* earlier,
                                         int32_t n_earlier, const zf_zen_state* state,
                                         zf_stream stream);

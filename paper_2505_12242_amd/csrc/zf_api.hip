@@ -1559,8 +1559,9 @@ zf_status zf_plan_update_zen_deferred(zf_plan* p, const zf_adam_hparams* hp, int
 zf_status zf_plan_handover_zen_deferred(zf_plan* p, const zf_plan* const* earlier,
                                         int32_t n_earlier, const zf_zen_state* state,
                                         zf_stream stream) {
-  if (p == nullptr || p->layout != zf::kChannelMajor || !p->can_handover || state == nullptr ||
-      !aligned(state, 4))
+  // (the gradient, the selection mask and `unpacked`, as the update it follows)
+  if (p == nullptr || p->layout != zf::kChannelMajor || !p->can_adam || !p->can_handover ||
+      state == nullptr || !aligned(state, 4))
     return ZF_EINVAL;
   zf::HistTable h{};
   bool rv = false;
