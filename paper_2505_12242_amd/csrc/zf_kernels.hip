@@ -21,7 +21,17 @@ namespace {
 // rounds once to fp32.  No atomics: the result is deterministic.
 // ---------------------------------------------------------------------------
 
-__device__ __forceinline__ void accum8(double (&acc)[8], uint4 v) {
+constexpr int kCnBatch = 4;  // rows per wave loaded before they are added
+
+// G is read once and the stage written once per pass: both non-temporal
+__device__ __forceinline__ u32x4 cn_load(const uint16_t* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
+__device__ __forceinline__ void cn_store(uint16_t* p, u32x4 v) {
+  __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
+}
+
+__device__ __forceinline__ void accum8(double (&acc)[8], u32x4 v) {
   const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
   for (int h = 0; h < 4; ++h) {
@@ -62,25 +72,20 @@ __global__ __launch_bounds__(kThreads) void colnorm_partial_kernel(const DevMat*
     const int64_t sld = d.ld_acc1;
     if (d.vec && c0 + 8 <= d.m) {
       int64_t i = r0 + wave;
-      for (; i + 12 < r1; i += 16) {
-        const uint4 v0 = *reinterpret_cast<const uint4*>(base + i * ld);
-        const uint4 v1 = *reinterpret_cast<const uint4*>(base + (i + 4) * ld);
-        const uint4 v2 = *reinterpret_cast<const uint4*>(base + (i + 8) * ld);
-        const uint4 v3 = *reinterpret_cast<const uint4*>(base + (i + 12) * ld);
+      for (; i + 4 * (kCnBatch - 1) < r1; i += 4 * kCnBatch) {
+        u32x4 v[kCnBatch];
+#pragma unroll
+        for (int b = 0; b < kCnBatch; ++b) v[b] = cn_load(base + (i + 4 * b) * ld);
         if (st) {
-          *reinterpret_cast<uint4*>(sbase + i * sld) = v0;
-          *reinterpret_cast<uint4*>(sbase + (i + 4) * sld) = v1;
-          *reinterpret_cast<uint4*>(sbase + (i + 8) * sld) = v2;
-          *reinterpret_cast<uint4*>(sbase + (i + 12) * sld) = v3;
+#pragma unroll
+          for (int b = 0; b < kCnBatch; ++b) cn_store(sbase + (i + 4 * b) * sld, v[b]);
         }
-        accum8(acc, v0);
-        accum8(acc, v1);
-        accum8(acc, v2);
-        accum8(acc, v3);
+#pragma unroll
+        for (int b = 0; b < kCnBatch; ++b) accum8(acc, v[b]);
       }
       for (; i < r1; i += 4) {
-        const uint4 v = *reinterpret_cast<const uint4*>(base + i * ld);
-        if (st) *reinterpret_cast<uint4*>(sbase + i * sld) = v;
+        const u32x4 v = cn_load(base + i * ld);
+        if (st) cn_store(sbase + i * sld, v);
         accum8(acc, v);
       }
     } else {
