@@ -510,8 +510,18 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def launch_kernels(kind: str, channel_major: bool, deferred: bool) -> str:
-    """The kernels behind one update launch kind of the runner."""
+def launch_kernels(kind: str, channel_major: bool, deferred: bool, stage: bool = False,
+                   scored_handover: bool = False) -> str:
+    """The kernels behind one launch kind of the runner."""
+    if kind == "colnorm":
+        what = ("column scores, and every channel's hand-over of the one-step interval"
+                if scored_handover else "column scores, and the bf16 first-step stage"
+                if stage else "column scores")
+        return (f"cm_colnorm_kernel ({what})" if channel_major else
+                f"colnorm_partial_kernel + colnorm_finalize_kernel ({what})")
+    if channel_major and kind == "update_adam_handover":
+        return ("cm_update_kernel, selected-only grid (Adam + bf16 write-back, +0.0 in the "
+                "selected channels' hand-over rows)")
     if channel_major:
         if deferred and kind == "update_zen":
             return ("cm_update_kernel, Zen-auto with deferred packing (Adam + statistics of the "
@@ -535,19 +545,29 @@ def launch_kernels(kind: str, channel_major: bool, deferred: bool) -> str:
     return f"rv_update_kernel / update_kernel ({kind}) (fused Adam + bf16 write-back + pack)"
 
 
-def recorded_traffic(launch_kind: str, workload: str, variant: str):
-    """HBM bytes per launch of one update launch kind, from rocprofv3 PMC
-    counters (FETCH_SIZE and WRITE_SIZE runs, scaled by the reference copy
-    stream's reading), if recorded for this workload, variant (layout, and
-    for the eager path "-every-step") and the current kernel sources."""
+def traffic_settings(config: dict) -> str:
+    """The settings of a run, beyond its workload and layout, that its
+    launches' bytes depend on (from the `config` object of the bench line)."""
+    keys = ("topk_ratio", "refresh_interval", "accum_interval", "zen_auto_tau",
+            "zen_interval_decided_on", "offload", "first_step_stage", "packing")
+    return json.dumps({k: config.get(k) for k in keys}, sort_keys=True)
+
+
+def recorded_traffic(launch_kind: str, workload: str, variant: str, settings: str):
+    """HBM bytes per launch of one launch kind, from rocprofv3 PMC counters
+    (FETCH_SIZE and WRITE_SIZE runs, scaled by the reference copy stream's
+    reading), if recorded for this workload, variant (layout, and for the
+    eager path "-every-step"), run settings (`traffic_settings`) and the
+    current kernel sources."""
     path = os.path.join(PROFILES, f"traffic_{workload}_{variant}.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
     h = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
+    c = re.search(r"profiled_settings:\s*(\{.*\})", text)
     v = re.search(r"traffic_bytes_per_launch\[" + re.escape(launch_kind) +
                   r"\]:\s*([0-9.eE+]+)", text)
-    if not h or not v or h.group(1) != kernel_source_hash():
+    if not h or not c or not v or h.group(1) != kernel_source_hash() or c.group(1) != settings:
         return None
     return float(v.group(1))
 
@@ -816,10 +836,10 @@ def main(argv=None) -> int:
     # the dominant kernel: the fused Adam + pack pass in its middle-step form
     # (states in place, accumulation; no hand-over): its bytes per launch are
     # the unfused method's per-unit figures, 28 per selected and 10 per unselected
-    # element; else the update launch kind with the most time
-    upd = [nm for nm in per if kernel_class(nm) == "update"]
-    dom = "update" if "update" in per else (max(upd, key=lambda nm: sum(per[nm]["ms"]))
-                                            if upd else None)
+    # element; else the launch kind with the most time
+    timed = [nm for nm in per if per[nm]["bytes"]]
+    dom = "update" if "update" in per else (max(timed, key=lambda nm: sum(per[nm]["ms"]))
+                                            if timed else None)
     roof = None
     if dom is not None:
         e = per[dom]
@@ -827,7 +847,8 @@ def main(argv=None) -> int:
         avg = sum(e["ms"]) / n
         nbytes = (e["unfused"] if dom == "update" else e["bytes"]) / n
         achieved = nbytes / (avg * 1e-3) / 1e9
-        kname = launch_kernels(dom, layout == zf.CHANNEL_MAJOR, runner.deferred)
+        kname = launch_kernels(dom, layout == zf.CHANNEL_MAJOR, runner.deferred,
+                               runner.use_stage, bool(runner.score_handover))
         roof = {
             "kernel": kname,
             "launch_kind": dom,
@@ -836,8 +857,7 @@ def main(argv=None) -> int:
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": recorded_traffic(dom, wl.name, args.layout + (
-                "" if runner.deferred else "-every-step")),
+            "traffic": None,
             "bytes_per_launch": round(nbytes),
             "byte_model": "unfused per-unit figures" if dom == "update" else "build",
             "avg_launch_ms": round(avg, 4),
@@ -880,7 +900,9 @@ def main(argv=None) -> int:
                         "Zen-auto statistics" if runner.deferred and args.zen_tau is not None
                         else "deferred to the interval's last step" if runner.deferred else
                         "every step"),
-            "handover": "fused into the interval's last update" if fused else
+            "handover": ("written by the score pass (one-step intervals)"
+                         if runner.score_handover and wl.refresh == 1 else
+                         "fused into the interval's last update") if fused else
                         ("device -> host copy of the packed buffer" if args.offload
                          else "fused into the update at forced ends, else the gated pass"
                          if runner.zen_device else "separate unpack pass"),
@@ -900,6 +922,9 @@ def main(argv=None) -> int:
         "reference_streams": calib,
         "roofline": roof,
     }
+    if roof is not None:
+        roof["traffic"] = recorded_traffic(dom, wl.name, args.layout + (
+            "" if runner.deferred else "-every-step"), traffic_settings(result["config"]))
     if args.offload:
         # host side of the deferred update: per unselected element it reads
         # the accumulated sum (4 B), reads and writes p, m, v (24 B) and

@@ -68,17 +68,6 @@ __device__ __forceinline__ void widen8(u32x4 v, float (&f)[kGroup]) {
   }
 }
 
-template <int AUX>
-__device__ __forceinline__ void f32x8_store(rsrc_t r, uint32_t byte_off, const float (&f)[kGroup]) {
-  u32x4 a, b;
-  a.x = __float_as_uint(f[0]); a.y = __float_as_uint(f[1]);
-  a.z = __float_as_uint(f[2]); a.w = __float_as_uint(f[3]);
-  b.x = __float_as_uint(f[4]); b.y = __float_as_uint(f[5]);
-  b.z = __float_as_uint(f[6]); b.w = __float_as_uint(f[7]);
-  buf_put_b128<AUX>(a, r, byte_off, 0);
-  buf_put_b128<AUX>(b, r, byte_off + 16, 0);
-}
-
 // The vector paths of the update, the deferred hand-over and the unpack
 // work in quads: 4 consecutive elements per lane access (8 bytes of bf16,
 // 16 of fp32), quad q of thread tid at elements (q * kThreads + tid) * 4 of
@@ -192,13 +181,36 @@ __global__ __launch_bounds__(kThreads) void cm_colnorm_kernel(const DevMat* __re
           a1 = __builtin_fma(static_cast<double>(f[c + 1]), static_cast<double>(f[c + 1]), a1);
         }
         if constexpr (OUT == 2) {
+          // The hand-over in whole lines.  Lane l holds elements 8l .. 8l+7
+          // of this load's 512; it stores elements 4l .. 4l+3 and 256+4l ..
+          // 256+4l+3, held by lanes l/2 and 32 + l/2 (their words 2(l&1)
+          // and 2(l&1)+1), so that each store of the wave fills 1 KiB.  (A
+          // lane storing its own 8 values fills half of every line with each
+          // of two stores: non-temporal, each half reached HBM on its own.)
+          const uint32_t w[4] = {v[b].x, v[b].y, v[b].z, v[b].w};
+          uint32_t x[4], y[4];
 #pragma unroll
-          for (int c = 0; c < kGroup; ++c) f[c] = f[c] * scale;
-          // a lane's 8 values go out as two 16-byte stores, each filling
-          // half of every line it touches: the default policy merges the
-          // halves in L2 (non-temporal, each half reaches HBM on its own and
-          // the pass ran at half speed)
-          f32x8_store<kCached>(rO, static_cast<uint32_t>((e0 + b * kStride + lo) * 4), f);
+          for (int k = 0; k < 4; ++k) {
+            x[k] = static_cast<uint32_t>(__shfl(static_cast<int>(w[k]), lane >> 1, 64));
+            y[k] = static_cast<uint32_t>(__shfl(static_cast<int>(w[k]), 32 + (lane >> 1), 64));
+          }
+          const bool odd = lane & 1;
+          u32x2 qa, qb;
+          qa.x = odd ? x[2] : x[0];
+          qa.y = odd ? x[3] : x[1];
+          qb.x = odd ? y[2] : y[0];
+          qb.y = odd ? y[3] : y[1];
+          float fa[kQuad], fb[kQuad];
+          widen4(qa, fa);
+          widen4(qb, fb);
+#pragma unroll
+          for (int c = 0; c < kQuad; ++c) {
+            fa[c] = fa[c] * scale;
+            fb[c] = fb[c] * scale;
+          }
+          const int64_t seg = e0 + b * kStride + kQuad * lane;
+          f32x4_store<kAuxWO>(rO, static_cast<uint32_t>(seg * 4), fa);
+          f32x4_store<kAuxWO>(rO, static_cast<uint32_t>((seg + kStride / 2) * 4), fb);
         }
       }
     }

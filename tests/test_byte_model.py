@@ -156,3 +156,49 @@ def test_zen_deferred_packing_bytes():
     per_u = sum(bench.step_bytes([(1, 1000)], [0], False, p == 1, p == 4, length=p,
                                  fused_handover=p == 4, **kw)["update"] for p in (1, 2, 3, 4))
     assert per_u == 24 * 1000
+
+
+def test_recorded_traffic_needs_the_profiled_settings(tmp_path, monkeypatch):
+    """PMC traffic recorded under profiles/ applies to a bench line only for
+    the same kernel sources, workload, layout variant and run settings (ratio,
+    schedule, packing, Zen-auto, offload): a run at another ratio or refresh
+    interval moves other bytes and reports no traffic."""
+    cfg = {"topk_ratio": 0.1, "refresh_interval": 4, "accum_interval": 4, "zen_auto_tau": None,
+           "zen_interval_decided_on": None, "offload": False, "first_step_stage": False,
+           "packing": "deferred to the interval's last step", "grad_slots": 4}
+    text = ("Machine-readable:\n\n"
+            f"kernel_source_sha256_16: {bench.kernel_source_hash()}\n"
+            f"profiled_settings: {bench.traffic_settings(cfg)}\n"
+            "traffic_bytes_per_launch[update_handover]: 9.4e+10\n")
+    (tmp_path / "traffic_wl_channel-major.md").write_text(text)
+    monkeypatch.setattr(bench, "PROFILES", str(tmp_path))
+    get = bench.recorded_traffic
+    assert get("update_handover", "wl", "channel-major", bench.traffic_settings(cfg)) == 9.4e10
+    # settings outside the byte model (the ring's slot count) do not matter
+    assert get("update_handover", "wl", "channel-major",
+               bench.traffic_settings(dict(cfg, grad_slots=3))) == 9.4e10
+    for change in ({"topk_ratio": 0.25}, {"refresh_interval": 1}, {"zen_auto_tau": 1.0},
+                   {"packing": "every step"}, {"offload": True}):
+        assert get("update_handover", "wl", "channel-major",
+                   bench.traffic_settings(dict(cfg, **change))) is None, change
+    assert get("update_adam", "wl", "channel-major", bench.traffic_settings(cfg)) is None
+    assert get("update_handover", "wl", "row-major", bench.traffic_settings(cfg)) is None
+    (tmp_path / "traffic_wl_channel-major.md").write_text(
+        text.replace(bench.kernel_source_hash(), "0" * 16))
+    assert get("update_handover", "wl", "channel-major", bench.traffic_settings(cfg)) is None
+
+
+def test_committed_profiles_record_their_settings():
+    """Every committed traffic summary names the settings it was taken with,
+    and the default 7B line's settings match the headline profile."""
+    import glob
+    import json
+    paths = glob.glob(os.path.join(ROOT, "profiles", "traffic_*.md"))
+    assert paths
+    for path in paths:
+        text = open(path).read()
+        line = [ln for ln in text.splitlines() if ln.startswith("profiled_settings:")]
+        assert len(line) == 1, path
+        json.loads(line[0].split(":", 1)[1])
+    head = open(os.path.join(ROOT, "profiles", "traffic_llama2-7b-full_channel-major.md")).read()
+    assert '"refresh_interval": 4' in head and '"topk_ratio": 0.1' in head
