@@ -35,6 +35,13 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 PROFILES = os.path.join(ROOT, "profiles")
+# Zen-auto with deferred packing reads 2p bytes per unselected element at the
+# interval's step p: p(p + 1) + 4 bytes over an interval of p steps ended by
+# force, against 10p - 8 packing every step with the bf16 stage.  Measured on
+# MI355X: 10.0-10.3 against 11.6-11.7 ms per 7B step at 4 steps, 16.8-17.0
+# against 15.5-15.6 ms for the 70B share at 8 steps.
+ZEN_DEFER_MAX = 6
+
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2505_12242_amd", "csrc", f)
                   for f in ("zf_device.hpp", "zf_internal.hpp", "zf_kernels.hip",
                             "zf_kernels_cm.hip", "zf_kernels_rv.hip", "zf_kernels_stream.hip")]
@@ -84,14 +91,15 @@ def parse_args(argv=None):
     ap.add_argument("--host-threads", type=int, default=None,
                     help="with --offload: host threads of the deferred update (default: "
                          "min(16, cpu count))")
-    ap.add_argument("--packing", choices=["deferred", "every-step"], default="deferred",
-                    help="deferred (default where it applies: fixed schedule or Zen-auto "
-                         "decided on the device in the channel-major layout, fused hand-over, "
-                         "no offload): every gradient of an interval stays in its slot and the "
-                         "interval's last step sums them into the hand-over (Zen-auto: every "
-                         "step sums them for its statistics), with no packed buffer (the ring "
-                         "gets at least min(S, R) slots); every-step: the unselected part is "
-                         "accumulated into the packed buffer at every step")
+    ap.add_argument("--packing", choices=["deferred", "every-step"], default=None,
+                    help="deferred (default where it applies: fixed schedule, or Zen-auto "
+                         "decided on the device in the channel-major layout with intervals of "
+                         "at most 6 steps; fused hand-over, no offload): every gradient of an "
+                         "interval stays in its slot and the interval's last step sums them "
+                         "into the hand-over (Zen-auto: every step sums them for its "
+                         "statistics), with no packed buffer (the ring gets at least min(S, R) "
+                         "slots); every-step: the unselected part is accumulated into the "
+                         "packed buffer at every step")
     ap.add_argument("--separate-handover", action="store_true",
                     help="hand over with a separate unpack pass after the last update of an "
                          "interval instead of fusing it into that update")
@@ -667,8 +675,12 @@ def main(argv=None) -> int:
               f"{calib['read_GB/s']}, copy {calib['copy_GB/s']}, read-modify-write "
               f"{calib['rmw_GB/s']} GB/s", file=sys.stderr, flush=True)
 
-    # (Zen-auto: with deferred packing when decided on the device, channel-major)
-    deferred = (args.packing == "deferred" and not args.offload and not args.separate_handover
+    # Zen-auto: with deferred packing when decided on the device, channel-major,
+    # and by default only for intervals of at most ZEN_DEFER_MAX steps (its
+    # statistics re-read the interval's kept gradients at every step)
+    packing = args.packing or ("every-step" if args.zen_tau is not None and
+                               min(wl.accum, wl.refresh) > ZEN_DEFER_MAX else "deferred")
+    deferred = (packing == "deferred" and not args.offload and not args.separate_handover
                 and (args.zen_tau is None
                      or (not args.zen_on_host and args.layout == "channel-major")))
     if deferred:

@@ -147,6 +147,39 @@ def test_colnorm_stage_then_adam_only_refresh(n, m, aligned):
                               np.ascontiguousarray(b).view(np.uint8))
 
 
+@pytest.mark.parametrize("scale", [1.0, 0.25, 1.0 / 3.0])
+@pytest.mark.parametrize("aligned", [True, False])
+@pytest.mark.parametrize("n,m", [(64, 300), (2056, 40), (6144, 24), (4101, 20), (5, 33)])
+def test_score_pass_handover(n, m, aligned, scale):
+    """zf_plan_colnorm_handover alone: every element of the hand-over is
+    fp32(scale x widen(g)), one IEEE product (checked with numpy), whatever
+    the buffer held before; the scores are those of the plain score pass,
+    bit for bit.  The vector path's lanes hand their values to the lanes that
+    store them (whole lines per store): shapes with one and several passes,
+    a ragged last pass and every lane pair; n % 8 != 0 and unaligned rows
+    take the element path."""
+    print(f"# score-pass hand-over n={n} m={m} aligned={aligned} scale={scale}",
+          file=sys.stderr, flush=True)
+    k, sel, (g1, _), G = _setup(n, m, aligned)
+    sc = np.float32(scale)
+    want = (O.widen(g1) * sc).astype(np.float32)  # [n][m], one product per element
+    D = _buf(m, n, torch.float32, aligned, np.nan)
+    A = _buf(m - k, n, torch.float32, aligned, np.nan)
+    norms = torch.full((m,), np.nan, device="cuda")
+    plan = zf.Plan([zf.MatrixBuffers(grad=G[0], k=k, sel=sel_dev(sel), acc=A, norms=norms,
+                                     unpacked=D, layout=CM)])
+    try:
+        plan.colnorm_handover(float(sc))
+        torch.cuda.synchronize()
+        got_norms = f32_np(norms).copy()
+        assert same_bits(f32_np(D).T, want)
+        plan.colnorm()
+        torch.cuda.synchronize()
+        assert same_bits(got_norms, f32_np(norms))
+    finally:
+        plan.close()
+
+
 @pytest.mark.parametrize("mode", ["init", "remap"])
 @pytest.mark.parametrize("aligned", [True, False])
 @pytest.mark.parametrize("n,m", [(64, 300), (4104, 70), (5, 33)])
