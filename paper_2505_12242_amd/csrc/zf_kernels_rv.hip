@@ -52,8 +52,9 @@
 // of each row, that row of every earlier gradient of the interval (the same
 // matrix in the earlier steps' plans) and of this step's, add them in step
 // order in fp32 with this step's last, and store the hand-over -- +0.0 at a
-// selected column, else the sum times `scale` -- with two 16-byte stores.
-// The step's Adam runs before it as the Adam-only instantiation over the
+// selected column, else the sum times `scale` -- with two 16-byte
+// non-temporal stores per lane, after lane shuffles that make each store of
+// a wave cover 1 KiB of the row (whole lines).  The step's Adam runs before it as the Adam-only instantiation over the
 // same tiles.  (Fused into one pass with the Adam lanes the kernel needs
 // registers for both and ran slower than the two passes.)
 //
@@ -347,10 +348,18 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
           }
         }
       }
+      // The stores in whole lines: lane l of a wave holds the wave's columns
+      // 8l .. 8l+7 and stores columns 4l .. 4l+3 and 256+4l .. 256+4l+3,
+      // held by lanes l/2 and 32 + l/2 (their values 4(l&1) .. 4(l&1)+3),
+      // so that each 16-byte store of the wave fills 1 KiB of the row.  wc:
+      // the tile's columns from the wave's first (the same for the wave).
+      const int lane = tid & 63;
+      const int32_t wc = width - (g8 - 8 * lane);
+      const uint32_t vw = static_cast<uint32_t>((c0 + g8 - 8 * lane) * 4);
 #pragma unroll
       for (int p = 0; p < kRvBatch / 2; ++p) {
         const int b = 2 * p + h;
-        if (b < nb && cols > 0) {
+        if (b < nb && wc > 0) {
           float g[8];
           widen_group(gv[p], g);
 #pragma unroll
@@ -358,13 +367,28 @@ __global__ __launch_bounds__(kThreads) void rv_update_kernel(const DevMat* __res
             const float sum = hist.n > 0 ? a[p][x] + g[x] : g[x];
             a[p][x] = ((sel8 >> x) & 1u) ? 0.0f : sum * scale;
           }
+          float lo[8], hi[8];
+#pragma unroll
+          for (int x = 0; x < 8; ++x) {
+            lo[x] = __shfl(a[p][x], lane >> 1, 64);
+            hi[x] = __shfl(a[p][x], 32 + (lane >> 1), 64);
+          }
+          const bool odd = lane & 1;
           const uint32_t so = static_cast<uint32_t>(i + b) * sD;
-          const uint32_t vd = static_cast<uint32_t>((c0 + g8) * 4);
-          if (cols >= 8) {
-            buf_put_b128(as_u4(a[p][0], a[p][1], a[p][2], a[p][3]), rD, vd, so);
-            buf_put_b128(as_u4(a[p][4], a[p][5], a[p][6], a[p][7]), rD, vd + 16, so);
-          } else {
-            for (int x = 0; x < cols; ++x) buf_put_f32(a[p][x], rD, vd + 4 * x, so);
+#pragma unroll
+          for (int half = 0; half < 2; ++half) {
+            float v[4];
+#pragma unroll
+            for (int x = 0; x < 4; ++x)
+              v[x] = half == 0 ? (odd ? lo[4 + x] : lo[x]) : (odd ? hi[4 + x] : hi[x]);
+            const int32_t cq = half * 256 + 4 * lane;  // the quad's first column in the wave
+            if (cq + 4 <= wc) {
+              buf_put_b128<kStream>(as_u4(v[0], v[1], v[2], v[3]), rD, vw + 4 * cq, so);
+            } else {
+#pragma unroll
+              for (int x = 0; x < 4; ++x)
+                if (cq + x < wc) buf_put_f32<kStream>(v[x], rD, vw + 4 * (cq + x), so);
+            }
           }
         }
       }
