@@ -626,6 +626,14 @@ UPDATE_NAMES = ("update", "update_first", "update_second", "update_handover", "u
                 "update_adam_handover", "update_zen", "update_zen_first")
 
 
+def default_packing(zen_tau, accum: int, refresh: int) -> str:
+    """--packing's default: deferred, except Zen-auto with intervals longer
+    than ZEN_DEFER_MAX steps (at most min(S, R)), which packs every step."""
+    if zen_tau is not None and min(accum, refresh) > ZEN_DEFER_MAX:
+        return "every-step"
+    return "deferred"
+
+
 def kernel_class(name: str):
     """Which entry of step_bytes a recorded launch belongs to."""
     if name in ("colnorm", "topk_select", "unpack"):
@@ -678,8 +686,7 @@ def main(argv=None) -> int:
     # Zen-auto: with deferred packing when decided on the device, channel-major,
     # and by default only for intervals of at most ZEN_DEFER_MAX steps (its
     # statistics re-read the interval's kept gradients at every step)
-    packing = args.packing or ("every-step" if args.zen_tau is not None and
-                               min(wl.accum, wl.refresh) > ZEN_DEFER_MAX else "deferred")
+    packing = args.packing or default_packing(args.zen_tau, wl.accum, wl.refresh)
     deferred = (packing == "deferred" and not args.offload and not args.separate_handover
                 and (args.zen_tau is None
                      or (not args.zen_on_host and args.layout == "channel-major")))

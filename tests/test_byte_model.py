@@ -202,3 +202,21 @@ def test_committed_profiles_record_their_settings():
         json.loads(line[0].split(":", 1)[1])
     head = open(os.path.join(ROOT, "profiles", "traffic_llama2-7b-full_channel-major.md")).read()
     assert '"refresh_interval": 4' in head and '"topk_ratio": 0.1' in head
+
+
+def test_default_packing():
+    """Deferred packing by default; Zen-auto keeps it for intervals of at most
+    ZEN_DEFER_MAX steps, where its per-step re-reads, p(p + 1) + 4 bytes per
+    unselected element over p >= 2 steps, stay below packing's 10p - 8 (the
+    bytes cross over at 8 steps; the time measured earlier, its read-heavy
+    passes streaming slower)."""
+    assert bench.ZEN_DEFER_MAX == 6
+    assert bench.default_packing(None, 8, 8) == "deferred"
+    assert bench.default_packing(None, 16, 16) == "deferred"
+    assert bench.default_packing(1.0, 4, 4) == "deferred"
+    assert bench.default_packing(1.0, 6, 16) == "deferred"
+    assert bench.default_packing(1.0, 8, 8) == "every-step"
+    assert bench.default_packing(0.5, 16, 7) == "every-step"
+    for p in range(2, bench.ZEN_DEFER_MAX + 1):
+        assert p * (p + 1) + 4 < 10 * p - 8, p
+    assert 8 * 9 + 4 > 10 * 8 - 8
